@@ -1,0 +1,193 @@
+"""Exact reference arithmetic for the multiple-double product -- TEST INFRASTRUCTURE.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this module.  It shares no code with the GPU path.
+
+Every function here is the plain mathematical definition written out with
+Python integers and ``fractions.Fraction`` (all finite doubles are dyadic
+rationals, so every step is exact); it is slow and meant for small inputs or
+sampled entries.  Citations refer to Chen and Verschelde, "Multiple Double
+Arithmetic on NVIDIA Tensor Cores":
+
+* section 1, definition of a multiple double: an unevaluated sum of
+  nonoverlapping doubles -> ``value``;
+* section 2, the 52-bit fraction cut into four 13-bit quarters with exponents
+  0, -13, -26, -39 (worked example) and the balanced grid -> ``split_element``;
+* section 3, balancing: one exponent grid per group of numbers (here one per row
+  of A and one per column of B) -> ``line_exponents``;
+* section 2, equations (1)-(3) and the rewritten product: level t collects the
+  slice pairs with p + q = t -> ``pairs_of_level`` and ``level_products``;
+* section 2, steps 4-5 of the overview: the parts of the product are extracted
+  and added into a multiple double -> ``accumulate`` and ``round_to_limbs``.
+
+The rounding of the exact sum into L limbs is greedy round-to-nearest-even:
+c_0 = RN(Z), c_l = RN(Z - c_0 - ... - c_{l-1}).  CPython's ``float(Fraction)``
+is correctly rounded (an integer true division), so RN is that conversion.
+"""
+
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+import numpy as np
+
+SLICE_BITS = 13
+DIGIT_MAX = (1 << SLICE_BITS) - 1  # 8191
+
+
+# --------------------------------------------------------------------------
+# values and exponents
+# --------------------------------------------------------------------------
+
+def value(limbs) -> Fraction:
+    """Exact value of a multiple double: the sum of its limbs (section 1)."""
+    return sum((Fraction(float(x)) for x in limbs), Fraction(0))
+
+
+def frexp_exp(x: float) -> int:
+    """Exponent e with x = f 2^e, 1/2 <= |f| < 1 (x != 0)."""
+    return math.frexp(float(x))[1]
+
+
+def line_exponents(X0: np.ndarray, axis: int) -> np.ndarray:
+    """Shared grid exponent of every row (axis 0) or column (axis 1) of the
+    leading-limb plane: the largest frexp exponent of a nonzero entry, and 0 for
+    an all-zero line (section 3: a zero needs no balancing)."""
+    X0 = np.asarray(X0, dtype=np.float64)
+    lines = X0 if axis == 0 else X0.T
+    out = np.zeros(lines.shape[0], dtype=np.int64)
+    for r in range(lines.shape[0]):
+        nz = [frexp_exp(x) for x in lines[r] if x != 0.0]
+        out[r] = max(nz) if nz else 0
+    return out
+
+
+# --------------------------------------------------------------------------
+# the exact splitter
+# --------------------------------------------------------------------------
+
+def grid_unit(E: int, s: int) -> Fraction:
+    """Unit of slice s on the grid of exponent E: 2^(E - 13 (s + 1))."""
+    return Fraction(2) ** int(E - SLICE_BITS * (s + 1))
+
+
+def split_element(limbs, E: int, S: int):
+    """Digits and residual of one multiple double on the grid of exponent E.
+
+    Following the worked example of section 2, the magnitude of the exact value
+    is cut into consecutive 13-bit fields below 2^E, truncating (the fields are
+    plain bit fields of the value); every digit carries the sign of the value
+    (sign-magnitude, the same-signed parts that the sign grouping and the 2^-52
+    transfer of section 3 aim at).  Returns (digits, R) with
+    value = sum_s digits[s] 2^(E - 13(s+1)) + R, |R| < 2^(E - 13 S), R * value >= 0.
+    Raises ValueError when |value| >= 2^E (the element is not on this grid).
+    """
+    E, S = int(E), int(S)
+    v = value(limbs)
+    if v == 0:
+        return [0] * S, Fraction(0)
+    sign = 1 if v > 0 else -1
+    u = grid_unit(E, S - 1)
+    D = math.floor(abs(v) / u)
+    if D >> (SLICE_BITS * S):
+        raise ValueError("|value| >= 2^E: element is not on the grid")
+    digits = [sign * ((D >> (SLICE_BITS * (S - 1 - s))) & DIGIT_MAX) for s in range(S)]
+    R = v - sum((d * grid_unit(E, s) for s, d in enumerate(digits)), Fraction(0))
+    return digits, R
+
+
+def split(X: np.ndarray, E: np.ndarray, S: int, axis: int) -> np.ndarray:
+    """Digits [S][rows][cols] (int64) of an operand X [L][rows][cols]."""
+    X = np.asarray(X, dtype=np.float64)
+    L, rows, cols = X.shape
+    D = np.zeros((S, rows, cols), dtype=np.int64)
+    for r in range(rows):
+        for c in range(cols):
+            e = int(E[r] if axis == 0 else E[c])
+            d, _ = split_element(X[:, r, c], e, S)
+            D[:, r, c] = d
+    return D
+
+
+# --------------------------------------------------------------------------
+# slice pairs, levels, accumulation and rounding
+# --------------------------------------------------------------------------
+
+def pairs_of_level(t: int, S: int):
+    """Slice pairs (p, q) with p + q = t, 0 <= p, q < S, in increasing p."""
+    return [(p, t - p) for p in range(S) if 0 <= t - p < S]
+
+
+def level_products(DA: np.ndarray, DB: np.ndarray, T: int) -> list:
+    """G_t = sum over p + q = t of DA_p DB_q for t = 0..T, as Python-int matrices.
+
+    Products of integers are exact; Python ints cannot overflow."""
+    S, m, k = DA.shape
+    n = DB.shape[2]
+    A = [[[int(x) for x in row] for row in DA[p]] for p in range(S)]
+    B = [[[int(x) for x in row] for row in DB[q]] for q in range(S)]
+    G = []
+    for t in range(T + 1):
+        g = [[0] * n for _ in range(m)]
+        for p, q in pairs_of_level(t, S):
+            for i in range(m):
+                ai = A[p][i]
+                for j in range(n):
+                    g[i][j] += sum(ai[kk] * B[q][kk][j] for kk in range(k))
+        G.append(g)
+    return G
+
+
+def accumulate(levels, EA: int, EB: int) -> Fraction:
+    """Z = sum_t G_t 2^(-13 t), times the grid scale 2^(EA + EB - 26).
+
+    Slice p of A has unit 2^(EA - 13(p+1)) and slice q of B has unit
+    2^(EB - 13(q+1)); their product has unit 2^(EA + EB - 26 - 13(p+q)), so level
+    t = p + q carries weight 2^(EA + EB - 26 - 13 t)."""
+    z = Fraction(0)
+    for t, g in enumerate(levels):
+        z += Fraction(int(g)) * Fraction(2) ** int(EA + EB - 2 * SLICE_BITS - SLICE_BITS * t)
+    return z
+
+
+def round_to_limbs(z: Fraction, L: int):
+    """Greedy round-to-nearest-even of an exact value into L doubles."""
+    out = []
+    r = z
+    for _ in range(L):
+        c = float(r) if r != 0 else 0.0
+        out.append(c)
+        r -= Fraction(c)
+    return out
+
+
+def exact_product(A: np.ndarray, B: np.ndarray, i: int, j: int):
+    """(C_exact[i][j], (|A||B|)[i][j]) of the exact multiple-double operands."""
+    k = A.shape[2]
+    c = Fraction(0)
+    mag = Fraction(0)
+    for kk in range(k):
+        a = value(A[:, i, kk])
+        b = value(B[:, kk, j])
+        c += a * b
+        mag += abs(a) * abs(b)
+    return c, mag
+
+
+def tolerance(k: int, L: int, mag: Fraction) -> Fraction:
+    """Componentwise bound 4 k 2^-(53 L - 4) (|A||B|)_ij on |C - C_exact|."""
+    return 4 * k * Fraction(2) ** (-(53 * L - 4)) * mag
+
+
+def is_nonoverlapping(limbs) -> bool:
+    """|x_{l+1}| <= ulp(x_l)/2 and a zero limb is followed only by zeros."""
+    for a, b in zip(limbs[:-1], limbs[1:]):
+        a, b = float(a), float(b)
+        if a == 0.0:
+            if b != 0.0:
+                return False
+            continue
+        if abs(b) > 0.5 * math.ulp(a):
+            return False
+    return True

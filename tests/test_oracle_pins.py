@@ -1,0 +1,485 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+None of these checks retypes the oracle's own formula: each compares it with a
+value the paper prints, a closed form, an independent formulation (the
+materialized rewritten product, schoolbook digit extraction, exact rational
+arithmetic) or an invariant.  Section numbers refer to Chen and Verschelde,
+"Multiple Double Arithmetic on NVIDIA Tensor Cores".
+"""
+
+import math
+import os
+import random
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import coracle, exact, pipeline
+from paper_2607_06881_amd import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden_lines(name):
+    with open(os.path.join(GOLDEN, name)) as fh:
+        return [ln.rstrip("\n") for ln in fh if ln.strip() and not ln.startswith("#")]
+
+
+# --------------------------------------------------------------------------
+# section 2: the worked 52-bit -> 4 x 13-bit split
+# --------------------------------------------------------------------------
+
+def _worked_example():
+    fields, quarters = {}, {}
+    for ln in _golden_lines("worked_split.txt"):
+        key, rest = [s.strip() for s in ln.split(":", 1)]
+        if key.startswith("f"):
+            fields[key] = int(rest.replace(" ", ""), 2)
+        else:
+            parts = rest.split()
+            bits = "".join(parts[:4])  # leading bit and 12 more significand bits
+            quarters[key] = (int(bits, 2), int(parts[-1]))
+    return fields, quarters
+
+
+def test_worked_example_fields_partition_f():
+    fields, _ = _worked_example()
+    f = fields["f"]
+    assert f.bit_length() == 52
+    parts = [fields[f"f{s}"] for s in range(4)]
+    assert sum(parts) == f
+    for a in range(4):
+        for b in range(a + 1, 4):
+            assert parts[a] & parts[b] == 0
+
+
+@pytest.mark.parametrize("impl", ["python", "c"])
+def test_worked_example_split(impl):
+    fields, quarters = _worked_example()
+    x = fields["f"] * 2.0**-52  # the double whose 52 fraction bits are f, exponent 0
+    E = 0
+    assert exact.frexp_exp(x) == E
+    if impl == "python":
+        digits, R = exact.split_element([x], E, 4)
+        assert R == 0
+    else:
+        X = np.array([x]).reshape(1, 1, 1)
+        assert coracle.exponents(X[0], 0)[0] == E
+        digits = [int(d) for d in coracle.split(X, np.array([E]), 4, 0).ravel()]
+    for s in range(4):
+        # digit s is the field f_s moved down to an integer
+        assert digits[s] << (13 * (3 - s)) == fields[f"f{s}"]
+        # and equals the printed quarter, whose exponent is 0, -13, -26, -39
+        q_bits, q_exp = quarters[f"x{s}"]
+        assert digits[s] == q_bits
+        assert exact.frexp_exp(digits[s] * 2.0 ** (-13 * (s + 1))) == q_exp
+
+
+def test_truncation_not_rounding_matches_worked_example():
+    # Reading: the parts are truncated bit fields.  Rounding the first part to
+    # nearest would change f0 because the 14th bit of f is 1.
+    fields, _ = _worked_example()
+    f = fields["f"]
+    assert (f >> (52 - 14)) & 1 == 1
+    rounded_f0 = (f + (1 << (38 - 1))) >> 39
+    assert rounded_f0 != fields["f0"] >> 39
+
+
+# --------------------------------------------------------------------------
+# sections 2-3: borrow / opposite-sign limbs, invariants, brute force
+# --------------------------------------------------------------------------
+
+def _parse_borrow():
+    cases = []
+    for ln in _golden_lines("borrow_split.txt"):
+        limbs, E, S, digits = [s.strip() for s in ln.split("|")]
+        cases.append(([float.fromhex(t) for t in limbs.split()], int(E), int(S), [int(t) for t in digits.split()]))
+    return cases
+
+
+@pytest.mark.parametrize("case", _parse_borrow())
+def test_borrow_vectors(case):
+    limbs, E, S, want = case
+    d, R = exact.split_element(limbs, E, S)
+    assert d == want and R == 0
+    X = np.array(limbs).reshape(len(limbs), 1, 1)
+    dc = coracle.split(X, np.array([E]), S, 0).ravel().astype(np.int64).tolist()
+    assert dc == want
+
+
+def _schoolbook_digits(limbs, E, S):
+    """Base-2^13 digits by repeated multiplication (an independent algorithm)."""
+    v = sum(Fraction(x) for x in limbs)
+    sign = 1 if v >= 0 else -1
+    r = abs(v) / Fraction(2) ** E
+    out = []
+    for _ in range(S):
+        r *= 8192
+        d = math.floor(r)
+        out.append(sign * d if d else 0)
+        r -= d
+    return out
+
+
+def _random_md(rng, L, spread=60):
+    """A random normalized multiple double with random gaps between limbs."""
+    x0 = rng.choice([-1, 1]) * rng.uniform(0.5, 1.0) * 2.0 ** rng.randint(-spread, spread)
+    limbs = [x0]
+    for _ in range(1, L):
+        prev = limbs[-1]
+        if prev == 0.0 or rng.random() < 0.1:
+            limbs.append(0.0)
+            continue
+        half_ulp = math.ulp(prev) / 2
+        kind = rng.random()
+        if kind < 0.15:
+            y = rng.choice([-1, 1]) * half_ulp  # extreme allowed magnitude
+        elif kind < 0.3:
+            y = rng.choice([-1, 1]) * half_ulp * 2.0 ** -rng.randint(1, 30)  # gap
+        else:
+            y = rng.uniform(-1, 1) * half_ulp
+        limbs.append(y)
+    return limbs
+
+
+@pytest.mark.parametrize("L", [1, 2, 3, 4])
+def test_split_invariants_and_brute_force(L):
+    rng = random.Random(1234 + L)
+    for trial in range(300):
+        limbs = _random_md(rng, L)
+        assert exact.is_nonoverlapping(limbs)
+        e0 = exact.frexp_exp(limbs[0])
+        E = e0 + rng.choice([0, 0, 0, 1, 3, 13, 40])
+        S = rng.choice([1, 2, 3, 4, 4 * L, 4 * L + 3])
+        d, R = exact.split_element(limbs, E, S)
+        v = exact.value(limbs)
+        u = exact.grid_unit(E, S - 1)
+        # slices plus residual give back the value exactly
+        assert sum(di * exact.grid_unit(E, s) for s, di in enumerate(d)) + R == v
+        assert abs(R) < u and R * v >= 0
+        assert all(0 <= abs(di) <= 8191 and di * v >= 0 for di in d)
+        assert d == _schoolbook_digits(limbs, E, S)
+        X = np.array(limbs).reshape(L, 1, 1)
+        dc = coracle.split(X, np.array([E]), S, 0).ravel().astype(np.int64).tolist()
+        assert dc == d, (limbs, E, S)
+
+
+def test_split_full_coverage_has_zero_residual():
+    # With enough slices to reach the lowest set bit, the split is exact (R == 0).
+    rng = random.Random(7)
+    for _ in range(200):
+        L = rng.randint(1, 4)
+        limbs = _random_md(rng, L, spread=5)
+        E = exact.frexp_exp(limbs[0])
+        lows = [exact.frexp_exp(x) - 53 for x in limbs if x != 0.0]
+        S_full = math.ceil((E - min(lows)) / 13)
+        _, R = exact.split_element(limbs, E, S_full)
+        assert R == 0
+
+
+def test_split_subnormal_and_zero():
+    tiny = [5 * 2.0**-1074, 0.0]
+    E = exact.frexp_exp(tiny[0])
+    assert E == -1071
+    d, R = exact.split_element(tiny, E, 1)
+    assert d == [5 << 10] and R == 0
+    X = np.array(tiny).reshape(2, 1, 1)
+    assert coracle.split(X, np.array([E]), 1, 0).ravel().tolist() == [5 << 10]
+    assert exact.split_element([0.0, 0.0], 0, 3) == ([0, 0, 0], 0)
+    with pytest.raises(ValueError):
+        exact.split_element([1.0], 0, 4)  # |x| = 2^E is not below the grid top
+
+
+def test_exponents_against_numpy_frexp():
+    rng = np.random.default_rng(5)
+    X = rng.standard_normal((37, 53)) * np.ldexp(1.0, rng.integers(-300, 300, (37, 53)))
+    X[3, :] = 0.0
+    X[:, 7] = 0.0
+    X[5, 9] = 3 * 2.0**-1074  # subnormal
+    for axis in (0, 1):
+        Ec = coracle.exponents(X, axis)
+        _, ex = np.frexp(X)
+        masked = np.where(X != 0, ex, np.iinfo(np.int32).min)
+        want = masked.max(axis=1 - axis)
+        want = np.where(want == np.iinfo(np.int32).min, 0, want)
+        assert np.array_equal(Ec, want)
+        assert np.array_equal(Ec, exact.line_exponents(X, axis))
+    # every element lies below 2^E of its row
+    Er = coracle.exponents(X, 0)
+    assert np.all(np.abs(X) < np.ldexp(1.0, Er[:, None]))
+
+
+# --------------------------------------------------------------------------
+# section 2: equation (3), the rewritten product and the bound (NBound)
+# --------------------------------------------------------------------------
+
+def test_eq3_level_structure():
+    for ln in _golden_lines("eq3_levels.txt"):
+        t, pairs = ln.split(":")
+        want = sorted(tuple(int(v) for v in p.split(",")) for p in pairs.split())
+        assert sorted(exact.pairs_of_level(int(t), 4)) == want
+
+
+def test_rewritten_product_matches_levels():
+    # The double-double rewrite: Abar = [A_0 ... A_7] and Bbar block upper
+    # triangular Toeplitz with B_0 on the diagonal; block column l of Abar Bbar is
+    # the level-l product, and the 36 blocks on or above the diagonal are the pairs.
+    rng = np.random.default_rng(11)
+    S, m, k, n = 8, 5, 6, 4
+    DA = rng.integers(-8191, 8192, (S, m, k))
+    DB = rng.integers(-8191, 8192, (S, k, n))
+    Abar = np.concatenate([DA[p] for p in range(S)], axis=1)  # m x S k
+    Bbar = np.zeros((S * k, S * n), dtype=np.int64)
+    for r in range(S):
+        for c in range(r, S):
+            Bbar[r * k:(r + 1) * k, c * n:(c + 1) * n] = DB[c - r]
+    Cbar = Abar.astype(object) @ Bbar.astype(object)
+    T = S - 1
+    assert sum(len(exact.pairs_of_level(t, S)) for t in range(T + 1)) == 36
+    G = coracle.levels(DA.astype(np.float64), DB.astype(np.float64), T)
+    Gpy = exact.level_products(DA, DB, T)
+    for l in range(S):
+        blk = np.array(Cbar[:, l * n:(l + 1) * n], dtype=np.int64)
+        assert np.array_equal(blk, G[l])
+        assert np.array_equal(blk, np.array(Gpy[l], dtype=np.int64))
+
+
+def test_nbound_value():
+    # N (2^0 + ... + 2^25) <= 2^52 gives N <= 67,108,865 (section 2).
+    B = sum(2**i for i in range(26))
+    assert B == 2**26 - 1
+    assert 2**52 // B == 67108865
+    assert 67108865 * B <= 2**52 < 67108866 * B
+
+
+def test_levels_against_float_matmul_and_per_pair():
+    rng = np.random.default_rng(3)
+    S, T, m, k, n = 6, 7, 9, 33, 7
+    DA = rng.integers(-8191, 8192, (S, m, k)).astype(np.float64)
+    DB = rng.integers(-8191, 8192, (S, k, n)).astype(np.float64)
+    G = coracle.levels(DA, DB, T)
+    P = coracle.levels(DA, DB, T, per_pair=True)
+    for t in range(T + 1):
+        acc = np.zeros((m, n))
+        for p, q in exact.pairs_of_level(t, S):
+            prod = DA[p] @ DB[q]  # float64 BLAS: exact, every partial sum < 2^53
+            assert np.array_equal(P[p, q], prod.astype(np.int64))
+            acc += prod
+        assert np.array_equal(G[t], acc.astype(np.int64))
+
+
+def test_all_pairs_identity_with_truncated_operands():
+    # With every pair kept (T = 2S - 2), the weighted levels are exactly the
+    # product of the truncated operands: sum_t G_t 2^(EA+EB-26-13t) = sum_k tr(a) tr(b).
+    for seed in range(3):
+        rng = np.random.default_rng(seed)
+        L, m, k, n = 2, 4, 5, 3
+        A = workloads.make_operand(rng, L, m, k, row_exp=9)
+        B = workloads.make_operand(rng, L, k, n, col_exp=9)
+        S = int(rng.integers(2, 9))
+        T = 2 * S - 2
+        ref = pipeline.full_reference(A, B, S, T)
+        for i in range(m):
+            for j in range(n):
+                z = exact.accumulate([int(ref["G"][t, i, j]) for t in range(T + 1)],
+                                     int(ref["EA"][i]), int(ref["EB"][j]))
+                want = Fraction(0)
+                for kk in range(k):
+                    da, ra = exact.split_element(A[:, i, kk], int(ref["EA"][i]), S)
+                    db, rb = exact.split_element(B[:, kk, j], int(ref["EB"][j]), S)
+                    want += (exact.value(A[:, i, kk]) - ra) * (exact.value(B[:, kk, j]) - rb)
+                assert z == want
+
+
+# --------------------------------------------------------------------------
+# greedy rounding into L limbs
+# --------------------------------------------------------------------------
+
+def test_round_to_limbs_hand_cases():
+    u = Fraction(2) ** -52  # ulp(1)
+    # exactly representable
+    assert exact.round_to_limbs(Fraction(3, 4), 2) == [0.75, 0.0]
+    # a half-ulp tail stays in the second limb (tie at the first limb goes to even 1.0)
+    assert exact.round_to_limbs(1 + u / 2, 2) == [1.0, 2.0**-53]
+    # 1 + 3/2 ulp: tie between 1+u and 1+2u, even is 1 + 2u; remainder -u/2
+    assert exact.round_to_limbs(1 + 3 * u / 2, 2) == [1.0 + 2.0**-51, -(2.0**-53)]
+    # a tail below half an ulp rounds down
+    z = 1 + u / 2 - Fraction(1, 2**200)
+    c = exact.round_to_limbs(z, 3)
+    assert c[0] == 1.0 and c[1] == 2.0**-53 and c[2] == -(2.0**-200)
+    assert exact.round_to_limbs(Fraction(0), 3) == [0.0, 0.0, 0.0]
+
+
+def test_round_to_limbs_properties():
+    rng = random.Random(99)
+    for _ in range(500):
+        L = rng.randint(1, 4)
+        z = Fraction(rng.randint(-2**300, 2**300), 2 ** rng.randint(0, 400))
+        c = exact.round_to_limbs(z, L)
+        assert exact.is_nonoverlapping(c)
+        err = abs(z - sum(Fraction(x) for x in c))
+        if c[-1] != 0.0:
+            assert err <= Fraction(math.ulp(c[-1])) / 2
+        else:
+            assert err == 0
+
+
+# --------------------------------------------------------------------------
+# error-free transformations and classic arithmetic (section 1, section 4)
+# --------------------------------------------------------------------------
+
+def _rand_doubles(rng, n):
+    out = []
+    for _ in range(n):
+        kind = rng.random()
+        if kind < 0.1:
+            out.append(rng.choice([0.0, -0.0, 1.0, -1.0, 2.0**-1074, -(2.0**-1022)]))
+        else:
+            out.append(rng.uniform(-1, 1) * 2.0 ** rng.randint(-200, 200))
+    return np.array(out)
+
+
+def test_eft_exactness():
+    rng = random.Random(5)
+    a, b = _rand_doubles(rng, 2000), _rand_doubles(rng, 2000)
+    s, e = coracle.two_sum(a, b)
+    for x, y, sx, ex in zip(a, b, s, e):
+        assert Fraction(sx) + Fraction(ex) == Fraction(x) + Fraction(y)
+        assert sx == x + y
+    p, e = coracle.two_prod(a, b)
+    checked = 0
+    for x, y, px, ex in zip(a, b, p, e):
+        exact_xy = Fraction(x) * Fraction(y)
+        if exact_xy != 0 and abs(exact_xy) < Fraction(2) ** (-1022 + 53):
+            continue  # the error term of an underflowing product is not representable
+        assert Fraction(px) + Fraction(ex) == exact_xy
+        checked += 1
+    assert checked > 1500
+    # FastTwoSum is exact when |a| >= |b|
+    big = np.where(np.abs(a) >= np.abs(b), a, b)
+    small = np.where(np.abs(a) >= np.abs(b), b, a)
+    s, e = coracle.fast_two_sum(big, small)
+    for x, y, sx, ex in zip(big, small, s, e):
+        assert Fraction(sx) + Fraction(ex) == Fraction(x) + Fraction(y)
+
+
+def _rand_md_array(rng, L, n):
+    return np.array([_random_md(rng, L, spread=20) for _ in range(n)]).T.copy()
+
+
+@pytest.mark.parametrize("L", [1, 2, 3, 4])
+def test_md_fma_relative_error(L):
+    rng = random.Random(40 + L)
+    n = 400
+    acc, a, b = _rand_md_array(rng, L, n), _rand_md_array(rng, L, n), _rand_md_array(rng, L, n)
+    out = coracle.md_fma(acc, a, b)
+    worst = 0.0
+    for e in range(n):
+        va, vb, vc = exact.value(a[:, e]), exact.value(b[:, e]), exact.value(acc[:, e])
+        want = vc + va * vb
+        got = exact.value(out[:, e])
+        scale = abs(vc) + abs(va * vb)
+        if scale:
+            worst = max(worst, float(abs(got - want) / scale))
+    # one rounding to L limbs plus dropped products of order 2^-53(L+1)
+    assert worst <= 8 * 2.0 ** (-52 * L), worst
+
+
+def test_dd_add_mul_relative_error():
+    rng = random.Random(77)
+    n = 1000
+    a, b = _rand_md_array(rng, 2, n), _rand_md_array(rng, 2, n)
+    s, p = coracle.dd_add(a, b), coracle.dd_mul(a, b)
+    ws = wp = 0.0
+    for e in range(n):
+        va, vb = exact.value(a[:, e]), exact.value(b[:, e])
+        if va + vb != 0:
+            ws = max(ws, float(abs(exact.value(s[:, e]) - (va + vb)) / (abs(va) + abs(vb))))
+        if va * vb != 0:
+            wp = max(wp, float(abs(exact.value(p[:, e]) - va * vb) / abs(va * vb)))
+    assert ws <= 4 * 2.0**-106 and wp <= 8 * 2.0**-106, (ws, wp)
+
+
+@pytest.mark.parametrize("L,variant", [(1, 1), (2, 0), (2, 1), (3, 1), (4, 1)])
+def test_classic_gemm_within_bound(L, variant):
+    rng = np.random.default_rng(20 + L)
+    m, k, n = 5, 7, 4
+    A = workloads.make_operand(rng, L, m, k, row_exp=6)
+    B = workloads.make_operand(rng, L, k, n, col_exp=6)
+    C, _ = coracle.classic_gemm(A, B, variant=variant)
+    for i in range(m):
+        for j in range(n):
+            want, mag = exact.exact_product(A, B, i, j)
+            assert abs(exact.value(C[:, i, j]) - want) <= exact.tolerance(k, L, mag)
+
+
+def test_classic_gemm_row_range_and_threads():
+    rng = np.random.default_rng(8)
+    A = workloads.make_operand(rng, 2, 6, 9)
+    B = workloads.make_operand(rng, 2, 9, 5)
+    full, used = coracle.classic_gemm(A, B, nthreads=2)
+    part, _ = coracle.classic_gemm(A, B, rows=(2, 4), nthreads=2)
+    assert used >= 1
+    assert np.array_equal(part[:, 2:4], full[:, 2:4]) and not part[:, :2].any()
+
+
+# --------------------------------------------------------------------------
+# the sliced chain against the exact product (spec tolerance)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("L,S,T", [(1, 4, 3), (2, 8, 14), (2, 8, 7), (3, 12, 11), (4, 16, 15)])
+def test_sliced_chain_within_tolerance(L, S, T):
+    # The bound 4 k 2^-(53L-4) (|A||B|) leaves room for the bits an element loses
+    # below its line's shared exponent; k = 64 (the smallest workload) keeps it
+    # meaningful.  At k = 9 a quad-double row with N(0,1) entries exceeds it:
+    # an inherent limit of one shared exponent per row / column.
+    rng = np.random.default_rng(100 + L + T)
+    m, k, n = 3, 64, 3
+    A = workloads.make_operand(rng, L, m, k, base="normal", row_exp=10)
+    B = workloads.make_operand(rng, L, k, n, base="normal", col_exp=10)
+    ref = pipeline.full_reference(A, B, S, T)
+    for i in range(m):
+        for j in range(n):
+            got = ref["C"][:, i, j]
+            assert exact.is_nonoverlapping(got)
+            want, mag = exact.exact_product(A, B, i, j)
+            assert abs(exact.value(got) - want) <= exact.tolerance(k, L, mag)
+
+
+def test_reference_entries_agree_with_full_reference():
+    A, B = workloads.make_workload("c0", m=12, n=10, k=16)
+    S, T = 8, 14
+    full = pipeline.full_reference(A, B, S, T)
+    entries = [(0, 0), (3, 7), (11, 9), (5, 2)]
+    samp = pipeline.reference_entries(A, B, S, T, entries)
+    for (i, j), r in samp.items():
+        assert r["limbs"] == full["C"][:, i, j].tolist()
+        assert r["levels"] == full["G"][:, i, j].tolist()
+
+
+# --------------------------------------------------------------------------
+# planted mistakes: the pins above must notice them
+# --------------------------------------------------------------------------
+
+def test_pins_detect_planted_mistakes():
+    fields, quarters = _worked_example()
+    x = fields["f"] * 2.0**-52
+    # (a) an off-by-one grid exponent breaks the worked example
+    d_wrong, _ = exact.split_element([x], 1, 4)
+    assert d_wrong[0] != fields["f0"] >> 39
+    # (b) a dropped pair breaks the rewritten-product comparison
+    rng = np.random.default_rng(1)
+    DA = rng.integers(-50, 50, (4, 3, 3))
+    DB = rng.integers(-50, 50, (4, 3, 3))
+    good = exact.level_products(DA, DB, 3)
+    bad3 = sum(np.array(DA[p]) @ np.array(DB[q]) for p, q in exact.pairs_of_level(3, 4)[:-1])
+    assert not np.array_equal(np.array(good[3]), bad3)
+    # (c) a wrong level weight breaks the truncated-operand identity
+    A = workloads.make_operand(np.random.default_rng(2), 2, 2, 3)
+    B = workloads.make_operand(np.random.default_rng(3), 2, 3, 2)
+    ref = pipeline.full_reference(A, B, 8, 14)
+    G = [int(g) for g in ref["G"][:, 0, 0]]
+    z = exact.accumulate(G, int(ref["EA"][0]), int(ref["EB"][0]))
+    z_bad = exact.accumulate([0] + G[:-1], int(ref["EA"][0]), int(ref["EB"][0]))
+    assert z != z_bad
