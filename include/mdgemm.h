@@ -1,0 +1,167 @@
+/*
+ * mdgemm -- multiple-double matrix product C = A.B on one AMD Instinct MI355X (gfx950).
+ *
+ * Method (Chen and Verschelde, "Multiple Double Arithmetic on NVIDIA Tensor Cores"):
+ * every multiple double (section 1: an unevaluated sum of nonoverlapping doubles)
+ * of A is placed on one power-of-two grid shared by its row, and every element of
+ * B on one grid shared by its column (section 3, balancing); its exact value is
+ * then cut into S signed 13-bit integer digits (section 2, the 52-bit fraction
+ * split into 13-bit quarters with exponents 0, -13, -26, -39).  Products of digits
+ * need at most 26 bits, so sums of them are exact in FP64 while they stay below
+ * 2^53 (section 2, the bound (NBound)).  The digit pairs (p, q) with p + q <= T are
+ * multiplied as plain FP64 GEMMs on the matrix cores, pairs of one level t = p + q
+ * summed together (section 2, equation (3) and the rewritten product); the levels
+ * are added exactly in increasing significance and rounded into L nonoverlapping
+ * limbs (section 2, steps 4-5 of the overview; section 1, renormalization).
+ *
+ * Conventions shared by every entry point
+ *  - All array pointers are DEVICE pointers (hipMalloc, or PyTorch tensors on the
+ *    GPU).  The caller allocates and owns every array.  Arrays are contiguous,
+ *    limb-major (or digit/level-major), row-major planes:
+ *        A [L][m][k]:  A[l*m*k + i*k + kk]      (limb 0 most significant)
+ *        B [L][k][n]:  B[l*k*n + kk*n + j]
+ *        C [L][m][n]:  C[l*m*n + i*n + j]
+ *  - Inputs are never modified.  Outputs are fully overwritten and must not
+ *    overlap any input.
+ *  - Every call is asynchronous and ordered on `stream` (a hipStream_t; NULL is
+ *    the default stream) unless MDGEMM_SYNC is set.  No C++ exception crosses the
+ *    ABI; errors are returned as status codes.  Argument errors are detected on
+ *    the host before any HIP call.
+ *  - Inputs must be finite and normalized: for each element and limb l,
+ *    |x[l+1]| <= ulp(x[l])/2, and x[l] == 0 implies x[l+1] == 0.  Otherwise the
+ *    result is unspecified (MDGEMM_CHECK_FINITE detects non-finite limbs).
+ *  - Output limbs whose magnitude falls below 2^-1022 (subnormal) are rounded by
+ *    the final power-of-two scaling and are then no longer the exact greedy
+ *    rounding; the products this library is built for stay far from that range.
+ */
+#ifndef MDGEMM_H
+#define MDGEMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------------- */
+#define MDGEMM_OK 0
+#define MDGEMM_EINVAL -1      /* invalid size, limb/slice/cutoff count, null or overlapping pointer */
+#define MDGEMM_EEXACT -2      /* pairs_t * k * 8191^2 >= 2^53 for some kept level t: sums not exact */
+#define MDGEMM_ENOMEM -3      /* the library's own workspace could not be allocated */
+#define MDGEMM_EHIP -4        /* a HIP call failed (no device, launch or runtime error) */
+#define MDGEMM_EWORKSPACE -5  /* the caller's workspace is smaller than mdgemm_workspace_bytes() */
+#define MDGEMM_ENONFINITE -6  /* MDGEMM_CHECK_FINITE: an input limb is inf or nan */
+
+/* ---- limits ---------------------------------------------------------------- */
+#define MDGEMM_MAX_LIMBS 4    /* double, double-double, triple-double, quad-double */
+#define MDGEMM_MAX_SLICES 16  /* digits per element */
+#define MDGEMM_SLICE_BITS 13
+#define MDGEMM_Z_WORDS 8      /* 64-bit words per element written by mdgemm_accumulate */
+
+/* ---- flags for mdgemm_opts.flags ------------------------------------------- */
+#define MDGEMM_CHECK_FINITE 1u /* scan A and B for inf/nan first; synchronizes the stream */
+#define MDGEMM_SYNC 2u         /* synchronize the stream before returning and report kernel errors */
+#define MDGEMM_TIME_STAGES 4u  /* record HIP events between stages; read with mdgemm_stage_times() */
+
+/* cutoff selectors for mdgemm_opts.cutoff (else an explicit T in 0 .. 2S-2) */
+#define MDGEMM_CUTOFF_DEFAULT -1  /* T = S - 1: the pair set of the rewritten product */
+#define MDGEMM_CUTOFF_ALL -2      /* T = 2S - 2: every slice pair */
+
+typedef struct mdgemm_opts {
+  void* stream;           /* hipStream_t to launch on; NULL = default stream */
+  void* workspace;        /* caller-owned device buffer; NULL = library-owned cache */
+  size_t workspace_bytes; /* size of `workspace` in bytes */
+  int slices_per_limb;    /* digits per limb, S = limbs * slices_per_limb <= 16; 0 = 4 */
+  int cutoff;             /* largest kept p + q; MDGEMM_CUTOFF_DEFAULT or _ALL or 0..2S-2 */
+  unsigned flags;         /* MDGEMM_CHECK_FINITE | MDGEMM_SYNC | MDGEMM_TIME_STAGES */
+} mdgemm_opts;
+
+/* Fill `opts` with the defaults: default stream, library workspace, 4 slices per
+ * limb, cutoff T = S - 1, no flags. */
+void mdgemm_opts_init(mdgemm_opts* opts);
+
+/* C = A.B for L-limb operands (L = limbs in 1..4) with the default options.
+ * m, n, k >= 0; m == 0 or n == 0 does nothing; k == 0 writes C = +0.0.
+ * Returns MDGEMM_OK or a negative status. */
+int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C);
+
+/* Bytes of device workspace mdgemm_ex needs for this product and these options
+ * (0 for an empty product; SIZE_MAX for invalid arguments).  Layout, each part
+ * aligned to 256 bytes: EA int32[m], EB int32[n], flag int32, DA f64[S][m][k],
+ * DB f64[S][k][n], G f64[T+1][m][n]. */
+size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts);
+
+/* C = A.B with explicit options (opts may be NULL for the defaults).  Runs, in
+ * stream order: row exponents of A and column exponents of B, the splits of A
+ * and B into digits, the level GEMMs, and the exact accumulation and rounding
+ * into C.  With a caller workspace smaller than mdgemm_workspace_bytes() it
+ * returns MDGEMM_EWORKSPACE and launches nothing. */
+int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
+              const mdgemm_opts* opts);
+
+/* Milliseconds spent in each stage of the last mdgemm_ex call that set
+ * MDGEMM_TIME_STAGES on this process: ms[0] exponents, ms[1] splits,
+ * ms[2] level GEMMs, ms[3] accumulation and rounding.  Waits for that call's
+ * last event.  Writes min(count, 4) values and returns how many, or a negative
+ * status.  Not meant for concurrent timed calls from several threads. */
+int mdgemm_stage_times(float* ms, int count);
+
+/* Static text for a status code. */
+const char* mdgemm_status_string(int status);
+
+/* Free the library-owned workspace of every device (after synchronizing them). */
+void mdgemm_release(void);
+
+/* ---- stage entry points (the same kernels as mdgemm_ex) --------------------- */
+
+/* Step a1, balancing (section 3; per-line grid after the worked example of
+ * section 2).  X0 is the leading-limb plane [rows][cols].  axis 0: E[i] for every
+ * row i (E has `rows` entries); axis 1: E[j] for every column j (`cols` entries).
+ * E = the largest frexp exponent (x = f 2^E, 1/2 <= |f| < 1) of a nonzero entry of
+ * the line; 0 for an all-zero line.  Subnormals get their true exponent. */
+int mdgemm_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, void* stream);
+
+/* Step a2, the exact split (section 2 worked example; sections 2-3 balancing and
+ * the opposite-sign transfer).  X [limbs][rows][cols], E from mdgemm_exponents
+ * with the same axis, D [slices][rows][cols] (float64, integer valued).  For each
+ * element with exact value V on grid exponent E: D_abs = floor(|V| / 2^(E - 13 S)),
+ * digit s = sign(V) * bits 13(S-1-s) .. 13(S-s)-1 of D_abs, so that
+ * V = sum_s digit_s 2^(E - 13(s+1)) + R with |R| < 2^(E - 13 S) and R V >= 0.
+ * Zero digits are +0.0.  Requires |V| < 2^E (true for normalized input and the
+ * exponents of mdgemm_exponents).  limbs 1..4, slices 1..16. */
+int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int axis, const double* X, const int32_t* E,
+                 double* D, void* stream);
+
+/* Step a3, the slice GEMMs (section 2, equation (3) and the rewritten product).
+ * DA [S][m][k], DB [S][k][n] integer-valued digits with |digit| <= 8191.
+ * per_pair == 0: out [T+1][m][n], out[t] = sum over p + q = t (0 <= p, q < S) of
+ * DA_p . DB_q for t = 0..cutoff.  per_pair != 0: out [S][S][m][n],
+ * out[p][q] = DA_p . DB_q for every p + q <= cutoff (other planes untouched).
+ * Exact in FP64 (any summation order) because every partial sum is an integer
+ * below 2^53; returns MDGEMM_EEXACT when pairs_t * k * 8191^2 >= 2^53.
+ * S in 1..16, cutoff in 0..2S-2. */
+int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, int per_pair, const double* DA,
+                      const double* DB, double* out, void* stream);
+
+/* Step a4 alone, the exact accumulation (section 2, steps 4-5), exported for
+ * checking.  G [levels][m][n] integer-valued with |G| < 2^53, levels 1..31.
+ * Writes the integer N = sum_t G_t 2^(13 (levels-1-t)) as MDGEMM_Z_WORDS 64-bit
+ * two's-complement words, least significant first: Z [8][m][n] int64.  The
+ * accumulated value is N 2^(-13 (levels-1)) (before the grid scale). */
+int mdgemm_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, void* stream);
+
+/* Steps a4 + a5: exact accumulation of the levels and rounding into `limbs`
+ * nonoverlapping doubles (section 1, renormalization; section 2, adding the parts
+ * into a multiple double), times the grid scale 2^(EA[i] + EB[j] - 26):
+ * with Z = sum_t G_t 2^(-13 t), C[.][i][j] = (c_0, .., c_{L-1}) 2^(EA[i]+EB[j]-26)
+ * where c_0 = RN(Z) and c_l = RN(Z - c_0 - .. - c_{l-1}) (round to nearest, ties
+ * to even).  G [levels][m][n], EA int32[m], EB int32[n], C [limbs][m][n]. */
+int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, const double* G, const int32_t* EA,
+                        const int32_t* EB, double* C, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MDGEMM_H */

@@ -1,0 +1,62 @@
+"""Compile ``libmdgemm.so`` (the HIP kernels and the C ABI) for gfx950.
+
+Flags:
+* ``--offload-arch=gfx950``: MI355X (CDNA4) code only.
+* ``-mllvm -amdgpu-mfma-vgpr-form=1``: keep MFMA accumulators in ordinary
+  VGPRs; otherwise the compiler copies loop-carried accumulators between
+  AGPRs and VGPRs around every MFMA block, which costs about a third of the
+  FP64 matrix-core throughput.
+* ``-Xclang -target-feature -Xclang -packed-fp32-ops``: no packed-FP32
+  instructions are generated (none of these kernels needs them).
+"""
+
+from __future__ import annotations
+
+import glob
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+SOURCES = sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
+INCLUDE = os.path.join(ROOT, "include")
+LIB = os.path.join(HERE, "libmdgemm.so")
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+FLAGS = [
+    "--offload-arch=gfx950",
+    "-O3",
+    "-std=c++17",
+    "-fPIC",
+    "-shared",
+    "-Wall",
+    "-Wno-unused-result",
+    "-mllvm",
+    "-amdgpu-mfma-vgpr-form=1",
+    "-Xclang",
+    "-target-feature",
+    "-Xclang",
+    "-packed-fp32-ops",
+]
+
+
+def build(verbose: bool = False) -> str:
+    tmp = LIB + ".tmp"
+    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-I", os.path.join(HERE, "csrc"), "-o", tmp, *SOURCES]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    proc = subprocess.run(cmd, capture_output=True, text=True)
+    noise = "unknown target feature"  # the host pass does not know -packed-fp32-ops
+    msgs = [ln for ln in (proc.stdout + proc.stderr).splitlines() if noise not in ln and "packed-fp32-ops" not in ln]
+    if proc.returncode != 0:
+        raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
+    if verbose and msgs:
+        print("\n".join(msgs))
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))
+    sys.exit(0)

@@ -1,0 +1,219 @@
+// Steps a4 and a5 -- exact accumulation of the level products and rounding
+// into nonoverlapping limbs.
+//
+// Section 2 (steps 4 and 5 of the overview) extracts the parts of the product
+// and adds them into a multiple double on the regular cores, a massively
+// parallel summation of the levels of every output element.  Section 1
+// (renormalization) requires the result to be a sum of nonoverlapping doubles.
+//
+// Level t of an output element is an integer G_t, |G_t| < 2^53, of weight
+// 2^(-13 t) (times the grid scale 2^(EA + EB - 26)).  Their sum is formed
+// exactly, in increasing significance (t = T down to 0), as the two's-complement
+// integer N = sum_t G_t 2^(13 (T - t)) held in NW 64-bit words in registers;
+// the value is Z = N 2^(-13 T).  The L limbs are then peeled off greedily with
+// round-to-nearest-even: c_0 = RN(Z), c_1 = RN(Z - c_0), ..., each taken from
+// the 53 leading bits of the remaining magnitude with the round bit and the
+// sticky bits below it; when a limb rounds up, the remainder changes sign.  The
+// result is the canonical nonoverlapping representation, |c_{l+1}| <= ulp(c_l)/2.
+//
+// One thread per output element; consecutive threads take consecutive columns,
+// so the T + 1 level loads and the L limb stores are contiguous 512-byte rows.
+#include "internal.h"
+
+namespace mdg {
+namespace {
+
+// N += g 2^sh (g sign-extended), modulo 2^(64 NW).
+template <int NW>
+__device__ inline void add_shifted_signed(uint64_t (&N)[NW], int64_t g, int sh) {
+  const int w = sh >> 6, b = sh & 63;
+  const uint64_t lo = static_cast<uint64_t>(g) << b;
+  const uint64_t hi = b ? static_cast<uint64_t>(g >> (64 - b)) : static_cast<uint64_t>(g >> 63);
+  const uint64_t ext = static_cast<uint64_t>(g >> 63);  // 0 or all ones
+  uint64_t carry = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const uint64_t t = (i < w) ? 0ull : ((i == w) ? lo : ((i == w + 1) ? hi : ext));
+    const uint64_t s = N[i] + t;
+    const uint64_t c1 = s < t;
+    const uint64_t s2 = s + carry;
+    const uint64_t c2 = s2 < s;
+    N[i] = s2;
+    carry = c1 | c2;
+  }
+}
+
+template <int NW>
+__device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __restrict__ G, int levels, int64_t plane,
+                                         int64_t idx) {
+#pragma unroll
+  for (int i = 0; i < NW; ++i) N[i] = 0;
+  const int T = levels - 1;
+  for (int t = T; t >= 0; --t) {
+    const int64_t g = static_cast<int64_t>(G[static_cast<int64_t>(t) * plane + idx]);  // exact: |G_t| < 2^53
+    if (g != 0) add_shifted_signed<NW>(N, g, kSliceBits * (T - t));
+  }
+}
+
+// Bit `pos` (0 <= pos < 64 NW) of v.
+template <int NW>
+__device__ inline uint64_t word_at(const uint64_t (&v)[NW], int w) {
+  uint64_t r = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) r = (i == w) ? v[i] : r;
+  return r;
+}
+
+template <int NW>
+__device__ inline void round_limbs(uint64_t (&N)[NW], int L, int scale, double* __restrict__ C, int64_t plane,
+                                   int64_t idx) {
+  // sign and magnitude
+  bool neg = (N[NW - 1] >> 63) != 0;
+  if (neg) {
+    uint64_t carry = 1;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const uint64_t v = ~N[i] + carry;
+      carry = (carry && v == 0) ? 1ull : 0ull;
+      N[i] = v;
+    }
+  }
+  for (int l = 0; l < L; ++l) {
+    // position of the leading one
+    int h = -1;
+#pragma unroll
+    for (int i = 0; i < NW; ++i)
+      if (N[i] != 0) h = 64 * i + 63 - __clzll(static_cast<long long>(N[i]));
+    double c;
+    if (h < 0) {
+      c = 0.0;
+    } else if (h <= 52) {
+      const double v = static_cast<double>(N[0]);  // below 2^53: exact
+      c = ldexp(neg ? -v : v, scale);
+#pragma unroll
+      for (int i = 0; i < NW; ++i) N[i] = 0;
+    } else {
+      const int sh = h - 52;  // the 53 leading bits start at bit sh
+      const int w = sh >> 6, b = sh & 63;
+      const uint64_t lo = word_at<NW>(N, w), hi = word_at<NW>(N, w + 1);
+      uint64_t M = (lo >> b) | (b ? (hi << (64 - b)) : 0ull);
+      M &= 0x001fffffffffffffull;
+      // round bit (bit sh-1) and sticky (any bit below sh-1)
+      const int rpos = sh - 1, rw = rpos >> 6, rb = rpos & 63;
+      const uint64_t rword = word_at<NW>(N, rw);
+      const bool round_bit = ((rword >> rb) & 1ull) != 0;
+      bool sticky = (rword & ((1ull << rb) - 1ull)) != 0;
+#pragma unroll
+      for (int i = 0; i < NW; ++i) sticky |= (i < rw) && (N[i] != 0);
+      const bool up = round_bit && (sticky || (M & 1ull));
+      const double v = static_cast<double>(M + (up ? 1ull : 0ull));  // <= 2^53: exact
+      c = ldexp(neg ? -v : v, scale + sh);
+      // remainder: the bits below sh, or 2^sh minus them (and the sign flips)
+#pragma unroll
+      for (int i = 0; i < NW; ++i) {
+        const int lo_bit = 64 * i;
+        uint64_t keep;
+        if (lo_bit + 64 <= sh) keep = ~0ull;
+        else if (lo_bit >= sh) keep = 0ull;
+        else keep = (1ull << (sh - lo_bit)) - 1ull;
+        N[i] &= keep;
+      }
+      if (up) {
+        uint64_t carry = 1;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) {
+          const int lo_bit = 64 * i;
+          uint64_t keep;
+          if (lo_bit + 64 <= sh) keep = ~0ull;
+          else if (lo_bit >= sh) keep = 0ull;
+          else keep = (1ull << (sh - lo_bit)) - 1ull;
+          const uint64_t v = ~N[i] + carry;
+          carry = (carry && v == 0) ? 1ull : 0ull;
+          N[i] = v & keep;
+        }
+        neg = !neg;
+      }
+    }
+    C[static_cast<int64_t>(l) * plane + idx] = c;
+  }
+}
+
+template <int NW>
+__global__ void __launch_bounds__(256) accum_renorm_kernel(int64_t m, int64_t n, int L, int levels,
+                                                           const double* __restrict__ G,
+                                                           const int32_t* __restrict__ EA,
+                                                           const int32_t* __restrict__ EB, double* __restrict__ C) {
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  const int64_t plane = m * n;
+  const int ebj = EB[j];
+  for (int64_t i = blockIdx.y; i < m; i += gridDim.y) {
+    const int64_t idx = i * n + j;
+    uint64_t N[NW];
+    accumulate_levels<NW>(N, G, levels, plane, idx);
+    const int scale = EA[i] + ebj - 2 * kSliceBits - kSliceBits * (levels - 1);
+    round_limbs<NW>(N, L, scale, C, plane, idx);
+  }
+}
+
+template <int NW>
+__global__ void __launch_bounds__(256) accumulate_kernel(int64_t m, int64_t n, int levels,
+                                                         const double* __restrict__ G, int64_t* __restrict__ Z) {
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  const int64_t plane = m * n;
+  for (int64_t i = blockIdx.y; i < m; i += gridDim.y) {
+    const int64_t idx = i * n + j;
+    uint64_t N[NW];
+    accumulate_levels<NW>(N, G, levels, plane, idx);
+    const uint64_t ext = (N[NW - 1] >> 63) ? ~0ull : 0ull;
+    for (int w = 0; w < kZWords; ++w) Z[static_cast<int64_t>(w) * plane + idx] = static_cast<int64_t>(w < NW ? word_at<NW>(N, w) : ext);
+  }
+}
+
+// Words for |N| < 2^(13 T + 54) plus a sign bit.
+inline int words_for_levels(int levels) {
+  const int bits = kSliceBits * (levels - 1) + 55;
+  return (bits + 63) / 64;
+}
+
+inline dim3 elem_grid(int64_t m, int64_t n) {
+  return dim3(static_cast<unsigned>((n + 255) / 256), static_cast<unsigned>(m < 65535 ? m : 65535));
+}
+
+}  // namespace
+
+hipError_t launch_accum_renorm(int64_t m, int64_t n, int L, int levels, const double* G, const int32_t* EA,
+                               const int32_t* EB, double* C, hipStream_t stream) {
+  if (m == 0 || n == 0) return hipSuccess;
+  const dim3 grid = elem_grid(m, n);
+  switch (words_for_levels(levels)) {
+    case 1:
+    case 2: hipLaunchKernelGGL(accum_renorm_kernel<2>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
+    case 3: hipLaunchKernelGGL(accum_renorm_kernel<3>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
+    case 4: hipLaunchKernelGGL(accum_renorm_kernel<4>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
+    case 5: hipLaunchKernelGGL(accum_renorm_kernel<5>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
+    case 6: hipLaunchKernelGGL(accum_renorm_kernel<6>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
+    case 7: hipLaunchKernelGGL(accum_renorm_kernel<7>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, hipStream_t stream) {
+  if (m == 0 || n == 0) return hipSuccess;
+  const dim3 grid = elem_grid(m, n);
+  switch (words_for_levels(levels)) {
+    case 1:
+    case 2: hipLaunchKernelGGL(accumulate_kernel<2>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
+    case 3: hipLaunchKernelGGL(accumulate_kernel<3>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
+    case 4: hipLaunchKernelGGL(accumulate_kernel<4>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
+    case 5: hipLaunchKernelGGL(accumulate_kernel<5>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
+    case 6: hipLaunchKernelGGL(accumulate_kernel<6>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
+    case 7: hipLaunchKernelGGL(accumulate_kernel<7>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mdg

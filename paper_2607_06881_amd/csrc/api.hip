@@ -1,0 +1,426 @@
+// Host side of libmdgemm: argument checks, workspace, job tables, stage timing
+// and the exported C ABI declared in include/mdgemm.h.
+//
+// The product C = A.B of multiple doubles follows the five steps of the
+// overview in section 2 of Chen and Verschelde, "Multiple Double Arithmetic on
+// NVIDIA Tensor Cores": split into parts, rewrite as products of doubles, run
+// the products on the matrix cores, extract the parts, add them into a multiple
+// double.  mdgemm_ex enqueues, on one stream, the kernels of the four stages:
+// exponents (a1), splits (a2), level GEMMs (a3), accumulation and rounding
+// (a4 + a5).
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "internal.h"
+#include "mdgemm.h"
+
+namespace {
+
+using mdg::JobTable;
+
+constexpr size_t kAlign = 256;
+constexpr int kStages = 4;
+
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// ---- exactness: pairs_t * k * 8191^2 < 2^53 for every kept level t ------------
+
+int max_pairs(int S, int T) {
+  int best = 0;
+  for (int t = 0; t <= T; ++t) {
+    int lo = t - (S - 1) > 0 ? t - (S - 1) : 0;
+    int hi = t < S - 1 ? t : S - 1;
+    if (hi - lo + 1 > best) best = hi - lo + 1;
+  }
+  return best;
+}
+
+bool exact_ok(int64_t k, int pairs) {
+  const unsigned __int128 lhs =
+      static_cast<unsigned __int128>(pairs) * static_cast<unsigned __int128>(k) * (8191u * 8191u);
+  return lhs < (static_cast<unsigned __int128>(1) << 53);
+}
+
+// ---- job tables ---------------------------------------------------------------
+
+// Levels t = 0..T, heaviest (most pairs) first so that long K loops start early.
+JobTable level_jobs(int S, int T) {
+  JobTable jt;
+  std::memset(&jt, 0, sizeof jt);
+  std::vector<int> order;
+  for (int t = 0; t <= T; ++t) order.push_back(t);
+  auto npairs = [S](int t) {
+    int lo = t - (S - 1) > 0 ? t - (S - 1) : 0;
+    int hi = t < S - 1 ? t : S - 1;
+    return hi - lo + 1;
+  };
+  // stable sort by decreasing pair count
+  for (size_t i = 1; i < order.size(); ++i)
+    for (size_t j = i; j > 0 && npairs(order[j]) > npairs(order[j - 1]); --j) std::swap(order[j], order[j - 1]);
+  jt.njobs = static_cast<int>(order.size());
+  for (int j = 0; j < jt.njobs; ++j) {
+    int t = order[j];
+    int lo = t - (S - 1) > 0 ? t - (S - 1) : 0;
+    jt.p_first[j] = static_cast<uint8_t>(lo);
+    jt.q_first[j] = static_cast<uint8_t>(t - lo);
+    jt.npairs[j] = static_cast<uint8_t>(npairs(t));
+    jt.out[j] = static_cast<uint8_t>(t);
+  }
+  return jt;
+}
+
+// Every pair (p, q) with p + q <= T, written to plane p*S + q.
+JobTable pair_jobs(int S, int T) {
+  JobTable jt;
+  std::memset(&jt, 0, sizeof jt);
+  int j = 0;
+  for (int p = 0; p < S; ++p)
+    for (int q = 0; q < S; ++q) {
+      if (p + q > T) continue;
+      jt.p_first[j] = static_cast<uint8_t>(p);
+      jt.q_first[j] = static_cast<uint8_t>(q);
+      jt.npairs[j] = 1;
+      jt.out[j] = static_cast<uint8_t>(p * S + q);
+      ++j;
+    }
+  jt.njobs = j;
+  return jt;
+}
+
+// ---- options ----------------------------------------------------------------
+
+struct Resolved {
+  int S = 0, T = 0;
+  hipStream_t stream = nullptr;
+  unsigned flags = 0;
+};
+
+int resolve(int limbs, const mdgemm_opts* opts, Resolved* r) {
+  if (limbs < 1 || limbs > MDGEMM_MAX_LIMBS) return MDGEMM_EINVAL;
+  int spl = opts ? opts->slices_per_limb : 0;
+  if (spl == 0) spl = 4;
+  if (spl < 0 || spl * limbs > MDGEMM_MAX_SLICES) return MDGEMM_EINVAL;
+  r->S = spl * limbs;
+  int cutoff = opts ? opts->cutoff : MDGEMM_CUTOFF_DEFAULT;
+  if (cutoff == MDGEMM_CUTOFF_DEFAULT)
+    r->T = r->S - 1;
+  else if (cutoff == MDGEMM_CUTOFF_ALL)
+    r->T = 2 * r->S - 2;
+  else if (cutoff >= 0 && cutoff <= 2 * r->S - 2)
+    r->T = cutoff;
+  else
+    return MDGEMM_EINVAL;
+  r->stream = opts ? static_cast<hipStream_t>(opts->stream) : nullptr;
+  r->flags = opts ? opts->flags : 0u;
+  return MDGEMM_OK;
+}
+
+struct Layout {
+  size_t ea = 0, eb = 0, flag = 0, da = 0, db = 0, g = 0, total = 0;
+};
+
+bool layout(int64_t m, int64_t n, int64_t k, const Resolved& r, Layout* L) {
+  // all products below 2^62 so that size arithmetic cannot overflow
+  const double approx = (double)r.S * (double)m * (double)k + (double)r.S * (double)k * (double)n +
+                        (double)(r.T + 1) * (double)m * (double)n;
+  if (approx * 8.0 > 4.0e18) return false;
+  size_t off = 0;
+  L->ea = off;
+  off += align_up(sizeof(int32_t) * static_cast<size_t>(m));
+  L->eb = off;
+  off += align_up(sizeof(int32_t) * static_cast<size_t>(n));
+  L->flag = off;
+  off += align_up(sizeof(int32_t));
+  L->da = off;
+  off += align_up(sizeof(double) * static_cast<size_t>(r.S) * static_cast<size_t>(m) * static_cast<size_t>(k));
+  L->db = off;
+  off += align_up(sizeof(double) * static_cast<size_t>(r.S) * static_cast<size_t>(k) * static_cast<size_t>(n));
+  L->g = off;
+  off += align_up(sizeof(double) * static_cast<size_t>(r.T + 1) * static_cast<size_t>(m) * static_cast<size_t>(n));
+  L->total = off;
+  return true;
+}
+
+bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+  return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+// ---- library-owned workspace (one per device) ---------------------------------
+
+struct Cache {
+  std::mutex mu;
+  std::vector<void*> ptr;
+  std::vector<size_t> bytes;
+};
+Cache& cache() {
+  static Cache c;
+  return c;
+}
+
+int cached_workspace(size_t need, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MDGEMM_EHIP;
+  Cache& c = cache();
+  std::lock_guard<std::mutex> lock(c.mu);
+  if (static_cast<size_t>(dev) >= c.ptr.size()) {
+    c.ptr.resize(dev + 1, nullptr);
+    c.bytes.resize(dev + 1, 0);
+  }
+  if (c.bytes[dev] < need) {
+    if (c.ptr[dev]) {
+      if (hipDeviceSynchronize() != hipSuccess) return MDGEMM_EHIP;
+      (void)hipFree(c.ptr[dev]);
+      c.ptr[dev] = nullptr;
+      c.bytes[dev] = 0;
+    }
+    void* p = nullptr;
+    if (hipMalloc(&p, need) != hipSuccess) {
+      (void)hipGetLastError();
+      return MDGEMM_ENOMEM;
+    }
+    c.ptr[dev] = p;
+    c.bytes[dev] = need;
+  }
+  *out = c.ptr[dev];
+  return MDGEMM_OK;
+}
+
+// ---- stage timing ------------------------------------------------------------
+
+struct Timing {
+  std::mutex mu;
+  hipEvent_t ev[kStages + 1] = {};
+  bool created = false;
+  bool valid = false;
+};
+Timing& timing() {
+  static Timing t;
+  return t;
+}
+
+int record(int i, hipStream_t s) {
+  Timing& t = timing();
+  if (!t.created) {
+    for (auto& e : t.ev)
+      if (hipEventCreate(&e) != hipSuccess) return MDGEMM_EHIP;
+    t.created = true;
+  }
+  return hipEventRecord(t.ev[i], s) == hipSuccess ? MDGEMM_OK : MDGEMM_EHIP;
+}
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? MDGEMM_OK : MDGEMM_EHIP; }
+
+#define MDG_TRY(expr)              \
+  do {                             \
+    int st_ = (expr);              \
+    if (st_ != MDGEMM_OK) return st_; \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+void mdgemm_opts_init(mdgemm_opts* opts) {
+  if (!opts) return;
+  std::memset(opts, 0, sizeof *opts);
+  opts->slices_per_limb = 4;
+  opts->cutoff = MDGEMM_CUTOFF_DEFAULT;
+}
+
+const char* mdgemm_status_string(int status) {
+  switch (status) {
+    case MDGEMM_OK: return "success";
+    case MDGEMM_EINVAL: return "invalid argument";
+    case MDGEMM_EEXACT: return "slice sums would reach 2^53 (k too large for exact FP64 accumulation)";
+    case MDGEMM_ENOMEM: return "device memory allocation failed";
+    case MDGEMM_EHIP: return "HIP runtime error";
+    case MDGEMM_EWORKSPACE: return "workspace too small";
+    case MDGEMM_ENONFINITE: return "input contains inf or nan";
+    default: return "unknown status";
+  }
+}
+
+size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts) {
+  Resolved r;
+  if (m < 0 || n < 0 || k < 0 || resolve(limbs, opts, &r) != MDGEMM_OK) return SIZE_MAX;
+  if (m == 0 || n == 0 || k == 0) return 0;
+  Layout L;
+  if (!layout(m, n, k, r, &L)) return SIZE_MAX;
+  return L.total;
+}
+
+int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
+              const mdgemm_opts* opts) {
+  Resolved r;
+  if (m < 0 || n < 0 || k < 0) return MDGEMM_EINVAL;
+  MDG_TRY(resolve(limbs, opts, &r));
+  if (m == 0 || n == 0) return MDGEMM_OK;
+  if (!C || (k > 0 && (!A || !B))) return MDGEMM_EINVAL;
+  const size_t abytes = sizeof(double) * limbs * static_cast<size_t>(m) * static_cast<size_t>(k);
+  const size_t bbytes = sizeof(double) * limbs * static_cast<size_t>(k) * static_cast<size_t>(n);
+  const size_t cbytes = sizeof(double) * limbs * static_cast<size_t>(m) * static_cast<size_t>(n);
+  if (k > 0 && (overlaps(C, cbytes, A, abytes) || overlaps(C, cbytes, B, bbytes))) return MDGEMM_EINVAL;
+  if (!exact_ok(k, max_pairs(r.S, r.T))) return MDGEMM_EEXACT;
+  hipStream_t s = r.stream;
+  const bool timed = (r.flags & MDGEMM_TIME_STAGES) != 0;
+
+  if (k == 0) {
+    MDG_TRY(hip_status(mdg::launch_zero_f64(C, static_cast<int64_t>(limbs) * m * n, s)));
+    if (r.flags & MDGEMM_SYNC) MDG_TRY(hip_status(hipStreamSynchronize(s)));
+    return MDGEMM_OK;
+  }
+
+  Layout L;
+  if (!layout(m, n, k, r, &L)) return MDGEMM_EINVAL;
+  char* ws = nullptr;
+  if (opts && opts->workspace) {
+    if (opts->workspace_bytes < L.total) return MDGEMM_EWORKSPACE;
+    ws = static_cast<char*>(opts->workspace);
+  } else {
+    void* p = nullptr;
+    MDG_TRY(cached_workspace(L.total, &p));
+    ws = static_cast<char*>(p);
+  }
+  int32_t* EA = reinterpret_cast<int32_t*>(ws + L.ea);
+  int32_t* EB = reinterpret_cast<int32_t*>(ws + L.eb);
+  int32_t* flag = reinterpret_cast<int32_t*>(ws + L.flag);
+  double* DA = reinterpret_cast<double*>(ws + L.da);
+  double* DB = reinterpret_cast<double*>(ws + L.db);
+  double* G = reinterpret_cast<double*>(ws + L.g);
+
+  if (r.flags & MDGEMM_CHECK_FINITE) {
+    MDG_TRY(hip_status(mdg::launch_set_i32(flag, 1, 0, s)));
+    MDG_TRY(hip_status(mdg::launch_nonfinite_scan(A, static_cast<int64_t>(limbs) * m * k, flag, s)));
+    MDG_TRY(hip_status(mdg::launch_nonfinite_scan(B, static_cast<int64_t>(limbs) * k * n, flag, s)));
+    int32_t h = 0;
+    MDG_TRY(hip_status(hipMemcpyAsync(&h, flag, sizeof h, hipMemcpyDeviceToHost, s)));
+    MDG_TRY(hip_status(hipStreamSynchronize(s)));
+    if (h) return MDGEMM_ENONFINITE;
+  }
+
+  std::unique_lock<std::mutex> tlock(timing().mu, std::defer_lock);
+  if (timed) {
+    tlock.lock();
+    timing().valid = false;
+    MDG_TRY(record(0, s));
+  }
+  // a1: grid exponents per row of A and per column of B
+  MDG_TRY(hip_status(mdg::launch_exponents(m, k, 0, A, EA, s)));
+  MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, EB, s)));
+  if (timed) MDG_TRY(record(1, s));
+  // a2: exact splits into S digit planes
+  MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, 0, A, EA, DA, s)));
+  MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, 1, B, EB, DB, s)));
+  if (timed) MDG_TRY(record(2, s));
+  // a3: level GEMMs on the FP64 matrix cores
+  MDG_TRY(hip_status(mdg::launch_slice_gemm(m, n, k, DA, DB, G, level_jobs(r.S, r.T), s)));
+  if (timed) MDG_TRY(record(3, s));
+  // a4 + a5: exact accumulation and greedy rounding into L limbs
+  MDG_TRY(hip_status(mdg::launch_accum_renorm(m, n, limbs, r.T + 1, G, EA, EB, C, s)));
+  if (timed) {
+    MDG_TRY(record(4, s));
+    timing().valid = true;
+  }
+  if (r.flags & MDGEMM_SYNC) MDG_TRY(hip_status(hipStreamSynchronize(s)));
+  return MDGEMM_OK;
+}
+
+int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C) {
+  return mdgemm_ex(m, n, k, limbs, A, B, C, nullptr);
+}
+
+int mdgemm_stage_times(float* ms, int count) {
+  if (!ms || count < 0) return MDGEMM_EINVAL;
+  Timing& t = timing();
+  std::lock_guard<std::mutex> lock(t.mu);
+  if (!t.valid) return MDGEMM_EINVAL;
+  if (hipEventSynchronize(t.ev[kStages]) != hipSuccess) return MDGEMM_EHIP;
+  int w = count < kStages ? count : kStages;
+  for (int i = 0; i < w; ++i)
+    if (hipEventElapsedTime(&ms[i], t.ev[i], t.ev[i + 1]) != hipSuccess) return MDGEMM_EHIP;
+  return w;
+}
+
+void mdgemm_release(void) {
+  Cache& c = cache();
+  std::lock_guard<std::mutex> lock(c.mu);
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  for (size_t d = 0; d < c.ptr.size(); ++d) {
+    if (!c.ptr[d]) continue;
+    if (hipSetDevice(static_cast<int>(d)) == hipSuccess) {
+      (void)hipDeviceSynchronize();
+      (void)hipFree(c.ptr[d]);
+    }
+    c.ptr[d] = nullptr;
+    c.bytes[d] = 0;
+  }
+  (void)hipSetDevice(cur);
+}
+
+// ---- stage entry points ----------------------------------------------------------
+
+int mdgemm_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, void* stream) {
+  if (rows < 0 || cols < 0 || (axis != 0 && axis != 1)) return MDGEMM_EINVAL;
+  const int64_t lines = axis == 0 ? rows : cols;
+  if (lines == 0) return MDGEMM_OK;
+  if (!E || (rows > 0 && cols > 0 && !X0)) return MDGEMM_EINVAL;
+  return hip_status(mdg::launch_exponents(rows, cols, axis, X0, E, static_cast<hipStream_t>(stream)));
+}
+
+int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int axis, const double* X, const int32_t* E,
+                 double* D, void* stream) {
+  if (rows < 0 || cols < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || slices < 1 || slices > MDGEMM_MAX_SLICES ||
+      (axis != 0 && axis != 1))
+    return MDGEMM_EINVAL;
+  if (rows == 0 || cols == 0) return MDGEMM_OK;
+  if (!X || !E || !D) return MDGEMM_EINVAL;
+  const size_t xbytes = sizeof(double) * limbs * static_cast<size_t>(rows) * static_cast<size_t>(cols);
+  const size_t dbytes = sizeof(double) * slices * static_cast<size_t>(rows) * static_cast<size_t>(cols);
+  if (overlaps(D, dbytes, X, xbytes)) return MDGEMM_EINVAL;
+  return hip_status(mdg::launch_split(rows, cols, limbs, slices, axis, X, E, D, static_cast<hipStream_t>(stream)));
+}
+
+int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, int per_pair, const double* DA,
+                      const double* DB, double* out, void* stream) {
+  if (m < 0 || n < 0 || k < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || cutoff < 0 ||
+      cutoff > 2 * slices - 2)
+    return MDGEMM_EINVAL;
+  if (m == 0 || n == 0) return MDGEMM_OK;
+  if (!out || (k > 0 && (!DA || !DB))) return MDGEMM_EINVAL;
+  const size_t obytes = sizeof(double) * static_cast<size_t>(per_pair ? slices * slices : cutoff + 1) *
+                        static_cast<size_t>(m) * static_cast<size_t>(n);
+  if (k > 0 && (overlaps(out, obytes, DA, sizeof(double) * slices * static_cast<size_t>(m) * k) ||
+                overlaps(out, obytes, DB, sizeof(double) * slices * static_cast<size_t>(k) * n)))
+    return MDGEMM_EINVAL;
+  if (!exact_ok(k, per_pair ? 1 : max_pairs(slices, cutoff))) return MDGEMM_EEXACT;
+  const JobTable jt = per_pair ? pair_jobs(slices, cutoff) : level_jobs(slices, cutoff);
+  return hip_status(mdg::launch_slice_gemm(m, n, k, DA, DB, out, jt, static_cast<hipStream_t>(stream)));
+}
+
+int mdgemm_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, void* stream) {
+  if (m < 0 || n < 0 || levels < 1 || levels > 31) return MDGEMM_EINVAL;
+  if (m == 0 || n == 0) return MDGEMM_OK;
+  if (!G || !Z) return MDGEMM_EINVAL;
+  return hip_status(mdg::launch_accumulate(m, n, levels, G, Z, static_cast<hipStream_t>(stream)));
+}
+
+int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, const double* G, const int32_t* EA,
+                        const int32_t* EB, double* C, void* stream) {
+  if (m < 0 || n < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || levels < 1 || levels > 31) return MDGEMM_EINVAL;
+  if (m == 0 || n == 0) return MDGEMM_OK;
+  if (!G || !EA || !EB || !C) return MDGEMM_EINVAL;
+  const size_t cbytes = sizeof(double) * limbs * static_cast<size_t>(m) * static_cast<size_t>(n);
+  const size_t gbytes = sizeof(double) * levels * static_cast<size_t>(m) * static_cast<size_t>(n);
+  if (overlaps(C, cbytes, G, gbytes)) return MDGEMM_EINVAL;
+  return hip_status(
+      mdg::launch_accum_renorm(m, n, limbs, levels, G, EA, EB, C, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,153 @@
+// Step a1 -- balancing exponents, plus small utility kernels.
+//
+// Section 3 balances numbers by grouping them on a common exponent grid; here
+// the group is one row of A or one column of B, and its grid exponent E is the
+// largest frexp exponent (x = f 2^E, 1/2 <= |f| < 1) among the leading limbs of
+// the line, so every element satisfies |x| < 2^E.  An all-zero line gets E = 0
+// (section 3: a zero needs nothing).  The exponent convention is the one of the
+// worked example of section 2, whose quarters have exponents 0, -13, -26, -39.
+//
+// Rows (axis 0): one wave64 per row reads the row with 8-byte coalesced loads
+// and reduces with cross-lane max.  Columns (axis 1): lanes span 64 consecutive
+// columns (coalesced 512-byte rows), the four waves of a block and the blocks
+// of grid.y split the rows, partial maxima meet in LDS and then in global
+// memory through a vector atomic max; a last pass maps "no nonzero" to 0.
+#include <climits>
+
+#include "internal.h"
+
+namespace mdg {
+namespace {
+
+constexpr int kNoExp = INT_MIN;
+
+// frexp exponent of x; INT_MIN for +-0.  Subnormals: bit length of the
+// significand minus 1074.
+__device__ inline int frexp_exp_or_min(double x) {
+  uint64_t mag = static_cast<uint64_t>(__double_as_longlong(x)) & 0x7fffffffffffffffull;
+  if (mag == 0) return kNoExp;
+  int be = static_cast<int>(mag >> 52);
+  if (be == 0) return (64 - __clzll(static_cast<long long>(mag))) - 1074;
+  return be - 1022;
+}
+
+__device__ inline int wave_max(int v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = max(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+__global__ void __launch_bounds__(256) row_exponents_kernel(int64_t rows, int64_t cols, const double* __restrict__ X0,
+                                                            int32_t* __restrict__ E) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;  // whole wave leaves together
+  const double* r = X0 + row * cols;
+  int best = kNoExp;
+  for (int64_t c = lane; c < cols; c += 64) best = max(best, frexp_exp_or_min(r[c]));
+  best = wave_max(best);
+  if (lane == 0) E[row] = (best == kNoExp) ? 0 : best;
+}
+
+__global__ void __launch_bounds__(256) col_exponents_kernel(int64_t rows, int64_t cols, const double* __restrict__ X0,
+                                                            int32_t* __restrict__ E) {
+  __shared__ int part[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t col = static_cast<int64_t>(blockIdx.x) * 64 + lane;
+  int best = kNoExp;
+  if (col < cols) {
+    const int64_t stride = static_cast<int64_t>(gridDim.y) * 4;
+    for (int64_t r = static_cast<int64_t>(blockIdx.y) * 4 + wave; r < rows; r += stride)
+      best = max(best, frexp_exp_or_min(X0[r * cols + col]));
+  }
+  part[wave][lane] = best;
+  __syncthreads();
+  if (wave == 0 && col < cols) {
+    best = max(max(part[0][lane], part[1][lane]), max(part[2][lane], part[3][lane]));
+    if (best != kNoExp) atomicMax(E + col, best);
+  }
+}
+
+__global__ void finalize_exponents_kernel(int64_t count, int32_t* __restrict__ E) {
+  int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < count && E[i] == kNoExp) E[i] = 0;
+}
+
+__global__ void set_i32_kernel(int32_t* __restrict__ p, int64_t count, int32_t value) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    p[i] = value;
+}
+
+__global__ void zero_f64_kernel(double* __restrict__ p, int64_t count) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    p[i] = 0.0;
+}
+
+__global__ void nonfinite_scan_kernel(const double* __restrict__ X, int64_t count, int32_t* __restrict__ flag) {
+  bool bad = false;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    uint64_t b = static_cast<uint64_t>(__double_as_longlong(X[i]));
+    bad |= ((b >> 52) & 0x7ff) == 0x7ff;
+  }
+  if (bad) *flag = 1;  // every writer stores the same value
+}
+
+inline unsigned grid_for(int64_t count, int block, int64_t cap = 65536) {
+  int64_t g = (count + block - 1) / block;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return static_cast<unsigned>(g);
+}
+
+}  // namespace
+
+hipError_t launch_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, hipStream_t stream) {
+  if (axis == 0) {
+    if (rows == 0) return hipSuccess;
+    if (cols == 0) return launch_set_i32(E, rows, 0, stream);
+    unsigned g = static_cast<unsigned>((rows + 3) / 4);
+    hipLaunchKernelGGL(row_exponents_kernel, dim3(g), dim3(256), 0, stream, rows, cols, X0, E);
+    return hipGetLastError();
+  }
+  if (cols == 0) return hipSuccess;
+  hipError_t err = launch_set_i32(E, cols, kNoExp, stream);
+  if (err != hipSuccess) return err;
+  if (rows > 0) {
+    // enough blocks to cover the chip; each block walks rows / (4 * gy) rows of 64 columns
+    int64_t gx = (cols + 63) / 64;
+    int64_t gy = (2048 + gx - 1) / gx;
+    int64_t max_gy = (rows + 63) / 64;  // keep at least ~64 rows per block row
+    if (gy > max_gy) gy = max_gy;
+    if (gy < 1) gy = 1;
+    if (gy > 65535) gy = 65535;
+    hipLaunchKernelGGL(col_exponents_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)), dim3(256),
+                       0, stream, rows, cols, X0, E);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  hipLaunchKernelGGL(finalize_exponents_kernel, dim3(grid_for(cols, 256, 1ll << 30)), dim3(256), 0, stream, cols, E);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_i32(int32_t* p, int64_t count, int32_t value, hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(set_i32_kernel, dim3(grid_for(count, 256)), dim3(256), 0, stream, p, count, value);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_f64(double* p, int64_t count, hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_f64_kernel, dim3(grid_for(count, 256)), dim3(256), 0, stream, p, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_nonfinite_scan(const double* X, int64_t count, int32_t* flag, hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(nonfinite_scan_kernel, dim3(grid_for(count, 256, 4096)), dim3(256), 0, stream, X, count, flag);
+  return hipGetLastError();
+}
+
+}  // namespace mdg

@@ -1,0 +1,163 @@
+// Step a2 -- exact split of multiple doubles into 13-bit integer digits.
+//
+// Section 2 cuts the 52-bit fraction of a double into four 13-bit quarters
+// whose exponents lie on the grid 0, -13, -26, -39; products of two quarters
+// keep at least 26 trailing zero bits, so long inner products of them are
+// exact.  Section 3 puts numbers that are multiplied together on one balanced
+// grid and moves a unit of 2^-52 between a high and a low double of opposite
+// signs so that both parts get the same sign.
+//
+// Here every element x (L limbs, exact value V) of a row of A or a column of B
+// is read on the grid of its line's exponent E with unit u = 2^(E - 13 S):
+//     D = floor(|V| / u),   digit_s = sign(V) * (13-bit field s of D),
+// which are the truncated 13-bit quarters of the exact value; a limb of
+// opposite sign lowers D by the floor, which is the borrow of section 3.
+//
+// The floor is formed exactly in 64-bit integer words: |V| / u is accumulated
+// as a fixed-point integer with 52 fraction bits.  For a normalized multiple
+// double every limb whose top bit is at or above u has its ulp at or above
+// 2^-52 u, so those limbs add exactly; the first limb entirely below u (and
+// everything after it, of smaller magnitude) only decides the floor through its
+// sign, when the fraction of the accumulated part is exactly zero.
+//
+// One thread per element; consecutive threads take consecutive columns, so the
+// L limb loads and the S digit stores of a wave are contiguous 512-byte rows.
+#include "internal.h"
+
+namespace mdg {
+namespace {
+
+// acc += M 2^sh (neg == false) or acc -= M 2^sh (neg == true), modulo 2^(64 NW);
+// M < 2^53 and sh + 53 <= 64 NW.
+template <int NW>
+__device__ inline void add_shifted(uint64_t (&acc)[NW], uint64_t M, int sh, bool neg) {
+  const int w = sh >> 6, b = sh & 63;
+  const uint64_t lo = M << b;
+  const uint64_t hi = b ? (M >> (64 - b)) : 0ull;
+  uint64_t carry = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const uint64_t t = (i == w) ? lo : ((i == w + 1) ? hi : 0ull);
+    const uint64_t a = acc[i];
+    if (!neg) {
+      const uint64_t s = a + t;
+      const uint64_t c1 = s < a;
+      const uint64_t s2 = s + carry;
+      const uint64_t c2 = s2 < s;
+      acc[i] = s2;
+      carry = c1 | c2;
+    } else {
+      const uint64_t s = a - t;
+      const uint64_t b1 = a < t;
+      const uint64_t s2 = s - carry;
+      const uint64_t b2 = s < carry;
+      acc[i] = s2;
+      carry = b1 | b2;
+    }
+  }
+}
+
+// 13-bit field of the NW-word integer v starting at bit pos.
+template <int NW>
+__device__ inline uint32_t field13(const uint64_t (&v)[NW], int pos) {
+  const int w = pos >> 6, b = pos & 63;
+  uint64_t lo = 0, hi = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    lo = (i == w) ? v[i] : lo;
+    hi = (i == w + 1) ? v[i] : hi;
+  }
+  uint64_t f = lo >> b;
+  if (b > 64 - kSliceBits) f |= hi << (64 - b);
+  return static_cast<uint32_t>(f) & kDigitMax;
+}
+
+template <int NW>
+__global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, int L, int S, int axis,
+                                                    const double* __restrict__ X, const int32_t* __restrict__ E,
+                                                    double* __restrict__ D) {
+  const int64_t plane = rows * cols;
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (c >= cols) return;
+  for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
+    const int64_t idx = r * cols + c;
+    const int e = axis == 0 ? E[r] : E[c];
+    const int g = e - kSliceBits * S;  // exponent of the grid unit u
+
+    const double x0 = X[idx];
+    const bool neg = x0 < 0.0;
+    uint64_t acc[NW];
+#pragma unroll
+    for (int i = 0; i < NW; ++i) acc[i] = 0;
+    int tail = 0;  // +1 / -1: sign, relative to V, of the part of V below u that is not in acc
+    if (x0 != 0.0) {
+      for (int l = 0; l < L; ++l) {
+        const double xl = X[static_cast<int64_t>(l) * plane + idx];
+        if (xl == 0.0) break;  // normalized: every later limb is zero too
+        const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(xl));
+        const bool lneg = (bits >> 63) != 0;
+        const uint64_t mag = bits & 0x7fffffffffffffffull;
+        const int be = static_cast<int>(mag >> 52);
+        uint64_t M;
+        int ex;  // |xl| = M 2^ex
+        if (be != 0) {
+          M = (mag & 0x000fffffffffffffull) | 0x0010000000000000ull;
+          ex = be - 1075;
+        } else {
+          M = mag;
+          ex = -1074;
+        }
+        const int fe = ex + (64 - __clzll(static_cast<long long>(M)));  // frexp exponent of xl
+        if (fe <= g) {  // |xl| < u: xl and the rest of the limbs lie below the grid unit
+          tail = (lneg == neg) ? 1 : -1;
+          break;
+        }
+        add_shifted<NW>(acc, M, ex - g + 52, lneg != neg);
+      }
+    }
+    // I = floor(acc / 2^52), lowered by one when the fraction is zero and the
+    // part below u is negative (relative to the sign of V).
+    const bool frac_zero = (acc[0] & 0x000fffffffffffffull) == 0;
+    uint64_t I[NW];
+#pragma unroll
+    for (int i = 0; i < NW; ++i) I[i] = (acc[i] >> 52) | (i + 1 < NW ? acc[i + 1] << 12 : 0ull);
+    if (frac_zero && tail < 0) {
+      uint64_t borrow = 1;
+#pragma unroll
+      for (int i = 0; i < NW; ++i) {
+        const uint64_t v = I[i];
+        I[i] = v - borrow;
+        borrow = (v < borrow) ? 1ull : 0ull;
+      }
+    }
+    for (int s = 0; s < S; ++s) {
+      const uint32_t d = field13<NW>(I, kSliceBits * (S - 1 - s));
+      const double v = static_cast<double>(d);
+      D[static_cast<int64_t>(s) * plane + idx] = (d == 0u) ? 0.0 : (neg ? -v : v);
+    }
+  }
+}
+
+template <int NW>
+hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E, double* D,
+                     hipStream_t stream) {
+  const unsigned gx = static_cast<unsigned>((cols + 255) / 256);
+  const unsigned gy = static_cast<unsigned>(rows < 65535 ? rows : 65535);
+  hipLaunchKernelGGL(split_kernel<NW>, dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, axis, X, E, D);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E,
+                        double* D, hipStream_t stream) {
+  if (rows == 0 || cols == 0) return hipSuccess;
+  // The accumulator holds |V| / u < 2^(13 S) with 52 fraction bits: 13 S + 52 bits.
+  const int bits = kSliceBits * S + 52;
+  if (bits <= 128) return launch_nw<2>(rows, cols, L, S, axis, X, E, D, stream);
+  if (bits <= 192) return launch_nw<3>(rows, cols, L, S, axis, X, E, D, stream);
+  if (bits <= 256) return launch_nw<4>(rows, cols, L, S, axis, X, E, D, stream);
+  return launch_nw<5>(rows, cols, L, S, axis, X, E, D, stream);
+}
+
+}  // namespace mdg

@@ -1,0 +1,278 @@
+"""Python binding of ``libmdgemm.so`` (C ABI in ``include/mdgemm.h``).
+
+Argument marshalling only: every step of the product runs in the library's
+HIP kernels.  PyTorch provides device memory (tensors, the workspace) and the
+stream (``torch.cuda.current_stream()``).  The functions carry the names of the
+C entry points.  If the library is missing this module raises: there is no
+fallback path.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmdgemm.so")
+
+MDGEMM_OK = 0
+MDGEMM_EINVAL = -1
+MDGEMM_EEXACT = -2
+MDGEMM_ENOMEM = -3
+MDGEMM_EHIP = -4
+MDGEMM_EWORKSPACE = -5
+MDGEMM_ENONFINITE = -6
+
+MDGEMM_CHECK_FINITE = 1
+MDGEMM_SYNC = 2
+MDGEMM_TIME_STAGES = 4
+
+MDGEMM_CUTOFF_DEFAULT = -1
+MDGEMM_CUTOFF_ALL = -2
+MDGEMM_Z_WORDS = 8
+
+EXPORTED = (
+    "mdgemm_opts_init",
+    "mdgemm",
+    "mdgemm_workspace_bytes",
+    "mdgemm_ex",
+    "mdgemm_stage_times",
+    "mdgemm_status_string",
+    "mdgemm_release",
+    "mdgemm_exponents",
+    "mdgemm_split",
+    "mdgemm_slice_gemm",
+    "mdgemm_accumulate",
+    "mdgemm_accum_renorm",
+)
+
+
+class MdgemmError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+class mdgemm_opts(ctypes.Structure):
+    _fields_ = [
+        ("stream", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t),
+        ("slices_per_limb", ctypes.c_int),
+        ("cutoff", ctypes.c_int),
+        ("flags", ctypes.c_uint),
+    ]
+
+
+_lib = None
+_i64 = ctypes.c_int64
+_vp = ctypes.c_void_p
+
+
+def lib() -> ctypes.CDLL:
+    """Load the in-tree ``libmdgemm.so``; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_06881_amd.build` "
+                               "or __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        L.mdgemm_opts_init.argtypes = [ctypes.POINTER(mdgemm_opts)]
+        L.mdgemm_opts_init.restype = None
+        L.mdgemm.argtypes = [_i64, _i64, _i64, ctypes.c_int, _vp, _vp, _vp]
+        L.mdgemm.restype = ctypes.c_int
+        L.mdgemm_workspace_bytes.argtypes = [_i64, _i64, _i64, ctypes.c_int, ctypes.POINTER(mdgemm_opts)]
+        L.mdgemm_workspace_bytes.restype = ctypes.c_size_t
+        L.mdgemm_ex.argtypes = [_i64, _i64, _i64, ctypes.c_int, _vp, _vp, _vp, ctypes.POINTER(mdgemm_opts)]
+        L.mdgemm_ex.restype = ctypes.c_int
+        L.mdgemm_stage_times.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_int]
+        L.mdgemm_stage_times.restype = ctypes.c_int
+        L.mdgemm_status_string.argtypes = [ctypes.c_int]
+        L.mdgemm_status_string.restype = ctypes.c_char_p
+        L.mdgemm_release.argtypes = []
+        L.mdgemm_release.restype = None
+        L.mdgemm_exponents.argtypes = [_i64, _i64, ctypes.c_int, _vp, _vp, _vp]
+        L.mdgemm_exponents.restype = ctypes.c_int
+        L.mdgemm_split.argtypes = [_i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp]
+        L.mdgemm_split.restype = ctypes.c_int
+        L.mdgemm_slice_gemm.argtypes = [_i64, _i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp,
+                                        _vp]
+        L.mdgemm_slice_gemm.restype = ctypes.c_int
+        L.mdgemm_accumulate.argtypes = [_i64, _i64, ctypes.c_int, _vp, _vp, _vp]
+        L.mdgemm_accumulate.restype = ctypes.c_int
+        L.mdgemm_accum_renorm.argtypes = [_i64, _i64, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp, _vp]
+        L.mdgemm_accum_renorm.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().mdgemm_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != MDGEMM_OK:
+        raise MdgemmError(status, where)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dev_tensor(t: torch.Tensor, dtype: torch.dtype, name: str) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def make_opts(*, slices_per_limb: int = 4, cutoff: int = MDGEMM_CUTOFF_DEFAULT, flags: int = 0, stream=None,
+              workspace: Optional[torch.Tensor] = None) -> mdgemm_opts:
+    o = mdgemm_opts()
+    lib().mdgemm_opts_init(ctypes.byref(o))
+    o.slices_per_limb = slices_per_limb
+    o.cutoff = cutoff
+    o.flags = flags
+    o.stream = _stream(stream)
+    if workspace is not None:
+        o.workspace = workspace.data_ptr()
+        o.workspace_bytes = workspace.numel() * workspace.element_size()
+    return o
+
+
+def mdgemm_workspace_bytes(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
+                           cutoff: int = MDGEMM_CUTOFF_DEFAULT) -> int:
+    o = mdgemm_opts()
+    lib().mdgemm_opts_init(ctypes.byref(o))
+    o.slices_per_limb = slices_per_limb
+    o.cutoff = cutoff
+    return int(lib().mdgemm_workspace_bytes(m, n, k, limbs, ctypes.byref(o)))
+
+
+def mdgemm_ex(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None, *, slices_per_limb: int = 4,
+              cutoff: int = MDGEMM_CUTOFF_DEFAULT, flags: int = 0, workspace: Optional[torch.Tensor] = None,
+              stream=None) -> torch.Tensor:
+    """C = A.B for limb-major float64 tensors A [L, m, k] and B [L, k, n] on the GPU.
+
+    The workspace is a torch uint8 tensor (allocated here when not given), so
+    device memory comes from PyTorch's allocator."""
+    _dev_tensor(A, torch.float64, "A")
+    _dev_tensor(B, torch.float64, "B")
+    if A.dim() != 3 or B.dim() != 3 or A.shape[0] != B.shape[0] or A.shape[2] != B.shape[1]:
+        raise ValueError(f"shapes {tuple(A.shape)} and {tuple(B.shape)} do not form a product [L,m,k].[L,k,n]")
+    L, m, k = A.shape
+    n = B.shape[2]
+    if C is None:
+        C = torch.empty((L, m, n), dtype=torch.float64, device=A.device)
+    else:
+        _dev_tensor(C, torch.float64, "C")
+        if tuple(C.shape) != (L, m, n):
+            raise ValueError("C has the wrong shape")
+    if workspace is None:
+        need = mdgemm_workspace_bytes(m, n, k, L, slices_per_limb=slices_per_limb, cutoff=cutoff)
+        if need == 2**64 - 1:
+            _check(MDGEMM_EINVAL, "mdgemm_workspace_bytes")
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=A.device)
+    o = make_opts(slices_per_limb=slices_per_limb, cutoff=cutoff, flags=flags, stream=stream, workspace=workspace)
+    _check(lib().mdgemm_ex(m, n, k, L, _ptr(A), _ptr(B), _ptr(C), ctypes.byref(o)), "mdgemm_ex")
+    return C
+
+
+def mdgemm(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """C = A.B with the default options through the plain ``mdgemm`` entry point
+    (default stream, library-owned workspace)."""
+    _dev_tensor(A, torch.float64, "A")
+    _dev_tensor(B, torch.float64, "B")
+    L, m, k = A.shape
+    n = B.shape[2]
+    if C is None:
+        C = torch.empty((L, m, n), dtype=torch.float64, device=A.device)
+    _check(lib().mdgemm(m, n, k, L, _ptr(A), _ptr(B), _ptr(C)), "mdgemm")
+    return C
+
+
+def mdgemm_stage_times() -> list:
+    buf = (ctypes.c_float * 4)()
+    n = lib().mdgemm_stage_times(buf, 4)
+    if n < 0:
+        _check(n, "mdgemm_stage_times")
+    return [float(buf[i]) for i in range(n)]
+
+
+def mdgemm_release() -> None:
+    lib().mdgemm_release()
+
+
+def mdgemm_exponents(X0: torch.Tensor, axis: int, E: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Grid exponents (int32) of every row (axis 0) or column (axis 1) of a [rows, cols] plane."""
+    _dev_tensor(X0, torch.float64, "X0")
+    rows, cols = X0.shape
+    if E is None:
+        E = torch.empty(rows if axis == 0 else cols, dtype=torch.int32, device=X0.device)
+    _check(lib().mdgemm_exponents(rows, cols, axis, _ptr(X0), _ptr(E), _stream(stream)), "mdgemm_exponents")
+    return E
+
+
+def mdgemm_split(X: torch.Tensor, E: torch.Tensor, slices: int, axis: int, D: Optional[torch.Tensor] = None,
+                 stream=None) -> torch.Tensor:
+    """Digits [slices, rows, cols] (float64) of X [L, rows, cols] on the grid exponents E."""
+    _dev_tensor(X, torch.float64, "X")
+    _dev_tensor(E, torch.int32, "E")
+    L, rows, cols = X.shape
+    if D is None:
+        D = torch.empty((slices, rows, cols), dtype=torch.float64, device=X.device)
+    _check(lib().mdgemm_split(rows, cols, L, slices, axis, _ptr(X), _ptr(E), _ptr(D), _stream(stream)),
+           "mdgemm_split")
+    return D
+
+
+def mdgemm_slice_gemm(DA: torch.Tensor, DB: torch.Tensor, cutoff: int, per_pair: bool = False,
+                      out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Level products [cutoff+1, m, n] (or pair products [S, S, m, n]) of digit planes."""
+    _dev_tensor(DA, torch.float64, "DA")
+    _dev_tensor(DB, torch.float64, "DB")
+    S, m, k = DA.shape
+    n = DB.shape[2]
+    if out is None:
+        shape = (S, S, m, n) if per_pair else (cutoff + 1, m, n)
+        out = torch.zeros(shape, dtype=torch.float64, device=DA.device)
+    _check(lib().mdgemm_slice_gemm(m, n, k, S, cutoff, int(per_pair), _ptr(DA), _ptr(DB), _ptr(out),
+                                   _stream(stream)), "mdgemm_slice_gemm")
+    return out
+
+
+def mdgemm_accumulate(G: torch.Tensor, Z: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Exact sums N = sum_t G_t 2^(13 (T - t)) as 8 int64 words [8, m, n], least significant first."""
+    _dev_tensor(G, torch.float64, "G")
+    levels, m, n = G.shape
+    if Z is None:
+        Z = torch.empty((MDGEMM_Z_WORDS, m, n), dtype=torch.int64, device=G.device)
+    _check(lib().mdgemm_accumulate(m, n, levels, _ptr(G), _ptr(Z), _stream(stream)), "mdgemm_accumulate")
+    return Z
+
+
+def mdgemm_accum_renorm(G: torch.Tensor, EA: torch.Tensor, EB: torch.Tensor, limbs: int,
+                        C: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """C [limbs, m, n]: exact sum of the levels rounded greedily into limbs, scaled by 2^(EA+EB-26)."""
+    _dev_tensor(G, torch.float64, "G")
+    _dev_tensor(EA, torch.int32, "EA")
+    _dev_tensor(EB, torch.int32, "EB")
+    levels, m, n = G.shape
+    if C is None:
+        C = torch.empty((limbs, m, n), dtype=torch.float64, device=G.device)
+    _check(lib().mdgemm_accum_renorm(m, n, limbs, levels, _ptr(G), _ptr(EA), _ptr(EB), _ptr(C), _stream(stream)),
+           "mdgemm_accum_renorm")
+    return C

@@ -1,0 +1,134 @@
+"""The C-ABI library: it loads, exports every function of include/mdgemm.h, and
+its host-side argument checks answer before any HIP call (no GPU needed)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_06881_amd import mdgemm as md
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mdgemm.h")
+
+# fake, non-overlapping device addresses: only the host-side checks read them
+FA, FB, FC = 1 << 40, 2 << 40, 3 << 40
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(mdgemm\w*)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(md.LIB_PATH):
+        import __graft_entry__
+
+        __graft_entry__.build()
+    return md.lib()
+
+
+def test_header_declares_the_exported_set(lib):
+    names = _declared_functions()
+    assert names == sorted(md.EXPORTED)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for st in range(0, -7, -1):
+        s = md.status_string(st)
+        assert s and s != "unknown status"
+    assert md.status_string(-99) == "unknown status"
+
+
+def test_opts_init_defaults(lib):
+    o = md.mdgemm_opts()
+    o.flags = 77
+    lib.mdgemm_opts_init(ctypes.byref(o))
+    assert (o.stream, o.workspace, o.workspace_bytes, o.slices_per_limb, o.cutoff, o.flags) == (None, None, 0, 4, -1,
+                                                                                              0)
+
+
+def _ex(lib, m, n, k, limbs, A=FA, B=FB, C=FC, **kw):
+    o = md.mdgemm_opts()
+    lib.mdgemm_opts_init(ctypes.byref(o))
+    for key, v in kw.items():
+        setattr(o, key, v)
+    return lib.mdgemm_ex(m, n, k, limbs, A, B, C, ctypes.byref(o))
+
+
+def test_invalid_arguments(lib):
+    E = md.MDGEMM_EINVAL
+    assert _ex(lib, -1, 4, 4, 2) == E
+    assert _ex(lib, 4, 4, -3, 2) == E
+    assert _ex(lib, 4, 4, 4, 0) == E
+    assert _ex(lib, 4, 4, 4, 5) == E
+    assert _ex(lib, 4, 4, 4, 2, slices_per_limb=9) == E  # S = 18 > 16
+    assert _ex(lib, 4, 4, 4, 2, cutoff=15) == E  # > 2S - 2
+    assert _ex(lib, 4, 4, 4, 2, cutoff=-3) == E
+    assert _ex(lib, 4, 4, 4, 2, A=None) == E
+    assert _ex(lib, 4, 4, 4, 2, C=None) == E
+    # C overlapping A
+    assert _ex(lib, 4, 4, 4, 2, C=FA + 8) == E
+    assert lib.mdgemm_split(4, 4, 2, 17, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_split(4, 4, 2, 8, 2, FA, FB, FC, None) == E
+    assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 15, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_accumulate(4, 4, 32, FA, FC, None) == E
+    assert lib.mdgemm_accum_renorm(4, 4, 5, 8, FA, FB, FB, FC, None) == E
+    assert lib.mdgemm_exponents(4, 4, 3, FA, FB, None) == E
+
+
+def test_empty_products_are_noops(lib):
+    assert _ex(lib, 0, 5, 5, 2, A=None, B=None, C=None) == md.MDGEMM_OK
+    assert _ex(lib, 5, 0, 5, 2, A=None, B=None, C=None) == md.MDGEMM_OK
+    assert lib.mdgemm_split(0, 5, 2, 8, 0, None, None, None, None) == md.MDGEMM_OK
+    assert lib.mdgemm_slice_gemm(0, 5, 5, 8, 7, 0, None, None, None, None) == md.MDGEMM_OK
+    assert lib.mdgemm_exponents(0, 5, 0, None, None, None) == md.MDGEMM_OK
+
+
+def _max_k(pairs):
+    # largest k with pairs * k * 8191^2 < 2^53 (the exactness bound of the level sums)
+    return (2**53 - 1) // (pairs * 8191**2)
+
+
+@pytest.mark.parametrize("limbs,cutoff,pairs", [(2, -1, 8), (2, -2, 8), (4, -1, 16), (1, 0, 1), (3, 5, 6)])
+def test_exactness_bound(lib, limbs, cutoff, pairs):
+    kmax = _max_k(pairs)
+    assert _ex(lib, 4, 4, kmax + 1, limbs, cutoff=cutoff) == md.MDGEMM_EEXACT
+    # at kmax the check passes and the call goes on to the workspace check
+    assert _ex(lib, 4, 4, kmax, limbs, cutoff=cutoff, workspace=FC + (1 << 40),
+               workspace_bytes=16) == md.MDGEMM_EWORKSPACE
+    assert lib.mdgemm_slice_gemm(4, 4, kmax + 1, 4 * limbs, cutoff if cutoff >= 0 else 4 * limbs - 1, 0, FA, FB, FC,
+                                 None) == md.MDGEMM_EEXACT
+
+
+def test_workspace_bytes_layout(lib):
+    def expect(m, n, k, L, S, T):
+        a = lambda x: (x + 255) // 256 * 256
+        return a(4 * m) + a(4 * n) + a(4) + a(8 * S * m * k) + a(8 * S * k * n) + a(8 * (T + 1) * m * n)
+
+    assert md.mdgemm_workspace_bytes(100, 70, 33, 2) == expect(100, 70, 33, 2, 8, 7)
+    assert md.mdgemm_workspace_bytes(100, 70, 33, 2, cutoff=-2) == expect(100, 70, 33, 2, 8, 14)
+    assert md.mdgemm_workspace_bytes(64, 64, 64, 4, slices_per_limb=3, cutoff=5) == expect(64, 64, 64, 4, 12, 5)
+    assert md.mdgemm_workspace_bytes(0, 64, 64, 2) == 0
+    assert md.mdgemm_workspace_bytes(4, 4, 4, 9) == 2**64 - 1
+
+
+def test_workspace_too_small_is_reported_before_any_launch(lib):
+    need = md.mdgemm_workspace_bytes(40, 30, 20, 3)
+    assert _ex(lib, 40, 30, 20, 3, workspace=FC + (1 << 40), workspace_bytes=need - 1) == md.MDGEMM_EWORKSPACE
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    import torch
+
+    A = torch.zeros(2, 4, 4, dtype=torch.float64)
+    with pytest.raises(ValueError):
+        md.mdgemm_ex(A, A)
+    with pytest.raises(TypeError):
+        md.mdgemm_ex(A.float(), A.float())

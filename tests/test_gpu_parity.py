@@ -1,0 +1,365 @@
+"""GPU parity of every stage of the product against the CPU oracle.
+
+Bit-exact: exponents, digits, level and pair products, the exact accumulated
+sums and the final greedy rounding.  Tolerance: the final limbs against the
+exact rational product, |C - C_exact| <= 4 k 2^-(53L-4) (|A||B|).  Sizes span
+several 128 x 128 tiles and 16-deep k blocks with ragged tails.
+"""
+
+import math
+import random
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import coracle, exact, pipeline
+from paper_2607_06881_amd import mdgemm as md
+from paper_2607_06881_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+def _gpu(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def _host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def _operands(L, m, k, n, seed, base="uniform", row_exp=0, col_exp=0, elem_exp=0):
+    rng = np.random.default_rng(seed)
+    A = workloads.make_operand(rng, L, m, k, base, row_exp=row_exp, elem_exp=elem_exp)
+    B = workloads.make_operand(rng, L, k, n, base, col_exp=col_exp, elem_exp=elem_exp)
+    return A, B
+
+
+# --------------------------------------------------------------------------
+# a1 exponents
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("rows,cols", [(1, 1), (7, 300), (300, 7), (129, 257), (1000, 64), (64, 5000)])
+def test_exponents(rows, cols):
+    print(f"[case] exponents {rows}x{cols}", flush=True)
+    rng = np.random.default_rng(rows * 7 + cols)
+    X = rng.standard_normal((rows, cols)) * np.ldexp(1.0, rng.integers(-900, 900, (rows, cols)))
+    X[rng.random((rows, cols)) < 0.05] = 0.0
+    X[0, :] = 0.0  # all-zero row
+    if cols > 2:
+        X[:, 2] = 0.0  # all-zero column
+    X[-1, -1] = 7 * 2.0**-1074  # subnormal
+    Xg = _gpu(X)
+    for axis in (0, 1):
+        got = _host(md.mdgemm_exponents(Xg, axis))
+        want = coracle.exponents(X, axis)
+        assert np.array_equal(got, want), axis
+
+
+# --------------------------------------------------------------------------
+# a2 split
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("L,S,rows,cols,axis", [(1, 4, 33, 70, 0), (2, 8, 65, 129, 0), (2, 8, 130, 17, 1),
+                                                 (3, 12, 40, 300, 1), (4, 16, 77, 91, 0), (2, 5, 20, 20, 1),
+                                                 (4, 13, 31, 33, 1), (3, 16, 9, 9, 0)])
+def test_split_random(L, S, rows, cols, axis):
+    print(f"[case] split L={L} S={S} {rows}x{cols} axis={axis}", flush=True)
+    rng = np.random.default_rng(L * 100 + S)
+    X = workloads.make_operand(rng, L, rows, cols, "normal", elem_exp=12,
+                               row_exp=20 if axis == 0 else 0, col_exp=20 if axis == 1 else 0)
+    X[:, rng.random((rows, cols)) < 0.05] = 0.0
+    E = coracle.exponents(X[0], axis)
+    Xg = _gpu(X)
+    Eg = md.mdgemm_exponents(Xg[0], axis)
+    assert np.array_equal(_host(Eg), E)
+    got = _host(md.mdgemm_split(Xg, Eg, S, axis))
+    want = coracle.split(X, E, S, axis)
+    assert np.array_equal(got, want)
+    assert not np.signbit(got[got == 0]).any()  # zero digits are +0.0
+
+
+def _adversarial_elements(L, count, seed):
+    """Multiple doubles with opposite-signed limbs, half-ulp tails, gaps,
+    exact zeros below nonzeros, powers of two and subnormal tails."""
+    rng = random.Random(seed)
+    out = []
+    for _ in range(count):
+        x0 = rng.choice([-1, 1]) * rng.choice([1.0, 0.5, 0.75, 1 - 2.0**-53, rng.uniform(0.5, 1)]) \
+            * 2.0 ** rng.randint(-30, 30)
+        limbs = [x0]
+        for _ in range(1, L):
+            prev = limbs[-1]
+            if prev == 0.0:
+                limbs.append(0.0)
+                continue
+            h = math.ulp(prev) / 2
+            kind = rng.random()
+            if kind < 0.2:
+                y = rng.choice([-1, 1]) * h
+            elif kind < 0.35:
+                y = 0.0
+            elif kind < 0.5:
+                y = rng.choice([-1, 1]) * h * 2.0 ** -rng.randint(1, 60)
+            else:
+                y = rng.uniform(-1, 1) * h
+            limbs.append(y)
+        out.append(limbs)
+    return out
+
+
+@pytest.mark.parametrize("L", [2, 3, 4])
+def test_split_adversarial(L):
+    print(f"[case] split adversarial L={L}", flush=True)
+    els = _adversarial_elements(L, 64 * 33, 900 + L)
+    X = np.array(els).T.reshape(L, 64, 33).copy()
+    assert all(exact.is_nonoverlapping(X[:, r, c]) for r in range(64) for c in range(33))
+    for axis in (0, 1):
+        E = coracle.exponents(X[0], axis)
+        for S in (4 * L, 4 * L - 1, 3):
+            got = _host(md.mdgemm_split(_gpu(X), _gpu(E), S, axis))
+            want = coracle.split(X, E, S, axis)
+            assert np.array_equal(got, want), (axis, S)
+
+
+def test_split_golden_cases():
+    print("[case] split golden", flush=True)
+    fbits = "1001000110100110011001001110110100100011010011001100"
+    x = int(fbits, 2) * 2.0**-52
+    X = np.array([x]).reshape(1, 1, 1)
+    got = _host(md.mdgemm_split(_gpu(X), _gpu(np.array([0], np.int32)), 4, 0)).ravel()
+    assert got.tolist() == [0x1234, 0x1993, 0x1691, 0x14CC]
+    # opposite-sign limbs (the borrow of section 3)
+    X = np.array([1.0, -(2.0**-60)]).reshape(2, 1, 1)
+    got = _host(md.mdgemm_split(_gpu(X), _gpu(np.array([1], np.int32)), 8, 0)).ravel()
+    assert got.tolist() == [4095, 8191, 8191, 8191, 8176, 0, 0, 0]
+
+
+# --------------------------------------------------------------------------
+# a3 level and pair GEMMs
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("S,T,m,k,n", [(8, 7, 65, 37, 129), (8, 14, 130, 50, 131), (4, 3, 1, 1, 1),
+                                       (12, 11, 200, 33, 70), (16, 15, 64, 16, 64), (16, 30, 33, 20, 17),
+                                       (3, 2, 257, 129, 300), (8, 7, 16, 1, 16)])
+def test_levels(S, T, m, k, n):
+    print(f"[case] levels S={S} T={T} {m}x{k}x{n}", flush=True)
+    rng = np.random.default_rng(S * 1000 + m)
+    DA = rng.integers(-8191, 8192, (S, m, k)).astype(np.float64)
+    DB = rng.integers(-8191, 8192, (S, k, n)).astype(np.float64)
+    DA[:, rng.random((m, k)) < 0.1] = 0.0
+    got = _host(md.mdgemm_slice_gemm(_gpu(DA), _gpu(DB), T))
+    want = coracle.levels(DA, DB, T)
+    assert np.array_equal(got, want.astype(np.float64))
+
+
+@pytest.mark.parametrize("S,T", [(8, 14), (8, 7), (4, 2)])
+def test_pair_products(S, T):
+    print(f"[case] pairs S={S} T={T}", flush=True)
+    rng = np.random.default_rng(S + T)
+    m, k, n = 70, 45, 140
+    DA = rng.integers(-8191, 8192, (S, m, k)).astype(np.float64)
+    DB = rng.integers(-8191, 8192, (S, k, n)).astype(np.float64)
+    out = torch.full((S, S, m, n), -1.0, dtype=torch.float64, device=DEV)
+    got = _host(md.mdgemm_slice_gemm(_gpu(DA), _gpu(DB), T, per_pair=True, out=out))
+    want = coracle.levels(DA, DB, T, per_pair=True)
+    for p in range(S):
+        for q in range(S):
+            if p + q <= T:
+                assert np.array_equal(got[p, q], want[p, q].astype(np.float64)), (p, q)
+            else:
+                assert (got[p, q] == -1.0).all(), (p, q)  # untouched
+
+
+def test_levels_near_exactness_limit():
+    # All digits 8191: G_t = pairs_t k 8191^2 in closed form, up to 2^51.
+    print("[case] levels near 2^53", flush=True)
+    S, T, m, n, k = 16, 15, 128, 128, 2**21
+    DA = torch.full((S, m, k), 8191.0, dtype=torch.float64, device=DEV)
+    DB = torch.full((S, k, n), -8191.0, dtype=torch.float64, device=DEV)
+    got = _host(md.mdgemm_slice_gemm(DA, DB, T))
+    for t in range(T + 1):
+        want = -float(len(exact.pairs_of_level(t, S)) * k * 8191**2)
+        assert (got[t] == want).all(), t
+    assert abs(got[15, 0, 0]) > 2**50
+    del DA, DB
+    torch.cuda.empty_cache()
+
+
+# --------------------------------------------------------------------------
+# a4 accumulation and a5 rounding
+# --------------------------------------------------------------------------
+
+def _words_to_int(words):
+    v = 0
+    for w in range(len(words)):
+        v |= (int(words[w]) & ((1 << 64) - 1)) << (64 * w)
+    if v >> (64 * len(words) - 1):
+        v -= 1 << (64 * len(words))
+    return v
+
+
+@pytest.mark.parametrize("levels", [1, 2, 5, 8, 12, 15, 16, 31])
+def test_accumulate_exact(levels):
+    print(f"[case] accumulate levels={levels}", flush=True)
+    rng = np.random.default_rng(levels)
+    m, n = 9, 300
+    G = rng.integers(-(2**53) + 1, 2**53, (levels, m, n)).astype(np.float64)
+    G[:, 0, :] = 2.0**53 - 1  # largest allowed magnitudes
+    G[:, 1, :] = -(2.0**53 - 1)
+    G[:, 2, :] = 0.0
+    G[:, 3, ::2] = rng.integers(-5, 5, (levels, (n + 1) // 2))
+    Z = _host(md.mdgemm_accumulate(_gpu(G)))
+    T = levels - 1
+    for i in range(m):
+        for j in range(0, n, 7):
+            want = sum(int(G[t, i, j]) << (13 * (T - t)) for t in range(levels))
+            assert _words_to_int(Z[:, i, j]) == want, (i, j)
+
+
+def _cases_for_rounding(levels, m, n, seed):
+    rng = np.random.default_rng(seed)
+    G = np.zeros((levels, m, n))
+    kind = rng.integers(0, 6, (m, n))
+    for i in range(m):
+        for j in range(n):
+            c = kind[i, j]
+            if c == 0:  # generic
+                G[:, i, j] = rng.integers(-(2**52), 2**52, levels)
+            elif c == 1:  # sparse, small
+                G[:, i, j] = rng.integers(-3, 4, levels) * (rng.random(levels) < 0.3)
+            elif c == 2:  # ties: value = odd * 2^s + exactly half an ulp
+                G[:, i, j] = 0
+                G[0, i, j] = 2**52 + 1
+                if levels > 4:
+                    G[4, i, j] = 2**51  # 2^51 2^-52 = 1/2 unit of the 53-bit lead
+            elif c == 3 and levels >= 2:  # cancellation across levels
+                g = int(rng.integers(1, 2**40))
+                G[:, i, j] = 0
+                G[0, i, j] = g
+                G[1, i, j] = -g * 8192 + int(rng.integers(-5, 5))
+            elif c == 4:  # only the last level
+                G[:, i, j] = 0
+                G[-1, i, j] = rng.integers(-(2**52), 2**52)
+            else:  # alternating signs of maximal size
+                G[:, i, j] = (2**53 - 1) * np.where(np.arange(levels) % 2 == 0, 1, -1)
+    return G
+
+
+@pytest.mark.parametrize("L,levels", [(1, 4), (2, 8), (2, 15), (3, 12), (4, 16), (4, 31), (2, 1)])
+def test_accum_renorm_greedy_rounding(L, levels):
+    print(f"[case] accum_renorm L={L} levels={levels}", flush=True)
+    m, n = 13, 71
+    G = _cases_for_rounding(levels, m, n, 10 * L + levels)
+    rng = np.random.default_rng(levels)
+    EA = rng.integers(-40, 40, m).astype(np.int32)
+    EB = rng.integers(-40, 40, n).astype(np.int32)
+    C = _host(md.mdgemm_accum_renorm(_gpu(G), _gpu(EA), _gpu(EB), L))
+    for i in range(m):
+        for j in range(n):
+            z = exact.accumulate([int(g) for g in G[:, i, j]], int(EA[i]), int(EB[j]))
+            want = exact.round_to_limbs(z, L)
+            assert C[:, i, j].tolist() == want, (i, j, G[:, i, j])
+            assert not any(v == 0 and math.copysign(1, v) < 0 for v in C[:, i, j])
+
+
+# --------------------------------------------------------------------------
+# end to end
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("L,m,k,n,cutoff,seed", [(2, 64, 64, 64, -2, 0), (2, 130, 47, 129, -1, 1),
+                                                 (1, 65, 33, 17, -2, 2), (3, 40, 100, 70, -1, 3),
+                                                 (4, 33, 20, 45, -1, 4), (4, 17, 64, 9, -2, 5),
+                                                 (2, 1, 1, 1, -1, 6), (3, 129, 16, 1, -2, 7)])
+def test_mdgemm_end_to_end(L, m, k, n, cutoff, seed):
+    print(f"[case] mdgemm L={L} {m}x{k}x{n} cutoff={cutoff}", flush=True)
+    A, B = _operands(L, m, k, n, seed, base="normal" if seed % 2 else "uniform", row_exp=15, col_exp=15)
+    S = 4 * L
+    T = S - 1 if cutoff == -1 else 2 * S - 2
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), cutoff=cutoff))
+    ref = pipeline.full_reference(A, B, S, T)
+    assert np.array_equal(C, ref["C"])
+    pick = random.Random(seed)
+    for _ in range(20):
+        i, j = pick.randrange(m), pick.randrange(n)
+        assert exact.is_nonoverlapping(C[:, i, j])
+
+
+def test_mdgemm_plain_entry_point_and_tolerance():
+    print("[case] mdgemm plain c0", flush=True)
+    A, B = workloads.make_workload("c0")
+    C = _host(md.mdgemm(_gpu(A), _gpu(B)))  # default: T = S - 1, default stream, library workspace
+    ref = pipeline.full_reference(A, B, 8, 7)
+    assert np.array_equal(C, ref["C"])
+    worst = 0.0
+    for i in range(0, 64, 9):
+        for j in range(0, 64, 7):
+            want, mag = exact.exact_product(A, B, i, j)
+            ratio = abs(exact.value(C[:, i, j]) - want) / exact.tolerance(64, 2, mag)
+            worst = max(worst, float(ratio))
+    assert worst <= 1.0, worst
+    md.mdgemm_release()
+
+
+def test_mdgemm_zero_lines_and_k0():
+    print("[case] mdgemm zero rows/cols and k=0", flush=True)
+    A, B = _operands(2, 50, 30, 40, 11)
+    A[:, 3, :] = 0.0
+    B[:, :, 5] = 0.0
+    A[:, 7, 4] = 0.0
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B)))
+    ref = pipeline.full_reference(A, B, 8, 7)
+    assert np.array_equal(C, ref["C"])
+    assert (C[:, 3, :] == 0).all() and (C[:, :, 5] == 0).all()
+    assert not np.signbit(C[:, 3, :]).any()
+    # k = 0: C = +0.0
+    Z = md.mdgemm_ex(torch.empty((2, 5, 0), dtype=torch.float64, device=DEV),
+                     torch.empty((2, 0, 6), dtype=torch.float64, device=DEV),
+                     C=torch.full((2, 5, 6), 3.0, dtype=torch.float64, device=DEV))
+    z = _host(Z)
+    assert (z == 0).all() and not np.signbit(z).any()
+
+
+def test_mdgemm_tiny_and_huge_magnitudes():
+    print("[case] mdgemm extreme exponents", flush=True)
+    A, B = _operands(2, 20, 24, 18, 12)
+    A[:, :5] *= 2.0**-600  # rows far below 1
+    B[:, :, :4] *= 2.0**500  # columns far above 1
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B)))
+    ref = pipeline.full_reference(A, B, 8, 7)
+    assert np.array_equal(C, ref["C"])
+
+
+def test_mdgemm_caller_workspace_and_stream():
+    print("[case] mdgemm caller workspace, side stream, stage timing", flush=True)
+    A, B = _operands(3, 100, 64, 90, 13, base="normal")
+    need = md.mdgemm_workspace_bytes(100, 90, 64, 3)
+    ws = torch.empty(need, dtype=torch.uint8, device=DEV)
+    s = torch.cuda.Stream()
+    Ag, Bg = _gpu(A), _gpu(B)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        C = md.mdgemm_ex(Ag, Bg, workspace=ws, flags=md.MDGEMM_TIME_STAGES)
+    s.synchronize()
+    times = md.mdgemm_stage_times()
+    assert len(times) == 4 and all(t >= 0 for t in times)
+    ref = pipeline.full_reference(A, B, 12, 11)
+    assert np.array_equal(C.cpu().numpy(), ref["C"])
+    with pytest.raises(md.MdgemmError) as ei:
+        md.mdgemm_ex(Ag, Bg, workspace=ws[: need - 1])
+    assert ei.value.status == md.MDGEMM_EWORKSPACE
+
+
+def test_mdgemm_check_finite():
+    print("[case] mdgemm nonfinite check", flush=True)
+    A, B = _operands(2, 8, 8, 8, 14)
+    A[1, 2, 3] = np.inf
+    with pytest.raises(md.MdgemmError) as ei:
+        md.mdgemm_ex(_gpu(A), _gpu(B), flags=md.MDGEMM_CHECK_FINITE)
+    assert ei.value.status == md.MDGEMM_ENONFINITE
+    A[1, 2, 3] = 0.0
+    C = md.mdgemm_ex(_gpu(A), _gpu(B), flags=md.MDGEMM_CHECK_FINITE | md.MDGEMM_SYNC)
+    assert np.array_equal(C.cpu().numpy(), pipeline.full_reference(A, B, 8, 7)["C"])
