@@ -1,0 +1,207 @@
+#!/usr/bin/env python3
+"""Throughput of the multiple-double product C = A.B on one MI355X.
+
+One step = one ``mdgemm_ex`` call over the whole path (row/column exponents,
+exact splits of A and B, the level GEMMs on the FP64 matrix cores, exact
+accumulation and rounding), with A, B, C and the workspace resident in HBM.
+
+Prints one JSON line:
+* ``value``: effective multiple-double GFLOP/s = 2 m n k / (time per step);
+* ``roofline``: the level-GEMM kernel (the dominant one) against the FP64 MFMA
+  peak: algorithmic flops 2 m n k |pairs| per launch over its average duration
+  from HIP events recorded on the launch stream around it in every timed step;
+  ``traffic`` is the HBM bytes per launch from the committed rocprofv3 counter
+  summary of this kernel and workload, or null when the kernel source changed
+  after the counters were taken;
+* ``stages``: every stage's average time and algorithmic rate;
+* ``cpu_baseline``: the CPU oracle's classic multiple-double GEMM (one
+  sequential inner product per element, all host cores) timed on a bounded
+  sample of the same product's rows.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+MFMA_F64_PEAK_TFLOPS = 78.6  # MI355X dense FP64 matrix peak (published)
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E (published)
+METRIC = "effective dd/qd GEMM GFLOP/s; % FP64 MFMA peak; bit-exact+tol vs CPU oracle"
+GEMM_SOURCE = os.path.join(ROOT, "paper_2607_06881_amd", "csrc", "slice_gemm.hip")
+DEFAULT_CONFIG = "c2"
+
+
+def kernel_source_hash(path: str = GEMM_SOURCE) -> str:
+    with open(path, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def stored_traffic(config: str):
+    """HBM bytes per level-GEMM launch from profiles/slice_gemm_<config>_pmc.txt
+    (lines ``key = value``), if its recorded source hash matches the kernel."""
+    path = os.path.join(ROOT, "profiles", f"slice_gemm_{config}_pmc.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for ln in fh:
+            if "=" in ln and not ln.lstrip().startswith("#"):
+                key, v = ln.split("=", 1)
+                vals[key.strip()] = v.strip()
+    if vals.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, A, B, target_s: float):
+    """Classic multiple-double GEMM of the CPU oracle on a sample of rows of C."""
+    import numpy as np  # noqa: F401
+
+    from oracle import coracle
+
+    coracle.lib()
+    # calibrate on a few rows per thread, then size the sample to about target_s seconds
+    threads = coracle.num_threads()
+    rows = min(w.m, 4 * threads)
+    t = time.perf_counter()
+    coracle.classic_gemm(A[:, :rows, :], B)
+    dt = max(time.perf_counter() - t, 1e-3)
+    rows = int(min(w.m, max(threads, rows * target_s / dt)))
+    t = time.perf_counter()
+    _, used = coracle.classic_gemm(A[:, :rows, :], B)
+    dt = time.perf_counter() - t
+    flops = 2.0 * rows * w.n * w.k
+    return {
+        "value": flops / dt / 1e9,
+        "unit": "GFLOP/s",
+        "cores": int(used),
+        "kind": "oracle",
+        "sample": f"classic {'double-double (Dekker/Hida-Li-Bailey add+mul)' if w.limbs == 2 else f'{w.limbs}-limb exact-expansion'}"
+                  f" GEMM, rows 0..{rows - 1} of C ({rows} x {w.n} x {w.k}), {dt:.1f} s on {used} threads",
+        "seconds": dt,
+    }
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default=DEFAULT_CONFIG, help="workload c0..c4 (default c2)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only (the product has no multi-GPU path); use --gpus 1",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2607_06881_amd import mdgemm as md
+    from paper_2607_06881_amd import workloads
+
+    w = workloads.WORKLOADS[args.config]
+    dev = torch.device("cuda:0")
+    md.lib()  # fail loudly if the HIP library is missing
+
+    A_h, B_h = workloads.make_workload(w)
+    A = torch.from_numpy(A_h).to(dev)
+    B = torch.from_numpy(B_h).to(dev)
+    C = torch.empty((w.limbs, w.m, w.n), dtype=torch.float64, device=dev)
+    spl = w.slices // w.limbs
+    ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, slices_per_limb=spl, cutoff=w.cutoff),
+                     dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(flags=0):
+        md.mdgemm_ex(A, B, C, slices_per_limb=spl, cutoff=w.cutoff, workspace=ws, flags=flags, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    stage_sum = np.zeros(4)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step(md.MDGEMM_TIME_STAGES)
+        stage_sum += np.array(md.mdgemm_stage_times())  # waits for this step's last event
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    stage_ms = stage_sum / args.steps
+
+    md_flops = w.md_flops()
+    slice_flops = w.slice_flops()
+    value = md_flops / (ms_per_step * 1e-3) / 1e9
+
+    m, n, k, L, S, T = w.m, w.n, w.k, w.limbs, w.slices, w.cutoff
+    bytes_exp = 8.0 * (m * k + k * n) + 4.0 * (m + n)
+    bytes_split = 8.0 * L * (m * k + k * n) + 8.0 * S * (m * k + k * n) + 4.0 * (m + n)
+    bytes_acc = 8.0 * (T + 1) * m * n + 8.0 * L * m * n + 4.0 * (m + n)
+    gemm_ms = stage_ms[2]
+    achieved = slice_flops / (gemm_ms * 1e-3) / 1e12
+    roofline = {
+        "bound": "mfma",
+        "achieved": round(achieved, 3),
+        "peak": MFMA_F64_PEAK_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": round(achieved / MFMA_F64_PEAK_TFLOPS, 4),
+        "traffic": stored_traffic(args.config),
+        "kernel": "slice_gemm_kernel (level GEMMs, v_mfma_f64_16x16x4f64)",
+        "flops_per_launch": slice_flops,
+        "avg_launch_ms": round(gemm_ms, 4),
+    }
+    stages = {
+        "exponents": {"ms": round(stage_ms[0], 4), "GB/s": round(bytes_exp / (stage_ms[0] * 1e-3) / 1e9, 1),
+                      "bytes": bytes_exp},
+        "split": {"ms": round(stage_ms[1], 4), "GB/s": round(bytes_split / (stage_ms[1] * 1e-3) / 1e9, 1),
+                  "bytes": bytes_split},
+        "slice_gemm": {"ms": round(stage_ms[2], 4), "TFLOP/s": round(achieved, 3)},
+        "accum_renorm": {"ms": round(stage_ms[3], 4), "GB/s": round(bytes_acc / (stage_ms[3] * 1e-3) / 1e9, 1),
+                         "bytes": bytes_acc},
+        "hbm_peak_GB/s": HBM_PEAK_GBS,
+    }
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}: {w.description}",
+            "m": m, "n": n, "k": k, "limbs": L, "slices": S, "cutoff": T, "pairs": w.pairs, "seed": w.seed,
+        },
+        "roofline": roofline,
+        "stages": stages,
+        "slice_gemm_share": round(stage_ms[2] / stage_ms.sum(), 4),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, A_h, B_h, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,112 @@
+"""The five synthetic workloads at full size, in the benchmark's launch
+configuration (caller workspace from PyTorch, PyTorch's current stream).
+
+Full-size outputs are checked where the oracle can follow them: exponents of
+every row and column; digits of sampled rows of A and columns of B; level
+products and final limbs of sampled output entries, bit-exact; the tolerance
+4 k 2^-(53L-4) (|A||B|) against the exact rational product on those entries;
+and the nonoverlap property of every output element.  The 64^3 workload is
+checked on every entry.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import coracle, exact, pipeline
+from paper_2607_06881_amd import mdgemm as md
+from paper_2607_06881_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+def _run(w):
+    A_h, B_h = workloads.make_workload(w)
+    A, B = torch.from_numpy(A_h).to(DEV), torch.from_numpy(B_h).to(DEV)
+    spl = w.slices // w.limbs
+    ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, slices_per_limb=spl, cutoff=w.cutoff),
+                     dtype=torch.uint8, device=DEV)
+    C = md.mdgemm_ex(A, B, slices_per_limb=spl, cutoff=w.cutoff, workspace=ws)
+    torch.cuda.synchronize()
+    return A_h, B_h, A, B, C
+
+
+def _sample_entries(EA, EB, count, seed):
+    rng = np.random.default_rng(seed)
+    m, n = len(EA), len(EB)
+    rows = {0, m - 1, int(np.argmin(EA)), int(np.argmax(EA))}
+    cols = {0, n - 1, int(np.argmin(EB)), int(np.argmax(EB))}
+    entries = {(i, j) for i in rows for j in cols}
+    while len(entries) < count:
+        entries.add((int(rng.integers(m)), int(rng.integers(n))))
+    return sorted(entries)
+
+
+def _nonoverlap_all(C):
+    ok = np.ones(C.shape[1:], dtype=bool)
+    for l in range(C.shape[0] - 1):
+        hi, lo = C[l], C[l + 1]
+        ok &= np.where(hi == 0, lo == 0, np.abs(lo) <= 0.5 * np.spacing(np.abs(hi)))
+    return ok.all()
+
+
+@pytest.mark.parametrize("name", ["c0", "c1", "c2", "c3", "c4"])
+def test_workload_full_size(name):
+    w = workloads.WORKLOADS[name]
+    print(f"[case] workload {name}: {w.description}", flush=True)
+    A_h, B_h, A, B, C = _run(w)
+    C_h = C.cpu().numpy()
+    del C
+    S, T, L = w.slices, w.cutoff, w.limbs
+
+    # a1: every exponent
+    EA_g = md.mdgemm_exponents(A[0], 0)
+    EB_g = md.mdgemm_exponents(B[0], 1)
+    EA = coracle.exponents(A_h[0], 0)
+    EB = coracle.exponents(B_h[0], 1)
+    assert np.array_equal(EA_g.cpu().numpy(), EA) and np.array_equal(EB_g.cpu().numpy(), EB)
+
+    assert _nonoverlap_all(C_h)
+    assert np.isfinite(C_h).all()
+
+    if name == "c0":
+        ref = pipeline.full_reference(A_h, B_h, S, T)
+        assert np.array_equal(C_h, ref["C"])
+        entries = [(i, j) for i in range(0, w.m, 3) for j in range(0, w.n, 5)]
+    else:
+        entries = _sample_entries(EA, EB, 40, w.seed)
+        ref = pipeline.reference_entries(A_h, B_h, S, T, entries)
+        for (i, j), r in ref.items():
+            assert C_h[:, i, j].tolist() == r["limbs"], (i, j)
+
+        # a2: digits of sampled rows of A / columns of B
+        rows = sorted({i for i, _ in entries})[:12]
+        cols = sorted({j for _, j in entries})[:12]
+        DA = md.mdgemm_split(A, EA_g, S, 0)
+        DB = md.mdgemm_split(B, EB_g, S, 1)
+        DA_rows = DA[:, rows, :].cpu().numpy()
+        DB_cols = DB[:, :, cols].cpu().numpy()
+        assert np.array_equal(DA_rows, coracle.split(np.ascontiguousarray(A_h[:, rows, :]), EA[rows], S, 0))
+        assert np.array_equal(DB_cols, coracle.split(np.ascontiguousarray(B_h[:, :, cols]), EB[cols], S, 1))
+        # a3: level products of the sampled entries
+        G = md.mdgemm_slice_gemm(DA, DB, T)
+        ii = torch.tensor([i for i, _ in entries], device=DEV)
+        jj = torch.tensor([j for _, j in entries], device=DEV)
+        G_s = G[:, ii, jj].cpu().numpy()
+        del DA, DB, G
+        torch.cuda.empty_cache()
+        for e, (i, j) in enumerate(entries):
+            assert G_s[:, e].astype(np.int64).tolist() == ref[(i, j)]["levels"], (i, j)
+
+    # final limbs against the exact product
+    worst = 0.0
+    for (i, j) in entries[:40]:
+        want, mag = exact.exact_product(A_h, B_h, i, j)
+        err = abs(exact.value(C_h[:, i, j]) - want)
+        bound = exact.tolerance(w.k, L, mag)
+        assert err <= bound, (i, j, float(err / bound))
+        worst = max(worst, float(err / bound))
+    print(f"[result] {name}: max |C - C_exact| / bound over {min(len(entries), 40)} entries = {worst:.3e}",
+          flush=True)
