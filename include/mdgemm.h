@@ -88,8 +88,9 @@ int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const do
 
 /* Bytes of device workspace mdgemm_ex needs for this product and these options
  * (0 for an empty product; SIZE_MAX for invalid arguments).  Layout, each part
- * aligned to 256 bytes: EA int32[m], EB int32[n], flag int32, DA f64[S][m][k],
- * DB f64[S][k][n], G f64[T+1][m][n]. */
+ * aligned to 256 bytes: EA int32[m], EB int32[n], flag int32, the digit panels
+ * DAt f64[S][kp][mp] and DBp f64[S][kp][np] (kp = k rounded up to 16, mp and np =
+ * m and n rounded up to 128), G f64[T+1][m][n]. */
 size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts);
 
 /* C = A.B with explicit options (opts may be NULL for the defaults).  Runs, in
@@ -133,16 +134,29 @@ int mdgemm_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int
 int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int axis, const double* X, const int32_t* E,
                  double* D, void* stream);
 
+/* Step a2 into the operand layout of mdgemm_slice_gemm ("panels"): the same
+ * digits as mdgemm_split, k-major and zero-padded to whole GEMM tiles, with
+ * kp = cols rounded up to 16 for axis 0 (rows up to 16 for axis 1) and
+ * cp = rows (axis 0) or cols (axis 1) rounded up to 128:
+ *   axis 0 (A, rows = m, cols = k):  D [slices][kp][cp], D[s][kk][i] = digit s of A[i][kk];
+ *   axis 1 (B, rows = k, cols = n):  D [slices][kp][cp], D[s][kk][j] = digit s of B[kk][j].
+ * Every padding entry is +0.0.  Arguments and requirements as mdgemm_split. */
+int mdgemm_split_panel(int64_t rows, int64_t cols, int limbs, int slices, int axis, const double* X,
+                       const int32_t* E, double* D, void* stream);
+
 /* Step a3, the slice GEMMs (section 2, equation (3) and the rewritten product).
- * DA [S][m][k], DB [S][k][n] integer-valued digits with |digit| <= 8191.
+ * DAt and DBp are digit panels (see mdgemm_split_panel) with |digit| <= 8191:
+ * DAt [S][kp][mp] holds A's digits transposed, DBp [S][kp][np] holds B's, where
+ * kp = k rounded up to 16, mp = m and np = n rounded up to 128, zero padding;
+ * both pointers 16-byte aligned.
  * per_pair == 0: out [T+1][m][n], out[t] = sum over p + q = t (0 <= p, q < S) of
  * DA_p . DB_q for t = 0..cutoff.  per_pair != 0: out [S][S][m][n],
  * out[p][q] = DA_p . DB_q for every p + q <= cutoff (other planes untouched).
  * Exact in FP64 (any summation order) because every partial sum is an integer
  * below 2^53; returns MDGEMM_EEXACT when pairs_t * k * 8191^2 >= 2^53.
  * S in 1..16, cutoff in 0..2S-2. */
-int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, int per_pair, const double* DA,
-                      const double* DB, double* out, void* stream);
+int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, int per_pair, const double* DAt,
+                      const double* DBp, double* out, void* stream);
 
 /* Step a4 alone, the exact accumulation (section 2, steps 4-5), exported for
  * checking.  G [levels][m][n] integer-valued with |G| < 2^53, levels 1..31.

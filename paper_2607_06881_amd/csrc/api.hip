@@ -137,9 +137,11 @@ bool layout(int64_t m, int64_t n, int64_t k, const Resolved& r, Layout* L) {
   L->flag = off;
   off += align_up(sizeof(int32_t));
   L->da = off;
-  off += align_up(sizeof(double) * static_cast<size_t>(r.S) * static_cast<size_t>(m) * static_cast<size_t>(k));
+  const size_t kp = static_cast<size_t>(mdg::panel_k(k)), mp = static_cast<size_t>(mdg::panel_mn(m)),
+               np = static_cast<size_t>(mdg::panel_mn(n));
+  off += align_up(sizeof(double) * static_cast<size_t>(r.S) * kp * mp);
   L->db = off;
-  off += align_up(sizeof(double) * static_cast<size_t>(r.S) * static_cast<size_t>(k) * static_cast<size_t>(n));
+  off += align_up(sizeof(double) * static_cast<size_t>(r.S) * kp * np);
   L->g = off;
   off += align_up(sizeof(double) * static_cast<size_t>(r.T + 1) * static_cast<size_t>(m) * static_cast<size_t>(n));
   L->total = off;
@@ -315,8 +317,8 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, EB, s)));
   if (timed) MDG_TRY(record(1, s));
   // a2: exact splits into S digit planes
-  MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, 0, A, EA, DA, s)));
-  MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, 1, B, EB, DB, s)));
+  MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, 0, A, EA, DA, true, s)));
+  MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, 1, B, EB, DB, true, s)));
   if (timed) MDG_TRY(record(2, s));
   // a3: level GEMMs on the FP64 matrix cores
   MDG_TRY(hip_status(mdg::launch_slice_gemm(m, n, k, DA, DB, G, level_jobs(r.S, r.T), s)));
@@ -384,24 +386,44 @@ int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int axis, co
   const size_t xbytes = sizeof(double) * limbs * static_cast<size_t>(rows) * static_cast<size_t>(cols);
   const size_t dbytes = sizeof(double) * slices * static_cast<size_t>(rows) * static_cast<size_t>(cols);
   if (overlaps(D, dbytes, X, xbytes)) return MDGEMM_EINVAL;
-  return hip_status(mdg::launch_split(rows, cols, limbs, slices, axis, X, E, D, static_cast<hipStream_t>(stream)));
+  return hip_status(
+      mdg::launch_split(rows, cols, limbs, slices, axis, X, E, D, false, static_cast<hipStream_t>(stream)));
 }
 
-int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, int per_pair, const double* DA,
-                      const double* DB, double* out, void* stream) {
+int mdgemm_split_panel(int64_t rows, int64_t cols, int limbs, int slices, int axis, const double* X,
+                       const int32_t* E, double* D, void* stream) {
+  if (rows < 0 || cols < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || slices < 1 || slices > MDGEMM_MAX_SLICES ||
+      (axis != 0 && axis != 1))
+    return MDGEMM_EINVAL;
+  if (rows == 0 || cols == 0) return MDGEMM_OK;
+  if (!X || !E || !D) return MDGEMM_EINVAL;
+  const int64_t K = axis == 0 ? cols : rows, Cn = axis == 0 ? rows : cols;
+  const size_t xbytes = sizeof(double) * limbs * static_cast<size_t>(rows) * static_cast<size_t>(cols);
+  const size_t dbytes = sizeof(double) * slices * static_cast<size_t>(mdg::panel_k(K)) *
+                        static_cast<size_t>(mdg::panel_mn(Cn));
+  if (overlaps(D, dbytes, X, xbytes)) return MDGEMM_EINVAL;
+  return hip_status(
+      mdg::launch_split(rows, cols, limbs, slices, axis, X, E, D, true, static_cast<hipStream_t>(stream)));
+}
+
+int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, int per_pair, const double* DAt,
+                      const double* DBp, double* out, void* stream) {
   if (m < 0 || n < 0 || k < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || cutoff < 0 ||
       cutoff > 2 * slices - 2)
     return MDGEMM_EINVAL;
   if (m == 0 || n == 0) return MDGEMM_OK;
-  if (!out || (k > 0 && (!DA || !DB))) return MDGEMM_EINVAL;
+  if (!out || (k > 0 && (!DAt || !DBp))) return MDGEMM_EINVAL;
+  // panel rows are read 16 bytes per lane
+  if ((reinterpret_cast<uintptr_t>(DAt) | reinterpret_cast<uintptr_t>(DBp)) & 15u) return MDGEMM_EINVAL;
+  const size_t kp = static_cast<size_t>(mdg::panel_k(k));
   const size_t obytes = sizeof(double) * static_cast<size_t>(per_pair ? slices * slices : cutoff + 1) *
                         static_cast<size_t>(m) * static_cast<size_t>(n);
-  if (k > 0 && (overlaps(out, obytes, DA, sizeof(double) * slices * static_cast<size_t>(m) * k) ||
-                overlaps(out, obytes, DB, sizeof(double) * slices * static_cast<size_t>(k) * n)))
+  if (k > 0 && (overlaps(out, obytes, DAt, sizeof(double) * slices * kp * static_cast<size_t>(mdg::panel_mn(m))) ||
+                overlaps(out, obytes, DBp, sizeof(double) * slices * kp * static_cast<size_t>(mdg::panel_mn(n)))))
     return MDGEMM_EINVAL;
   if (!exact_ok(k, per_pair ? 1 : max_pairs(slices, cutoff))) return MDGEMM_EEXACT;
   const JobTable jt = per_pair ? pair_jobs(slices, cutoff) : level_jobs(slices, cutoff);
-  return hip_status(mdg::launch_slice_gemm(m, n, k, DA, DB, out, jt, static_cast<hipStream_t>(stream)));
+  return hip_status(mdg::launch_slice_gemm(m, n, k, DAt, DBp, out, jt, static_cast<hipStream_t>(stream)));
 }
 
 int mdgemm_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, void* stream) {

@@ -12,6 +12,13 @@ constexpr int kDigitMax = (1 << kSliceBits) - 1;  // 8191
 constexpr int kMaxSlices = 16;
 constexpr int kMaxLimbs = 4;
 constexpr int kZWords = 8;
+constexpr int kTileMN = 128;  // level-GEMM tile rows / columns
+constexpr int kTileK = 16;    // level-GEMM k step
+
+// Panel dimensions of the level-GEMM operands: k rounded up to the k step,
+// m / n rounded up to the tile.
+inline int64_t panel_k(int64_t k) { return (k + kTileK - 1) / kTileK * kTileK; }
+inline int64_t panel_mn(int64_t x) { return (x + kTileMN - 1) / kTileMN * kTileMN; }
 
 // Slice-pair jobs of the level GEMM: job j multiplies the pairs
 // (p_first + i, q_first - i) for i < npairs into output plane out[j].
@@ -26,12 +33,16 @@ struct JobTable {
 // a1: per-row (axis 0) or per-column (axis 1) grid exponents of a [rows][cols] plane.
 hipError_t launch_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, hipStream_t stream);
 
-// a2: digits [S][rows][cols] of X [L][rows][cols] on the grid exponents E.
+// a2: digits of X [L][rows][cols] on the grid exponents E, either row-major
+// D [S][rows][cols] (panel == false) or as a level-GEMM panel (panel == true):
+// axis 0: D [S][panel_k(cols)][panel_mn(rows)] (transposed), axis 1:
+// D [S][panel_k(rows)][panel_mn(cols)], zeros in the padding.
 hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E,
-                        double* D, hipStream_t stream);
+                        double* D, bool panel, hipStream_t stream);
 
-// a3: level or pair products; `jobs` lists the pair groups, outputs are [*][m][n].
-hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DA, const double* DB, double* out,
+// a3: level or pair products of the panels DAt [S][panel_k(k)][panel_mn(m)] and
+// DBp [S][panel_k(k)][panel_mn(n)]; `jobs` lists the pair groups, outputs are [*][m][n].
+hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DAt, const double* DBp, double* out,
                              const JobTable& jobs, hipStream_t stream);
 
 // a4: exact accumulation of `levels` planes into 8-word integers Z [8][m][n].

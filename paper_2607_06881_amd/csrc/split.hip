@@ -20,8 +20,10 @@
 // everything after it, of smaller magnitude) only decides the floor through its
 // sign, when the fraction of the accumulated part is exactly zero.
 //
-// One thread per element; consecutive threads take consecutive columns, so the
-// L limb loads and the S digit stores of a wave are contiguous 512-byte rows.
+// Two output layouts share this arithmetic: row-major digit planes (one thread
+// per element, consecutive threads on consecutive columns, so limb loads and
+// digit stores of a wave are contiguous 512-byte rows), and the k-major padded
+// panels the level GEMM reads (see split_panel_kernel).
 #include "internal.h"
 
 namespace mdg {
@@ -72,6 +74,64 @@ __device__ inline uint32_t field13(const uint64_t (&v)[NW], int pos) {
   return static_cast<uint32_t>(f) & kDigitMax;
 }
 
+// D = floor(|V| / u) for one element (L limbs at stride ls, grid unit 2^g) as an
+// NW-word integer; returns true when V < 0.
+template <int NW>
+__device__ inline bool floor_on_grid(const double* __restrict__ x, int64_t ls, int L, int g, uint64_t (&I)[NW]) {
+  const double x0 = x[0];
+  const bool neg = x0 < 0.0;
+  uint64_t acc[NW];
+#pragma unroll
+  for (int i = 0; i < NW; ++i) acc[i] = 0;
+  int tail = 0;  // +1 / -1: sign, relative to V, of the part of V below u that is not in acc
+  if (x0 != 0.0) {
+    for (int l = 0; l < L; ++l) {
+      const double xl = x[static_cast<int64_t>(l) * ls];
+      if (xl == 0.0) break;  // normalized: every later limb is zero too
+      const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(xl));
+      const bool lneg = (bits >> 63) != 0;
+      const uint64_t mag = bits & 0x7fffffffffffffffull;
+      const int be = static_cast<int>(mag >> 52);
+      uint64_t M;
+      int ex;  // |xl| = M 2^ex
+      if (be != 0) {
+        M = (mag & 0x000fffffffffffffull) | 0x0010000000000000ull;
+        ex = be - 1075;
+      } else {
+        M = mag;
+        ex = -1074;
+      }
+      const int fe = ex + (64 - __clzll(static_cast<long long>(M)));  // frexp exponent of xl
+      if (fe <= g) {  // |xl| < u: xl and the rest of the limbs lie below the grid unit
+        tail = (lneg == neg) ? 1 : -1;
+        break;
+      }
+      add_shifted<NW>(acc, M, ex - g + 52, lneg != neg);
+    }
+  }
+  // I = floor(acc / 2^52), lowered by one when the fraction is zero and the
+  // part below u is negative (relative to the sign of V).
+  const bool frac_zero = (acc[0] & 0x000fffffffffffffull) == 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) I[i] = (acc[i] >> 52) | (i + 1 < NW ? acc[i + 1] << 12 : 0ull);
+  if (frac_zero && tail < 0) {
+    uint64_t borrow = 1;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const uint64_t v = I[i];
+      I[i] = v - borrow;
+      borrow = (v < borrow) ? 1ull : 0ull;
+    }
+  }
+  return neg;
+}
+
+__device__ inline double signed_digit(uint32_t d, bool neg) {
+  const double v = static_cast<double>(d);
+  return (d == 0u) ? 0.0 : (neg ? -v : v);  // zero digits are +0.0
+}
+
+// Row-major output: D [S][rows][cols], the layout of the input planes.
 template <int NW>
 __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, int L, int S, int axis,
                                                     const double* __restrict__ X, const int32_t* __restrict__ E,
@@ -82,82 +142,76 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
   for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
     const int64_t idx = r * cols + c;
     const int e = axis == 0 ? E[r] : E[c];
-    const int g = e - kSliceBits * S;  // exponent of the grid unit u
-
-    const double x0 = X[idx];
-    const bool neg = x0 < 0.0;
-    uint64_t acc[NW];
-#pragma unroll
-    for (int i = 0; i < NW; ++i) acc[i] = 0;
-    int tail = 0;  // +1 / -1: sign, relative to V, of the part of V below u that is not in acc
-    if (x0 != 0.0) {
-      for (int l = 0; l < L; ++l) {
-        const double xl = X[static_cast<int64_t>(l) * plane + idx];
-        if (xl == 0.0) break;  // normalized: every later limb is zero too
-        const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(xl));
-        const bool lneg = (bits >> 63) != 0;
-        const uint64_t mag = bits & 0x7fffffffffffffffull;
-        const int be = static_cast<int>(mag >> 52);
-        uint64_t M;
-        int ex;  // |xl| = M 2^ex
-        if (be != 0) {
-          M = (mag & 0x000fffffffffffffull) | 0x0010000000000000ull;
-          ex = be - 1075;
-        } else {
-          M = mag;
-          ex = -1074;
-        }
-        const int fe = ex + (64 - __clzll(static_cast<long long>(M)));  // frexp exponent of xl
-        if (fe <= g) {  // |xl| < u: xl and the rest of the limbs lie below the grid unit
-          tail = (lneg == neg) ? 1 : -1;
-          break;
-        }
-        add_shifted<NW>(acc, M, ex - g + 52, lneg != neg);
-      }
-    }
-    // I = floor(acc / 2^52), lowered by one when the fraction is zero and the
-    // part below u is negative (relative to the sign of V).
-    const bool frac_zero = (acc[0] & 0x000fffffffffffffull) == 0;
     uint64_t I[NW];
+    const bool neg = floor_on_grid<NW>(X + idx, plane, L, e - kSliceBits * S, I);
+    for (int s = 0; s < S; ++s)
+      D[static_cast<int64_t>(s) * plane + idx] = signed_digit(field13<NW>(I, kSliceBits * (S - 1 - s)), neg);
+  }
+}
+
+// Panel output for the level GEMM: both operands k-major and padded,
+//   axis 0 (A, rows = m, cols = k):  D [S][kp][mp],  D[s][kk][i] = digit s of A[i][kk]
+//   axis 1 (B, rows = k, cols = n):  D [S][kp][np],  D[s][kk][j] = digit s of B[kk][j]
+// with kp, mp, np rounded up to the GEMM tile (16 and 128) and zeros in the padding.
+// A block covers 64 lines (c) x 16 k: its reads of A touch 64 full 128-byte lines
+// and its stores are 512-byte rows of the panel.
+template <int NW>
+__global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t cols, int L, int S, int axis,
+                                                          int64_t kp, int64_t cp, const double* __restrict__ X,
+                                                          const int32_t* __restrict__ E, double* __restrict__ D) {
+  const int64_t plane = rows * cols, pplane = kp * cp;
+  const int64_t K = axis == 0 ? cols : rows;   // reduction length
+  const int64_t Cn = axis == 0 ? rows : cols;  // lines (rows of A or columns of B)
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * 64 + (threadIdx.x & 63);
+  for (int64_t kb = blockIdx.y; kb * 16 < kp; kb += gridDim.y) {
 #pragma unroll
-    for (int i = 0; i < NW; ++i) I[i] = (acc[i] >> 52) | (i + 1 < NW ? acc[i + 1] << 12 : 0ull);
-    if (frac_zero && tail < 0) {
-      uint64_t borrow = 1;
-#pragma unroll
-      for (int i = 0; i < NW; ++i) {
-        const uint64_t v = I[i];
-        I[i] = v - borrow;
-        borrow = (v < borrow) ? 1ull : 0ull;
+    for (int r = 0; r < 4; ++r) {
+      const int64_t kk = kb * 16 + (threadIdx.x >> 6) + 4 * r;
+      if (c >= cp) continue;
+      double* out = D + kk * cp + c;
+      if (c < Cn && kk < K) {
+        const int64_t idx = axis == 0 ? c * cols + kk : kk * cols + c;
+        uint64_t I[NW];
+        const bool neg = floor_on_grid<NW>(X + idx, plane, L, E[c] - kSliceBits * S, I);
+        for (int s = 0; s < S; ++s)
+          out[static_cast<int64_t>(s) * pplane] = signed_digit(field13<NW>(I, kSliceBits * (S - 1 - s)), neg);
+      } else {
+        for (int s = 0; s < S; ++s) out[static_cast<int64_t>(s) * pplane] = 0.0;
       }
-    }
-    for (int s = 0; s < S; ++s) {
-      const uint32_t d = field13<NW>(I, kSliceBits * (S - 1 - s));
-      const double v = static_cast<double>(d);
-      D[static_cast<int64_t>(s) * plane + idx] = (d == 0u) ? 0.0 : (neg ? -v : v);
     }
   }
 }
 
 template <int NW>
 hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E, double* D,
-                     hipStream_t stream) {
-  const unsigned gx = static_cast<unsigned>((cols + 255) / 256);
-  const unsigned gy = static_cast<unsigned>(rows < 65535 ? rows : 65535);
-  hipLaunchKernelGGL(split_kernel<NW>, dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, axis, X, E, D);
+                     bool panel, hipStream_t stream) {
+  if (!panel) {
+    const unsigned gx = static_cast<unsigned>((cols + 255) / 256);
+    const unsigned gy = static_cast<unsigned>(rows < 65535 ? rows : 65535);
+    hipLaunchKernelGGL(split_kernel<NW>, dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, axis, X, E, D);
+    return hipGetLastError();
+  }
+  const int64_t K = axis == 0 ? cols : rows, Cn = axis == 0 ? rows : cols;
+  const int64_t kp = panel_k(K), cp = panel_mn(Cn);
+  const unsigned gx = static_cast<unsigned>(cp / 64);
+  const int64_t nkb = kp / 16;
+  const unsigned gy = static_cast<unsigned>(nkb < 65535 ? nkb : 65535);
+  hipLaunchKernelGGL(split_panel_kernel<NW>, dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, axis, kp, cp, X,
+                     E, D);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E,
-                        double* D, hipStream_t stream) {
+                        double* D, bool panel, hipStream_t stream) {
   if (rows == 0 || cols == 0) return hipSuccess;
   // The accumulator holds |V| / u < 2^(13 S) with 52 fraction bits: 13 S + 52 bits.
   const int bits = kSliceBits * S + 52;
-  if (bits <= 128) return launch_nw<2>(rows, cols, L, S, axis, X, E, D, stream);
-  if (bits <= 192) return launch_nw<3>(rows, cols, L, S, axis, X, E, D, stream);
-  if (bits <= 256) return launch_nw<4>(rows, cols, L, S, axis, X, E, D, stream);
-  return launch_nw<5>(rows, cols, L, S, axis, X, E, D, stream);
+  if (bits <= 128) return launch_nw<2>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (bits <= 192) return launch_nw<3>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (bits <= 256) return launch_nw<4>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  return launch_nw<5>(rows, cols, L, S, axis, X, E, D, panel, stream);
 }
 
 }  // namespace mdg

@@ -33,6 +33,16 @@ MDGEMM_TIME_STAGES = 4
 MDGEMM_CUTOFF_DEFAULT = -1
 MDGEMM_CUTOFF_ALL = -2
 MDGEMM_Z_WORDS = 8
+PANEL_K = 16  # level-GEMM panels: k rounded up to 16,
+PANEL_MN = 128  # m and n rounded up to 128
+
+
+def panel_k(k: int) -> int:
+    return (k + PANEL_K - 1) // PANEL_K * PANEL_K
+
+
+def panel_mn(x: int) -> int:
+    return (x + PANEL_MN - 1) // PANEL_MN * PANEL_MN
 
 EXPORTED = (
     "mdgemm_opts_init",
@@ -44,6 +54,7 @@ EXPORTED = (
     "mdgemm_release",
     "mdgemm_exponents",
     "mdgemm_split",
+    "mdgemm_split_panel",
     "mdgemm_slice_gemm",
     "mdgemm_accumulate",
     "mdgemm_accum_renorm",
@@ -98,6 +109,8 @@ def lib() -> ctypes.CDLL:
         L.mdgemm_exponents.restype = ctypes.c_int
         L.mdgemm_split.argtypes = [_i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp]
         L.mdgemm_split.restype = ctypes.c_int
+        L.mdgemm_split_panel.argtypes = [_i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp]
+        L.mdgemm_split_panel.restype = ctypes.c_int
         L.mdgemm_slice_gemm.argtypes = [_i64, _i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp,
                                         _vp]
         L.mdgemm_slice_gemm.restype = ctypes.c_int
@@ -239,17 +252,35 @@ def mdgemm_split(X: torch.Tensor, E: torch.Tensor, slices: int, axis: int, D: Op
     return D
 
 
-def mdgemm_slice_gemm(DA: torch.Tensor, DB: torch.Tensor, cutoff: int, per_pair: bool = False,
-                      out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """Level products [cutoff+1, m, n] (or pair products [S, S, m, n]) of digit planes."""
-    _dev_tensor(DA, torch.float64, "DA")
-    _dev_tensor(DB, torch.float64, "DB")
-    S, m, k = DA.shape
-    n = DB.shape[2]
+def mdgemm_split_panel(X: torch.Tensor, E: torch.Tensor, slices: int, axis: int, D: Optional[torch.Tensor] = None,
+                       stream=None) -> torch.Tensor:
+    """Digits of X [L, rows, cols] as a level-GEMM panel: axis 0 (A):
+    [slices, panel_k(cols), panel_mn(rows)] (transposed); axis 1 (B):
+    [slices, panel_k(rows), panel_mn(cols)]; zero padding."""
+    _dev_tensor(X, torch.float64, "X")
+    _dev_tensor(E, torch.int32, "E")
+    L, rows, cols = X.shape
+    shape = (slices, panel_k(cols), panel_mn(rows)) if axis == 0 else (slices, panel_k(rows), panel_mn(cols))
+    if D is None:
+        D = torch.empty(shape, dtype=torch.float64, device=X.device)
+    _check(lib().mdgemm_split_panel(rows, cols, L, slices, axis, _ptr(X), _ptr(E), _ptr(D), _stream(stream)),
+           "mdgemm_split_panel")
+    return D
+
+
+def mdgemm_slice_gemm(DAt: torch.Tensor, DBp: torch.Tensor, m: int, n: int, k: int, cutoff: int,
+                      per_pair: bool = False, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Level products [cutoff+1, m, n] (or pair products [S, S, m, n]) of the digit
+    panels DAt [S, panel_k(k), panel_mn(m)] and DBp [S, panel_k(k), panel_mn(n)]."""
+    _dev_tensor(DAt, torch.float64, "DAt")
+    _dev_tensor(DBp, torch.float64, "DBp")
+    S = DAt.shape[0]
+    if tuple(DAt.shape) != (S, panel_k(k), panel_mn(m)) or tuple(DBp.shape) != (S, panel_k(k), panel_mn(n)):
+        raise ValueError("digit panels have the wrong shape")
     if out is None:
         shape = (S, S, m, n) if per_pair else (cutoff + 1, m, n)
-        out = torch.zeros(shape, dtype=torch.float64, device=DA.device)
-    _check(lib().mdgemm_slice_gemm(m, n, k, S, cutoff, int(per_pair), _ptr(DA), _ptr(DB), _ptr(out),
+        out = torch.zeros(shape, dtype=torch.float64, device=DAt.device)
+    _check(lib().mdgemm_slice_gemm(m, n, k, S, cutoff, int(per_pair), _ptr(DAt), _ptr(DBp), _ptr(out),
                                    _stream(stream)), "mdgemm_slice_gemm")
     return out
 

@@ -77,6 +77,8 @@ def test_invalid_arguments(lib):
     assert _ex(lib, 4, 4, 4, 2, C=FA + 8) == E
     assert lib.mdgemm_split(4, 4, 2, 17, 0, FA, FB, FC, None) == E
     assert lib.mdgemm_split(4, 4, 2, 8, 2, FA, FB, FC, None) == E
+    assert lib.mdgemm_split_panel(4, 4, 2, 0, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 7, 0, FA + 8, FB, FC, None) == E  # panels must be 16-byte aligned
     assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 15, 0, FA, FB, FC, None) == E
     assert lib.mdgemm_accumulate(4, 4, 32, FA, FC, None) == E
     assert lib.mdgemm_accum_renorm(4, 4, 5, 8, FA, FB, FB, FC, None) == E
@@ -110,7 +112,8 @@ def test_exactness_bound(lib, limbs, cutoff, pairs):
 def test_workspace_bytes_layout(lib):
     def expect(m, n, k, L, S, T):
         a = lambda x: (x + 255) // 256 * 256
-        return a(4 * m) + a(4 * n) + a(4) + a(8 * S * m * k) + a(8 * S * k * n) + a(8 * (T + 1) * m * n)
+        kp, mp, np_ = md.panel_k(k), md.panel_mn(m), md.panel_mn(n)
+        return a(4 * m) + a(4 * n) + a(4) + a(8 * S * kp * mp) + a(8 * S * kp * np_) + a(8 * (T + 1) * m * n)
 
     assert md.mdgemm_workspace_bytes(100, 70, 33, 2) == expect(100, 70, 33, 2, 8, 7)
     assert md.mdgemm_workspace_bytes(100, 70, 33, 2, cutoff=-2) == expect(100, 70, 33, 2, 8, 14)

@@ -91,11 +91,19 @@ def test_workload_full_size(name):
         assert np.array_equal(DA_rows, coracle.split(np.ascontiguousarray(A_h[:, rows, :]), EA[rows], S, 0))
         assert np.array_equal(DB_cols, coracle.split(np.ascontiguousarray(B_h[:, :, cols]), EB[cols], S, 1))
         # a3: level products of the sampled entries
-        G = md.mdgemm_slice_gemm(DA, DB, T)
+        DA_p = md.mdgemm_split_panel(A, EA_g, S, 0)
+        DB_p = md.mdgemm_split_panel(B, EB_g, S, 1)
+        # the panels hold the same digits (A transposed), zeros elsewhere
+        assert torch.equal(DA_p[:, :w.k, :w.m], DA.transpose(1, 2))
+        assert torch.equal(DB_p[:, :w.k, :w.n], DB)
+        assert DA_p[:, w.k:, :].abs().sum().item() == 0 and DA_p[:, :, w.m:].abs().sum().item() == 0
+        assert DB_p[:, w.k:, :].abs().sum().item() == 0 and DB_p[:, :, w.n:].abs().sum().item() == 0
+        del DA, DB
+        G = md.mdgemm_slice_gemm(DA_p, DB_p, w.m, w.n, w.k, T)
         ii = torch.tensor([i for i, _ in entries], device=DEV)
         jj = torch.tensor([j for _, j in entries], device=DEV)
         G_s = G[:, ii, jj].cpu().numpy()
-        del DA, DB, G
+        del DA_p, DB_p, G
         torch.cuda.empty_cache()
         for e, (i, j) in enumerate(entries):
             assert G_s[:, e].astype(np.int64).tolist() == ref[(i, j)]["levels"], (i, j)

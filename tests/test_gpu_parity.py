@@ -31,6 +31,18 @@ def _host(t):
     return t.cpu().numpy()
 
 
+def _panel(D, axis):
+    """Digit planes [S][rows][cols] -> level-GEMM panel (k-major, zero padded)."""
+    S, rows, cols = D.shape
+    if axis == 0:  # A: [S][kp(cols)][mp(rows)], transposed
+        P = np.zeros((S, md.panel_k(cols), md.panel_mn(rows)))
+        P[:, :cols, :rows] = D.transpose(0, 2, 1)
+    else:  # B: [S][kp(rows)][np(cols)]
+        P = np.zeros((S, md.panel_k(rows), md.panel_mn(cols)))
+        P[:, :rows, :cols] = D
+    return P
+
+
 def _operands(L, m, k, n, seed, base="uniform", row_exp=0, col_exp=0, elem_exp=0):
     rng = np.random.default_rng(seed)
     A = workloads.make_operand(rng, L, m, k, base, row_exp=row_exp, elem_exp=elem_exp)
@@ -80,6 +92,10 @@ def test_split_random(L, S, rows, cols, axis):
     want = coracle.split(X, E, S, axis)
     assert np.array_equal(got, want)
     assert not np.signbit(got[got == 0]).any()  # zero digits are +0.0
+    # the same digits as a level-GEMM panel, padding included
+    pan = _host(md.mdgemm_split_panel(Xg, Eg, S, axis))
+    assert np.array_equal(pan, _panel(want, axis))
+    assert not np.signbit(pan[pan == 0]).any()
 
 
 def _adversarial_elements(L, count, seed):
@@ -123,6 +139,8 @@ def test_split_adversarial(L):
             got = _host(md.mdgemm_split(_gpu(X), _gpu(E), S, axis))
             want = coracle.split(X, E, S, axis)
             assert np.array_equal(got, want), (axis, S)
+            pan = _host(md.mdgemm_split_panel(_gpu(X), _gpu(E), S, axis))
+            assert np.array_equal(pan, _panel(want, axis)), (axis, S)
 
 
 def test_split_golden_cases():
@@ -151,7 +169,7 @@ def test_levels(S, T, m, k, n):
     DA = rng.integers(-8191, 8192, (S, m, k)).astype(np.float64)
     DB = rng.integers(-8191, 8192, (S, k, n)).astype(np.float64)
     DA[:, rng.random((m, k)) < 0.1] = 0.0
-    got = _host(md.mdgemm_slice_gemm(_gpu(DA), _gpu(DB), T))
+    got = _host(md.mdgemm_slice_gemm(_gpu(_panel(DA, 0)), _gpu(_panel(DB, 1)), m, n, k, T))
     want = coracle.levels(DA, DB, T)
     assert np.array_equal(got, want.astype(np.float64))
 
@@ -164,7 +182,7 @@ def test_pair_products(S, T):
     DA = rng.integers(-8191, 8192, (S, m, k)).astype(np.float64)
     DB = rng.integers(-8191, 8192, (S, k, n)).astype(np.float64)
     out = torch.full((S, S, m, n), -1.0, dtype=torch.float64, device=DEV)
-    got = _host(md.mdgemm_slice_gemm(_gpu(DA), _gpu(DB), T, per_pair=True, out=out))
+    got = _host(md.mdgemm_slice_gemm(_gpu(_panel(DA, 0)), _gpu(_panel(DB, 1)), m, n, k, T, per_pair=True, out=out))
     want = coracle.levels(DA, DB, T, per_pair=True)
     for p in range(S):
         for q in range(S):
@@ -178,9 +196,9 @@ def test_levels_near_exactness_limit():
     # All digits 8191: G_t = pairs_t k 8191^2 in closed form, up to 2^51.
     print("[case] levels near 2^53", flush=True)
     S, T, m, n, k = 16, 15, 128, 128, 2**21
-    DA = torch.full((S, m, k), 8191.0, dtype=torch.float64, device=DEV)
+    DA = torch.full((S, k, m), 8191.0, dtype=torch.float64, device=DEV)  # panels: k-major, already whole tiles
     DB = torch.full((S, k, n), -8191.0, dtype=torch.float64, device=DEV)
-    got = _host(md.mdgemm_slice_gemm(DA, DB, T))
+    got = _host(md.mdgemm_slice_gemm(DA, DB, m, n, k, T))
     for t in range(T + 1):
         want = -float(len(exact.pairs_of_level(t, S)) * k * 8191**2)
         assert (got[t] == want).all(), t
