@@ -101,6 +101,9 @@ def main(argv=None) -> int:
     ap.add_argument("--config", default=DEFAULT_CONFIG, help="workload c0..c4 (default c2)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after the timed steps, run 3 device copies of this many MiB (calibrates the HBM byte "
+                         "counters of a profiler run against a known size)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -144,6 +147,14 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
     ms_per_step = e0.elapsed_time(e1) / args.steps
     stage_ms = stage_sum / args.steps
+
+    if args.copy_probe_mib > 0:
+        src = torch.ones(args.copy_probe_mib * (1 << 20) // 8, dtype=torch.float64, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     md_flops = w.md_flops()
     slice_flops = w.slice_flops()

@@ -26,30 +26,35 @@
 //   D[4r + l/16][l%16]).  One instruction occupies a SIMD's matrix pipe for 64
 //   cycles; four waves (one per SIMD), each with a 64 x 64 sub-tile held in 16
 //   independent accumulators, keep the pipes busy.
-// * Tiles go global -> registers -> LDS in 16-byte pieces (a wave reads one
-//   1 KB panel row per instruction).  Two LDS stages: the global loads of step
-//   it+1 are issued before the 64 MFMAs of step it and written to the other
-//   stage after them; one barrier per step.
+// * Tiles go global -> LDS directly with global_load_lds_dwordx4 (64 lanes x
+//   16 bytes = one 1 KB panel row per wave instruction; no staging registers).
+//   Two LDS stages, one barrier per step.  Within a step a wave first reads
+//   all its fragments of the current stage (32 doubles), then issues the
+//   copies of the next step into the other stage, then runs its 64 MFMAs:
+//   since no LDS read follows a copy in flight, nothing waits for the copies
+//   until the next step's barrier, and they land while the MFMAs run.
 // * LDS rows are padded to 144 doubles so that the two 16-lane halves of a
 //   fragment read (consecutive k rows) fall on different banks.
-// * Fragments of the next k-group are read from LDS while the current group's
-//   MFMAs run (two register buffers).
 //
 // Work decomposition: grid.x = output tiles, grid.y = jobs (levels, heaviest
 // first, or single pairs).  Tiles are renumbered so that each of the 8 XCDs
-// (blocks are dealt to XCDs round-robin) works on a contiguous band of tiles
-// that share rows of DAt, which keeps them in that XCD's L2.
+// (blocks are dealt to XCDs round-robin) works on its own chunk of tiles, and
+// the blocks resident on one XCD at a time cover an about 8 x 8 patch whose
+// panel rows stay in that XCD's L2.
 #include "internal.h"
 
 namespace mdg {
 namespace {
 
 typedef double d4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int BM = kTileMN, BN = kTileMN, BK = kTileK;
 constexpr int LDS_LD = BM + 16;  // doubles per LDS row
 constexpr int kThreads = 256;
 constexpr int kXcds = 8;
+constexpr int kGroup = 8;  // tile-rows per group of the tile order
+constexpr unsigned kWaitVmcnt0 = 0x0F70;  // s_waitcnt vmcnt(0)
 
 static_assert(BM == 128 && BN == 128 && BK == 16, "the load mapping assumes 128 x 128 x 16 tiles and 4 waves");
 
@@ -61,15 +66,20 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
   __shared__ double As[2][BK * LDS_LD];
   __shared__ double Bs[2][BK * LDS_LD];
 
-  // XCD-aware renumbering: block b runs on XCD b % 8; give XCD x the tiles
-  // [x * per, (x+1) * per) in row-major tile order.
-  int tile = blockIdx.x;
+  // Tile order.  Block b runs on XCD b % 8 (round-robin dispatch); XCD x takes
+  // the chunk [x * per, (x+1) * per) of an order that walks groups of kGroup
+  // tile-rows column by column, so the ~64 blocks resident on one XCD at a time
+  // form a near-square patch of tiles and share their panel rows in its L2.
+  int t = blockIdx.x;
   {
     const int per = ntiles / kXcds;
-    if (tile < per * kXcds) tile = (tile % kXcds) * per + tile / kXcds;
+    if (t < per * kXcds) t = (t % kXcds) * per + t / kXcds;
   }
-  const int64_t m0 = static_cast<int64_t>(tile / tiles_n) * BM;
-  const int64_t n0 = static_cast<int64_t>(tile % tiles_n) * BN;
+  const int tiles_m = ntiles / tiles_n;
+  const int gsz = kGroup * tiles_n, g = t / gsz, first = g * kGroup;
+  const int rows_in = min(kGroup, tiles_m - first), within = t - g * gsz;
+  const int64_t m0 = static_cast<int64_t>(first + within % rows_in) * BM;
+  const int64_t n0 = static_cast<int64_t>(within / rows_in) * BN;
   const int job = blockIdx.y;
   const int p_first = jobs.p_first[job], q_first = jobs.q_first[job], npairs = jobs.npairs[job];
   const int64_t plane_a = kp * mp, plane_b = kp * np;
@@ -80,26 +90,27 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
   const int64_t nkb = kp / BK;
   const int64_t niter = nkb * npairs;
 
-  // Step copies: 16 panel rows x 128 doubles per operand = 1024 16-byte pieces,
-  // four per thread; piece idx = r * 256 + tid covers row idx / 64, doubles
-  // 2 (idx % 64) .. +1.  A wave reads 1 KB contiguous per instruction.
-  typedef double d2 __attribute__((ext_vector_type(2)));
-  d2 ra[4], rb[4];
-  const int prow = tid >> 6, pcol = 2 * (tid & 63);
-  auto load = [&](int pi, int64_t kb) {
-    const double* a = DAt + static_cast<int64_t>(p_first + pi) * plane_a + (kb * BK + prow) * mp + m0 + pcol;
-    const double* b = DBp + static_cast<int64_t>(q_first - pi) * plane_b + (kb * BK + prow) * np + n0 + pcol;
+  // Direct global -> LDS copies (global_load_lds_dwordx4, 1 KB panel row per wave
+  // instruction); wave w copies rows 4w .. 4w+3 of the A and of the B tile.
+  const int lane_off = 2 * lane;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  int lpi = 0;
+  int64_t lkb = 0;  // the step the next copy fetches
+  auto issue = [&](int stage) {
+    const double* a = DAt + static_cast<int64_t>(p_first + lpi) * plane_a + (lkb * BK + 4 * wave_u) * mp + m0;
+    const double* b = DBp + static_cast<int64_t>(q_first - lpi) * plane_b + (lkb * BK + 4 * wave_u) * np + n0;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      ra[r] = *reinterpret_cast<const d2*>(a + 4 * r * mp);
-      rb[r] = *reinterpret_cast<const d2*>(b + 4 * r * np);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a + r * mp + lane_off),
+                                       (lds_void*)(&As[stage][(4 * wave_u + r) * LDS_LD]),
+                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(b + r * np + lane_off),
+                                       (lds_void*)(&Bs[stage][(4 * wave_u + r) * LDS_LD]),
+                                       16, 0, 0);
     }
-  };
-  auto store = [&](int stage) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      *reinterpret_cast<d2*>(&As[stage][(prow + 4 * r) * LDS_LD + pcol]) = ra[r];
-      *reinterpret_cast<d2*>(&Bs[stage][(prow + 4 * r) * LDS_LD + pcol]) = rb[r];
+    if (++lkb == nkb) {
+      lkb = 0;
+      ++lpi;
     }
   };
 
@@ -109,53 +120,32 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
 
-  int pi = 0;
-  int64_t kb = 0;
-  if (niter > 0) {
-    load(0, 0);
-    store(0);
-  }
-  __syncthreads();
-
   const int frag_col = lane & 15, frag_k = lane >> 4;
+  if (niter > 0) issue(0);
   for (int64_t it = 0; it < niter; ++it) {
     const int cur = static_cast<int>(it & 1);
-    const bool more = it + 1 < niter;
-    if (more) {
-      if (++kb == nkb) {
-        kb = 0;
-        ++pi;
-      }
-      load(pi, kb);  // in flight during this step's MFMAs
-    }
-    // 16 x 64 x 64 per wave: four k-groups of 16 MFMAs, the fragments of
-    // group kg+1 read while group kg runs.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // this wave's copies of step it are in LDS
+    __syncthreads();                     // everyone's are; everyone is done reading the other stage
+    // all fragments of this step first, then the copies for the next step, then
+    // the MFMAs: no LDS read follows a copy in flight, so nothing waits for it.
     const double* as = As[cur] + frag_k * LDS_LD + wr * 64 + frag_col;
     const double* bs = Bs[cur] + frag_k * LDS_LD + wc * 64 + frag_col;
-    double af[2][4], bf[2][4];
+    double af[4][4], bf[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      af[0][i] = as[i * 16];
-      bf[0][i] = bs[i * 16];
-    }
+    for (int kg = 0; kg < BK / 4; ++kg)
 #pragma unroll
-    for (int kg = 0; kg < BK / 4; ++kg) {
-      const int c = kg & 1;
-      if (kg + 1 < BK / 4) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          af[c ^ 1][i] = as[(kg + 1) * 4 * LDS_LD + i * 16];
-          bf[c ^ 1][i] = bs[(kg + 1) * 4 * LDS_LD + i * 16];
-        }
+      for (int i = 0; i < 4; ++i) {
+        af[kg][i] = as[kg * 4 * LDS_LD + i * 16];
+        bf[kg][i] = bs[kg * 4 * LDS_LD + i * 16];
       }
+    if (it + 1 < niter) issue(cur ^ 1);
+#pragma unroll
+    for (int kg = 0; kg < BK / 4; ++kg)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[c][i], bf[c][j], acc[i][j], 0, 0, 0);
-    }
-    if (more) store(cur ^ 1);
-    __syncthreads();
+          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[kg][i], bf[kg][j], acc[i][j], 0, 0, 0);
   }
 
   double* o = out + static_cast<int64_t>(jobs.out[job]) * m * n;
