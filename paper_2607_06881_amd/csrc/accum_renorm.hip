@@ -9,7 +9,8 @@
 // Level t of an output element is an integer G_t, |G_t| < 2^53, of weight
 // 2^(-13 t) (times the grid scale 2^(EA + EB - 26)).  Their sum is formed
 // exactly, in increasing significance (t = T down to 0), as the two's-complement
-// integer N = sum_t G_t 2^(13 (T - t)) held in NW 64-bit words in registers;
+// integer N = sum_t G_t 2^(13 (T - t)) held in NW 64-bit words in registers
+// (a base-2^13 carry chain: one int64 add, mask and shift per level);
 // the value is Z = N 2^(-13 T).  The L limbs are then peeled off greedily with
 // round-to-nearest-even: c_0 = RN(Z), c_1 = RN(Z - c_0), ..., each taken from
 // the 53 leading bits of the remaining magnitude with the round bit and the
@@ -43,16 +44,44 @@ __device__ inline void add_shifted_signed(uint64_t (&N)[NW], int64_t g, int sh) 
   }
 }
 
+// N = sum_t G_t 2^(13 (T - t)) exactly.  Level t is column j = T - t of weight
+// 2^(13 j); the columns are visited in increasing significance (t = T down to
+// 0) with a running carry in base 2^13: v = G_t + carry, the low 13 bits of v
+// are the digit of column j (placed into N, whose bits there are still zero)
+// and carry = floor(v / 2^13).  |G_t| < 2^53 keeps |v| < 2^54, so int64 never
+// overflows; the last carry, signed, is added above column T.
+// Loads are issued eight levels at a time before any of them is used, so a
+// thread keeps up to eight independent loads in flight.
 template <int NW>
 __device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __restrict__ G, int levels, int64_t plane,
                                          int64_t idx) {
 #pragma unroll
   for (int i = 0; i < NW; ++i) N[i] = 0;
   const int T = levels - 1;
-  for (int t = T; t >= 0; --t) {
-    const int64_t g = static_cast<int64_t>(G[static_cast<int64_t>(t) * plane + idx]);  // exact: |G_t| < 2^53
-    if (g != 0) add_shifted_signed<NW>(N, g, kSliceBits * (T - t));
+  int64_t carry = 0;
+  for (int t0 = T; t0 >= 0; t0 -= 8) {
+    // unconditional loads (levels below 0 re-read level 0 and are discarded),
+    // so that the eight loads go out back to back
+    double g[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int t = t0 - u;
+      g[u] = G[static_cast<int64_t>(t >= 0 ? t : 0) * plane + idx];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int t = t0 - u;
+      if (t < 0) break;
+      const int64_t v = static_cast<int64_t>(g[u]) + carry;  // exact: |G_t| < 2^53
+      const uint64_t d = static_cast<uint64_t>(v) & kDigitMax;
+      carry = v >> kSliceBits;  // arithmetic shift: floor division
+      const int pos = kSliceBits * (T - t), w = pos >> 6, b = pos & 63;
+      const uint64_t lo = d << b, hi = b > 64 - kSliceBits ? d >> (64 - b) : 0ull;
+#pragma unroll
+      for (int i = 0; i < NW; ++i) N[i] |= (i == w) ? lo : ((i == w + 1) ? hi : 0ull);
+    }
   }
+  if (carry != 0) add_shifted_signed<NW>(N, carry, kSliceBits * (T + 1));
 }
 
 // Bit `pos` (0 <= pos < 64 NW) of v.

@@ -74,20 +74,21 @@ __device__ inline uint32_t field13(const uint64_t (&v)[NW], int pos) {
   return static_cast<uint32_t>(f) & kDigitMax;
 }
 
-// D = floor(|V| / u) for one element (L limbs at stride ls, grid unit 2^g) as an
-// NW-word integer; returns true when V < 0.
+// D = floor(|V| / u) for one element with limbs xs[0..L-1] on the grid unit
+// 2^g, as an NW-word integer; returns true when V < 0.
 template <int NW>
-__device__ inline bool floor_on_grid(const double* __restrict__ x, int64_t ls, int L, int g, uint64_t (&I)[NW]) {
-  const double x0 = x[0];
+__device__ inline bool floor_on_grid(const double (&xs)[kMaxLimbs], int L, int g, uint64_t (&I)[NW]) {
+  const double x0 = xs[0];
   const bool neg = x0 < 0.0;
   uint64_t acc[NW];
 #pragma unroll
   for (int i = 0; i < NW; ++i) acc[i] = 0;
   int tail = 0;  // +1 / -1: sign, relative to V, of the part of V below u that is not in acc
   if (x0 != 0.0) {
-    for (int l = 0; l < L; ++l) {
-      const double xl = x[static_cast<int64_t>(l) * ls];
-      if (xl == 0.0) break;  // normalized: every later limb is zero too
+#pragma unroll
+    for (int l = 0; l < kMaxLimbs; ++l) {
+      const double xl = xs[l];
+      if (l >= L || xl == 0.0) break;  // normalized: every later limb is zero too
       const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(xl));
       const bool lneg = (bits >> 63) != 0;
       const uint64_t mag = bits & 0x7fffffffffffffffull;
@@ -126,6 +127,14 @@ __device__ inline bool floor_on_grid(const double* __restrict__ x, int64_t ls, i
   return neg;
 }
 
+// The L limbs of the element at idx (limb stride ls), all loads issued together;
+// limbs beyond L are +0.0 (L is the same for every thread).
+__device__ inline void load_limbs(const double* __restrict__ X, int64_t ls, int L, int64_t idx,
+                                  double (&xs)[kMaxLimbs]) {
+#pragma unroll
+  for (int l = 0; l < kMaxLimbs; ++l) xs[l] = l < L ? X[static_cast<int64_t>(l) * ls + idx] : 0.0;
+}
+
 __device__ inline double signed_digit(uint32_t d, bool neg) {
   const double v = static_cast<double>(d);
   return (d == 0u) ? 0.0 : (neg ? -v : v);  // zero digits are +0.0
@@ -142,8 +151,10 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
   for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
     const int64_t idx = r * cols + c;
     const int e = axis == 0 ? E[r] : E[c];
+    double xs[kMaxLimbs];
+    load_limbs(X, plane, L, idx, xs);
     uint64_t I[NW];
-    const bool neg = floor_on_grid<NW>(X + idx, plane, L, e - kSliceBits * S, I);
+    const bool neg = floor_on_grid<NW>(xs, L, e - kSliceBits * S, I);
     for (int s = 0; s < S; ++s)
       D[static_cast<int64_t>(s) * plane + idx] = signed_digit(field13<NW>(I, kSliceBits * (S - 1 - s)), neg);
   }
@@ -163,16 +174,27 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
   const int64_t K = axis == 0 ? cols : rows;   // reduction length
   const int64_t Cn = axis == 0 ? rows : cols;  // lines (rows of A or columns of B)
   const int64_t c = static_cast<int64_t>(blockIdx.x) * 64 + (threadIdx.x & 63);
+  if (c >= cp) return;
+  const int64_t cc = c < Cn ? c : 0;  // clamped line for the unconditional loads
+  const int e = E[cc];
   for (int64_t kb = blockIdx.y; kb * 16 < kp; kb += gridDim.y) {
+    // the limbs of this thread's four elements are loaded before any is split
+    double xs[4][kMaxLimbs];
+    bool valid[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int64_t kk = kb * 16 + (threadIdx.x >> 6) + 4 * r;
-      if (c >= cp) continue;
+      valid[r] = c < Cn && kk < K;
+      const int64_t kc = kk < K ? kk : 0;
+      load_limbs(X, plane, L, axis == 0 ? cc * cols + kc : kc * cols + cc, xs[r]);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t kk = kb * 16 + (threadIdx.x >> 6) + 4 * r;
       double* out = D + kk * cp + c;
-      if (c < Cn && kk < K) {
-        const int64_t idx = axis == 0 ? c * cols + kk : kk * cols + c;
+      if (valid[r]) {
         uint64_t I[NW];
-        const bool neg = floor_on_grid<NW>(X + idx, plane, L, E[c] - kSliceBits * S, I);
+        const bool neg = floor_on_grid<NW>(xs[r], L, e - kSliceBits * S, I);
         for (int s = 0; s < S; ++s)
           out[static_cast<int64_t>(s) * pplane] = signed_digit(field13<NW>(I, kSliceBits * (S - 1 - s)), neg);
       } else {

@@ -162,7 +162,9 @@ def test_split_golden_cases():
 
 @pytest.mark.parametrize("S,T,m,k,n", [(8, 7, 65, 37, 129), (8, 14, 130, 50, 131), (4, 3, 1, 1, 1),
                                        (12, 11, 200, 33, 70), (16, 15, 64, 16, 64), (16, 30, 33, 20, 17),
-                                       (3, 2, 257, 129, 300), (8, 7, 16, 1, 16)])
+                                       (3, 2, 257, 129, 300), (8, 7, 16, 1, 16),
+                                       # tile grids with partial tile-row groups and uneven XCD chunks
+                                       (8, 7, 1100, 40, 900), (4, 3, 3000, 17, 130), (2, 2, 130, 33, 2900)])
 def test_levels(S, T, m, k, n):
     print(f"[case] levels S={S} T={T} {m}x{k}x{n}", flush=True)
     rng = np.random.default_rng(S * 1000 + m)
