@@ -383,3 +383,43 @@ def test_mdgemm_check_finite():
     A[1, 2, 3] = 0.0
     C = md.mdgemm_ex(_gpu(A), _gpu(B), flags=md.MDGEMM_CHECK_FINITE | md.MDGEMM_SYNC)
     assert np.array_equal(C.cpu().numpy(), pipeline.full_reference(A, B, 8, 7)["C"])
+
+
+def test_mdgemm_library_workspace_grows():
+    print("[case] mdgemm library workspace: small then larger product", flush=True)
+    md.mdgemm_release()
+    for (m, k, n, seed) in [(20, 16, 12, 21), (150, 70, 140, 22), (40, 33, 30, 23)]:
+        A, B = _operands(2, m, k, n, seed)
+        C = _host(md.mdgemm(_gpu(A), _gpu(B)))
+        assert np.array_equal(C, pipeline.full_reference(A, B, 8, 7)["C"]), (m, k, n)
+    md.mdgemm_release()
+
+
+def test_mdgemm_graph_capture_replays():
+    # The product uses no memsets, no events (without MDGEMM_TIME_STAGES) and no
+    # synchronization (without CHECK_FINITE / SYNC), so it can be captured into a
+    # HIP graph; every replay must equal the eager result.
+    print("[case] mdgemm captured in a HIP graph", flush=True)
+    A, B = _operands(3, 130, 48, 140, 24, base="normal", row_exp=5, col_exp=5)
+    Ag, Bg = _gpu(A), _gpu(B)
+    ws = torch.empty(md.mdgemm_workspace_bytes(130, 140, 48, 3), dtype=torch.uint8, device=DEV)
+    eager = md.mdgemm_ex(Ag, Bg, workspace=ws)
+    torch.cuda.synchronize()
+    want = eager.cpu().numpy()
+    assert np.array_equal(want, pipeline.full_reference(A, B, 12, 11)["C"])
+    C = torch.empty_like(eager)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        md.mdgemm_ex(Ag, Bg, C, workspace=ws)  # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        md.mdgemm_ex(Ag, Bg, C, workspace=ws)
+    for r in range(4):
+        C.fill_(7.0)
+        md.mdgemm_ex(Ag, Bg, workspace=ws)  # eager work between replays
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(C.cpu().numpy(), want), r

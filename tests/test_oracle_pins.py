@@ -425,7 +425,7 @@ def test_classic_gemm_row_range_and_threads():
 
 
 # --------------------------------------------------------------------------
-# the sliced chain against the exact product (spec tolerance)
+# the sliced chain against the exact product (the componentwise tolerance)
 # --------------------------------------------------------------------------
 
 @pytest.mark.parametrize("L,S,T", [(1, 4, 3), (2, 8, 14), (2, 8, 7), (3, 12, 11), (4, 16, 15)])
