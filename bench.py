@@ -71,9 +71,9 @@ def cpu_baseline(w, A, B, target_s: float):
     from oracle import coracle
 
     coracle.lib()
-    # calibrate on a few rows per thread, then size the sample to about target_s seconds
+    # calibrate on one row per thread, then size the sample to about target_s seconds
     threads = coracle.num_threads()
-    rows = min(w.m, 4 * threads)
+    rows = min(w.m, threads)
     t = time.perf_counter()
     coracle.classic_gemm(A[:, :rows, :], B)
     dt = max(time.perf_counter() - t, 1e-3)
@@ -98,7 +98,7 @@ def main(argv=None) -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default=DEFAULT_CONFIG, help="workload c0..c4 (default c2)")
+    ap.add_argument("--config", default=DEFAULT_CONFIG, help="workload c0..c6 (default c2)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,

@@ -33,6 +33,7 @@
  *  - Output limbs whose magnitude falls below 2^-1022 (subnormal) are rounded by
  *    the final power-of-two scaling and are then no longer the exact greedy
  *    rounding; the products this library is built for stay far from that range.
+ *    Zero limbs, including limbs that underflow to zero, are +0.0.
  */
 #ifndef MDGEMM_H
 #define MDGEMM_H
@@ -54,10 +55,11 @@ extern "C" {
 #define MDGEMM_ENONFINITE -6  /* MDGEMM_CHECK_FINITE: an input limb is inf or nan */
 
 /* ---- limits ---------------------------------------------------------------- */
-#define MDGEMM_MAX_LIMBS 4    /* double, double-double, triple-double, quad-double */
-#define MDGEMM_MAX_SLICES 16  /* digits per element */
+#define MDGEMM_MAX_LIMBS 16   /* double (1), double-double (2), ... quad (4), octo (8), hexa double (16) */
+#define MDGEMM_MAX_SLICES 64  /* digits per element */
+#define MDGEMM_MAX_LEVELS 127 /* 2 * MDGEMM_MAX_SLICES - 1 */
 #define MDGEMM_SLICE_BITS 13
-#define MDGEMM_Z_WORDS 8      /* 64-bit words per element written by mdgemm_accumulate */
+#define MDGEMM_Z_WORDS 28     /* 64-bit words per element written by mdgemm_accumulate */
 
 /* ---- flags for mdgemm_opts.flags ------------------------------------------- */
 #define MDGEMM_CHECK_FINITE 1u /* scan A and B for inf/nan first; synchronizes the stream */
@@ -72,7 +74,7 @@ typedef struct mdgemm_opts {
   void* stream;           /* hipStream_t to launch on; NULL = default stream */
   void* workspace;        /* caller-owned device buffer; NULL = library-owned cache */
   size_t workspace_bytes; /* size of `workspace` in bytes */
-  int slices_per_limb;    /* digits per limb, S = limbs * slices_per_limb <= 16; 0 = 4 */
+  int slices_per_limb;    /* digits per limb, S = limbs * slices_per_limb <= 64; 0 = 4 */
   int cutoff;             /* largest kept p + q; MDGEMM_CUTOFF_DEFAULT or _ALL or 0..2S-2 */
   unsigned flags;         /* MDGEMM_CHECK_FINITE | MDGEMM_SYNC | MDGEMM_TIME_STAGES */
 } mdgemm_opts;
@@ -81,7 +83,7 @@ typedef struct mdgemm_opts {
  * limb, cutoff T = S - 1, no flags. */
 void mdgemm_opts_init(mdgemm_opts* opts);
 
-/* C = A.B for L-limb operands (L = limbs in 1..4) with the default options.
+/* C = A.B for L-limb operands (L = limbs in 1..16) with the default options.
  * m, n, k >= 0; m == 0 or n == 0 does nothing; k == 0 writes C = +0.0.
  * Returns MDGEMM_OK or a negative status. */
 int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C);
@@ -130,7 +132,7 @@ int mdgemm_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int
  * digit s = sign(V) * bits 13(S-1-s) .. 13(S-s)-1 of D_abs, so that
  * V = sum_s digit_s 2^(E - 13(s+1)) + R with |R| < 2^(E - 13 S) and R V >= 0.
  * Zero digits are +0.0.  Requires |V| < 2^E (true for normalized input and the
- * exponents of mdgemm_exponents).  limbs 1..4, slices 1..16. */
+ * exponents of mdgemm_exponents).  limbs 1..16, slices 1..64. */
 int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int axis, const double* X, const int32_t* E,
                  double* D, void* stream);
 
@@ -151,17 +153,18 @@ int mdgemm_split_panel(int64_t rows, int64_t cols, int limbs, int slices, int ax
  * both pointers 16-byte aligned.
  * per_pair == 0: out [T+1][m][n], out[t] = sum over p + q = t (0 <= p, q < S) of
  * DA_p . DB_q for t = 0..cutoff.  per_pair != 0: out [S][S][m][n],
- * out[p][q] = DA_p . DB_q for every p + q <= cutoff (other planes untouched).
+ * out[p][q] = DA_p . DB_q for every p + q <= cutoff (other planes untouched; one
+ * launch per 256 pairs).
  * Exact in FP64 (any summation order) because every partial sum is an integer
  * below 2^53; returns MDGEMM_EEXACT when pairs_t * k * 8191^2 >= 2^53.
- * S in 1..16, cutoff in 0..2S-2. */
+ * S in 1..64, cutoff in 0..2S-2. */
 int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, int per_pair, const double* DAt,
                       const double* DBp, double* out, void* stream);
 
 /* Step a4 alone, the exact accumulation (section 2, steps 4-5), exported for
- * checking.  G [levels][m][n] integer-valued with |G| < 2^53, levels 1..31.
+ * checking.  G [levels][m][n] integer-valued with |G| < 2^53, levels 1..127.
  * Writes the integer N = sum_t G_t 2^(13 (levels-1-t)) as MDGEMM_Z_WORDS 64-bit
- * two's-complement words, least significant first: Z [8][m][n] int64.  The
+ * two's-complement words, least significant first: Z [MDGEMM_Z_WORDS][m][n] int64.  The
  * accumulated value is N 2^(-13 (levels-1)) (before the grid scale). */
 int mdgemm_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, void* stream);
 
@@ -170,7 +173,8 @@ int mdgemm_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t
  * into a multiple double), times the grid scale 2^(EA[i] + EB[j] - 26):
  * with Z = sum_t G_t 2^(-13 t), C[.][i][j] = (c_0, .., c_{L-1}) 2^(EA[i]+EB[j]-26)
  * where c_0 = RN(Z) and c_l = RN(Z - c_0 - .. - c_{l-1}) (round to nearest, ties
- * to even).  G [levels][m][n], EA int32[m], EB int32[n], C [limbs][m][n]. */
+ * to even).  G [levels][m][n] (levels 1..127), EA int32[m], EB int32[n],
+ * C [limbs][m][n] (limbs 1..16). */
 int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, const double* G, const int32_t* EA,
                         const int32_t* EB, double* C, void* stream);
 

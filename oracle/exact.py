@@ -180,6 +180,38 @@ def tolerance(k: int, L: int, mag: Fraction) -> Fraction:
     return 4 * k * Fraction(2) ** (-(53 * L - 4)) * mag
 
 
+def method_bound(A: np.ndarray, B: np.ndarray, i: int, j: int, S: int, T: int, EA: int, EB: int) -> Fraction:
+    """Bound on |C[i][j] - C_exact[i][j]| of the sliced product with S digits per
+    element and the pairs p + q <= T, from the parts of section 2:
+
+    * truncation: a = alpha + r_a with |r_a| < 2^(EA - 13 S) and |alpha| <= |a|
+      (the digits are the truncated quarters), likewise b, so
+      |a b - alpha beta| <= |a| 2^(EB - 13 S) + |b| 2^(EA - 13 S) + 2^(EA + EB - 26 S);
+    * dropped pairs: a product of digits is below 2^26 and the pair (p, q) weighs
+      2^(EA + EB - 13 (p + q + 2)), so level t > T adds at most
+      pairs_t 2^26 2^(EA + EB - 13 (t + 2)) per term of the inner product;
+    * the final rounding into L limbs, greedy round to nearest: at most
+      2^(-53 L) (1 + 2^-53) |Z| with |Z| <= |C_exact| + the two terms above.
+
+    With S = 4 L this is about 2^(5 - 13 S) k 2^(EA + EB) relative, which for
+    L >= 5 is looser than 4 k 2^-(53 L - 4) (|A||B|): four 13-bit digits carry 52
+    of the 53 bits of every limb."""
+    k = A.shape[2]
+    two = Fraction(2)
+    L = A.shape[0]
+    trunc = Fraction(0)
+    mag = Fraction(0)
+    for kk in range(k):
+        a, b = abs(value(A[:, i, kk])), abs(value(B[:, kk, j]))
+        mag += a * b
+        trunc += a * two ** (EB - 13 * S) + b * two ** (EA - 13 * S) + two ** (EA + EB - 26 * S)
+    dropped = Fraction(0)
+    for t in range(T + 1, 2 * S - 1):
+        dropped += len(pairs_of_level(t, S)) * two ** (26 + EA + EB - 13 * (t + 2))
+    dropped *= k
+    return trunc + dropped + 2 * two ** (-53 * L) * (mag + trunc + dropped)
+
+
 def is_nonoverlapping(limbs) -> bool:
     """|x_{l+1}| <= ulp(x_l)/2 and a zero limb is followed only by zeros."""
     for a, b in zip(limbs[:-1], limbs[1:]):

@@ -109,7 +109,9 @@ static inline void dd_mul(const double* a, const double* b, double* r) {
 /* 2b. Any limb count: exact expansions (Shewchuk 1997) rounded to L limbs    */
 /* ------------------------------------------------------------------------- */
 
-#define MAXTERMS 128
+#define MAXLIMBS 16
+/* terms of one multiply-add: L + L(L+1) + L - 1 = 303 for L = 16 */
+#define MAXTERMS 320
 
 /* Grow-Expansion with zero elimination: h = e + b exactly.  e holds elen
  * nonoverlapping components in increasing magnitude; so does h. */
@@ -193,7 +195,8 @@ static void md_fma(int L, double* acc, const double* a, const double* b) {
 
 /* Per-operation entry points, vectorized over n elements (limb-major [L][n]). */
 void oracle_md_fma(int L, int64_t n, const double* acc, const double* a, const double* b, double* out) {
-  double x[8], y[8], z[8];
+  double x[MAXLIMBS], y[MAXLIMBS], z[MAXLIMBS];
+  if (L < 1 || L > MAXLIMBS) return;
   for (int64_t e = 0; e < n; ++e) {
     for (int l = 0; l < L; ++l) {
       z[l] = acc[l * n + e];
@@ -226,14 +229,13 @@ void oracle_dd_mul(int64_t n, const double* a, const double* b, double* out) {
 /* Classic GEMM: C[i][j] = sum over kk of A[i][kk] * B[kk][j], each inner product
  * accumulated sequentially in kk in L-limb arithmetic, one element at a time.
  * variant 0: double-double add and multiply (L must be 2), rounded twice per step;
- * variant 1: exact multiply-add rounded once per step (any L in 1..6).
+ * variant 1: exact multiply-add rounded once per step (any L in 1..16).
  * Rows [row_begin, row_end) are computed; nthreads <= 0 uses the OpenMP default.
  * Returns the number of threads used, or a negative status. */
 int oracle_classic_gemm(int64_t m, int64_t n, int64_t k, int L, const double* A, const double* B, double* C,
                         int64_t row_begin, int64_t row_end, int variant, int nthreads) {
-  if (L < 1 || L > 8 || m < 0 || n < 0 || k < 0) return ORACLE_EINVAL;
+  if (L < 1 || L > MAXLIMBS || m < 0 || n < 0 || k < 0) return ORACLE_EINVAL;
   if (variant == 0 && L != 2) return ORACLE_EINVAL;
-  if (variant == 1 && L > 6) return ORACLE_EINVAL; /* terms: L + L(L+1) + L - 1 <= MAXTERMS */
   if (row_begin < 0) row_begin = 0;
   if (row_end > m || row_end < 0) row_end = m;
   /* B transposed once so that every inner product reads contiguous limbs. */
@@ -258,7 +260,7 @@ int oracle_classic_gemm(int64_t m, int64_t n, int64_t k, int L, const double* A,
       for (int64_t kk = 0; kk < k; ++kk)
         for (int l = 0; l < L; ++l) a[kk * L + l] = A[(int64_t)l * m * k + i * k + kk];
       for (int64_t j = 0; j < n; ++j) {
-        double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        double acc[MAXLIMBS] = {0};
         const double* bj = Bt + j * k * L;
         if (variant == 0) {
           for (int64_t kk = 0; kk < k; ++kk) {

@@ -19,6 +19,8 @@
 //
 // One thread per output element; consecutive threads take consecutive columns,
 // so the T + 1 level loads and the L limb stores are contiguous 512-byte rows.
+#include <type_traits>
+
 #include "internal.h"
 
 namespace mdg {
@@ -163,7 +165,8 @@ __device__ inline void round_limbs(uint64_t (&N)[NW], int L, int scale, double* 
         neg = !neg;
       }
     }
-    C[static_cast<int64_t>(l) * plane + idx] = c;
+    // a limb that underflows in the final scaling is +0.0, like every zero limb
+    C[static_cast<int64_t>(l) * plane + idx] = c == 0.0 ? 0.0 : c;
   }
 }
 
@@ -210,39 +213,48 @@ inline dim3 elem_grid(int64_t m, int64_t n) {
   return dim3(static_cast<unsigned>((n + 255) / 256), static_cast<unsigned>(m < 65535 ? m : 65535));
 }
 
+template <int NW>
+using Words = std::integral_constant<int, NW>;
+
+// Calls f(Words<NW>{}) for the smallest instantiated NW >= words (levels up to
+// 2 * 64 - 1 need 27 words).
+template <class F>
+hipError_t with_words(int words, F&& f) {
+  if (words <= 2) f(Words<2>{});
+  else if (words <= 3) f(Words<3>{});
+  else if (words <= 4) f(Words<4>{});
+  else if (words <= 5) f(Words<5>{});
+  else if (words <= 6) f(Words<6>{});
+  else if (words <= 7) f(Words<7>{});
+  else if (words <= 8) f(Words<8>{});
+  else if (words <= 10) f(Words<10>{});
+  else if (words <= 12) f(Words<12>{});
+  else if (words <= 14) f(Words<14>{});
+  else if (words <= 20) f(Words<20>{});
+  else if (words <= kZWords) f(Words<kZWords>{});
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_accum_renorm(int64_t m, int64_t n, int L, int levels, const double* G, const int32_t* EA,
                                const int32_t* EB, double* C, hipStream_t stream) {
   if (m == 0 || n == 0) return hipSuccess;
   const dim3 grid = elem_grid(m, n);
-  switch (words_for_levels(levels)) {
-    case 1:
-    case 2: hipLaunchKernelGGL(accum_renorm_kernel<2>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
-    case 3: hipLaunchKernelGGL(accum_renorm_kernel<3>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
-    case 4: hipLaunchKernelGGL(accum_renorm_kernel<4>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
-    case 5: hipLaunchKernelGGL(accum_renorm_kernel<5>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
-    case 6: hipLaunchKernelGGL(accum_renorm_kernel<6>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
-    case 7: hipLaunchKernelGGL(accum_renorm_kernel<7>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA, EB, C); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+  // the next word count instantiated (the extra words hold the sign extension)
+  return with_words(words_for_levels(levels), [&](auto nw) {
+    hipLaunchKernelGGL(accum_renorm_kernel<decltype(nw)::value>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA,
+                       EB, C);
+  });
 }
 
 hipError_t launch_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, hipStream_t stream) {
   if (m == 0 || n == 0) return hipSuccess;
   const dim3 grid = elem_grid(m, n);
-  switch (words_for_levels(levels)) {
-    case 1:
-    case 2: hipLaunchKernelGGL(accumulate_kernel<2>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
-    case 3: hipLaunchKernelGGL(accumulate_kernel<3>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
-    case 4: hipLaunchKernelGGL(accumulate_kernel<4>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
-    case 5: hipLaunchKernelGGL(accumulate_kernel<5>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
-    case 6: hipLaunchKernelGGL(accumulate_kernel<6>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
-    case 7: hipLaunchKernelGGL(accumulate_kernel<7>, grid, dim3(256), 0, stream, m, n, levels, G, Z); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+  return with_words(words_for_levels(levels), [&](auto nw) {
+    hipLaunchKernelGGL(accumulate_kernel<decltype(nw)::value>, grid, dim3(256), 0, stream, m, n, levels, G, Z);
+  });
 }
 
 }  // namespace mdg

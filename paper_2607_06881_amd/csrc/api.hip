@@ -19,6 +19,11 @@
 #include "internal.h"
 #include "mdgemm.h"
 
+static_assert(MDGEMM_MAX_LIMBS == mdg::kMaxLimbs && MDGEMM_MAX_SLICES == mdg::kMaxSlices &&
+                  MDGEMM_Z_WORDS == mdg::kZWords && MDGEMM_SLICE_BITS == mdg::kSliceBits &&
+                  MDGEMM_MAX_LEVELS == mdg::kMaxLevels,
+              "the limits of include/mdgemm.h and csrc/internal.h must agree");
+
 namespace {
 
 using mdg::JobTable;
@@ -66,30 +71,33 @@ JobTable level_jobs(int S, int T) {
   for (int j = 0; j < jt.njobs; ++j) {
     int t = order[j];
     int lo = t - (S - 1) > 0 ? t - (S - 1) : 0;
-    jt.p_first[j] = static_cast<uint8_t>(lo);
-    jt.q_first[j] = static_cast<uint8_t>(t - lo);
-    jt.npairs[j] = static_cast<uint8_t>(npairs(t));
-    jt.out[j] = static_cast<uint8_t>(t);
+    jt.p_first[j] = static_cast<uint16_t>(lo);
+    jt.q_first[j] = static_cast<uint16_t>(t - lo);
+    jt.npairs[j] = static_cast<uint16_t>(npairs(t));
+    jt.out[j] = static_cast<uint16_t>(t);
   }
   return jt;
 }
 
-// Every pair (p, q) with p + q <= T, written to plane p*S + q.
-JobTable pair_jobs(int S, int T) {
-  JobTable jt;
-  std::memset(&jt, 0, sizeof jt);
-  int j = 0;
+// Every pair (p, q) with p + q <= T, written to plane p*S + q; one table per
+// launch of at most kMaxJobs pairs.
+std::vector<JobTable> pair_jobs(int S, int T) {
+  std::vector<JobTable> tables;
   for (int p = 0; p < S; ++p)
     for (int q = 0; q < S; ++q) {
       if (p + q > T) continue;
-      jt.p_first[j] = static_cast<uint8_t>(p);
-      jt.q_first[j] = static_cast<uint8_t>(q);
+      if (tables.empty() || tables.back().njobs == mdg::kMaxJobs) {
+        tables.emplace_back();
+        std::memset(&tables.back(), 0, sizeof(JobTable));
+      }
+      JobTable& jt = tables.back();
+      const int j = jt.njobs++;
+      jt.p_first[j] = static_cast<uint16_t>(p);
+      jt.q_first[j] = static_cast<uint16_t>(q);
       jt.npairs[j] = 1;
-      jt.out[j] = static_cast<uint8_t>(p * S + q);
-      ++j;
+      jt.out[j] = static_cast<uint16_t>(p * S + q);
     }
-  jt.njobs = j;
-  return jt;
+  return tables;
 }
 
 // ---- options ----------------------------------------------------------------
@@ -422,12 +430,15 @@ int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, i
                 overlaps(out, obytes, DBp, sizeof(double) * slices * kp * static_cast<size_t>(mdg::panel_mn(n)))))
     return MDGEMM_EINVAL;
   if (!exact_ok(k, per_pair ? 1 : max_pairs(slices, cutoff))) return MDGEMM_EEXACT;
-  const JobTable jt = per_pair ? pair_jobs(slices, cutoff) : level_jobs(slices, cutoff);
-  return hip_status(mdg::launch_slice_gemm(m, n, k, DAt, DBp, out, jt, static_cast<hipStream_t>(stream)));
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!per_pair) return hip_status(mdg::launch_slice_gemm(m, n, k, DAt, DBp, out, level_jobs(slices, cutoff), s));
+  for (const JobTable& jt : pair_jobs(slices, cutoff))
+    MDG_TRY(hip_status(mdg::launch_slice_gemm(m, n, k, DAt, DBp, out, jt, s)));
+  return MDGEMM_OK;
 }
 
 int mdgemm_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, void* stream) {
-  if (m < 0 || n < 0 || levels < 1 || levels > 31) return MDGEMM_EINVAL;
+  if (m < 0 || n < 0 || levels < 1 || levels > mdg::kMaxLevels) return MDGEMM_EINVAL;
   if (m == 0 || n == 0) return MDGEMM_OK;
   if (!G || !Z) return MDGEMM_EINVAL;
   return hip_status(mdg::launch_accumulate(m, n, levels, G, Z, static_cast<hipStream_t>(stream)));
@@ -435,7 +446,8 @@ int mdgemm_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t
 
 int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, const double* G, const int32_t* EA,
                         const int32_t* EB, double* C, void* stream) {
-  if (m < 0 || n < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || levels < 1 || levels > 31) return MDGEMM_EINVAL;
+  if (m < 0 || n < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || levels < 1 || levels > mdg::kMaxLevels)
+    return MDGEMM_EINVAL;
   if (m == 0 || n == 0) return MDGEMM_OK;
   if (!G || !EA || !EB || !C) return MDGEMM_EINVAL;
   const size_t cbytes = sizeof(double) * limbs * static_cast<size_t>(m) * static_cast<size_t>(n);

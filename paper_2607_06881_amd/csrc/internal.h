@@ -9,9 +9,11 @@ namespace mdg {
 
 constexpr int kSliceBits = 13;
 constexpr int kDigitMax = (1 << kSliceBits) - 1;  // 8191
-constexpr int kMaxSlices = 16;
-constexpr int kMaxLimbs = 4;
-constexpr int kZWords = 8;
+constexpr int kMaxSlices = 64;  // 4 digits per limb of a hexa double
+constexpr int kMaxLimbs = 16;   // hexa double
+constexpr int kMaxLevels = 2 * kMaxSlices - 1;
+constexpr int kZWords = 28;     // 64-bit words of an exact level sum (13 (kMaxLevels - 1) + 55 bits)
+constexpr int kMaxJobs = 256;   // jobs of one level-GEMM launch (grid.y)
 constexpr int kTileMN = 128;  // level-GEMM tile rows / columns
 constexpr int kTileK = 16;    // level-GEMM k step
 
@@ -24,10 +26,10 @@ inline int64_t panel_mn(int64_t x) { return (x + kTileMN - 1) / kTileMN * kTileM
 // (p_first + i, q_first - i) for i < npairs into output plane out[j].
 struct JobTable {
   int njobs;
-  uint8_t p_first[256];
-  uint8_t q_first[256];
-  uint8_t npairs[256];
-  uint8_t out[256];
+  uint16_t p_first[kMaxJobs];
+  uint16_t q_first[kMaxJobs];
+  uint16_t npairs[kMaxJobs];
+  uint16_t out[kMaxJobs];
 };
 
 // a1: per-row (axis 0) or per-column (axis 1) grid exponents of a [rows][cols] plane.
@@ -45,7 +47,7 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int axis, cons
 hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DAt, const double* DBp, double* out,
                              const JobTable& jobs, hipStream_t stream);
 
-// a4: exact accumulation of `levels` planes into 8-word integers Z [8][m][n].
+// a4: exact accumulation of `levels` planes into kZWords-word integers Z [kZWords][m][n].
 hipError_t launch_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, hipStream_t stream);
 
 // a4 + a5: exact accumulation and greedy rounding into L limbs, scaled by 2^(EA+EB-26).

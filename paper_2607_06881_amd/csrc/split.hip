@@ -74,10 +74,10 @@ __device__ inline uint32_t field13(const uint64_t (&v)[NW], int pos) {
   return static_cast<uint32_t>(f) & kDigitMax;
 }
 
-// D = floor(|V| / u) for one element with limbs xs[0..L-1] on the grid unit
-// 2^g, as an NW-word integer; returns true when V < 0.
-template <int NW>
-__device__ inline bool floor_on_grid(const double (&xs)[kMaxLimbs], int L, int g, uint64_t (&I)[NW]) {
+// D = floor(|V| / u) for one element with limbs xs[0..L-1] (L <= ML) on the
+// grid unit 2^g, as an NW-word integer; returns true when V < 0.
+template <int NW, int ML>
+__device__ inline bool floor_on_grid(const double (&xs)[ML], int L, int g, uint64_t (&I)[NW]) {
   const double x0 = xs[0];
   const bool neg = x0 < 0.0;
   uint64_t acc[NW];
@@ -86,7 +86,7 @@ __device__ inline bool floor_on_grid(const double (&xs)[kMaxLimbs], int L, int g
   int tail = 0;  // +1 / -1: sign, relative to V, of the part of V below u that is not in acc
   if (x0 != 0.0) {
 #pragma unroll
-    for (int l = 0; l < kMaxLimbs; ++l) {
+    for (int l = 0; l < ML; ++l) {
       const double xl = xs[l];
       if (l >= L || xl == 0.0) break;  // normalized: every later limb is zero too
       const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(xl));
@@ -129,10 +129,10 @@ __device__ inline bool floor_on_grid(const double (&xs)[kMaxLimbs], int L, int g
 
 // The L limbs of the element at idx (limb stride ls), all loads issued together;
 // limbs beyond L are +0.0 (L is the same for every thread).
-__device__ inline void load_limbs(const double* __restrict__ X, int64_t ls, int L, int64_t idx,
-                                  double (&xs)[kMaxLimbs]) {
+template <int ML>
+__device__ inline void load_limbs(const double* __restrict__ X, int64_t ls, int L, int64_t idx, double (&xs)[ML]) {
 #pragma unroll
-  for (int l = 0; l < kMaxLimbs; ++l) xs[l] = l < L ? X[static_cast<int64_t>(l) * ls + idx] : 0.0;
+  for (int l = 0; l < ML; ++l) xs[l] = l < L ? X[static_cast<int64_t>(l) * ls + idx] : 0.0;
 }
 
 __device__ inline double signed_digit(uint32_t d, bool neg) {
@@ -141,7 +141,7 @@ __device__ inline double signed_digit(uint32_t d, bool neg) {
 }
 
 // Row-major output: D [S][rows][cols], the layout of the input planes.
-template <int NW>
+template <int NW, int ML>
 __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, int L, int S, int axis,
                                                     const double* __restrict__ X, const int32_t* __restrict__ E,
                                                     double* __restrict__ D) {
@@ -151,10 +151,10 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
   for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
     const int64_t idx = r * cols + c;
     const int e = axis == 0 ? E[r] : E[c];
-    double xs[kMaxLimbs];
-    load_limbs(X, plane, L, idx, xs);
+    double xs[ML];
+    load_limbs<ML>(X, plane, L, idx, xs);
     uint64_t I[NW];
-    const bool neg = floor_on_grid<NW>(xs, L, e - kSliceBits * S, I);
+    const bool neg = floor_on_grid<NW, ML>(xs, L, e - kSliceBits * S, I);
     for (int s = 0; s < S; ++s)
       D[static_cast<int64_t>(s) * plane + idx] = signed_digit(field13<NW>(I, kSliceBits * (S - 1 - s)), neg);
   }
@@ -166,7 +166,7 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
 // with kp, mp, np rounded up to the GEMM tile (16 and 128) and zeros in the padding.
 // A block covers 64 lines (c) x 16 k: its reads of A touch 64 full 128-byte lines
 // and its stores are 512-byte rows of the panel.
-template <int NW>
+template <int NW, int ML>
 __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t cols, int L, int S, int axis,
                                                           int64_t kp, int64_t cp, const double* __restrict__ X,
                                                           const int32_t* __restrict__ E, double* __restrict__ D) {
@@ -177,40 +177,45 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
   if (c >= cp) return;
   const int64_t cc = c < Cn ? c : 0;  // clamped line for the unconditional loads
   const int e = E[cc];
+  // the limbs of kBatch of this thread's four elements are loaded before any of
+  // them is split (fewer at a time for long multiple doubles, to stay in registers)
+  constexpr int kBatch = ML <= 4 ? 4 : (ML <= 8 ? 2 : 1);
   for (int64_t kb = blockIdx.y; kb * 16 < kp; kb += gridDim.y) {
-    // the limbs of this thread's four elements are loaded before any is split
-    double xs[4][kMaxLimbs];
-    bool valid[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int64_t kk = kb * 16 + (threadIdx.x >> 6) + 4 * r;
-      valid[r] = c < Cn && kk < K;
-      const int64_t kc = kk < K ? kk : 0;
-      load_limbs(X, plane, L, axis == 0 ? cc * cols + kc : kc * cols + cc, xs[r]);
-    }
+    for (int r0 = 0; r0 < 4; r0 += kBatch) {
+      double xs[kBatch][ML];
+      bool valid[kBatch];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int64_t kk = kb * 16 + (threadIdx.x >> 6) + 4 * r;
-      double* out = D + kk * cp + c;
-      if (valid[r]) {
-        uint64_t I[NW];
-        const bool neg = floor_on_grid<NW>(xs[r], L, e - kSliceBits * S, I);
-        for (int s = 0; s < S; ++s)
-          out[static_cast<int64_t>(s) * pplane] = signed_digit(field13<NW>(I, kSliceBits * (S - 1 - s)), neg);
-      } else {
-        for (int s = 0; s < S; ++s) out[static_cast<int64_t>(s) * pplane] = 0.0;
+      for (int b = 0; b < kBatch; ++b) {
+        const int64_t kk = kb * 16 + (threadIdx.x >> 6) + 4 * (r0 + b);
+        valid[b] = c < Cn && kk < K;
+        const int64_t kc = kk < K ? kk : 0;
+        load_limbs<ML>(X, plane, L, axis == 0 ? cc * cols + kc : kc * cols + cc, xs[b]);
+      }
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b) {
+        const int64_t kk = kb * 16 + (threadIdx.x >> 6) + 4 * (r0 + b);
+        double* out = D + kk * cp + c;
+        if (valid[b]) {
+          uint64_t I[NW];
+          const bool neg = floor_on_grid<NW, ML>(xs[b], L, e - kSliceBits * S, I);
+          for (int s = 0; s < S; ++s)
+            out[static_cast<int64_t>(s) * pplane] = signed_digit(field13<NW>(I, kSliceBits * (S - 1 - s)), neg);
+        } else {
+          for (int s = 0; s < S; ++s) out[static_cast<int64_t>(s) * pplane] = 0.0;
+        }
       }
     }
   }
 }
 
-template <int NW>
+template <int NW, int ML>
 hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E, double* D,
                      bool panel, hipStream_t stream) {
   if (!panel) {
     const unsigned gx = static_cast<unsigned>((cols + 255) / 256);
     const unsigned gy = static_cast<unsigned>(rows < 65535 ? rows : 65535);
-    hipLaunchKernelGGL(split_kernel<NW>, dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, axis, X, E, D);
+    hipLaunchKernelGGL((split_kernel<NW, ML>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, axis, X, E, D);
     return hipGetLastError();
   }
   const int64_t K = axis == 0 ? cols : rows, Cn = axis == 0 ? rows : cols;
@@ -218,9 +223,24 @@ hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int axis, const d
   const unsigned gx = static_cast<unsigned>(cp / 64);
   const int64_t nkb = kp / 16;
   const unsigned gy = static_cast<unsigned>(nkb < 65535 ? nkb : 65535);
-  hipLaunchKernelGGL(split_panel_kernel<NW>, dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, axis, kp, cp, X,
+  hipLaunchKernelGGL((split_panel_kernel<NW, ML>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, axis, kp, cp, X,
                      E, D);
   return hipGetLastError();
+}
+
+// Word counts instantiated for S up to 64 digits (884 bits).
+template <int ML>
+hipError_t split_words(int words, int64_t rows, int64_t cols, int L, int S, int axis, const double* X,
+                       const int32_t* E, double* D, bool panel, hipStream_t stream) {
+  if (words <= 2) return launch_nw<2, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (words <= 3) return launch_nw<3, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (words <= 4) return launch_nw<4, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (words <= 5) return launch_nw<5, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (words <= 6) return launch_nw<6, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (words <= 8) return launch_nw<8, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (words <= 10) return launch_nw<10, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (words <= 14) return launch_nw<14, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
@@ -228,12 +248,12 @@ hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int axis, const d
 hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E,
                         double* D, bool panel, hipStream_t stream) {
   if (rows == 0 || cols == 0) return hipSuccess;
-  // The accumulator holds |V| / u < 2^(13 S) with 52 fraction bits: 13 S + 52 bits.
-  const int bits = kSliceBits * S + 52;
-  if (bits <= 128) return launch_nw<2>(rows, cols, L, S, axis, X, E, D, panel, stream);
-  if (bits <= 192) return launch_nw<3>(rows, cols, L, S, axis, X, E, D, panel, stream);
-  if (bits <= 256) return launch_nw<4>(rows, cols, L, S, axis, X, E, D, panel, stream);
-  return launch_nw<5>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  // The accumulator holds |V| / u < 2^(13 S) with 52 fraction bits: 13 S + 52 bits,
+  // in the next word count instantiated (extra words stay zero).
+  const int words = (kSliceBits * S + 52 + 63) / 64;
+  if (L <= 4) return split_words<4>(words, rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (L <= 8) return split_words<8>(words, rows, cols, L, S, axis, X, E, D, panel, stream);
+  return split_words<16>(words, rows, cols, L, S, axis, X, E, D, panel, stream);
 }
 
 }  // namespace mdg

@@ -32,7 +32,11 @@ MDGEMM_TIME_STAGES = 4
 
 MDGEMM_CUTOFF_DEFAULT = -1
 MDGEMM_CUTOFF_ALL = -2
-MDGEMM_Z_WORDS = 8
+MDGEMM_MAX_LIMBS = 16
+MDGEMM_MAX_SLICES = 64
+MDGEMM_MAX_LEVELS = 127
+MDGEMM_SLICE_BITS = 13
+MDGEMM_Z_WORDS = 28
 PANEL_K = 16  # level-GEMM panels: k rounded up to 16,
 PANEL_MN = 128  # m and n rounded up to 128
 
@@ -286,7 +290,8 @@ def mdgemm_slice_gemm(DAt: torch.Tensor, DBp: torch.Tensor, m: int, n: int, k: i
 
 
 def mdgemm_accumulate(G: torch.Tensor, Z: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """Exact sums N = sum_t G_t 2^(13 (T - t)) as 8 int64 words [8, m, n], least significant first."""
+    """Exact sums N = sum_t G_t 2^(13 (T - t)) as MDGEMM_Z_WORDS int64 words [MDGEMM_Z_WORDS, m, n],
+    least significant first."""
     _dev_tensor(G, torch.float64, "G")
     levels, m, n = G.shape
     if Z is None:

@@ -94,6 +94,16 @@ WORKLOADS = {
     "c4": Workload(
         "c4", 3, 8192, 8192, 512, 12, 11, 4, "normal", row_exp=30, col_exp=30,
         description="triple-double 8192x8192x512, N(0,1) times row/column scales 2^e, e ~ U{-30..30}, pairs p+q <= 11"),
+    # More limbs: the octo- and hexa-double shapes of the top-down method (section 4,
+    # the table of dimensions adapted for dd, qd, od and hd), A 256 x 128 (od) and
+    # 128 x 64 (hd), B with the 8192 columns of the rewritten second operand;
+    # the paper's four digits per limb.
+    "c5": Workload(
+        "c5", 8, 256, 8192, 128, 32, 31, 5, "normal",
+        description="octo-double 256x8192x128, limb 0 ~ N(0,1), pairs p+q <= 31"),
+    "c6": Workload(
+        "c6", 16, 128, 8192, 64, 64, 63, 6, "normal",
+        description="hexa-double 128x8192x64, limb 0 ~ N(0,1), pairs p+q <= 63"),
 }
 
 

@@ -67,21 +67,25 @@ def test_invalid_arguments(lib):
     assert _ex(lib, -1, 4, 4, 2) == E
     assert _ex(lib, 4, 4, -3, 2) == E
     assert _ex(lib, 4, 4, 4, 0) == E
-    assert _ex(lib, 4, 4, 4, 5) == E
-    assert _ex(lib, 4, 4, 4, 2, slices_per_limb=9) == E  # S = 18 > 16
+    assert _ex(lib, 4, 4, 4, md.MDGEMM_MAX_LIMBS + 1) == E
+    assert _ex(lib, 4, 4, 4, 2, slices_per_limb=33) == E  # S = 66 > 64
+    assert _ex(lib, 4, 4, 4, 16, slices_per_limb=5) == E  # S = 80 > 64
     assert _ex(lib, 4, 4, 4, 2, cutoff=15) == E  # > 2S - 2
     assert _ex(lib, 4, 4, 4, 2, cutoff=-3) == E
     assert _ex(lib, 4, 4, 4, 2, A=None) == E
     assert _ex(lib, 4, 4, 4, 2, C=None) == E
     # C overlapping A
     assert _ex(lib, 4, 4, 4, 2, C=FA + 8) == E
-    assert lib.mdgemm_split(4, 4, 2, 17, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_split(4, 4, 2, md.MDGEMM_MAX_SLICES + 1, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_split(4, 4, md.MDGEMM_MAX_LIMBS + 1, 8, 0, FA, FB, FC, None) == E
     assert lib.mdgemm_split(4, 4, 2, 8, 2, FA, FB, FC, None) == E
     assert lib.mdgemm_split_panel(4, 4, 2, 0, 0, FA, FB, FC, None) == E
     assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 7, 0, FA + 8, FB, FC, None) == E  # panels must be 16-byte aligned
     assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 15, 0, FA, FB, FC, None) == E
-    assert lib.mdgemm_accumulate(4, 4, 32, FA, FC, None) == E
-    assert lib.mdgemm_accum_renorm(4, 4, 5, 8, FA, FB, FB, FC, None) == E
+    assert lib.mdgemm_slice_gemm(4, 4, 4, md.MDGEMM_MAX_SLICES + 1, 7, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_accumulate(4, 4, md.MDGEMM_MAX_LEVELS + 1, FA, FC, None) == E
+    assert lib.mdgemm_accum_renorm(4, 4, md.MDGEMM_MAX_LIMBS + 1, 8, FA, FB, FB, FC, None) == E
+    assert lib.mdgemm_accum_renorm(4, 4, 2, md.MDGEMM_MAX_LEVELS + 1, FA, FB, FB, FC, None) == E
     assert lib.mdgemm_exponents(4, 4, 3, FA, FB, None) == E
 
 
@@ -98,7 +102,8 @@ def _max_k(pairs):
     return (2**53 - 1) // (pairs * 8191**2)
 
 
-@pytest.mark.parametrize("limbs,cutoff,pairs", [(2, -1, 8), (2, -2, 8), (4, -1, 16), (1, 0, 1), (3, 5, 6)])
+@pytest.mark.parametrize("limbs,cutoff,pairs", [(2, -1, 8), (2, -2, 8), (4, -1, 16), (1, 0, 1), (3, 5, 6),
+                                                (8, -1, 32), (16, -1, 64), (16, -2, 64)])
 def test_exactness_bound(lib, limbs, cutoff, pairs):
     kmax = _max_k(pairs)
     assert _ex(lib, 4, 4, kmax + 1, limbs, cutoff=cutoff) == md.MDGEMM_EEXACT
@@ -119,7 +124,9 @@ def test_workspace_bytes_layout(lib):
     assert md.mdgemm_workspace_bytes(100, 70, 33, 2, cutoff=-2) == expect(100, 70, 33, 2, 8, 14)
     assert md.mdgemm_workspace_bytes(64, 64, 64, 4, slices_per_limb=3, cutoff=5) == expect(64, 64, 64, 4, 12, 5)
     assert md.mdgemm_workspace_bytes(0, 64, 64, 2) == 0
-    assert md.mdgemm_workspace_bytes(4, 4, 4, 9) == 2**64 - 1
+    assert md.mdgemm_workspace_bytes(256, 8192, 128, 8) == expect(256, 8192, 128, 8, 32, 31)
+    assert md.mdgemm_workspace_bytes(128, 8192, 64, 16) == expect(128, 8192, 64, 16, 64, 63)
+    assert md.mdgemm_workspace_bytes(4, 4, 4, md.MDGEMM_MAX_LIMBS + 1) == 2**64 - 1
 
 
 def test_workspace_too_small_is_reported_before_any_launch(lib):

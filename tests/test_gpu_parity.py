@@ -77,7 +77,9 @@ def test_exponents(rows, cols):
 
 @pytest.mark.parametrize("L,S,rows,cols,axis", [(1, 4, 33, 70, 0), (2, 8, 65, 129, 0), (2, 8, 130, 17, 1),
                                                  (3, 12, 40, 300, 1), (4, 16, 77, 91, 0), (2, 5, 20, 20, 1),
-                                                 (4, 13, 31, 33, 1), (3, 16, 9, 9, 0)])
+                                                 (4, 13, 31, 33, 1), (3, 16, 9, 9, 0),
+                                                 (8, 32, 40, 70, 0), (8, 40, 17, 130, 1), (16, 64, 20, 33, 1),
+                                                 (16, 64, 129, 18, 0), (16, 16, 9, 9, 0), (5, 20, 33, 17, 1)])
 def test_split_random(L, S, rows, cols, axis):
     print(f"[case] split L={L} S={S} {rows}x{cols} axis={axis}", flush=True)
     rng = np.random.default_rng(L * 100 + S)
@@ -127,7 +129,7 @@ def _adversarial_elements(L, count, seed):
     return out
 
 
-@pytest.mark.parametrize("L", [2, 3, 4])
+@pytest.mark.parametrize("L", [2, 3, 4, 8, 16])
 def test_split_adversarial(L):
     print(f"[case] split adversarial L={L}", flush=True)
     els = _adversarial_elements(L, 64 * 33, 900 + L)
@@ -164,7 +166,10 @@ def test_split_golden_cases():
                                        (12, 11, 200, 33, 70), (16, 15, 64, 16, 64), (16, 30, 33, 20, 17),
                                        (3, 2, 257, 129, 300), (8, 7, 16, 1, 16),
                                        # tile grids with partial tile-row groups and uneven XCD chunks
-                                       (8, 7, 1100, 40, 900), (4, 3, 3000, 17, 130), (2, 2, 130, 33, 2900)])
+                                       (8, 7, 1100, 40, 900), (4, 3, 3000, 17, 130), (2, 2, 130, 33, 2900),
+                                       # octo / hexa doubles: 32 and 64 digits, up to 127 levels
+                                       (32, 31, 130, 20, 140), (64, 63, 70, 17, 129), (64, 126, 20, 5, 30),
+                                       (40, 32, 33, 45, 257)])
 def test_levels(S, T, m, k, n):
     print(f"[case] levels S={S} T={T} {m}x{k}x{n}", flush=True)
     rng = np.random.default_rng(S * 1000 + m)
@@ -176,7 +181,7 @@ def test_levels(S, T, m, k, n):
     assert np.array_equal(got, want.astype(np.float64))
 
 
-@pytest.mark.parametrize("S,T", [(8, 14), (8, 7), (4, 2)])
+@pytest.mark.parametrize("S,T", [(8, 14), (8, 7), (4, 2), (32, 31), (24, 46)])
 def test_pair_products(S, T):
     print(f"[case] pairs S={S} T={T}", flush=True)
     rng = np.random.default_rng(S + T)
@@ -222,7 +227,7 @@ def _words_to_int(words):
     return v
 
 
-@pytest.mark.parametrize("levels", [1, 2, 5, 8, 12, 15, 16, 31])
+@pytest.mark.parametrize("levels", [1, 2, 5, 8, 12, 15, 16, 31, 32, 63, 64, 100, 127])
 def test_accumulate_exact(levels):
     print(f"[case] accumulate levels={levels}", flush=True)
     rng = np.random.default_rng(levels)
@@ -269,7 +274,8 @@ def _cases_for_rounding(levels, m, n, seed):
     return G
 
 
-@pytest.mark.parametrize("L,levels", [(1, 4), (2, 8), (2, 15), (3, 12), (4, 16), (4, 31), (2, 1)])
+@pytest.mark.parametrize("L,levels", [(1, 4), (2, 8), (2, 15), (3, 12), (4, 16), (4, 31), (2, 1), (8, 32), (8, 63),
+                                      (16, 64), (16, 127), (5, 40)])
 def test_accum_renorm_greedy_rounding(L, levels):
     print(f"[case] accum_renorm L={L} levels={levels}", flush=True)
     m, n = 13, 71
@@ -293,7 +299,9 @@ def test_accum_renorm_greedy_rounding(L, levels):
 @pytest.mark.parametrize("L,m,k,n,cutoff,seed", [(2, 64, 64, 64, -2, 0), (2, 130, 47, 129, -1, 1),
                                                  (1, 65, 33, 17, -2, 2), (3, 40, 100, 70, -1, 3),
                                                  (4, 33, 20, 45, -1, 4), (4, 17, 64, 9, -2, 5),
-                                                 (2, 1, 1, 1, -1, 6), (3, 129, 16, 1, -2, 7)])
+                                                 (2, 1, 1, 1, -1, 6), (3, 129, 16, 1, -2, 7),
+                                                 (8, 70, 33, 129, -1, 8), (16, 20, 17, 130, -1, 9),
+                                                 (8, 9, 40, 5, -2, 10), (16, 129, 3, 2, -2, 11)])
 def test_mdgemm_end_to_end(L, m, k, n, cutoff, seed):
     print(f"[case] mdgemm L={L} {m}x{k}x{n} cutoff={cutoff}", flush=True)
     A, B = _operands(L, m, k, n, seed, base="normal" if seed % 2 else "uniform", row_exp=15, col_exp=15)

@@ -143,15 +143,15 @@ def _random_md(rng, L, spread=60):
     return limbs
 
 
-@pytest.mark.parametrize("L", [1, 2, 3, 4])
+@pytest.mark.parametrize("L", [1, 2, 3, 4, 8, 16])
 def test_split_invariants_and_brute_force(L):
     rng = random.Random(1234 + L)
-    for trial in range(300):
+    for trial in range(300 if L <= 4 else 80):
         limbs = _random_md(rng, L)
         assert exact.is_nonoverlapping(limbs)
         e0 = exact.frexp_exp(limbs[0])
         E = e0 + rng.choice([0, 0, 0, 1, 3, 13, 40])
-        S = rng.choice([1, 2, 3, 4, 4 * L, 4 * L + 3])
+        S = rng.choice([1, 2, 3, 4, 4 * L, min(4 * L + 3, 64)])
         d, R = exact.split_element(limbs, E, S)
         v = exact.value(limbs)
         u = exact.grid_unit(E, S - 1)
@@ -368,10 +368,10 @@ def _rand_md_array(rng, L, n):
     return np.array([_random_md(rng, L, spread=20) for _ in range(n)]).T.copy()
 
 
-@pytest.mark.parametrize("L", [1, 2, 3, 4])
+@pytest.mark.parametrize("L", [1, 2, 3, 4, 8, 16])
 def test_md_fma_relative_error(L):
     rng = random.Random(40 + L)
-    n = 400
+    n = 400 if L <= 4 else 60
     acc, a, b = _rand_md_array(rng, L, n), _rand_md_array(rng, L, n), _rand_md_array(rng, L, n)
     out = coracle.md_fma(acc, a, b)
     worst = 0.0
@@ -401,7 +401,7 @@ def test_dd_add_mul_relative_error():
     assert ws <= 4 * 2.0**-106 and wp <= 8 * 2.0**-106, (ws, wp)
 
 
-@pytest.mark.parametrize("L,variant", [(1, 1), (2, 0), (2, 1), (3, 1), (4, 1)])
+@pytest.mark.parametrize("L,variant", [(1, 1), (2, 0), (2, 1), (3, 1), (4, 1), (8, 1), (16, 1)])
 def test_classic_gemm_within_bound(L, variant):
     rng = np.random.default_rng(20 + L)
     m, k, n = 5, 7, 4
@@ -445,6 +445,47 @@ def test_sliced_chain_within_tolerance(L, S, T):
             assert exact.is_nonoverlapping(got)
             want, mag = exact.exact_product(A, B, i, j)
             assert abs(exact.value(got) - want) <= exact.tolerance(k, L, mag)
+
+
+@pytest.mark.parametrize("L,S,T,k", [(2, 8, 7, 64), (4, 16, 15, 40), (3, 12, 20, 9), (8, 32, 31, 24),
+                                     (16, 64, 63, 9), (8, 40, 32, 12)])
+def test_sliced_chain_within_method_bound(L, S, T, k):
+    # The truncation and dropped-pair bound of the sliced product (exact.method_bound)
+    # holds for every digit count and cutoff, including octo and hexa doubles with
+    # four digits per limb, where the 53 L-bit tolerance cannot.
+    rng = np.random.default_rng(300 + L + S + T)
+    m, n = 2, 3
+    A = workloads.make_operand(rng, L, m, k, base="normal", row_exp=10)
+    B = workloads.make_operand(rng, L, k, n, base="normal", col_exp=10)
+    ref = pipeline.full_reference(A, B, S, T)
+    EA, EB = coracle.exponents(A[0], 0), coracle.exponents(B[0], 1)
+    for i in range(m):
+        for j in range(n):
+            got = ref["C"][:, i, j]
+            assert exact.is_nonoverlapping(got)
+            want, mag = exact.exact_product(A, B, i, j)
+            bound = exact.method_bound(A, B, i, j, S, T, int(EA[i]), int(EB[j]))
+            err = abs(exact.value(got) - want)
+            assert err <= bound, (i, j, float(err / bound))
+            # not vacuous: far below the magnitude, at the scale of 2^-13S per unit of the grid
+            assert bound < mag * Fraction(2) ** (-13 * min(S, T + 1) + 30)
+
+
+def test_method_bound_catches_a_dropped_kept_pair():
+    # Planted in the oracle's chain: leave out pair (0, T) of the last kept level.
+    L, S, T, k = 8, 32, 31, 16
+    rng = np.random.default_rng(5)
+    A = workloads.make_operand(rng, L, 1, k, base="normal")
+    B = workloads.make_operand(rng, L, k, 1, base="normal")
+    EA, EB = coracle.exponents(A[0], 0), coracle.exponents(B[0], 1)
+    DA, DB = coracle.split(A, EA, S, 0), coracle.split(B, EB, S, 1)
+    per = coracle.levels(DA, DB, T, per_pair=True)
+    levels = [int(sum(per[p, t - p, 0, 0] for p, q in exact.pairs_of_level(t, S) if not (t == T and p == 0)))
+              for t in range(T + 1)]
+    bad = exact.round_to_limbs(exact.accumulate(levels, int(EA[0]), int(EB[0])), L)
+    want, _ = exact.exact_product(A, B, 0, 0)
+    bound = exact.method_bound(A, B, 0, 0, S, T, int(EA[0]), int(EB[0]))
+    assert abs(exact.value(bad) - want) > bound
 
 
 def test_reference_entries_agree_with_full_reference():
