@@ -35,13 +35,17 @@ if ROOT not in sys.path:
 MFMA_F64_PEAK_TFLOPS = 78.6  # MI355X dense FP64 matrix peak (published)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E (published)
 METRIC = "effective dd/qd GEMM GFLOP/s; % FP64 MFMA peak; bit-exact+tol vs CPU oracle"
-GEMM_SOURCE = os.path.join(ROOT, "paper_2607_06881_amd", "csrc", "slice_gemm.hip")
+# the level-GEMM kernel is built from these sources (its job table is declared in internal.h)
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2607_06881_amd", "csrc", f) for f in ("slice_gemm.hip", "internal.h")]
 DEFAULT_CONFIG = "c2"
 
 
-def kernel_source_hash(path: str = GEMM_SOURCE) -> str:
-    with open(path, "rb") as fh:
-        return hashlib.sha256(fh.read()).hexdigest()[:16]
+def kernel_source_hash(paths=GEMM_SOURCES) -> str:
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def stored_traffic(config: str):
