@@ -75,12 +75,17 @@ def cpu_baseline(w, A, B, target_s: float):
     from oracle import coracle
 
     coracle.lib()
-    # calibrate on one row per thread, then size the sample to about target_s seconds
+    # calibrate on one row per thread, four times more until the run lasts half a
+    # second (or covers C), then size the sample to about target_s seconds
     threads = coracle.num_threads()
     rows = min(w.m, threads)
-    t = time.perf_counter()
-    coracle.classic_gemm(A[:, :rows, :], B)
-    dt = max(time.perf_counter() - t, 1e-3)
+    while True:
+        t = time.perf_counter()
+        coracle.classic_gemm(A[:, :rows, :], B)
+        dt = max(time.perf_counter() - t, 1e-3)
+        if dt >= 0.5 or rows >= w.m:
+            break
+        rows = min(w.m, 4 * rows)
     rows = int(min(w.m, max(threads, rows * target_s / dt)))
     t = time.perf_counter()
     _, used = coracle.classic_gemm(A[:, :rows, :], B)
