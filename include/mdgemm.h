@@ -48,7 +48,7 @@ extern "C" {
 /* ---- status codes ---------------------------------------------------------- */
 #define MDGEMM_OK 0
 #define MDGEMM_EINVAL -1      /* invalid size, limb/slice/cutoff count, null or overlapping pointer */
-#define MDGEMM_EEXACT -2      /* pairs_t * k * 8191^2 >= 2^53 for some kept level t: sums not exact */
+#define MDGEMM_EEXACT -2      /* pairs_t * k * (2^w - 1)^2 >= 2^53 for some kept level t: sums not exact */
 #define MDGEMM_ENOMEM -3      /* the library's own workspace could not be allocated */
 #define MDGEMM_EHIP -4        /* a HIP call failed (no device, launch or runtime error) */
 #define MDGEMM_EWORKSPACE -5  /* the caller's workspace is smaller than mdgemm_workspace_bytes() */
@@ -58,8 +58,13 @@ extern "C" {
 #define MDGEMM_MAX_LIMBS 16   /* double (1), double-double (2), ... quad (4), octo (8), hexa double (16) */
 #define MDGEMM_MAX_SLICES 64  /* digits per element */
 #define MDGEMM_MAX_LEVELS 127 /* 2 * MDGEMM_MAX_SLICES - 1 */
-#define MDGEMM_SLICE_BITS 13
-#define MDGEMM_Z_WORDS 28     /* 64-bit words per element written by mdgemm_accumulate */
+#define MDGEMM_SLICE_BITS 13      /* digit width of section 2 */
+#define MDGEMM_MAX_SLICE_BITS 26  /* widest digit: a product of two stays below 2^52 */
+#define MDGEMM_MAX_DIGIT_BITS 844 /* slices * slice_bits + 52 <= 14 64-bit words */
+#define MDGEMM_Z_WORDS 28         /* 64-bit words per element written by mdgemm_accumulate */
+
+/* slice_bits selector for mdgemm_opts.slice_bits (else an explicit width 1..26) */
+#define MDGEMM_SLICE_BITS_AUTO -1 /* the width with the fewest pairs that stays exact for this k */
 
 /* ---- flags for mdgemm_opts.flags ------------------------------------------- */
 #define MDGEMM_CHECK_FINITE 1u /* scan A and B for inf/nan first; synchronizes the stream */
@@ -74,16 +79,37 @@ typedef struct mdgemm_opts {
   void* stream;           /* hipStream_t to launch on; NULL = default stream */
   void* workspace;        /* caller-owned device buffer; NULL = library-owned cache */
   size_t workspace_bytes; /* size of `workspace` in bytes */
-  int slices_per_limb;    /* digits per limb, S = limbs * slices_per_limb <= 64; 0 = 4 */
+  int slices_per_limb;    /* 13-bit digits per limb, S = limbs * slices_per_limb <= 64; 0 = 4 */
   int cutoff;             /* largest kept p + q; MDGEMM_CUTOFF_DEFAULT or _ALL or 0..2S-2 */
   unsigned flags;         /* MDGEMM_CHECK_FINITE | MDGEMM_SYNC | MDGEMM_TIME_STAGES */
+  int slice_bits;         /* digit width w: 0 = 13 (section 2), 1..26, or MDGEMM_SLICE_BITS_AUTO */
+  int slices;             /* digits per element S; 0 = derived (see below) */
 } mdgemm_opts;
 
+/* Digit width and count.
+ *  - slice_bits 0 or 13: w = 13 and S = slices, else limbs * slices_per_limb.
+ *  - slice_bits 1..26 (the adaptive width, wider digits and fewer of them): S =
+ *    slices, else ceil(52 limbs / w), the digit bits of four 13-bit digits per limb.
+ *  - MDGEMM_SLICE_BITS_AUTO (slices must be 0): among w = 13..26 with
+ *    S = ceil(52 limbs / w) and S k (2^w - 1)^2 < 2^53 (every level with T <= S - 1
+ *    stays exact), the one with the fewest pairs S (S + 1) / 2, the wider on a tie;
+ *    MDGEMM_EEXACT when none qualifies.  Double-double at k = 4096 gets w = 19,
+ *    S = 6 (21 pairs instead of 36); the digits cover at least as many bits as
+ *    four 13-bit digits per limb, so the product is at least as accurate.
+ * In every case S <= 64 and S w <= MDGEMM_MAX_DIGIT_BITS. */
+
 /* Fill `opts` with the defaults: default stream, library workspace, 4 slices per
- * limb, cutoff T = S - 1, no flags. */
+ * limb of 13 bits, cutoff T = S - 1, no flags. */
 void mdgemm_opts_init(mdgemm_opts* opts);
 
-/* C = A.B for L-limb operands (L = limbs in 1..16) with the default options.
+/* The digit width, digit count and cutoff mdgemm_ex uses for this product and
+ * these options (opts may be NULL), written to *slice_bits, *slices, *cutoff
+ * (each pointer may be NULL).  Returns MDGEMM_OK, MDGEMM_EINVAL or MDGEMM_EEXACT. */
+int mdgemm_plan(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts, int* slice_bits, int* slices,
+                int* cutoff);
+
+/* C = A.B for L-limb operands (L = limbs in 1..16) with the default options (13-bit
+ * digits, four per limb).
  * m, n, k >= 0; m == 0 or n == 0 does nothing; k == 0 writes C = +0.0.
  * Returns MDGEMM_OK or a negative status. */
 int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C);
@@ -128,13 +154,15 @@ int mdgemm_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int
 /* Step a2, the exact split (section 2 worked example; sections 2-3 balancing and
  * the opposite-sign transfer).  X [limbs][rows][cols], E from mdgemm_exponents
  * with the same axis, D [slices][rows][cols] (float64, integer valued).  For each
- * element with exact value V on grid exponent E: D_abs = floor(|V| / 2^(E - 13 S)),
- * digit s = sign(V) * bits 13(S-1-s) .. 13(S-s)-1 of D_abs, so that
- * V = sum_s digit_s 2^(E - 13(s+1)) + R with |R| < 2^(E - 13 S) and R V >= 0.
+ * element with exact value V on grid exponent E and digit width w = slice_bits
+ * (13 in section 2): D_abs = floor(|V| / 2^(E - w S)),
+ * digit s = sign(V) * bits w(S-1-s) .. w(S-s)-1 of D_abs, so that
+ * V = sum_s digit_s 2^(E - w(s+1)) + R with |R| < 2^(E - w S) and R V >= 0.
  * Zero digits are +0.0.  Requires |V| < 2^E (true for normalized input and the
- * exponents of mdgemm_exponents).  limbs 1..16, slices 1..64. */
-int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int axis, const double* X, const int32_t* E,
-                 double* D, void* stream);
+ * exponents of mdgemm_exponents).  limbs 1..16, slices 1..64, slice_bits 1..26,
+ * slices * slice_bits <= 844. */
+int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int slice_bits, int axis, const double* X,
+                 const int32_t* E, double* D, void* stream);
 
 /* Step a2 into the operand layout of mdgemm_slice_gemm ("panels"): the same
  * digits as mdgemm_split, k-major and zero-padded to whole GEMM tiles, with
@@ -143,11 +171,12 @@ int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int axis, co
  *   axis 0 (A, rows = m, cols = k):  D [slices][kp][cp], D[s][kk][i] = digit s of A[i][kk];
  *   axis 1 (B, rows = k, cols = n):  D [slices][kp][cp], D[s][kk][j] = digit s of B[kk][j].
  * Every padding entry is +0.0.  Arguments and requirements as mdgemm_split. */
-int mdgemm_split_panel(int64_t rows, int64_t cols, int limbs, int slices, int axis, const double* X,
-                       const int32_t* E, double* D, void* stream);
+int mdgemm_split_panel(int64_t rows, int64_t cols, int limbs, int slices, int slice_bits, int axis,
+                       const double* X, const int32_t* E, double* D, void* stream);
 
 /* Step a3, the slice GEMMs (section 2, equation (3) and the rewritten product).
- * DAt and DBp are digit panels (see mdgemm_split_panel) with |digit| <= 8191:
+ * DAt and DBp are digit panels (see mdgemm_split_panel) with |digit| <= 2^w - 1,
+ * w = slice_bits (8191 for the 13-bit digits of section 2):
  * DAt [S][kp][mp] holds A's digits transposed, DBp [S][kp][np] holds B's, where
  * kp = k rounded up to 16, mp = m and np = n rounded up to 128, zero padding;
  * both pointers 16-byte aligned.
@@ -156,27 +185,29 @@ int mdgemm_split_panel(int64_t rows, int64_t cols, int limbs, int slices, int ax
  * out[p][q] = DA_p . DB_q for every p + q <= cutoff (other planes untouched; one
  * launch per 256 pairs).
  * Exact in FP64 (any summation order) because every partial sum is an integer
- * below 2^53; returns MDGEMM_EEXACT when pairs_t * k * 8191^2 >= 2^53.
- * S in 1..64, cutoff in 0..2S-2. */
-int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, int per_pair, const double* DAt,
-                      const double* DBp, double* out, void* stream);
+ * below 2^53; returns MDGEMM_EEXACT when pairs_t * k * (2^w - 1)^2 >= 2^53.
+ * S in 1..64, slice_bits 1..26, cutoff in 0..2S-2. */
+int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, int per_pair,
+                      const double* DAt, const double* DBp, double* out, void* stream);
 
 /* Step a4 alone, the exact accumulation (section 2, steps 4-5), exported for
- * checking.  G [levels][m][n] integer-valued with |G| < 2^53, levels 1..127.
- * Writes the integer N = sum_t G_t 2^(13 (levels-1-t)) as MDGEMM_Z_WORDS 64-bit
- * two's-complement words, least significant first: Z [MDGEMM_Z_WORDS][m][n] int64.  The
- * accumulated value is N 2^(-13 (levels-1)) (before the grid scale). */
-int mdgemm_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, void* stream);
+ * checking.  G [levels][m][n] integer-valued with |G| < 2^53, levels 1..127,
+ * w = slice_bits 1..26 with w (levels - 1) + 55 <= 1792 (the sum fits 28 words).  Writes the integer
+ * N = sum_t G_t 2^(w (levels-1-t)) as MDGEMM_Z_WORDS 64-bit two's-complement
+ * words, least significant first: Z [MDGEMM_Z_WORDS][m][n] int64.  The
+ * accumulated value is N 2^(-w (levels-1)) (before the grid scale). */
+int mdgemm_accumulate(int64_t m, int64_t n, int levels, int slice_bits, const double* G, int64_t* Z, void* stream);
 
 /* Steps a4 + a5: exact accumulation of the levels and rounding into `limbs`
  * nonoverlapping doubles (section 1, renormalization; section 2, adding the parts
- * into a multiple double), times the grid scale 2^(EA[i] + EB[j] - 26):
- * with Z = sum_t G_t 2^(-13 t), C[.][i][j] = (c_0, .., c_{L-1}) 2^(EA[i]+EB[j]-26)
+ * into a multiple double), times the grid scale 2^(EA[i] + EB[j] - 2w),
+ * w = slice_bits (13: 2^(EA + EB - 26)):
+ * with Z = sum_t G_t 2^(-w t), C[.][i][j] = (c_0, .., c_{L-1}) 2^(EA[i]+EB[j]-2w)
  * where c_0 = RN(Z) and c_l = RN(Z - c_0 - .. - c_{l-1}) (round to nearest, ties
- * to even).  G [levels][m][n] (levels 1..127), EA int32[m], EB int32[n],
- * C [limbs][m][n] (limbs 1..16). */
-int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, const double* G, const int32_t* EA,
-                        const int32_t* EB, double* C, void* stream);
+ * to even).  G [levels][m][n] (levels 1..127, w (levels - 1) + 55 <= 1792), EA int32[m],
+ * EB int32[n], C [limbs][m][n] (limbs 1..16). */
+int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, int slice_bits, const double* G,
+                        const int32_t* EA, const int32_t* EB, double* C, void* stream);
 
 #ifdef __cplusplus
 }

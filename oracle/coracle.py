@@ -41,6 +41,9 @@ def lib():
         L.oracle_exponents.restype = ctypes.c_int
         L.oracle_split.argtypes = [_i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _dp, _ip, _dp]
         L.oracle_split.restype = ctypes.c_int
+        L.oracle_split_bits.argtypes = [_i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, _dp, _ip,
+                                        _dp]
+        L.oracle_split_bits.restype = ctypes.c_int
         L.oracle_levels.argtypes = [_i64, _i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _dp, _dp, _lp]
         L.oracle_levels.restype = ctypes.c_int
         L.oracle_num_threads.restype = ctypes.c_int
@@ -129,13 +132,16 @@ def exponents(X0, axis):
     return E
 
 
-def split(X, E, S, axis):
-    """Digits [S][rows][cols] (float64, integer valued)."""
+def split(X, E, S, axis, bits=13):
+    """Digits [S][rows][cols] (float64, integer valued) of `bits` bits each."""
     X = _f64(X)
     L, rows, cols = X.shape
     E = np.ascontiguousarray(E, dtype=np.int32)
     D = np.empty((S, rows, cols), dtype=np.float64)
-    st = lib().oracle_split(rows, cols, L, S, axis, _d(X), E.ctypes.data_as(_ip), _d(D))
+    if bits == 13:
+        st = lib().oracle_split(rows, cols, L, S, axis, _d(X), E.ctypes.data_as(_ip), _d(D))
+    else:
+        st = lib().oracle_split_bits(rows, cols, L, S, bits, axis, _d(X), E.ctypes.data_as(_ip), _d(D))
     if st:
         raise ValueError(f"oracle_split failed: {st}")
     return D

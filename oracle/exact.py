@@ -67,37 +67,40 @@ def line_exponents(X0: np.ndarray, axis: int) -> np.ndarray:
 # the exact splitter
 # --------------------------------------------------------------------------
 
-def grid_unit(E: int, s: int) -> Fraction:
-    """Unit of slice s on the grid of exponent E: 2^(E - 13 (s + 1))."""
-    return Fraction(2) ** int(E - SLICE_BITS * (s + 1))
+def grid_unit(E: int, s: int, bits: int = SLICE_BITS) -> Fraction:
+    """Unit of slice s on the grid of exponent E: 2^(E - w (s + 1)), w = bits
+    (13 in section 2)."""
+    return Fraction(2) ** int(E - bits * (s + 1))
 
 
-def split_element(limbs, E: int, S: int):
+def split_element(limbs, E: int, S: int, bits: int = SLICE_BITS):
     """Digits and residual of one multiple double on the grid of exponent E.
 
     Following the worked example of section 2, the magnitude of the exact value
     is cut into consecutive 13-bit fields below 2^E, truncating (the fields are
     plain bit fields of the value); every digit carries the sign of the value
     (sign-magnitude, the same-signed parts that the sign grouping and the 2^-52
-    transfer of section 3 aim at).  Returns (digits, R) with
-    value = sum_s digits[s] 2^(E - 13(s+1)) + R, |R| < 2^(E - 13 S), R * value >= 0.
+    transfer of section 3 aim at).  With bits = w the fields are w bits wide
+    (the adaptive slice width; w = 13 is section 2's cut).  Returns (digits, R) with
+    value = sum_s digits[s] 2^(E - w(s+1)) + R, |R| < 2^(E - w S), R * value >= 0.
     Raises ValueError when |value| >= 2^E (the element is not on this grid).
     """
-    E, S = int(E), int(S)
+    E, S, bits = int(E), int(S), int(bits)
     v = value(limbs)
     if v == 0:
         return [0] * S, Fraction(0)
     sign = 1 if v > 0 else -1
-    u = grid_unit(E, S - 1)
+    u = grid_unit(E, S - 1, bits)
     D = math.floor(abs(v) / u)
-    if D >> (SLICE_BITS * S):
+    if D >> (bits * S):
         raise ValueError("|value| >= 2^E: element is not on the grid")
-    digits = [sign * ((D >> (SLICE_BITS * (S - 1 - s))) & DIGIT_MAX) for s in range(S)]
-    R = v - sum((d * grid_unit(E, s) for s, d in enumerate(digits)), Fraction(0))
+    mask = (1 << bits) - 1
+    digits = [sign * ((D >> (bits * (S - 1 - s))) & mask) for s in range(S)]
+    R = v - sum((d * grid_unit(E, s, bits) for s, d in enumerate(digits)), Fraction(0))
     return digits, R
 
 
-def split(X: np.ndarray, E: np.ndarray, S: int, axis: int) -> np.ndarray:
+def split(X: np.ndarray, E: np.ndarray, S: int, axis: int, bits: int = SLICE_BITS) -> np.ndarray:
     """Digits [S][rows][cols] (int64) of an operand X [L][rows][cols]."""
     X = np.asarray(X, dtype=np.float64)
     L, rows, cols = X.shape
@@ -105,7 +108,7 @@ def split(X: np.ndarray, E: np.ndarray, S: int, axis: int) -> np.ndarray:
     for r in range(rows):
         for c in range(cols):
             e = int(E[r] if axis == 0 else E[c])
-            d, _ = split_element(X[:, r, c], e, S)
+            d, _ = split_element(X[:, r, c], e, S, bits)
             D[:, r, c] = d
     return D
 
@@ -139,15 +142,16 @@ def level_products(DA: np.ndarray, DB: np.ndarray, T: int) -> list:
     return G
 
 
-def accumulate(levels, EA: int, EB: int) -> Fraction:
+def accumulate(levels, EA: int, EB: int, bits: int = SLICE_BITS) -> Fraction:
     """Z = sum_t G_t 2^(-13 t), times the grid scale 2^(EA + EB - 26).
 
     Slice p of A has unit 2^(EA - 13(p+1)) and slice q of B has unit
     2^(EB - 13(q+1)); their product has unit 2^(EA + EB - 26 - 13(p+q)), so level
-    t = p + q carries weight 2^(EA + EB - 26 - 13 t)."""
+    t = p + q carries weight 2^(EA + EB - 26 - 13 t).  With w-bit digits
+    (bits = w) the weights are 2^(EA + EB - 2w - w t)."""
     z = Fraction(0)
     for t, g in enumerate(levels):
-        z += Fraction(int(g)) * Fraction(2) ** int(EA + EB - 2 * SLICE_BITS - SLICE_BITS * t)
+        z += Fraction(int(g)) * Fraction(2) ** int(EA + EB - 2 * bits - bits * t)
     return z
 
 
@@ -180,7 +184,8 @@ def tolerance(k: int, L: int, mag: Fraction) -> Fraction:
     return 4 * k * Fraction(2) ** (-(53 * L - 4)) * mag
 
 
-def method_bound(A: np.ndarray, B: np.ndarray, i: int, j: int, S: int, T: int, EA: int, EB: int) -> Fraction:
+def method_bound(A: np.ndarray, B: np.ndarray, i: int, j: int, S: int, T: int, EA: int, EB: int,
+                 bits: int = SLICE_BITS) -> Fraction:
     """Bound on |C[i][j] - C_exact[i][j]| of the sliced product with S digits per
     element and the pairs p + q <= T, from the parts of section 2:
 
@@ -195,7 +200,9 @@ def method_bound(A: np.ndarray, B: np.ndarray, i: int, j: int, S: int, T: int, E
 
     With S = 4 L this is about 2^(5 - 13 S) k 2^(EA + EB) relative, which for
     L >= 5 is looser than 4 k 2^-(53 L - 4) (|A||B|): four 13-bit digits carry 52
-    of the 53 bits of every limb."""
+    of the 53 bits of every limb.  With w-bit digits (bits = w) every 13 above is w
+    and a product of digits is below 2^(2w)."""
+    w = int(bits)
     k = A.shape[2]
     two = Fraction(2)
     L = A.shape[0]
@@ -204,12 +211,29 @@ def method_bound(A: np.ndarray, B: np.ndarray, i: int, j: int, S: int, T: int, E
     for kk in range(k):
         a, b = abs(value(A[:, i, kk])), abs(value(B[:, kk, j]))
         mag += a * b
-        trunc += a * two ** (EB - 13 * S) + b * two ** (EA - 13 * S) + two ** (EA + EB - 26 * S)
+        trunc += a * two ** (EB - w * S) + b * two ** (EA - w * S) + two ** (EA + EB - 2 * w * S)
     dropped = Fraction(0)
     for t in range(T + 1, 2 * S - 1):
-        dropped += len(pairs_of_level(t, S)) * two ** (26 + EA + EB - 13 * (t + 2))
+        dropped += len(pairs_of_level(t, S)) * two ** (2 * w + EA + EB - w * (t + 2))
     dropped *= k
     return trunc + dropped + 2 * two ** (-53 * L) * (mag + trunc + dropped)
+
+
+def adaptive_width(L: int, k: int, max_digit_bits: int = 844):
+    """(w, S) of the adaptive slice width: among w = 13..26 with S = ceil(52 L / w)
+    digits (the bits of four 13-bit digits per limb) such that every level with
+    T <= S - 1 stays exact, S k (2^w - 1)^2 < 2^53 (the bound (NBound) of
+    section 2 with w-bit digits), the fewest pairs S (S + 1) / 2, the wider digit
+    on a tie; S <= 64 and S w <= max_digit_bits.  None when no width qualifies."""
+    best = None
+    for w in range(13, 27):
+        S = -(-52 * L // w)
+        if S > 64 or S * w > max_digit_bits or S * k * (2**w - 1) ** 2 >= 2**53:
+            continue
+        key = (S * (S + 1) // 2, -w)
+        if best is None or key < best[0]:
+            best = (key, w, S)
+    return None if best is None else (best[1], best[2])
 
 
 def is_nonoverlapping(limbs) -> bool:

@@ -364,16 +364,18 @@ static inline int big_bit(const bigint* x, int pos) {
 }
 
 /* Split one element with L limbs (stride between limbs `ls`) on the grid of
- * exponent E into S digits (stride between digits `ds`).
+ * exponent E into S digits of w bits (stride between digits `ds`).
  *
  * The exact value V = sum of the limbs is formed as the integer V * 2^1074.  Its
- * magnitude, read on the grid whose unit is u = 2^(E - 13 S), gives
- * D = floor(|V| / u) < 2^(13 S); digit s is the 13-bit field of D holding
- * 2^(13 (S-1-s)) .. 2^(13 (S-s)) - 1, carrying the sign of V.  These are the
- * truncated 13-bit quarters of the worked example of section 2, taken of the
+ * magnitude, read on the grid whose unit is u = 2^(E - w S), gives
+ * D = floor(|V| / u) < 2^(w S); digit s is the w-bit field of D holding
+ * 2^(w (S-1-s)) .. 2^(w (S-s)) - 1, carrying the sign of V.  For w = 13 these are
+ * the truncated 13-bit quarters of the worked example of section 2, taken of the
  * exact value on a balanced grid (sections 2 and 3), so a limb of opposite sign
- * borrows from the limbs above it exactly as the 2^-52 transfer of section 3 does. */
-static int split_one(const double* x, int64_t ls, int L, int E, int S, double* d, int64_t ds) {
+ * borrows from the limbs above it exactly as the 2^-52 transfer of section 3 does.
+ * Wider digits are the same cut with fewer, longer fields (the slice width is
+ * bounded by the exactness condition (NBound) of section 2, not by 13). */
+static int split_one(const double* x, int64_t ls, int L, int E, int S, int w, double* d, int64_t ds) {
   bigint v;
   memset(&v, 0, sizeof v);
   for (int l = 0; l < L; ++l) {
@@ -391,38 +393,45 @@ static int split_one(const double* x, int64_t ls, int L, int E, int S, double* d
   }
   int neg = big_is_negative(&v);
   if (neg) big_negate(&v);
-  /* bit position (in v) of the grid unit u = 2^(E - 13 S) */
-  int base = E - 13 * S + 1074;
+  /* bit position (in v) of the grid unit u = 2^(E - w S) */
+  int base = E - w * S + 1074;
   /* every bit of |V| at or above 2^E must be zero */
-  for (int pos = (base + 13 * S < 0 ? 0 : base + 13 * S); pos < 64 * BIGW; ++pos)
+  for (int pos = (base + w * S < 0 ? 0 : base + w * S); pos < 64 * BIGW; ++pos)
     if (big_bit(&v, pos)) return ORACLE_ERANGE;
   for (int s = 0; s < S; ++s) {
-    int lo = base + 13 * (S - 1 - s);
+    int lo = base + w * (S - 1 - s);
     int digit = 0;
-    for (int b = 12; b >= 0; --b) digit = 2 * digit + big_bit(&v, lo + b);
+    for (int b = w - 1; b >= 0; --b) digit = 2 * digit + big_bit(&v, lo + b);
     d[s * ds] = neg ? -(double)digit : (double)digit;
     if (digit == 0) d[s * ds] = 0.0;
   }
   return ORACLE_OK;
 }
 
-/* Digits of an operand X [L][rows][cols] on the grids E (per row for axis 0,
- * per column for axis 1), written to D [S][rows][cols]. */
-int oracle_split(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E, double* D) {
-  if (rows < 0 || cols < 0 || L < 1 || L > 16 || S < 1 || S > 64 || (axis != 0 && axis != 1)) return ORACLE_EINVAL;
+/* Digits of w bits (1 <= w <= 26) of an operand X [L][rows][cols] on the grids E
+ * (per row for axis 0, per column for axis 1), written to D [S][rows][cols]. */
+int oracle_split_bits(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
+                      double* D) {
+  if (rows < 0 || cols < 0 || L < 1 || L > 16 || S < 1 || S > 64 || w < 1 || w > 26 || (axis != 0 && axis != 1))
+    return ORACLE_EINVAL;
   int64_t plane = rows * cols;
   int status = ORACLE_OK;
 #pragma omp parallel for schedule(static)
   for (int64_t idx = 0; idx < plane; ++idx) {
     int64_t r = idx / (cols ? cols : 1), c = idx % (cols ? cols : 1);
     int e = axis == 0 ? E[r] : E[c];
-    int st = split_one(X + idx, plane, L, e, S, D + idx, plane);
+    int st = split_one(X + idx, plane, L, e, S, w, D + idx, plane);
     if (st != ORACLE_OK) {
 #pragma omp atomic write
       status = st;
     }
   }
   return status;
+}
+
+/* The 13-bit digits of section 2. */
+int oracle_split(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E, double* D) {
+  return oracle_split_bits(rows, cols, L, S, 13, axis, X, E, D);
 }
 
 /* ------------------------------------------------------------------------- */

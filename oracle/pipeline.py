@@ -30,21 +30,21 @@ def exponents(A: np.ndarray, B: np.ndarray):
     return coracle.exponents(A[0], 0).astype(np.int64), coracle.exponents(B[0], 1).astype(np.int64)
 
 
-def row_digits(A: np.ndarray, EA: np.ndarray, rows, S: int) -> dict:
+def row_digits(A: np.ndarray, EA: np.ndarray, rows, S: int, bits: int = 13) -> dict:
     """Digits [S][k] (int64) of the chosen rows of A."""
     out = {}
     for i in rows:
         X = np.ascontiguousarray(A[:, i:i + 1, :])
-        out[i] = coracle.split(X, np.array([EA[i]], dtype=np.int32), S, 0)[:, 0, :].astype(np.int64)
+        out[i] = coracle.split(X, np.array([EA[i]], dtype=np.int32), S, 0, bits)[:, 0, :].astype(np.int64)
     return out
 
 
-def col_digits(B: np.ndarray, EB: np.ndarray, cols, S: int) -> dict:
+def col_digits(B: np.ndarray, EB: np.ndarray, cols, S: int, bits: int = 13) -> dict:
     """Digits [S][k] (int64) of the chosen columns of B."""
     out = {}
     for j in cols:
         X = np.ascontiguousarray(B[:, :, j:j + 1])
-        out[j] = coracle.split(X, np.array([EB[j]], dtype=np.int32), S, 1)[:, :, 0].astype(np.int64)
+        out[j] = coracle.split(X, np.array([EB[j]], dtype=np.int32), S, 1, bits)[:, :, 0].astype(np.int64)
     return out
 
 
@@ -52,8 +52,8 @@ def levels_of_entry(da: np.ndarray, db: np.ndarray, T: int) -> list:
     """G_t for one output entry from the digit row da [S][k] and column db [S][k].
 
     int64 dot products are exact: every partial sum is below 2^53 under the
-    exactness condition pairs * k * 8191^2 < 2^53 (the analogue of the bound
-    N (2^26 - 1) <= 2^52 of section 2)."""
+    exactness condition pairs * k * (2^w - 1)^2 < 2^53 (w = 13: the analogue of
+    the bound N (2^26 - 1) <= 2^52 of section 2)."""
     S = da.shape[0]
     G = []
     for t in range(T + 1):
@@ -64,19 +64,19 @@ def levels_of_entry(da: np.ndarray, db: np.ndarray, T: int) -> list:
     return G
 
 
-def reference_entries(A: np.ndarray, B: np.ndarray, S: int, T: int, entries):
+def reference_entries(A: np.ndarray, B: np.ndarray, S: int, T: int, entries, bits: int = 13):
     """For each (i, j): dict with exponents, level products, exact Z and the
     greedy L-limb rounding of Z (the product's expected limbs)."""
     L = A.shape[0]
     EA, EB = exponents(A, B)
     rows = sorted({i for i, _ in entries})
     cols = sorted({j for _, j in entries})
-    dA = row_digits(A, EA, rows, S)
-    dB = col_digits(B, EB, cols, S)
+    dA = row_digits(A, EA, rows, S, bits)
+    dB = col_digits(B, EB, cols, S, bits)
     out = {}
     for i, j in entries:
         G = levels_of_entry(dA[i], dB[j], T)
-        z = exact.accumulate(G, int(EA[i]), int(EB[j]))
+        z = exact.accumulate(G, int(EA[i]), int(EB[j]), bits)
         out[(i, j)] = {
             "EA": int(EA[i]),
             "EB": int(EB[j]),
@@ -87,18 +87,18 @@ def reference_entries(A: np.ndarray, B: np.ndarray, S: int, T: int, entries):
     return out
 
 
-def full_reference(A: np.ndarray, B: np.ndarray, S: int, T: int):
+def full_reference(A: np.ndarray, B: np.ndarray, S: int, T: int, bits: int = 13):
     """Whole-matrix chain for small products: exponents, digits, int64 levels
     and the rounded limbs C [L][m][n]."""
     L, m, k = A.shape
     n = B.shape[2]
     EA, EB = exponents(A, B)
-    DA = coracle.split(A, EA.astype(np.int32), S, 0)
-    DB = coracle.split(B, EB.astype(np.int32), S, 1)
+    DA = coracle.split(A, EA.astype(np.int32), S, 0, bits)
+    DB = coracle.split(B, EB.astype(np.int32), S, 1, bits)
     G = coracle.levels(DA, DB, T)
     C = np.zeros((L, m, n), dtype=np.float64)
     for i in range(m):
         for j in range(n):
-            z = exact.accumulate([int(G[t, i, j]) for t in range(T + 1)], int(EA[i]), int(EB[j]))
+            z = exact.accumulate([int(G[t, i, j]) for t in range(T + 1)], int(EA[i]), int(EB[j]), bits)
             C[:, i, j] = exact.round_to_limbs(z, L)
     return {"EA": EA, "EB": EB, "DA": DA, "DB": DB, "G": G, "C": C}

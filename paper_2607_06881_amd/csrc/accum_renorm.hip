@@ -7,11 +7,12 @@
 // (renormalization) requires the result to be a sum of nonoverlapping doubles.
 //
 // Level t of an output element is an integer G_t, |G_t| < 2^53, of weight
-// 2^(-13 t) (times the grid scale 2^(EA + EB - 26)).  Their sum is formed
-// exactly, in increasing significance (t = T down to 0), as the two's-complement
-// integer N = sum_t G_t 2^(13 (T - t)) held in NW 64-bit words in registers
-// (a base-2^13 carry chain: one int64 add, mask and shift per level);
-// the value is Z = N 2^(-13 T).  The L limbs are then peeled off greedily with
+// 2^(-w t) (times the grid scale 2^(EA + EB - 2w)); w = 13 for the digits of
+// section 2, up to 26 for the adaptive width.  Their sum is formed exactly, in
+// increasing significance (t = T down to 0), as the two's-complement integer
+// N = sum_t G_t 2^(w (T - t)) held in NW 64-bit words in registers (a base-2^w
+// carry chain: one int64 add, mask and shift per level); the value is
+// Z = N 2^(-w T).  The L limbs are then peeled off greedily with
 // round-to-nearest-even: c_0 = RN(Z), c_1 = RN(Z - c_0), ..., each taken from
 // the 53 leading bits of the remaining magnitude with the round bit and the
 // sticky bits below it; when a limb rounds up, the remainder changes sign.  The
@@ -46,20 +47,21 @@ __device__ inline void add_shifted_signed(uint64_t (&N)[NW], int64_t g, int sh) 
   }
 }
 
-// N = sum_t G_t 2^(13 (T - t)) exactly.  Level t is column j = T - t of weight
-// 2^(13 j); the columns are visited in increasing significance (t = T down to
-// 0) with a running carry in base 2^13: v = G_t + carry, the low 13 bits of v
+// N = sum_t G_t 2^(w (T - t)) exactly.  Level t is column j = T - t of weight
+// 2^(w j); the columns are visited in increasing significance (t = T down to
+// 0) with a running carry in base 2^w: v = G_t + carry, the low w bits of v
 // are the digit of column j (placed into N, whose bits there are still zero)
-// and carry = floor(v / 2^13).  |G_t| < 2^53 keeps |v| < 2^54, so int64 never
+// and carry = floor(v / 2^w).  |G_t| < 2^53 keeps |v| < 2^54, so int64 never
 // overflows; the last carry, signed, is added above column T.
 // Loads are issued eight levels at a time before any of them is used, so a
 // thread keeps up to eight independent loads in flight.
 template <int NW>
-__device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __restrict__ G, int levels, int64_t plane,
-                                         int64_t idx) {
+__device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __restrict__ G, int levels, int w,
+                                         int64_t plane, int64_t idx) {
 #pragma unroll
   for (int i = 0; i < NW; ++i) N[i] = 0;
   const int T = levels - 1;
+  const uint64_t mask = (1ull << w) - 1ull;
   int64_t carry = 0;
   for (int t0 = T; t0 >= 0; t0 -= 8) {
     // unconditional loads (levels below 0 re-read level 0 and are discarded),
@@ -75,15 +77,15 @@ __device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __rest
       const int t = t0 - u;
       if (t < 0) break;
       const int64_t v = static_cast<int64_t>(g[u]) + carry;  // exact: |G_t| < 2^53
-      const uint64_t d = static_cast<uint64_t>(v) & kDigitMax;
-      carry = v >> kSliceBits;  // arithmetic shift: floor division
-      const int pos = kSliceBits * (T - t), w = pos >> 6, b = pos & 63;
-      const uint64_t lo = d << b, hi = b > 64 - kSliceBits ? d >> (64 - b) : 0ull;
+      const uint64_t d = static_cast<uint64_t>(v) & mask;
+      carry = v >> w;  // arithmetic shift: floor division
+      const int pos = w * (T - t), wi = pos >> 6, b = pos & 63;
+      const uint64_t lo = d << b, hi = b > 64 - w ? d >> (64 - b) : 0ull;
 #pragma unroll
-      for (int i = 0; i < NW; ++i) N[i] |= (i == w) ? lo : ((i == w + 1) ? hi : 0ull);
+      for (int i = 0; i < NW; ++i) N[i] |= (i == wi) ? lo : ((i == wi + 1) ? hi : 0ull);
     }
   }
-  if (carry != 0) add_shifted_signed<NW>(N, carry, kSliceBits * (T + 1));
+  if (carry != 0) add_shifted_signed<NW>(N, carry, w * (T + 1));
 }
 
 // Bit `pos` (0 <= pos < 64 NW) of v.
@@ -171,7 +173,7 @@ __device__ inline void round_limbs(uint64_t (&N)[NW], int L, int scale, double* 
 }
 
 template <int NW>
-__global__ void __launch_bounds__(256) accum_renorm_kernel(int64_t m, int64_t n, int L, int levels,
+__global__ void __launch_bounds__(256) accum_renorm_kernel(int64_t m, int64_t n, int L, int levels, int w,
                                                            const double* __restrict__ G,
                                                            const int32_t* __restrict__ EA,
                                                            const int32_t* __restrict__ EB, double* __restrict__ C) {
@@ -182,14 +184,14 @@ __global__ void __launch_bounds__(256) accum_renorm_kernel(int64_t m, int64_t n,
   for (int64_t i = blockIdx.y; i < m; i += gridDim.y) {
     const int64_t idx = i * n + j;
     uint64_t N[NW];
-    accumulate_levels<NW>(N, G, levels, plane, idx);
-    const int scale = EA[i] + ebj - 2 * kSliceBits - kSliceBits * (levels - 1);
+    accumulate_levels<NW>(N, G, levels, w, plane, idx);
+    const int scale = EA[i] + ebj - 2 * w - w * (levels - 1);
     round_limbs<NW>(N, L, scale, C, plane, idx);
   }
 }
 
 template <int NW>
-__global__ void __launch_bounds__(256) accumulate_kernel(int64_t m, int64_t n, int levels,
+__global__ void __launch_bounds__(256) accumulate_kernel(int64_t m, int64_t n, int levels, int w,
                                                          const double* __restrict__ G, int64_t* __restrict__ Z) {
   const int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (j >= n) return;
@@ -197,17 +199,21 @@ __global__ void __launch_bounds__(256) accumulate_kernel(int64_t m, int64_t n, i
   for (int64_t i = blockIdx.y; i < m; i += gridDim.y) {
     const int64_t idx = i * n + j;
     uint64_t N[NW];
-    accumulate_levels<NW>(N, G, levels, plane, idx);
+    accumulate_levels<NW>(N, G, levels, w, plane, idx);
     const uint64_t ext = (N[NW - 1] >> 63) ? ~0ull : 0ull;
     for (int w = 0; w < kZWords; ++w) Z[static_cast<int64_t>(w) * plane + idx] = static_cast<int64_t>(w < NW ? word_at<NW>(N, w) : ext);
   }
 }
 
-// Words for |N| < 2^(13 T + 54) plus a sign bit.
-inline int words_for_levels(int levels) {
-  const int bits = kSliceBits * (levels - 1) + 55;
+}  // namespace
+
+// Words for |N| < 2^(w T + 54) plus a sign bit.
+int accum_words(int levels, int w) {
+  const int bits = w * (levels - 1) + 55;
   return (bits + 63) / 64;
 }
+
+namespace {
 
 inline dim3 elem_grid(int64_t m, int64_t n) {
   return dim3(static_cast<unsigned>((n + 255) / 256), static_cast<unsigned>(m < 65535 ? m : 65535));
@@ -238,22 +244,23 @@ hipError_t with_words(int words, F&& f) {
 
 }  // namespace
 
-hipError_t launch_accum_renorm(int64_t m, int64_t n, int L, int levels, const double* G, const int32_t* EA,
+hipError_t launch_accum_renorm(int64_t m, int64_t n, int L, int levels, int w, const double* G, const int32_t* EA,
                                const int32_t* EB, double* C, hipStream_t stream) {
   if (m == 0 || n == 0) return hipSuccess;
   const dim3 grid = elem_grid(m, n);
   // the next word count instantiated (the extra words hold the sign extension)
-  return with_words(words_for_levels(levels), [&](auto nw) {
-    hipLaunchKernelGGL(accum_renorm_kernel<decltype(nw)::value>, grid, dim3(256), 0, stream, m, n, L, levels, G, EA,
-                       EB, C);
+  return with_words(accum_words(levels, w), [&](auto nw) {
+    hipLaunchKernelGGL(accum_renorm_kernel<decltype(nw)::value>, grid, dim3(256), 0, stream, m, n, L, levels, w, G,
+                       EA, EB, C);
   });
 }
 
-hipError_t launch_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, hipStream_t stream) {
+hipError_t launch_accumulate(int64_t m, int64_t n, int levels, int w, const double* G, int64_t* Z,
+                             hipStream_t stream) {
   if (m == 0 || n == 0) return hipSuccess;
   const dim3 grid = elem_grid(m, n);
-  return with_words(words_for_levels(levels), [&](auto nw) {
-    hipLaunchKernelGGL(accumulate_kernel<decltype(nw)::value>, grid, dim3(256), 0, stream, m, n, levels, G, Z);
+  return with_words(accum_words(levels, w), [&](auto nw) {
+    hipLaunchKernelGGL(accumulate_kernel<decltype(nw)::value>, grid, dim3(256), 0, stream, m, n, levels, w, G, Z);
   });
 }
 

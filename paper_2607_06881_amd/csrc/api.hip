@@ -21,7 +21,8 @@
 
 static_assert(MDGEMM_MAX_LIMBS == mdg::kMaxLimbs && MDGEMM_MAX_SLICES == mdg::kMaxSlices &&
                   MDGEMM_Z_WORDS == mdg::kZWords && MDGEMM_SLICE_BITS == mdg::kSliceBits &&
-                  MDGEMM_MAX_LEVELS == mdg::kMaxLevels,
+                  MDGEMM_MAX_LEVELS == mdg::kMaxLevels && MDGEMM_MAX_SLICE_BITS == mdg::kMaxSliceBits &&
+                  MDGEMM_MAX_DIGIT_BITS == mdg::kMaxDigitBits,
               "the limits of include/mdgemm.h and csrc/internal.h must agree");
 
 namespace {
@@ -33,7 +34,7 @@ constexpr int kStages = 4;
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// ---- exactness: pairs_t * k * 8191^2 < 2^53 for every kept level t ------------
+// ---- exactness: pairs_t * k * (2^w - 1)^2 < 2^53 for every kept level t ------
 
 int max_pairs(int S, int T) {
   int best = 0;
@@ -45,11 +46,18 @@ int max_pairs(int S, int T) {
   return best;
 }
 
-bool exact_ok(int64_t k, int pairs) {
+bool exact_ok(int64_t k, int pairs, int w) {
+  const uint64_t dmax = (1ull << w) - 1ull;
   const unsigned __int128 lhs =
-      static_cast<unsigned __int128>(pairs) * static_cast<unsigned __int128>(k) * (8191u * 8191u);
+      static_cast<unsigned __int128>(pairs) * static_cast<unsigned __int128>(k) * (dmax * dmax);
   return lhs < (static_cast<unsigned __int128>(1) << 53);
 }
+
+bool width_ok(int S, int w) { return S >= 1 && S <= MDGEMM_MAX_SLICES && w >= 1 && w <= mdg::kMaxSliceBits &&
+                                     S * w <= mdg::kMaxDigitBits; }
+
+// w (levels - 1) + 55 bits must fit the widest accumulation (kZWords words)
+bool levels_ok(int levels, int w) { return levels >= 1 && levels <= mdg::kMaxLevels && mdg::accum_words(levels, w) <= mdg::kZWords; }
 
 // ---- job tables ---------------------------------------------------------------
 
@@ -103,17 +111,53 @@ std::vector<JobTable> pair_jobs(int S, int T) {
 // ---- options ----------------------------------------------------------------
 
 struct Resolved {
-  int S = 0, T = 0;
+  int S = 0, T = 0, w = mdg::kSliceBits;
   hipStream_t stream = nullptr;
   unsigned flags = 0;
 };
 
-int resolve(int limbs, const mdgemm_opts* opts, Resolved* r) {
+// Adaptive width: among w = 13..26 with S = ceil(52 L / w) digits (the digit bits
+// of four 13-bit digits per limb) and S k (2^w - 1)^2 < 2^53, the fewest pairs
+// S (S + 1) / 2, the wider digit on a tie.  Returns false when none qualifies.
+bool auto_width(int limbs, int64_t k, int* w_out, int* S_out) {
+  int best_pairs = 0;
+  bool found = false;
+  for (int w = mdg::kSliceBits; w <= mdg::kMaxSliceBits; ++w) {
+    const int S = (4 * mdg::kSliceBits * limbs + w - 1) / w;
+    if (!width_ok(S, w) || !exact_ok(k, S, w)) continue;
+    const int pairs = S * (S + 1) / 2;
+    if (!found || pairs <= best_pairs) {
+      best_pairs = pairs;
+      *w_out = w;
+      *S_out = S;
+      found = true;
+    }
+  }
+  return found;
+}
+
+// Digit width, digit count and cutoff of a product with reduction length k.
+int resolve(int limbs, int64_t k, const mdgemm_opts* opts, Resolved* r) {
   if (limbs < 1 || limbs > MDGEMM_MAX_LIMBS) return MDGEMM_EINVAL;
-  int spl = opts ? opts->slices_per_limb : 0;
-  if (spl == 0) spl = 4;
-  if (spl < 0 || spl * limbs > MDGEMM_MAX_SLICES) return MDGEMM_EINVAL;
-  r->S = spl * limbs;
+  const int bits = opts ? opts->slice_bits : 0;
+  const int slices = opts ? opts->slices : 0;
+  if (slices < 0) return MDGEMM_EINVAL;
+  if (bits == MDGEMM_SLICE_BITS_AUTO) {
+    if (slices != 0) return MDGEMM_EINVAL;
+    if (!auto_width(limbs, k, &r->w, &r->S)) return MDGEMM_EEXACT;
+  } else if (bits == 0 || bits == mdg::kSliceBits) {
+    r->w = mdg::kSliceBits;
+    int spl = opts ? opts->slices_per_limb : 0;
+    if (spl == 0) spl = 4;
+    if (spl < 0) return MDGEMM_EINVAL;
+    r->S = slices ? slices : spl * limbs;
+  } else if (bits >= 1 && bits <= mdg::kMaxSliceBits) {
+    r->w = bits;
+    r->S = slices ? slices : (4 * mdg::kSliceBits * limbs + bits - 1) / bits;
+  } else {
+    return MDGEMM_EINVAL;
+  }
+  if (!width_ok(r->S, r->w)) return MDGEMM_EINVAL;
   int cutoff = opts ? opts->cutoff : MDGEMM_CUTOFF_DEFAULT;
   if (cutoff == MDGEMM_CUTOFF_DEFAULT)
     r->T = r->S - 1;
@@ -123,6 +167,7 @@ int resolve(int limbs, const mdgemm_opts* opts, Resolved* r) {
     r->T = cutoff;
   else
     return MDGEMM_EINVAL;
+  if (!levels_ok(r->T + 1, r->w)) return MDGEMM_EINVAL;
   r->stream = opts ? static_cast<hipStream_t>(opts->stream) : nullptr;
   r->flags = opts ? opts->flags : 0u;
   return MDGEMM_OK;
@@ -241,6 +286,20 @@ void mdgemm_opts_init(mdgemm_opts* opts) {
   std::memset(opts, 0, sizeof *opts);
   opts->slices_per_limb = 4;
   opts->cutoff = MDGEMM_CUTOFF_DEFAULT;
+  opts->slice_bits = 0;
+  opts->slices = 0;
+}
+
+int mdgemm_plan(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts, int* slice_bits, int* slices,
+                int* cutoff) {
+  Resolved r;
+  if (m < 0 || n < 0 || k < 0) return MDGEMM_EINVAL;
+  MDG_TRY(resolve(limbs, k, opts, &r));
+  if (!exact_ok(k, max_pairs(r.S, r.T), r.w)) return MDGEMM_EEXACT;
+  if (slice_bits) *slice_bits = r.w;
+  if (slices) *slices = r.S;
+  if (cutoff) *cutoff = r.T;
+  return MDGEMM_OK;
 }
 
 const char* mdgemm_status_string(int status) {
@@ -258,7 +317,7 @@ const char* mdgemm_status_string(int status) {
 
 size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts) {
   Resolved r;
-  if (m < 0 || n < 0 || k < 0 || resolve(limbs, opts, &r) != MDGEMM_OK) return SIZE_MAX;
+  if (m < 0 || n < 0 || k < 0 || resolve(limbs, k, opts, &r) != MDGEMM_OK) return SIZE_MAX;
   if (m == 0 || n == 0 || k == 0) return 0;
   Layout L;
   if (!layout(m, n, k, r, &L)) return SIZE_MAX;
@@ -269,14 +328,14 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
               const mdgemm_opts* opts) {
   Resolved r;
   if (m < 0 || n < 0 || k < 0) return MDGEMM_EINVAL;
-  MDG_TRY(resolve(limbs, opts, &r));
+  MDG_TRY(resolve(limbs, k, opts, &r));
   if (m == 0 || n == 0) return MDGEMM_OK;
   if (!C || (k > 0 && (!A || !B))) return MDGEMM_EINVAL;
   const size_t abytes = sizeof(double) * limbs * static_cast<size_t>(m) * static_cast<size_t>(k);
   const size_t bbytes = sizeof(double) * limbs * static_cast<size_t>(k) * static_cast<size_t>(n);
   const size_t cbytes = sizeof(double) * limbs * static_cast<size_t>(m) * static_cast<size_t>(n);
   if (k > 0 && (overlaps(C, cbytes, A, abytes) || overlaps(C, cbytes, B, bbytes))) return MDGEMM_EINVAL;
-  if (!exact_ok(k, max_pairs(r.S, r.T))) return MDGEMM_EEXACT;
+  if (!exact_ok(k, max_pairs(r.S, r.T), r.w)) return MDGEMM_EEXACT;
   hipStream_t s = r.stream;
   const bool timed = (r.flags & MDGEMM_TIME_STAGES) != 0;
 
@@ -325,14 +384,14 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, EB, s)));
   if (timed) MDG_TRY(record(1, s));
   // a2: exact splits into S digit planes
-  MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, 0, A, EA, DA, true, s)));
-  MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, 1, B, EB, DB, true, s)));
+  MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, r.w, 0, A, EA, DA, true, s)));
+  MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, r.w, 1, B, EB, DB, true, s)));
   if (timed) MDG_TRY(record(2, s));
   // a3: level GEMMs on the FP64 matrix cores
   MDG_TRY(hip_status(mdg::launch_slice_gemm(m, n, k, DA, DB, G, level_jobs(r.S, r.T), s)));
   if (timed) MDG_TRY(record(3, s));
   // a4 + a5: exact accumulation and greedy rounding into L limbs
-  MDG_TRY(hip_status(mdg::launch_accum_renorm(m, n, limbs, r.T + 1, G, EA, EB, C, s)));
+  MDG_TRY(hip_status(mdg::launch_accum_renorm(m, n, limbs, r.T + 1, r.w, G, EA, EB, C, s)));
   if (timed) {
     MDG_TRY(record(4, s));
     timing().valid = true;
@@ -384,9 +443,9 @@ int mdgemm_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int
   return hip_status(mdg::launch_exponents(rows, cols, axis, X0, E, static_cast<hipStream_t>(stream)));
 }
 
-int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int axis, const double* X, const int32_t* E,
-                 double* D, void* stream) {
-  if (rows < 0 || cols < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || slices < 1 || slices > MDGEMM_MAX_SLICES ||
+int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int slice_bits, int axis, const double* X,
+                 const int32_t* E, double* D, void* stream) {
+  if (rows < 0 || cols < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || !width_ok(slices, slice_bits) ||
       (axis != 0 && axis != 1))
     return MDGEMM_EINVAL;
   if (rows == 0 || cols == 0) return MDGEMM_OK;
@@ -394,13 +453,13 @@ int mdgemm_split(int64_t rows, int64_t cols, int limbs, int slices, int axis, co
   const size_t xbytes = sizeof(double) * limbs * static_cast<size_t>(rows) * static_cast<size_t>(cols);
   const size_t dbytes = sizeof(double) * slices * static_cast<size_t>(rows) * static_cast<size_t>(cols);
   if (overlaps(D, dbytes, X, xbytes)) return MDGEMM_EINVAL;
-  return hip_status(
-      mdg::launch_split(rows, cols, limbs, slices, axis, X, E, D, false, static_cast<hipStream_t>(stream)));
+  return hip_status(mdg::launch_split(rows, cols, limbs, slices, slice_bits, axis, X, E, D, false,
+                                       static_cast<hipStream_t>(stream)));
 }
 
-int mdgemm_split_panel(int64_t rows, int64_t cols, int limbs, int slices, int axis, const double* X,
-                       const int32_t* E, double* D, void* stream) {
-  if (rows < 0 || cols < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || slices < 1 || slices > MDGEMM_MAX_SLICES ||
+int mdgemm_split_panel(int64_t rows, int64_t cols, int limbs, int slices, int slice_bits, int axis,
+                       const double* X, const int32_t* E, double* D, void* stream) {
+  if (rows < 0 || cols < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || !width_ok(slices, slice_bits) ||
       (axis != 0 && axis != 1))
     return MDGEMM_EINVAL;
   if (rows == 0 || cols == 0) return MDGEMM_OK;
@@ -410,14 +469,14 @@ int mdgemm_split_panel(int64_t rows, int64_t cols, int limbs, int slices, int ax
   const size_t dbytes = sizeof(double) * slices * static_cast<size_t>(mdg::panel_k(K)) *
                         static_cast<size_t>(mdg::panel_mn(Cn));
   if (overlaps(D, dbytes, X, xbytes)) return MDGEMM_EINVAL;
-  return hip_status(
-      mdg::launch_split(rows, cols, limbs, slices, axis, X, E, D, true, static_cast<hipStream_t>(stream)));
+  return hip_status(mdg::launch_split(rows, cols, limbs, slices, slice_bits, axis, X, E, D, true,
+                                       static_cast<hipStream_t>(stream)));
 }
 
-int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, int per_pair, const double* DAt,
-                      const double* DBp, double* out, void* stream) {
-  if (m < 0 || n < 0 || k < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || cutoff < 0 ||
-      cutoff > 2 * slices - 2)
+int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, int per_pair,
+                      const double* DAt, const double* DBp, double* out, void* stream) {
+  if (m < 0 || n < 0 || k < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || slice_bits < 1 ||
+      slice_bits > mdg::kMaxSliceBits || cutoff < 0 || cutoff > 2 * slices - 2)
     return MDGEMM_EINVAL;
   if (m == 0 || n == 0) return MDGEMM_OK;
   if (!out || (k > 0 && (!DAt || !DBp))) return MDGEMM_EINVAL;
@@ -429,7 +488,7 @@ int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, i
   if (k > 0 && (overlaps(out, obytes, DAt, sizeof(double) * slices * kp * static_cast<size_t>(mdg::panel_mn(m))) ||
                 overlaps(out, obytes, DBp, sizeof(double) * slices * kp * static_cast<size_t>(mdg::panel_mn(n)))))
     return MDGEMM_EINVAL;
-  if (!exact_ok(k, per_pair ? 1 : max_pairs(slices, cutoff))) return MDGEMM_EEXACT;
+  if (!exact_ok(k, per_pair ? 1 : max_pairs(slices, cutoff), slice_bits)) return MDGEMM_EEXACT;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (!per_pair) return hip_status(mdg::launch_slice_gemm(m, n, k, DAt, DBp, out, level_jobs(slices, cutoff), s));
   for (const JobTable& jt : pair_jobs(slices, cutoff))
@@ -437,24 +496,26 @@ int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int cutoff, i
   return MDGEMM_OK;
 }
 
-int mdgemm_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, void* stream) {
-  if (m < 0 || n < 0 || levels < 1 || levels > mdg::kMaxLevels) return MDGEMM_EINVAL;
+int mdgemm_accumulate(int64_t m, int64_t n, int levels, int slice_bits, const double* G, int64_t* Z, void* stream) {
+  if (m < 0 || n < 0 || slice_bits < 1 || slice_bits > mdg::kMaxSliceBits || !levels_ok(levels, slice_bits))
+    return MDGEMM_EINVAL;
   if (m == 0 || n == 0) return MDGEMM_OK;
   if (!G || !Z) return MDGEMM_EINVAL;
-  return hip_status(mdg::launch_accumulate(m, n, levels, G, Z, static_cast<hipStream_t>(stream)));
+  return hip_status(mdg::launch_accumulate(m, n, levels, slice_bits, G, Z, static_cast<hipStream_t>(stream)));
 }
 
-int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, const double* G, const int32_t* EA,
-                        const int32_t* EB, double* C, void* stream) {
-  if (m < 0 || n < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || levels < 1 || levels > mdg::kMaxLevels)
+int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, int slice_bits, const double* G,
+                        const int32_t* EA, const int32_t* EB, double* C, void* stream) {
+  if (m < 0 || n < 0 || limbs < 1 || limbs > MDGEMM_MAX_LIMBS || slice_bits < 1 || slice_bits > mdg::kMaxSliceBits ||
+      !levels_ok(levels, slice_bits))
     return MDGEMM_EINVAL;
   if (m == 0 || n == 0) return MDGEMM_OK;
   if (!G || !EA || !EB || !C) return MDGEMM_EINVAL;
   const size_t cbytes = sizeof(double) * limbs * static_cast<size_t>(m) * static_cast<size_t>(n);
   const size_t gbytes = sizeof(double) * levels * static_cast<size_t>(m) * static_cast<size_t>(n);
   if (overlaps(C, cbytes, G, gbytes)) return MDGEMM_EINVAL;
-  return hip_status(
-      mdg::launch_accum_renorm(m, n, limbs, levels, G, EA, EB, C, static_cast<hipStream_t>(stream)));
+  return hip_status(mdg::launch_accum_renorm(m, n, limbs, levels, slice_bits, G, EA, EB, C,
+                                             static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -14,6 +14,8 @@ constexpr int kMaxLimbs = 16;   // hexa double
 constexpr int kMaxLevels = 2 * kMaxSlices - 1;
 constexpr int kZWords = 28;     // 64-bit words of an exact level sum (13 (kMaxLevels - 1) + 55 bits)
 constexpr int kMaxJobs = 256;   // jobs of one level-GEMM launch (grid.y)
+constexpr int kMaxSliceBits = 26;                  // widest digit: products of two stay below 2^52
+constexpr int kMaxDigitBits = 64 * 14 - 52;  // w S + 52 <= 896: the split's integer fits 14 words
 constexpr int kTileMN = 128;  // level-GEMM tile rows / columns
 constexpr int kTileK = 16;    // level-GEMM k step
 
@@ -35,11 +37,11 @@ struct JobTable {
 // a1: per-row (axis 0) or per-column (axis 1) grid exponents of a [rows][cols] plane.
 hipError_t launch_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, hipStream_t stream);
 
-// a2: digits of X [L][rows][cols] on the grid exponents E, either row-major
+// a2: w-bit digits of X [L][rows][cols] on the grid exponents E, either row-major
 // D [S][rows][cols] (panel == false) or as a level-GEMM panel (panel == true):
 // axis 0: D [S][panel_k(cols)][panel_mn(rows)] (transposed), axis 1:
 // D [S][panel_k(rows)][panel_mn(cols)], zeros in the padding.
-hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E,
+hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
                         double* D, bool panel, hipStream_t stream);
 
 // a3: level or pair products of the panels DAt [S][panel_k(k)][panel_mn(m)] and
@@ -47,12 +49,17 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int axis, cons
 hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DAt, const double* DBp, double* out,
                              const JobTable& jobs, hipStream_t stream);
 
-// a4: exact accumulation of `levels` planes into kZWords-word integers Z [kZWords][m][n].
-hipError_t launch_accumulate(int64_t m, int64_t n, int levels, const double* G, int64_t* Z, hipStream_t stream);
+// a4: exact accumulation of `levels` planes of w-bit digit products (weights
+// 2^(-w t)) into kZWords-word integers Z [kZWords][m][n].
+hipError_t launch_accumulate(int64_t m, int64_t n, int levels, int w, const double* G, int64_t* Z,
+                             hipStream_t stream);
 
-// a4 + a5: exact accumulation and greedy rounding into L limbs, scaled by 2^(EA+EB-26).
-hipError_t launch_accum_renorm(int64_t m, int64_t n, int L, int levels, const double* G, const int32_t* EA,
+// a4 + a5: exact accumulation and greedy rounding into L limbs, scaled by 2^(EA+EB-2w).
+hipError_t launch_accum_renorm(int64_t m, int64_t n, int L, int levels, int w, const double* G, const int32_t* EA,
                                const int32_t* EB, double* C, hipStream_t stream);
+
+// 64-bit words of the exact sum of `levels` levels of w-bit digits (sign included).
+int accum_words(int levels, int w);
 
 // Utilities: fill `count` doubles with +0.0; zero/set a device flag; scan for inf/nan.
 hipError_t launch_zero_f64(double* p, int64_t count, hipStream_t stream);

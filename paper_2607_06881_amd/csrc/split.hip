@@ -8,10 +8,12 @@
 // signs so that both parts get the same sign.
 //
 // Here every element x (L limbs, exact value V) of a row of A or a column of B
-// is read on the grid of its line's exponent E with unit u = 2^(E - 13 S):
-//     D = floor(|V| / u),   digit_s = sign(V) * (13-bit field s of D),
-// which are the truncated 13-bit quarters of the exact value; a limb of
-// opposite sign lowers D by the floor, which is the borrow of section 3.
+// is read on the grid of its line's exponent E with unit u = 2^(E - w S):
+//     D = floor(|V| / u),   digit_s = sign(V) * (w-bit field s of D),
+// which for w = 13 are the truncated 13-bit quarters of the exact value; a limb
+// of opposite sign lowers D by the floor, which is the borrow of section 3.
+// Wider digits (w up to 26, the adaptive width) are the same cut with fewer,
+// longer fields; the level sums stay exact while pairs k (2^w - 1)^2 < 2^53.
 //
 // The floor is formed exactly in 64-bit integer words: |V| / u is accumulated
 // as a fixed-point integer with 52 fraction bits.  For a normalized multiple
@@ -59,19 +61,19 @@ __device__ inline void add_shifted(uint64_t (&acc)[NW], uint64_t M, int sh, bool
   }
 }
 
-// 13-bit field of the NW-word integer v starting at bit pos.
+// The `bits`-bit field (bits <= 26) of the NW-word integer v starting at bit pos.
 template <int NW>
-__device__ inline uint32_t field13(const uint64_t (&v)[NW], int pos) {
-  const int w = pos >> 6, b = pos & 63;
+__device__ inline uint32_t field(const uint64_t (&v)[NW], int pos, int bits) {
+  const int wi = pos >> 6, b = pos & 63;
   uint64_t lo = 0, hi = 0;
 #pragma unroll
   for (int i = 0; i < NW; ++i) {
-    lo = (i == w) ? v[i] : lo;
-    hi = (i == w + 1) ? v[i] : hi;
+    lo = (i == wi) ? v[i] : lo;
+    hi = (i == wi + 1) ? v[i] : hi;
   }
   uint64_t f = lo >> b;
-  if (b > 64 - kSliceBits) f |= hi << (64 - b);
-  return static_cast<uint32_t>(f) & kDigitMax;
+  if (b + bits > 64) f |= hi << (64 - b);
+  return static_cast<uint32_t>(f) & ((1u << bits) - 1u);
 }
 
 // D = floor(|V| / u) for one element with limbs xs[0..L-1] (L <= ML) on the
@@ -142,7 +144,7 @@ __device__ inline double signed_digit(uint32_t d, bool neg) {
 
 // Row-major output: D [S][rows][cols], the layout of the input planes.
 template <int NW, int ML>
-__global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, int L, int S, int axis,
+__global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, int L, int S, int w, int axis,
                                                     const double* __restrict__ X, const int32_t* __restrict__ E,
                                                     double* __restrict__ D) {
   const int64_t plane = rows * cols;
@@ -154,9 +156,9 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
     double xs[ML];
     load_limbs<ML>(X, plane, L, idx, xs);
     uint64_t I[NW];
-    const bool neg = floor_on_grid<NW, ML>(xs, L, e - kSliceBits * S, I);
+    const bool neg = floor_on_grid<NW, ML>(xs, L, e - w * S, I);
     for (int s = 0; s < S; ++s)
-      D[static_cast<int64_t>(s) * plane + idx] = signed_digit(field13<NW>(I, kSliceBits * (S - 1 - s)), neg);
+      D[static_cast<int64_t>(s) * plane + idx] = signed_digit(field<NW>(I, w * (S - 1 - s), w), neg);
   }
 }
 
@@ -167,7 +169,7 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
 // A block covers 64 lines (c) x 16 k: its reads of A touch 64 full 128-byte lines
 // and its stores are 512-byte rows of the panel.
 template <int NW, int ML>
-__global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t cols, int L, int S, int axis,
+__global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t cols, int L, int S, int w, int axis,
                                                           int64_t kp, int64_t cp, const double* __restrict__ X,
                                                           const int32_t* __restrict__ E, double* __restrict__ D) {
   const int64_t plane = rows * cols, pplane = kp * cp;
@@ -198,9 +200,9 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
         double* out = D + kk * cp + c;
         if (valid[b]) {
           uint64_t I[NW];
-          const bool neg = floor_on_grid<NW, ML>(xs[b], L, e - kSliceBits * S, I);
+          const bool neg = floor_on_grid<NW, ML>(xs[b], L, e - w * S, I);
           for (int s = 0; s < S; ++s)
-            out[static_cast<int64_t>(s) * pplane] = signed_digit(field13<NW>(I, kSliceBits * (S - 1 - s)), neg);
+            out[static_cast<int64_t>(s) * pplane] = signed_digit(field<NW>(I, w * (S - 1 - s), w), neg);
         } else {
           for (int s = 0; s < S; ++s) out[static_cast<int64_t>(s) * pplane] = 0.0;
         }
@@ -210,12 +212,13 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
 }
 
 template <int NW, int ML>
-hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E, double* D,
-                     bool panel, hipStream_t stream) {
+hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
+                     double* D, bool panel, hipStream_t stream) {
   if (!panel) {
     const unsigned gx = static_cast<unsigned>((cols + 255) / 256);
     const unsigned gy = static_cast<unsigned>(rows < 65535 ? rows : 65535);
-    hipLaunchKernelGGL((split_kernel<NW, ML>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, axis, X, E, D);
+    hipLaunchKernelGGL((split_kernel<NW, ML>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, w, axis, X, E,
+                       D);
     return hipGetLastError();
   }
   const int64_t K = axis == 0 ? cols : rows, Cn = axis == 0 ? rows : cols;
@@ -223,37 +226,37 @@ hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int axis, const d
   const unsigned gx = static_cast<unsigned>(cp / 64);
   const int64_t nkb = kp / 16;
   const unsigned gy = static_cast<unsigned>(nkb < 65535 ? nkb : 65535);
-  hipLaunchKernelGGL((split_panel_kernel<NW, ML>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, axis, kp, cp, X,
-                     E, D);
+  hipLaunchKernelGGL((split_panel_kernel<NW, ML>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, w, axis, kp,
+                     cp, X, E, D);
   return hipGetLastError();
 }
 
-// Word counts instantiated for S up to 64 digits (884 bits).
+// Word counts instantiated for w S up to 844 digit bits (896 bits).
 template <int ML>
-hipError_t split_words(int words, int64_t rows, int64_t cols, int L, int S, int axis, const double* X,
+hipError_t split_words(int words, int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
                        const int32_t* E, double* D, bool panel, hipStream_t stream) {
-  if (words <= 2) return launch_nw<2, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
-  if (words <= 3) return launch_nw<3, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
-  if (words <= 4) return launch_nw<4, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
-  if (words <= 5) return launch_nw<5, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
-  if (words <= 6) return launch_nw<6, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
-  if (words <= 8) return launch_nw<8, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
-  if (words <= 10) return launch_nw<10, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
-  if (words <= 14) return launch_nw<14, ML>(rows, cols, L, S, axis, X, E, D, panel, stream);
+  if (words <= 2) return launch_nw<2, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
+  if (words <= 3) return launch_nw<3, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
+  if (words <= 4) return launch_nw<4, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
+  if (words <= 5) return launch_nw<5, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
+  if (words <= 6) return launch_nw<6, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
+  if (words <= 8) return launch_nw<8, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
+  if (words <= 10) return launch_nw<10, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
+  if (words <= 14) return launch_nw<14, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int axis, const double* X, const int32_t* E,
+hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
                         double* D, bool panel, hipStream_t stream) {
   if (rows == 0 || cols == 0) return hipSuccess;
-  // The accumulator holds |V| / u < 2^(13 S) with 52 fraction bits: 13 S + 52 bits,
+  // The accumulator holds |V| / u < 2^(w S) with 52 fraction bits: w S + 52 bits,
   // in the next word count instantiated (extra words stay zero).
-  const int words = (kSliceBits * S + 52 + 63) / 64;
-  if (L <= 4) return split_words<4>(words, rows, cols, L, S, axis, X, E, D, panel, stream);
-  if (L <= 8) return split_words<8>(words, rows, cols, L, S, axis, X, E, D, panel, stream);
-  return split_words<16>(words, rows, cols, L, S, axis, X, E, D, panel, stream);
+  const int words = (w * S + 52 + 63) / 64;
+  if (L <= 4) return split_words<4>(words, rows, cols, L, S, w, axis, X, E, D, panel, stream);
+  if (L <= 8) return split_words<8>(words, rows, cols, L, S, w, axis, X, E, D, panel, stream);
+  return split_words<16>(words, rows, cols, L, S, w, axis, X, E, D, panel, stream);
 }
 
 }  // namespace mdg

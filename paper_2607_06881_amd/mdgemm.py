@@ -36,6 +36,9 @@ MDGEMM_MAX_LIMBS = 16
 MDGEMM_MAX_SLICES = 64
 MDGEMM_MAX_LEVELS = 127
 MDGEMM_SLICE_BITS = 13
+MDGEMM_MAX_SLICE_BITS = 26
+MDGEMM_MAX_DIGIT_BITS = 844
+MDGEMM_SLICE_BITS_AUTO = -1
 MDGEMM_Z_WORDS = 28
 PANEL_K = 16  # level-GEMM panels: k rounded up to 16,
 PANEL_MN = 128  # m and n rounded up to 128
@@ -50,6 +53,7 @@ def panel_mn(x: int) -> int:
 
 EXPORTED = (
     "mdgemm_opts_init",
+    "mdgemm_plan",
     "mdgemm",
     "mdgemm_workspace_bytes",
     "mdgemm_ex",
@@ -79,6 +83,8 @@ class mdgemm_opts(ctypes.Structure):
         ("slices_per_limb", ctypes.c_int),
         ("cutoff", ctypes.c_int),
         ("flags", ctypes.c_uint),
+        ("slice_bits", ctypes.c_int),
+        ("slices", ctypes.c_int),
     ]
 
 
@@ -97,6 +103,9 @@ def lib() -> ctypes.CDLL:
         L = ctypes.CDLL(LIB_PATH)
         L.mdgemm_opts_init.argtypes = [ctypes.POINTER(mdgemm_opts)]
         L.mdgemm_opts_init.restype = None
+        _ip = ctypes.POINTER(ctypes.c_int)
+        L.mdgemm_plan.argtypes = [_i64, _i64, _i64, ctypes.c_int, ctypes.POINTER(mdgemm_opts), _ip, _ip, _ip]
+        L.mdgemm_plan.restype = ctypes.c_int
         L.mdgemm.argtypes = [_i64, _i64, _i64, ctypes.c_int, _vp, _vp, _vp]
         L.mdgemm.restype = ctypes.c_int
         L.mdgemm_workspace_bytes.argtypes = [_i64, _i64, _i64, ctypes.c_int, ctypes.POINTER(mdgemm_opts)]
@@ -111,16 +120,16 @@ def lib() -> ctypes.CDLL:
         L.mdgemm_release.restype = None
         L.mdgemm_exponents.argtypes = [_i64, _i64, ctypes.c_int, _vp, _vp, _vp]
         L.mdgemm_exponents.restype = ctypes.c_int
-        L.mdgemm_split.argtypes = [_i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp]
+        _c = ctypes.c_int
+        L.mdgemm_split.argtypes = [_i64, _i64, _c, _c, _c, _c, _vp, _vp, _vp, _vp]
         L.mdgemm_split.restype = ctypes.c_int
-        L.mdgemm_split_panel.argtypes = [_i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp]
+        L.mdgemm_split_panel.argtypes = [_i64, _i64, _c, _c, _c, _c, _vp, _vp, _vp, _vp]
         L.mdgemm_split_panel.restype = ctypes.c_int
-        L.mdgemm_slice_gemm.argtypes = [_i64, _i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp,
-                                        _vp]
+        L.mdgemm_slice_gemm.argtypes = [_i64, _i64, _i64, _c, _c, _c, _c, _vp, _vp, _vp, _vp]
         L.mdgemm_slice_gemm.restype = ctypes.c_int
-        L.mdgemm_accumulate.argtypes = [_i64, _i64, ctypes.c_int, _vp, _vp, _vp]
+        L.mdgemm_accumulate.argtypes = [_i64, _i64, _c, _c, _vp, _vp, _vp]
         L.mdgemm_accumulate.restype = ctypes.c_int
-        L.mdgemm_accum_renorm.argtypes = [_i64, _i64, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp, _vp, _vp]
+        L.mdgemm_accum_renorm.argtypes = [_i64, _i64, _c, _c, _c, _vp, _vp, _vp, _vp, _vp]
         L.mdgemm_accum_renorm.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -157,12 +166,14 @@ def _stream(stream) -> int:
 
 
 def make_opts(*, slices_per_limb: int = 4, cutoff: int = MDGEMM_CUTOFF_DEFAULT, flags: int = 0, stream=None,
-              workspace: Optional[torch.Tensor] = None) -> mdgemm_opts:
+              workspace: Optional[torch.Tensor] = None, slice_bits: int = 0, slices: int = 0) -> mdgemm_opts:
     o = mdgemm_opts()
     lib().mdgemm_opts_init(ctypes.byref(o))
     o.slices_per_limb = slices_per_limb
     o.cutoff = cutoff
     o.flags = flags
+    o.slice_bits = slice_bits
+    o.slices = slices
     o.stream = _stream(stream)
     if workspace is not None:
         o.workspace = workspace.data_ptr()
@@ -171,17 +182,34 @@ def make_opts(*, slices_per_limb: int = 4, cutoff: int = MDGEMM_CUTOFF_DEFAULT, 
 
 
 def mdgemm_workspace_bytes(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
-                           cutoff: int = MDGEMM_CUTOFF_DEFAULT) -> int:
+                           cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0) -> int:
     o = mdgemm_opts()
     lib().mdgemm_opts_init(ctypes.byref(o))
     o.slices_per_limb = slices_per_limb
     o.cutoff = cutoff
+    o.slice_bits = slice_bits
+    o.slices = slices
     return int(lib().mdgemm_workspace_bytes(m, n, k, limbs, ctypes.byref(o)))
+
+
+def mdgemm_plan(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
+                cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0):
+    """(digit width w, digit count S, cutoff T) that mdgemm_ex uses for these options."""
+    o = mdgemm_opts()
+    lib().mdgemm_opts_init(ctypes.byref(o))
+    o.slices_per_limb = slices_per_limb
+    o.cutoff = cutoff
+    o.slice_bits = slice_bits
+    o.slices = slices
+    w, S, T = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _check(lib().mdgemm_plan(m, n, k, limbs, ctypes.byref(o), ctypes.byref(w), ctypes.byref(S), ctypes.byref(T)),
+           "mdgemm_plan")
+    return w.value, S.value, T.value
 
 
 def mdgemm_ex(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None, *, slices_per_limb: int = 4,
               cutoff: int = MDGEMM_CUTOFF_DEFAULT, flags: int = 0, workspace: Optional[torch.Tensor] = None,
-              stream=None) -> torch.Tensor:
+              stream=None, slice_bits: int = 0, slices: int = 0) -> torch.Tensor:
     """C = A.B for limb-major float64 tensors A [L, m, k] and B [L, k, n] on the GPU.
 
     The workspace is a torch uint8 tensor (allocated here when not given), so
@@ -199,11 +227,13 @@ def mdgemm_ex(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None
         if tuple(C.shape) != (L, m, n):
             raise ValueError("C has the wrong shape")
     if workspace is None:
-        need = mdgemm_workspace_bytes(m, n, k, L, slices_per_limb=slices_per_limb, cutoff=cutoff)
+        need = mdgemm_workspace_bytes(m, n, k, L, slices_per_limb=slices_per_limb, cutoff=cutoff,
+                                      slice_bits=slice_bits, slices=slices)
         if need == 2**64 - 1:
             _check(MDGEMM_EINVAL, "mdgemm_workspace_bytes")
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=A.device)
-    o = make_opts(slices_per_limb=slices_per_limb, cutoff=cutoff, flags=flags, stream=stream, workspace=workspace)
+    o = make_opts(slices_per_limb=slices_per_limb, cutoff=cutoff, flags=flags, stream=stream, workspace=workspace,
+                  slice_bits=slice_bits, slices=slices)
     _check(lib().mdgemm_ex(m, n, k, L, _ptr(A), _ptr(B), _ptr(C), ctypes.byref(o)), "mdgemm_ex")
     return C
 
@@ -244,20 +274,20 @@ def mdgemm_exponents(X0: torch.Tensor, axis: int, E: Optional[torch.Tensor] = No
 
 
 def mdgemm_split(X: torch.Tensor, E: torch.Tensor, slices: int, axis: int, D: Optional[torch.Tensor] = None,
-                 stream=None) -> torch.Tensor:
-    """Digits [slices, rows, cols] (float64) of X [L, rows, cols] on the grid exponents E."""
+                 stream=None, bits: int = MDGEMM_SLICE_BITS) -> torch.Tensor:
+    """Digits [slices, rows, cols] (float64) of `bits` bits of X [L, rows, cols] on the grid exponents E."""
     _dev_tensor(X, torch.float64, "X")
     _dev_tensor(E, torch.int32, "E")
     L, rows, cols = X.shape
     if D is None:
         D = torch.empty((slices, rows, cols), dtype=torch.float64, device=X.device)
-    _check(lib().mdgemm_split(rows, cols, L, slices, axis, _ptr(X), _ptr(E), _ptr(D), _stream(stream)),
+    _check(lib().mdgemm_split(rows, cols, L, slices, bits, axis, _ptr(X), _ptr(E), _ptr(D), _stream(stream)),
            "mdgemm_split")
     return D
 
 
 def mdgemm_split_panel(X: torch.Tensor, E: torch.Tensor, slices: int, axis: int, D: Optional[torch.Tensor] = None,
-                       stream=None) -> torch.Tensor:
+                       stream=None, bits: int = MDGEMM_SLICE_BITS) -> torch.Tensor:
     """Digits of X [L, rows, cols] as a level-GEMM panel: axis 0 (A):
     [slices, panel_k(cols), panel_mn(rows)] (transposed); axis 1 (B):
     [slices, panel_k(rows), panel_mn(cols)]; zero padding."""
@@ -267,13 +297,14 @@ def mdgemm_split_panel(X: torch.Tensor, E: torch.Tensor, slices: int, axis: int,
     shape = (slices, panel_k(cols), panel_mn(rows)) if axis == 0 else (slices, panel_k(rows), panel_mn(cols))
     if D is None:
         D = torch.empty(shape, dtype=torch.float64, device=X.device)
-    _check(lib().mdgemm_split_panel(rows, cols, L, slices, axis, _ptr(X), _ptr(E), _ptr(D), _stream(stream)),
-           "mdgemm_split_panel")
+    _check(lib().mdgemm_split_panel(rows, cols, L, slices, bits, axis, _ptr(X), _ptr(E), _ptr(D),
+                                    _stream(stream)), "mdgemm_split_panel")
     return D
 
 
 def mdgemm_slice_gemm(DAt: torch.Tensor, DBp: torch.Tensor, m: int, n: int, k: int, cutoff: int,
-                      per_pair: bool = False, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+                      per_pair: bool = False, out: Optional[torch.Tensor] = None, stream=None,
+                      bits: int = MDGEMM_SLICE_BITS) -> torch.Tensor:
     """Level products [cutoff+1, m, n] (or pair products [S, S, m, n]) of the digit
     panels DAt [S, panel_k(k), panel_mn(m)] and DBp [S, panel_k(k), panel_mn(n)]."""
     _dev_tensor(DAt, torch.float64, "DAt")
@@ -284,31 +315,33 @@ def mdgemm_slice_gemm(DAt: torch.Tensor, DBp: torch.Tensor, m: int, n: int, k: i
     if out is None:
         shape = (S, S, m, n) if per_pair else (cutoff + 1, m, n)
         out = torch.zeros(shape, dtype=torch.float64, device=DAt.device)
-    _check(lib().mdgemm_slice_gemm(m, n, k, S, cutoff, int(per_pair), _ptr(DAt), _ptr(DBp), _ptr(out),
+    _check(lib().mdgemm_slice_gemm(m, n, k, S, bits, cutoff, int(per_pair), _ptr(DAt), _ptr(DBp), _ptr(out),
                                    _stream(stream)), "mdgemm_slice_gemm")
     return out
 
 
-def mdgemm_accumulate(G: torch.Tensor, Z: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """Exact sums N = sum_t G_t 2^(13 (T - t)) as MDGEMM_Z_WORDS int64 words [MDGEMM_Z_WORDS, m, n],
-    least significant first."""
+def mdgemm_accumulate(G: torch.Tensor, Z: Optional[torch.Tensor] = None, stream=None,
+                      bits: int = MDGEMM_SLICE_BITS) -> torch.Tensor:
+    """Exact sums N = sum_t G_t 2^(w (T - t)), w = bits, as MDGEMM_Z_WORDS int64 words
+    [MDGEMM_Z_WORDS, m, n], least significant first."""
     _dev_tensor(G, torch.float64, "G")
     levels, m, n = G.shape
     if Z is None:
         Z = torch.empty((MDGEMM_Z_WORDS, m, n), dtype=torch.int64, device=G.device)
-    _check(lib().mdgemm_accumulate(m, n, levels, _ptr(G), _ptr(Z), _stream(stream)), "mdgemm_accumulate")
+    _check(lib().mdgemm_accumulate(m, n, levels, bits, _ptr(G), _ptr(Z), _stream(stream)), "mdgemm_accumulate")
     return Z
 
 
 def mdgemm_accum_renorm(G: torch.Tensor, EA: torch.Tensor, EB: torch.Tensor, limbs: int,
-                        C: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """C [limbs, m, n]: exact sum of the levels rounded greedily into limbs, scaled by 2^(EA+EB-26)."""
+                        C: Optional[torch.Tensor] = None, stream=None, bits: int = MDGEMM_SLICE_BITS) -> torch.Tensor:
+    """C [limbs, m, n]: exact sum of the levels (weights 2^(-w t), w = bits) rounded greedily
+    into limbs, scaled by 2^(EA+EB-2w)."""
     _dev_tensor(G, torch.float64, "G")
     _dev_tensor(EA, torch.int32, "EA")
     _dev_tensor(EB, torch.int32, "EB")
     levels, m, n = G.shape
     if C is None:
         C = torch.empty((limbs, m, n), dtype=torch.float64, device=G.device)
-    _check(lib().mdgemm_accum_renorm(m, n, limbs, levels, _ptr(G), _ptr(EA), _ptr(EB), _ptr(C), _stream(stream)),
-           "mdgemm_accum_renorm")
+    _check(lib().mdgemm_accum_renorm(m, n, limbs, levels, bits, _ptr(G), _ptr(EA), _ptr(EB), _ptr(C),
+                                     _stream(stream)), "mdgemm_accum_renorm")
     return C

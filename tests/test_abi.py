@@ -7,6 +7,7 @@ import re
 
 import pytest
 
+from oracle import exact
 from paper_2607_06881_amd import mdgemm as md
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -76,24 +77,34 @@ def test_invalid_arguments(lib):
     assert _ex(lib, 4, 4, 4, 2, C=None) == E
     # C overlapping A
     assert _ex(lib, 4, 4, 4, 2, C=FA + 8) == E
-    assert lib.mdgemm_split(4, 4, 2, md.MDGEMM_MAX_SLICES + 1, 0, FA, FB, FC, None) == E
-    assert lib.mdgemm_split(4, 4, md.MDGEMM_MAX_LIMBS + 1, 8, 0, FA, FB, FC, None) == E
-    assert lib.mdgemm_split(4, 4, 2, 8, 2, FA, FB, FC, None) == E
-    assert lib.mdgemm_split_panel(4, 4, 2, 0, 0, FA, FB, FC, None) == E
-    assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 7, 0, FA + 8, FB, FC, None) == E  # panels must be 16-byte aligned
-    assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 15, 0, FA, FB, FC, None) == E
-    assert lib.mdgemm_slice_gemm(4, 4, 4, md.MDGEMM_MAX_SLICES + 1, 7, 0, FA, FB, FC, None) == E
-    assert lib.mdgemm_accumulate(4, 4, md.MDGEMM_MAX_LEVELS + 1, FA, FC, None) == E
-    assert lib.mdgemm_accum_renorm(4, 4, md.MDGEMM_MAX_LIMBS + 1, 8, FA, FB, FB, FC, None) == E
-    assert lib.mdgemm_accum_renorm(4, 4, 2, md.MDGEMM_MAX_LEVELS + 1, FA, FB, FB, FC, None) == E
+    assert lib.mdgemm_split(4, 4, 2, md.MDGEMM_MAX_SLICES + 1, 13, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_split(4, 4, md.MDGEMM_MAX_LIMBS + 1, 8, 13, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_split(4, 4, 2, 8, 13, 2, FA, FB, FC, None) == E
+    assert lib.mdgemm_split(4, 4, 2, 8, 27, 0, FA, FB, FC, None) == E  # digits wider than 26 bits
+    assert lib.mdgemm_split(4, 4, 2, 8, 0, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_split(4, 4, 2, 33, 26, 0, FA, FB, FC, None) == E  # 33 x 26 > 844 digit bits
+    assert lib.mdgemm_split_panel(4, 4, 2, 0, 13, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 13, 7, 0, FA + 8, FB, FC, None) == E  # panels must be 16-byte aligned
+    assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 13, 15, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_slice_gemm(4, 4, 4, md.MDGEMM_MAX_SLICES + 1, 13, 7, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 27, 7, 0, FA, FB, FC, None) == E
+    assert lib.mdgemm_accumulate(4, 4, md.MDGEMM_MAX_LEVELS + 1, 13, FA, FC, None) == E
+    assert lib.mdgemm_accumulate(4, 4, 80, 26, FA, FC, None) == E  # 26 x 79 + 55 bits > 28 words
+    assert lib.mdgemm_accum_renorm(4, 4, md.MDGEMM_MAX_LIMBS + 1, 8, 13, FA, FB, FB, FC, None) == E
+    assert lib.mdgemm_accum_renorm(4, 4, 2, md.MDGEMM_MAX_LEVELS + 1, 13, FA, FB, FB, FC, None) == E
+    assert lib.mdgemm_accum_renorm(4, 4, 2, 8, 0, FA, FB, FB, FC, None) == E
+    assert _ex(lib, 4, 4, 4, 2, slice_bits=27) == E
+    assert _ex(lib, 4, 4, 4, 2, slice_bits=-2) == E
+    assert _ex(lib, 4, 4, 4, 2, slice_bits=md.MDGEMM_SLICE_BITS_AUTO, slices=6) == E
+    assert _ex(lib, 4, 4, 4, 16, slice_bits=23) == E  # S = ceil(832 / 23) = 37, 37 x 23 > 844
     assert lib.mdgemm_exponents(4, 4, 3, FA, FB, None) == E
 
 
 def test_empty_products_are_noops(lib):
     assert _ex(lib, 0, 5, 5, 2, A=None, B=None, C=None) == md.MDGEMM_OK
     assert _ex(lib, 5, 0, 5, 2, A=None, B=None, C=None) == md.MDGEMM_OK
-    assert lib.mdgemm_split(0, 5, 2, 8, 0, None, None, None, None) == md.MDGEMM_OK
-    assert lib.mdgemm_slice_gemm(0, 5, 5, 8, 7, 0, None, None, None, None) == md.MDGEMM_OK
+    assert lib.mdgemm_split(0, 5, 2, 8, 13, 0, None, None, None, None) == md.MDGEMM_OK
+    assert lib.mdgemm_slice_gemm(0, 5, 5, 8, 13, 7, 0, None, None, None, None) == md.MDGEMM_OK
     assert lib.mdgemm_exponents(0, 5, 0, None, None, None) == md.MDGEMM_OK
 
 
@@ -110,7 +121,7 @@ def test_exactness_bound(lib, limbs, cutoff, pairs):
     # at kmax the check passes and the call goes on to the workspace check
     assert _ex(lib, 4, 4, kmax, limbs, cutoff=cutoff, workspace=FC + (1 << 40),
                workspace_bytes=16) == md.MDGEMM_EWORKSPACE
-    assert lib.mdgemm_slice_gemm(4, 4, kmax + 1, 4 * limbs, cutoff if cutoff >= 0 else 4 * limbs - 1, 0, FA, FB, FC,
+    assert lib.mdgemm_slice_gemm(4, 4, kmax + 1, 4 * limbs, 13, cutoff if cutoff >= 0 else 4 * limbs - 1, 0, FA, FB, FC,
                                  None) == md.MDGEMM_EEXACT
 
 
@@ -142,3 +153,40 @@ def test_binding_refuses_cpu_tensors(lib):
         md.mdgemm_ex(A, A)
     with pytest.raises(TypeError):
         md.mdgemm_ex(A.float(), A.float())
+
+
+def test_plan_digit_width_and_count(lib):
+    auto = md.MDGEMM_SLICE_BITS_AUTO
+    # 13-bit digits: four per limb, or slices_per_limb, or an explicit count
+    assert md.mdgemm_plan(64, 64, 64, 2) == (13, 8, 7)
+    assert md.mdgemm_plan(64, 64, 64, 3, slices_per_limb=3, cutoff=-2) == (13, 9, 16)
+    assert md.mdgemm_plan(64, 64, 64, 2, slices=9, cutoff=4) == (13, 9, 4)
+    # explicit width: ceil(52 L / w) digits unless given
+    assert md.mdgemm_plan(64, 64, 64, 2, slice_bits=19) == (19, 6, 5)
+    assert md.mdgemm_plan(64, 64, 4, 4, slice_bits=21) == (21, 10, 9)
+    assert md.mdgemm_plan(64, 64, 64, 2, slice_bits=17, slices=5, cutoff=-2) == (17, 5, 8)
+    # the adaptive width at the workloads' k: closed forms worked by hand
+    assert md.mdgemm_plan(4096, 4096, 4096, 2, slice_bits=auto) == (19, 6, 5)  # 21 pairs instead of 36
+    assert md.mdgemm_plan(2048, 2048, 1024, 4, slice_bits=auto) == (19, 11, 10)  # 66 instead of 136
+    assert md.mdgemm_plan(8192, 8192, 512, 3, slice_bits=auto) == (20, 8, 7)  # 36 instead of 78
+    assert md.mdgemm_plan(128, 8192, 64, 16, slice_bits=auto) == (20, 42, 41)  # 903 instead of 2080
+    for L in (1, 2, 3, 4, 8, 16):
+        for k in (1, 7, 64, 512, 1000, 4096, 2**16, 2**20, 2**22):
+            want = exact.adaptive_width(L, k)
+            if want is None:
+                with pytest.raises(md.MdgemmError):
+                    md.mdgemm_plan(8, 8, k, L, slice_bits=auto)
+            else:
+                assert md.mdgemm_plan(8, 8, k, L, slice_bits=auto) == (*want, want[1] - 1), (L, k)
+
+
+def test_exactness_bound_wide_digits(lib):
+    # pairs * k * (2^w - 1)^2 < 2^53 with the width in the check
+    w, S = 19, 6
+    kmax = (2**53 - 1) // (S * (2**w - 1) ** 2)
+    assert md.mdgemm_plan(4, 4, kmax, 2, slice_bits=w) == (w, S, S - 1)
+    with pytest.raises(md.MdgemmError):
+        md.mdgemm_plan(4, 4, kmax + 1, 2, slice_bits=w)
+    assert lib.mdgemm_slice_gemm(4, 4, kmax + 1, S, w, S - 1, 0, FA, FB, FC, None) == md.MDGEMM_EEXACT
+    assert md.mdgemm_workspace_bytes(4096, 4096, 4096, 2, slice_bits=md.MDGEMM_SLICE_BITS_AUTO) < \
+        md.mdgemm_workspace_bytes(4096, 4096, 4096, 2)

@@ -123,3 +123,34 @@ def test_workload_full_size(name):
         worst = max(worst, float(err / bound))
     print(f"[result] {name}: max |C - C_exact| / bound over {min(len(entries), 40)} entries = {worst:.3e}",
           flush=True)
+
+
+@pytest.mark.parametrize("name", ["c2", "c3", "c4"])
+def test_workload_adaptive_width(name):
+    # The same workloads with the adaptive width: fewer, wider digits, sampled
+    # entries bit-exact against the oracle's chain at that width, within the
+    # stated tolerance.
+    w = workloads.WORKLOADS[name]
+    auto = md.MDGEMM_SLICE_BITS_AUTO
+    bits, S, T = md.mdgemm_plan(w.m, w.n, w.k, w.limbs, slice_bits=auto)
+    assert (bits, S) == exact.adaptive_width(w.limbs, w.k)
+    print(f"[case] workload {name} adaptive width: w={bits} S={S} T={T}", flush=True)
+    A_h, B_h = workloads.make_workload(w)
+    A, B = torch.from_numpy(A_h).to(DEV), torch.from_numpy(B_h).to(DEV)
+    ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, slice_bits=auto), dtype=torch.uint8,
+                     device=DEV)
+    C_h = md.mdgemm_ex(A, B, slice_bits=auto, workspace=ws).cpu().numpy()
+    del ws
+    assert _nonoverlap_all(C_h) and np.isfinite(C_h).all()
+    EA, EB = coracle.exponents(A_h[0], 0), coracle.exponents(B_h[0], 1)
+    entries = _sample_entries(EA, EB, 24, w.seed + 50)
+    ref = pipeline.reference_entries(A_h, B_h, S, T, entries, bits)
+    worst = 0.0
+    for (i, j), r in ref.items():
+        assert C_h[:, i, j].tolist() == r["limbs"], (i, j)
+        want, mag = exact.exact_product(A_h, B_h, i, j)
+        err = abs(exact.value(C_h[:, i, j]) - want)
+        bound = exact.tolerance(w.k, w.limbs, mag)
+        assert err <= bound, (i, j, float(err / bound))
+        worst = max(worst, float(err / bound))
+    print(f"[result] {name} adaptive width: max |C - C_exact| / bound = {worst:.3e}", flush=True)

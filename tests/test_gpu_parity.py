@@ -100,6 +100,26 @@ def test_split_random(L, S, rows, cols, axis):
     assert not np.signbit(pan[pan == 0]).any()
 
 
+@pytest.mark.parametrize("L,S,bits,rows,cols,axis", [(2, 6, 19, 65, 129, 0), (4, 11, 19, 40, 300, 1),
+                                                      (16, 42, 20, 20, 33, 1), (1, 2, 26, 33, 70, 0),
+                                                      (3, 8, 20, 130, 17, 1), (8, 21, 20, 9, 129, 0),
+                                                      (2, 5, 22, 129, 16, 0), (16, 64, 13, 5, 7, 1)])
+def test_split_wide_digits(L, S, bits, rows, cols, axis):
+    print(f"[case] split L={L} S={S} bits={bits} {rows}x{cols} axis={axis}", flush=True)
+    rng = np.random.default_rng(L * 100 + S + bits)
+    X = workloads.make_operand(rng, L, rows, cols, "normal", elem_exp=12,
+                               row_exp=20 if axis == 0 else 0, col_exp=20 if axis == 1 else 0)
+    X[:, rng.random((rows, cols)) < 0.05] = 0.0
+    E = coracle.exponents(X[0], axis)
+    Xg, Eg = _gpu(X), _gpu(E)
+    want = coracle.split(X, E, S, axis, bits)
+    got = _host(md.mdgemm_split(Xg, Eg, S, axis, bits=bits))
+    assert np.array_equal(got, want)
+    assert not np.signbit(got[got == 0]).any()
+    pan = _host(md.mdgemm_split_panel(Xg, Eg, S, axis, bits=bits))
+    assert np.array_equal(pan, _panel(want, axis))
+
+
 def _adversarial_elements(L, count, seed):
     """Multiple doubles with opposite-signed limbs, half-ulp tails, gaps,
     exact zeros below nonzeros, powers of two and subnormal tails."""
@@ -181,6 +201,23 @@ def test_levels(S, T, m, k, n):
     assert np.array_equal(got, want.astype(np.float64))
 
 
+@pytest.mark.parametrize("S,T,bits,m,k,n", [(6, 5, 19, 130, 40, 129), (2, 0, 26, 65, 1, 70), (5, 4, 22, 33, 64, 257),
+                                            (11, 10, 19, 40, 100, 45), (42, 41, 20, 20, 9, 130), (8, 14, 20, 17, 64, 17)])
+def test_levels_wide_digits(S, T, bits, m, k, n):
+    # digits up to 2^w - 1 at the largest k the exactness condition allows nearby
+    print(f"[case] levels S={S} T={T} bits={bits} {m}x{k}x{n}", flush=True)
+    assert min(S, T + 1) * k * (2**bits - 1) ** 2 < 2**53
+    rng = np.random.default_rng(S * 1000 + bits)
+    top = 2**bits
+    DA = rng.integers(-top + 1, top, (S, m, k)).astype(np.float64)
+    DB = rng.integers(-top + 1, top, (S, k, n)).astype(np.float64)
+    DA[:, 0, :] = top - 1  # largest digits
+    DB[:, :, 0] = -(top - 1)
+    got = _host(md.mdgemm_slice_gemm(_gpu(_panel(DA, 0)), _gpu(_panel(DB, 1)), m, n, k, T, bits=bits))
+    want = coracle.levels(DA, DB, T)
+    assert np.array_equal(got, want.astype(np.float64))
+
+
 @pytest.mark.parametrize("S,T", [(8, 14), (8, 7), (4, 2), (32, 31), (24, 46)])
 def test_pair_products(S, T):
     print(f"[case] pairs S={S} T={T}", flush=True)
@@ -245,6 +282,23 @@ def test_accumulate_exact(levels):
             assert _words_to_int(Z[:, i, j]) == want, (i, j)
 
 
+@pytest.mark.parametrize("levels,bits", [(6, 19), (3, 26), (83, 20), (100, 14), (11, 19), (1, 22)])
+def test_accumulate_wide_digits(levels, bits):
+    print(f"[case] accumulate levels={levels} bits={bits}", flush=True)
+    rng = np.random.default_rng(levels + 1000 * bits)
+    m, n = 7, 200
+    G = rng.integers(-(2**53) + 1, 2**53, (levels, m, n)).astype(np.float64)
+    G[:, 0, :] = 2.0**53 - 1
+    G[:, 1, :] = -(2.0**53 - 1)
+    G[:, 2, :] = 0.0
+    Z = _host(md.mdgemm_accumulate(_gpu(G), bits=bits))
+    T = levels - 1
+    for i in range(m):
+        for j in range(0, n, 7):
+            want = sum(int(G[t, i, j]) << (bits * (T - t)) for t in range(levels))
+            assert _words_to_int(Z[:, i, j]) == want, (i, j)
+
+
 def _cases_for_rounding(levels, m, n, seed):
     rng = np.random.default_rng(seed)
     G = np.zeros((levels, m, n))
@@ -289,6 +343,22 @@ def test_accum_renorm_greedy_rounding(L, levels):
             z = exact.accumulate([int(g) for g in G[:, i, j]], int(EA[i]), int(EB[j]))
             want = exact.round_to_limbs(z, L)
             assert C[:, i, j].tolist() == want, (i, j, G[:, i, j])
+            assert not any(v == 0 and math.copysign(1, v) < 0 for v in C[:, i, j])
+
+
+@pytest.mark.parametrize("L,levels,bits", [(2, 6, 19), (4, 11, 19), (16, 42, 20), (3, 8, 20), (1, 2, 26), (8, 21, 20)])
+def test_accum_renorm_wide_digits(L, levels, bits):
+    print(f"[case] accum_renorm L={L} levels={levels} bits={bits}", flush=True)
+    m, n = 13, 71
+    G = _cases_for_rounding(levels, m, n, 10 * L + levels + bits)
+    rng = np.random.default_rng(levels + bits)
+    EA = rng.integers(-40, 40, m).astype(np.int32)
+    EB = rng.integers(-40, 40, n).astype(np.int32)
+    C = _host(md.mdgemm_accum_renorm(_gpu(G), _gpu(EA), _gpu(EB), L, bits=bits))
+    for i in range(m):
+        for j in range(n):
+            z = exact.accumulate([int(g) for g in G[:, i, j]], int(EA[i]), int(EB[j]), bits)
+            assert C[:, i, j].tolist() == exact.round_to_limbs(z, L), (i, j)
             assert not any(v == 0 and math.copysign(1, v) < 0 for v in C[:, i, j])
 
 
@@ -431,3 +501,34 @@ def test_mdgemm_graph_capture_replays():
         g.replay()
         torch.cuda.synchronize()
         assert np.array_equal(C.cpu().numpy(), want), r
+
+
+@pytest.mark.parametrize("L,m,k,n,seed", [(2, 130, 64, 129, 20), (4, 33, 64, 45, 21), (3, 40, 100, 70, 22),
+                                          (16, 20, 17, 130, 23), (8, 9, 40, 5, 24), (1, 65, 200, 17, 25),
+                                          (2, 1, 1, 1, 26)])
+def test_mdgemm_adaptive_width_end_to_end(L, m, k, n, seed):
+    auto = md.MDGEMM_SLICE_BITS_AUTO
+    w, S, T = md.mdgemm_plan(m, n, k, L, slice_bits=auto)
+    assert (w, S) == exact.adaptive_width(L, k) and T == S - 1
+    print(f"[case] mdgemm auto width L={L} {m}x{k}x{n}: w={w} S={S}", flush=True)
+    A, B = _operands(L, m, k, n, seed, base="normal", row_exp=15, col_exp=15)
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), slice_bits=auto))
+    ref = pipeline.full_reference(A, B, S, T, w)
+    assert np.array_equal(C, ref["C"])
+    for i in range(0, m, max(1, m // 3)):
+        for j in range(0, n, max(1, n // 3)):
+            want, mag = exact.exact_product(A, B, i, j)
+            err = abs(exact.value(C[:, i, j]) - want)
+            bound = exact.tolerance(k, L, mag) if L <= 4 else \
+                exact.method_bound(A, B, i, j, S, T, int(ref["EA"][i]), int(ref["EB"][j]), w)
+            assert err <= bound, (i, j)
+
+
+@pytest.mark.parametrize("L,bits,slices,cutoff", [(2, 17, 0, -2), (3, 22, 8, -1), (2, 20, 6, 3), (4, 13, 12, -1)])
+def test_mdgemm_explicit_width_end_to_end(L, bits, slices, cutoff):
+    m, k, n = 70, 20, 65
+    w, S, T = md.mdgemm_plan(m, n, k, L, slice_bits=bits, slices=slices, cutoff=cutoff)
+    print(f"[case] mdgemm width {w} S={S} T={T} L={L}", flush=True)
+    A, B = _operands(L, m, k, n, 30 + bits, base="normal", row_exp=5, col_exp=5)
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), slice_bits=bits, slices=slices, cutoff=cutoff))
+    assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])

@@ -108,14 +108,14 @@ def test_borrow_vectors(case):
     assert dc == want
 
 
-def _schoolbook_digits(limbs, E, S):
-    """Base-2^13 digits by repeated multiplication (an independent algorithm)."""
+def _schoolbook_digits(limbs, E, S, base=8192):
+    """Base-2^13 (or `base`) digits by repeated multiplication (an independent algorithm)."""
     v = sum(Fraction(x) for x in limbs)
     sign = 1 if v >= 0 else -1
     r = abs(v) / Fraction(2) ** E
     out = []
     for _ in range(S):
-        r *= 8192
+        r *= base
         d = math.floor(r)
         out.append(sign * d if d else 0)
         r -= d
@@ -163,6 +163,26 @@ def test_split_invariants_and_brute_force(L):
         X = np.array(limbs).reshape(L, 1, 1)
         dc = coracle.split(X, np.array([E]), S, 0).ravel().astype(np.int64).tolist()
         assert dc == d, (limbs, E, S)
+
+
+@pytest.mark.parametrize("L", [1, 2, 4, 8, 16])
+def test_split_wide_digits(L):
+    # The adaptive width cuts the same value into fewer, wider fields: the same
+    # invariants, and the digits of repeated multiplication by 2^w.
+    rng = random.Random(777 + L)
+    for trial in range(150 if L <= 4 else 40):
+        limbs = _random_md(rng, L)
+        E = exact.frexp_exp(limbs[0]) + rng.choice([0, 0, 1, 5])
+        bits = rng.randint(14, 26)
+        S = rng.randint(1, min(64, 844 // bits))
+        d, R = exact.split_element(limbs, E, S, bits)
+        v = exact.value(limbs)
+        assert sum(di * exact.grid_unit(E, s, bits) for s, di in enumerate(d)) + R == v
+        assert abs(R) < exact.grid_unit(E, S - 1, bits) and R * v >= 0
+        assert all(abs(di) < 2**bits and di * v >= 0 for di in d)
+        assert d == _schoolbook_digits(limbs, E, S, 2**bits), (limbs, E, S, bits)
+        X = np.array(limbs).reshape(L, 1, 1)
+        assert coracle.split(X, np.array([E]), S, 0, bits).ravel().astype(np.int64).tolist() == d
 
 
 def test_split_full_coverage_has_zero_residual():
@@ -269,9 +289,10 @@ def test_levels_against_float_matmul_and_per_pair():
         assert np.array_equal(G[t], acc.astype(np.int64))
 
 
-def test_all_pairs_identity_with_truncated_operands():
+@pytest.mark.parametrize("bits", [13, 19, 24])
+def test_all_pairs_identity_with_truncated_operands(bits):
     # With every pair kept (T = 2S - 2), the weighted levels are exactly the
-    # product of the truncated operands: sum_t G_t 2^(EA+EB-26-13t) = sum_k tr(a) tr(b).
+    # product of the truncated operands: sum_t G_t 2^(EA+EB-2w-wt) = sum_k tr(a) tr(b).
     for seed in range(3):
         rng = np.random.default_rng(seed)
         L, m, k, n = 2, 4, 5, 3
@@ -279,15 +300,15 @@ def test_all_pairs_identity_with_truncated_operands():
         B = workloads.make_operand(rng, L, k, n, col_exp=9)
         S = int(rng.integers(2, 9))
         T = 2 * S - 2
-        ref = pipeline.full_reference(A, B, S, T)
+        ref = pipeline.full_reference(A, B, S, T, bits)
         for i in range(m):
             for j in range(n):
                 z = exact.accumulate([int(ref["G"][t, i, j]) for t in range(T + 1)],
-                                     int(ref["EA"][i]), int(ref["EB"][j]))
+                                     int(ref["EA"][i]), int(ref["EB"][j]), bits)
                 want = Fraction(0)
                 for kk in range(k):
-                    da, ra = exact.split_element(A[:, i, kk], int(ref["EA"][i]), S)
-                    db, rb = exact.split_element(B[:, kk, j], int(ref["EB"][j]), S)
+                    da, ra = exact.split_element(A[:, i, kk], int(ref["EA"][i]), S, bits)
+                    db, rb = exact.split_element(B[:, kk, j], int(ref["EB"][j]), S, bits)
                     want += (exact.value(A[:, i, kk]) - ra) * (exact.value(B[:, kk, j]) - rb)
                 assert z == want
 
@@ -469,6 +490,52 @@ def test_sliced_chain_within_method_bound(L, S, T, k):
             assert err <= bound, (i, j, float(err / bound))
             # not vacuous: far below the magnitude, at the scale of 2^-13S per unit of the grid
             assert bound < mag * Fraction(2) ** (-13 * min(S, T + 1) + 30)
+
+
+@pytest.mark.parametrize("L,k", [(1, 64), (2, 64), (3, 100), (4, 64), (2, 4096)])
+def test_adaptive_width_chain_within_tolerance(L, k):
+    # Fewer, wider digits at the adaptive width keep at least the digit bits of
+    # four 13-bit digits per limb, so the stated tolerance still holds.
+    w, S = exact.adaptive_width(L, k)
+    assert w * S >= 52 * L and S * k * (2**w - 1) ** 2 < 2**53
+    T = S - 1
+    rng = np.random.default_rng(400 + L + k)
+    m, n = 2, 2
+    A = workloads.make_operand(rng, L, m, k, base="normal", row_exp=10)
+    B = workloads.make_operand(rng, L, k, n, base="normal", col_exp=10)
+    ref = pipeline.full_reference(A, B, S, T, w)
+    for i in range(m):
+        for j in range(n):
+            got = ref["C"][:, i, j]
+            assert exact.is_nonoverlapping(got)
+            want, mag = exact.exact_product(A, B, i, j)
+            err = abs(exact.value(got) - want)
+            assert err <= exact.tolerance(k, L, mag), (i, j)
+            assert err <= exact.method_bound(A, B, i, j, S, T, int(ref["EA"][i]), int(ref["EB"][j]), w)
+
+
+def test_adaptive_width_closed_forms():
+    # worked by hand from S k (2^w - 1)^2 < 2^53 and S = ceil(52 L / w)
+    assert exact.adaptive_width(2, 4096) == (19, 6)   # 21 pairs instead of 36
+    assert exact.adaptive_width(4, 1024) == (19, 11)  # 66 instead of 136
+    assert exact.adaptive_width(3, 512) == (20, 8)    # 36 instead of 78
+    assert exact.adaptive_width(2, 64) == (22, 5)     # 15 instead of 36
+    assert exact.adaptive_width(2, 2**26) is None     # 8 k 8191^2 >= 2^53: no width stays exact
+    assert exact.adaptive_width(2, 2**22) == (14, 8)  # 8 k (2^14 - 1)^2 < 2^53 <= 7 k (2^15 - 1)^2;
+    # at equal pair counts the wider digit is taken
+
+
+def test_wrong_level_weight_for_wide_digits_is_caught():
+    # Planted: 19-bit digits accumulated with the 13-bit weights.
+    L, k = 2, 64
+    rng = np.random.default_rng(9)
+    A = workloads.make_operand(rng, L, 1, k, base="normal")
+    B = workloads.make_operand(rng, L, k, 1, base="normal")
+    ref = pipeline.full_reference(A, B, 6, 5, 19)
+    G = [int(ref["G"][t, 0, 0]) for t in range(6)]
+    bad = exact.accumulate(G, int(ref["EA"][0]), int(ref["EB"][0]), 13)
+    want, mag = exact.exact_product(A, B, 0, 0)
+    assert abs(bad - want) > exact.tolerance(k, L, mag)
 
 
 def test_method_bound_catches_a_dropped_kept_pair():
