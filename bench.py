@@ -14,6 +14,10 @@ Prints one JSON line:
   summary of this kernel and workload, or null when the kernel source changed
   after the counters were taken;
 * ``stages``: every stage's average time and algorithmic rate;
+* ``adaptive_width``: the same workload with the adaptive digit width (fewer,
+  wider digits whose level sums stay exact at this k; at least the digit bits of
+  four 13-bit digits per limb), timed over a few steps; the headline ``value``
+  keeps the workload's 13-bit digits unless ``--slice-bits`` says otherwise;
 * ``cpu_baseline``: the CPU oracle's classic multiple-double GEMM (one
   sequential inner product per element, all host cores) timed on a bounded
   sample of the same product's rows.
@@ -110,6 +114,11 @@ def main(argv=None) -> int:
     ap.add_argument("--config", default=DEFAULT_CONFIG, help="workload c0..c6 (default c2)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--slice-bits", default="13",
+                    help="digit width of the timed product: 13 (the workload's digits and cutoff, default), "
+                         "'auto' (the adaptive width) or 14..26")
+    ap.add_argument("--adaptive-steps", type=int, default=5,
+                    help="steps of an extra adaptive-width measurement reported beside the 13-bit one (0: none)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, run 3 device copies of this many MiB (calibrates the HBM byte "
                          "counters of a profiler run against a known size)")
@@ -134,28 +143,39 @@ def main(argv=None) -> int:
     A = torch.from_numpy(A_h).to(dev)
     B = torch.from_numpy(B_h).to(dev)
     C = torch.empty((w.limbs, w.m, w.n), dtype=torch.float64, device=dev)
-    spl = w.slices // w.limbs
-    ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, slices_per_limb=spl, cutoff=w.cutoff),
-                     dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
-    def step(flags=0):
-        md.mdgemm_ex(A, B, C, slices_per_limb=spl, cutoff=w.cutoff, workspace=ws, flags=flags, stream=stream)
+    def mode_opts(slice_bits):
+        """Options of one digit mode: the workload's 13-bit digits and cutoff, or a width."""
+        if slice_bits == 13:
+            return {"slices_per_limb": w.slices // w.limbs, "cutoff": w.cutoff}
+        return {"slice_bits": slice_bits}
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    def measure(opts, steps, warmup):
+        """ms per step and per-stage ms of mdgemm_ex with these options."""
+        ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, **opts), dtype=torch.uint8, device=dev)
 
-    stage_sum = np.zeros(4)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.steps):
-        step(md.MDGEMM_TIME_STAGES)
-        stage_sum += np.array(md.mdgemm_stage_times())  # waits for this step's last event
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = e0.elapsed_time(e1) / args.steps
-    stage_ms = stage_sum / args.steps
+        def step(flags=0):
+            md.mdgemm_ex(A, B, C, workspace=ws, flags=flags, stream=stream, **opts)
+
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        stage_sum = np.zeros(4)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            step(md.MDGEMM_TIME_STAGES)
+            stage_sum += np.array(md.mdgemm_stage_times())  # waits for this step's last event
+        e1.record(stream)
+        torch.cuda.synchronize()
+        del ws
+        return e0.elapsed_time(e1) / steps, stage_sum / steps
+
+    bits_arg = md.MDGEMM_SLICE_BITS_AUTO if args.slice_bits == "auto" else int(args.slice_bits)
+    opts = mode_opts(bits_arg)
+    bits, S, T = md.mdgemm_plan(w.m, w.n, w.k, w.limbs, **opts)
+    ms_per_step, stage_ms = measure(opts, args.steps, args.warmup)
 
     if args.copy_probe_mib > 0:
         src = torch.ones(args.copy_probe_mib * (1 << 20) // 8, dtype=torch.float64, device=dev)
@@ -165,11 +185,12 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         del src, dst
 
+    m, n, k, L = w.m, w.n, w.k, w.limbs
+    pairs = workloads.pair_count(S, T)
     md_flops = w.md_flops()
-    slice_flops = w.slice_flops()
+    slice_flops = 2.0 * m * n * k * pairs
     value = md_flops / (ms_per_step * 1e-3) / 1e9
 
-    m, n, k, L, S, T = w.m, w.n, w.k, w.limbs, w.slices, w.cutoff
     bytes_exp = 8.0 * (m * k + k * n) + 4.0 * (m + n)
     bytes_split = 8.0 * L * (m * k + k * n) + 8.0 * S * (m * k + k * n) + 4.0 * (m + n)
     bytes_acc = 8.0 * (T + 1) * m * n + 8.0 * L * m * n + 4.0 * (m + n)
@@ -181,7 +202,8 @@ def main(argv=None) -> int:
         "peak": MFMA_F64_PEAK_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(achieved / MFMA_F64_PEAK_TFLOPS, 4),
-        "traffic": stored_traffic(args.config),
+        # the stored counters were taken with the workload's 13-bit digits
+        "traffic": stored_traffic(args.config) if bits_arg == 13 else None,
         "kernel": "slice_gemm_kernel (level GEMMs, v_mfma_f64_16x16x4f64)",
         "flops_per_launch": slice_flops,
         "avg_launch_ms": round(gemm_ms, 4),
@@ -196,6 +218,11 @@ def main(argv=None) -> int:
                          "bytes": bytes_acc},
         "hbm_peak_GB/s": HBM_PEAK_GBS,
     }
+    config = {"workload": f"{w.name}: {w.description}", "m": m, "n": n, "k": k, "limbs": L, "slices": S,
+              "cutoff": T, "pairs": pairs, "seed": w.seed}
+    if bits != 13:
+        config["slice_bits"] = bits
+        config["workload"] += f"; adaptive width: {S} digits of {bits} bits, pairs p+q <= {T}"
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -209,14 +236,23 @@ def main(argv=None) -> int:
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic",
-        "config": {
-            "workload": f"{w.name}: {w.description}",
-            "m": m, "n": n, "k": k, "limbs": L, "slices": S, "cutoff": T, "pairs": w.pairs, "seed": w.seed,
-        },
+        "config": config,
         "roofline": roofline,
         "stages": stages,
         "slice_gemm_share": round(stage_ms[2] / stage_ms.sum(), 4),
     }
+    if bits_arg == 13 and args.adaptive_steps > 0:
+        # the same workload with the adaptive width, reported beside the 13-bit digits
+        a_opts = mode_opts(md.MDGEMM_SLICE_BITS_AUTO)
+        a_bits, a_S, a_T = md.mdgemm_plan(m, n, k, L, **a_opts)
+        a_ms, a_stage = measure(a_opts, args.adaptive_steps, 2)
+        a_pairs = workloads.pair_count(a_S, a_T)
+        a_tflops = 2.0 * m * n * k * a_pairs / (a_stage[2] * 1e-3) / 1e12
+        out["adaptive_width"] = {
+            "slice_bits": a_bits, "slices": a_S, "cutoff": a_T, "pairs": a_pairs, "steps": args.adaptive_steps,
+            "ms_per_step": round(a_ms, 4), "value": round(md_flops / (a_ms * 1e-3) / 1e9, 3),
+            "slice_gemm_TFLOP/s": round(a_tflops, 3), "frac": round(a_tflops / MFMA_F64_PEAK_TFLOPS, 4),
+        }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, A_h, B_h, args.cpu_seconds)
     print(json.dumps(out), flush=True)
