@@ -84,6 +84,7 @@ typedef struct mdgemm_opts {
   unsigned flags;         /* MDGEMM_CHECK_FINITE | MDGEMM_SYNC | MDGEMM_TIME_STAGES */
   int slice_bits;         /* digit width w: 0 = 13 (section 2), 1..26, or MDGEMM_SLICE_BITS_AUTO */
   int slices;             /* digits per element S; 0 = derived (see below) */
+  int range_bits;         /* range balancing: full precision down to 2^-range_bits of the line; 0 = off */
 } mdgemm_opts;
 
 /* Digit width and count.
@@ -91,15 +92,25 @@ typedef struct mdgemm_opts {
  *  - slice_bits 1..26 (the adaptive width, wider digits and fewer of them): S =
  *    slices, else ceil(52 limbs / w), the digit bits of four 13-bit digits per limb.
  *  - MDGEMM_SLICE_BITS_AUTO (slices must be 0): among w = 13..26 with
- *    S = ceil(52 limbs / w) and S k (2^w - 1)^2 < 2^53 (every level with T <= S - 1
- *    stays exact), the one with the fewest pairs S (S + 1) / 2, the wider on a tie;
- *    MDGEMM_EEXACT when none qualifies.  Double-double at k = 4096 gets w = 19,
+ *    S = ceil(52 limbs / w) and the requested cutoff (T = S - 1 by default), those
+ *    whose levels stay exact (max pairs of a level times k (2^w - 1)^2 < 2^53), the
+ *    one with the fewest pairs, the wider on a tie; MDGEMM_EEXACT when none
+ *    qualifies.  Double-double at k = 4096 gets w = 19,
  *    S = 6 (21 pairs instead of 36); the digits cover at least as many bits as
  *    four 13-bit digits per limb, so the product is at least as accurate.
+ * Range balancing (section 3, grouping by exponent so that smaller numbers keep
+ * their bits): with range_bits > 0 every line keeps its one grid and gets
+ * D = ceil(range_bits / w) more digits, S = S0 + D where S0 is the count above,
+ * and the default cutoff becomes T = S0 - 1 + 2D.  An element whose exponent is
+ * at most range_bits below its line's exponent then keeps S0 digits of its own,
+ * and the product of two such elements keeps its levels down to S0 - 1 below
+ * its own leading level.  With MDGEMM_SLICE_BITS_AUTO the width is chosen for the
+ * fewest pairs of (S, T) including D.  mdgemm_line_spread measures the range of
+ * the data.
  * In every case S <= 64 and S w <= MDGEMM_MAX_DIGIT_BITS. */
 
 /* Fill `opts` with the defaults: default stream, library workspace, 4 slices per
- * limb of 13 bits, cutoff T = S - 1, no flags. */
+ * limb of 13 bits, cutoff T = S - 1, no range balancing, no flags. */
 void mdgemm_opts_init(mdgemm_opts* opts);
 
 /* The digit width, digit count and cutoff mdgemm_ex uses for this product and
@@ -150,6 +161,14 @@ void mdgemm_release(void);
  * E = the largest frexp exponent (x = f 2^E, 1/2 <= |f| < 1) of a nonzero entry of
  * the line; 0 for an all-zero line.  Subnormals get their true exponent. */
 int mdgemm_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, void* stream);
+
+/* The exponent range of every line, for choosing mdgemm_opts.range_bits (section
+ * 3: the exponents a group of numbers spans).  E as mdgemm_exponents; spread[line]
+ * = E[line] - the smallest frexp exponent of a nonzero entry of the line, 0 for an
+ * all-zero line.  E and spread have `rows` (axis 0) or `cols` (axis 1) entries
+ * and must not overlap. */
+int mdgemm_line_spread(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, int32_t* spread,
+                       void* stream);
 
 /* Step a2, the exact split (section 2 worked example; sections 2-3 balancing and
  * the opposite-sign transfer).  X [limbs][rows][cols], E from mdgemm_exponents

@@ -236,6 +236,83 @@ def adaptive_width(L: int, k: int, max_digit_bits: int = 844):
     return None if best is None else (best[1], best[2])
 
 
+def line_spread(X0: np.ndarray, axis: int) -> np.ndarray:
+    """Exponent range of every row (axis 0) or column (axis 1) of a leading-limb
+    plane: the line's grid exponent minus the smallest frexp exponent of a nonzero
+    entry (section 3: the exponents a group of numbers spans); 0 for a zero line."""
+    X0 = np.asarray(X0, dtype=np.float64)
+    lines = X0 if axis == 0 else X0.T
+    out = np.zeros(lines.shape[0], dtype=np.int64)
+    for i, line in enumerate(lines):
+        exps = [frexp_exp(float(x)) for x in line if x != 0.0]
+        if exps:
+            out[i] = max(exps) - min(exps)
+    return out
+
+
+def _pair_count(S: int, T: int) -> int:
+    return sum(len(pairs_of_level(t, S)) for t in range(T + 1))
+
+
+def _max_pairs(S: int, T: int) -> int:
+    return max(len(pairs_of_level(t, S)) for t in range(T + 1))
+
+
+def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_limb: int = 4, cutoff: int = -1,
+         range_bits: int = 0):
+    """(w, S, T) of the product's digit width, digit count and cutoff, or None when
+    the levels cannot stay exact.  Written from the options' definitions:
+
+    * w = 13 (slice_bits 0 or 13): S0 = slices or slices_per_limb L;
+      w explicit: S0 = slices or ceil(52 L / w);
+      automatic (slice_bits -1): the width of 13..26 with the fewest pairs of the
+      resulting (S, T) among those whose levels stay exact, the wider on a tie;
+    * range balancing: D = ceil(range_bits / w) more digits, S = S0 + D, default
+      cutoff T = S0 - 1 + 2 D (a product of two elements D digits below their
+      lines' grids keeps its S0 leading levels); cutoff -2 keeps every pair;
+    * exactness: max pairs of a kept level times k (2^w - 1)^2 below 2^53.
+    Raises ValueError for invalid options (S > 64, S w > 844, ...)."""
+    def finish(w, S0):
+        D = -(-range_bits // w)
+        S = S0 + D
+        if S < 1 or S > 64 or S * w > 844:
+            raise ValueError("digit count")
+        T = S0 - 1 + 2 * D if cutoff == -1 else (2 * S - 2 if cutoff == -2 else cutoff)
+        if not 0 <= T <= 2 * S - 2:
+            raise ValueError("cutoff")
+        if w * T + 55 > 64 * 28:  # the exact level sum fits 28 words
+            raise ValueError("levels")
+        return w, S, T
+
+    def exact_ok(w, S, T):
+        return _max_pairs(S, T) * k * (2**w - 1) ** 2 < 2**53
+
+    if slice_bits == -1:
+        if slices:
+            raise ValueError("slices with the automatic width")
+        best = None
+        for w in range(13, 27):
+            try:
+                cand = finish(w, -(-52 * L // w))
+            except ValueError:
+                continue
+            if not exact_ok(*cand):
+                continue
+            key = (_pair_count(cand[1], cand[2]), -w)
+            if best is None or key < best[0]:
+                best = (key, cand)
+        return None if best is None else best[1]
+    w = 13 if slice_bits in (0, 13) else slice_bits
+    if not 1 <= w <= 26:
+        raise ValueError("width")
+    if w == 13:
+        S0 = slices or slices_per_limb * L
+    else:
+        S0 = slices or -(-52 * L // w)
+    cand = finish(w, S0)
+    return cand if exact_ok(*cand) else None
+
+
 def is_nonoverlapping(limbs) -> bool:
     """|x_{l+1}| <= ulp(x_l)/2 and a zero limb is followed only by zeros."""
     for a, b in zip(limbs[:-1], limbs[1:]):

@@ -36,6 +36,17 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // ---- exactness: pairs_t * k * (2^w - 1)^2 < 2^53 for every kept level t ------
 
+// Pairs (p, q), 0 <= p, q < S, with p + q <= T.
+int pair_count(int S, int T) {
+  int n = 0;
+  for (int t = 0; t <= T; ++t) {
+    int lo = t - (S - 1) > 0 ? t - (S - 1) : 0;
+    int hi = t < S - 1 ? t : S - 1;
+    if (hi >= lo) n += hi - lo + 1;
+  }
+  return n;
+}
+
 int max_pairs(int S, int T) {
   int best = 0;
   for (int t = 0; t <= T; ++t) {
@@ -116,20 +127,34 @@ struct Resolved {
   unsigned flags = 0;
 };
 
-// Adaptive width: among w = 13..26 with S = ceil(52 L / w) digits (the digit bits
-// of four 13-bit digits per limb) and S k (2^w - 1)^2 < 2^53, the fewest pairs
-// S (S + 1) / 2, the wider digit on a tie.  Returns false when none qualifies.
-bool auto_width(int limbs, int64_t k, int* w_out, int* S_out) {
+// Extra digits for elements down to range_bits below their line's exponent.
+inline int range_digits(int range_bits, int w) { return (range_bits + w - 1) / w; }
+
+// The cutoff selector applied to S0 base digits and D range digits.
+int cutoff_for(int cutoff, int S0, int D) {
+  if (cutoff == MDGEMM_CUTOFF_DEFAULT) return S0 - 1 + 2 * D;
+  if (cutoff == MDGEMM_CUTOFF_ALL) return 2 * (S0 + D) - 2;
+  return cutoff;
+}
+
+// Adaptive width: among w = 13..26 with S0 = ceil(52 L / w) base digits (the digit
+// bits of four 13-bit digits per limb), D = ceil(range_bits / w) extra digits,
+// S = S0 + D and the requested cutoff, those that are valid and whose levels stay
+// exact, the fewest pairs, the wider digit on a tie.  Returns false when none
+// qualifies.
+bool auto_width(int limbs, int64_t k, int range_bits, int cutoff, int* w_out, int* S0_out) {
   int best_pairs = 0;
   bool found = false;
   for (int w = mdg::kSliceBits; w <= mdg::kMaxSliceBits; ++w) {
-    const int S = (4 * mdg::kSliceBits * limbs + w - 1) / w;
-    if (!width_ok(S, w) || !exact_ok(k, S, w)) continue;
-    const int pairs = S * (S + 1) / 2;
+    const int S0 = (4 * mdg::kSliceBits * limbs + w - 1) / w, D = range_digits(range_bits, w);
+    const int S = S0 + D, T = cutoff_for(cutoff, S0, D);
+    if (!width_ok(S, w) || T < 0 || T > 2 * S - 2 || !levels_ok(T + 1, w) || !exact_ok(k, max_pairs(S, T), w))
+      continue;
+    const int pairs = pair_count(S, T);
     if (!found || pairs <= best_pairs) {
       best_pairs = pairs;
       *w_out = w;
-      *S_out = S;
+      *S0_out = S0;
       found = true;
     }
   }
@@ -141,10 +166,11 @@ int resolve(int limbs, int64_t k, const mdgemm_opts* opts, Resolved* r) {
   if (limbs < 1 || limbs > MDGEMM_MAX_LIMBS) return MDGEMM_EINVAL;
   const int bits = opts ? opts->slice_bits : 0;
   const int slices = opts ? opts->slices : 0;
-  if (slices < 0) return MDGEMM_EINVAL;
+  const int range_bits = opts ? opts->range_bits : 0;
+  if (slices < 0 || range_bits < 0 || range_bits > mdg::kMaxDigitBits) return MDGEMM_EINVAL;
   if (bits == MDGEMM_SLICE_BITS_AUTO) {
     if (slices != 0) return MDGEMM_EINVAL;
-    if (!auto_width(limbs, k, &r->w, &r->S)) return MDGEMM_EEXACT;
+    if (!auto_width(limbs, k, range_bits, opts->cutoff, &r->w, &r->S)) return MDGEMM_EEXACT;
   } else if (bits == 0 || bits == mdg::kSliceBits) {
     r->w = mdg::kSliceBits;
     int spl = opts ? opts->slices_per_limb : 0;
@@ -157,16 +183,16 @@ int resolve(int limbs, int64_t k, const mdgemm_opts* opts, Resolved* r) {
   } else {
     return MDGEMM_EINVAL;
   }
+  // range balancing: D more digits on the same line grid, and the cutoff raised by
+  // 2D so that a product of two elements D digits below their lines' exponents
+  // keeps its S0 leading levels
+  const int S0 = r->S, D = range_digits(range_bits, r->w);
+  r->S = S0 + D;
   if (!width_ok(r->S, r->w)) return MDGEMM_EINVAL;
-  int cutoff = opts ? opts->cutoff : MDGEMM_CUTOFF_DEFAULT;
-  if (cutoff == MDGEMM_CUTOFF_DEFAULT)
-    r->T = r->S - 1;
-  else if (cutoff == MDGEMM_CUTOFF_ALL)
-    r->T = 2 * r->S - 2;
-  else if (cutoff >= 0 && cutoff <= 2 * r->S - 2)
-    r->T = cutoff;
-  else
-    return MDGEMM_EINVAL;
+  const int cutoff = opts ? opts->cutoff : MDGEMM_CUTOFF_DEFAULT;
+  if (cutoff < 0 && cutoff != MDGEMM_CUTOFF_DEFAULT && cutoff != MDGEMM_CUTOFF_ALL) return MDGEMM_EINVAL;
+  r->T = cutoff_for(cutoff, S0, D);
+  if (r->T < 0 || r->T > 2 * r->S - 2) return MDGEMM_EINVAL;
   if (!levels_ok(r->T + 1, r->w)) return MDGEMM_EINVAL;
   r->stream = opts ? static_cast<hipStream_t>(opts->stream) : nullptr;
   r->flags = opts ? opts->flags : 0u;
@@ -288,6 +314,7 @@ void mdgemm_opts_init(mdgemm_opts* opts) {
   opts->cutoff = MDGEMM_CUTOFF_DEFAULT;
   opts->slice_bits = 0;
   opts->slices = 0;
+  opts->range_bits = 0;
 }
 
 int mdgemm_plan(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts, int* slice_bits, int* slices,
@@ -434,6 +461,17 @@ void mdgemm_release(void) {
 }
 
 // ---- stage entry points ----------------------------------------------------------
+
+int mdgemm_line_spread(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, int32_t* spread,
+                       void* stream) {
+  if (rows < 0 || cols < 0 || (axis != 0 && axis != 1)) return MDGEMM_EINVAL;
+  const int64_t lines = axis == 0 ? rows : cols;
+  if (lines == 0) return MDGEMM_OK;
+  if (!E || !spread || (rows > 0 && cols > 0 && !X0)) return MDGEMM_EINVAL;
+  if (overlaps(E, sizeof(int32_t) * static_cast<size_t>(lines), spread, sizeof(int32_t) * static_cast<size_t>(lines)))
+    return MDGEMM_EINVAL;
+  return hip_status(mdg::launch_line_spread(rows, cols, axis, X0, E, spread, static_cast<hipStream_t>(stream)));
+}
 
 int mdgemm_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, void* stream) {
   if (rows < 0 || cols < 0 || (axis != 0 && axis != 1)) return MDGEMM_EINVAL;

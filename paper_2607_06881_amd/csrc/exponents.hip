@@ -68,6 +68,59 @@ __global__ void __launch_bounds__(256) col_exponents_kernel(int64_t rows, int64_
   }
 }
 
+// Smallest frexp exponent of a nonzero entry of every row (one wave per row) or
+// column (64 columns per block, as col_exponents_kernel, vector atomic min);
+// INT_MAX for a line without a nonzero entry.
+__device__ inline int frexp_exp_or_max(double x) {
+  const int e = frexp_exp_or_min(x);
+  return e == kNoExp ? INT_MAX : e;
+}
+
+__device__ inline int wave_min(int v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = min(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+__global__ void __launch_bounds__(256) row_min_exponents_kernel(int64_t rows, int64_t cols,
+                                                                const double* __restrict__ X0,
+                                                                int32_t* __restrict__ Emin) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const double* r = X0 + row * cols;
+  int best = INT_MAX;
+  for (int64_t c = lane; c < cols; c += 64) best = min(best, frexp_exp_or_max(r[c]));
+  best = wave_min(best);
+  if (lane == 0) Emin[row] = best;
+}
+
+__global__ void __launch_bounds__(256) col_min_exponents_kernel(int64_t rows, int64_t cols,
+                                                                const double* __restrict__ X0,
+                                                                int32_t* __restrict__ Emin) {
+  __shared__ int part[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t col = static_cast<int64_t>(blockIdx.x) * 64 + lane;
+  int best = INT_MAX;
+  if (col < cols) {
+    const int64_t stride = static_cast<int64_t>(gridDim.y) * 4;
+    for (int64_t r = static_cast<int64_t>(blockIdx.y) * 4 + wave; r < rows; r += stride)
+      best = min(best, frexp_exp_or_max(X0[r * cols + col]));
+  }
+  part[wave][lane] = best;
+  __syncthreads();
+  if (wave == 0 && col < cols) {
+    best = min(min(part[0][lane], part[1][lane]), min(part[2][lane], part[3][lane]));
+    if (best != INT_MAX) atomicMin(Emin + col, best);
+  }
+}
+
+// spread = E - Emin, 0 for a line without a nonzero entry (in place over Emin).
+__global__ void spread_kernel(int64_t count, const int32_t* __restrict__ E, int32_t* __restrict__ spread) {
+  int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < count) spread[i] = spread[i] == INT_MAX ? 0 : E[i] - spread[i];
+}
+
 __global__ void finalize_exponents_kernel(int64_t count, int32_t* __restrict__ E) {
   int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i < count && E[i] == kNoExp) E[i] = 0;
@@ -129,6 +182,35 @@ hipError_t launch_exponents(int64_t rows, int64_t cols, int axis, const double* 
     if (err != hipSuccess) return err;
   }
   hipLaunchKernelGGL(finalize_exponents_kernel, dim3(grid_for(cols, 256, 1ll << 30)), dim3(256), 0, stream, cols, E);
+  return hipGetLastError();
+}
+
+hipError_t launch_line_spread(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, int32_t* spread,
+                              hipStream_t stream) {
+  hipError_t err = launch_exponents(rows, cols, axis, X0, E, stream);
+  if (err != hipSuccess) return err;
+  const int64_t lines = axis == 0 ? rows : cols;
+  if (lines == 0) return hipSuccess;
+  err = launch_set_i32(spread, lines, INT_MAX, stream);
+  if (err != hipSuccess) return err;
+  if (rows > 0 && cols > 0) {
+    if (axis == 0) {
+      hipLaunchKernelGGL(row_min_exponents_kernel, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream,
+                         rows, cols, X0, spread);
+    } else {
+      int64_t gx = (cols + 63) / 64;
+      int64_t gy = (2048 + gx - 1) / gx;
+      int64_t max_gy = (rows + 63) / 64;
+      if (gy > max_gy) gy = max_gy;
+      if (gy < 1) gy = 1;
+      if (gy > 65535) gy = 65535;
+      hipLaunchKernelGGL(col_min_exponents_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)),
+                         dim3(256), 0, stream, rows, cols, X0, spread);
+    }
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  hipLaunchKernelGGL(spread_kernel, dim3(grid_for(lines, 256, 1ll << 30)), dim3(256), 0, stream, lines, E, spread);
   return hipGetLastError();
 }
 

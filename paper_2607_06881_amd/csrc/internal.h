@@ -37,6 +37,11 @@ struct JobTable {
 // a1: per-row (axis 0) or per-column (axis 1) grid exponents of a [rows][cols] plane.
 hipError_t launch_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, hipStream_t stream);
 
+// Exponent spread of every line: E as launch_exponents, spread = E - (smallest
+// frexp exponent of a nonzero entry of the line), 0 for an all-zero line.
+hipError_t launch_line_spread(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, int32_t* spread,
+                              hipStream_t stream);
+
 // a2: w-bit digits of X [L][rows][cols] on the grid exponents E, either row-major
 // D [S][rows][cols] (panel == false) or as a level-GEMM panel (panel == true):
 // axis 0: D [S][panel_k(cols)][panel_mn(rows)] (transposed), axis 1:

@@ -61,6 +61,7 @@ EXPORTED = (
     "mdgemm_status_string",
     "mdgemm_release",
     "mdgemm_exponents",
+    "mdgemm_line_spread",
     "mdgemm_split",
     "mdgemm_split_panel",
     "mdgemm_slice_gemm",
@@ -85,6 +86,7 @@ class mdgemm_opts(ctypes.Structure):
         ("flags", ctypes.c_uint),
         ("slice_bits", ctypes.c_int),
         ("slices", ctypes.c_int),
+        ("range_bits", ctypes.c_int),
     ]
 
 
@@ -120,6 +122,8 @@ def lib() -> ctypes.CDLL:
         L.mdgemm_release.restype = None
         L.mdgemm_exponents.argtypes = [_i64, _i64, ctypes.c_int, _vp, _vp, _vp]
         L.mdgemm_exponents.restype = ctypes.c_int
+        L.mdgemm_line_spread.argtypes = [_i64, _i64, ctypes.c_int, _vp, _vp, _vp, _vp]
+        L.mdgemm_line_spread.restype = ctypes.c_int
         _c = ctypes.c_int
         L.mdgemm_split.argtypes = [_i64, _i64, _c, _c, _c, _c, _vp, _vp, _vp, _vp]
         L.mdgemm_split.restype = ctypes.c_int
@@ -166,7 +170,8 @@ def _stream(stream) -> int:
 
 
 def make_opts(*, slices_per_limb: int = 4, cutoff: int = MDGEMM_CUTOFF_DEFAULT, flags: int = 0, stream=None,
-              workspace: Optional[torch.Tensor] = None, slice_bits: int = 0, slices: int = 0) -> mdgemm_opts:
+              workspace: Optional[torch.Tensor] = None, slice_bits: int = 0, slices: int = 0,
+              range_bits: int = 0) -> mdgemm_opts:
     o = mdgemm_opts()
     lib().mdgemm_opts_init(ctypes.byref(o))
     o.slices_per_limb = slices_per_limb
@@ -174,6 +179,7 @@ def make_opts(*, slices_per_limb: int = 4, cutoff: int = MDGEMM_CUTOFF_DEFAULT, 
     o.flags = flags
     o.slice_bits = slice_bits
     o.slices = slices
+    o.range_bits = range_bits
     o.stream = _stream(stream)
     if workspace is not None:
         o.workspace = workspace.data_ptr()
@@ -182,18 +188,20 @@ def make_opts(*, slices_per_limb: int = 4, cutoff: int = MDGEMM_CUTOFF_DEFAULT, 
 
 
 def mdgemm_workspace_bytes(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
-                           cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0) -> int:
+                           cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0,
+                           range_bits: int = 0) -> int:
     o = mdgemm_opts()
     lib().mdgemm_opts_init(ctypes.byref(o))
     o.slices_per_limb = slices_per_limb
     o.cutoff = cutoff
     o.slice_bits = slice_bits
     o.slices = slices
+    o.range_bits = range_bits
     return int(lib().mdgemm_workspace_bytes(m, n, k, limbs, ctypes.byref(o)))
 
 
 def mdgemm_plan(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
-                cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0):
+                cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0, range_bits: int = 0):
     """(digit width w, digit count S, cutoff T) that mdgemm_ex uses for these options."""
     o = mdgemm_opts()
     lib().mdgemm_opts_init(ctypes.byref(o))
@@ -201,6 +209,7 @@ def mdgemm_plan(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
     o.cutoff = cutoff
     o.slice_bits = slice_bits
     o.slices = slices
+    o.range_bits = range_bits
     w, S, T = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
     _check(lib().mdgemm_plan(m, n, k, limbs, ctypes.byref(o), ctypes.byref(w), ctypes.byref(S), ctypes.byref(T)),
            "mdgemm_plan")
@@ -209,7 +218,7 @@ def mdgemm_plan(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
 
 def mdgemm_ex(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None, *, slices_per_limb: int = 4,
               cutoff: int = MDGEMM_CUTOFF_DEFAULT, flags: int = 0, workspace: Optional[torch.Tensor] = None,
-              stream=None, slice_bits: int = 0, slices: int = 0) -> torch.Tensor:
+              stream=None, slice_bits: int = 0, slices: int = 0, range_bits: int = 0) -> torch.Tensor:
     """C = A.B for limb-major float64 tensors A [L, m, k] and B [L, k, n] on the GPU.
 
     The workspace is a torch uint8 tensor (allocated here when not given), so
@@ -228,12 +237,12 @@ def mdgemm_ex(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None
             raise ValueError("C has the wrong shape")
     if workspace is None:
         need = mdgemm_workspace_bytes(m, n, k, L, slices_per_limb=slices_per_limb, cutoff=cutoff,
-                                      slice_bits=slice_bits, slices=slices)
+                                      slice_bits=slice_bits, slices=slices, range_bits=range_bits)
         if need == 2**64 - 1:
             _check(MDGEMM_EINVAL, "mdgemm_workspace_bytes")
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=A.device)
     o = make_opts(slices_per_limb=slices_per_limb, cutoff=cutoff, flags=flags, stream=stream, workspace=workspace,
-                  slice_bits=slice_bits, slices=slices)
+                  slice_bits=slice_bits, slices=slices, range_bits=range_bits)
     _check(lib().mdgemm_ex(m, n, k, L, _ptr(A), _ptr(B), _ptr(C), ctypes.byref(o)), "mdgemm_ex")
     return C
 
@@ -271,6 +280,19 @@ def mdgemm_exponents(X0: torch.Tensor, axis: int, E: Optional[torch.Tensor] = No
         E = torch.empty(rows if axis == 0 else cols, dtype=torch.int32, device=X0.device)
     _check(lib().mdgemm_exponents(rows, cols, axis, _ptr(X0), _ptr(E), _stream(stream)), "mdgemm_exponents")
     return E
+
+
+def mdgemm_line_spread(X0: torch.Tensor, axis: int, stream=None):
+    """(E, spread) int32 per row (axis 0) or column (axis 1): the grid exponents and
+    E minus the smallest exponent of a nonzero entry of the line."""
+    _dev_tensor(X0, torch.float64, "X0")
+    rows, cols = X0.shape
+    lines = rows if axis == 0 else cols
+    E = torch.empty(lines, dtype=torch.int32, device=X0.device)
+    spread = torch.empty(lines, dtype=torch.int32, device=X0.device)
+    _check(lib().mdgemm_line_spread(rows, cols, axis, _ptr(X0), _ptr(E), _ptr(spread), _stream(stream)),
+           "mdgemm_line_spread")
+    return E, spread
 
 
 def mdgemm_split(X: torch.Tensor, E: torch.Tensor, slices: int, axis: int, D: Optional[torch.Tensor] = None,

@@ -58,7 +58,23 @@ class Workload:
     row_exp: int = 0  # A rows scaled by 2^e, e ~ U{-row_exp..row_exp}
     col_exp: int = 0  # B columns scaled by 2^e, e ~ U{-col_exp..col_exp}
     elem_exp: int = 0  # every element scaled by 2^e, e ~ U{-elem_exp..elem_exp}
+    # column k of A scaled by 2^-e_k and row k of B by 2^(e_k - inner_exp), e_k ~ U{0..inner_exp}:
+    # every product a_ik b_kj has the same scale while each line of A and B spans inner_exp bits
+    inner_exp: int = 0
+    range_bits: int = 0  # the product's range balancing (extra digits for inner_exp bits of range)
     description: str = field(default="", compare=False)
+
+    def options(self, adaptive: bool = False) -> dict:
+        """Keyword options of mdgemm_ex for this workload's digits and cutoff, or
+        for the adaptive width (with the same range balancing)."""
+        if adaptive:
+            opts = {"slice_bits": -1}
+            if self.range_bits:
+                opts["range_bits"] = self.range_bits
+            return opts
+        if self.range_bits:
+            return {"range_bits": self.range_bits}
+        return {"slices_per_limb": self.slices // self.limbs, "cutoff": self.cutoff}
 
     @property
     def pairs(self) -> int:
@@ -104,6 +120,14 @@ WORKLOADS = {
     "c6": Workload(
         "c6", 16, 128, 8192, 64, 64, 63, 6, "normal",
         description="hexa-double 128x8192x64, limb 0 ~ N(0,1), pairs p+q <= 63"),
+    # A wide range inside every line (section 3, balancing): the inner dimension is
+    # scaled oppositely in A and B, so each row of A and column of B spans 60
+    # bits while every term a_ik b_kj has the same size; one shared grid per line
+    # loses the small elements' bits unless the lines get range balancing.
+    "c7": Workload(
+        "c7", 2, 2048, 2048, 2048, 13, 17, 7, "normal", inner_exp=60, range_bits=60,
+        description="double-double 2048^3, A column k x 2^-e_k, B row k x 2^(e_k-60), e_k ~ U{0..60}; "
+                    "range balancing over 60 bits: 13 digits, pairs p+q <= 17"),
 }
 
 
@@ -190,4 +214,8 @@ def make_workload(w: Workload | str, m: int | None = None, n: int | None = None,
     rng = np.random.default_rng(w.seed if seed is None else seed)
     A = make_operand(rng, w.limbs, m, k, w.base, row_exp=w.row_exp, elem_exp=w.elem_exp)
     B = make_operand(rng, w.limbs, k, n, w.base, col_exp=w.col_exp, elem_exp=w.elem_exp)
+    if w.inner_exp:
+        e = rng.integers(0, w.inner_exp + 1, k)
+        A *= np.ldexp(1.0, -e)[None, None, :]  # powers of two: the limbs stay normalized
+        B *= np.ldexp(1.0, e - w.inner_exp)[None, :, None]
     return A, B

@@ -190,3 +190,44 @@ def test_exactness_bound_wide_digits(lib):
     assert lib.mdgemm_slice_gemm(4, 4, kmax + 1, S, w, S - 1, 0, FA, FB, FC, None) == md.MDGEMM_EEXACT
     assert md.mdgemm_workspace_bytes(4096, 4096, 4096, 2, slice_bits=md.MDGEMM_SLICE_BITS_AUTO) < \
         md.mdgemm_workspace_bytes(4096, 4096, 4096, 2)
+
+
+def test_plan_matches_the_oracle_reading_of_the_options(lib):
+    # The library's option resolution against the oracle's, written separately
+    # from the same definitions (exact.plan), over a grid of option combinations.
+    combos = 0
+    for L in (1, 2, 3, 4, 8, 16):
+        for k in (1, 64, 2048, 2**20):
+            for slice_bits in (0, 13, 17, 22, md.MDGEMM_SLICE_BITS_AUTO):
+                for slices in (0, 9):
+                    for cutoff in (-1, -2, 5):
+                        for range_bits in (0, 13, 60):
+                            kw = dict(slice_bits=slice_bits, slices=slices, cutoff=cutoff, range_bits=range_bits)
+                            try:
+                                want = exact.plan(L, k, **kw)
+                                err = None if want is not None else md.MDGEMM_EEXACT
+                            except ValueError:
+                                want, err = None, md.MDGEMM_EINVAL
+                            if err is None:
+                                assert md.mdgemm_plan(8, 8, k, L, **kw) == want, (L, k, kw)
+                            else:
+                                with pytest.raises(md.MdgemmError) as ei:
+                                    md.mdgemm_plan(8, 8, k, L, **kw)
+                                assert ei.value.status == err, (L, k, kw)
+                            combos += 1
+    assert combos == 6 * 4 * 5 * 2 * 3 * 3
+
+
+def test_range_balancing_plans(lib):
+    # D = ceil(range / w) more digits, default cutoff S0 - 1 + 2D
+    assert md.mdgemm_plan(64, 64, 2048, 2, range_bits=60) == (13, 13, 17)
+    assert md.mdgemm_plan(64, 64, 2048, 2, range_bits=13) == (13, 9, 9)
+    assert md.mdgemm_plan(64, 64, 2048, 2, range_bits=1) == (13, 9, 9)
+    assert md.mdgemm_plan(64, 64, 2048, 2, range_bits=60, slice_bits=md.MDGEMM_SLICE_BITS_AUTO) == (19, 10, 13)
+    assert md.mdgemm_plan(64, 64, 2048, 2, range_bits=60, cutoff=-2) == (13, 13, 24)
+    assert _ex(lib, 4, 4, 4, 2, range_bits=-1) == md.MDGEMM_EINVAL
+    assert _ex(lib, 4, 4, 4, 16, range_bits=13) == md.MDGEMM_EINVAL  # 65 digits
+    E = md.MDGEMM_EINVAL
+    assert lib.mdgemm_line_spread(4, 4, 2, FA, FB, FC, None) == E
+    assert lib.mdgemm_line_spread(4, 4, 0, FA, FB, FB, None) == E  # E and spread overlap
+    assert lib.mdgemm_line_spread(0, 4, 0, None, None, None, None) == md.MDGEMM_OK

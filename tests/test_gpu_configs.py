@@ -27,10 +27,10 @@ DEV = torch.device("cuda:0")
 def _run(w):
     A_h, B_h = workloads.make_workload(w)
     A, B = torch.from_numpy(A_h).to(DEV), torch.from_numpy(B_h).to(DEV)
-    spl = w.slices // w.limbs
-    ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, slices_per_limb=spl, cutoff=w.cutoff),
-                     dtype=torch.uint8, device=DEV)
-    C = md.mdgemm_ex(A, B, slices_per_limb=spl, cutoff=w.cutoff, workspace=ws)
+    opts = w.options()
+    assert md.mdgemm_plan(w.m, w.n, w.k, w.limbs, **opts) == (13, w.slices, w.cutoff)
+    ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, **opts), dtype=torch.uint8, device=DEV)
+    C = md.mdgemm_ex(A, B, workspace=ws, **opts)
     torch.cuda.synchronize()
     return A_h, B_h, A, B, C
 
@@ -54,7 +54,7 @@ def _nonoverlap_all(C):
     return ok.all()
 
 
-@pytest.mark.parametrize("name", ["c0", "c1", "c2", "c3", "c4", "c5", "c6"])
+@pytest.mark.parametrize("name", ["c0", "c1", "c2", "c3", "c4", "c5", "c6", "c7"])
 def test_workload_full_size(name):
     w = workloads.WORKLOADS[name]
     print(f"[case] workload {name}: {w.description}", flush=True)
@@ -125,21 +125,20 @@ def test_workload_full_size(name):
           flush=True)
 
 
-@pytest.mark.parametrize("name", ["c2", "c3", "c4"])
+@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c7"])
 def test_workload_adaptive_width(name):
     # The same workloads with the adaptive width: fewer, wider digits, sampled
     # entries bit-exact against the oracle's chain at that width, within the
     # stated tolerance.
     w = workloads.WORKLOADS[name]
-    auto = md.MDGEMM_SLICE_BITS_AUTO
-    bits, S, T = md.mdgemm_plan(w.m, w.n, w.k, w.limbs, slice_bits=auto)
-    assert (bits, S) == exact.adaptive_width(w.limbs, w.k)
+    opts = w.options(adaptive=True)
+    bits, S, T = md.mdgemm_plan(w.m, w.n, w.k, w.limbs, **opts)
+    assert (bits, S, T) == exact.plan(w.limbs, w.k, **opts)
     print(f"[case] workload {name} adaptive width: w={bits} S={S} T={T}", flush=True)
     A_h, B_h = workloads.make_workload(w)
     A, B = torch.from_numpy(A_h).to(DEV), torch.from_numpy(B_h).to(DEV)
-    ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, slice_bits=auto), dtype=torch.uint8,
-                     device=DEV)
-    C_h = md.mdgemm_ex(A, B, slice_bits=auto, workspace=ws).cpu().numpy()
+    ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, **opts), dtype=torch.uint8, device=DEV)
+    C_h = md.mdgemm_ex(A, B, workspace=ws, **opts).cpu().numpy()
     del ws
     assert _nonoverlap_all(C_h) and np.isfinite(C_h).all()
     EA, EB = coracle.exponents(A_h[0], 0), coracle.exponents(B_h[0], 1)
@@ -154,3 +153,18 @@ def test_workload_adaptive_width(name):
         assert err <= bound, (i, j, float(err / bound))
         worst = max(worst, float(err / bound))
     print(f"[result] {name} adaptive width: max |C - C_exact| / bound = {worst:.3e}", flush=True)
+
+
+def test_workload_line_spread():
+    # the measured range of the wide-range workload's lines, against the oracle
+    w = workloads.WORKLOADS["c7"]
+    print("[case] line spread c7", flush=True)
+    A_h, B_h = workloads.make_workload(w)
+    EA, SA = md.mdgemm_line_spread(torch.from_numpy(A_h[0]).to(DEV), 0)
+    EB, SB = md.mdgemm_line_spread(torch.from_numpy(B_h[0]).to(DEV), 1)
+    assert np.array_equal(EA.cpu().numpy(), coracle.exponents(A_h[0], 0))
+    assert np.array_equal(EB.cpu().numpy(), coracle.exponents(B_h[0], 1))
+    rows, cols = [0, 5, 1000, w.m - 1], [0, 77, w.n - 1]
+    assert SA.cpu().numpy()[rows].tolist() == exact.line_spread(A_h[0, rows, :], 0).tolist()
+    assert SB.cpu().numpy()[cols].tolist() == exact.line_spread(B_h[0][:, cols], 1).tolist()
+    assert w.range_bits - 10 <= int(SA.min()) and int(SA.max()) <= w.range_bits + 30  # N(0,1) tails add bits

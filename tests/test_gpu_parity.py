@@ -71,6 +71,24 @@ def test_exponents(rows, cols):
         assert np.array_equal(got, want), axis
 
 
+@pytest.mark.parametrize("rows,cols", [(1, 1), (7, 300), (300, 7), (129, 257), (64, 5000)])
+def test_line_spread(rows, cols):
+    print(f"[case] line spread {rows}x{cols}", flush=True)
+    rng = np.random.default_rng(rows * 7 + cols)
+    X = rng.standard_normal((rows, cols)) * np.ldexp(1.0, rng.integers(-80, 80, (rows, cols)))
+    X[rng.random((rows, cols)) < 0.1] = 0.0
+    if rows > 2:
+        X[1, :] = 0.0          # an all-zero row
+        X[2, :] = 0.0
+        X[2, 0] = 5e-324       # a lone subnormal
+    if cols > 2:
+        X[:, 1] = 0.0          # an all-zero column
+    for axis in (0, 1):
+        E, spread = md.mdgemm_line_spread(_gpu(X), axis)
+        assert np.array_equal(_host(E), coracle.exponents(X, axis))
+        assert _host(spread).tolist() == exact.line_spread(X, axis).tolist()
+
+
 # --------------------------------------------------------------------------
 # a2 split
 # --------------------------------------------------------------------------
@@ -532,3 +550,33 @@ def test_mdgemm_explicit_width_end_to_end(L, bits, slices, cutoff):
     A, B = _operands(L, m, k, n, 30 + bits, base="normal", row_exp=5, col_exp=5)
     C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), slice_bits=bits, slices=slices, cutoff=cutoff))
     assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])
+
+
+@pytest.mark.parametrize("L,m,k,n,range_bits,auto", [(2, 70, 48, 65, 60, False), (2, 33, 100, 129, 60, True),
+                                                     (3, 20, 40, 17, 30, False), (4, 17, 33, 9, 26, True),
+                                                     (8, 9, 20, 8, 40, False)])
+def test_mdgemm_range_balancing_end_to_end(L, m, k, n, range_bits, auto):
+    opts = {"range_bits": range_bits}
+    if auto:
+        opts["slice_bits"] = md.MDGEMM_SLICE_BITS_AUTO
+    w, S, T = md.mdgemm_plan(m, n, k, L, **opts)
+    assert (w, S, T) == exact.plan(L, k, **opts)
+    print(f"[case] mdgemm range {range_bits} L={L} {m}x{k}x{n}: w={w} S={S} T={T}", flush=True)
+    wl = workloads.WORKLOADS["c7"]
+    rng = np.random.default_rng(L + k + range_bits)
+    A = workloads.make_operand(rng, L, m, k, "normal")
+    B = workloads.make_operand(rng, L, k, n, "normal")
+    e = rng.integers(0, range_bits + 1, k)  # the wide-range recipe of workload c7
+    A *= np.ldexp(1.0, -e)[None, None, :]
+    B *= np.ldexp(1.0, e - range_bits)[None, :, None]
+    assert wl.inner_exp == 60
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), **opts))
+    ref = pipeline.full_reference(A, B, S, T, w)
+    assert np.array_equal(C, ref["C"])
+    for i in range(0, m, max(1, m // 3)):
+        for j in range(0, n, max(1, n // 3)):
+            want, mag = exact.exact_product(A, B, i, j)
+            err = abs(exact.value(C[:, i, j]) - want)
+            bound = exact.tolerance(k, L, mag) if L <= 4 else \
+                exact.method_bound(A, B, i, j, S, T, int(ref["EA"][i]), int(ref["EB"][j]), w)
+            assert err <= bound, (i, j, float(err / bound))

@@ -538,6 +538,53 @@ def test_wrong_level_weight_for_wide_digits_is_caught():
     assert abs(bad - want) > exact.tolerance(k, L, mag)
 
 
+def test_line_spread_against_numpy_frexp():
+    rng = np.random.default_rng(12)
+    X = rng.standard_normal((9, 40)) * np.ldexp(1.0, rng.integers(-50, 50, (9, 40)))
+    X[2, :] = 0.0
+    X[3, :] = 0.0
+    X[3, 5] = 5e-324  # a lone subnormal: its line spans nothing
+    X[4, ::3] = 0.0
+    for axis in (0, 1):
+        lines = X if axis == 0 else X.T
+        want = []
+        for line in lines:
+            nz = line[line != 0]
+            _, e = np.frexp(nz)
+            want.append(int(e.max() - e.min()) if nz.size else 0)
+        assert exact.line_spread(X, axis).tolist() == want
+
+
+def test_range_balancing_restores_the_tolerance():
+    # Rows of A and columns of B spanning 60 bits with balanced products
+    # (workload c7's recipe, small): with one grid per line and four digits per
+    # limb the small elements lose their bits and the tolerance fails; with 60 bits
+    # of range balancing the chain is back within it.
+    w = workloads.WORKLOADS["c7"]
+    A, B = workloads.make_workload(w, m=3, n=3, k=48, seed=3)
+    assert max(exact.line_spread(A[0], 0)) >= 40 and max(exact.line_spread(B[0], 1)) >= 40
+    L, k = 2, 48
+    plain = pipeline.full_reference(A, B, 8, 7)
+    wb, Sb, Tb = exact.plan(L, k, range_bits=60)
+    balanced = pipeline.full_reference(A, B, Sb, Tb, wb)
+    worst_plain = worst_bal = 0.0
+    for i in range(3):
+        for j in range(3):
+            want, mag = exact.exact_product(A, B, i, j)
+            tol = exact.tolerance(k, L, mag)
+            worst_plain = max(worst_plain, float(abs(exact.value(plain["C"][:, i, j]) - want) / tol))
+            worst_bal = max(worst_bal, float(abs(exact.value(balanced["C"][:, i, j]) - want) / tol))
+    assert worst_plain > 1e6  # the shared grid alone misses the tolerance by far
+    assert worst_bal <= 1.0
+    # the adaptive width with the same balancing stays within it too
+    wa, Sa, Ta = exact.plan(L, k, range_bits=60, slice_bits=-1)
+    adaptive = pipeline.full_reference(A, B, Sa, Ta, wa)
+    for i in range(3):
+        for j in range(3):
+            want, mag = exact.exact_product(A, B, i, j)
+            assert abs(exact.value(adaptive["C"][:, i, j]) - want) <= exact.tolerance(k, L, mag)
+
+
 def test_method_bound_catches_a_dropped_kept_pair():
     # Planted in the oracle's chain: leave out pair (0, T) of the last kept level.
     L, S, T, k = 8, 32, 31, 16
