@@ -146,10 +146,16 @@ def main(argv=None) -> int:
     stream = torch.cuda.current_stream()
 
     def mode_opts(slice_bits):
-        """Options of one digit mode: the workload's 13-bit digits and cutoff, or a width."""
+        """Options of one digit mode: the workload's 13-bit digits and cutoff, the
+        adaptive width or an explicit width (with the workload's range balancing)."""
         if slice_bits == 13:
-            return {"slices_per_limb": w.slices // w.limbs, "cutoff": w.cutoff}
-        return {"slice_bits": slice_bits}
+            return w.options()
+        if slice_bits == md.MDGEMM_SLICE_BITS_AUTO:
+            return w.options(adaptive=True)
+        opts = {"slice_bits": slice_bits}
+        if w.range_bits:
+            opts["range_bits"] = w.range_bits
+        return opts
 
     def measure(opts, steps, warmup):
         """ms per step and per-stage ms of mdgemm_ex with these options."""
@@ -220,6 +226,8 @@ def main(argv=None) -> int:
     }
     config = {"workload": f"{w.name}: {w.description}", "m": m, "n": n, "k": k, "limbs": L, "slices": S,
               "cutoff": T, "pairs": pairs, "seed": w.seed}
+    if w.range_bits:
+        config["range_bits"] = w.range_bits
     if bits != 13:
         config["slice_bits"] = bits
         config["workload"] += f"; adaptive width: {S} digits of {bits} bits, pairs p+q <= {T}"
