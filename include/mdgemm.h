@@ -77,7 +77,7 @@ extern "C" {
 
 typedef struct mdgemm_opts {
   void* stream;           /* hipStream_t to launch on; NULL = default stream */
-  void* workspace;        /* caller-owned device buffer; NULL = library-owned cache */
+  void* workspace;        /* caller-owned device buffer; NULL = library-owned buffer (see below) */
   size_t workspace_bytes; /* size of `workspace` in bytes */
   int slices_per_limb;    /* 13-bit digits per limb, S = limbs * slices_per_limb <= 64; 0 = 4 */
   int cutoff;             /* largest kept p + q; MDGEMM_CUTOFF_DEFAULT or _ALL or 0..2S-2 */
@@ -86,6 +86,13 @@ typedef struct mdgemm_opts {
   int slices;             /* digits per element S; 0 = derived (see below) */
   int range_bits;         /* range balancing: full precision down to 2^-range_bits of the line; 0 = off */
 } mdgemm_opts;
+
+/* Workspace.  A caller workspace is used by this call only; calls that share one
+ * must be ordered by the caller.  Without one, the library keeps one buffer per
+ * device, grown on demand: calls that use it are ordered among themselves on the
+ * GPU (each waits for the previous user's work, across streams), and such a call
+ * is refused with MDGEMM_EINVAL while its stream is capturing a graph (the graph
+ * would keep an address that a later, larger call may free). */
 
 /* Digit width and count.
  *  - slice_bits 0 or 13: w = 13 and S = slices, else limbs * slices_per_limb.

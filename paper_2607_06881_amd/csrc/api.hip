@@ -234,24 +234,34 @@ bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
 
 // ---- library-owned workspace (one per device) ---------------------------------
 
+// One buffer per device, shared by every call that brings no workspace.  Calls
+// on different streams are ordered through `last`: a call waits for the
+// previous user's event before its first kernel and records the event after its
+// last one, all while holding `mu`, so two calls never use the buffer at once.
 struct Cache {
   std::mutex mu;
   std::vector<void*> ptr;
   std::vector<size_t> bytes;
+  std::vector<hipEvent_t> last;
 };
 Cache& cache() {
   static Cache c;
   return c;
 }
 
-int cached_workspace(size_t need, void** out) {
+// With c.mu held: the buffer of the current device, grown to `need` bytes.
+int cached_workspace(Cache& c, size_t need, void** out, int* dev_out) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return MDGEMM_EHIP;
-  Cache& c = cache();
-  std::lock_guard<std::mutex> lock(c.mu);
+  *dev_out = dev;
   if (static_cast<size_t>(dev) >= c.ptr.size()) {
     c.ptr.resize(dev + 1, nullptr);
     c.bytes.resize(dev + 1, 0);
+    c.last.resize(dev + 1, nullptr);
+  }
+  if (!c.last[dev] && hipEventCreateWithFlags(&c.last[dev], hipEventDisableTiming) != hipSuccess) {
+    c.last[dev] = nullptr;
+    return MDGEMM_EHIP;
   }
   if (c.bytes[dev] < need) {
     if (c.ptr[dev]) {
@@ -375,12 +385,21 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   Layout L;
   if (!layout(m, n, k, r, &L)) return MDGEMM_EINVAL;
   char* ws = nullptr;
+  std::unique_lock<std::mutex> wlock(cache().mu, std::defer_lock);
+  int wdev = -1;  // device whose library buffer this call uses, or -1
   if (opts && opts->workspace) {
     if (opts->workspace_bytes < L.total) return MDGEMM_EWORKSPACE;
     ws = static_cast<char*>(opts->workspace);
   } else {
+    // a captured graph would keep the library buffer's address, which a later
+    // call may free: capture needs a caller workspace
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    MDG_TRY(hip_status(hipStreamIsCapturing(s, &cap)));
+    if (cap != hipStreamCaptureStatusNone) return MDGEMM_EINVAL;
+    wlock.lock();
     void* p = nullptr;
-    MDG_TRY(cached_workspace(L.total, &p));
+    MDG_TRY(cached_workspace(cache(), L.total, &p, &wdev));
+    MDG_TRY(hip_status(hipStreamWaitEvent(s, cache().last[wdev], 0)));
     ws = static_cast<char*>(p);
   }
   int32_t* EA = reinterpret_cast<int32_t*>(ws + L.ea);
@@ -390,39 +409,50 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   double* DB = reinterpret_cast<double*>(ws + L.db);
   double* G = reinterpret_cast<double*>(ws + L.g);
 
-  if (r.flags & MDGEMM_CHECK_FINITE) {
-    MDG_TRY(hip_status(mdg::launch_set_i32(flag, 1, 0, s)));
-    MDG_TRY(hip_status(mdg::launch_nonfinite_scan(A, static_cast<int64_t>(limbs) * m * k, flag, s)));
-    MDG_TRY(hip_status(mdg::launch_nonfinite_scan(B, static_cast<int64_t>(limbs) * k * n, flag, s)));
-    int32_t h = 0;
-    MDG_TRY(hip_status(hipMemcpyAsync(&h, flag, sizeof h, hipMemcpyDeviceToHost, s)));
-    MDG_TRY(hip_status(hipStreamSynchronize(s)));
-    if (h) return MDGEMM_ENONFINITE;
+  auto enqueue = [&]() -> int {
+    if (r.flags & MDGEMM_CHECK_FINITE) {
+      MDG_TRY(hip_status(mdg::launch_set_i32(flag, 1, 0, s)));
+      MDG_TRY(hip_status(mdg::launch_nonfinite_scan(A, static_cast<int64_t>(limbs) * m * k, flag, s)));
+      MDG_TRY(hip_status(mdg::launch_nonfinite_scan(B, static_cast<int64_t>(limbs) * k * n, flag, s)));
+      int32_t h = 0;
+      MDG_TRY(hip_status(hipMemcpyAsync(&h, flag, sizeof h, hipMemcpyDeviceToHost, s)));
+      MDG_TRY(hip_status(hipStreamSynchronize(s)));
+      if (h) return MDGEMM_ENONFINITE;
+    }
+    std::unique_lock<std::mutex> tlock(timing().mu, std::defer_lock);
+    if (timed) {
+      tlock.lock();
+      timing().valid = false;
+      MDG_TRY(record(0, s));
+    }
+    // a1: grid exponents per row of A and per column of B
+    MDG_TRY(hip_status(mdg::launch_exponents(m, k, 0, A, EA, s)));
+    MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, EB, s)));
+    if (timed) MDG_TRY(record(1, s));
+    // a2: exact splits into S digit planes
+    MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, r.w, 0, A, EA, DA, true, s)));
+    MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, r.w, 1, B, EB, DB, true, s)));
+    if (timed) MDG_TRY(record(2, s));
+    // a3: level GEMMs on the FP64 matrix cores
+    MDG_TRY(hip_status(mdg::launch_slice_gemm(m, n, k, DA, DB, G, level_jobs(r.S, r.T), s)));
+    if (timed) MDG_TRY(record(3, s));
+    // a4 + a5: exact accumulation and greedy rounding into L limbs
+    MDG_TRY(hip_status(mdg::launch_accum_renorm(m, n, limbs, r.T + 1, r.w, G, EA, EB, C, s)));
+    if (timed) {
+      MDG_TRY(record(4, s));
+      timing().valid = true;
+    }
+    return MDGEMM_OK;
+  };
+  int st = enqueue();
+  if (wdev >= 0) {
+    // the next user of the library buffer waits for everything enqueued here,
+    // also when enqueueing stopped at an error
+    const int rec = hip_status(hipEventRecord(cache().last[wdev], s));
+    wlock.unlock();
+    if (st == MDGEMM_OK) st = rec;
   }
-
-  std::unique_lock<std::mutex> tlock(timing().mu, std::defer_lock);
-  if (timed) {
-    tlock.lock();
-    timing().valid = false;
-    MDG_TRY(record(0, s));
-  }
-  // a1: grid exponents per row of A and per column of B
-  MDG_TRY(hip_status(mdg::launch_exponents(m, k, 0, A, EA, s)));
-  MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, EB, s)));
-  if (timed) MDG_TRY(record(1, s));
-  // a2: exact splits into S digit planes
-  MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, r.w, 0, A, EA, DA, true, s)));
-  MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, r.w, 1, B, EB, DB, true, s)));
-  if (timed) MDG_TRY(record(2, s));
-  // a3: level GEMMs on the FP64 matrix cores
-  MDG_TRY(hip_status(mdg::launch_slice_gemm(m, n, k, DA, DB, G, level_jobs(r.S, r.T), s)));
-  if (timed) MDG_TRY(record(3, s));
-  // a4 + a5: exact accumulation and greedy rounding into L limbs
-  MDG_TRY(hip_status(mdg::launch_accum_renorm(m, n, limbs, r.T + 1, r.w, G, EA, EB, C, s)));
-  if (timed) {
-    MDG_TRY(record(4, s));
-    timing().valid = true;
-  }
+  if (st != MDGEMM_OK) return st;
   if (r.flags & MDGEMM_SYNC) MDG_TRY(hip_status(hipStreamSynchronize(s)));
   return MDGEMM_OK;
 }
@@ -449,13 +479,15 @@ void mdgemm_release(void) {
   int cur = 0;
   (void)hipGetDevice(&cur);
   for (size_t d = 0; d < c.ptr.size(); ++d) {
-    if (!c.ptr[d]) continue;
+    if (!c.ptr[d] && !c.last[d]) continue;
     if (hipSetDevice(static_cast<int>(d)) == hipSuccess) {
       (void)hipDeviceSynchronize();
-      (void)hipFree(c.ptr[d]);
+      if (c.ptr[d]) (void)hipFree(c.ptr[d]);
+      if (c.last[d]) (void)hipEventDestroy(c.last[d]);
     }
     c.ptr[d] = nullptr;
     c.bytes[d] = 0;
+    c.last[d] = nullptr;
   }
   (void)hipSetDevice(cur);
 }

@@ -6,6 +6,7 @@ exact rational product, |C - C_exact| <= 4 k 2^-(53L-4) (|A||B|).  Sizes span
 several 128 x 128 tiles and 16-deep k blocks with ragged tails.
 """
 
+import ctypes
 import math
 import random
 
@@ -489,6 +490,51 @@ def test_mdgemm_library_workspace_grows():
         C = _host(md.mdgemm(_gpu(A), _gpu(B)))
         assert np.array_equal(C, pipeline.full_reference(A, B, 8, 7)["C"]), (m, k, n)
     md.mdgemm_release()
+
+
+def _library_ex(A, B, C, stream):
+    """mdgemm_ex through the C ABI with the library-owned workspace on `stream`."""
+    o = md.make_opts(stream=stream)
+    o.workspace, o.workspace_bytes = None, 0
+    L, m, k = A.shape
+    n = B.shape[2]
+    return md.lib().mdgemm_ex(m, n, k, L, A.data_ptr(), B.data_ptr(), C.data_ptr(), ctypes.byref(o))
+
+
+def test_mdgemm_library_workspace_across_streams():
+    # Products on two streams at once share the library buffer; they are ordered
+    # on the GPU, so each one still computes its own product.
+    print("[case] library workspace shared by two streams", flush=True)
+    md.mdgemm_release()
+    cases = [_operands(2, 130, 100, 140, 40 + i, base="normal", row_exp=4, col_exp=4) for i in range(4)]
+    dev = [(_gpu(A), _gpu(B)) for A, B in cases]
+    outs = [torch.full((2, 130, 140), 3.0, dtype=torch.float64, device=DEV) for _ in cases]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for i, ((Ag, Bg), C) in enumerate(zip(dev, outs)):
+        assert _library_ex(Ag, Bg, C, streams[i % 2]) == md.MDGEMM_OK
+    torch.cuda.synchronize()
+    for (A, B), C in zip(cases, outs):
+        assert np.array_equal(C.cpu().numpy(), pipeline.full_reference(A, B, 8, 7)["C"])
+    md.mdgemm_release()
+
+
+@pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")  # the refused call leaves the graph empty
+def test_mdgemm_library_workspace_refuses_capture():
+    print("[case] capture with the library workspace is refused", flush=True)
+    A, B = _operands(2, 40, 30, 50, 45)
+    Ag, Bg = _gpu(A), _gpu(B)
+    C = torch.empty((2, 40, 50), dtype=torch.float64, device=DEV)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        st = _library_ex(Ag, Bg, C, s)
+    assert st == md.MDGEMM_EINVAL
+    # outside capture the same call works
+    assert _library_ex(Ag, Bg, C, s) == md.MDGEMM_OK
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy(), pipeline.full_reference(A, B, 8, 7)["C"])
 
 
 def test_mdgemm_graph_capture_replays():
