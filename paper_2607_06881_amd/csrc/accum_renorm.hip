@@ -63,6 +63,10 @@ __device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __rest
   const int T = levels - 1;
   const uint64_t mask = (1ull << w) - 1ull;
   int64_t carry = 0;
+  // the digits fill N from bit 0 upward: `word` collects the bits of word wi of N,
+  // `fill` of them so far; a full word is placed with one select over the words
+  uint64_t word = 0;
+  int fill = 0, wi = 0;
   for (int t0 = T; t0 >= 0; t0 -= 8) {
     // unconditional loads (levels below 0 re-read level 0 and are discarded),
     // so that the eight loads go out back to back
@@ -79,12 +83,19 @@ __device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __rest
       const int64_t v = static_cast<int64_t>(g[u]) + carry;  // exact: |G_t| < 2^53
       const uint64_t d = static_cast<uint64_t>(v) & mask;
       carry = v >> w;  // arithmetic shift: floor division
-      const int pos = w * (T - t), wi = pos >> 6, b = pos & 63;
-      const uint64_t lo = d << b, hi = b > 64 - w ? d >> (64 - b) : 0ull;
+      word |= d << fill;
+      fill += w;
+      if (fill >= 64) {
 #pragma unroll
-      for (int i = 0; i < NW; ++i) N[i] |= (i == wi) ? lo : ((i == wi + 1) ? hi : 0ull);
+        for (int i = 0; i < NW; ++i) N[i] = (i == wi) ? word : N[i];
+        ++wi;
+        fill -= 64;
+        word = fill ? d >> (w - fill) : 0ull;  // the bits of d beyond the full word
+      }
     }
   }
+#pragma unroll
+  for (int i = 0; i < NW; ++i) N[i] = (i == wi) ? word : N[i];
   if (carry != 0) add_shifted_signed<NW>(N, carry, w * (T + 1));
 }
 

@@ -61,21 +61,6 @@ __device__ inline void add_shifted(uint64_t (&acc)[NW], uint64_t M, int sh, bool
   }
 }
 
-// The `bits`-bit field (bits <= 26) of the NW-word integer v starting at bit pos.
-template <int NW>
-__device__ inline uint32_t field(const uint64_t (&v)[NW], int pos, int bits) {
-  const int wi = pos >> 6, b = pos & 63;
-  uint64_t lo = 0, hi = 0;
-#pragma unroll
-  for (int i = 0; i < NW; ++i) {
-    lo = (i == wi) ? v[i] : lo;
-    hi = (i == wi + 1) ? v[i] : hi;
-  }
-  uint64_t f = lo >> b;
-  if (b + bits > 64) f |= hi << (64 - b);
-  return static_cast<uint32_t>(f) & ((1u << bits) - 1u);
-}
-
 // D = floor(|V| / u) for one element with limbs xs[0..L-1] (L <= ML) on the
 // grid unit 2^g, as an NW-word integer; returns true when V < 0.
 template <int NW, int ML>
@@ -142,6 +127,38 @@ __device__ inline double signed_digit(uint32_t d, bool neg) {
   return (d == 0u) ? 0.0 : (neg ? -v : v);  // zero digits are +0.0
 }
 
+// Word i of v (0 beyond the top), by an unrolled select: no dynamic register indexing.
+template <int NW>
+__device__ inline uint64_t word_or_zero(const uint64_t (&v)[NW], int i) {
+  uint64_t r = 0;
+#pragma unroll
+  for (int j = 0; j < NW; ++j) r = (j == i) ? v[j] : r;
+  return r;
+}
+
+// Digit s of I (bits w(S-1-s) .. w(S-s)-1) to out[s * stride] for every s, read
+// upward from bit 0 through a two-word window: one select over the words per
+// 64 bits consumed instead of one per digit.
+template <int NW>
+__device__ inline void store_digits(const uint64_t (&I)[NW], int S, int w, bool neg, double* __restrict__ out,
+                                    int64_t stride) {
+  const uint64_t mask = (1ull << w) - 1ull;
+  uint64_t cur = I[0], nxt = NW > 1 ? I[1] : 0ull;
+  int wi = 0, b = 0;  // cur = word wi of I; b = next unread bit of cur
+  for (int j = 0; j < S; ++j) {
+    uint64_t f = cur >> b;
+    if (b + w > 64) f |= nxt << (64 - b);  // b > 64 - w > 0 here
+    out[static_cast<int64_t>(S - 1 - j) * stride] = signed_digit(static_cast<uint32_t>(f & mask), neg);
+    b += w;
+    if (b >= 64) {
+      b -= 64;
+      cur = nxt;
+      ++wi;
+      nxt = word_or_zero<NW>(I, wi + 1);
+    }
+  }
+}
+
 // Row-major output: D [S][rows][cols], the layout of the input planes.
 template <int NW, int ML>
 __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, int L, int S, int w, int axis,
@@ -157,8 +174,7 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
     load_limbs<ML>(X, plane, L, idx, xs);
     uint64_t I[NW];
     const bool neg = floor_on_grid<NW, ML>(xs, L, e - w * S, I);
-    for (int s = 0; s < S; ++s)
-      D[static_cast<int64_t>(s) * plane + idx] = signed_digit(field<NW>(I, w * (S - 1 - s), w), neg);
+    store_digits<NW>(I, S, w, neg, D + idx, plane);
   }
 }
 
@@ -201,8 +217,7 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
         if (valid[b]) {
           uint64_t I[NW];
           const bool neg = floor_on_grid<NW, ML>(xs[b], L, e - w * S, I);
-          for (int s = 0; s < S; ++s)
-            out[static_cast<int64_t>(s) * pplane] = signed_digit(field<NW>(I, w * (S - 1 - s), w), neg);
+          store_digits<NW>(I, S, w, neg, out, pplane);
         } else {
           for (int s = 0; s < S; ++s) out[static_cast<int64_t>(s) * pplane] = 0.0;
         }
