@@ -18,6 +18,11 @@ Prints one JSON line:
   wider digits whose level sums stay exact at this k; at least the digit bits of
   four 13-bit digits per limb), timed over a few steps; the headline ``value``
   keeps the workload's 13-bit digits unless ``--slice-bits`` says otherwise;
+* ``karatsuba`` and ``karatsuba_adaptive``: the same workload with the Karatsuba
+  schedule of the level products (fewer GEMMs of digit sums, the levels formed
+  exactly from their planes, bit-identical results), with the 13-bit digits and
+  with the adaptive width; the headline keeps the paper's pair schedule unless
+  ``--schedule karatsuba`` says otherwise;
 * ``cpu_baseline``: the CPU oracle's classic multiple-double GEMM (one
   sequential inner product per element, all host cores) timed on a bounded
   sample of the same product's rows.
@@ -118,7 +123,11 @@ def main(argv=None) -> int:
                     help="digit width of the timed product: 13 (the workload's digits and cutoff, default), "
                          "'auto' (the adaptive width) or 14..26")
     ap.add_argument("--adaptive-steps", type=int, default=5,
-                    help="steps of an extra adaptive-width measurement reported beside the 13-bit one (0: none)")
+                    help="steps of each extra measurement (adaptive width, Karatsuba schedule) reported beside "
+                         "the headline (0: none)")
+    ap.add_argument("--schedule", choices=("pairs", "karatsuba"), default="pairs",
+                    help="schedule of the level products of the timed product: the paper's digit pairs (default) "
+                         "or the Karatsuba schedule")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, run 3 device copies of this many MiB (calibrates the HBM byte "
                          "counters of a profiler run against a known size)")
@@ -157,12 +166,13 @@ def main(argv=None) -> int:
             opts["range_bits"] = w.range_bits
         return opts
 
-    def measure(opts, steps, warmup):
+    def measure(opts, steps, warmup, base_flags=0):
         """ms per step and per-stage ms of mdgemm_ex with these options."""
-        ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, **opts), dtype=torch.uint8, device=dev)
+        ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, flags=base_flags, **opts),
+                         dtype=torch.uint8, device=dev)
 
         def step(flags=0):
-            md.mdgemm_ex(A, B, C, workspace=ws, flags=flags, stream=stream, **opts)
+            md.mdgemm_ex(A, B, C, workspace=ws, flags=flags | base_flags, stream=stream, **opts)
 
         for _ in range(warmup):
             step()
@@ -179,9 +189,10 @@ def main(argv=None) -> int:
         return e0.elapsed_time(e1) / steps, stage_sum / steps
 
     bits_arg = md.MDGEMM_SLICE_BITS_AUTO if args.slice_bits == "auto" else int(args.slice_bits)
+    sched_flags = md.MDGEMM_KARATSUBA if args.schedule == "karatsuba" else 0
     opts = mode_opts(bits_arg)
-    bits, S, T = md.mdgemm_plan(w.m, w.n, w.k, w.limbs, **opts)
-    ms_per_step, stage_ms = measure(opts, args.steps, args.warmup)
+    bits, S, T = md.mdgemm_plan(w.m, w.n, w.k, w.limbs, flags=sched_flags, **opts)
+    ms_per_step, stage_ms = measure(opts, args.steps, args.warmup, sched_flags)
 
     if args.copy_probe_mib > 0:
         src = torch.ones(args.copy_probe_mib * (1 << 20) // 8, dtype=torch.float64, device=dev)
@@ -193,13 +204,17 @@ def main(argv=None) -> int:
 
     m, n, k, L = w.m, w.n, w.k, w.limbs
     pairs = workloads.pair_count(S, T)
+    info = md.mdgemm_schedule_info(m, n, k, S, T, bits=bits, flags=sched_flags)
     md_flops = w.md_flops()
-    slice_flops = 2.0 * m * n * k * pairs
+    # the GEMMs actually run: one per digit pair, or the Karatsuba schedule's products
+    slice_flops = 2.0 * m * n * k * info["terms"]
     value = md_flops / (ms_per_step * 1e-3) / 1e9
 
     bytes_exp = 8.0 * (m * k + k * n) + 4.0 * (m + n)
     bytes_split = 8.0 * L * (m * k + k * n) + 8.0 * S * (m * k + k * n) + 4.0 * (m + n)
-    bytes_acc = 8.0 * (T + 1) * m * n + 8.0 * L * m * n + 4.0 * (m + n)
+    # the Karatsuba schedule's combinations: each one reads two panels and writes one
+    bytes_split += 24.0 * k * ((info["combos_a"] - S) * m + (info["combos_b"] - S) * n)
+    bytes_acc = 8.0 * info["planes"] * m * n + 8.0 * L * m * n + 4.0 * (m + n)
     gemm_ms = stage_ms[2]
     achieved = slice_flops / (gemm_ms * 1e-3) / 1e12
     roofline = {
@@ -208,8 +223,8 @@ def main(argv=None) -> int:
         "peak": MFMA_F64_PEAK_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(achieved / MFMA_F64_PEAK_TFLOPS, 4),
-        # the stored counters were taken with the workload's 13-bit digits
-        "traffic": stored_traffic(args.config) if bits_arg == 13 else None,
+        # the stored counters were taken with the workload's 13-bit digits and pair schedule
+        "traffic": stored_traffic(args.config) if bits_arg == 13 and not sched_flags else None,
         "kernel": "slice_gemm_kernel (level GEMMs, v_mfma_f64_16x16x4f64)",
         "flops_per_launch": slice_flops,
         "avg_launch_ms": round(gemm_ms, 4),
@@ -226,6 +241,10 @@ def main(argv=None) -> int:
     }
     config = {"workload": f"{w.name}: {w.description}", "m": m, "n": n, "k": k, "limbs": L, "slices": S,
               "cutoff": T, "pairs": pairs, "seed": w.seed}
+    if sched_flags:
+        config["schedule"] = "karatsuba"
+        config["products"] = info["terms"]
+        config["workload"] += f"; Karatsuba schedule: {info['terms']} digit-sum products for the {pairs} pairs"
     if w.range_bits:
         config["range_bits"] = w.range_bits
     if bits != 13:
@@ -249,18 +268,27 @@ def main(argv=None) -> int:
         "stages": stages,
         "slice_gemm_share": round(stage_ms[2] / stage_ms.sum(), 4),
     }
-    if bits_arg == 13 and args.adaptive_steps > 0:
-        # the same workload with the adaptive width, reported beside the 13-bit digits
-        a_opts = mode_opts(md.MDGEMM_SLICE_BITS_AUTO)
-        a_bits, a_S, a_T = md.mdgemm_plan(m, n, k, L, **a_opts)
-        a_ms, a_stage = measure(a_opts, args.adaptive_steps, 2)
+    def extra(a_opts, flags):
+        """A few timed steps of the same workload with other digit options or schedule."""
+        a_bits, a_S, a_T = md.mdgemm_plan(m, n, k, L, flags=flags, **a_opts)
+        a_info = md.mdgemm_schedule_info(m, n, k, a_S, a_T, bits=a_bits, flags=flags)
+        a_ms, a_stage = measure(a_opts, args.adaptive_steps, 2, flags)
         a_pairs = workloads.pair_count(a_S, a_T)
-        a_tflops = 2.0 * m * n * k * a_pairs / (a_stage[2] * 1e-3) / 1e12
-        out["adaptive_width"] = {
-            "slice_bits": a_bits, "slices": a_S, "cutoff": a_T, "pairs": a_pairs, "steps": args.adaptive_steps,
-            "ms_per_step": round(a_ms, 4), "value": round(md_flops / (a_ms * 1e-3) / 1e9, 3),
+        a_tflops = 2.0 * m * n * k * a_info["terms"] / (a_stage[2] * 1e-3) / 1e12
+        return {
+            "slice_bits": a_bits, "slices": a_S, "cutoff": a_T, "pairs": a_pairs, "products": a_info["terms"],
+            "planes": a_info["planes"], "steps": args.adaptive_steps, "ms_per_step": round(a_ms, 4),
+            "value": round(md_flops / (a_ms * 1e-3) / 1e9, 3),
+            "stage_ms": [round(float(x), 4) for x in a_stage],
             "slice_gemm_TFLOP/s": round(a_tflops, 3), "frac": round(a_tflops / MFMA_F64_PEAK_TFLOPS, 4),
         }
+
+    if bits_arg == 13 and not sched_flags and args.adaptive_steps > 0:
+        # the same workload with the adaptive width and with the Karatsuba
+        # schedule, reported beside the paper's 13-bit digit pairs
+        out["adaptive_width"] = extra(mode_opts(md.MDGEMM_SLICE_BITS_AUTO), 0)
+        out["karatsuba"] = extra(mode_opts(13), md.MDGEMM_KARATSUBA)
+        out["karatsuba_adaptive"] = extra(mode_opts(md.MDGEMM_SLICE_BITS_AUTO), md.MDGEMM_KARATSUBA)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, A_h, B_h, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -70,6 +70,8 @@ extern "C" {
 #define MDGEMM_CHECK_FINITE 1u /* scan A and B for inf/nan first; synchronizes the stream */
 #define MDGEMM_SYNC 2u         /* synchronize the stream before returning and report kernel errors */
 #define MDGEMM_TIME_STAGES 4u  /* record HIP events between stages; read with mdgemm_stage_times() */
+#define MDGEMM_KARATSUBA 8u    /* level products by the Karatsuba schedule where it pays (see below) */
+#define MDGEMM_KARATSUBA_MIN_TERMS 16u /* the Karatsuba schedule with the fewest GEMMs, always */
 
 /* cutoff selectors for mdgemm_opts.cutoff (else an explicit T in 0 .. 2S-2) */
 #define MDGEMM_CUTOFF_DEFAULT -1  /* T = S - 1: the pair set of the rewritten product */
@@ -81,7 +83,7 @@ typedef struct mdgemm_opts {
   size_t workspace_bytes; /* size of `workspace` in bytes */
   int slices_per_limb;    /* 13-bit digits per limb, S = limbs * slices_per_limb <= 64; 0 = 4 */
   int cutoff;             /* largest kept p + q; MDGEMM_CUTOFF_DEFAULT or _ALL or 0..2S-2 */
-  unsigned flags;         /* MDGEMM_CHECK_FINITE | MDGEMM_SYNC | MDGEMM_TIME_STAGES */
+  unsigned flags;         /* MDGEMM_CHECK_FINITE, _SYNC, _TIME_STAGES, _KARATSUBA, _KARATSUBA_MIN_TERMS */
   int slice_bits;         /* digit width w: 0 = 13 (section 2), 1..26, or MDGEMM_SLICE_BITS_AUTO */
   int slices;             /* digits per element S; 0 = derived (see below) */
   int range_bits;         /* range balancing: full precision down to 2^-range_bits of the line; 0 = off */
@@ -134,9 +136,12 @@ int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const do
 
 /* Bytes of device workspace mdgemm_ex needs for this product and these options
  * (0 for an empty product; SIZE_MAX for invalid arguments).  Layout, each part
- * aligned to 256 bytes: EA int32[m], EB int32[n], flag int32, the digit panels
- * DAt f64[S][kp][mp] and DBp f64[S][kp][np] (kp = k rounded up to 16, mp and np =
- * m and n rounded up to 128), G f64[T+1][m][n]. */
+ * aligned to 256 bytes: EA int32[m], EB int32[n], flag int32, the schedule's
+ * job table (32-bit words), the combination panels of A f64[CA][kp][mp] and of
+ * B f64[CB][kp][np] (kp = k rounded up to 16, mp and np = m and n rounded up to
+ * 128; the first S combinations are the digits, CA = CB = S for the pair
+ * schedule), the GEMM output planes f64[P][m][n] (P = T+1 levels for the pair
+ * schedule, the schedule's planes for MDGEMM_KARATSUBA). */
 size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts);
 
 /* C = A.B with explicit options (opts may be NULL for the defaults).  Runs, in
@@ -209,12 +214,82 @@ int mdgemm_split_panel(int64_t rows, int64_t cols, int limbs, int slices, int sl
  * per_pair == 0: out [T+1][m][n], out[t] = sum over p + q = t (0 <= p, q < S) of
  * DA_p . DB_q for t = 0..cutoff.  per_pair != 0: out [S][S][m][n],
  * out[p][q] = DA_p . DB_q for every p + q <= cutoff (other planes untouched; one
- * launch per 256 pairs).
+ * launch).
  * Exact in FP64 (any summation order) because every partial sum is an integer
  * below 2^53; returns MDGEMM_EEXACT when pairs_t * k * (2^w - 1)^2 >= 2^53.
  * S in 1..64, slice_bits 1..26, cutoff in 0..2S-2. */
 int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, int per_pair,
                       const double* DAt, const double* DBp, double* out, void* stream);
+/* (The job table of mdgemm_slice_gemm is placed in the library buffer, so the
+ * call is refused with MDGEMM_EINVAL while `stream` captures a graph.) */
+
+/* ---- schedules of the level products ----------------------------------------
+ * Section 2 (equation (3), the rewritten product) multiplies every digit pair
+ * (p, q) with p + q <= T and sums the pairs of a level t = p + q: the pair
+ * schedule, (T+1) levels from sum_t pairs_t GEMMs of length k.  With the digits
+ * of an element read as the coefficients of a polynomial in 2^-w, level t is
+ * coefficient t of the product of two polynomials, and Karatsuba's identity
+ * (a0 + a1 x)(b0 + b1 x) = a0 b0 + x [(a0 + a1)(b0 + b1) - a0 b0 - a1 b1] + x^2 a1 b1,
+ * applied recursively and truncated at T, forms the same coefficients from
+ * fewer products of digit sums ("combinations").  Everything stays integer:
+ * combinations are exact, every GEMM job keeps k * sum(|comb a| |comb b|) *
+ * (2^w - 1)^2 < 2^53 (|comb| = digits in the sum), and the levels are formed
+ * from the planes in 64-bit integers, so both schedules give bit-identical
+ * levels and products.  Double-double with T = 7 takes 24 products instead of
+ * 36, quad-double (16 digits, T = 15) 69 instead of 136.  The schedule also
+ * costs output planes (one per distinct set of level coefficients), level
+ * entries in the accumulation and combination panels; the planner weighs them
+ * against the GEMMs for the product's shape (m, n, k) with rates measured on
+ * MI355X and keeps the pair schedule where Karatsuba would not pay (small
+ * products, whose combination panels cost as much as a GEMM).
+ * MDGEMM_KARATSUBA_MIN_TERMS takes the plan with the fewest GEMMs whatever the
+ * other costs (it overrides MDGEMM_KARATSUBA). */
+
+#define MDGEMM_SCHEDULE_INFO 9 /* entries written by mdgemm_schedule_info */
+
+/* Size of the schedule mdgemm_ex uses for an m x k by k x n product with
+ * S = slices digits of slice_bits bits, cutoff T, and flags (MDGEMM_KARATSUBA,
+ * MDGEMM_KARATSUBA_MIN_TERMS, or 0 for the pair schedule).  Writes min(count, MDGEMM_SCHEDULE_INFO) values:
+ *   info[0] GEMM terms (products of two combinations, k long each),
+ *   info[1] GEMM jobs, info[2] output planes, info[3] combinations of A,
+ *   info[4] combinations of B, info[5] level entries, info[6] largest job weight
+ *   sum(|comb a| |comb b|), info[7] deepest combination (0 = digits only),
+ *   info[8] 1 when the planes are the levels themselves (pair schedule).
+ * Host only (no HIP call).  Returns the count written or MDGEMM_EINVAL. */
+int mdgemm_schedule_info(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, unsigned flags,
+                         int64_t* info, int count);
+
+/* The schedule itself, for checking (host only).  Any pointer may be NULL;
+ * sizes from mdgemm_schedule_info:
+ *   mask_a[CA], mask_b[CB]: the digit set of every combination (bit p = digit p);
+ *   parents_a[2 CA], parents_b[2 CB]: combination c >= S is the sum of
+ *     combinations parents[2c] and parents[2c+1] (-1, -1 for the digits c < S);
+ *   jobs[3 J]: first pair, pair count, output plane of job j;
+ *   pairs[2 terms]: (combination of A, combination of B) of every pair;
+ *   plane_first[P + 1], entries[2 E]: plane j enters the levels
+ *     entries[2e] with coefficient entries[2e+1] for plane_first[j] <= e < plane_first[j+1].
+ * Returns MDGEMM_OK or MDGEMM_EINVAL. */
+int mdgemm_schedule_export(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, unsigned flags,
+                           uint64_t* mask_a, int32_t* parents_a, uint64_t* mask_b, int32_t* parents_b, int32_t* jobs,
+                           int32_t* pairs, int32_t* plane_first, int32_t* entries);
+
+/* Workspace bytes of mdgemm_schedule_levels (SIZE_MAX for invalid arguments). */
+size_t mdgemm_schedule_workspace_bytes(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff,
+                                       unsigned flags);
+
+/* Step a3 by a schedule: the levels G [cutoff+1][m][n] (integer-valued doubles)
+ * of the digit panels DAt [S][kp][mp] and DBp [S][kp][np] (as for
+ * mdgemm_slice_gemm), computed by the schedule that `flags` selects
+ * (MDGEMM_KARATSUBA or 0): the digit panels are copied into the workspace, the
+ * combinations formed, the schedule's GEMMs run, and for the Karatsuba schedule
+ * the levels formed from the planes in 64-bit integers.  The result equals
+ * mdgemm_slice_gemm(per_pair = 0) bit for bit.  workspace: caller-owned device
+ * buffer of mdgemm_schedule_workspace_bytes() bytes, or NULL for the library
+ * buffer (then refused with MDGEMM_EINVAL while `stream` captures a graph).
+ * Returns MDGEMM_EEXACT when pairs_t * k * (2^w - 1)^2 >= 2^53. */
+int mdgemm_schedule_levels(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, unsigned flags,
+                           const double* DAt, const double* DBp, double* G, void* workspace, size_t workspace_bytes,
+                           void* stream);
 
 /* Step a4 alone, the exact accumulation (section 2, steps 4-5), exported for
  * checking.  G [levels][m][n] integer-valued with |G| < 2^53, levels 1..127,

@@ -53,6 +53,36 @@ __device__ inline void add_shifted_signed(uint64_t (&N)[NW], int64_t g, int sh) 
 // are the digit of column j (placed into N, whose bits there are still zero)
 // and carry = floor(v / 2^w).  |G_t| < 2^53 keeps |v| < 2^54, so int64 never
 // overflows; the last carry, signed, is added above column T.
+// The digits fill N from bit 0 upward: `word` collects the bits of word wi of
+// N, `fill` of them so far; a full word is placed with one select over the words.
+template <int NW>
+struct CarryChain {
+  uint64_t word = 0;
+  int fill = 0, wi = 0;
+  int64_t carry = 0;
+
+  __device__ inline void step(uint64_t (&N)[NW], int64_t g, int w, uint64_t mask) {
+    const int64_t v = g + carry;
+    const uint64_t d = static_cast<uint64_t>(v) & mask;
+    carry = v >> w;  // arithmetic shift: floor division
+    word |= d << fill;
+    fill += w;
+    if (fill >= 64) {
+#pragma unroll
+      for (int i = 0; i < NW; ++i) N[i] = (i == wi) ? word : N[i];
+      ++wi;
+      fill -= 64;
+      word = fill ? d >> (w - fill) : 0ull;  // the bits of d beyond the full word
+    }
+  }
+  __device__ inline void finish(uint64_t (&N)[NW], int w, int T) {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) N[i] = (i == wi) ? word : N[i];
+    if (carry != 0) add_shifted_signed<NW>(N, carry, w * (T + 1));
+  }
+};
+
+// The chain over levels read from G [levels][m][n] (integer-valued doubles).
 // Loads are issued eight levels at a time before any of them is used, so a
 // thread keeps up to eight independent loads in flight.
 template <int NW>
@@ -62,11 +92,7 @@ __device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __rest
   for (int i = 0; i < NW; ++i) N[i] = 0;
   const int T = levels - 1;
   const uint64_t mask = (1ull << w) - 1ull;
-  int64_t carry = 0;
-  // the digits fill N from bit 0 upward: `word` collects the bits of word wi of N,
-  // `fill` of them so far; a full word is placed with one select over the words
-  uint64_t word = 0;
-  int fill = 0, wi = 0;
+  CarryChain<NW> chain;
   for (int t0 = T; t0 >= 0; t0 -= 8) {
     // unconditional loads (levels below 0 re-read level 0 and are discarded),
     // so that the eight loads go out back to back
@@ -78,25 +104,11 @@ __device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __rest
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int t = t0 - u;
-      if (t < 0) break;
-      const int64_t v = static_cast<int64_t>(g[u]) + carry;  // exact: |G_t| < 2^53
-      const uint64_t d = static_cast<uint64_t>(v) & mask;
-      carry = v >> w;  // arithmetic shift: floor division
-      word |= d << fill;
-      fill += w;
-      if (fill >= 64) {
-#pragma unroll
-        for (int i = 0; i < NW; ++i) N[i] = (i == wi) ? word : N[i];
-        ++wi;
-        fill -= 64;
-        word = fill ? d >> (w - fill) : 0ull;  // the bits of d beyond the full word
-      }
+      if (t0 - u < 0) break;
+      chain.step(N, static_cast<int64_t>(g[u]), w, mask);  // exact: |G_t| < 2^53
     }
   }
-#pragma unroll
-  for (int i = 0; i < NW; ++i) N[i] = (i == wi) ? word : N[i];
-  if (carry != 0) add_shifted_signed<NW>(N, carry, w * (T + 1));
+  chain.finish(N, w, T);
 }
 
 // Bit `pos` (0 <= pos < 64 NW) of v.
@@ -216,6 +228,92 @@ __global__ void __launch_bounds__(256) accumulate_kernel(int64_t m, int64_t n, i
   }
 }
 
+// Levels from the output planes of a Karatsuba schedule: each plane enters a
+// few levels with small integer coefficients.  Every thread keeps its levels
+// as 64-bit integers in LDS (level t of thread x at lv[t * blockDim.x + x], one
+// more slot t = T + 1 takes the padding entries), reads each plane once (a
+// batch of 8 loads in flight while the previous batch is applied) and adds
+// coef * plane to the levels of the plane's entries.
+// The entries come four at a time (one 8-byte scalar load); the levels of one
+// plane are distinct, so the four old values are read before any is written
+// and the four read-modify-writes overlap.  Plane values are integers below
+// 2^53 and the level sums are the exact G_t (|G_t| < 2^53), so no step rounds.
+// Then the carry chain and rounding of accum_renorm_kernel, or (C == nullptr)
+// the levels written out as doubles.
+constexpr int kBatch = 8;
+
+template <int NW>
+__global__ void __launch_bounds__(256) plan_accum_kernel(int64_t m, int64_t n, int L, int levels, int w, int planes,
+                                                         const double* __restrict__ P,
+                                                         const uint32_t* __restrict__ chunk_first,
+                                                         const uint2* __restrict__ chunks,
+                                                         const int32_t* __restrict__ EA,
+                                                         const int32_t* __restrict__ EB, double* __restrict__ C,
+                                                         double* __restrict__ Gout) {
+  extern __shared__ int64_t lv[];
+  const int bd = blockDim.x;
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * bd + threadIdx.x;
+  if (j >= n) return;  // no barriers below: every thread owns its own LDS slots
+  int64_t* my = lv + threadIdx.x;
+  const int64_t plane = m * n;
+  const int T = levels - 1;
+  const uint64_t mask = (1ull << w) - 1ull;
+  const int ebj = C ? EB[j] : 0;
+  for (int64_t i = blockIdx.y; i < m; i += gridDim.y) {
+    const int64_t idx = i * n + j;
+    for (int t = 0; t <= levels; ++t) my[t * bd] = 0;
+    // planes in batches of kBatch: the next batch's loads are in flight while
+    // the current batch's entries are applied
+    double cur[kBatch], nxt[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) cur[u] = P[static_cast<int64_t>(u < planes ? u : planes - 1) * plane + idx];
+    for (int p0 = 0; p0 < planes; p0 += kBatch) {
+      if (p0 + kBatch < planes) {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          const int pl = p0 + kBatch + u < planes ? p0 + kBatch + u : planes - 1;
+          nxt[u] = P[static_cast<int64_t>(pl) * plane + idx];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int pl = p0 + u;
+        if (pl >= planes) break;
+        const int64_t v = static_cast<int64_t>(cur[u]);  // exact: integer below 2^53
+        const uint32_t c1 = chunk_first[pl + 1];
+        for (uint32_t c = chunk_first[pl]; c < c1; ++c) {
+          const uint2 ch = chunks[c];
+          const uint32_t e[4] = {ch.x & 0xffffu, ch.x >> 16, ch.y & 0xffffu, ch.y >> 16};
+          int64_t* a[4];
+          int64_t old[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            a[q] = my + static_cast<int>(e[q] & 0xffu) * bd;
+            old[q] = *a[q];
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            *a[q] = old[q] + static_cast<int64_t>(static_cast<int8_t>(e[q] >> 8)) * v;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) cur[u] = nxt[u];
+    }
+    if (!C) {
+      for (int t = 0; t < levels; ++t) Gout[static_cast<int64_t>(t) * plane + idx] = static_cast<double>(my[t * bd]);
+      continue;
+    }
+    uint64_t N[NW];
+#pragma unroll
+    for (int q = 0; q < NW; ++q) N[q] = 0;
+    CarryChain<NW> chain;
+    for (int t = T; t >= 0; --t) chain.step(N, my[t * bd], w, mask);
+    chain.finish(N, w, T);
+    const int scale = EA[i] + ebj - 2 * w - w * T;
+    round_limbs<NW>(N, L, scale, C, plane, idx);
+  }
+}
+
 }  // namespace
 
 // Words for |N| < 2^(w T + 54) plus a sign bit.
@@ -263,6 +361,26 @@ hipError_t launch_accum_renorm(int64_t m, int64_t n, int L, int levels, int w, c
   return with_words(accum_words(levels, w), [&](auto nw) {
     hipLaunchKernelGGL(accum_renorm_kernel<decltype(nw)::value>, grid, dim3(256), 0, stream, m, n, L, levels, w, G,
                        EA, EB, C);
+  });
+}
+
+hipError_t launch_plan_accum(int64_t m, int64_t n, int L, int levels, int w, int planes, const double* P,
+                             const uint32_t* chunk_first, const uint32_t* chunks, const int32_t* EA,
+                             const int32_t* EB, double* C, double* Gout, hipStream_t stream) {
+  if (m == 0 || n == 0) return hipSuccess;
+  // (levels + 1) x threads x 8 bytes of LDS: at most 32 KB up to 63 levels, 64 KB for 127
+  const int bd = levels < 16 ? 256 : (levels < 32 ? 128 : 64);
+  const dim3 grid(static_cast<unsigned>((n + bd - 1) / bd), static_cast<unsigned>(m < 65535 ? m : 65535));
+  const size_t lds = sizeof(int64_t) * static_cast<size_t>(levels + 1) * bd;
+  const uint2* ch = reinterpret_cast<const uint2*>(chunks);
+  if (!C) {
+    hipLaunchKernelGGL(plan_accum_kernel<2>, grid, dim3(bd), lds, stream, m, n, L, levels, w, planes, P,
+                       chunk_first, ch, EA, EB, C, Gout);
+    return hipGetLastError();
+  }
+  return with_words(accum_words(levels, w), [&](auto nw) {
+    hipLaunchKernelGGL(plan_accum_kernel<decltype(nw)::value>, grid, dim3(bd), lds, stream, m, n, L, levels, w,
+                       planes, P, chunk_first, ch, EA, EB, C, Gout);
   });
 }
 

@@ -10,10 +10,15 @@
 // (a4 + a5).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
+#include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <map>
+#include <memory>
 #include <mutex>
+#include <tuple>
 #include <vector>
 
 #include "internal.h"
@@ -27,7 +32,6 @@ static_assert(MDGEMM_MAX_LIMBS == mdg::kMaxLimbs && MDGEMM_MAX_SLICES == mdg::kM
 
 namespace {
 
-using mdg::JobTable;
 
 constexpr size_t kAlign = 256;
 constexpr int kStages = 4;
@@ -70,53 +74,103 @@ bool width_ok(int S, int w) { return S >= 1 && S <= MDGEMM_MAX_SLICES && w >= 1 
 // w (levels - 1) + 55 bits must fit the widest accumulation (kZWords words)
 bool levels_ok(int levels, int w) { return levels >= 1 && levels <= mdg::kMaxLevels && mdg::accum_words(levels, w) <= mdg::kZWords; }
 
-// ---- job tables ---------------------------------------------------------------
+// ---- schedules -------------------------------------------------------------
 
-// Levels t = 0..T, heaviest (most pairs) first so that long K loops start early.
-JobTable level_jobs(int S, int T) {
-  JobTable jt;
-  std::memset(&jt, 0, sizeof jt);
-  std::vector<int> order;
-  for (int t = 0; t <= T; ++t) order.push_back(t);
-  auto npairs = [S](int t) {
-    int lo = t - (S - 1) > 0 ? t - (S - 1) : 0;
-    int hi = t < S - 1 ? t : S - 1;
-    return hi - lo + 1;
-  };
-  // stable sort by decreasing pair count
-  for (size_t i = 1; i < order.size(); ++i)
-    for (size_t j = i; j > 0 && npairs(order[j]) > npairs(order[j - 1]); --j) std::swap(order[j], order[j - 1]);
-  jt.njobs = static_cast<int>(order.size());
-  for (int j = 0; j < jt.njobs; ++j) {
-    int t = order[j];
-    int lo = t - (S - 1) > 0 ? t - (S - 1) : 0;
-    jt.p_first[j] = static_cast<uint16_t>(lo);
-    jt.q_first[j] = static_cast<uint16_t>(t - lo);
-    jt.npairs[j] = static_cast<uint16_t>(npairs(t));
-    jt.out[j] = static_cast<uint16_t>(t);
-  }
-  return jt;
+// Largest digit-count weight |combination a| |combination b| one GEMM job may
+// sum: k weight (2^w - 1)^2 < 2^53, rounded down to a power of two (so that
+// nearby k share a cached schedule), at most 2^20.
+int64_t job_budget(int64_t k, int w) {
+  const uint64_t dmax = (1ull << w) - 1ull;
+  const unsigned __int128 per = static_cast<unsigned __int128>(k < 1 ? 1 : k) * (dmax * dmax);
+  const unsigned __int128 lim = (static_cast<unsigned __int128>(1) << 53) - 1;
+  int64_t b = static_cast<int64_t>(std::min<unsigned __int128>(lim / per, 1u << 20));
+  int64_t p = 1;
+  while (p * 2 <= b) p *= 2;
+  return b < 1 ? 0 : p;
 }
 
-// Every pair (p, q) with p + q <= T, written to plane p*S + q; one table per
-// launch of at most kMaxJobs pairs.
-std::vector<JobTable> pair_jobs(int S, int T) {
-  std::vector<JobTable> tables;
-  for (int p = 0; p < S; ++p)
-    for (int q = 0; q < S; ++q) {
-      if (p + q > T) continue;
-      if (tables.empty() || tables.back().njobs == mdg::kMaxJobs) {
-        tables.emplace_back();
-        std::memset(&tables.back(), 0, sizeof(JobTable));
-      }
-      JobTable& jt = tables.back();
-      const int j = jt.njobs++;
-      jt.p_first[j] = static_cast<uint16_t>(p);
-      jt.q_first[j] = static_cast<uint16_t>(q);
-      jt.npairs[j] = 1;
-      jt.out[j] = static_cast<uint16_t>(p * S + q);
-    }
-  return tables;
+// Costs of a schedule's planes, level entries and combination panels relative
+// to one GEMM term, from rates measured on MI355X: a GEMM term costs 2k flops per
+// output element at ~70 TFLOP/s; a plane 16 bytes per element (written by the
+// GEMM, read by the accumulation) at ~4.5 TB/s, times the accumulation's
+// occupancy penalty (its LDS holds every level of a thread's element: 256
+// threads per block up to 15 levels, 128 up to 31, 64 beyond, where the plane
+// reads become latency-bound: measured ~1.4x and ~4x the HBM time); a level
+// entry ~0.1 ps per element; a combination panel of A reads two m x k panels
+// and writes one (24 m k bytes at ~4.5 TB/s), of B likewise with k x n.  Each
+// size enters as a power of sqrt(2) (its code 2 log2(x), rounded), so that
+// nearby shapes share a cached schedule.
+constexpr double kTermRate = 70e12, kHbmRate = 4.5e12, kEntrySeconds = 0.1e-12;
+
+int size_code(int64_t x) { return static_cast<int>(std::lround(2.0 * std::log2(static_cast<double>(x < 1 ? 1 : x)))); }
+double from_code(int c) { return std::exp2(0.5 * c); }
+
+mdg::ScheduleCosts schedule_costs(int mcode, int ncode, int kcode, int levels) {
+  const double m = from_code(mcode), n = from_code(ncode), k = from_code(kcode);
+  const double term = 2.0 * k / kTermRate;  // seconds per output element
+  const double occupancy = levels < 16 ? 1.0 : (levels < 32 ? 1.4 : 4.0);
+  mdg::ScheduleCosts c;
+  c.plane = 16.0 * occupancy / kHbmRate / term;
+  c.entry = kEntrySeconds / term;
+  c.combo_a = 24.0 * m * k / kHbmRate / (term * m * n);
+  c.combo_b = 24.0 * k * n / kHbmRate / (term * m * n);
+  return c;
+}
+
+// A schedule with its device table.
+struct Planned {
+  mdg::Schedule s;
+  mdg::ScheduleTable t;
+};
+
+struct ScheduleCache {
+  std::mutex mu;
+  std::map<std::tuple<int, int, int64_t, int, int, int, int>, std::shared_ptr<const Planned>> map;
+};
+ScheduleCache& schedule_cache() {
+  static ScheduleCache c;
+  return c;
+}
+
+// kKaratsuba: the cost model's choice (may be the pair schedule);
+// kKaratsubaMin: the Karatsuba schedule with the fewest GEMM terms.
+enum class Kind { kLevels = 0, kPerPair = 1, kKaratsuba = 2, kKaratsubaMin = 3 };
+
+Kind kind_of(unsigned flags) {
+  if (flags & MDGEMM_KARATSUBA_MIN_TERMS) return Kind::kKaratsubaMin;
+  return (flags & MDGEMM_KARATSUBA) ? Kind::kKaratsuba : Kind::kLevels;
+}
+
+// The schedule of the level products for S digits, cutoff T, an m x k by k x n
+// product and width w; built once per key and kept for the life of the process.
+std::shared_ptr<const Planned> schedule_for(int S, int T, int64_t m, int64_t n, int64_t k, int w, Kind kind) {
+  const bool kara = kind == Kind::kKaratsuba || kind == Kind::kKaratsubaMin;
+  const bool model = kind == Kind::kKaratsuba;
+  const int64_t budget = kara ? job_budget(k, w) : 0;
+  const int mc = model ? size_code(m) : 0, nc = model ? size_code(n) : 0, kc = model ? size_code(k) : 0;
+  const auto key = std::make_tuple(S, T, budget, mc, nc, kc, static_cast<int>(kind));
+  ScheduleCache& c = schedule_cache();
+  {
+    std::lock_guard<std::mutex> lock(c.mu);
+    auto it = c.map.find(key);
+    if (it != c.map.end()) return it->second;
+  }
+  auto pl = std::make_shared<Planned>();
+  if (kind == Kind::kLevels) pl->s = mdg::pair_schedule(S, T);
+  else if (kind == Kind::kPerPair) pl->s = mdg::per_pair_schedule(S, T);
+  else if (kind == Kind::kKaratsuba)
+    pl->s = mdg::karatsuba_schedule(S, T, budget, schedule_costs(mc, nc, kc, T + 1), true);
+  else pl->s = mdg::karatsuba_schedule(S, T, budget, mdg::ScheduleCosts{}, false);
+  pl->t = mdg::schedule_table(pl->s);
+  std::shared_ptr<const Planned> sp = pl;
+  std::lock_guard<std::mutex> lock(c.mu);
+  return c.map.emplace(key, sp).first->second;
+}
+
+// Every job's digit weight within the exactness bound (the budget guarantees it
+// for Karatsuba schedules; pair schedules are covered by the level check).
+bool schedule_exact(const mdg::Schedule& s, int64_t k, int w) {
+  return s.direct_levels || exact_ok(k, static_cast<int>(s.max_job_weight), w);
 }
 
 // ---- options ----------------------------------------------------------------
@@ -125,6 +179,7 @@ struct Resolved {
   int S = 0, T = 0, w = mdg::kSliceBits;
   hipStream_t stream = nullptr;
   unsigned flags = 0;
+  Kind kind = Kind::kLevels;  // pair schedule, or Karatsuba (see kind_of)
 };
 
 // Extra digits for elements down to range_bits below their line's exponent.
@@ -140,19 +195,28 @@ int cutoff_for(int cutoff, int S0, int D) {
 // Adaptive width: among w = 13..26 with S0 = ceil(52 L / w) base digits (the digit
 // bits of four 13-bit digits per limb), D = ceil(range_bits / w) extra digits,
 // S = S0 + D and the requested cutoff, those that are valid and whose levels stay
-// exact, the fewest pairs, the wider digit on a tie.  Returns false when none
-// qualifies.
-bool auto_width(int limbs, int64_t k, int range_bits, int cutoff, int* w_out, int* S0_out) {
-  int best_pairs = 0;
+// exact, the cheapest, the wider digit on a tie.  The cost is the pair count, or
+// with the Karatsuba schedule the schedule's cost for this shape (GEMM terms plus
+// planes, level entries and combinations; wider digits leave less room for
+// digit sums).  Returns false when none qualifies.
+bool auto_width(int limbs, int64_t m, int64_t n, int64_t k, int range_bits, int cutoff, Kind kind, int* w_out,
+                int* S0_out) {
+  double best_cost = 0.0;
   bool found = false;
   for (int w = mdg::kSliceBits; w <= mdg::kMaxSliceBits; ++w) {
     const int S0 = (4 * mdg::kSliceBits * limbs + w - 1) / w, D = range_digits(range_bits, w);
     const int S = S0 + D, T = cutoff_for(cutoff, S0, D);
     if (!width_ok(S, w) || T < 0 || T > 2 * S - 2 || !levels_ok(T + 1, w) || !exact_ok(k, max_pairs(S, T), w))
       continue;
-    const int pairs = pair_count(S, T);
-    if (!found || pairs <= best_pairs) {
-      best_pairs = pairs;
+    double cost = pair_count(S, T);
+    if (kind == Kind::kKaratsuba) {
+      const auto pl = schedule_for(S, T, m, n, k, w, kind);
+      cost = mdg::schedule_cost(pl->s, schedule_costs(size_code(m), size_code(n), size_code(k), T + 1));
+    } else if (kind == Kind::kKaratsubaMin) {
+      cost = schedule_for(S, T, m, n, k, w, kind)->s.terms;
+    }
+    if (!found || cost <= best_cost) {
+      best_cost = cost;
       *w_out = w;
       *S0_out = S0;
       found = true;
@@ -162,15 +226,16 @@ bool auto_width(int limbs, int64_t k, int range_bits, int cutoff, int* w_out, in
 }
 
 // Digit width, digit count and cutoff of a product with reduction length k.
-int resolve(int limbs, int64_t k, const mdgemm_opts* opts, Resolved* r) {
+int resolve(int limbs, int64_t m, int64_t n, int64_t k, const mdgemm_opts* opts, Resolved* r) {
   if (limbs < 1 || limbs > MDGEMM_MAX_LIMBS) return MDGEMM_EINVAL;
+  r->kind = kind_of(opts ? opts->flags : 0u);
   const int bits = opts ? opts->slice_bits : 0;
   const int slices = opts ? opts->slices : 0;
   const int range_bits = opts ? opts->range_bits : 0;
   if (slices < 0 || range_bits < 0 || range_bits > mdg::kMaxDigitBits) return MDGEMM_EINVAL;
   if (bits == MDGEMM_SLICE_BITS_AUTO) {
     if (slices != 0) return MDGEMM_EINVAL;
-    if (!auto_width(limbs, k, range_bits, opts->cutoff, &r->w, &r->S)) return MDGEMM_EEXACT;
+    if (!auto_width(limbs, m, n, k, range_bits, opts->cutoff, r->kind, &r->w, &r->S)) return MDGEMM_EEXACT;
   } else if (bits == 0 || bits == mdg::kSliceBits) {
     r->w = mdg::kSliceBits;
     int spl = opts ? opts->slices_per_limb : 0;
@@ -200,13 +265,17 @@ int resolve(int limbs, int64_t k, const mdgemm_opts* opts, Resolved* r) {
 }
 
 struct Layout {
-  size_t ea = 0, eb = 0, flag = 0, da = 0, db = 0, g = 0, total = 0;
+  size_t ea = 0, eb = 0, flag = 0, table = 0, da = 0, db = 0, g = 0, total = 0;
 };
 
-bool layout(int64_t m, int64_t n, int64_t k, const Resolved& r, Layout* L) {
+// EA | EB | flag | schedule table | A's combinations | B's combinations | planes,
+// each aligned to 256 bytes (combinations 0..S-1 are the digit panels).
+bool layout(int64_t m, int64_t n, int64_t k, const Planned& pl, Layout* L) {
+  const mdg::Schedule& sch = pl.s;
+  const double ca = static_cast<double>(sch.mask_a.size()), cb = static_cast<double>(sch.mask_b.size());
   // all products below 2^62 so that size arithmetic cannot overflow
-  const double approx = (double)r.S * (double)m * (double)k + (double)r.S * (double)k * (double)n +
-                        (double)(r.T + 1) * (double)m * (double)n;
+  const double approx = ca * (double)m * (double)k + cb * (double)k * (double)n +
+                        (double)sch.planes * (double)m * (double)n;
   if (approx * 8.0 > 4.0e18) return false;
   size_t off = 0;
   L->ea = off;
@@ -215,14 +284,16 @@ bool layout(int64_t m, int64_t n, int64_t k, const Resolved& r, Layout* L) {
   off += align_up(sizeof(int32_t) * static_cast<size_t>(n));
   L->flag = off;
   off += align_up(sizeof(int32_t));
+  L->table = off;
+  off += align_up(sizeof(uint32_t) * pl.t.words.size());
   L->da = off;
   const size_t kp = static_cast<size_t>(mdg::panel_k(k)), mp = static_cast<size_t>(mdg::panel_mn(m)),
                np = static_cast<size_t>(mdg::panel_mn(n));
-  off += align_up(sizeof(double) * static_cast<size_t>(r.S) * kp * mp);
+  off += align_up(sizeof(double) * sch.mask_a.size() * kp * mp);
   L->db = off;
-  off += align_up(sizeof(double) * static_cast<size_t>(r.S) * kp * np);
+  off += align_up(sizeof(double) * sch.mask_b.size() * kp * np);
   L->g = off;
-  off += align_up(sizeof(double) * static_cast<size_t>(r.T + 1) * static_cast<size_t>(m) * static_cast<size_t>(n));
+  off += align_up(sizeof(double) * static_cast<size_t>(sch.planes) * static_cast<size_t>(m) * static_cast<size_t>(n));
   L->total = off;
   return true;
 }
@@ -282,6 +353,47 @@ int cached_workspace(Cache& c, size_t need, void** out, int* dev_out) {
   return MDGEMM_OK;
 }
 
+// The library buffer of the current device, held for one call: acquire() takes
+// the cache's mutex, grows the buffer and makes `stream` wait for the previous
+// user's work; release() records this call's end for the next user and lets go
+// of the mutex (also when enqueueing stopped at an error).  Refused while
+// `stream` is capturing a graph: the graph would keep an address that a later,
+// larger call may free.
+class LibraryBuffer {
+ public:
+  ~LibraryBuffer() { release(MDGEMM_OK); }
+  int acquire(size_t need, hipStream_t stream, char** out) {
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cap) != hipSuccess) return MDGEMM_EHIP;
+    if (cap != hipStreamCaptureStatusNone) return MDGEMM_EINVAL;
+    lock_ = std::unique_lock<std::mutex>(cache().mu);
+    void* p = nullptr;
+    int dev = -1;
+    const int st = cached_workspace(cache(), need, &p, &dev);
+    if (st != MDGEMM_OK) {
+      lock_.unlock();
+      return st;
+    }
+    dev_ = dev;
+    stream_ = stream;
+    if (hipStreamWaitEvent(stream, cache().last[dev_], 0) != hipSuccess) return release(MDGEMM_EHIP);
+    *out = static_cast<char*>(p);
+    return MDGEMM_OK;
+  }
+  int release(int st) {
+    if (dev_ < 0) return st;
+    const bool ok = hipEventRecord(cache().last[dev_], stream_) == hipSuccess;
+    dev_ = -1;
+    lock_.unlock();
+    return (st == MDGEMM_OK && !ok) ? MDGEMM_EHIP : st;
+  }
+
+ private:
+  std::unique_lock<std::mutex> lock_;
+  int dev_ = -1;
+  hipStream_t stream_ = nullptr;
+};
+
 // ---- stage timing ------------------------------------------------------------
 
 struct Timing {
@@ -313,6 +425,36 @@ inline int hip_status(hipError_t e) { return e == hipSuccess ? MDGEMM_OK : MDGEM
     if (st_ != MDGEMM_OK) return st_; \
   } while (0)
 
+// Pointers into a workspace laid out by layout().
+struct Parts {
+  int32_t *EA, *EB, *flag;
+  uint32_t* table;
+  double *DA, *DB, *G;
+};
+Parts parts(char* ws, const Layout& L) {
+  return Parts{reinterpret_cast<int32_t*>(ws + L.ea), reinterpret_cast<int32_t*>(ws + L.eb),
+               reinterpret_cast<int32_t*>(ws + L.flag), reinterpret_cast<uint32_t*>(ws + L.table),
+               reinterpret_cast<double*>(ws + L.da),   reinterpret_cast<double*>(ws + L.db),
+               reinterpret_cast<double*>(ws + L.g)};
+}
+
+// Before the level GEMMs: the combinations of both operands (from their digit
+// panels, already in place) and the schedule's device table.
+int enqueue_schedule_inputs(const Planned& pl, int64_t m, int64_t n, int64_t k, const Parts& w, hipStream_t s) {
+  const int64_t kp = mdg::panel_k(k), mp = mdg::panel_mn(m), np = mdg::panel_mn(n);
+  MDG_TRY(hip_status(mdg::launch_combinations(pl.s, true, w.DA, kp * mp, s)));
+  MDG_TRY(hip_status(mdg::launch_combinations(pl.s, false, w.DB, kp * np, s)));
+  return hip_status(mdg::launch_upload(pl.t.words, w.table, s));
+}
+
+int enqueue_gemm(const Planned& pl, int64_t m, int64_t n, int64_t k, const Parts& w, double* out, hipStream_t s) {
+  mdg::GemmJobs jobs;
+  jobs.jobs = w.table + pl.t.jobs_off;
+  jobs.pairs = w.table + pl.t.pairs_off;
+  jobs.njobs = static_cast<int>(pl.s.job_first.size());
+  return hip_status(mdg::launch_slice_gemm(m, n, k, w.DA, w.DB, out, jobs, s));
+}
+
 }  // namespace
 
 extern "C" {
@@ -331,7 +473,7 @@ int mdgemm_plan(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* o
                 int* cutoff) {
   Resolved r;
   if (m < 0 || n < 0 || k < 0) return MDGEMM_EINVAL;
-  MDG_TRY(resolve(limbs, k, opts, &r));
+  MDG_TRY(resolve(limbs, m, n, k, opts, &r));
   if (!exact_ok(k, max_pairs(r.S, r.T), r.w)) return MDGEMM_EEXACT;
   if (slice_bits) *slice_bits = r.w;
   if (slices) *slices = r.S;
@@ -354,10 +496,10 @@ const char* mdgemm_status_string(int status) {
 
 size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts) {
   Resolved r;
-  if (m < 0 || n < 0 || k < 0 || resolve(limbs, k, opts, &r) != MDGEMM_OK) return SIZE_MAX;
+  if (m < 0 || n < 0 || k < 0 || resolve(limbs, m, n, k, opts, &r) != MDGEMM_OK) return SIZE_MAX;
   if (m == 0 || n == 0 || k == 0) return 0;
   Layout L;
-  if (!layout(m, n, k, r, &L)) return SIZE_MAX;
+  if (!layout(m, n, k, *schedule_for(r.S, r.T, m, n, k, r.w, r.kind), &L)) return SIZE_MAX;
   return L.total;
 }
 
@@ -365,7 +507,7 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
               const mdgemm_opts* opts) {
   Resolved r;
   if (m < 0 || n < 0 || k < 0) return MDGEMM_EINVAL;
-  MDG_TRY(resolve(limbs, k, opts, &r));
+  MDG_TRY(resolve(limbs, m, n, k, opts, &r));
   if (m == 0 || n == 0) return MDGEMM_OK;
   if (!C || (k > 0 && (!A || !B))) return MDGEMM_EINVAL;
   const size_t abytes = sizeof(double) * limbs * static_cast<size_t>(m) * static_cast<size_t>(k);
@@ -382,40 +524,27 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
     return MDGEMM_OK;
   }
 
+  const auto pl = schedule_for(r.S, r.T, m, n, k, r.w, r.kind);
+  if (!schedule_exact(pl->s, k, r.w)) return MDGEMM_EEXACT;
   Layout L;
-  if (!layout(m, n, k, r, &L)) return MDGEMM_EINVAL;
+  if (!layout(m, n, k, *pl, &L)) return MDGEMM_EINVAL;
   char* ws = nullptr;
-  std::unique_lock<std::mutex> wlock(cache().mu, std::defer_lock);
-  int wdev = -1;  // device whose library buffer this call uses, or -1
+  LibraryBuffer lib;
   if (opts && opts->workspace) {
     if (opts->workspace_bytes < L.total) return MDGEMM_EWORKSPACE;
     ws = static_cast<char*>(opts->workspace);
   } else {
-    // a captured graph would keep the library buffer's address, which a later
-    // call may free: capture needs a caller workspace
-    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-    MDG_TRY(hip_status(hipStreamIsCapturing(s, &cap)));
-    if (cap != hipStreamCaptureStatusNone) return MDGEMM_EINVAL;
-    wlock.lock();
-    void* p = nullptr;
-    MDG_TRY(cached_workspace(cache(), L.total, &p, &wdev));
-    MDG_TRY(hip_status(hipStreamWaitEvent(s, cache().last[wdev], 0)));
-    ws = static_cast<char*>(p);
+    MDG_TRY(lib.acquire(L.total, s, &ws));
   }
-  int32_t* EA = reinterpret_cast<int32_t*>(ws + L.ea);
-  int32_t* EB = reinterpret_cast<int32_t*>(ws + L.eb);
-  int32_t* flag = reinterpret_cast<int32_t*>(ws + L.flag);
-  double* DA = reinterpret_cast<double*>(ws + L.da);
-  double* DB = reinterpret_cast<double*>(ws + L.db);
-  double* G = reinterpret_cast<double*>(ws + L.g);
+  const Parts w = parts(ws, L);
 
   auto enqueue = [&]() -> int {
     if (r.flags & MDGEMM_CHECK_FINITE) {
-      MDG_TRY(hip_status(mdg::launch_set_i32(flag, 1, 0, s)));
-      MDG_TRY(hip_status(mdg::launch_nonfinite_scan(A, static_cast<int64_t>(limbs) * m * k, flag, s)));
-      MDG_TRY(hip_status(mdg::launch_nonfinite_scan(B, static_cast<int64_t>(limbs) * k * n, flag, s)));
+      MDG_TRY(hip_status(mdg::launch_set_i32(w.flag, 1, 0, s)));
+      MDG_TRY(hip_status(mdg::launch_nonfinite_scan(A, static_cast<int64_t>(limbs) * m * k, w.flag, s)));
+      MDG_TRY(hip_status(mdg::launch_nonfinite_scan(B, static_cast<int64_t>(limbs) * k * n, w.flag, s)));
       int32_t h = 0;
-      MDG_TRY(hip_status(hipMemcpyAsync(&h, flag, sizeof h, hipMemcpyDeviceToHost, s)));
+      MDG_TRY(hip_status(hipMemcpyAsync(&h, w.flag, sizeof h, hipMemcpyDeviceToHost, s)));
       MDG_TRY(hip_status(hipStreamSynchronize(s)));
       if (h) return MDGEMM_ENONFINITE;
     }
@@ -426,32 +555,34 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
       MDG_TRY(record(0, s));
     }
     // a1: grid exponents per row of A and per column of B
-    MDG_TRY(hip_status(mdg::launch_exponents(m, k, 0, A, EA, s)));
-    MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, EB, s)));
+    MDG_TRY(hip_status(mdg::launch_exponents(m, k, 0, A, w.EA, s)));
+    MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, w.EB, s)));
     if (timed) MDG_TRY(record(1, s));
-    // a2: exact splits into S digit planes
-    MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, r.w, 0, A, EA, DA, true, s)));
-    MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, r.w, 1, B, EB, DB, true, s)));
+    // a2: exact splits into S digit panels, then the schedule's digit sums
+    MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, r.w, 0, A, w.EA, w.DA, true, s)));
+    MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, r.w, 1, B, w.EB, w.DB, true, s)));
+    MDG_TRY(enqueue_schedule_inputs(*pl, m, n, k, w, s));
     if (timed) MDG_TRY(record(2, s));
-    // a3: level GEMMs on the FP64 matrix cores
-    MDG_TRY(hip_status(mdg::launch_slice_gemm(m, n, k, DA, DB, G, level_jobs(r.S, r.T), s)));
+    // a3: level GEMMs (or the Karatsuba products) on the FP64 matrix cores
+    MDG_TRY(enqueue_gemm(*pl, m, n, k, w, w.G, s));
     if (timed) MDG_TRY(record(3, s));
     // a4 + a5: exact accumulation and greedy rounding into L limbs
-    MDG_TRY(hip_status(mdg::launch_accum_renorm(m, n, limbs, r.T + 1, r.w, G, EA, EB, C, s)));
+    if (pl->s.direct_levels) {
+      MDG_TRY(hip_status(mdg::launch_accum_renorm(m, n, limbs, r.T + 1, r.w, w.G, w.EA, w.EB, C, s)));
+    } else {
+      MDG_TRY(hip_status(mdg::launch_plan_accum(m, n, limbs, r.T + 1, r.w, pl->s.planes, w.G,
+                                                w.table + pl->t.chunk_first_off, w.table + pl->t.chunks_off, w.EA,
+                                                w.EB, C, nullptr, s)));
+    }
     if (timed) {
       MDG_TRY(record(4, s));
       timing().valid = true;
     }
     return MDGEMM_OK;
   };
-  int st = enqueue();
-  if (wdev >= 0) {
-    // the next user of the library buffer waits for everything enqueued here,
-    // also when enqueueing stopped at an error
-    const int rec = hip_status(hipEventRecord(cache().last[wdev], s));
-    wlock.unlock();
-    if (st == MDGEMM_OK) st = rec;
-  }
+  // the next user of the library buffer waits for everything enqueued here,
+  // also when enqueueing stopped at an error
+  const int st = lib.release(enqueue());
   if (st != MDGEMM_OK) return st;
   if (r.flags & MDGEMM_SYNC) MDG_TRY(hip_status(hipStreamSynchronize(s)));
   return MDGEMM_OK;
@@ -560,10 +691,143 @@ int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int slice_bit
     return MDGEMM_EINVAL;
   if (!exact_ok(k, per_pair ? 1 : max_pairs(slices, cutoff), slice_bits)) return MDGEMM_EEXACT;
   const hipStream_t s = static_cast<hipStream_t>(stream);
-  if (!per_pair) return hip_status(mdg::launch_slice_gemm(m, n, k, DAt, DBp, out, level_jobs(slices, cutoff), s));
-  for (const JobTable& jt : pair_jobs(slices, cutoff))
-    MDG_TRY(hip_status(mdg::launch_slice_gemm(m, n, k, DAt, DBp, out, jt, s)));
+  const auto pl = schedule_for(slices, cutoff, m, n, k, slice_bits, per_pair ? Kind::kPerPair : Kind::kLevels);
+  // the job table goes into the library buffer
+  LibraryBuffer lib;
+  char* tab = nullptr;
+  MDG_TRY(lib.acquire(sizeof(uint32_t) * pl->t.words.size(), s, &tab));
+  Parts w{};
+  w.table = reinterpret_cast<uint32_t*>(tab);
+  w.DA = const_cast<double*>(DAt);
+  w.DB = const_cast<double*>(DBp);
+  int st = hip_status(mdg::launch_upload(pl->t.words, w.table, s));
+  if (st == MDGEMM_OK) st = enqueue_gemm(*pl, m, n, k, w, out, s);
+  return lib.release(st);
+}
+
+int mdgemm_schedule_info(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, unsigned flags,
+                         int64_t* info, int count) {
+  if (m < 0 || n < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || slice_bits < 1 || slice_bits > mdg::kMaxSliceBits ||
+      cutoff < 0 || cutoff > 2 * slices - 2 || k < 0 || count < 0 || (count > 0 && !info))
+    return MDGEMM_EINVAL;
+  const auto pl = schedule_for(slices, cutoff, m, n, k, slice_bits,
+                               kind_of(flags));
+  const mdg::Schedule& sc = pl->s;
+  int max_depth = 0;
+  for (int d : sc.depth_a) max_depth = std::max(max_depth, d);
+  for (int d : sc.depth_b) max_depth = std::max(max_depth, d);
+  const int64_t v[MDGEMM_SCHEDULE_INFO] = {sc.terms,
+                                           static_cast<int64_t>(sc.job_first.size()),
+                                           sc.planes,
+                                           static_cast<int64_t>(sc.mask_a.size()),
+                                           static_cast<int64_t>(sc.mask_b.size()),
+                                           static_cast<int64_t>(sc.entry_level.size()),
+                                           sc.max_job_weight,
+                                           max_depth,
+                                           sc.direct_levels ? 1 : 0};
+  const int nw = std::min(count, MDGEMM_SCHEDULE_INFO);
+  for (int i = 0; i < nw; ++i) info[i] = v[i];
+  return nw;
+}
+
+int mdgemm_schedule_export(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, unsigned flags,
+                           uint64_t* mask_a, int32_t* parents_a, uint64_t* mask_b, int32_t* parents_b, int32_t* jobs,
+                           int32_t* pairs, int32_t* plane_first, int32_t* entries) {
+  if (m < 0 || n < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || slice_bits < 1 || slice_bits > mdg::kMaxSliceBits ||
+      cutoff < 0 || cutoff > 2 * slices - 2 || k < 0)
+    return MDGEMM_EINVAL;
+  const auto pl = schedule_for(slices, cutoff, m, n, k, slice_bits,
+                               kind_of(flags));
+  const mdg::Schedule& sc = pl->s;
+  for (size_t c = 0; c < sc.mask_a.size(); ++c) {
+    if (mask_a) mask_a[c] = sc.mask_a[c];
+    if (parents_a) {
+      parents_a[2 * c] = sc.par1_a[c];
+      parents_a[2 * c + 1] = sc.par2_a[c];
+    }
+  }
+  for (size_t c = 0; c < sc.mask_b.size(); ++c) {
+    if (mask_b) mask_b[c] = sc.mask_b[c];
+    if (parents_b) {
+      parents_b[2 * c] = sc.par1_b[c];
+      parents_b[2 * c + 1] = sc.par2_b[c];
+    }
+  }
+  for (size_t j = 0; jobs && j < sc.job_first.size(); ++j) {
+    jobs[3 * j] = sc.job_first[j];
+    jobs[3 * j + 1] = sc.job_count[j];
+    jobs[3 * j + 2] = sc.job_out[j];
+  }
+  for (size_t i = 0; pairs && i < sc.pair_a.size(); ++i) {
+    pairs[2 * i] = sc.pair_a[i];
+    pairs[2 * i + 1] = sc.pair_b[i];
+  }
+  for (size_t i = 0; plane_first && i < sc.plane_first.size(); ++i) plane_first[i] = sc.plane_first[i];
+  for (size_t e = 0; entries && e < sc.entry_level.size(); ++e) {
+    entries[2 * e] = sc.entry_level[e];
+    entries[2 * e + 1] = sc.entry_coef[e];
+  }
   return MDGEMM_OK;
+}
+
+size_t mdgemm_schedule_workspace_bytes(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff,
+                                       unsigned flags) {
+  if (m < 0 || n < 0 || k < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || slice_bits < 1 ||
+      slice_bits > mdg::kMaxSliceBits || cutoff < 0 || cutoff > 2 * slices - 2)
+    return SIZE_MAX;
+  const auto pl = schedule_for(slices, cutoff, m, n, k, slice_bits,
+                               kind_of(flags));
+  Layout L;
+  if (!layout(m, n, k, *pl, &L)) return SIZE_MAX;
+  return L.total;
+}
+
+int mdgemm_schedule_levels(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, unsigned flags,
+                           const double* DAt, const double* DBp, double* G, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  if (m < 0 || n < 0 || k < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || slice_bits < 1 ||
+      slice_bits > mdg::kMaxSliceBits || cutoff < 0 || cutoff > 2 * slices - 2 || !levels_ok(cutoff + 1, slice_bits))
+    return MDGEMM_EINVAL;
+  if (m == 0 || n == 0) return MDGEMM_OK;
+  if (!G || (k > 0 && (!DAt || !DBp))) return MDGEMM_EINVAL;
+  if (!exact_ok(k, max_pairs(slices, cutoff), slice_bits)) return MDGEMM_EEXACT;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t levels = cutoff + 1;
+  if (k == 0) return hip_status(mdg::launch_zero_f64(G, levels * m * n, s));
+  const auto pl = schedule_for(slices, cutoff, m, n, k, slice_bits,
+                               kind_of(flags));
+  if (!schedule_exact(pl->s, k, slice_bits)) return MDGEMM_EEXACT;
+  Layout L;
+  if (!layout(m, n, k, *pl, &L)) return MDGEMM_EINVAL;
+  const size_t kp = static_cast<size_t>(mdg::panel_k(k)), mp = static_cast<size_t>(mdg::panel_mn(m)),
+               np = static_cast<size_t>(mdg::panel_mn(n));
+  const size_t abytes = sizeof(double) * slices * kp * mp, bbytes = sizeof(double) * slices * kp * np;
+  const size_t gbytes = sizeof(double) * static_cast<size_t>(levels) * static_cast<size_t>(m) * static_cast<size_t>(n);
+  if (overlaps(G, gbytes, DAt, abytes) || overlaps(G, gbytes, DBp, bbytes)) return MDGEMM_EINVAL;
+  char* ws = nullptr;
+  LibraryBuffer lib;
+  if (workspace) {
+    if (workspace_bytes < L.total) return MDGEMM_EWORKSPACE;
+    if (overlaps(workspace, L.total, G, gbytes) || overlaps(workspace, L.total, DAt, abytes) ||
+        overlaps(workspace, L.total, DBp, bbytes))
+      return MDGEMM_EINVAL;
+    ws = static_cast<char*>(workspace);
+  } else {
+    MDG_TRY(lib.acquire(L.total, s, &ws));
+  }
+  const Parts w = parts(ws, L);
+  auto enqueue = [&]() -> int {
+    // the digit panels are combinations 0..S-1 of the schedule
+    MDG_TRY(hip_status(hipMemcpyAsync(w.DA, DAt, abytes, hipMemcpyDeviceToDevice, s)));
+    MDG_TRY(hip_status(hipMemcpyAsync(w.DB, DBp, bbytes, hipMemcpyDeviceToDevice, s)));
+    MDG_TRY(enqueue_schedule_inputs(*pl, m, n, k, w, s));
+    if (pl->s.direct_levels) return enqueue_gemm(*pl, m, n, k, w, G, s);
+    MDG_TRY(enqueue_gemm(*pl, m, n, k, w, w.G, s));
+    return hip_status(mdg::launch_plan_accum(m, n, 1, static_cast<int>(levels), slice_bits, pl->s.planes, w.G,
+                                             w.table + pl->t.chunk_first_off, w.table + pl->t.chunks_off, nullptr,
+                                             nullptr, nullptr, G, s));
+  };
+  return lib.release(enqueue());
 }
 
 int mdgemm_accumulate(int64_t m, int64_t n, int levels, int slice_bits, const double* G, int64_t* Z, void* stream) {

@@ -5,6 +5,10 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
+#include "schedule.h"
+
 namespace mdg {
 
 constexpr int kSliceBits = 13;
@@ -13,7 +17,7 @@ constexpr int kMaxSlices = 64;  // 4 digits per limb of a hexa double
 constexpr int kMaxLimbs = 16;   // hexa double
 constexpr int kMaxLevels = 2 * kMaxSlices - 1;
 constexpr int kZWords = 28;     // 64-bit words of an exact level sum (13 (kMaxLevels - 1) + 55 bits)
-constexpr int kMaxJobs = 256;   // jobs of one level-GEMM launch (grid.y)
+constexpr int kMaxJobs = 65535;  // jobs of one level-GEMM launch (grid.y)
 constexpr int kMaxSliceBits = 26;                  // widest digit: products of two stay below 2^52
 constexpr int kMaxDigitBits = 64 * 14 - 52;  // w S + 52 <= 896: the split's integer fits 14 words
 constexpr int kTileMN = 128;  // level-GEMM tile rows / columns
@@ -24,14 +28,15 @@ constexpr int kTileK = 16;    // level-GEMM k step
 inline int64_t panel_k(int64_t k) { return (k + kTileK - 1) / kTileK * kTileK; }
 inline int64_t panel_mn(int64_t x) { return (x + kTileMN - 1) / kTileMN * kTileMN; }
 
-// Slice-pair jobs of the level GEMM: job j multiplies the pairs
-// (p_first + i, q_first - i) for i < npairs into output plane out[j].
-struct JobTable {
-  int njobs;
-  uint16_t p_first[kMaxJobs];
-  uint16_t q_first[kMaxJobs];
-  uint16_t npairs[kMaxJobs];
-  uint16_t out[kMaxJobs];
+// Slice-pair jobs of the level GEMM, read from a device table in the format of
+// ScheduleTable (schedule.h): `jobs` holds two words per job (first pair |
+// pair count << 16, output plane), `pairs` one word per pair (combination of A
+// | combination of B << 16).  Job j sums the products of its pairs into plane
+// out[j].
+struct GemmJobs {
+  const uint32_t* jobs = nullptr;
+  const uint32_t* pairs = nullptr;
+  int njobs = 0;
 };
 
 // a1: per-row (axis 0) or per-column (axis 1) grid exponents of a [rows][cols] plane.
@@ -49,10 +54,20 @@ hipError_t launch_line_spread(int64_t rows, int64_t cols, int axis, const double
 hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
                         double* D, bool panel, hipStream_t stream);
 
-// a3: level or pair products of the panels DAt [S][panel_k(k)][panel_mn(m)] and
-// DBp [S][panel_k(k)][panel_mn(n)]; `jobs` lists the pair groups, outputs are [*][m][n].
+// a3: products of the combination panels DAt [*][panel_k(k)][panel_mn(m)] and
+// DBp [*][panel_k(k)][panel_mn(n)] (combinations 0..S-1 are the digits); one
+// job per grid row, outputs [*][m][n].
 hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DAt, const double* DBp, double* out,
-                             const JobTable& jobs, hipStream_t stream);
+                             const GemmJobs& jobs, hipStream_t stream);
+
+// Copies `words` into the device array dst (stream-ordered kernel launches that
+// carry the words as arguments, so that no host memory is read later).
+hipError_t launch_upload(const std::vector<uint32_t>& words, uint32_t* dst, hipStream_t stream);
+
+// The combinations c >= S of one operand (mask/parents of the schedule, `a`
+// selects A's or B's): panel c = panel par1[c] + panel par2[c], whole panels of
+// `plane` doubles, in order of depth.
+hipError_t launch_combinations(const Schedule& s, bool a, double* D, int64_t plane, hipStream_t stream);
 
 // a4: exact accumulation of `levels` planes of w-bit digit products (weights
 // 2^(-w t)) into kZWords-word integers Z [kZWords][m][n].
@@ -62,6 +77,15 @@ hipError_t launch_accumulate(int64_t m, int64_t n, int levels, int w, const doub
 // a4 + a5: exact accumulation and greedy rounding into L limbs, scaled by 2^(EA+EB-2w).
 hipError_t launch_accum_renorm(int64_t m, int64_t n, int L, int levels, int w, const double* G, const int32_t* EA,
                                const int32_t* EB, double* C, hipStream_t stream);
+
+// a4 + a5 for a schedule whose planes enter several levels: level t =
+// sum of coef * plane over the entries (chunk_first / chunks of ScheduleTable;
+// chunks 8-byte aligned), formed exactly in 64-bit integers, then accumulated
+// and rounded as launch_accum_renorm (C != nullptr), or written as
+// integer-valued doubles Gout [levels][m][n] (C == nullptr).
+hipError_t launch_plan_accum(int64_t m, int64_t n, int L, int levels, int w, int planes, const double* P,
+                             const uint32_t* chunk_first, const uint32_t* chunks, const int32_t* EA,
+                             const int32_t* EB, double* C, double* Gout, hipStream_t stream);
 
 // 64-bit words of the exact sum of `levels` levels of w-bit digits (sign included).
 int accum_words(int levels, int w);

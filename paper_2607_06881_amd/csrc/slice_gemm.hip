@@ -37,10 +37,13 @@
 //   fragment read (consecutive k rows) fall on different banks.
 //
 // Work decomposition: grid.x = output tiles, grid.y = jobs (levels, heaviest
-// first, or single pairs).  Tiles are renumbered so that each of the 8 XCDs
+// first, single pairs, or the products of combinations of a Karatsuba
+// schedule; each job lists its pairs in a device table, see schedule.h).  Tiles are renumbered so that each of the 8 XCDs
 // (blocks are dealt to XCDs round-robin) works on its own chunk of tiles, and
 // the blocks resident on one XCD at a time cover an about 8 x 8 patch whose
 // panel rows stay in that XCD's L2.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace mdg {
@@ -62,7 +65,9 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
                                                                  int64_t np, int tiles_n, int ntiles,
                                                                  const double* __restrict__ DAt,
                                                                  const double* __restrict__ DBp,
-                                                                 double* __restrict__ out, const JobTable jobs) {
+                                                                 double* __restrict__ out,
+                                                                 const uint32_t* __restrict__ jobs,
+                                                                 const uint32_t* __restrict__ pairs) {
   __shared__ double As[2][BK * LDS_LD];
   __shared__ double Bs[2][BK * LDS_LD];
 
@@ -80,8 +85,12 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
   const int rows_in = min(kGroup, tiles_m - first), within = t - g * gsz;
   const int64_t m0 = static_cast<int64_t>(first + within % rows_in) * BM;
   const int64_t n0 = static_cast<int64_t>(within / rows_in) * BN;
+  // the job's pairs (uniform: scalar loads); the pair after the one being
+  // copied is fetched one pair ahead
   const int job = blockIdx.y;
-  const int p_first = jobs.p_first[job], q_first = jobs.q_first[job], npairs = jobs.npairs[job];
+  const uint32_t jw = jobs[2 * job];
+  const int pfirst = static_cast<int>(jw & 0xffffu), npairs = static_cast<int>(jw >> 16);
+  const int64_t out_plane = jobs[2 * job + 1];
   const int64_t plane_a = kp * mp, plane_b = kp * np;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -96,9 +105,13 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   int lpi = 0;
   int64_t lkb = 0;  // the step the next copy fetches
+  uint32_t pr = pairs[pfirst];                             // pair lpi
+  uint32_t pr_next = npairs > 1 ? pairs[pfirst + 1] : 0u;  // pair lpi + 1
+  // this wave's first copy row of the pair's panels; advanced by one k step per copy
+  const int64_t row_a = 4 * wave_u * mp + m0, row_b = 4 * wave_u * np + n0;
+  const double* a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
+  const double* b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
   auto issue = [&](int stage) {
-    const double* a = DAt + static_cast<int64_t>(p_first + lpi) * plane_a + (lkb * BK + 4 * wave_u) * mp + m0;
-    const double* b = DBp + static_cast<int64_t>(q_first - lpi) * plane_b + (lkb * BK + 4 * wave_u) * np + n0;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(a + r * mp + lane_off),
@@ -111,6 +124,13 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
     if (++lkb == nkb) {
       lkb = 0;
       ++lpi;
+      pr = pr_next;
+      if (lpi + 1 < npairs) pr_next = pairs[pfirst + lpi + 1];
+      a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
+      b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
+    } else {
+      a += BK * mp;
+      b += BK * np;
     }
   };
 
@@ -148,7 +168,7 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
           acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[kg][i], bf[kg][j], acc[i][j], 0, 0, 0);
   }
 
-  double* o = out + static_cast<int64_t>(jobs.out[job]) * m * n;
+  double* o = out + out_plane * m * n;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -164,7 +184,7 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
 }  // namespace
 
 hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DAt, const double* DBp, double* out,
-                             const JobTable& jobs, hipStream_t stream) {
+                             const GemmJobs& jobs, hipStream_t stream) {
   if (m == 0 || n == 0 || jobs.njobs == 0) return hipSuccess;
   const int64_t mp = panel_mn(m), np = panel_mn(n), kp = panel_k(k);
   const int64_t tiles_n = np / BN;
@@ -172,8 +192,89 @@ hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DAt,
   if (ntiles > 0x7fffffff || jobs.njobs > 65535) return hipErrorInvalidValue;
   hipLaunchKernelGGL(slice_gemm_kernel, dim3(static_cast<unsigned>(ntiles), static_cast<unsigned>(jobs.njobs)),
                      dim3(kThreads), 0, stream, m, n, kp, mp, np, static_cast<int>(tiles_n),
-                     static_cast<int>(ntiles), DAt, DBp, out, jobs);
+                     static_cast<int>(ntiles), DAt, DBp, out, jobs.jobs, jobs.pairs);
   return hipGetLastError();
+}
+
+namespace {
+
+constexpr int kUploadWords = 480;
+struct WordChunk {
+  uint32_t count;
+  uint32_t w[kUploadWords];
+};
+
+__global__ void __launch_bounds__(256) upload_kernel(const WordChunk c, uint32_t* __restrict__ dst) {
+  for (uint32_t i = threadIdx.x; i < c.count; i += blockDim.x) dst[i] = c.w[i];
+}
+
+constexpr int kComboChunk = 160;
+struct ComboChunk {
+  int count;
+  uint16_t child[kComboChunk], p1[kComboChunk], p2[kComboChunk];
+};
+
+// panel child = panel p1 + panel p2 (integers: exact), two doubles per thread
+__global__ void __launch_bounds__(256) combination_kernel(const ComboChunk c, double* __restrict__ D, int64_t plane) {
+  const int e = blockIdx.y;
+  const double2* a = reinterpret_cast<const double2*>(D + static_cast<int64_t>(c.p1[e]) * plane);
+  const double2* b = reinterpret_cast<const double2*>(D + static_cast<int64_t>(c.p2[e]) * plane);
+  double2* d = reinterpret_cast<double2*>(D + static_cast<int64_t>(c.child[e]) * plane);
+  const int64_t half = plane / 2;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < half;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const double2 x = a[i], y = b[i];
+    d[i] = double2{x.x + y.x, x.y + y.y};
+  }
+}
+
+}  // namespace
+
+hipError_t launch_upload(const std::vector<uint32_t>& words, uint32_t* dst, hipStream_t stream) {
+  for (size_t off = 0; off < words.size(); off += kUploadWords) {
+    WordChunk c;
+    c.count = static_cast<uint32_t>(std::min<size_t>(kUploadWords, words.size() - off));
+    for (uint32_t i = 0; i < c.count; ++i) c.w[i] = words[off + i];
+    hipLaunchKernelGGL(upload_kernel, dim3(1), dim3(256), 0, stream, c, dst + off);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_combinations(const Schedule& s, bool a, double* D, int64_t plane, hipStream_t stream) {
+  const std::vector<int>& depth = a ? s.depth_a : s.depth_b;
+  const std::vector<int>& p1 = a ? s.par1_a : s.par1_b;
+  const std::vector<int>& p2 = a ? s.par2_a : s.par2_b;
+  int max_depth = 0;
+  for (int d : depth) max_depth = std::max(max_depth, d);
+  // panels are whole multiples of 16 x 128 doubles: an even count
+  const int64_t half = plane / 2;
+  const unsigned gx = static_cast<unsigned>(std::min<int64_t>((half + 255) / 256, 1024));
+  for (int d = 1; d <= max_depth; ++d) {
+    ComboChunk c;
+    c.count = 0;
+    auto flush = [&]() -> hipError_t {
+      if (c.count == 0) return hipSuccess;
+      hipLaunchKernelGGL(combination_kernel, dim3(gx, static_cast<unsigned>(c.count)), dim3(256), 0, stream, c, D,
+                         plane);
+      c.count = 0;
+      return hipGetLastError();
+    };
+    for (size_t i = 0; i < depth.size(); ++i) {
+      if (depth[i] != d) continue;
+      c.child[c.count] = static_cast<uint16_t>(i);
+      c.p1[c.count] = static_cast<uint16_t>(p1[i]);
+      c.p2[c.count] = static_cast<uint16_t>(p2[i]);
+      if (++c.count == kComboChunk) {
+        const hipError_t err = flush();
+        if (err != hipSuccess) return err;
+      }
+    }
+    const hipError_t err = flush();
+    if (err != hipSuccess) return err;
+  }
+  return hipSuccess;
 }
 
 }  // namespace mdg

@@ -29,6 +29,9 @@ MDGEMM_ENONFINITE = -6
 MDGEMM_CHECK_FINITE = 1
 MDGEMM_SYNC = 2
 MDGEMM_TIME_STAGES = 4
+MDGEMM_KARATSUBA = 8
+MDGEMM_KARATSUBA_MIN_TERMS = 16
+MDGEMM_SCHEDULE_INFO = 9
 
 MDGEMM_CUTOFF_DEFAULT = -1
 MDGEMM_CUTOFF_ALL = -2
@@ -67,6 +70,10 @@ EXPORTED = (
     "mdgemm_slice_gemm",
     "mdgemm_accumulate",
     "mdgemm_accum_renorm",
+    "mdgemm_schedule_info",
+    "mdgemm_schedule_export",
+    "mdgemm_schedule_workspace_bytes",
+    "mdgemm_schedule_levels",
 )
 
 
@@ -135,6 +142,16 @@ def lib() -> ctypes.CDLL:
         L.mdgemm_accumulate.restype = ctypes.c_int
         L.mdgemm_accum_renorm.argtypes = [_i64, _i64, _c, _c, _c, _vp, _vp, _vp, _vp, _vp]
         L.mdgemm_accum_renorm.restype = ctypes.c_int
+        _u = ctypes.c_uint
+        L.mdgemm_schedule_info.argtypes = [_i64, _i64, _i64, _c, _c, _c, _u, ctypes.POINTER(ctypes.c_int64), _c]
+        L.mdgemm_schedule_info.restype = ctypes.c_int
+        L.mdgemm_schedule_export.argtypes = [_i64, _i64, _i64, _c, _c, _c, _u] + [_vp] * 8
+        L.mdgemm_schedule_export.restype = ctypes.c_int
+        L.mdgemm_schedule_workspace_bytes.argtypes = [_i64, _i64, _i64, _c, _c, _c, _u]
+        L.mdgemm_schedule_workspace_bytes.restype = ctypes.c_size_t
+        L.mdgemm_schedule_levels.argtypes = [_i64, _i64, _i64, _c, _c, _c, _u, _vp, _vp, _vp, _vp, ctypes.c_size_t,
+                                             _vp]
+        L.mdgemm_schedule_levels.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -189,11 +206,12 @@ def make_opts(*, slices_per_limb: int = 4, cutoff: int = MDGEMM_CUTOFF_DEFAULT, 
 
 def mdgemm_workspace_bytes(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
                            cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0,
-                           range_bits: int = 0) -> int:
+                           range_bits: int = 0, flags: int = 0) -> int:
     o = mdgemm_opts()
     lib().mdgemm_opts_init(ctypes.byref(o))
     o.slices_per_limb = slices_per_limb
     o.cutoff = cutoff
+    o.flags = flags
     o.slice_bits = slice_bits
     o.slices = slices
     o.range_bits = range_bits
@@ -201,12 +219,14 @@ def mdgemm_workspace_bytes(m: int, n: int, k: int, limbs: int, *, slices_per_lim
 
 
 def mdgemm_plan(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
-                cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0, range_bits: int = 0):
+                cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0, range_bits: int = 0,
+                flags: int = 0):
     """(digit width w, digit count S, cutoff T) that mdgemm_ex uses for these options."""
     o = mdgemm_opts()
     lib().mdgemm_opts_init(ctypes.byref(o))
     o.slices_per_limb = slices_per_limb
     o.cutoff = cutoff
+    o.flags = flags
     o.slice_bits = slice_bits
     o.slices = slices
     o.range_bits = range_bits
@@ -237,7 +257,7 @@ def mdgemm_ex(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None
             raise ValueError("C has the wrong shape")
     if workspace is None:
         need = mdgemm_workspace_bytes(m, n, k, L, slices_per_limb=slices_per_limb, cutoff=cutoff,
-                                      slice_bits=slice_bits, slices=slices, range_bits=range_bits)
+                                      slice_bits=slice_bits, slices=slices, range_bits=range_bits, flags=flags)
         if need == 2**64 - 1:
             _check(MDGEMM_EINVAL, "mdgemm_workspace_bytes")
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=A.device)
@@ -367,3 +387,72 @@ def mdgemm_accum_renorm(G: torch.Tensor, EA: torch.Tensor, EB: torch.Tensor, lim
     _check(lib().mdgemm_accum_renorm(m, n, limbs, levels, bits, _ptr(G), _ptr(EA), _ptr(EB), _ptr(C),
                                      _stream(stream)), "mdgemm_accum_renorm")
     return C
+
+
+SCHEDULE_INFO_KEYS = ("terms", "jobs", "planes", "combos_a", "combos_b", "entries", "max_job_weight", "max_depth",
+                      "direct_levels")
+
+
+def mdgemm_schedule_info(m: int, n: int, k: int, slices: int, cutoff: int, *, bits: int = MDGEMM_SLICE_BITS,
+                         flags: int = 0) -> dict:
+    """Sizes of the schedule of the level products of an m x k by k x n product (host only)."""
+    buf = (ctypes.c_int64 * MDGEMM_SCHEDULE_INFO)()
+    cnt = lib().mdgemm_schedule_info(m, n, k, slices, bits, cutoff, flags, buf, MDGEMM_SCHEDULE_INFO)
+    if cnt < 0:
+        _check(cnt, "mdgemm_schedule_info")
+    return {key: int(buf[i]) for i, key in enumerate(SCHEDULE_INFO_KEYS[:cnt])}
+
+
+def mdgemm_schedule_export(m: int, n: int, k: int, slices: int, cutoff: int, *, bits: int = MDGEMM_SLICE_BITS,
+                           flags: int = 0) -> dict:
+    """The schedule's tables as numpy arrays (host only): mask_a/mask_b (uint64 digit
+    sets), parents_a/parents_b [C, 2], jobs [J, 3] (first pair, count, plane),
+    pairs [terms, 2], plane_first [P + 1], entries [E, 2] (level, coefficient)."""
+    import numpy as np
+
+    info = mdgemm_schedule_info(m, n, k, slices, cutoff, bits=bits, flags=flags)
+    out = {
+        "mask_a": np.zeros(info["combos_a"], dtype=np.uint64),
+        "parents_a": np.zeros((info["combos_a"], 2), dtype=np.int32),
+        "mask_b": np.zeros(info["combos_b"], dtype=np.uint64),
+        "parents_b": np.zeros((info["combos_b"], 2), dtype=np.int32),
+        "jobs": np.zeros((info["jobs"], 3), dtype=np.int32),
+        "pairs": np.zeros((info["terms"], 2), dtype=np.int32),
+        "plane_first": np.zeros(info["planes"] + 1, dtype=np.int32),
+        "entries": np.zeros((info["entries"], 2), dtype=np.int32),
+    }
+    order = ("mask_a", "parents_a", "mask_b", "parents_b", "jobs", "pairs", "plane_first", "entries")
+    _check(lib().mdgemm_schedule_export(m, n, k, slices, bits, cutoff, flags,
+                                        *[out[key].ctypes.data_as(ctypes.c_void_p) for key in order]),
+           "mdgemm_schedule_export")
+    out["info"] = info
+    return out
+
+
+def mdgemm_schedule_workspace_bytes(m: int, n: int, k: int, slices: int, cutoff: int, *,
+                                    bits: int = MDGEMM_SLICE_BITS, flags: int = 0) -> int:
+    return int(lib().mdgemm_schedule_workspace_bytes(m, n, k, slices, bits, cutoff, flags))
+
+
+def mdgemm_schedule_levels(DAt: torch.Tensor, DBp: torch.Tensor, m: int, n: int, k: int, cutoff: int, *,
+                           flags: int = 0, bits: int = MDGEMM_SLICE_BITS, out: Optional[torch.Tensor] = None,
+                           workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Levels [cutoff+1, m, n] of the digit panels by the schedule `flags` selects
+    (MDGEMM_KARATSUBA or 0); workspace: a torch uint8 tensor, allocated here when
+    not given."""
+    _dev_tensor(DAt, torch.float64, "DAt")
+    _dev_tensor(DBp, torch.float64, "DBp")
+    S = DAt.shape[0]
+    if tuple(DAt.shape) != (S, panel_k(k), panel_mn(m)) or tuple(DBp.shape) != (S, panel_k(k), panel_mn(n)):
+        raise ValueError("digit panels have the wrong shape")
+    if out is None:
+        out = torch.empty((cutoff + 1, m, n), dtype=torch.float64, device=DAt.device)
+    if workspace is None:
+        need = mdgemm_schedule_workspace_bytes(m, n, k, S, cutoff, bits=bits, flags=flags)
+        if need == 2**64 - 1:
+            _check(MDGEMM_EINVAL, "mdgemm_schedule_workspace_bytes")
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=DAt.device)
+    _check(lib().mdgemm_schedule_levels(m, n, k, S, bits, cutoff, flags, _ptr(DAt), _ptr(DBp), _ptr(out),
+                                        _ptr(workspace), workspace.numel(), _stream(stream)),
+           "mdgemm_schedule_levels")
+    return out

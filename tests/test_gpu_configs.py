@@ -168,3 +168,31 @@ def test_workload_line_spread():
     assert SA.cpu().numpy()[rows].tolist() == exact.line_spread(A_h[0, rows, :], 0).tolist()
     assert SB.cpu().numpy()[cols].tolist() == exact.line_spread(B_h[0][:, cols], 1).tolist()
     assert w.range_bits - 10 <= int(SA.min()) and int(SA.max()) <= w.range_bits + 30  # N(0,1) tails add bits
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c7"])
+def test_workload_karatsuba(name):
+    # The same workloads with the Karatsuba schedule of the level products
+    # (fewer GEMMs of digit sums, levels formed exactly from their planes):
+    # sampled entries bit-exact against the oracle's chain, which does not
+    # depend on the schedule.  (For the octo/hexa-double workloads the cost
+    # model keeps the pair schedule.)
+    w = workloads.WORKLOADS[name]
+    opts = w.options()
+    info = md.mdgemm_schedule_info(w.m, w.n, w.k, w.slices, w.cutoff, flags=md.MDGEMM_KARATSUBA)
+    print(f"[case] workload {name} karatsuba: {info['terms']} products instead of {w.pairs}, "
+          f"{info['planes']} planes", flush=True)
+    assert info["terms"] < w.pairs
+    A_h, B_h = workloads.make_workload(w)
+    A, B = torch.from_numpy(A_h).to(DEV), torch.from_numpy(B_h).to(DEV)
+    ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, flags=md.MDGEMM_KARATSUBA, **opts),
+                     dtype=torch.uint8, device=DEV)
+    C_h = md.mdgemm_ex(A, B, workspace=ws, flags=md.MDGEMM_KARATSUBA, **opts).cpu().numpy()
+    del ws
+    torch.cuda.empty_cache()
+    assert _nonoverlap_all(C_h) and np.isfinite(C_h).all()
+    EA, EB = coracle.exponents(A_h[0], 0), coracle.exponents(B_h[0], 1)
+    entries = _sample_entries(EA, EB, 16, w.seed + 90)
+    ref = pipeline.reference_entries(A_h, B_h, w.slices, w.cutoff, entries)
+    for (i, j), r in ref.items():
+        assert C_h[:, i, j].tolist() == r["limbs"], (i, j)

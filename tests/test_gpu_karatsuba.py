@@ -1,0 +1,192 @@
+"""GPU parity of the Karatsuba schedule of the level products.
+
+The schedule replaces the digit-pair GEMMs by fewer GEMMs of digit sums and
+forms the levels from their planes in 64-bit integers; every step is exact, so
+levels and final limbs must equal the oracle's bit for bit (the same values as
+the pair schedule).  Checked: the levels of random and extreme digit panels
+(stage entry point), whole products against the oracle's chain for every limb
+count, cutoff, digit width and range balancing, a caller workspace on a side
+stream, and graph replays.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import coracle, exact, pipeline
+from paper_2607_06881_amd import mdgemm as md
+from paper_2607_06881_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+KARA = md.MDGEMM_KARATSUBA
+# the small shapes below would mostly keep the pair schedule under the cost
+# model; the minimum-products plan exercises every combination and plane
+KMIN = md.MDGEMM_KARATSUBA_MIN_TERMS
+
+
+def _gpu(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def _host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def _panel(D, axis):
+    """Digit planes [S][rows][cols] -> level-GEMM panel (k-major, zero padded)."""
+    S, rows, cols = D.shape
+    if axis == 0:
+        P = np.zeros((S, md.panel_k(cols), md.panel_mn(rows)))
+        P[:, :cols, :rows] = D.transpose(0, 2, 1)
+    else:
+        P = np.zeros((S, md.panel_k(rows), md.panel_mn(cols)))
+        P[:, :rows, :cols] = D
+    return P
+
+
+@pytest.mark.parametrize("S,T,m,k,n", [(8, 7, 65, 37, 129), (8, 14, 130, 50, 131), (4, 3, 1, 1, 1),
+                                       (12, 11, 200, 33, 70), (16, 15, 64, 16, 64), (16, 30, 33, 20, 17),
+                                       (13, 17, 140, 40, 9), (8, 7, 1100, 40, 300), (5, 8, 3, 70, 260),
+                                       (32, 31, 130, 20, 140), (64, 63, 70, 17, 129), (64, 126, 20, 5, 30)])
+def test_schedule_levels(S, T, m, k, n):
+    info = md.mdgemm_schedule_info(m, n, k, S, T, flags=KMIN)
+    print(f"[case] karatsuba levels S={S} T={T} {m}x{k}x{n}: {info['terms']} products, "
+          f"{info['planes']} planes", flush=True)
+    assert S < 2 or info["direct_levels"] == 0
+    rng = np.random.default_rng(S * 1000 + T + m)
+    DA = rng.integers(-8191, 8192, (S, m, k)).astype(np.float64)
+    DB = rng.integers(-8191, 8192, (S, k, n)).astype(np.float64)
+    DA[:, rng.random((m, k)) < 0.1] = 0.0
+    DA_p, DB_p = _gpu(_panel(DA, 0)), _gpu(_panel(DB, 1))
+    got = _host(md.mdgemm_schedule_levels(DA_p, DB_p, m, n, k, T, flags=KMIN))
+    want = coracle.levels(DA, DB, T).astype(np.float64)
+    assert np.array_equal(got, want)
+    # the pair schedule through the same entry point, and the level GEMM itself
+    assert np.array_equal(_host(md.mdgemm_schedule_levels(DA_p, DB_p, m, n, k, T)), want)
+    assert np.array_equal(_host(md.mdgemm_slice_gemm(DA_p, DB_p, m, n, k, T)), want)
+
+
+@pytest.mark.parametrize("S,T,k,bits", [(8, 7, 16000, 13), (8, 14, 16000, 13), (6, 5, 4096, 19), (12, 11, 3000, 16)])
+def test_schedule_levels_extreme_digits(S, T, k, bits):
+    # every digit of A at +(2^w - 1), of B at -(2^w - 1): level t is
+    # -pairs_t k (2^w - 1)^2 in closed form, near the exactness limit (the job
+    # budget must keep every digit-sum product below 2^53)
+    top = (1 << bits) - 1
+    pairs = max(len(exact.pairs_of_level(t, S)) for t in range(T + 1))
+    assert pairs * k * top * top < 2**53
+    info = md.mdgemm_schedule_info(20, 130, k, S, T, bits=bits, flags=KMIN)
+    print(f"[case] karatsuba extreme digits S={S} T={T} k={k} w={bits}: {info}", flush=True)
+    assert k * info["max_job_weight"] * top * top < 2**53
+    m, n = 20, 130
+    DA_p = torch.zeros((S, md.panel_k(k), md.panel_mn(m)), dtype=torch.float64, device=DEV)
+    DB_p = torch.zeros((S, md.panel_k(k), md.panel_mn(n)), dtype=torch.float64, device=DEV)
+    DA_p[:, :k, :m] = float(top)
+    DB_p[:, :k, :n] = -float(top)
+    got = _host(md.mdgemm_schedule_levels(DA_p, DB_p, m, n, k, T, bits=bits, flags=KMIN))
+    for t in range(T + 1):
+        want = -len(exact.pairs_of_level(t, S)) * k * top * top
+        assert (got[t] == float(want)).all(), t
+
+
+@pytest.mark.parametrize("L,m,k,n,cutoff,seed", [(2, 64, 64, 64, -2, 0), (2, 130, 47, 129, -1, 1),
+                                                 (1, 65, 33, 17, -2, 2), (3, 40, 100, 70, -1, 3),
+                                                 (4, 33, 20, 45, -1, 4), (4, 17, 64, 9, -2, 5),
+                                                 (2, 1, 1, 1, -1, 6), (3, 129, 16, 1, -2, 7),
+                                                 (8, 70, 33, 129, -1, 8), (16, 20, 17, 130, -1, 9),
+                                                 (2, 300, 200, 260, 5, 10)])
+def test_mdgemm_karatsuba_end_to_end(L, m, k, n, cutoff, seed):
+    print(f"[case] mdgemm karatsuba L={L} {m}x{k}x{n} cutoff={cutoff}", flush=True)
+    rng = np.random.default_rng(seed)
+    base = "normal" if seed % 2 else "uniform"
+    A = workloads.make_operand(rng, L, m, k, base, row_exp=15)
+    B = workloads.make_operand(rng, L, k, n, base, col_exp=15)
+    S = 4 * L
+    T = {-1: S - 1, -2: 2 * S - 2}.get(cutoff, cutoff)
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), cutoff=cutoff, flags=KMIN))
+    ref = pipeline.full_reference(A, B, S, T)
+    assert np.array_equal(C, ref["C"])
+    # the cost model's choice for this shape gives the same limbs
+    assert np.array_equal(_host(md.mdgemm_ex(_gpu(A), _gpu(B), cutoff=cutoff, flags=KARA)), ref["C"])
+
+
+@pytest.mark.parametrize("L,m,k,n,opts", [(2, 130, 64, 129, {"slice_bits": -1}), (4, 33, 64, 45, {"slice_bits": -1}),
+                                          (3, 40, 100, 70, {"slice_bits": 20}),
+                                          (2, 70, 48, 65, {"range_bits": 60}),
+                                          (2, 33, 100, 129, {"range_bits": 60, "slice_bits": -1})])
+def test_mdgemm_karatsuba_digit_options(L, m, k, n, opts):
+    w, S, T = md.mdgemm_plan(m, n, k, L, flags=KMIN, **opts)
+    print(f"[case] mdgemm karatsuba {opts} L={L} {m}x{k}x{n}: w={w} S={S} T={T}", flush=True)
+    rng = np.random.default_rng(L + k)
+    A = workloads.make_operand(rng, L, m, k, "normal", row_exp=5)
+    B = workloads.make_operand(rng, L, k, n, "normal", col_exp=5)
+    if "range_bits" in opts:
+        e = rng.integers(0, opts["range_bits"] + 1, k)
+        A *= np.ldexp(1.0, -e)[None, None, :]
+        B *= np.ldexp(1.0, e - opts["range_bits"])[None, :, None]
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), flags=KMIN, **opts))
+    ref = pipeline.full_reference(A, B, S, T, w)
+    assert np.array_equal(C, ref["C"])
+    for i in range(0, m, max(1, m // 3)):
+        for j in range(0, n, max(1, n // 3)):
+            want, mag = exact.exact_product(A, B, i, j)
+            assert abs(exact.value(C[:, i, j]) - want) <= exact.tolerance(k, L, mag), (i, j)
+
+
+def test_mdgemm_karatsuba_workspace_stream_and_graph():
+    print("[case] mdgemm karatsuba caller workspace, side stream, graph replays", flush=True)
+    L, m, k, n = 3, 150, 70, 140
+    rng = np.random.default_rng(99)
+    A_h = workloads.make_operand(rng, L, m, k, "normal", row_exp=10)
+    B_h = workloads.make_operand(rng, L, k, n, "normal", col_exp=10)
+    want = pipeline.full_reference(A_h, B_h, 4 * L, 4 * L - 1)["C"]
+    A, B = _gpu(A_h), _gpu(B_h)
+    need = md.mdgemm_workspace_bytes(m, n, k, L, flags=KMIN)
+    assert need > md.mdgemm_workspace_bytes(m, n, k, L)
+    ws = torch.empty(need, dtype=torch.uint8, device=DEV)
+    C = torch.empty((L, m, n), dtype=torch.float64, device=DEV)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        md.mdgemm_ex(A, B, C, workspace=ws, flags=KMIN)
+    side.synchronize()
+    assert np.array_equal(C.cpu().numpy(), want)
+    # capture with the caller workspace; replays with eager work in between
+    C.fill_(7.0)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            md.mdgemm_ex(A, B, C, workspace=ws, flags=KMIN, stream=s)
+    torch.cuda.current_stream().wait_stream(s)
+    for r in range(3):
+        C.fill_(-1.0)
+        ws.fill_(0x55)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(C.cpu().numpy(), want), r
+
+
+@pytest.mark.parametrize("L,m,k,n,cutoff", [(2, 1024, 300, 900, -1), (3, 700, 256, 1100, -1), (2, 513, 200, 640, -2)])
+def test_mdgemm_karatsuba_cost_model_shapes(L, m, k, n, cutoff):
+    # shapes where the cost model takes the Karatsuba schedule; sampled
+    # entries against the oracle's chain (bit-exact) and every entry against
+    # the pair schedule's product (bit-identical)
+    S = 4 * L
+    T = S - 1 if cutoff == -1 else 2 * S - 2
+    info = md.mdgemm_schedule_info(m, n, k, S, T, flags=KARA)
+    print(f"[case] mdgemm karatsuba (cost model) L={L} {m}x{k}x{n}: {info}", flush=True)
+    assert info["direct_levels"] == 0
+    rng = np.random.default_rng(m + n + k)
+    A_h = workloads.make_operand(rng, L, m, k, "normal", row_exp=12)
+    B_h = workloads.make_operand(rng, L, k, n, "normal", col_exp=12)
+    A, B = _gpu(A_h), _gpu(B_h)
+    C = _host(md.mdgemm_ex(A, B, cutoff=cutoff, flags=KARA))
+    assert np.array_equal(C, _host(md.mdgemm_ex(A, B, cutoff=cutoff)))
+    entries = [(0, 0), (m - 1, n - 1), (m // 2, n // 3), (7, n - 2), (m - 3, 5)]
+    ref = pipeline.reference_entries(A_h, B_h, S, T, entries)
+    for (i, j), r in ref.items():
+        assert C[:, i, j].tolist() == r["limbs"], (i, j)
