@@ -212,8 +212,8 @@ def main(argv=None) -> int:
 
     bytes_exp = 8.0 * (m * k + k * n) + 4.0 * (m + n)
     bytes_split = 8.0 * L * (m * k + k * n) + 8.0 * S * (m * k + k * n) + 4.0 * (m + n)
-    # the Karatsuba schedule's combinations: each one reads two panels and writes one
-    bytes_split += 24.0 * k * ((info["combos_a"] - S) * m + (info["combos_b"] - S) * n)
+    # the Karatsuba schedule's combinations (digit sums), written by the split beside the digits
+    bytes_split += 8.0 * k * ((info["combos_a"] - S) * m + (info["combos_b"] - S) * n)
     bytes_acc = 8.0 * info["planes"] * m * n + 8.0 * L * m * n + 4.0 * (m + n)
     gemm_ms = stage_ms[2]
     achieved = slice_flops / (gemm_ms * 1e-3) / 1e12

@@ -96,8 +96,8 @@ int64_t job_budget(int64_t k, int w) {
 // occupancy penalty (its LDS holds every level of a thread's element: 256
 // threads per block up to 15 levels, 128 up to 31, 64 beyond, where the plane
 // reads become latency-bound: measured ~1.4x and ~4x the HBM time); a level
-// entry ~0.1 ps per element; a combination panel of A reads two m x k panels
-// and writes one (24 m k bytes at ~4.5 TB/s), of B likewise with k x n.  Each
+// entry ~0.1 ps per element; a combination panel of A is written by the split
+// beside the digits (8 m k bytes at ~4.5 TB/s), of B likewise with k x n.  Each
 // size enters as a power of sqrt(2) (its code 2 log2(x), rounded), so that
 // nearby shapes share a cached schedule.
 constexpr double kTermRate = 70e12, kHbmRate = 4.5e12, kEntrySeconds = 0.1e-12;
@@ -112,8 +112,8 @@ mdg::ScheduleCosts schedule_costs(int mcode, int ncode, int kcode, int levels) {
   mdg::ScheduleCosts c;
   c.plane = 16.0 * occupancy / kHbmRate / term;
   c.entry = kEntrySeconds / term;
-  c.combo_a = 24.0 * m * k / kHbmRate / (term * m * n);
-  c.combo_b = 24.0 * k * n / kHbmRate / (term * m * n);
+  c.combo_a = 8.0 * m * k / kHbmRate / (term * m * n);
+  c.combo_b = 8.0 * k * n / kHbmRate / (term * m * n);
   return c;
 }
 
@@ -438,8 +438,8 @@ Parts parts(char* ws, const Layout& L) {
                reinterpret_cast<double*>(ws + L.g)};
 }
 
-// Before the level GEMMs: the combinations of both operands (from their digit
-// panels, already in place) and the schedule's device table.
+// Before the level GEMMs, when the digit panels are given (not split here): the
+// combinations of both operands from the panels, and the schedule's device table.
 int enqueue_schedule_inputs(const Planned& pl, int64_t m, int64_t n, int64_t k, const Parts& w, hipStream_t s) {
   const int64_t kp = mdg::panel_k(k), mp = mdg::panel_mn(m), np = mdg::panel_mn(n);
   MDG_TRY(hip_status(mdg::launch_combinations(pl.s, true, w.DA, kp * mp, s)));
@@ -558,10 +558,13 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
     MDG_TRY(hip_status(mdg::launch_exponents(m, k, 0, A, w.EA, s)));
     MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, w.EB, s)));
     if (timed) MDG_TRY(record(1, s));
-    // a2: exact splits into S digit panels, then the schedule's digit sums
-    MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, r.w, 0, A, w.EA, w.DA, true, s)));
-    MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, r.w, 1, B, w.EB, w.DB, true, s)));
-    MDG_TRY(enqueue_schedule_inputs(*pl, m, n, k, w, s));
+    // a2: exact splits into S digit panels and, beside them, the schedule's
+    // combinations (digit sums) from the same integers
+    MDG_TRY(hip_status(mdg::launch_upload(pl->t.words, w.table, s)));
+    MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, r.w, 0, A, w.EA, w.DA, true, s,
+                                         w.table + pl->t.masks_a_off, static_cast<int>(pl->s.mask_a.size()))));
+    MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, r.w, 1, B, w.EB, w.DB, true, s,
+                                         w.table + pl->t.masks_b_off, static_cast<int>(pl->s.mask_b.size()))));
     if (timed) MDG_TRY(record(2, s));
     // a3: level GEMMs (or the Karatsuba products) on the FP64 matrix cores
     MDG_TRY(enqueue_gemm(*pl, m, n, k, w, w.G, s));

@@ -51,8 +51,12 @@ hipError_t launch_line_spread(int64_t rows, int64_t cols, int axis, const double
 // D [S][rows][cols] (panel == false) or as a level-GEMM panel (panel == true):
 // axis 0: D [S][panel_k(cols)][panel_mn(rows)] (transposed), axis 1:
 // D [S][panel_k(rows)][panel_mn(cols)], zeros in the padding.
+// With panel == true and masks (the schedule's combination digit sets, two
+// words per combination, in device memory) and combos > S, panels S .. combos-1
+// receive the schedule's combinations (sums of digits) as well.
 hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
-                        double* D, bool panel, hipStream_t stream);
+                        double* D, bool panel, hipStream_t stream, const uint32_t* masks = nullptr,
+                        int combos = 0);
 
 // a3: products of the combination panels DAt [*][panel_k(k)][panel_mn(m)] and
 // DBp [*][panel_k(k)][panel_mn(n)] (combinations 0..S-1 are the digits); one

@@ -76,13 +76,14 @@ double schedule_cost(const Schedule& s, const ScheduleCosts& costs);
 // Device table of a schedule: 32-bit words
 //   [2 J job words: first | count << 16, out plane] [P pair words: a | b << 16]
 //   [planes + 1 chunk_first words] [2 words per chunk]
+//   [2 words per combination of A: digit set, low word first] [same for B]
 // The entries of plane j are chunks chunk_first[j] .. chunk_first[j+1]-1 of
 // four 16-bit entries each (level | (uint8)coef << 8, entry i in bits 16 (i%2)
 // of word i/2); a plane's last chunk is padded with (trash level, coef 0),
 // trash level = T + 1 (a slot the accumulation keeps and never reads).
 struct ScheduleTable {
   std::vector<uint32_t> words;
-  int64_t jobs_off = 0, pairs_off = 0, chunk_first_off = 0, chunks_off = 0;
+  int64_t jobs_off = 0, pairs_off = 0, chunk_first_off = 0, chunks_off = 0, masks_a_off = 0, masks_b_off = 0;
 };
 ScheduleTable schedule_table(const Schedule& s);
 

@@ -417,6 +417,17 @@ ScheduleTable schedule_table(const Schedule& s) {
   if (t.words.size() % 2) t.words.push_back(0);
   t.chunks_off = static_cast<int64_t>(t.words.size());
   t.words.insert(t.words.end(), chunks.begin(), chunks.end());
+  // combination digit sets (the split writes the combinations beside the digits)
+  t.masks_a_off = static_cast<int64_t>(t.words.size());
+  for (uint64_t m : s.mask_a) {
+    t.words.push_back(static_cast<uint32_t>(m));
+    t.words.push_back(static_cast<uint32_t>(m >> 32));
+  }
+  t.masks_b_off = static_cast<int64_t>(t.words.size());
+  for (uint64_t m : s.mask_b) {
+    t.words.push_back(static_cast<uint32_t>(m));
+    t.words.push_back(static_cast<uint32_t>(m >> 32));
+  }
   return t;
 }
 

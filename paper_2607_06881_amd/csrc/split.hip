@@ -159,6 +159,31 @@ __device__ inline void store_digits(const uint64_t (&I)[NW], int S, int w, bool 
   }
 }
 
+// The combinations c = S .. C-1 of the Karatsuba schedule (sums of digits of
+// this element, digit set masks[c] as two 32-bit words) to out[c * stride]:
+// every digit of a combination carries sign(V), so a combination is sign(V)
+// times the sum of the digits' w-bit fields of D, below 64 * 2^26 (exact).
+template <int NW>
+__device__ inline void store_combos(const uint64_t (&I)[NW], int S, int C, int w, bool neg,
+                                    const uint32_t* __restrict__ masks, double* __restrict__ out, int64_t stride) {
+  const uint64_t fmask = (1ull << w) - 1ull;
+  for (int c = S; c < C; ++c) {
+    uint64_t m = static_cast<uint64_t>(masks[2 * c]) | (static_cast<uint64_t>(masks[2 * c + 1]) << 32);
+    uint64_t sum = 0;
+    while (m) {
+      const int p = __builtin_ctzll(m);
+      m &= m - 1;
+      const int o = w * (S - 1 - p);  // digit p: bits o .. o + w - 1 of D
+      const int wi = o >> 6, b = o & 63;
+      uint64_t f = word_or_zero<NW>(I, wi) >> b;
+      if (b + w > 64) f |= word_or_zero<NW>(I, wi + 1) << (64 - b);
+      sum += f & fmask;
+    }
+    const double v = static_cast<double>(sum);  // below 2^32: exact
+    out[static_cast<int64_t>(c) * stride] = sum == 0 ? 0.0 : (neg ? -v : v);
+  }
+}
+
 // Row-major output: D [S][rows][cols], the layout of the input planes.
 template <int NW, int ML>
 __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, int L, int S, int w, int axis,
@@ -184,10 +209,13 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
 // with kp, mp, np rounded up to the GEMM tile (16 and 128) and zeros in the padding.
 // A block covers 64 lines (c) x 16 k: its reads of A touch 64 full 128-byte lines
 // and its stores are 512-byte rows of the panel.
+// With C > S, panels S .. C-1 receive the combinations of the Karatsuba
+// schedule (store_combos), computed from the same integer as the digits.
 template <int NW, int ML>
 __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t cols, int L, int S, int w, int axis,
                                                           int64_t kp, int64_t cp, const double* __restrict__ X,
-                                                          const int32_t* __restrict__ E, double* __restrict__ D) {
+                                                          const int32_t* __restrict__ E, double* __restrict__ D,
+                                                          const uint32_t* __restrict__ masks, int C) {
   const int64_t plane = rows * cols, pplane = kp * cp;
   const int64_t K = axis == 0 ? cols : rows;   // reduction length
   const int64_t Cn = axis == 0 ? rows : cols;  // lines (rows of A or columns of B)
@@ -218,8 +246,9 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
           uint64_t I[NW];
           const bool neg = floor_on_grid<NW, ML>(xs[b], L, e - w * S, I);
           store_digits<NW>(I, S, w, neg, out, pplane);
+          if (C > S) store_combos<NW>(I, S, C, w, neg, masks, out, pplane);
         } else {
-          for (int s = 0; s < S; ++s) out[static_cast<int64_t>(s) * pplane] = 0.0;
+          for (int s = 0; s < (C > S ? C : S); ++s) out[static_cast<int64_t>(s) * pplane] = 0.0;
         }
       }
     }
@@ -228,7 +257,7 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
 
 template <int NW, int ML>
 hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
-                     double* D, bool panel, hipStream_t stream) {
+                     double* D, bool panel, const uint32_t* masks, int C, hipStream_t stream) {
   if (!panel) {
     const unsigned gx = static_cast<unsigned>((cols + 255) / 256);
     const unsigned gy = static_cast<unsigned>(rows < 65535 ? rows : 65535);
@@ -242,36 +271,37 @@ hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int w, int axis, 
   const int64_t nkb = kp / 16;
   const unsigned gy = static_cast<unsigned>(nkb < 65535 ? nkb : 65535);
   hipLaunchKernelGGL((split_panel_kernel<NW, ML>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, w, axis, kp,
-                     cp, X, E, D);
+                     cp, X, E, D, masks, C);
   return hipGetLastError();
 }
 
 // Word counts instantiated for w S up to 844 digit bits (896 bits).
 template <int ML>
 hipError_t split_words(int words, int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
-                       const int32_t* E, double* D, bool panel, hipStream_t stream) {
-  if (words <= 2) return launch_nw<2, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
-  if (words <= 3) return launch_nw<3, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
-  if (words <= 4) return launch_nw<4, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
-  if (words <= 5) return launch_nw<5, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
-  if (words <= 6) return launch_nw<6, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
-  if (words <= 8) return launch_nw<8, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
-  if (words <= 10) return launch_nw<10, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
-  if (words <= 14) return launch_nw<14, ML>(rows, cols, L, S, w, axis, X, E, D, panel, stream);
+                       const int32_t* E, double* D, bool panel, const uint32_t* masks, int C, hipStream_t stream) {
+  if (words <= 2) return launch_nw<2, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+  if (words <= 3) return launch_nw<3, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+  if (words <= 4) return launch_nw<4, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+  if (words <= 5) return launch_nw<5, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+  if (words <= 6) return launch_nw<6, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+  if (words <= 8) return launch_nw<8, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+  if (words <= 10) return launch_nw<10, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+  if (words <= 14) return launch_nw<14, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
 hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
-                        double* D, bool panel, hipStream_t stream) {
+                        double* D, bool panel, hipStream_t stream, const uint32_t* masks, int combos) {
+  const int C = (panel && masks && combos > S) ? combos : S;
   if (rows == 0 || cols == 0) return hipSuccess;
   // The accumulator holds |V| / u < 2^(w S) with 52 fraction bits: w S + 52 bits,
   // in the next word count instantiated (extra words stay zero).
   const int words = (w * S + 52 + 63) / 64;
-  if (L <= 4) return split_words<4>(words, rows, cols, L, S, w, axis, X, E, D, panel, stream);
-  if (L <= 8) return split_words<8>(words, rows, cols, L, S, w, axis, X, E, D, panel, stream);
-  return split_words<16>(words, rows, cols, L, S, w, axis, X, E, D, panel, stream);
+  if (L <= 4) return split_words<4>(words, rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+  if (L <= 8) return split_words<8>(words, rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+  return split_words<16>(words, rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
 }
 
 }  // namespace mdg
