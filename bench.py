@@ -205,15 +205,17 @@ def main(argv=None) -> int:
     m, n, k, L = w.m, w.n, w.k, w.limbs
     pairs = workloads.pair_count(S, T)
     info = md.mdgemm_schedule_info(m, n, k, S, T, bits=bits, flags=sched_flags)
+    panels_f32 = bool(info["panels_f32"])  # digit panels kept in FP32 (every digit sum below 2^24)
     md_flops = w.md_flops()
     # the GEMMs actually run: one per digit pair, or the Karatsuba schedule's products
     slice_flops = 2.0 * m * n * k * info["terms"]
     value = md_flops / (ms_per_step * 1e-3) / 1e9
 
     bytes_exp = 8.0 * (m * k + k * n) + 4.0 * (m + n)
-    bytes_split = 8.0 * L * (m * k + k * n) + 8.0 * S * (m * k + k * n) + 4.0 * (m + n)
+    pe = 4.0 if panels_f32 else 8.0  # bytes per panel value
+    bytes_split = 8.0 * L * (m * k + k * n) + pe * S * (m * k + k * n) + 4.0 * (m + n)
     # the Karatsuba schedule's combinations (digit sums), written by the split beside the digits
-    bytes_split += 8.0 * k * ((info["combos_a"] - S) * m + (info["combos_b"] - S) * n)
+    bytes_split += pe * k * ((info["combos_a"] - S) * m + (info["combos_b"] - S) * n)
     bytes_acc = 8.0 * info["planes"] * m * n + 8.0 * L * m * n + 4.0 * (m + n)
     gemm_ms = stage_ms[2]
     achieved = slice_flops / (gemm_ms * 1e-3) / 1e12
@@ -225,7 +227,8 @@ def main(argv=None) -> int:
         "frac": round(achieved / MFMA_F64_PEAK_TFLOPS, 4),
         # the stored counters were taken with the workload's 13-bit digits and pair schedule
         "traffic": stored_traffic(args.config) if bits_arg == 13 and not sched_flags else None,
-        "kernel": "slice_gemm_kernel (level GEMMs, v_mfma_f64_16x16x4f64)",
+        "kernel": ("slice_gemm32_kernel (level GEMMs on FP32 digit panels, v_mfma_f64_16x16x4f64)"
+                   if panels_f32 else "slice_gemm_kernel (level GEMMs on FP64 digit panels, v_mfma_f64_16x16x4f64)"),
         "flops_per_launch": slice_flops,
         "avg_launch_ms": round(gemm_ms, 4),
     }
@@ -240,7 +243,7 @@ def main(argv=None) -> int:
         "hbm_peak_GB/s": HBM_PEAK_GBS,
     }
     config = {"workload": f"{w.name}: {w.description}", "m": m, "n": n, "k": k, "limbs": L, "slices": S,
-              "cutoff": T, "pairs": pairs, "seed": w.seed}
+              "cutoff": T, "pairs": pairs, "seed": w.seed, "panels": "f32" if panels_f32 else "f64"}
     if sched_flags:
         config["schedule"] = "karatsuba"
         config["products"] = info["terms"]

@@ -137,11 +137,13 @@ int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const do
 /* Bytes of device workspace mdgemm_ex needs for this product and these options
  * (0 for an empty product; SIZE_MAX for invalid arguments).  Layout, each part
  * aligned to 256 bytes: EA int32[m], EB int32[n], flag int32, the schedule's
- * job table (32-bit words), the combination panels of A f64[CA][kp][mp] and of
- * B f64[CB][kp][np] (kp = k rounded up to 16, mp and np = m and n rounded up to
- * 128; the first S combinations are the digits, CA = CB = S for the pair
- * schedule), the GEMM output planes f64[P][m][n] (P = T+1 levels for the pair
- * schedule, the schedule's planes for MDGEMM_KARATSUBA). */
+ * job table (32-bit words), the combination panels of A [CA][kp][mp] and of
+ * B [CB][kp][np] (FP32 with kp = k rounded up to 32 when every panel value is
+ * below 2^24 (mdgemm_schedule_info, info[10]), else FP64 with kp = k rounded up
+ * to 16; mp and np = m and n rounded up to 128; the first S combinations are the
+ * digits, CA = CB = S for the pair schedule), the GEMM output planes f64[P][m][n]
+ * (P = T+1 levels for the pair schedule, the schedule's planes for
+ * MDGEMM_KARATSUBA). */
 size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts);
 
 /* C = A.B with explicit options (opts may be NULL for the defaults).  Runs, in
@@ -245,7 +247,7 @@ int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int slice_bit
  * MDGEMM_KARATSUBA_MIN_TERMS takes the plan with the fewest GEMMs whatever the
  * other costs (it overrides MDGEMM_KARATSUBA). */
 
-#define MDGEMM_SCHEDULE_INFO 9 /* entries written by mdgemm_schedule_info */
+#define MDGEMM_SCHEDULE_INFO 11 /* entries written by mdgemm_schedule_info */
 
 /* Size of the schedule mdgemm_ex uses for an m x k by k x n product with
  * S = slices digits of slice_bits bits, cutoff T, and flags (MDGEMM_KARATSUBA,
@@ -254,7 +256,10 @@ int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int slice_bit
  *   info[1] GEMM jobs, info[2] output planes, info[3] combinations of A,
  *   info[4] combinations of B, info[5] level entries, info[6] largest job weight
  *   sum(|comb a| |comb b|), info[7] deepest combination (0 = digits only),
- *   info[8] 1 when the planes are the levels themselves (pair schedule).
+ *   info[8] 1 when the planes are the levels themselves (pair schedule),
+ *   info[9] digits in the largest combination (1 for the pair schedule),
+ *   info[10] 1 when mdgemm_ex keeps the panels in FP32 (every panel value, at
+ *     most info[9] (2^w - 1), below 2^24: exact; k rounded up to 32), else FP64.
  * Host only (no HIP call).  Returns the count written or MDGEMM_EINVAL. */
 int mdgemm_schedule_info(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, unsigned flags,
                          int64_t* info, int count);

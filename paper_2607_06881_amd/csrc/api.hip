@@ -121,6 +121,7 @@ mdg::ScheduleCosts schedule_costs(int mcode, int ncode, int kcode, int levels) {
 struct Planned {
   mdg::Schedule s;
   mdg::ScheduleTable t;
+  int max_digits = 1;  // digits in the largest combination of A or B
 };
 
 struct ScheduleCache {
@@ -162,6 +163,8 @@ std::shared_ptr<const Planned> schedule_for(int S, int T, int64_t m, int64_t n, 
     pl->s = mdg::karatsuba_schedule(S, T, budget, schedule_costs(mc, nc, kc, T + 1), true);
   else pl->s = mdg::karatsuba_schedule(S, T, budget, mdg::ScheduleCosts{}, false);
   pl->t = mdg::schedule_table(pl->s);
+  for (uint64_t x : pl->s.mask_a) pl->max_digits = std::max(pl->max_digits, __builtin_popcountll(x));
+  for (uint64_t x : pl->s.mask_b) pl->max_digits = std::max(pl->max_digits, __builtin_popcountll(x));
   std::shared_ptr<const Planned> sp = pl;
   std::lock_guard<std::mutex> lock(c.mu);
   return c.map.emplace(key, sp).first->second;
@@ -264,19 +267,28 @@ int resolve(int limbs, int64_t m, int64_t n, int64_t k, const mdgemm_opts* opts,
   return MDGEMM_OK;
 }
 
+// FP32 panels when every panel value (a digit, or a combination of up to
+// max_digits digits) is an integer below 2^24, so that FP32 holds it exactly.
+bool panels_f32(const Planned& pl, int w) {
+  return static_cast<uint64_t>(pl.max_digits) * ((1ull << w) - 1ull) < (1ull << 24);
+}
+
 struct Layout {
   size_t ea = 0, eb = 0, flag = 0, table = 0, da = 0, db = 0, g = 0, total = 0;
+  bool f32 = false;  // FP32 panels with panel_k32 rows, else FP64 with panel_k rows
 };
 
 // EA | EB | flag | schedule table | A's combinations | B's combinations | planes,
 // each aligned to 256 bytes (combinations 0..S-1 are the digit panels).
-bool layout(int64_t m, int64_t n, int64_t k, const Planned& pl, Layout* L) {
+bool layout(int64_t m, int64_t n, int64_t k, const Planned& pl, int w, Layout* L) {
   const mdg::Schedule& sch = pl.s;
   const double ca = static_cast<double>(sch.mask_a.size()), cb = static_cast<double>(sch.mask_b.size());
   // all products below 2^62 so that size arithmetic cannot overflow
-  const double approx = ca * (double)m * (double)k + cb * (double)k * (double)n +
+  const double approx = ca * (double)m * (double)(k + 32) + cb * (double)(k + 32) * (double)n +
                         (double)sch.planes * (double)m * (double)n;
   if (approx * 8.0 > 4.0e18) return false;
+  L->f32 = panels_f32(pl, w);
+  const size_t esz = L->f32 ? sizeof(float) : sizeof(double);
   size_t off = 0;
   L->ea = off;
   off += align_up(sizeof(int32_t) * static_cast<size_t>(m));
@@ -287,11 +299,11 @@ bool layout(int64_t m, int64_t n, int64_t k, const Planned& pl, Layout* L) {
   L->table = off;
   off += align_up(sizeof(uint32_t) * pl.t.words.size());
   L->da = off;
-  const size_t kp = static_cast<size_t>(mdg::panel_k(k)), mp = static_cast<size_t>(mdg::panel_mn(m)),
-               np = static_cast<size_t>(mdg::panel_mn(n));
-  off += align_up(sizeof(double) * sch.mask_a.size() * kp * mp);
+  const size_t kp = static_cast<size_t>(L->f32 ? mdg::panel_k32(k) : mdg::panel_k(k)),
+               mp = static_cast<size_t>(mdg::panel_mn(m)), np = static_cast<size_t>(mdg::panel_mn(n));
+  off += align_up(esz * sch.mask_a.size() * kp * mp);
   L->db = off;
-  off += align_up(sizeof(double) * sch.mask_b.size() * kp * np);
+  off += align_up(esz * sch.mask_b.size() * kp * np);
   L->g = off;
   off += align_up(sizeof(double) * static_cast<size_t>(sch.planes) * static_cast<size_t>(m) * static_cast<size_t>(n));
   L->total = off;
@@ -425,25 +437,34 @@ inline int hip_status(hipError_t e) { return e == hipSuccess ? MDGEMM_OK : MDGEM
     if (st_ != MDGEMM_OK) return st_; \
   } while (0)
 
-// Pointers into a workspace laid out by layout().
+// Pointers into a workspace laid out by layout(); DA / DB are float* for FP32 panels.
 struct Parts {
   int32_t *EA, *EB, *flag;
   uint32_t* table;
-  double *DA, *DB, *G;
+  void *DA, *DB;
+  double* G;
+  bool f32;
 };
 Parts parts(char* ws, const Layout& L) {
   return Parts{reinterpret_cast<int32_t*>(ws + L.ea), reinterpret_cast<int32_t*>(ws + L.eb),
                reinterpret_cast<int32_t*>(ws + L.flag), reinterpret_cast<uint32_t*>(ws + L.table),
-               reinterpret_cast<double*>(ws + L.da),   reinterpret_cast<double*>(ws + L.db),
-               reinterpret_cast<double*>(ws + L.g)};
+               ws + L.da,
+               ws + L.db,
+               reinterpret_cast<double*>(ws + L.g),
+               L.f32};
 }
 
 // Before the level GEMMs, when the digit panels are given (not split here): the
 // combinations of both operands from the panels, and the schedule's device table.
 int enqueue_schedule_inputs(const Planned& pl, int64_t m, int64_t n, int64_t k, const Parts& w, hipStream_t s) {
-  const int64_t kp = mdg::panel_k(k), mp = mdg::panel_mn(m), np = mdg::panel_mn(n);
-  MDG_TRY(hip_status(mdg::launch_combinations(pl.s, true, w.DA, kp * mp, s)));
-  MDG_TRY(hip_status(mdg::launch_combinations(pl.s, false, w.DB, kp * np, s)));
+  const int64_t kp = w.f32 ? mdg::panel_k32(k) : mdg::panel_k(k), mp = mdg::panel_mn(m), np = mdg::panel_mn(n);
+  if (w.f32) {
+    MDG_TRY(hip_status(mdg::launch_combinations32(pl.s, true, static_cast<float*>(w.DA), kp * mp, s)));
+    MDG_TRY(hip_status(mdg::launch_combinations32(pl.s, false, static_cast<float*>(w.DB), kp * np, s)));
+  } else {
+    MDG_TRY(hip_status(mdg::launch_combinations(pl.s, true, static_cast<double*>(w.DA), kp * mp, s)));
+    MDG_TRY(hip_status(mdg::launch_combinations(pl.s, false, static_cast<double*>(w.DB), kp * np, s)));
+  }
   return hip_status(mdg::launch_upload(pl.t.words, w.table, s));
 }
 
@@ -452,7 +473,11 @@ int enqueue_gemm(const Planned& pl, int64_t m, int64_t n, int64_t k, const Parts
   jobs.jobs = w.table + pl.t.jobs_off;
   jobs.pairs = w.table + pl.t.pairs_off;
   jobs.njobs = static_cast<int>(pl.s.job_first.size());
-  return hip_status(mdg::launch_slice_gemm(m, n, k, w.DA, w.DB, out, jobs, s));
+  if (w.f32)
+    return hip_status(mdg::launch_slice_gemm32(m, n, k, static_cast<const float*>(w.DA),
+                                               static_cast<const float*>(w.DB), out, jobs, s));
+  return hip_status(mdg::launch_slice_gemm(m, n, k, static_cast<const double*>(w.DA),
+                                           static_cast<const double*>(w.DB), out, jobs, s));
 }
 
 }  // namespace
@@ -499,7 +524,7 @@ size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const 
   if (m < 0 || n < 0 || k < 0 || resolve(limbs, m, n, k, opts, &r) != MDGEMM_OK) return SIZE_MAX;
   if (m == 0 || n == 0 || k == 0) return 0;
   Layout L;
-  if (!layout(m, n, k, *schedule_for(r.S, r.T, m, n, k, r.w, r.kind), &L)) return SIZE_MAX;
+  if (!layout(m, n, k, *schedule_for(r.S, r.T, m, n, k, r.w, r.kind), r.w, &L)) return SIZE_MAX;
   return L.total;
 }
 
@@ -527,7 +552,7 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   const auto pl = schedule_for(r.S, r.T, m, n, k, r.w, r.kind);
   if (!schedule_exact(pl->s, k, r.w)) return MDGEMM_EEXACT;
   Layout L;
-  if (!layout(m, n, k, *pl, &L)) return MDGEMM_EINVAL;
+  if (!layout(m, n, k, *pl, r.w, &L)) return MDGEMM_EINVAL;
   char* ws = nullptr;
   LibraryBuffer lib;
   if (opts && opts->workspace) {
@@ -562,9 +587,11 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
     // combinations (digit sums) from the same integers
     MDG_TRY(hip_status(mdg::launch_upload(pl->t.words, w.table, s)));
     MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, r.w, 0, A, w.EA, w.DA, true, s,
-                                         w.table + pl->t.masks_a_off, static_cast<int>(pl->s.mask_a.size()))));
+                                         w.table + pl->t.masks_a_off, static_cast<int>(pl->s.mask_a.size()),
+                                         w.f32)));
     MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, r.w, 1, B, w.EB, w.DB, true, s,
-                                         w.table + pl->t.masks_b_off, static_cast<int>(pl->s.mask_b.size()))));
+                                         w.table + pl->t.masks_b_off, static_cast<int>(pl->s.mask_b.size()),
+                                         w.f32)));
     if (timed) MDG_TRY(record(2, s));
     // a3: level GEMMs (or the Karatsuba products) on the FP64 matrix cores
     MDG_TRY(enqueue_gemm(*pl, m, n, k, w, w.G, s));
@@ -701,8 +728,9 @@ int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int slice_bit
   MDG_TRY(lib.acquire(sizeof(uint32_t) * pl->t.words.size(), s, &tab));
   Parts w{};
   w.table = reinterpret_cast<uint32_t*>(tab);
-  w.DA = const_cast<double*>(DAt);
+  w.DA = const_cast<double*>(DAt);  // the caller's FP64 panels, read in place
   w.DB = const_cast<double*>(DBp);
+  w.f32 = false;
   int st = hip_status(mdg::launch_upload(pl->t.words, w.table, s));
   if (st == MDGEMM_OK) st = enqueue_gemm(*pl, m, n, k, w, out, s);
   return lib.release(st);
@@ -727,7 +755,9 @@ int mdgemm_schedule_info(int64_t m, int64_t n, int64_t k, int slices, int slice_
                                            static_cast<int64_t>(sc.entry_level.size()),
                                            sc.max_job_weight,
                                            max_depth,
-                                           sc.direct_levels ? 1 : 0};
+                                           sc.direct_levels ? 1 : 0,
+                                           pl->max_digits,
+                                           panels_f32(*pl, slice_bits) ? 1 : 0};
   const int nw = std::min(count, MDGEMM_SCHEDULE_INFO);
   for (int i = 0; i < nw; ++i) info[i] = v[i];
   return nw;
@@ -781,7 +811,7 @@ size_t mdgemm_schedule_workspace_bytes(int64_t m, int64_t n, int64_t k, int slic
   const auto pl = schedule_for(slices, cutoff, m, n, k, slice_bits,
                                kind_of(flags));
   Layout L;
-  if (!layout(m, n, k, *pl, &L)) return SIZE_MAX;
+  if (!layout(m, n, k, *pl, slice_bits, &L)) return SIZE_MAX;
   return L.total;
 }
 
@@ -801,7 +831,7 @@ int mdgemm_schedule_levels(int64_t m, int64_t n, int64_t k, int slices, int slic
                                kind_of(flags));
   if (!schedule_exact(pl->s, k, slice_bits)) return MDGEMM_EEXACT;
   Layout L;
-  if (!layout(m, n, k, *pl, &L)) return MDGEMM_EINVAL;
+  if (!layout(m, n, k, *pl, slice_bits, &L)) return MDGEMM_EINVAL;
   const size_t kp = static_cast<size_t>(mdg::panel_k(k)), mp = static_cast<size_t>(mdg::panel_mn(m)),
                np = static_cast<size_t>(mdg::panel_mn(n));
   const size_t abytes = sizeof(double) * slices * kp * mp, bbytes = sizeof(double) * slices * kp * np;
@@ -820,9 +850,18 @@ int mdgemm_schedule_levels(int64_t m, int64_t n, int64_t k, int slices, int slic
   }
   const Parts w = parts(ws, L);
   auto enqueue = [&]() -> int {
-    // the digit panels are combinations 0..S-1 of the schedule
-    MDG_TRY(hip_status(hipMemcpyAsync(w.DA, DAt, abytes, hipMemcpyDeviceToDevice, s)));
-    MDG_TRY(hip_status(hipMemcpyAsync(w.DB, DBp, bbytes, hipMemcpyDeviceToDevice, s)));
+    // the digit panels are combinations 0..S-1 of the schedule (as FP32 panels
+    // with 32-row k steps when every value fits, like mdgemm_ex)
+    if (w.f32) {
+      const int64_t kp32 = mdg::panel_k32(k);
+      MDG_TRY(hip_status(mdg::launch_panel_to_f32(DAt, static_cast<float*>(w.DA), static_cast<int64_t>(kp), kp32,
+                                                  static_cast<int64_t>(mp), slices, s)));
+      MDG_TRY(hip_status(mdg::launch_panel_to_f32(DBp, static_cast<float*>(w.DB), static_cast<int64_t>(kp), kp32,
+                                                  static_cast<int64_t>(np), slices, s)));
+    } else {
+      MDG_TRY(hip_status(hipMemcpyAsync(w.DA, DAt, abytes, hipMemcpyDeviceToDevice, s)));
+      MDG_TRY(hip_status(hipMemcpyAsync(w.DB, DBp, bbytes, hipMemcpyDeviceToDevice, s)));
+    }
     MDG_TRY(enqueue_schedule_inputs(*pl, m, n, k, w, s));
     if (pl->s.direct_levels) return enqueue_gemm(*pl, m, n, k, w, G, s);
     MDG_TRY(enqueue_gemm(*pl, m, n, k, w, w.G, s));

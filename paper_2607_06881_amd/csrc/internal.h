@@ -26,6 +26,9 @@ constexpr int kTileK = 16;    // level-GEMM k step
 // Panel dimensions of the level-GEMM operands: k rounded up to the k step,
 // m / n rounded up to the tile.
 inline int64_t panel_k(int64_t k) { return (k + kTileK - 1) / kTileK * kTileK; }
+// FP32 panels (every digit and digit sum below 2^24) use 32-deep k steps.
+constexpr int kTileK32 = 32;
+inline int64_t panel_k32(int64_t k) { return (k + kTileK32 - 1) / kTileK32 * kTileK32; }
 inline int64_t panel_mn(int64_t x) { return (x + kTileMN - 1) / kTileMN * kTileMN; }
 
 // Slice-pair jobs of the level GEMM, read from a device table in the format of
@@ -53,16 +56,22 @@ hipError_t launch_line_spread(int64_t rows, int64_t cols, int axis, const double
 // D [S][panel_k(rows)][panel_mn(cols)], zeros in the padding.
 // With panel == true and masks (the schedule's combination digit sets, two
 // words per combination, in device memory) and combos > S, panels S .. combos-1
-// receive the schedule's combinations (sums of digits) as well.
+// receive the schedule's combinations (sums of digits) as well.  D is double*,
+// or float* with f32 (panels only: panel_k32 rows, every value below 2^24).
 hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
-                        double* D, bool panel, hipStream_t stream, const uint32_t* masks = nullptr,
-                        int combos = 0);
+                        void* D, bool panel, hipStream_t stream, const uint32_t* masks = nullptr,
+                        int combos = 0, bool f32 = false);
 
 // a3: products of the combination panels DAt [*][panel_k(k)][panel_mn(m)] and
 // DBp [*][panel_k(k)][panel_mn(n)] (combinations 0..S-1 are the digits); one
 // job per grid row, outputs [*][m][n].
 hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DAt, const double* DBp, double* out,
                              const GemmJobs& jobs, hipStream_t stream);
+
+// a3 on FP32 panels DAt [*][panel_k32(k)][panel_mn(m)], DBp [*][panel_k32(k)][panel_mn(n)]
+// whose values are integers below 2^24 (exact in FP32); same jobs and outputs.
+hipError_t launch_slice_gemm32(int64_t m, int64_t n, int64_t k, const float* DAt, const float* DBp, double* out,
+                               const GemmJobs& jobs, hipStream_t stream);
 
 // Copies `words` into the device array dst (stream-ordered kernel launches that
 // carry the words as arguments, so that no host memory is read later).
@@ -72,6 +81,12 @@ hipError_t launch_upload(const std::vector<uint32_t>& words, uint32_t* dst, hipS
 // selects A's or B's): panel c = panel par1[c] + panel par2[c], whole panels of
 // `plane` doubles, in order of depth.
 hipError_t launch_combinations(const Schedule& s, bool a, double* D, int64_t plane, hipStream_t stream);
+hipError_t launch_combinations32(const Schedule& s, bool a, float* D, int64_t plane, hipStream_t stream);
+
+// FP64 panels [S][kp_src][cp] -> FP32 panels [S][kp_dst][cp], rows kp_src .. kp_dst-1
+// zero; every value an integer below 2^24.
+hipError_t launch_panel_to_f32(const double* src, float* dst, int64_t kp_src, int64_t kp_dst, int64_t cp, int S,
+                               hipStream_t stream);
 
 // a4: exact accumulation of `levels` planes of w-bit digit products (weights
 // 2^(-w t)) into kZWords-word integers Z [kZWords][m][n].

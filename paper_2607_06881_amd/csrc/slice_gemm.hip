@@ -181,6 +181,158 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
       }
 }
 
+// ---- the same product on FP32 panels ------------------------------------------
+//
+// Every digit and digit sum is an integer below 2^24 (checked on the host), so
+// the panels hold it exactly as FP32: half the split's writes and half the
+// GEMM's panel traffic.  The LDS footprint of a 16-deep FP64 step then holds a
+// 32-deep FP32 step, so each barrier is followed by 128 MFMAs per wave instead
+// of 64.  Each fragment value is widened back to FP64 (v_cvt_f64_f32, exact)
+// right before its MFMAs.
+//
+// LDS rows are 128 floats without padding, so that one global_load_lds_dwordx4
+// (64 lanes x 16 bytes) fills two rows in place; instead of padding, the 16-byte
+// granules of row r are stored XOR-swizzled by (r & 3) << 2.  A fragment read
+// (lanes 16h..16h+15 read row 4kg + h, 16 consecutive columns) then touches four
+// different 16-bank groups for h = 0..3: conflict-free.  Panels are k-major and
+// zero-padded to k multiple of 32, m / n multiple of 128.
+constexpr int BK32 = 32;
+constexpr int ROW32 = 128;  // floats per LDS row
+
+__global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, int64_t n, int64_t kp, int64_t mp,
+                                                                   int64_t np, int tiles_n, int ntiles,
+                                                                   const float* __restrict__ DAt,
+                                                                   const float* __restrict__ DBp,
+                                                                   double* __restrict__ out,
+                                                                   const uint32_t* __restrict__ jobs,
+                                                                   const uint32_t* __restrict__ pairs) {
+  __shared__ float As[2][BK32 * ROW32];
+  __shared__ float Bs[2][BK32 * ROW32];
+
+  // tile order as in slice_gemm_kernel
+  int t = blockIdx.x;
+  {
+    const int per = ntiles / kXcds;
+    if (t < per * kXcds) t = (t % kXcds) * per + t / kXcds;
+  }
+  const int tiles_m = ntiles / tiles_n;
+  const int gsz = kGroup * tiles_n, g = t / gsz, first = g * kGroup;
+  const int rows_in = min(kGroup, tiles_m - first), within = t - g * gsz;
+  const int64_t m0 = static_cast<int64_t>(first + within % rows_in) * BM;
+  const int64_t n0 = static_cast<int64_t>(within / rows_in) * BN;
+  const int job = blockIdx.y;
+  const uint32_t jw = jobs[2 * job];
+  const int pfirst = static_cast<int>(jw & 0xffffu), npairs = static_cast<int>(jw >> 16);
+  const int64_t out_plane = jobs[2 * job + 1];
+  const int64_t plane_a = kp * mp, plane_b = kp * np;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+
+  const int64_t nkb = kp / BK32;
+  const int64_t niter = nkb * npairs;
+
+  // Copies: wave w fills rows 8w .. 8w+7 of each tile, two rows per instruction
+  // (q = 0..3); lane L lands at row 8w + 2q + L/32, granule L%32, and fetches
+  // the panel granule (L%32) ^ (((2q + L/32) & 3) << 2) of that row.
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int half = lane >> 5, gran = lane & 31;
+  int32_t off_a[4], off_b[4];  // per-lane source offsets in floats, rows 2q + half of the wave's block
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int r = 2 * q + half;
+    const int sg = gran ^ ((r & 3) << 2);
+    off_a[q] = static_cast<int32_t>(r * mp + 4 * sg);
+    off_b[q] = static_cast<int32_t>(r * np + 4 * sg);
+  }
+  int lpi = 0;
+  int64_t lkb = 0;
+  uint32_t pr = pairs[pfirst];
+  uint32_t pr_next = npairs > 1 ? pairs[pfirst + 1] : 0u;
+  const int64_t row_a = 8 * wave_u * mp + m0, row_b = 8 * wave_u * np + n0;
+  const float* a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
+  const float* b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
+  auto issue = [&](int stage) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a + off_a[q]),
+                                       (lds_void*)(&As[stage][(8 * wave_u + 2 * q) * ROW32]), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(b + off_b[q]),
+                                       (lds_void*)(&Bs[stage][(8 * wave_u + 2 * q) * ROW32]), 16, 0, 0);
+    }
+    if (++lkb == nkb) {
+      lkb = 0;
+      ++lpi;
+      pr = pr_next;
+      if (lpi + 1 < npairs) pr_next = pairs[pfirst + lpi + 1];
+      a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
+      b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
+    } else {
+      a += BK32 * mp;
+      b += BK32 * np;
+    }
+  };
+
+  d4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
+
+  // Fragments: lane l = 16h + c reads row 4kg + h, column block i at
+  // ((i ^ h) * 16 + c) after the swizzle (wr * 64 floats = 16 granules is untouched).
+  const int h = lane >> 4, c = lane & 15;
+  int fa[4], fb[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    fa[i] = h * ROW32 + wr * 64 + ((i ^ h) << 4) + c;
+    fb[i] = h * ROW32 + wc * 64 + ((i ^ h) << 4) + c;
+  }
+  if (niter > 0) issue(0);
+  for (int64_t it = 0; it < niter; ++it) {
+    const int cur = static_cast<int>(it & 1);
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // this wave's copies of step it are in LDS
+    __syncthreads();                     // everyone's are; everyone is done reading the other stage
+    const float* as = As[cur];
+    const float* bs = Bs[cur];
+    float af[BK32 / 4][4], bf[BK32 / 4][4];
+#pragma unroll
+    for (int kg = 0; kg < BK32 / 4; ++kg)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        af[kg][i] = as[kg * 4 * ROW32 + fa[i]];
+        bf[kg][i] = bs[kg * 4 * ROW32 + fb[i]];
+      }
+    if (it + 1 < niter) issue(cur ^ 1);
+#pragma unroll
+    for (int kg = 0; kg < BK32 / 4; ++kg) {
+      double ad[4], bd[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        ad[i] = static_cast<double>(af[kg][i]);
+        bd[i] = static_cast<double>(bf[kg][i]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ad[i], bd[j], acc[i][j], 0, 0, 0);
+    }
+  }
+
+  double* o = out + out_plane * m * n;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t gi = m0 + wr * 64 + i * 16 + 4 * r + (lane >> 4);
+        const int64_t gj = n0 + wc * 64 + j * 16 + (lane & 15);
+        if (gi < m && gj < n) o[gi * n + gj] = acc[i][j][r];
+      }
+}
+
 }  // namespace
 
 hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DAt, const double* DBp, double* out,
@@ -191,6 +343,20 @@ hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DAt,
   const int64_t ntiles = (mp / BM) * tiles_n;
   if (ntiles > 0x7fffffff || jobs.njobs > 65535) return hipErrorInvalidValue;
   hipLaunchKernelGGL(slice_gemm_kernel, dim3(static_cast<unsigned>(ntiles), static_cast<unsigned>(jobs.njobs)),
+                     dim3(kThreads), 0, stream, m, n, kp, mp, np, static_cast<int>(tiles_n),
+                     static_cast<int>(ntiles), DAt, DBp, out, jobs.jobs, jobs.pairs);
+  return hipGetLastError();
+}
+
+hipError_t launch_slice_gemm32(int64_t m, int64_t n, int64_t k, const float* DAt, const float* DBp, double* out,
+                               const GemmJobs& jobs, hipStream_t stream) {
+  if (m == 0 || n == 0 || jobs.njobs == 0) return hipSuccess;
+  const int64_t mp = panel_mn(m), np = panel_mn(n), kp = panel_k32(k);
+  const int64_t tiles_n = np / BN;
+  const int64_t ntiles = (mp / BM) * tiles_n;
+  // per-lane copy offsets are 32-bit: 7 rows of a panel plus a row's width
+  if (ntiles > 0x7fffffff || jobs.njobs > 65535 || mp > (1 << 27) || np > (1 << 27)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(slice_gemm32_kernel, dim3(static_cast<unsigned>(ntiles), static_cast<unsigned>(jobs.njobs)),
                      dim3(kThreads), 0, stream, m, n, kp, mp, np, static_cast<int>(tiles_n),
                      static_cast<int>(ntiles), DAt, DBp, out, jobs.jobs, jobs.pairs);
   return hipGetLastError();
@@ -214,17 +380,31 @@ struct ComboChunk {
   uint16_t child[kComboChunk], p1[kComboChunk], p2[kComboChunk];
 };
 
-// panel child = panel p1 + panel p2 (integers: exact), two doubles per thread
-__global__ void __launch_bounds__(256) combination_kernel(const ComboChunk c, double* __restrict__ D, int64_t plane) {
+// panel child = panel p1 + panel p2 (integers below 2^24 for FP32 panels, below
+// 2^53 for FP64: exact), two values per thread
+template <class T>
+__global__ void __launch_bounds__(256) combination_kernel(const ComboChunk c, T* __restrict__ D, int64_t plane) {
   const int e = blockIdx.y;
-  const double2* a = reinterpret_cast<const double2*>(D + static_cast<int64_t>(c.p1[e]) * plane);
-  const double2* b = reinterpret_cast<const double2*>(D + static_cast<int64_t>(c.p2[e]) * plane);
-  double2* d = reinterpret_cast<double2*>(D + static_cast<int64_t>(c.child[e]) * plane);
-  const int64_t half = plane / 2;
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < half;
+  const T* a = D + static_cast<int64_t>(c.p1[e]) * plane;
+  const T* b = D + static_cast<int64_t>(c.p2[e]) * plane;
+  T* d = D + static_cast<int64_t>(c.child[e]) * plane;
+  for (int64_t i = 2 * (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x); i < plane;
+       i += 2 * static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const T x0 = a[i], x1 = a[i + 1], y0 = b[i], y1 = b[i + 1];
+    d[i] = x0 + y0;
+    d[i + 1] = x1 + y1;
+  }
+}
+
+// FP64 panels [S][kp_src][cp] -> FP32 panels [S][kp_dst][cp] (kp_dst >= kp_src, zero
+// rows beyond kp_src); values are integers below 2^24, so the conversion is exact.
+__global__ void __launch_bounds__(256) panel_to_f32_kernel(const double* __restrict__ src, float* __restrict__ dst,
+                                                           int64_t kp_src, int64_t kp_dst, int64_t cp, int S) {
+  const int64_t total = static_cast<int64_t>(S) * kp_dst * cp;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
        i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-    const double2 x = a[i], y = b[i];
-    d[i] = double2{x.x + y.x, x.y + y.y};
+    const int64_t s = i / (kp_dst * cp), r = (i / cp) % kp_dst, c = i % cp;
+    dst[i] = r < kp_src ? static_cast<float>(src[(s * kp_src + r) * cp + c]) : 0.0f;
   }
 }
 
@@ -242,21 +422,21 @@ hipError_t launch_upload(const std::vector<uint32_t>& words, uint32_t* dst, hipS
   return hipSuccess;
 }
 
-hipError_t launch_combinations(const Schedule& s, bool a, double* D, int64_t plane, hipStream_t stream) {
+template <class T>
+hipError_t combinations(const Schedule& s, bool a, T* D, int64_t plane, hipStream_t stream) {
   const std::vector<int>& depth = a ? s.depth_a : s.depth_b;
   const std::vector<int>& p1 = a ? s.par1_a : s.par1_b;
   const std::vector<int>& p2 = a ? s.par2_a : s.par2_b;
   int max_depth = 0;
   for (int d : depth) max_depth = std::max(max_depth, d);
-  // panels are whole multiples of 16 x 128 doubles: an even count
-  const int64_t half = plane / 2;
-  const unsigned gx = static_cast<unsigned>(std::min<int64_t>((half + 255) / 256, 1024));
+  // panels are whole multiples of 16 x 128 values: an even count
+  const unsigned gx = static_cast<unsigned>(std::min<int64_t>((plane / 2 + 255) / 256, 1024));
   for (int d = 1; d <= max_depth; ++d) {
     ComboChunk c;
     c.count = 0;
     auto flush = [&]() -> hipError_t {
       if (c.count == 0) return hipSuccess;
-      hipLaunchKernelGGL(combination_kernel, dim3(gx, static_cast<unsigned>(c.count)), dim3(256), 0, stream, c, D,
+      hipLaunchKernelGGL(combination_kernel<T>, dim3(gx, static_cast<unsigned>(c.count)), dim3(256), 0, stream, c, D,
                          plane);
       c.count = 0;
       return hipGetLastError();
@@ -275,6 +455,23 @@ hipError_t launch_combinations(const Schedule& s, bool a, double* D, int64_t pla
     if (err != hipSuccess) return err;
   }
   return hipSuccess;
+}
+
+hipError_t launch_combinations(const Schedule& s, bool a, double* D, int64_t plane, hipStream_t stream) {
+  return combinations<double>(s, a, D, plane, stream);
+}
+
+hipError_t launch_combinations32(const Schedule& s, bool a, float* D, int64_t plane, hipStream_t stream) {
+  return combinations<float>(s, a, D, plane, stream);
+}
+
+hipError_t launch_panel_to_f32(const double* src, float* dst, int64_t kp_src, int64_t kp_dst, int64_t cp, int S,
+                               hipStream_t stream) {
+  const int64_t total = static_cast<int64_t>(S) * kp_dst * cp;
+  if (total == 0) return hipSuccess;
+  const unsigned g = static_cast<unsigned>(std::min<int64_t>((total + 255) / 256, 4096));
+  hipLaunchKernelGGL(panel_to_f32_kernel, dim3(g), dim3(256), 0, stream, src, dst, kp_src, kp_dst, cp, S);
+  return hipGetLastError();
 }
 
 }  // namespace mdg

@@ -139,8 +139,8 @@ __device__ inline uint64_t word_or_zero(const uint64_t (&v)[NW], int i) {
 // Digit s of I (bits w(S-1-s) .. w(S-s)-1) to out[s * stride] for every s, read
 // upward from bit 0 through a two-word window: one select over the words per
 // 64 bits consumed instead of one per digit.
-template <int NW>
-__device__ inline void store_digits(const uint64_t (&I)[NW], int S, int w, bool neg, double* __restrict__ out,
+template <int NW, class OutT>
+__device__ inline void store_digits(const uint64_t (&I)[NW], int S, int w, bool neg, OutT* __restrict__ out,
                                     int64_t stride) {
   const uint64_t mask = (1ull << w) - 1ull;
   uint64_t cur = I[0], nxt = NW > 1 ? I[1] : 0ull;
@@ -148,7 +148,7 @@ __device__ inline void store_digits(const uint64_t (&I)[NW], int S, int w, bool 
   for (int j = 0; j < S; ++j) {
     uint64_t f = cur >> b;
     if (b + w > 64) f |= nxt << (64 - b);  // b > 64 - w > 0 here
-    out[static_cast<int64_t>(S - 1 - j) * stride] = signed_digit(static_cast<uint32_t>(f & mask), neg);
+    out[static_cast<int64_t>(S - 1 - j) * stride] = static_cast<OutT>(signed_digit(static_cast<uint32_t>(f & mask), neg));
     b += w;
     if (b >= 64) {
       b -= 64;
@@ -163,9 +163,9 @@ __device__ inline void store_digits(const uint64_t (&I)[NW], int S, int w, bool 
 // this element, digit set masks[c] as two 32-bit words) to out[c * stride]:
 // every digit of a combination carries sign(V), so a combination is sign(V)
 // times the sum of the digits' w-bit fields of D, below 64 * 2^26 (exact).
-template <int NW>
+template <int NW, class OutT>
 __device__ inline void store_combos(const uint64_t (&I)[NW], int S, int C, int w, bool neg,
-                                    const uint32_t* __restrict__ masks, double* __restrict__ out, int64_t stride) {
+                                    const uint32_t* __restrict__ masks, OutT* __restrict__ out, int64_t stride) {
   const uint64_t fmask = (1ull << w) - 1ull;
   for (int c = S; c < C; ++c) {
     uint64_t m = static_cast<uint64_t>(masks[2 * c]) | (static_cast<uint64_t>(masks[2 * c + 1]) << 32);
@@ -180,7 +180,7 @@ __device__ inline void store_combos(const uint64_t (&I)[NW], int S, int C, int w
       sum += f & fmask;
     }
     const double v = static_cast<double>(sum);  // below 2^32: exact
-    out[static_cast<int64_t>(c) * stride] = sum == 0 ? 0.0 : (neg ? -v : v);
+    out[static_cast<int64_t>(c) * stride] = static_cast<OutT>(sum == 0 ? 0.0 : (neg ? -v : v));
   }
 }
 
@@ -199,7 +199,7 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
     load_limbs<ML>(X, plane, L, idx, xs);
     uint64_t I[NW];
     const bool neg = floor_on_grid<NW, ML>(xs, L, e - w * S, I);
-    store_digits<NW>(I, S, w, neg, D + idx, plane);
+    store_digits<NW, double>(I, S, w, neg, D + idx, plane);
   }
 }
 
@@ -211,10 +211,12 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
 // and its stores are 512-byte rows of the panel.
 // With C > S, panels S .. C-1 receive the combinations of the Karatsuba
 // schedule (store_combos), computed from the same integer as the digits.
-template <int NW, int ML>
+// OutT = float for FP32 panels (the host checks that every value is below 2^24,
+// so the conversion is exact; kp is then a multiple of 32).
+template <int NW, int ML, class OutT>
 __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t cols, int L, int S, int w, int axis,
                                                           int64_t kp, int64_t cp, const double* __restrict__ X,
-                                                          const int32_t* __restrict__ E, double* __restrict__ D,
+                                                          const int32_t* __restrict__ E, OutT* __restrict__ D,
                                                           const uint32_t* __restrict__ masks, int C) {
   const int64_t plane = rows * cols, pplane = kp * cp;
   const int64_t K = axis == 0 ? cols : rows;   // reduction length
@@ -241,14 +243,14 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
 #pragma unroll
       for (int b = 0; b < kBatch; ++b) {
         const int64_t kk = kb * 16 + (threadIdx.x >> 6) + 4 * (r0 + b);
-        double* out = D + kk * cp + c;
+        OutT* out = D + kk * cp + c;
         if (valid[b]) {
           uint64_t I[NW];
           const bool neg = floor_on_grid<NW, ML>(xs[b], L, e - w * S, I);
-          store_digits<NW>(I, S, w, neg, out, pplane);
-          if (C > S) store_combos<NW>(I, S, C, w, neg, masks, out, pplane);
+          store_digits<NW, OutT>(I, S, w, neg, out, pplane);
+          if (C > S) store_combos<NW, OutT>(I, S, C, w, neg, masks, out, pplane);
         } else {
-          for (int s = 0; s < (C > S ? C : S); ++s) out[static_cast<int64_t>(s) * pplane] = 0.0;
+          for (int s = 0; s < (C > S ? C : S); ++s) out[static_cast<int64_t>(s) * pplane] = OutT(0);
         }
       }
     }
@@ -257,51 +259,57 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
 
 template <int NW, int ML>
 hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
-                     double* D, bool panel, const uint32_t* masks, int C, hipStream_t stream) {
+                     void* D, bool panel, bool f32, const uint32_t* masks, int C, hipStream_t stream) {
   if (!panel) {
     const unsigned gx = static_cast<unsigned>((cols + 255) / 256);
     const unsigned gy = static_cast<unsigned>(rows < 65535 ? rows : 65535);
     hipLaunchKernelGGL((split_kernel<NW, ML>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, w, axis, X, E,
-                       D);
+                       static_cast<double*>(D));
     return hipGetLastError();
   }
   const int64_t K = axis == 0 ? cols : rows, Cn = axis == 0 ? rows : cols;
-  const int64_t kp = panel_k(K), cp = panel_mn(Cn);
+  const int64_t kp = f32 ? panel_k32(K) : panel_k(K), cp = panel_mn(Cn);
   const unsigned gx = static_cast<unsigned>(cp / 64);
   const int64_t nkb = kp / 16;
   const unsigned gy = static_cast<unsigned>(nkb < 65535 ? nkb : 65535);
-  hipLaunchKernelGGL((split_panel_kernel<NW, ML>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, w, axis, kp,
-                     cp, X, E, D, masks, C);
+  if (f32)
+    hipLaunchKernelGGL((split_panel_kernel<NW, ML, float>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, w,
+                       axis, kp, cp, X, E, static_cast<float*>(D), masks, C);
+  else
+    hipLaunchKernelGGL((split_panel_kernel<NW, ML, double>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, w,
+                       axis, kp, cp, X, E, static_cast<double*>(D), masks, C);
   return hipGetLastError();
 }
 
 // Word counts instantiated for w S up to 844 digit bits (896 bits).
 template <int ML>
 hipError_t split_words(int words, int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
-                       const int32_t* E, double* D, bool panel, const uint32_t* masks, int C, hipStream_t stream) {
-  if (words <= 2) return launch_nw<2, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
-  if (words <= 3) return launch_nw<3, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
-  if (words <= 4) return launch_nw<4, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
-  if (words <= 5) return launch_nw<5, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
-  if (words <= 6) return launch_nw<6, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
-  if (words <= 8) return launch_nw<8, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
-  if (words <= 10) return launch_nw<10, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
-  if (words <= 14) return launch_nw<14, ML>(rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+                       const int32_t* E, void* D, bool panel, bool f32, const uint32_t* masks, int C,
+                       hipStream_t stream) {
+  if (words <= 2) return launch_nw<2, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+  if (words <= 3) return launch_nw<3, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+  if (words <= 4) return launch_nw<4, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+  if (words <= 5) return launch_nw<5, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+  if (words <= 6) return launch_nw<6, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+  if (words <= 8) return launch_nw<8, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+  if (words <= 10) return launch_nw<10, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+  if (words <= 14) return launch_nw<14, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
 hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
-                        double* D, bool panel, hipStream_t stream, const uint32_t* masks, int combos) {
+                        void* D, bool panel, hipStream_t stream, const uint32_t* masks, int combos, bool f32) {
+  if (f32 && !panel) return hipErrorInvalidValue;
   const int C = (panel && masks && combos > S) ? combos : S;
   if (rows == 0 || cols == 0) return hipSuccess;
   // The accumulator holds |V| / u < 2^(w S) with 52 fraction bits: w S + 52 bits,
   // in the next word count instantiated (extra words stay zero).
   const int words = (w * S + 52 + 63) / 64;
-  if (L <= 4) return split_words<4>(words, rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
-  if (L <= 8) return split_words<8>(words, rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
-  return split_words<16>(words, rows, cols, L, S, w, axis, X, E, D, panel, masks, C, stream);
+  if (L <= 4) return split_words<4>(words, rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+  if (L <= 8) return split_words<8>(words, rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+  return split_words<16>(words, rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
 }
 
 }  // namespace mdg

@@ -31,7 +31,7 @@ MDGEMM_SYNC = 2
 MDGEMM_TIME_STAGES = 4
 MDGEMM_KARATSUBA = 8
 MDGEMM_KARATSUBA_MIN_TERMS = 16
-MDGEMM_SCHEDULE_INFO = 9
+MDGEMM_SCHEDULE_INFO = 11
 
 MDGEMM_CUTOFF_DEFAULT = -1
 MDGEMM_CUTOFF_ALL = -2
@@ -45,10 +45,15 @@ MDGEMM_SLICE_BITS_AUTO = -1
 MDGEMM_Z_WORDS = 28
 PANEL_K = 16  # level-GEMM panels: k rounded up to 16,
 PANEL_MN = 128  # m and n rounded up to 128
+PANEL_K32 = 32  # FP32 panels inside mdgemm_ex: k rounded up to 32
 
 
 def panel_k(k: int) -> int:
     return (k + PANEL_K - 1) // PANEL_K * PANEL_K
+
+
+def panel_k32(k: int) -> int:
+    return (k + PANEL_K32 - 1) // PANEL_K32 * PANEL_K32
 
 
 def panel_mn(x: int) -> int:
@@ -390,7 +395,7 @@ def mdgemm_accum_renorm(G: torch.Tensor, EA: torch.Tensor, EB: torch.Tensor, lim
 
 
 SCHEDULE_INFO_KEYS = ("terms", "jobs", "planes", "combos_a", "combos_b", "entries", "max_job_weight", "max_depth",
-                      "direct_levels")
+                      "direct_levels", "max_digits", "panels_f32")
 
 
 def mdgemm_schedule_info(m: int, n: int, k: int, slices: int, cutoff: int, *, bits: int = MDGEMM_SLICE_BITS,

@@ -177,3 +177,17 @@ def test_karatsuba_workspace_and_plan():
     assert 4096 * info["max_job_weight"] * ((1 << w) - 1) ** 2 < 2**53
     with pytest.raises(md.MdgemmError):
         md.mdgemm_schedule_info(64, 64, 4096, 8, 15, flags=KARA)  # cutoff beyond 2S - 2
+
+
+def test_fp32_panels_only_when_exact():
+    # the library keeps digit panels in FP32 exactly when every panel value, at
+    # most (digits in the largest combination) (2^w - 1), is below 2^24
+    for m, n, k, S, T, w, flags in [(4096, 4096, 4096, 8, 7, 13, 0), (4096, 4096, 4096, 8, 7, 13, KARA),
+                                    (512, 512, 512, 4, 3, 24, 0), (512, 512, 512, 4, 3, 25, 0),
+                                    (512, 512, 64, 8, 7, 20, KMIN), (512, 512, 16, 8, 7, 22, KMIN),
+                                    (128, 8192, 64, 64, 63, 13, KMIN)]:
+        info = md.mdgemm_schedule_info(m, n, k, S, T, bits=w, flags=flags)
+        sch = md.mdgemm_schedule_export(m, n, k, S, T, bits=w, flags=flags)
+        digits = max(popcount(x) for x in list(sch["mask_a"]) + list(sch["mask_b"]))
+        assert info["max_digits"] == digits
+        assert info["panels_f32"] == int(digits * (2**w - 1) < 2**24), (m, n, k, S, T, w, flags, digits)
