@@ -247,7 +247,7 @@ int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int slice_bit
  * MDGEMM_KARATSUBA_MIN_TERMS takes the plan with the fewest GEMMs whatever the
  * other costs (it overrides MDGEMM_KARATSUBA). */
 
-#define MDGEMM_SCHEDULE_INFO 11 /* entries written by mdgemm_schedule_info */
+#define MDGEMM_SCHEDULE_INFO 12 /* entries written by mdgemm_schedule_info */
 
 /* Size of the schedule mdgemm_ex uses for an m x k by k x n product with
  * S = slices digits of slice_bits bits, cutoff T, and flags (MDGEMM_KARATSUBA,
@@ -259,7 +259,10 @@ int mdgemm_slice_gemm(int64_t m, int64_t n, int64_t k, int slices, int slice_bit
  *   info[8] 1 when the planes are the levels themselves (pair schedule),
  *   info[9] digits in the largest combination (1 for the pair schedule),
  *   info[10] 1 when mdgemm_ex keeps the panels in FP32 (every panel value, at
- *     most info[9] (2^w - 1), below 2^24: exact; k rounded up to 32), else FP64.
+ *     most info[9] (2^w - 1), below 2^24: exact; k rounded up to 32), else FP64,
+ *   info[11] k chunks per job: products whose tile jobs would not fill the GPU
+ *     split k into up to 8 chunks, each writing its own plane (the planes of a
+ *     job's chunks enter the same levels; partial sums of integers, exact).
  * Host only (no HIP call).  Returns the count written or MDGEMM_EINVAL. */
 int mdgemm_schedule_info(int64_t m, int64_t n, int64_t k, int slices, int slice_bits, int cutoff, unsigned flags,
                          int64_t* info, int count);
@@ -269,7 +272,8 @@ int mdgemm_schedule_info(int64_t m, int64_t n, int64_t k, int slices, int slice_
  *   mask_a[CA], mask_b[CB]: the digit set of every combination (bit p = digit p);
  *   parents_a[2 CA], parents_b[2 CB]: combination c >= S is the sum of
  *     combinations parents[2c] and parents[2c+1] (-1, -1 for the digits c < S);
- *   jobs[3 J]: first pair, pair count, output plane of job j;
+ *   jobs[4 J]: first pair, pair count, output plane and k chunk (0 .. info[11]-1,
+ *     a 1/info[11] share of the k steps of every pair) of job j;
  *   pairs[2 terms]: (combination of A, combination of B) of every pair;
  *   plane_first[P + 1], entries[2 E]: plane j enters the levels
  *     entries[2e] with coefficient entries[2e+1] for plane_first[j] <= e < plane_first[j+1].

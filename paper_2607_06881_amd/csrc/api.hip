@@ -126,7 +126,7 @@ struct Planned {
 
 struct ScheduleCache {
   std::mutex mu;
-  std::map<std::tuple<int, int, int64_t, int, int, int, int>, std::shared_ptr<const Planned>> map;
+  std::map<std::tuple<int, int, int64_t, int, int, int, int, int>, std::shared_ptr<const Planned>> map;
 };
 ScheduleCache& schedule_cache() {
   static ScheduleCache c;
@@ -143,13 +143,15 @@ Kind kind_of(unsigned flags) {
 }
 
 // The schedule of the level products for S digits, cutoff T, an m x k by k x n
-// product and width w; built once per key and kept for the life of the process.
-std::shared_ptr<const Planned> schedule_for(int S, int T, int64_t m, int64_t n, int64_t k, int w, Kind kind) {
+// product and width w, its jobs split into `sigma` k chunks; built once per key
+// and kept for the life of the process.
+std::shared_ptr<const Planned> schedule_for(int S, int T, int64_t m, int64_t n, int64_t k, int w, Kind kind,
+                                            int sigma = 1) {
   const bool kara = kind == Kind::kKaratsuba || kind == Kind::kKaratsubaMin;
   const bool model = kind == Kind::kKaratsuba;
   const int64_t budget = kara ? job_budget(k, w) : 0;
   const int mc = model ? size_code(m) : 0, nc = model ? size_code(n) : 0, kc = model ? size_code(k) : 0;
-  const auto key = std::make_tuple(S, T, budget, mc, nc, kc, static_cast<int>(kind));
+  const auto key = std::make_tuple(S, T, budget, mc, nc, kc, static_cast<int>(kind), sigma);
   ScheduleCache& c = schedule_cache();
   {
     std::lock_guard<std::mutex> lock(c.mu);
@@ -157,7 +159,8 @@ std::shared_ptr<const Planned> schedule_for(int S, int T, int64_t m, int64_t n, 
     if (it != c.map.end()) return it->second;
   }
   auto pl = std::make_shared<Planned>();
-  if (kind == Kind::kLevels) pl->s = mdg::pair_schedule(S, T);
+  if (sigma > 1) pl->s = mdg::split_k(schedule_for(S, T, m, n, k, w, kind, 1)->s, sigma);
+  else if (kind == Kind::kLevels) pl->s = mdg::pair_schedule(S, T);
   else if (kind == Kind::kPerPair) pl->s = mdg::per_pair_schedule(S, T);
   else if (kind == Kind::kKaratsuba)
     pl->s = mdg::karatsuba_schedule(S, T, budget, schedule_costs(mc, nc, kc, T + 1), true);
@@ -271,6 +274,30 @@ int resolve(int limbs, int64_t m, int64_t n, int64_t k, const mdgemm_opts* opts,
 // max_digits digits) is an integer below 2^24, so that FP32 holds it exactly.
 bool panels_f32(const Planned& pl, int w) {
   return static_cast<uint64_t>(pl.max_digits) * ((1ull << w) - 1ull) < (1ull << 24);
+}
+
+// K split of a product whose tile jobs would not fill the chip: below 1.5
+// rounds of the 512 blocks resident at a time (two 256-thread blocks per CU),
+// split to about 2.5 rounds, at most 8 chunks, each at least 8 k steps of every
+// pair.  (Measured on 1024^3 double-double: 384 blocks split 4 ways run the
+// level GEMM at 87% of peak instead of 58%; 960 blocks gain nothing from a
+// split and the extra planes cost accumulation time.)
+int ksplit_for(int64_t m, int64_t n, int64_t k, const Planned& pl, bool f32) {
+  const int64_t tiles = (mdg::panel_mn(m) / mdg::kTileMN) * (mdg::panel_mn(n) / mdg::kTileMN);
+  const int64_t blocks = tiles * static_cast<int64_t>(pl.s.job_first.size());
+  const int64_t nkb = f32 ? mdg::panel_k32(k) / mdg::kTileK32 : mdg::panel_k(k) / mdg::kTileK;
+  constexpr int64_t kFull = 768, kTarget = 1280;
+  if (blocks <= 0 || blocks >= kFull) return 1;
+  int64_t sigma = (kTarget + blocks - 1) / blocks;
+  sigma = std::min<int64_t>(sigma, std::min<int64_t>(8, nkb / 8));
+  return static_cast<int>(std::max<int64_t>(sigma, 1));
+}
+
+// The schedule a product runs: the planned one, split in k when it is small.
+std::shared_ptr<const Planned> planned_for(int S, int T, int64_t m, int64_t n, int64_t k, int w, Kind kind) {
+  auto base = schedule_for(S, T, m, n, k, w, kind);
+  const int sigma = ksplit_for(m, n, k, *base, panels_f32(*base, w));
+  return sigma > 1 ? schedule_for(S, T, m, n, k, w, kind, sigma) : base;
 }
 
 struct Layout {
@@ -524,7 +551,7 @@ size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const 
   if (m < 0 || n < 0 || k < 0 || resolve(limbs, m, n, k, opts, &r) != MDGEMM_OK) return SIZE_MAX;
   if (m == 0 || n == 0 || k == 0) return 0;
   Layout L;
-  if (!layout(m, n, k, *schedule_for(r.S, r.T, m, n, k, r.w, r.kind), r.w, &L)) return SIZE_MAX;
+  if (!layout(m, n, k, *planned_for(r.S, r.T, m, n, k, r.w, r.kind), r.w, &L)) return SIZE_MAX;
   return L.total;
 }
 
@@ -549,7 +576,7 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
     return MDGEMM_OK;
   }
 
-  const auto pl = schedule_for(r.S, r.T, m, n, k, r.w, r.kind);
+  const auto pl = planned_for(r.S, r.T, m, n, k, r.w, r.kind);
   if (!schedule_exact(pl->s, k, r.w)) return MDGEMM_EEXACT;
   Layout L;
   if (!layout(m, n, k, *pl, r.w, &L)) return MDGEMM_EINVAL;
@@ -741,8 +768,7 @@ int mdgemm_schedule_info(int64_t m, int64_t n, int64_t k, int slices, int slice_
   if (m < 0 || n < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || slice_bits < 1 || slice_bits > mdg::kMaxSliceBits ||
       cutoff < 0 || cutoff > 2 * slices - 2 || k < 0 || count < 0 || (count > 0 && !info))
     return MDGEMM_EINVAL;
-  const auto pl = schedule_for(slices, cutoff, m, n, k, slice_bits,
-                               kind_of(flags));
+  const auto pl = planned_for(slices, cutoff, m, n, k, slice_bits, kind_of(flags));
   const mdg::Schedule& sc = pl->s;
   int max_depth = 0;
   for (int d : sc.depth_a) max_depth = std::max(max_depth, d);
@@ -757,7 +783,8 @@ int mdgemm_schedule_info(int64_t m, int64_t n, int64_t k, int slices, int slice_
                                            max_depth,
                                            sc.direct_levels ? 1 : 0,
                                            pl->max_digits,
-                                           panels_f32(*pl, slice_bits) ? 1 : 0};
+                                           panels_f32(*pl, slice_bits) ? 1 : 0,
+                                           sc.ksplit};
   const int nw = std::min(count, MDGEMM_SCHEDULE_INFO);
   for (int i = 0; i < nw; ++i) info[i] = v[i];
   return nw;
@@ -769,8 +796,7 @@ int mdgemm_schedule_export(int64_t m, int64_t n, int64_t k, int slices, int slic
   if (m < 0 || n < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || slice_bits < 1 || slice_bits > mdg::kMaxSliceBits ||
       cutoff < 0 || cutoff > 2 * slices - 2 || k < 0)
     return MDGEMM_EINVAL;
-  const auto pl = schedule_for(slices, cutoff, m, n, k, slice_bits,
-                               kind_of(flags));
+  const auto pl = planned_for(slices, cutoff, m, n, k, slice_bits, kind_of(flags));
   const mdg::Schedule& sc = pl->s;
   for (size_t c = 0; c < sc.mask_a.size(); ++c) {
     if (mask_a) mask_a[c] = sc.mask_a[c];
@@ -787,9 +813,10 @@ int mdgemm_schedule_export(int64_t m, int64_t n, int64_t k, int slices, int slic
     }
   }
   for (size_t j = 0; jobs && j < sc.job_first.size(); ++j) {
-    jobs[3 * j] = sc.job_first[j];
-    jobs[3 * j + 1] = sc.job_count[j];
-    jobs[3 * j + 2] = sc.job_out[j];
+    jobs[4 * j] = sc.job_first[j];
+    jobs[4 * j + 1] = sc.job_count[j];
+    jobs[4 * j + 2] = sc.job_out[j];
+    jobs[4 * j + 3] = sc.job_chunk.empty() ? 0 : sc.job_chunk[j];
   }
   for (size_t i = 0; pairs && i < sc.pair_a.size(); ++i) {
     pairs[2 * i] = sc.pair_a[i];
@@ -808,8 +835,7 @@ size_t mdgemm_schedule_workspace_bytes(int64_t m, int64_t n, int64_t k, int slic
   if (m < 0 || n < 0 || k < 0 || slices < 1 || slices > MDGEMM_MAX_SLICES || slice_bits < 1 ||
       slice_bits > mdg::kMaxSliceBits || cutoff < 0 || cutoff > 2 * slices - 2)
     return SIZE_MAX;
-  const auto pl = schedule_for(slices, cutoff, m, n, k, slice_bits,
-                               kind_of(flags));
+  const auto pl = planned_for(slices, cutoff, m, n, k, slice_bits, kind_of(flags));
   Layout L;
   if (!layout(m, n, k, *pl, slice_bits, &L)) return SIZE_MAX;
   return L.total;
@@ -827,8 +853,7 @@ int mdgemm_schedule_levels(int64_t m, int64_t n, int64_t k, int slices, int slic
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t levels = cutoff + 1;
   if (k == 0) return hip_status(mdg::launch_zero_f64(G, levels * m * n, s));
-  const auto pl = schedule_for(slices, cutoff, m, n, k, slice_bits,
-                               kind_of(flags));
+  const auto pl = planned_for(slices, cutoff, m, n, k, slice_bits, kind_of(flags));
   if (!schedule_exact(pl->s, k, slice_bits)) return MDGEMM_EEXACT;
   Layout L;
   if (!layout(m, n, k, *pl, slice_bits, &L)) return MDGEMM_EINVAL;

@@ -32,10 +32,10 @@ inline int64_t panel_k32(int64_t k) { return (k + kTileK32 - 1) / kTileK32 * kTi
 inline int64_t panel_mn(int64_t x) { return (x + kTileMN - 1) / kTileMN * kTileMN; }
 
 // Slice-pair jobs of the level GEMM, read from a device table in the format of
-// ScheduleTable (schedule.h): `jobs` holds two words per job (first pair |
-// pair count << 16, output plane), `pairs` one word per pair (combination of A
-// | combination of B << 16).  Job j sums the products of its pairs into plane
-// out[j].
+// ScheduleTable (schedule.h): `jobs` holds three words per job (first pair |
+// pair count << 16, output plane, k chunk | k chunks << 16), `pairs` one word
+// per pair (combination of A | combination of B << 16).  Job j sums the
+// products of its pairs over its k chunk into plane out[j].
 struct GemmJobs {
   const uint32_t* jobs = nullptr;
   const uint32_t* pairs = nullptr;

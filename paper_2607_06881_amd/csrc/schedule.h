@@ -38,6 +38,11 @@ struct Schedule {
   // pairs pairs[job_first[j] .. job_first[j] + job_count[j]) into plane job_out[j].
   std::vector<int> job_first, job_count, job_out;
   std::vector<int> pair_a, pair_b;
+  // K split: job j runs k chunk job_chunk[j] of ksplit (empty: the whole k).
+  // The chunks of a job write separate planes with the same level entries, and
+  // the accumulation adds them (partial sums of integers: exact).
+  int ksplit = 1;
+  std::vector<int> job_chunk;
   // Levels from planes (Karatsuba schedule): level t = sum over the entries
   // (plane, t, coef) of coef * plane; entries sorted by plane, plane_first[j]
   // indexes the first entry of plane j (size planes + 1).
@@ -73,8 +78,13 @@ Schedule karatsuba_schedule(int S, int T, int64_t budget, const ScheduleCosts& c
 // The cost of a schedule in GEMM terms, as karatsuba_schedule counts it.
 double schedule_cost(const Schedule& s, const ScheduleCosts& costs);
 
+// The schedule with every job split into `sigma` k chunks (sigma > 1 turns a
+// pair schedule into one whose planes enter the levels through entries).
+Schedule split_k(const Schedule& s, int sigma);
+
 // Device table of a schedule: 32-bit words
-//   [2 J job words: first | count << 16, out plane] [P pair words: a | b << 16]
+//   [3 J job words: first | count << 16, out plane, chunk | ksplit << 16]
+//   [P pair words: a | b << 16]
 //   [planes + 1 chunk_first words] [2 words per chunk]
 //   [2 words per combination of A: digit set, low word first] [same for B]
 // The entries of plane j are chunks chunk_first[j] .. chunk_first[j+1]-1 of

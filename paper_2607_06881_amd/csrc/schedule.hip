@@ -387,6 +387,44 @@ Schedule karatsuba_schedule(int S, int T, int64_t budget, const ScheduleCosts& c
   return s;
 }
 
+Schedule split_k(const Schedule& s, int sigma) {
+  if (sigma <= 1) return s;
+  Schedule r = s;
+  r.direct_levels = false;
+  r.ksplit = sigma;
+  r.job_first.clear();
+  r.job_count.clear();
+  r.job_out.clear();
+  r.job_chunk.clear();
+  r.plane_first.clear();
+  r.entry_level.clear();
+  r.entry_coef.clear();
+  int plane = 0;
+  for (size_t j = 0; j < s.job_first.size(); ++j) {
+    std::vector<std::pair<int, int>> ent;  // the level entries of job j's plane
+    if (s.direct_levels) {
+      ent.push_back({s.job_out[j], 1});
+    } else {
+      const int pl = s.job_out[j];
+      for (int e = s.plane_first[pl]; e < s.plane_first[pl + 1]; ++e) ent.push_back({s.entry_level[e], s.entry_coef[e]});
+    }
+    for (int c = 0; c < sigma; ++c) {
+      r.job_first.push_back(s.job_first[j]);
+      r.job_count.push_back(s.job_count[j]);
+      r.job_out.push_back(plane++);
+      r.job_chunk.push_back(c);
+      r.plane_first.push_back(static_cast<int>(r.entry_level.size()));
+      for (const auto& lc : ent) {
+        r.entry_level.push_back(lc.first);
+        r.entry_coef.push_back(lc.second);
+      }
+    }
+  }
+  r.plane_first.push_back(static_cast<int>(r.entry_level.size()));
+  r.planes = plane;
+  return r;
+}
+
 ScheduleTable schedule_table(const Schedule& s) {
   ScheduleTable t;
   const size_t J = s.job_first.size();
@@ -394,6 +432,8 @@ ScheduleTable schedule_table(const Schedule& s) {
   for (size_t j = 0; j < J; ++j) {
     t.words.push_back(static_cast<uint32_t>(s.job_first[j]) | (static_cast<uint32_t>(s.job_count[j]) << 16));
     t.words.push_back(static_cast<uint32_t>(s.job_out[j]));
+    const uint32_t chunk = s.job_chunk.empty() ? 0u : static_cast<uint32_t>(s.job_chunk[j]);
+    t.words.push_back(chunk | (static_cast<uint32_t>(s.ksplit) << 16));
   }
   t.pairs_off = static_cast<int64_t>(t.words.size());
   for (size_t i = 0; i < s.pair_a.size(); ++i)

@@ -38,7 +38,9 @@
 //
 // Work decomposition: grid.x = output tiles, grid.y = jobs (levels, heaviest
 // first, single pairs, or the products of combinations of a Karatsuba
-// schedule; each job lists its pairs in a device table, see schedule.h).  Tiles are renumbered so that each of the 8 XCDs
+// schedule; each job lists its pairs in a device table, see schedule.h).  A
+// job may cover one k chunk of its pairs (small products split k so that
+// enough blocks fill the chip; the chunks' planes are added exactly later).  Tiles are renumbered so that each of the 8 XCDs
 // (blocks are dealt to XCDs round-robin) works on its own chunk of tiles, and
 // the blocks resident on one XCD at a time cover an about 8 x 8 patch whose
 // panel rows stay in that XCD's L2.
@@ -88,15 +90,18 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
   // the job's pairs (uniform: scalar loads); the pair after the one being
   // copied is fetched one pair ahead
   const int job = blockIdx.y;
-  const uint32_t jw = jobs[2 * job];
+  const uint32_t jw = jobs[3 * job], kw = jobs[3 * job + 2];
   const int pfirst = static_cast<int>(jw & 0xffffu), npairs = static_cast<int>(jw >> 16);
-  const int64_t out_plane = jobs[2 * job + 1];
+  const int64_t out_plane = jobs[3 * job + 1];
+  // k chunk kw & 0xffff of kw >> 16: k steps [kb0, kb0 + nkb) of every pair (maybe none)
+  const int64_t ksplit = kw >> 16, chunk = kw & 0xffffu;
   const int64_t plane_a = kp * mp, plane_b = kp * np;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave >> 1, wc = wave & 1;  // 2 x 2 waves, 64 x 64 each
 
-  const int64_t nkb = kp / BK;
+  const int64_t nkb_all = kp / BK, csz = (nkb_all + ksplit - 1) / ksplit;
+  const int64_t kb0 = min(chunk * csz, nkb_all), nkb = min(csz, nkb_all - kb0);
   const int64_t niter = nkb * npairs;
 
   // Direct global -> LDS copies (global_load_lds_dwordx4, 1 KB panel row per wave
@@ -108,7 +113,7 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
   uint32_t pr = pairs[pfirst];                             // pair lpi
   uint32_t pr_next = npairs > 1 ? pairs[pfirst + 1] : 0u;  // pair lpi + 1
   // this wave's first copy row of the pair's panels; advanced by one k step per copy
-  const int64_t row_a = 4 * wave_u * mp + m0, row_b = 4 * wave_u * np + n0;
+  const int64_t row_a = (kb0 * BK + 4 * wave_u) * mp + m0, row_b = (kb0 * BK + 4 * wave_u) * np + n0;
   const double* a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
   const double* b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
   auto issue = [&](int stage) {
@@ -221,15 +226,18 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
   const int64_t m0 = static_cast<int64_t>(first + within % rows_in) * BM;
   const int64_t n0 = static_cast<int64_t>(within / rows_in) * BN;
   const int job = blockIdx.y;
-  const uint32_t jw = jobs[2 * job];
+  const uint32_t jw = jobs[3 * job], kw = jobs[3 * job + 2];
   const int pfirst = static_cast<int>(jw & 0xffffu), npairs = static_cast<int>(jw >> 16);
-  const int64_t out_plane = jobs[2 * job + 1];
+  const int64_t out_plane = jobs[3 * job + 1];
+  // k chunk kw & 0xffff of kw >> 16: k steps [kb0, kb0 + nkb) of every pair (maybe none)
+  const int64_t ksplit = kw >> 16, chunk = kw & 0xffffu;
   const int64_t plane_a = kp * mp, plane_b = kp * np;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave >> 1, wc = wave & 1;
 
-  const int64_t nkb = kp / BK32;
+  const int64_t nkb_all = kp / BK32, csz = (nkb_all + ksplit - 1) / ksplit;
+  const int64_t kb0 = min(chunk * csz, nkb_all), nkb = min(csz, nkb_all - kb0);
   const int64_t niter = nkb * npairs;
 
   // Copies: wave w fills rows 8w .. 8w+7 of each tile, two rows per instruction
@@ -249,7 +257,7 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
   int64_t lkb = 0;
   uint32_t pr = pairs[pfirst];
   uint32_t pr_next = npairs > 1 ? pairs[pfirst + 1] : 0u;
-  const int64_t row_a = 8 * wave_u * mp + m0, row_b = 8 * wave_u * np + n0;
+  const int64_t row_a = (kb0 * BK32 + 8 * wave_u) * mp + m0, row_b = (kb0 * BK32 + 8 * wave_u) * np + n0;
   const float* a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
   const float* b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
   auto issue = [&](int stage) {

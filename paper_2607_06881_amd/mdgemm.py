@@ -31,7 +31,7 @@ MDGEMM_SYNC = 2
 MDGEMM_TIME_STAGES = 4
 MDGEMM_KARATSUBA = 8
 MDGEMM_KARATSUBA_MIN_TERMS = 16
-MDGEMM_SCHEDULE_INFO = 11
+MDGEMM_SCHEDULE_INFO = 12
 
 MDGEMM_CUTOFF_DEFAULT = -1
 MDGEMM_CUTOFF_ALL = -2
@@ -395,7 +395,7 @@ def mdgemm_accum_renorm(G: torch.Tensor, EA: torch.Tensor, EB: torch.Tensor, lim
 
 
 SCHEDULE_INFO_KEYS = ("terms", "jobs", "planes", "combos_a", "combos_b", "entries", "max_job_weight", "max_depth",
-                      "direct_levels", "max_digits", "panels_f32")
+                      "direct_levels", "max_digits", "panels_f32", "ksplit")
 
 
 def mdgemm_schedule_info(m: int, n: int, k: int, slices: int, cutoff: int, *, bits: int = MDGEMM_SLICE_BITS,
@@ -411,7 +411,7 @@ def mdgemm_schedule_info(m: int, n: int, k: int, slices: int, cutoff: int, *, bi
 def mdgemm_schedule_export(m: int, n: int, k: int, slices: int, cutoff: int, *, bits: int = MDGEMM_SLICE_BITS,
                            flags: int = 0) -> dict:
     """The schedule's tables as numpy arrays (host only): mask_a/mask_b (uint64 digit
-    sets), parents_a/parents_b [C, 2], jobs [J, 3] (first pair, count, plane),
+    sets), parents_a/parents_b [C, 2], jobs [J, 4] (first pair, count, plane, k chunk),
     pairs [terms, 2], plane_first [P + 1], entries [E, 2] (level, coefficient)."""
     import numpy as np
 
@@ -421,7 +421,7 @@ def mdgemm_schedule_export(m: int, n: int, k: int, slices: int, cutoff: int, *, 
         "parents_a": np.zeros((info["combos_a"], 2), dtype=np.int32),
         "mask_b": np.zeros(info["combos_b"], dtype=np.uint64),
         "parents_b": np.zeros((info["combos_b"], 2), dtype=np.int32),
-        "jobs": np.zeros((info["jobs"], 3), dtype=np.int32),
+        "jobs": np.zeros((info["jobs"], 4), dtype=np.int32),
         "pairs": np.zeros((info["terms"], 2), dtype=np.int32),
         "plane_first": np.zeros(info["planes"] + 1, dtype=np.int32),
         "entries": np.zeros((info["entries"], 2), dtype=np.int32),

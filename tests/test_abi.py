@@ -130,10 +130,11 @@ def test_workspace_bytes_layout(lib):
         a = lambda x: (x + 255) // 256 * 256
         # 13-bit digits: FP32 panels with k rounded up to 32
         kp, mp, np_ = md.panel_k32(k), md.panel_mn(m), md.panel_mn(n)
-        # pair schedule table: 2 words per level job, one per pair, T + 2 chunk starts,
-        # an even word, one chunk (2 words) per level, 2 words per digit of A and of B
+        # pair schedule table (these shapes keep whole k): 3 words per level job, one per
+        # pair, T + 2 chunk starts, an even word, one chunk (2 words) per level, 2 words
+        # per digit of A and of B
         pairs = sum(len(exact.pairs_of_level(t, S)) for t in range(T + 1))
-        words = 2 * (T + 1) + pairs + (T + 2)
+        words = 3 * (T + 1) + pairs + (T + 2)
         words += words % 2 + 2 * (T + 1) + 4 * S
         return (a(4 * m) + a(4 * n) + a(4) + a(4 * words) + a(4 * S * kp * mp) + a(4 * S * kp * np_) +
                 a(8 * (T + 1) * m * n))

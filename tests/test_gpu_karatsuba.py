@@ -190,3 +190,35 @@ def test_mdgemm_karatsuba_cost_model_shapes(L, m, k, n, cutoff):
     ref = pipeline.reference_entries(A_h, B_h, S, T, entries)
     for (i, j), r in ref.items():
         assert C[:, i, j].tolist() == r["limbs"], (i, j)
+
+
+@pytest.mark.parametrize("L,m,k,n,flags,opts", [(2, 130, 2000, 129, 0, {}), (2, 130, 2000, 129, KMIN, {}),
+                                                (3, 70, 1500, 250, 0, {"cutoff": -2}),
+                                                (2, 200, 1200, 140, KARA, {"slice_bits": -1}),
+                                                (4, 40, 900, 60, KMIN, {})])
+def test_mdgemm_k_split(L, m, k, n, flags, opts):
+    # few tiles and long k: each job is split into k chunks whose planes the
+    # accumulation adds (partial sums of integers: exact); bit-exact vs the oracle
+    w, S, T = md.mdgemm_plan(m, n, k, L, flags=flags, **opts)
+    info = md.mdgemm_schedule_info(m, n, k, S, T, bits=w, flags=flags)
+    print(f"[case] k split L={L} {m}x{k}x{n} flags={flags} {opts}: w={w} S={S} T={T} "
+          f"ksplit={info['ksplit']} jobs={info['jobs']}", flush=True)
+    assert info["ksplit"] > 1
+    rng = np.random.default_rng(m * k + n)
+    A = workloads.make_operand(rng, L, m, k, "normal", row_exp=6)
+    B = workloads.make_operand(rng, L, k, n, "normal", col_exp=6)
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), flags=flags, **opts))
+    assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])
+
+
+@pytest.mark.parametrize("S,T,m,k,n,flags", [(8, 7, 100, 3000, 140, 0), (8, 7, 100, 3000, 140, KMIN),
+                                             (12, 11, 60, 1100, 70, KMIN)])
+def test_schedule_levels_k_split(S, T, m, k, n, flags):
+    info = md.mdgemm_schedule_info(m, n, k, S, T, flags=flags)
+    print(f"[case] levels k split S={S} T={T} {m}x{k}x{n} flags={flags}: ksplit={info['ksplit']}", flush=True)
+    assert info["ksplit"] > 1
+    rng = np.random.default_rng(S + k)
+    DA = rng.integers(-8191, 8192, (S, m, k)).astype(np.float64)
+    DB = rng.integers(-8191, 8192, (S, k, n)).astype(np.float64)
+    got = _host(md.mdgemm_schedule_levels(_gpu(_panel(DA, 0)), _gpu(_panel(DB, 1)), m, n, k, T, flags=flags))
+    assert np.array_equal(got, coracle.levels(DA, DB, T).astype(np.float64))

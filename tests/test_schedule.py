@@ -40,12 +40,16 @@ def digits_of(mask: int, S: int):
 
 
 def coefficients(sch: dict, S: int, T: int) -> np.ndarray:
-    """coef[t, p, q]: the schedule's coefficient of DA_p DB_q in level t."""
+    """coef[t, p, q]: the schedule's coefficient of DA_p DB_q in level t.  With a
+    k split every job appears once per k chunk, each covering a share of k:
+    the chunks of one job together count once."""
     coef = np.zeros((T + 1, S, S), dtype=np.int64)
     vec_a = np.array([[(int(m) >> p) & 1 for p in range(S)] for m in sch["mask_a"]], dtype=np.int64)
     vec_b = np.array([[(int(m) >> q) & 1 for q in range(S)] for m in sch["mask_b"]], dtype=np.int64)
     pf, ent = sch["plane_first"], sch["entries"]
-    for first, count, plane in sch["jobs"]:
+    for first, count, plane, chunk in sch["jobs"]:
+        if chunk != 0:
+            continue  # chunk 0 stands for the job; check_chunks sees that all chunks are there
         outer = np.zeros((S, S), dtype=np.int64)
         for a, b in sch["pairs"][first:first + count]:
             outer += np.outer(vec_a[a], vec_b[b])
@@ -53,6 +57,19 @@ def coefficients(sch: dict, S: int, T: int) -> np.ndarray:
             level, c = ent[e]
             coef[level] += c * outer
     return coef
+
+
+def check_chunks(sch: dict):
+    """Every job appears with k chunks 0 .. ksplit-1, each chunk with the same
+    pairs and level entries."""
+    sigma = sch["info"]["ksplit"]
+    groups = {}
+    pf, ent = sch["plane_first"], sch["entries"]
+    for first, count, plane, chunk in sch["jobs"]:
+        key = (int(first), int(count), tuple(map(tuple, ent[pf[plane]:pf[plane + 1]].tolist())))
+        groups.setdefault(key, []).append(int(chunk))
+    for key, chunks in groups.items():
+        assert sorted(chunks) == list(range(sigma)) * (len(chunks) // sigma), (key, chunks)
 
 
 def expected(S: int, T: int) -> np.ndarray:
@@ -80,14 +97,16 @@ def test_schedule_computes_the_levels(m, n, k, S, T, w, flags):
     sch = md.mdgemm_schedule_export(m, n, k, S, T, bits=w, flags=flags)
     info = sch["info"]
     np.testing.assert_array_equal(coefficients(sch, S, T), expected(S, T))
+    check_chunks(sch)
     check_combinations(sch["mask_a"], sch["parents_a"], S)
     check_combinations(sch["mask_b"], sch["parents_b"], S)
-    # every pair belongs to exactly one job; planes are distinct
-    assert sum(int(c) for _, c, _ in sch["jobs"]) == info["terms"] == len(sch["pairs"])
-    assert len({int(p) for _, _, p in sch["jobs"]}) == len(sch["jobs"])
+    # every pair belongs to exactly one job (per k chunk); planes are distinct
+    assert sum(int(c) for _, c, _, ch in sch["jobs"] if ch == 0) == info["terms"]
+    assert info["terms"] * info["ksplit"] == sum(int(c) for _, c, _, _ in sch["jobs"]) or info["ksplit"] == 1
+    assert len({int(p) for _, _, p, _ in sch["jobs"]}) == len(sch["jobs"])
     # exactness of every job: k * sum |comb a| |comb b| * (2^w - 1)^2 < 2^53
     dmax = (1 << w) - 1
-    for first, count, _ in sch["jobs"]:
+    for first, count, _, _ in sch["jobs"]:
         weight = sum(popcount(sch["mask_a"][a]) * popcount(sch["mask_b"][b]) for a, b in sch["pairs"][first:first + count])
         # (a pair schedule's jobs are its levels, covered by the library's level check)
         if not info["direct_levels"]:
@@ -103,7 +122,8 @@ def test_karatsuba_schedule_uses_fewer_products(m, n, k, S, T):
     kara = md.mdgemm_schedule_info(m, n, k, S, T, flags=KARA)
     kmin = md.mdgemm_schedule_info(m, n, k, S, T, flags=KMIN)
     assert pairs["terms"] == sum(len(exact.pairs_of_level(t, S)) for t in range(T + 1))
-    assert pairs["direct_levels"] == 1 and kmin["direct_levels"] == 0
+    # (a k split turns the pair schedule's level planes into planes with entries)
+    assert pairs["direct_levels"] == int(pairs["ksplit"] == 1) and kmin["direct_levels"] == 0
     # the fewest products: well under the pair count; the cost model's choice
     # trades some products for fewer planes, entries and combinations, and keeps
     # the pair schedule for octo and hexa doubles at their short k (128, 64),
@@ -132,8 +152,9 @@ def test_schedule_on_random_digits():
     comb_a = [sum(da[p] for p in digits_of(m, S)) for m in sch["mask_a"]]
     comb_b = [sum(db[q] for q in digits_of(m, S)) for m in sch["mask_b"]]
     planes = {}
-    for first, count, plane in sch["jobs"]:
-        planes[int(plane)] = sum(comb_a[a] * comb_b[b] for a, b in sch["pairs"][first:first + count])
+    for first, count, plane, chunk in sch["jobs"]:
+        if chunk == 0:
+            planes[int(plane)] = sum(comb_a[a] * comb_b[b] for a, b in sch["pairs"][first:first + count])
     levels = [0] * (T + 1)
     pf, ent = sch["plane_first"], sch["entries"]
     for plane, v in planes.items():
@@ -155,7 +176,7 @@ def test_planted_schedule_mistakes_are_caught():
     assert not np.array_equal(coefficients(bad, S, T), want)
     # a dropped pair (job count one short)
     bad = {key: (v.copy() if isinstance(v, np.ndarray) else v) for key, v in base.items()}
-    j = int(np.argmax(bad["jobs"][:, 1]))
+    j = int(np.argmax(bad["jobs"][:, 1] * (bad["jobs"][:, 3] == 0)))
     bad["jobs"][j, 1] -= 1
     assert not np.array_equal(coefficients(bad, S, T), want)
     # a combination whose digit set is off by one digit
@@ -191,3 +212,23 @@ def test_fp32_panels_only_when_exact():
         digits = max(popcount(x) for x in list(sch["mask_a"]) + list(sch["mask_b"]))
         assert info["max_digits"] == digits
         assert info["panels_f32"] == int(digits * (2**w - 1) < 2**24), (m, n, k, S, T, w, flags, digits)
+
+
+def test_small_products_split_k():
+    # 1024^3 double-double at 19-bit digits: 6 level jobs x 64 tiles would fill
+    # only 384 of the 512 resident blocks; k is split so that the chip fills
+    info = md.mdgemm_schedule_info(1024, 1024, 1024, 6, 5, bits=19)
+    assert info["ksplit"] > 1 and info["direct_levels"] == 0
+    assert info["jobs"] == 6 * info["ksplit"] and info["planes"] == info["jobs"]
+    # big products keep whole k
+    assert md.mdgemm_schedule_info(4096, 4096, 4096, 8, 7)["ksplit"] == 1
+    # short k cannot be split below 8 k steps a chunk
+    assert md.mdgemm_schedule_info(128, 128, 100, 8, 7)["ksplit"] == 1
+    # the split schedule still computes the levels
+    sch = md.mdgemm_schedule_export(1024, 1024, 1024, 6, 5, bits=19)
+    np.testing.assert_array_equal(coefficients(sch, 6, 5), expected(6, 5))
+    check_chunks(sch)
+    sch = md.mdgemm_schedule_export(1024, 1024, 1024, 6, 5, bits=18, flags=KARA)
+    assert sch["info"]["ksplit"] > 1
+    np.testing.assert_array_equal(coefficients(sch, 6, 5), expected(6, 5))
+    check_chunks(sch)
