@@ -130,7 +130,8 @@ int mdgemm_plan(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* o
 
 /* C = A.B for L-limb operands (L = limbs in 1..16) with the default options (13-bit
  * digits, four per limb).
- * m, n, k >= 0; m == 0 or n == 0 does nothing; k == 0 writes C = +0.0.
+ * m, n, k >= 0; m == 0 or n == 0 does nothing; k == 0 writes C = +0.0; m and n at
+ * most 2^27 (MDGEMM_EINVAL beyond).
  * Returns MDGEMM_OK or a negative status. */
 int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C);
 

@@ -314,6 +314,11 @@ bool layout(int64_t m, int64_t n, int64_t k, const Planned& pl, int w, Layout* L
   const double approx = ca * (double)m * (double)(k + 32) + cb * (double)(k + 32) * (double)n +
                         (double)sch.planes * (double)m * (double)n;
   if (approx * 8.0 > 4.0e18) return false;
+  // the level GEMM addresses panel rows with 32-bit lane offsets (m, n up to 2^27)
+  // and numbers its tiles in 31 bits
+  const int64_t mp = mdg::panel_mn(m), np = mdg::panel_mn(n);
+  if (mp > (int64_t{1} << 27) || np > (int64_t{1} << 27) || (mp / mdg::kTileMN) * (np / mdg::kTileMN) > INT_MAX)
+    return false;
   L->f32 = panels_f32(pl, w);
   const size_t esz = L->f32 ? sizeof(float) : sizeof(double);
   size_t off = 0;
@@ -326,11 +331,10 @@ bool layout(int64_t m, int64_t n, int64_t k, const Planned& pl, int w, Layout* L
   L->table = off;
   off += align_up(sizeof(uint32_t) * pl.t.words.size());
   L->da = off;
-  const size_t kp = static_cast<size_t>(L->f32 ? mdg::panel_k32(k) : mdg::panel_k(k)),
-               mp = static_cast<size_t>(mdg::panel_mn(m)), np = static_cast<size_t>(mdg::panel_mn(n));
-  off += align_up(esz * sch.mask_a.size() * kp * mp);
+  const size_t kp = static_cast<size_t>(L->f32 ? mdg::panel_k32(k) : mdg::panel_k(k));
+  off += align_up(esz * sch.mask_a.size() * kp * static_cast<size_t>(mp));
   L->db = off;
-  off += align_up(esz * sch.mask_b.size() * kp * np);
+  off += align_up(esz * sch.mask_b.size() * kp * static_cast<size_t>(np));
   L->g = off;
   off += align_up(sizeof(double) * static_cast<size_t>(sch.planes) * static_cast<size_t>(m) * static_cast<size_t>(n));
   L->total = off;

@@ -98,6 +98,10 @@ def test_invalid_arguments(lib):
     assert _ex(lib, 4, 4, 4, 2, slice_bits=md.MDGEMM_SLICE_BITS_AUTO, slices=6) == E
     assert _ex(lib, 4, 4, 4, 16, slice_bits=23) == E  # S = ceil(832 / 23) = 37, 37 x 23 > 844
     assert lib.mdgemm_exponents(4, 4, 3, FA, FB, None) == E
+    # m, n at most 2^27 (the level GEMM's 32-bit panel row offsets)
+    assert _ex(lib, 2**27 + 1, 4, 4, 2, C=FC + (1 << 44)) == E
+    assert _ex(lib, 4, 2**27 + 1, 4, 2, C=FC + (1 << 44)) == E
+    assert md.mdgemm_workspace_bytes(2**27 + 1, 16, 16, 2) == 2**64 - 1
 
 
 def test_empty_products_are_noops(lib):
