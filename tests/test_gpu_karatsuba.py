@@ -222,3 +222,67 @@ def test_schedule_levels_k_split(S, T, m, k, n, flags):
     DB = rng.integers(-8191, 8192, (S, k, n)).astype(np.float64)
     got = _host(md.mdgemm_schedule_levels(_gpu(_panel(DA, 0)), _gpu(_panel(DB, 1)), m, n, k, T, flags=flags))
     assert np.array_equal(got, coracle.levels(DA, DB, T).astype(np.float64))
+
+
+def _sweep_cases(count, seed):
+    """Seeded random products over shapes, limb counts, cutoffs, digit widths,
+    range balancing and schedules (some with few tiles and long k, which split k)."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for c in range(count):
+        L = int(rng.choice([1, 2, 2, 3, 4, 8]))
+        if c % 3 == 0:  # few tiles, long k
+            m, n, k = int(rng.integers(1, 140)), int(rng.integers(1, 140)), int(rng.integers(600, 2500))
+        else:
+            m, n, k = (int(x) for x in rng.integers(1, 300, 3))
+        opts = {}
+        if rng.random() < 0.3:
+            opts["cutoff"] = int(rng.choice([-2, 4 * L - 2, 4 * L + 1]))
+        if rng.random() < 0.3 and L <= 4:
+            opts["slice_bits"] = -1
+        if rng.random() < 0.15 and L <= 4:
+            opts["range_bits"] = int(rng.integers(5, 60))
+        flags = int(rng.choice([0, KARA, KMIN]))
+        cases.append((c, L, m, n, k, flags, opts))
+    return cases
+
+
+@pytest.mark.parametrize("case", _sweep_cases(16, 2026), ids=lambda c: f"sweep{c[0]}")
+def test_random_sweep(case):
+    c, L, m, n, k, flags, opts = case
+    try:
+        w, S, T = md.mdgemm_plan(m, n, k, L, flags=flags, **opts)
+    except md.MdgemmError as e:  # a cutoff or width this k does not allow
+        assert e.status in (md.MDGEMM_EINVAL, md.MDGEMM_EEXACT)
+        pytest.skip(f"options not valid for this product: {e}")
+    info = md.mdgemm_schedule_info(m, n, k, S, T, bits=w, flags=flags)
+    print(f"[case] sweep {c}: L={L} {m}x{k}x{n} flags={flags} {opts}: w={w} S={S} T={T} "
+          f"products={info['terms']} ksplit={info['ksplit']} f32={info['panels_f32']}", flush=True)
+    rng = np.random.default_rng(1000 + c)
+    A = workloads.make_operand(rng, L, m, k, "normal", row_exp=8)
+    B = workloads.make_operand(rng, L, k, n, "normal", col_exp=8)
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), flags=flags, **opts))
+    if m * n <= 20000:
+        assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])
+    else:
+        pick = np.random.default_rng(c)
+        entries = sorted({(int(pick.integers(m)), int(pick.integers(n))) for _ in range(30)} | {(0, 0), (m - 1, n - 1)})
+        ref = pipeline.reference_entries(A, B, S, T, entries, w)
+        for (i, j), r in ref.items():
+            assert C[:, i, j].tolist() == r["limbs"], (i, j)
+
+
+@pytest.mark.parametrize("L,m,k,n,bits,slices,flags", [(1, 70, 4, 130, 24, 3, KMIN), (2, 129, 1, 65, 25, 5, 0),
+                                                        (1, 40, 1, 300, 26, 2, 0), (2, 33, 5, 140, 24, 5, KMIN)])
+def test_mdgemm_fp64_panels(L, m, k, n, bits, slices, flags):
+    # panel values at or above 2^24 (digits wider than 24 bits, or sums of two
+    # 24-bit digits) keep FP64 panels and the 16-deep FP64 level GEMM
+    w, S, T = md.mdgemm_plan(m, n, k, L, slice_bits=bits, slices=slices, flags=flags)
+    info = md.mdgemm_schedule_info(m, n, k, S, T, bits=w, flags=flags)
+    print(f"[case] fp64 panels L={L} {m}x{k}x{n} w={w} S={S} T={T} flags={flags}: {info}", flush=True)
+    assert info["panels_f32"] == 0
+    rng = np.random.default_rng(bits * 100 + k)
+    A = workloads.make_operand(rng, L, m, k, "normal", row_exp=4)
+    B = workloads.make_operand(rng, L, k, n, "normal", col_exp=4)
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), slice_bits=bits, slices=slices, flags=flags))
+    assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])
