@@ -255,8 +255,11 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
   }
   int lpi = 0;
   int64_t lkb = 0;
+  // The pair word is read (scalar load) where the copies switch to the next pair
+  // and used at once, so that no scalar load is pending while the fragment reads
+  // are: the LDS counter then orders the reads alone and each group of MFMAs
+  // waits for its own reads only.
   uint32_t pr = pairs[pfirst];
-  uint32_t pr_next = npairs > 1 ? pairs[pfirst + 1] : 0u;
   const int64_t row_a = (kb0 * BK32 + 8 * wave_u) * mp + m0, row_b = (kb0 * BK32 + 8 * wave_u) * np + n0;
   const float* a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
   const float* b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
@@ -271,8 +274,7 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
     if (++lkb == nkb) {
       lkb = 0;
       ++lpi;
-      pr = pr_next;
-      if (lpi + 1 < npairs) pr_next = pairs[pfirst + lpi + 1];
+      if (lpi < npairs) pr = pairs[pfirst + lpi];
       a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
       b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
     } else {
@@ -304,16 +306,17 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
     const float* as = As[cur];
     const float* bs = Bs[cur];
     float af[BK32 / 4][4], bf[BK32 / 4][4];
+    // fragments of k groups 2g and 2g + 1 (8 LDS instructions)
+    auto read = [&](int g) {
 #pragma unroll
-    for (int kg = 0; kg < BK32 / 4; ++kg)
+      for (int kg = 2 * g; kg < 2 * g + 2; ++kg)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        af[kg][i] = as[kg * 4 * ROW32 + fa[i]];
-        bf[kg][i] = bs[kg * 4 * ROW32 + fb[i]];
-      }
-    if (it + 1 < niter) issue(cur ^ 1);
-#pragma unroll
-    for (int kg = 0; kg < BK32 / 4; ++kg) {
+        for (int i = 0; i < 4; ++i) {
+          af[kg][i] = as[kg * 4 * ROW32 + fa[i]];
+          bf[kg][i] = bs[kg * 4 * ROW32 + fb[i]];
+        }
+    };
+    auto mfma = [&](int kg) {
       double ad[4], bd[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -325,7 +328,32 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ad[i], bd[j], acc[i][j], 0, 0, 0);
-    }
+    };
+    // The reads go out in four groups, each one MFMA group ahead of its use, so
+    // that at most 16 are outstanding and every wait is a partial one; the copies
+    // of the next step follow the last read (no LDS read of this step comes after
+    // a copy in flight) and land while the last 32 MFMAs run.  sched_barrier
+    // keeps the compiler from merging the groups back together.
+    read(0);
+    read(1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(0);
+    mfma(1);
+    __builtin_amdgcn_sched_barrier(0);
+    read(2);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(2);
+    mfma(3);
+    __builtin_amdgcn_sched_barrier(0);
+    read(3);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(4);
+    mfma(5);
+    __builtin_amdgcn_sched_barrier(0);
+    if (it + 1 < niter) issue(cur ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(6);
+    mfma(7);
   }
 
   double* o = out + out_plane * m * n;
