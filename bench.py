@@ -116,7 +116,7 @@ def main(argv=None) -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default=DEFAULT_CONFIG, help="workload c0..c6 (default c2)")
+    ap.add_argument("--config", default=DEFAULT_CONFIG, help="workload c0..c7 (default c2)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--slice-bits", default="13",
