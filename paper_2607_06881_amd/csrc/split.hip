@@ -207,13 +207,16 @@ __global__ void __launch_bounds__(256) split_kernel(int64_t rows, int64_t cols, 
 //   axis 0 (A, rows = m, cols = k):  D [S][kp][mp],  D[s][kk][i] = digit s of A[i][kk]
 //   axis 1 (B, rows = k, cols = n):  D [S][kp][np],  D[s][kk][j] = digit s of B[kk][j]
 // with kp, mp, np rounded up to the GEMM tile (16 and 128) and zeros in the padding.
-// A block covers 64 lines (c) x 16 k: its reads of A touch 64 full 128-byte lines
-// and its stores are 512-byte rows of the panel.
+// A block covers 64 lines (c) x 4 RPT k, each thread RPT elements of one line:
+// with RPT = 4 its reads of A touch 64 full 128-byte lines; RPT = 1 gives four
+// times the blocks for panels too small to fill the GPU otherwise (the split of
+// a long multiple double is integer work, bound by latency at low occupancy).
+// Stores are rows of 64 consecutive panel values.
 // With C > S, panels S .. C-1 receive the combinations of the Karatsuba
 // schedule (store_combos), computed from the same integer as the digits.
 // OutT = float for FP32 panels (the host checks that every value is below 2^24,
 // so the conversion is exact; kp is then a multiple of 32).
-template <int NW, int ML, class OutT>
+template <int NW, int ML, class OutT, int RPT>
 __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t cols, int L, int S, int w, int axis,
                                                           int64_t kp, int64_t cp, const double* __restrict__ X,
                                                           const int32_t* __restrict__ E, OutT* __restrict__ D,
@@ -225,24 +228,26 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
   if (c >= cp) return;
   const int64_t cc = c < Cn ? c : 0;  // clamped line for the unconditional loads
   const int e = E[cc];
-  // the limbs of kBatch of this thread's four elements are loaded before any of
+  // the limbs of kBatch of this thread's RPT elements are loaded before any of
   // them is split (fewer at a time for long multiple doubles, to stay in registers)
-  constexpr int kBatch = ML <= 4 ? 4 : (ML <= 8 ? 2 : 1);
-  for (int64_t kb = blockIdx.y; kb * 16 < kp; kb += gridDim.y) {
+  constexpr int kBatchL = ML <= 4 ? 4 : (ML <= 8 ? 2 : 1);
+  constexpr int kBatch = kBatchL < RPT ? kBatchL : RPT;
+  constexpr int kRows = 4 * RPT;  // k rows per block
+  for (int64_t kb = blockIdx.y; kb * kRows < kp; kb += gridDim.y) {
 #pragma unroll
-    for (int r0 = 0; r0 < 4; r0 += kBatch) {
+    for (int r0 = 0; r0 < RPT; r0 += kBatch) {
       double xs[kBatch][ML];
       bool valid[kBatch];
 #pragma unroll
       for (int b = 0; b < kBatch; ++b) {
-        const int64_t kk = kb * 16 + (threadIdx.x >> 6) + 4 * (r0 + b);
+        const int64_t kk = kb * kRows + (threadIdx.x >> 6) + 4 * (r0 + b);
         valid[b] = c < Cn && kk < K;
         const int64_t kc = kk < K ? kk : 0;
         load_limbs<ML>(X, plane, L, axis == 0 ? cc * cols + kc : kc * cols + cc, xs[b]);
       }
 #pragma unroll
       for (int b = 0; b < kBatch; ++b) {
-        const int64_t kk = kb * 16 + (threadIdx.x >> 6) + 4 * (r0 + b);
+        const int64_t kk = kb * kRows + (threadIdx.x >> 6) + 4 * (r0 + b);
         OutT* out = D + kk * cp + c;
         if (valid[b]) {
           uint64_t I[NW];
@@ -270,14 +275,27 @@ hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int w, int axis, 
   const int64_t K = axis == 0 ? cols : rows, Cn = axis == 0 ? rows : cols;
   const int64_t kp = f32 ? panel_k32(K) : panel_k(K), cp = panel_mn(Cn);
   const unsigned gx = static_cast<unsigned>(cp / 64);
-  const int64_t nkb = kp / 16;
+  // four elements per thread while that still gives 2048 blocks (8 per CU),
+  // one per thread below (kp is a multiple of 16)
+  const bool wide = (cp / 64) * (kp / 16) >= 2048;
+  const int64_t nkb = kp / (wide ? 16 : 4);
   const unsigned gy = static_cast<unsigned>(nkb < 65535 ? nkb : 65535);
-  if (f32)
-    hipLaunchKernelGGL((split_panel_kernel<NW, ML, float>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, w,
-                       axis, kp, cp, X, E, static_cast<float*>(D), masks, C);
-  else
-    hipLaunchKernelGGL((split_panel_kernel<NW, ML, double>), dim3(gx, gy), dim3(256), 0, stream, rows, cols, L, S, w,
-                       axis, kp, cp, X, E, static_cast<double*>(D), masks, C);
+  const dim3 grid(gx, gy);
+  if (f32) {
+    if (wide)
+      hipLaunchKernelGGL((split_panel_kernel<NW, ML, float, 4>), grid, dim3(256), 0, stream, rows, cols, L, S, w, axis,
+                         kp, cp, X, E, static_cast<float*>(D), masks, C);
+    else
+      hipLaunchKernelGGL((split_panel_kernel<NW, ML, float, 1>), grid, dim3(256), 0, stream, rows, cols, L, S, w, axis,
+                         kp, cp, X, E, static_cast<float*>(D), masks, C);
+  } else {
+    if (wide)
+      hipLaunchKernelGGL((split_panel_kernel<NW, ML, double, 4>), grid, dim3(256), 0, stream, rows, cols, L, S, w,
+                         axis, kp, cp, X, E, static_cast<double*>(D), masks, C);
+    else
+      hipLaunchKernelGGL((split_panel_kernel<NW, ML, double, 1>), grid, dim3(256), 0, stream, rows, cols, L, S, w,
+                         axis, kp, cp, X, E, static_cast<double*>(D), masks, C);
+  }
   return hipGetLastError();
 }
 
