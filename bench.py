@@ -23,6 +23,10 @@ Prints one JSON line:
   exactly from their planes, bit-identical results), with the 13-bit digits and
   with the adaptive width; the headline keeps the paper's pair schedule unless
   ``--schedule karatsuba`` says otherwise;
+* ``int8``: the same workload with the level products on the int8 matrix
+  cores (MDGEMM_INT8: digits of at most 7 bits, one int8 GEMM with exact int32
+  sums per level, the same exact accumulation), its level GEMMs against the
+  5.0 POP/s dense int8 peak;
 * ``cpu_baseline``: the CPU oracle's classic multiple-double GEMM (one
   sequential inner product per element, all host cores) timed on a bounded
   sample of the same product's rows.
@@ -43,6 +47,7 @@ if ROOT not in sys.path:
 
 MFMA_F64_PEAK_TFLOPS = 78.6  # MI355X dense FP64 matrix peak (published)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E (published)
+INT8_PEAK_TOPS = 5000.0  # MI355X dense int8 matrix peak (published)
 METRIC = "effective dd/qd GEMM GFLOP/s; % FP64 MFMA peak; bit-exact+tol vs CPU oracle"
 # the level-GEMM kernel is built from these sources (its job table is declared in internal.h)
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2607_06881_amd", "csrc", f) for f in ("slice_gemm.hip", "internal.h")]
@@ -286,12 +291,32 @@ def main(argv=None) -> int:
             "slice_gemm_TFLOP/s": round(a_tflops, 3), "frac": round(a_tflops / MFMA_F64_PEAK_TFLOPS, 4),
         }
 
+    def int8_mode():
+        """A few timed steps of the same workload with the int8 level products."""
+        i_opts = {"range_bits": w.range_bits} if w.range_bits else {}
+        I8 = md.MDGEMM_INT8
+        try:
+            i_bits, i_S, i_T = md.mdgemm_plan(m, n, k, L, flags=I8, **i_opts)
+        except md.MdgemmError as e:  # e.g. more than 8 limbs: S > 64 at 7 bits
+            return {"skipped": str(e)}
+        i_ms, i_stage = measure(i_opts, args.adaptive_steps, 2, I8)
+        i_pairs = workloads.pair_count(i_S, i_T)
+        tops = 2.0 * m * n * k * i_pairs / (i_stage[2] * 1e-3) / 1e12
+        return {
+            "slice_bits": i_bits, "slices": i_S, "cutoff": i_T, "pairs": i_pairs, "gemms": i_T + 1,
+            "steps": args.adaptive_steps, "ms_per_step": round(i_ms, 4),
+            "value": round(md_flops / (i_ms * 1e-3) / 1e9, 3),
+            "stage_ms": [round(float(x), 4) for x in i_stage],
+            "level_gemm_TOPS": round(tops, 1), "frac": round(tops / INT8_PEAK_TOPS, 4),
+        }
+
     if bits_arg == 13 and not sched_flags and args.adaptive_steps > 0:
         # the same workload with the adaptive width and with the Karatsuba
         # schedule, reported beside the paper's 13-bit digit pairs
         out["adaptive_width"] = extra(mode_opts(md.MDGEMM_SLICE_BITS_AUTO), 0)
         out["karatsuba"] = extra(mode_opts(13), md.MDGEMM_KARATSUBA)
         out["karatsuba_adaptive"] = extra(mode_opts(md.MDGEMM_SLICE_BITS_AUTO), md.MDGEMM_KARATSUBA)
+        out["int8"] = int8_mode()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, A_h, B_h, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -48,7 +48,7 @@ extern "C" {
 /* ---- status codes ---------------------------------------------------------- */
 #define MDGEMM_OK 0
 #define MDGEMM_EINVAL -1      /* invalid size, limb/slice/cutoff count, null or overlapping pointer */
-#define MDGEMM_EEXACT -2      /* pairs_t * k * (2^w - 1)^2 >= 2^53 for some kept level t: sums not exact */
+#define MDGEMM_EEXACT -2      /* pairs_t * k * (2^w - 1)^2 >= 2^53 (2^31 with MDGEMM_INT8) for a kept level t */
 #define MDGEMM_ENOMEM -3      /* the library's own workspace could not be allocated */
 #define MDGEMM_EHIP -4        /* a HIP call failed (no device, launch or runtime error) */
 #define MDGEMM_EWORKSPACE -5  /* the caller's workspace is smaller than mdgemm_workspace_bytes() */
@@ -72,6 +72,7 @@ extern "C" {
 #define MDGEMM_TIME_STAGES 4u  /* record HIP events between stages; read with mdgemm_stage_times() */
 #define MDGEMM_KARATSUBA 8u    /* level products by the Karatsuba schedule where it pays (see below) */
 #define MDGEMM_KARATSUBA_MIN_TERMS 16u /* the Karatsuba schedule with the fewest GEMMs, always */
+#define MDGEMM_INT8 32u        /* level products on the int8 matrix cores, digits of at most 7 bits (see below) */
 
 /* cutoff selectors for mdgemm_opts.cutoff (else an explicit T in 0 .. 2S-2) */
 #define MDGEMM_CUTOFF_DEFAULT -1  /* T = S - 1: the pair set of the rewritten product */
@@ -83,7 +84,7 @@ typedef struct mdgemm_opts {
   size_t workspace_bytes; /* size of `workspace` in bytes */
   int slices_per_limb;    /* 13-bit digits per limb, S = limbs * slices_per_limb <= 64; 0 = 4 */
   int cutoff;             /* largest kept p + q; MDGEMM_CUTOFF_DEFAULT or _ALL or 0..2S-2 */
-  unsigned flags;         /* MDGEMM_CHECK_FINITE, _SYNC, _TIME_STAGES, _KARATSUBA, _KARATSUBA_MIN_TERMS */
+  unsigned flags;         /* MDGEMM_CHECK_FINITE, _SYNC, _TIME_STAGES, _KARATSUBA, _KARATSUBA_MIN_TERMS, _INT8 */
   int slice_bits;         /* digit width w: 0 = 13 (section 2), 1..26, or MDGEMM_SLICE_BITS_AUTO */
   int slices;             /* digits per element S; 0 = derived (see below) */
   int range_bits;         /* range balancing: full precision down to 2^-range_bits of the line; 0 = off */
@@ -116,7 +117,22 @@ typedef struct mdgemm_opts {
  * its own leading level.  With MDGEMM_SLICE_BITS_AUTO the width is chosen for the
  * fewest pairs of (S, T) including D.  mdgemm_line_spread measures the range of
  * the data.
- * In every case S <= 64 and S w <= MDGEMM_MAX_DIGIT_BITS. */
+ * In every case S <= 64 and S w <= MDGEMM_MAX_DIGIT_BITS.
+ *
+ * MDGEMM_INT8.  The level sums of section 2 are exact integer sums, so with
+ * digits of at most 7 bits (|d| <= 127) they are formed on the int8 matrix cores
+ * with exact int32 sums: each level t is one int8 GEMM (hipBLASLt) of the
+ * contiguous digit ranges of its pairs, which requires
+ * max pairs of a level times k (2^w - 1)^2 < 2^31.  slice_bits 0 or
+ * MDGEMM_SLICE_BITS_AUTO: the widest w <= 7 whose levels stay exact for this k,
+ * S = ceil(52 limbs / w) (plus the range digits), T by the cutoff rules above
+ * (T = S - 1 by default); slice_bits 1..7: that width; wider, the Karatsuba flags,
+ * or S > 64 (more than 8 limbs at w = 7) return MDGEMM_EINVAL, and no exact width
+ * MDGEMM_EEXACT.  Digits, levels and C are bit-identical to the FP64 path run
+ * with the same slice_bits, slices and cutoff.  Double-double at k = 4096:
+ * w = 7, S = 15, T = 14 (120 pairs, 15 GEMMs).  The call allocates nothing
+ * beyond the workspace; hipBLASLt's handle and chosen algorithms are created on
+ * a device's first such call and kept until the process ends. */
 
 /* Fill `opts` with the defaults: default stream, library workspace, 4 slices per
  * limb of 13 bits, cutoff T = S - 1, no range balancing, no flags. */

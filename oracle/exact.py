@@ -259,7 +259,7 @@ def _max_pairs(S: int, T: int) -> int:
 
 
 def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_limb: int = 4, cutoff: int = -1,
-         range_bits: int = 0):
+         range_bits: int = 0, int8: bool = False):
     """(w, S, T) of the product's digit width, digit count and cutoff, or None when
     the levels cannot stay exact.  Written from the options' definitions:
 
@@ -270,7 +270,11 @@ def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_lim
     * range balancing: D = ceil(range_bits / w) more digits, S = S0 + D, default
       cutoff T = S0 - 1 + 2 D (a product of two elements D digits below their
       lines' grids keeps its S0 leading levels); cutoff -2 keeps every pair;
-    * exactness: max pairs of a kept level times k (2^w - 1)^2 below 2^53.
+    * exactness: max pairs of a kept level times k (2^w - 1)^2 below 2^53;
+    * int8 (level sums in int32 on the int8 matrix cores): digits of at most 7
+      bits; slice_bits 0 or -1 take the widest w = 7, 6, ..., 1 whose (S, T) is
+      valid and whose level sums stay below 2^31 (the same bound with 2^31 in
+      place of 2^53), slice_bits 1..7 that width, S0 = slices or ceil(52 L / w).
     Raises ValueError for invalid options (S > 64, S w > 844, ...)."""
     def finish(w, S0):
         D = -(-range_bits // w)
@@ -286,6 +290,30 @@ def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_lim
 
     def exact_ok(w, S, T):
         return _max_pairs(S, T) * k * (2**w - 1) ** 2 < 2**53
+
+    if int8:
+        def exact32(w, S, T):
+            return _max_pairs(S, T) * k * (2**w - 1) ** 2 < 2**31
+
+        if slice_bits in (0, -1):
+            if slices:
+                raise ValueError("slices with the automatic width")
+            sized = False
+            for w in range(7, 0, -1):
+                try:
+                    cand = finish(w, -(-52 * L // w))
+                except ValueError:
+                    continue
+                sized = True
+                if exact32(*cand):
+                    return cand
+            if not sized:
+                raise ValueError("digit count")
+            return None
+        if not 1 <= slice_bits <= 7:
+            raise ValueError("width")
+        cand = finish(slice_bits, slices or -(-52 * L // slice_bits))
+        return cand if exact32(*cand) else None
 
     if slice_bits == -1:
         if slices:

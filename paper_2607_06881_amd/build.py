@@ -8,6 +8,9 @@ Flags:
   FP64 matrix-core throughput.
 * ``-Xclang -target-feature -Xclang -packed-fp32-ops``: no packed-FP32
   instructions are generated (none of these kernels needs them).
+
+The library links hipBLASLt, which runs the int8 level GEMMs of the
+MDGEMM_INT8 option (the FP64 path uses only the kernels built here).
 """
 
 from __future__ import annotations
@@ -66,7 +69,7 @@ def build(verbose: bool = False) -> str:
         for fut in [pool.submit(_run, cmd, verbose) for cmd in cmds]:
             fut.result()
     tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=gfx950", "-fPIC", "-shared", "-o", tmp, *objs], verbose)
+    _run([HIPCC, "--offload-arch=gfx950", "-fPIC", "-shared", "-o", tmp, *objs, "-lhipblaslt"], verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -82,11 +82,12 @@ struct CarryChain {
   }
 };
 
-// The chain over levels read from G [levels][m][n] (integer-valued doubles).
-// Loads are issued eight levels at a time before any of them is used, so a
-// thread keeps up to eight independent loads in flight.
-template <int NW>
-__device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __restrict__ G, int levels, int w,
+// The chain over levels read from G [levels][m][n] (integer-valued doubles, or
+// int32 planes of the int8 level products).  Loads are issued eight levels at a
+// time before any of them is used, so a thread keeps up to eight independent
+// loads in flight.
+template <int NW, class PT = double>
+__device__ inline void accumulate_levels(uint64_t (&N)[NW], const PT* __restrict__ G, int levels, int w,
                                          int64_t plane, int64_t idx) {
 #pragma unroll
   for (int i = 0; i < NW; ++i) N[i] = 0;
@@ -96,7 +97,7 @@ __device__ inline void accumulate_levels(uint64_t (&N)[NW], const double* __rest
   for (int t0 = T; t0 >= 0; t0 -= 8) {
     // unconditional loads (levels below 0 re-read level 0 and are discarded),
     // so that the eight loads go out back to back
-    double g[8];
+    PT g[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int t = t0 - u;
@@ -195,9 +196,9 @@ __device__ inline void round_limbs(uint64_t (&N)[NW], int L, int scale, double* 
   }
 }
 
-template <int NW>
+template <int NW, class PT>
 __global__ void __launch_bounds__(256) accum_renorm_kernel(int64_t m, int64_t n, int L, int levels, int w,
-                                                           const double* __restrict__ G,
+                                                           const PT* __restrict__ G,
                                                            const int32_t* __restrict__ EA,
                                                            const int32_t* __restrict__ EB, double* __restrict__ C) {
   const int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -207,7 +208,7 @@ __global__ void __launch_bounds__(256) accum_renorm_kernel(int64_t m, int64_t n,
   for (int64_t i = blockIdx.y; i < m; i += gridDim.y) {
     const int64_t idx = i * n + j;
     uint64_t N[NW];
-    accumulate_levels<NW>(N, G, levels, w, plane, idx);
+    accumulate_levels<NW, PT>(N, G, levels, w, plane, idx);
     const int scale = EA[i] + ebj - 2 * w - w * (levels - 1);
     round_limbs<NW>(N, L, scale, C, plane, idx);
   }
@@ -359,8 +360,18 @@ hipError_t launch_accum_renorm(int64_t m, int64_t n, int L, int levels, int w, c
   const dim3 grid = elem_grid(m, n);
   // the next word count instantiated (the extra words hold the sign extension)
   return with_words(accum_words(levels, w), [&](auto nw) {
-    hipLaunchKernelGGL(accum_renorm_kernel<decltype(nw)::value>, grid, dim3(256), 0, stream, m, n, L, levels, w, G,
-                       EA, EB, C);
+    hipLaunchKernelGGL((accum_renorm_kernel<decltype(nw)::value, double>), grid, dim3(256), 0, stream, m, n, L,
+                       levels, w, G, EA, EB, C);
+  });
+}
+
+hipError_t launch_accum_renorm_i32(int64_t m, int64_t n, int L, int levels, int w, const int32_t* G,
+                                   const int32_t* EA, const int32_t* EB, double* C, hipStream_t stream) {
+  if (m == 0 || n == 0) return hipSuccess;
+  const dim3 grid = elem_grid(m, n);
+  return with_words(accum_words(levels, w), [&](auto nw) {
+    hipLaunchKernelGGL((accum_renorm_kernel<decltype(nw)::value, int32_t>), grid, dim3(256), 0, stream, m, n, L,
+                       levels, w, G, EA, EB, C);
   });
 }
 

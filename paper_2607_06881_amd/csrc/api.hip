@@ -38,6 +38,15 @@ constexpr int kStages = 4;
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+#define MDG_TRY(expr)              \
+  do {                             \
+    int st_ = (expr);              \
+    if (st_ != MDGEMM_OK) return st_; \
+  } while (0)
+
+// Widest digit of the int8 level products: |d| <= 127 fits int8.
+constexpr int kInt8MaxBits = 7;
+
 // ---- exactness: pairs_t * k * (2^w - 1)^2 < 2^53 for every kept level t ------
 
 // Pairs (p, q), 0 <= p, q < S, with p + q <= T.
@@ -66,6 +75,14 @@ bool exact_ok(int64_t k, int pairs, int w) {
   const unsigned __int128 lhs =
       static_cast<unsigned __int128>(pairs) * static_cast<unsigned __int128>(k) * (dmax * dmax);
   return lhs < (static_cast<unsigned __int128>(1) << 53);
+}
+
+// The int8 level products (MDGEMM_INT8) sum in int32: pairs_t * k * (2^w - 1)^2 < 2^31.
+bool exact_ok_i32(int64_t k, int pairs, int w) {
+  const uint64_t dmax = (1ull << w) - 1ull;
+  const unsigned __int128 lhs =
+      static_cast<unsigned __int128>(pairs) * static_cast<unsigned __int128>(k) * (dmax * dmax);
+  return lhs < (static_cast<unsigned __int128>(1) << 31);
 }
 
 bool width_ok(int S, int w) { return S >= 1 && S <= MDGEMM_MAX_SLICES && w >= 1 && w <= mdg::kMaxSliceBits &&
@@ -231,6 +248,25 @@ bool auto_width(int limbs, int64_t m, int64_t n, int64_t k, int range_bits, int 
   return found;
 }
 
+// Widest digit for the int8 level products: w = 7 down to 1 with S0 =
+// ceil(52 L / w), D range digits and the requested cutoff, valid and exact in
+// int32.  Returns MDGEMM_EINVAL when no width has S <= 64, MDGEMM_EEXACT when
+// none of those is exact for this k.
+int int8_width(int limbs, int64_t k, int range_bits, int cutoff, int* w_out, int* S0_out) {
+  bool sized = false;
+  for (int w = kInt8MaxBits; w >= 1; --w) {
+    const int S0 = (4 * mdg::kSliceBits * limbs + w - 1) / w, D = range_digits(range_bits, w);
+    const int S = S0 + D, T = cutoff_for(cutoff, S0, D);
+    if (!width_ok(S, w) || T < 0 || T > 2 * S - 2 || !levels_ok(T + 1, w)) continue;
+    sized = true;
+    if (!exact_ok_i32(k, max_pairs(S, T), w)) continue;
+    *w_out = w;
+    *S0_out = S0;
+    return MDGEMM_OK;
+  }
+  return sized ? MDGEMM_EEXACT : MDGEMM_EINVAL;
+}
+
 // Digit width, digit count and cutoff of a product with reduction length k.
 int resolve(int limbs, int64_t m, int64_t n, int64_t k, const mdgemm_opts* opts, Resolved* r) {
   if (limbs < 1 || limbs > MDGEMM_MAX_LIMBS) return MDGEMM_EINVAL;
@@ -239,7 +275,19 @@ int resolve(int limbs, int64_t m, int64_t n, int64_t k, const mdgemm_opts* opts,
   const int slices = opts ? opts->slices : 0;
   const int range_bits = opts ? opts->range_bits : 0;
   if (slices < 0 || range_bits < 0 || range_bits > mdg::kMaxDigitBits) return MDGEMM_EINVAL;
-  if (bits == MDGEMM_SLICE_BITS_AUTO) {
+  const bool int8 = opts && (opts->flags & MDGEMM_INT8);
+  if (int8) {
+    if (opts->flags & (MDGEMM_KARATSUBA | MDGEMM_KARATSUBA_MIN_TERMS)) return MDGEMM_EINVAL;
+    if (bits == 0 || bits == MDGEMM_SLICE_BITS_AUTO) {
+      if (slices != 0) return MDGEMM_EINVAL;
+      MDG_TRY(int8_width(limbs, k, range_bits, opts->cutoff, &r->w, &r->S));
+    } else if (bits >= 1 && bits <= kInt8MaxBits) {
+      r->w = bits;
+      r->S = slices ? slices : (4 * mdg::kSliceBits * limbs + bits - 1) / bits;
+    } else {
+      return MDGEMM_EINVAL;
+    }
+  } else if (bits == MDGEMM_SLICE_BITS_AUTO) {
     if (slices != 0) return MDGEMM_EINVAL;
     if (!auto_width(limbs, m, n, k, range_bits, opts->cutoff, r->kind, &r->w, &r->S)) return MDGEMM_EEXACT;
   } else if (bits == 0 || bits == mdg::kSliceBits) {
@@ -337,6 +385,42 @@ bool layout(int64_t m, int64_t n, int64_t k, const Planned& pl, int w, Layout* L
   off += align_up(esz * sch.mask_b.size() * kp * static_cast<size_t>(np));
   L->g = off;
   off += align_up(sizeof(double) * static_cast<size_t>(sch.planes) * static_cast<size_t>(m) * static_cast<size_t>(n));
+  L->total = off;
+  return true;
+}
+
+// The level sums of a resolved product stay exact: below 2^53 on the FP64
+// matrix cores, below 2^31 on the int8 ones.
+bool resolved_exact(const Resolved& r, int64_t k) {
+  const int pairs = max_pairs(r.S, r.T);
+  return (r.flags & MDGEMM_INT8) ? exact_ok_i32(k, pairs, r.w) : exact_ok(k, pairs, r.w);
+}
+
+// Workspace of the int8 level products: EA | EB | flag | A's digits [m][S][kp] |
+// B's digits [S][kp][np] | int32 levels [T+1][m][n], each aligned to 256 bytes;
+// kp = k and np = n rounded up to 16 (int8 operand columns of whole 16 bytes).
+struct LayoutI8 {
+  size_t ea = 0, eb = 0, flag = 0, da = 0, db = 0, g = 0, total = 0;
+  int64_t kp = 0, np = 0;
+};
+bool layout_int8(int64_t m, int64_t n, int64_t k, int S, int T, LayoutI8* L) {
+  L->kp = (k + 15) / 16 * 16;
+  L->np = (n + 15) / 16 * 16;
+  const double approx = (double)S * (double)L->kp * ((double)m + (double)L->np) + 4.0 * (T + 1) * (double)m * (double)n;
+  if (approx > 4.0e18 || m > (int64_t{1} << 31) || n > (int64_t{1} << 31)) return false;
+  size_t off = 0;
+  L->ea = off;
+  off += align_up(sizeof(int32_t) * static_cast<size_t>(m));
+  L->eb = off;
+  off += align_up(sizeof(int32_t) * static_cast<size_t>(n));
+  L->flag = off;
+  off += align_up(sizeof(int32_t));
+  L->da = off;
+  off += align_up(static_cast<size_t>(m) * S * static_cast<size_t>(L->kp));
+  L->db = off;
+  off += align_up(static_cast<size_t>(S) * static_cast<size_t>(L->kp) * static_cast<size_t>(L->np));
+  L->g = off;
+  off += align_up(sizeof(int32_t) * static_cast<size_t>(T + 1) * static_cast<size_t>(m) * static_cast<size_t>(n));
   L->total = off;
   return true;
 }
@@ -462,12 +546,6 @@ int record(int i, hipStream_t s) {
 
 inline int hip_status(hipError_t e) { return e == hipSuccess ? MDGEMM_OK : MDGEMM_EHIP; }
 
-#define MDG_TRY(expr)              \
-  do {                             \
-    int st_ = (expr);              \
-    if (st_ != MDGEMM_OK) return st_; \
-  } while (0)
-
 // Pointers into a workspace laid out by layout(); DA / DB are float* for FP32 panels.
 struct Parts {
   int32_t *EA, *EB, *flag;
@@ -511,6 +589,69 @@ int enqueue_gemm(const Planned& pl, int64_t m, int64_t n, int64_t k, const Parts
                                            static_cast<const double*>(w.DB), out, jobs, s));
 }
 
+// MDGEMM_CHECK_FINITE: scan A and B for inf/nan (synchronizes the stream).
+int check_finite(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, int32_t* flag,
+                 hipStream_t s) {
+  MDG_TRY(hip_status(mdg::launch_set_i32(flag, 1, 0, s)));
+  MDG_TRY(hip_status(mdg::launch_nonfinite_scan(A, static_cast<int64_t>(limbs) * m * k, flag, s)));
+  MDG_TRY(hip_status(mdg::launch_nonfinite_scan(B, static_cast<int64_t>(limbs) * k * n, flag, s)));
+  int32_t h = 0;
+  MDG_TRY(hip_status(hipMemcpyAsync(&h, flag, sizeof h, hipMemcpyDeviceToHost, s)));
+  MDG_TRY(hip_status(hipStreamSynchronize(s)));
+  return h ? MDGEMM_ENONFINITE : MDGEMM_OK;
+}
+
+// mdgemm_ex with MDGEMM_INT8 (m, n, k > 0, arguments checked): exponents, int8
+// digits, one int8 GEMM per level into int32 planes, exact accumulation.
+int run_int8(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
+             const mdgemm_opts* opts, const Resolved& r) {
+  LayoutI8 L;
+  if (!layout_int8(m, n, k, r.S, r.T, &L)) return MDGEMM_EINVAL;
+  hipStream_t s = r.stream;
+  const bool timed = (r.flags & MDGEMM_TIME_STAGES) != 0;
+  char* ws = nullptr;
+  LibraryBuffer lib;
+  if (opts && opts->workspace) {
+    if (opts->workspace_bytes < L.total) return MDGEMM_EWORKSPACE;
+    ws = static_cast<char*>(opts->workspace);
+  } else {
+    MDG_TRY(lib.acquire(L.total, s, &ws));
+  }
+  int32_t* EA = reinterpret_cast<int32_t*>(ws + L.ea);
+  int32_t* EB = reinterpret_cast<int32_t*>(ws + L.eb);
+  int32_t* flag = reinterpret_cast<int32_t*>(ws + L.flag);
+  int8_t* DA = reinterpret_cast<int8_t*>(ws + L.da);
+  int8_t* DB = reinterpret_cast<int8_t*>(ws + L.db);
+  int32_t* G = reinterpret_cast<int32_t*>(ws + L.g);
+  auto enqueue = [&]() -> int {
+    if (r.flags & MDGEMM_CHECK_FINITE) MDG_TRY(check_finite(m, n, k, limbs, A, B, flag, s));
+    std::unique_lock<std::mutex> tlock(timing().mu, std::defer_lock);
+    if (timed) {
+      tlock.lock();
+      timing().valid = false;
+      MDG_TRY(record(0, s));
+    }
+    MDG_TRY(hip_status(mdg::launch_exponents(m, k, 0, A, EA, s)));
+    MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, EB, s)));
+    if (timed) MDG_TRY(record(1, s));
+    MDG_TRY(hip_status(mdg::launch_split_int8(m, k, limbs, r.S, r.w, 0, A, EA, DA, L.kp, L.np, s)));
+    MDG_TRY(hip_status(mdg::launch_split_int8(k, n, limbs, r.S, r.w, 1, B, EB, DB, L.kp, L.np, s)));
+    if (timed) MDG_TRY(record(2, s));
+    MDG_TRY(hip_status(mdg::launch_levels_int8(m, n, L.kp, L.np, r.S, r.T, DA, DB, G, s)));
+    if (timed) MDG_TRY(record(3, s));
+    MDG_TRY(hip_status(mdg::launch_accum_renorm_i32(m, n, limbs, r.T + 1, r.w, G, EA, EB, C, s)));
+    if (timed) {
+      MDG_TRY(record(4, s));
+      timing().valid = true;
+    }
+    return MDGEMM_OK;
+  };
+  const int st = lib.release(enqueue());
+  if (st != MDGEMM_OK) return st;
+  if (r.flags & MDGEMM_SYNC) MDG_TRY(hip_status(hipStreamSynchronize(s)));
+  return MDGEMM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -530,7 +671,7 @@ int mdgemm_plan(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* o
   Resolved r;
   if (m < 0 || n < 0 || k < 0) return MDGEMM_EINVAL;
   MDG_TRY(resolve(limbs, m, n, k, opts, &r));
-  if (!exact_ok(k, max_pairs(r.S, r.T), r.w)) return MDGEMM_EEXACT;
+  if (!resolved_exact(r, k)) return MDGEMM_EEXACT;
   if (slice_bits) *slice_bits = r.w;
   if (slices) *slices = r.S;
   if (cutoff) *cutoff = r.T;
@@ -554,6 +695,10 @@ size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const 
   Resolved r;
   if (m < 0 || n < 0 || k < 0 || resolve(limbs, m, n, k, opts, &r) != MDGEMM_OK) return SIZE_MAX;
   if (m == 0 || n == 0 || k == 0) return 0;
+  if (r.flags & MDGEMM_INT8) {
+    LayoutI8 L8;
+    return layout_int8(m, n, k, r.S, r.T, &L8) ? L8.total : SIZE_MAX;
+  }
   Layout L;
   if (!layout(m, n, k, *planned_for(r.S, r.T, m, n, k, r.w, r.kind), r.w, &L)) return SIZE_MAX;
   return L.total;
@@ -570,7 +715,7 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   const size_t bbytes = sizeof(double) * limbs * static_cast<size_t>(k) * static_cast<size_t>(n);
   const size_t cbytes = sizeof(double) * limbs * static_cast<size_t>(m) * static_cast<size_t>(n);
   if (k > 0 && (overlaps(C, cbytes, A, abytes) || overlaps(C, cbytes, B, bbytes))) return MDGEMM_EINVAL;
-  if (!exact_ok(k, max_pairs(r.S, r.T), r.w)) return MDGEMM_EEXACT;
+  if (!resolved_exact(r, k)) return MDGEMM_EEXACT;
   hipStream_t s = r.stream;
   const bool timed = (r.flags & MDGEMM_TIME_STAGES) != 0;
 
@@ -580,6 +725,7 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
     return MDGEMM_OK;
   }
 
+  if (r.flags & MDGEMM_INT8) return run_int8(m, n, k, limbs, A, B, C, opts, r);
   const auto pl = planned_for(r.S, r.T, m, n, k, r.w, r.kind);
   if (!schedule_exact(pl->s, k, r.w)) return MDGEMM_EEXACT;
   Layout L;
@@ -595,15 +741,7 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   const Parts w = parts(ws, L);
 
   auto enqueue = [&]() -> int {
-    if (r.flags & MDGEMM_CHECK_FINITE) {
-      MDG_TRY(hip_status(mdg::launch_set_i32(w.flag, 1, 0, s)));
-      MDG_TRY(hip_status(mdg::launch_nonfinite_scan(A, static_cast<int64_t>(limbs) * m * k, w.flag, s)));
-      MDG_TRY(hip_status(mdg::launch_nonfinite_scan(B, static_cast<int64_t>(limbs) * k * n, w.flag, s)));
-      int32_t h = 0;
-      MDG_TRY(hip_status(hipMemcpyAsync(&h, w.flag, sizeof h, hipMemcpyDeviceToHost, s)));
-      MDG_TRY(hip_status(hipStreamSynchronize(s)));
-      if (h) return MDGEMM_ENONFINITE;
-    }
+    if (r.flags & MDGEMM_CHECK_FINITE) MDG_TRY(check_finite(m, n, k, limbs, A, B, w.flag, s));
     std::unique_lock<std::mutex> tlock(timing().mu, std::defer_lock);
     if (timed) {
       tlock.lock();

@@ -62,6 +62,18 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
                         void* D, bool panel, hipStream_t stream, const uint32_t* masks = nullptr,
                         int combos = 0, bool f32 = false);
 
+// a2 for the int8 level products: digits of at most 7 bits as int8, A (axis 0,
+// rows = m, cols = k) as D [m][S][kp], B (axis 1, rows = k, cols = n) as
+// D [S][kp][np] with digit q in plane S-1-q; zeros in the padding.
+hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
+                             const int32_t* E, int8_t* D, int64_t kp, int64_t np, hipStream_t stream);
+
+// a3 on the int8 matrix cores: levels t = 0..T of the layouts of
+// launch_split_int8 into int32 planes G [T+1][m][n], one hipBLASLt GEMM per
+// level; every level sum must stay below 2^31 (checked by the caller).
+hipError_t launch_levels_int8(int64_t m, int64_t n, int64_t kp, int64_t np, int S, int T, const int8_t* DA,
+                              const int8_t* DB, int32_t* G, hipStream_t stream);
+
 // a3: products of the combination panels DAt [*][panel_k(k)][panel_mn(m)] and
 // DBp [*][panel_k(k)][panel_mn(n)] (combinations 0..S-1 are the digits); one
 // job per grid row, outputs [*][m][n].
@@ -96,6 +108,10 @@ hipError_t launch_accumulate(int64_t m, int64_t n, int levels, int w, const doub
 // a4 + a5: exact accumulation and greedy rounding into L limbs, scaled by 2^(EA+EB-2w).
 hipError_t launch_accum_renorm(int64_t m, int64_t n, int L, int levels, int w, const double* G, const int32_t* EA,
                                const int32_t* EB, double* C, hipStream_t stream);
+
+// a4 + a5 from int32 level planes (the int8 level products).
+hipError_t launch_accum_renorm_i32(int64_t m, int64_t n, int L, int levels, int w, const int32_t* G,
+                                   const int32_t* EA, const int32_t* EB, double* C, hipStream_t stream);
 
 // a4 + a5 for a schedule whose planes enter several levels: level t =
 // sum of coef * plane over the entries (chunk_first / chunks of ScheduleTable;

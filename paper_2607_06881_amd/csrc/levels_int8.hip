@@ -1,0 +1,128 @@
+// Step a3 on the int8 matrix cores (the MDGEMM_INT8 option).
+//
+// The level products of section 2 are exact integer sums, so any matrix unit
+// that sums integer products exactly computes them.  With digits of at most 7
+// bits (|d| <= 127) a product is below 2^14 and a level sum of pairs x k
+// products stays below 2^31 when pairs k 127^2 < 2^31 (checked by the caller),
+// so the int8 x int8 -> int32 matrix cores (5 POP/s on MI355X, 64 times the
+// FP64 rate) form every level exactly.
+//
+// Layouts (launch_split_int8): A's digits D_A [m][S][kp], B's digits in reverse
+// order D_B [S][kp][np].  The pairs (p, t - p) of level t, p = p0 .. p1, are then
+// the contiguous k range p0 kp .. (p1 + 1) kp of every row of D_A and of every
+// column of D_B, so a level is one plain GEMM (column-major, no transposes):
+//     G_t^T (n x m, ld n) = D_B[rows S-1-t+p0 ..] (n x K, ld np) . D_A[cols p0 kp ..] (K x m, ld S kp)
+// with K = (p1 - p0 + 1) kp; G_t^T in column-major is the row-major plane
+// G_t [m][n] that the accumulation reads.  Each level is one hipBLASLt int8
+// GEMM; the handle, the operation descriptor and the algorithm per shape are
+// created once per device and kept.
+#include <hipblaslt/hipblaslt.h>
+
+#include <array>
+#include <map>
+#include <mutex>
+#include <vector>
+
+#include "internal.h"
+
+namespace mdg {
+namespace {
+
+struct Blt {
+  hipblasLtHandle_t handle = nullptr;
+  hipblasLtMatmulDesc_t desc = nullptr;
+  hipblasLtMatmulPreference_t pref = nullptr;
+  std::map<std::array<int64_t, 5>, hipblasLtMatmulAlgo_t> algos;  // (M, N, K, lda, ldb)
+};
+
+struct BltState {
+  std::mutex mu;
+  std::vector<Blt*> dev;  // per device, created on first use and kept until the process ends
+};
+
+BltState& blt_state() {
+  static BltState s;
+  return s;
+}
+
+// The hipBLASLt objects of the current device (with blt_state().mu held).
+Blt* blt_for_device() {
+  int d = 0;
+  if (hipGetDevice(&d) != hipSuccess) return nullptr;
+  BltState& s = blt_state();
+  if (static_cast<size_t>(d) >= s.dev.size()) s.dev.resize(d + 1, nullptr);
+  if (s.dev[d]) return s.dev[d];
+  Blt* b = new Blt;
+  bool ok = hipblasLtCreate(&b->handle) == HIPBLAS_STATUS_SUCCESS &&
+            hipblasLtMatmulDescCreate(&b->desc, HIPBLAS_COMPUTE_32I, HIP_R_32I) == HIPBLAS_STATUS_SUCCESS &&
+            hipblasLtMatmulPreferenceCreate(&b->pref) == HIPBLAS_STATUS_SUCCESS;
+  if (ok) {
+    const hipblasOperation_t op = HIPBLAS_OP_N;
+    const uint64_t ws = 0;  // no workspace: the call allocates nothing
+    ok = hipblasLtMatmulDescSetAttribute(b->desc, HIPBLASLT_MATMUL_DESC_TRANSA, &op, sizeof op) ==
+             HIPBLAS_STATUS_SUCCESS &&
+         hipblasLtMatmulDescSetAttribute(b->desc, HIPBLASLT_MATMUL_DESC_TRANSB, &op, sizeof op) ==
+             HIPBLAS_STATUS_SUCCESS &&
+         hipblasLtMatmulPreferenceSetAttribute(b->pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &ws, sizeof ws) ==
+             HIPBLAS_STATUS_SUCCESS;
+  }
+  if (!ok) {
+    if (b->pref) hipblasLtMatmulPreferenceDestroy(b->pref);
+    if (b->desc) hipblasLtMatmulDescDestroy(b->desc);
+    if (b->handle) hipblasLtDestroy(b->handle);
+    delete b;
+    return nullptr;
+  }
+  s.dev[d] = b;
+  return b;
+}
+
+struct Layouts {
+  hipblasLtMatrixLayout_t a = nullptr, b = nullptr, d = nullptr;
+  ~Layouts() {
+    if (a) hipblasLtMatrixLayoutDestroy(a);
+    if (b) hipblasLtMatrixLayoutDestroy(b);
+    if (d) hipblasLtMatrixLayoutDestroy(d);
+  }
+};
+
+}  // namespace
+
+hipError_t launch_levels_int8(int64_t m, int64_t n, int64_t kp, int64_t np, int S, int T, const int8_t* DA,
+                              const int8_t* DB, int32_t* G, hipStream_t stream) {
+  if (m == 0 || n == 0) return hipSuccess;
+  if (S < 1 || T < 0 || T > 2 * S - 2 || kp <= 0 || np < n) return hipErrorInvalidValue;
+  std::lock_guard<std::mutex> lock(blt_state().mu);
+  Blt* b = blt_for_device();
+  if (!b) return hipErrorNotInitialized;
+  const int32_t alpha = 1, beta = 0;
+  for (int t = 0; t <= T; ++t) {
+    const int p0 = t - (S - 1) > 0 ? t - (S - 1) : 0, p1 = t < S - 1 ? t : S - 1;
+    const int64_t K = static_cast<int64_t>(p1 - p0 + 1) * kp;
+    const int8_t* mat1 = DB + static_cast<int64_t>(S - 1 - t + p0) * kp * np;  // n x K, ld np
+    const int8_t* mat2 = DA + static_cast<int64_t>(p0) * kp;                   // K x m, ld S kp
+    int32_t* out = G + static_cast<int64_t>(t) * m * n;                        // n x m, ld n
+    Layouts l;
+    if (hipblasLtMatrixLayoutCreate(&l.a, HIP_R_8I, n, K, np) != HIPBLAS_STATUS_SUCCESS ||
+        hipblasLtMatrixLayoutCreate(&l.b, HIP_R_8I, K, m, static_cast<int64_t>(S) * kp) != HIPBLAS_STATUS_SUCCESS ||
+        hipblasLtMatrixLayoutCreate(&l.d, HIP_R_32I, n, m, n) != HIPBLAS_STATUS_SUCCESS)
+      return hipErrorInvalidValue;
+    const std::array<int64_t, 5> key{n, m, K, np, static_cast<int64_t>(S) * kp};
+    auto it = b->algos.find(key);
+    if (it == b->algos.end()) {
+      hipblasLtMatmulHeuristicResult_t res;
+      int nres = 0;
+      if (hipblasLtMatmulAlgoGetHeuristic(b->handle, b->desc, l.a, l.b, l.d, l.d, b->pref, 1, &res, &nres) !=
+              HIPBLAS_STATUS_SUCCESS ||
+          nres < 1)
+        return hipErrorNotSupported;
+      it = b->algos.emplace(key, res.algo).first;
+    }
+    if (hipblasLtMatmul(b->handle, b->desc, &alpha, mat1, l.a, mat2, l.b, &beta, out, l.d, out, l.d, &it->second,
+                        nullptr, 0, stream) != HIPBLAS_STATUS_SUCCESS)
+      return hipErrorLaunchFailure;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mdg

@@ -262,6 +262,45 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
   }
 }
 
+// Digit layouts of the int8 level products (digits of at most 7 bits):
+//   axis 0 (A, rows = m lines, cols = k):  D [m][S][kp],  D[i][s][kk] = digit s of A[i][kk]
+//   axis 1 (B, rows = k, cols = n lines):  D [S][kp][np], D[S-1-q][kk][j] = digit q of B[kk][j]
+// B's digits in reverse order, so that the pairs (p, t - p) of a level, p
+// ascending, are one contiguous k range of A's row and of B's column:
+// the level is a single int8 GEMM.  Zeros in the padding (kk >= k, j >= n).
+// One thread per element of the padded grid [rows_p][cols_p], consecutive
+// threads on consecutive columns: limb loads and digit stores are contiguous.
+template <int NW, int ML>
+__global__ void __launch_bounds__(256) split_int8_kernel(int64_t rows, int64_t cols, int64_t rows_p, int64_t cols_p,
+                                                         int L, int S, int w, int axis, int64_t kp,
+                                                         const double* __restrict__ X,
+                                                         const int32_t* __restrict__ E, int8_t* __restrict__ D) {
+  const int64_t plane = rows * cols;
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (c >= cols_p) return;
+  for (int64_t r = blockIdx.y; r < rows_p; r += gridDim.y) {
+    int8_t* out;
+    int64_t stride;
+    if (axis == 0) {
+      out = D + r * S * kp + c;
+      stride = kp;
+    } else {
+      out = D + static_cast<int64_t>(S - 1) * kp * cols_p + r * cols_p + c;
+      stride = -kp * cols_p;
+    }
+    if (r < rows && c < cols) {
+      const int e = axis == 0 ? E[r] : E[c];
+      double xs[ML];
+      load_limbs<ML>(X, plane, L, r * cols + c, xs);
+      uint64_t I[NW];
+      const bool neg = floor_on_grid<NW, ML>(xs, L, e - w * S, I);
+      store_digits<NW, int8_t>(I, S, w, neg, out, stride);
+    } else {
+      for (int q = 0; q < S; ++q) out[static_cast<int64_t>(q) * stride] = 0;
+    }
+  }
+}
+
 template <int NW, int ML>
 hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
                      void* D, bool panel, bool f32, const uint32_t* masks, int C, hipStream_t stream) {
@@ -315,6 +354,24 @@ hipError_t split_words(int words, int64_t rows, int64_t cols, int L, int S, int 
   return hipErrorInvalidValue;
 }
 
+template <int ML>
+hipError_t split_int8_words(int words, int64_t rows, int64_t cols, int64_t rows_p, int64_t cols_p, int L, int S,
+                            int w, int axis, int64_t kp, const double* X, const int32_t* E, int8_t* D,
+                            hipStream_t stream) {
+  const dim3 grid(static_cast<unsigned>((cols_p + 255) / 256), static_cast<unsigned>(rows_p < 65535 ? rows_p : 65535));
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, stream, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D);
+    return hipGetLastError();
+  };
+  // w <= 7 and S <= 64: w S + 52 <= 500 bits, at most 8 words
+  if (words <= 2) return go(split_int8_kernel<2, ML>);
+  if (words <= 3) return go(split_int8_kernel<3, ML>);
+  if (words <= 4) return go(split_int8_kernel<4, ML>);
+  if (words <= 6) return go(split_int8_kernel<6, ML>);
+  if (words <= 8) return go(split_int8_kernel<8, ML>);
+  return hipErrorInvalidValue;
+}
+
 }  // namespace
 
 hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
@@ -328,6 +385,17 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
   if (L <= 4) return split_words<4>(words, rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
   if (L <= 8) return split_words<8>(words, rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
   return split_words<16>(words, rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+}
+
+hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
+                             const int32_t* E, int8_t* D, int64_t kp, int64_t np, hipStream_t stream) {
+  if (w < 1 || w > 7 || S < 1 || S > kMaxSlices) return hipErrorInvalidValue;
+  const int64_t rows_p = axis == 0 ? rows : kp, cols_p = axis == 0 ? kp : np;
+  if (rows_p == 0 || cols_p == 0) return hipSuccess;
+  const int words = (w * S + 52 + 63) / 64;
+  if (L <= 4) return split_int8_words<4>(words, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D, stream);
+  if (L <= 8) return split_int8_words<8>(words, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D, stream);
+  return split_int8_words<16>(words, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D, stream);
 }
 
 }  // namespace mdg

@@ -31,6 +31,7 @@ MDGEMM_SYNC = 2
 MDGEMM_TIME_STAGES = 4
 MDGEMM_KARATSUBA = 8
 MDGEMM_KARATSUBA_MIN_TERMS = 16
+MDGEMM_INT8 = 32
 MDGEMM_SCHEDULE_INFO = 12
 
 MDGEMM_CUTOFF_DEFAULT = -1

@@ -230,6 +230,63 @@ def test_plan_matches_the_oracle_reading_of_the_options(lib):
     assert combos == 6 * 4 * 5 * 2 * 3 * 3
 
 
+def test_int8_plans(lib):
+    I8 = md.MDGEMM_INT8
+    # double-double at k = 4096: 7-bit digits, ceil(104 / 7) = 15, T = 14 (120 pairs);
+    # 15 k 127^2 < 2^31 up to k = 8876, beyond that narrower digits
+    assert md.mdgemm_plan(4096, 4096, 4096, 2, flags=I8) == (7, 15, 14)
+    assert md.mdgemm_plan(64, 64, 8876, 2, flags=I8) == (7, 15, 14)
+    assert md.mdgemm_plan(64, 64, 8877, 2, flags=I8) == (6, 18, 17)
+    assert md.mdgemm_plan(64, 64, 65536, 2, flags=I8) == (5, 21, 20)
+    assert md.mdgemm_plan(64, 64, 64, 8, flags=I8) == (7, 60, 59)
+    assert md.mdgemm_plan(64, 64, 64, 2, flags=I8, slice_bits=4) == (4, 26, 25)
+    assert md.mdgemm_plan(64, 64, 2048, 2, flags=I8, range_bits=60) == (7, 24, 32)
+    E = md.MDGEMM_EINVAL
+    for kw in (dict(slice_bits=8), dict(slice_bits=13), dict(slices=9), dict(flags=I8 | md.MDGEMM_KARATSUBA),
+               dict(flags=I8 | md.MDGEMM_KARATSUBA_MIN_TERMS)):
+        kw.setdefault("flags", I8)
+        with pytest.raises(md.MdgemmError) as ei:
+            md.mdgemm_plan(64, 64, 64, 2, **kw)
+        assert ei.value.status == E, kw
+    with pytest.raises(md.MdgemmError) as ei:  # hexa-double: ceil(832 / 7) = 119 digits > 64
+        md.mdgemm_plan(64, 64, 64, 16, flags=I8)
+    assert ei.value.status == E
+    with pytest.raises(md.MdgemmError) as ei:  # even 1-bit digits overflow int32 sums
+        md.mdgemm_plan(4, 4, 2**31, 1, flags=I8)
+    assert ei.value.status == md.MDGEMM_EEXACT
+    assert _ex(lib, 4, 4, 2**31, 1, flags=I8) == md.MDGEMM_EEXACT
+    # workspace: EA, EB, flag, int8 digits of A and B, int32 levels, 256-byte aligned
+    def al(x):
+        return (x + 255) // 256 * 256
+    m, n, k, S, T = 100, 70, 300, 15, 14
+    kp, np_ = 304, 80
+    want = al(4 * m) + al(4 * n) + al(4) + al(m * S * kp) + al(S * kp * np_) + al(4 * (T + 1) * m * n)
+    assert md.mdgemm_workspace_bytes(m, n, k, 2, flags=I8) == want
+
+
+def test_int8_plans_match_the_oracle_reading(lib):
+    combos = 0
+    for L in (1, 2, 3, 4, 8, 16):
+        for k in (1, 64, 4096, 9000, 2**20):
+            for slice_bits in (0, 3, 7, md.MDGEMM_SLICE_BITS_AUTO):
+                for cutoff in (-1, -2, 5):
+                    for range_bits in (0, 60):
+                        kw = dict(slice_bits=slice_bits, cutoff=cutoff, range_bits=range_bits)
+                        try:
+                            want = exact.plan(L, k, int8=True, **kw)
+                            err = None if want is not None else md.MDGEMM_EEXACT
+                        except ValueError:
+                            want, err = None, md.MDGEMM_EINVAL
+                        if err is None:
+                            assert md.mdgemm_plan(8, 8, k, L, flags=md.MDGEMM_INT8, **kw) == want, (L, k, kw)
+                        else:
+                            with pytest.raises(md.MdgemmError) as ei:
+                                md.mdgemm_plan(8, 8, k, L, flags=md.MDGEMM_INT8, **kw)
+                            assert ei.value.status == err, (L, k, kw)
+                        combos += 1
+    assert combos == 6 * 5 * 4 * 3 * 2
+
+
 def test_range_balancing_plans(lib):
     # D = ceil(range / w) more digits, default cutoff S0 - 1 + 2D
     assert md.mdgemm_plan(64, 64, 2048, 2, range_bits=60) == (13, 13, 17)
