@@ -397,16 +397,17 @@ bool resolved_exact(const Resolved& r, int64_t k) {
 }
 
 // Workspace of the int8 level products: EA | EB | flag | A's digits [m][S][kp] |
-// B's digits [S][kp][np] | int32 levels [T+1][m][n], each aligned to 256 bytes;
-// kp = k and np = n rounded up to 16 (int8 operand columns of whole 16 bytes).
+// B's digits as split [S][kp][np] | B's digits transposed [np][S kp] | int32
+// levels [T+1][m][n], each aligned to 256 bytes; kp = k and np = n rounded up
+// to 16 (int8 operand columns of whole 16 bytes).
 struct LayoutI8 {
-  size_t ea = 0, eb = 0, flag = 0, da = 0, db = 0, g = 0, total = 0;
+  size_t ea = 0, eb = 0, flag = 0, da = 0, db = 0, dbt = 0, g = 0, total = 0;
   int64_t kp = 0, np = 0;
 };
 bool layout_int8(int64_t m, int64_t n, int64_t k, int S, int T, LayoutI8* L) {
   L->kp = (k + 15) / 16 * 16;
   L->np = (n + 15) / 16 * 16;
-  const double approx = (double)S * (double)L->kp * ((double)m + (double)L->np) + 4.0 * (T + 1) * (double)m * (double)n;
+  const double approx = (double)S * (double)L->kp * ((double)m + 2.0 * (double)L->np) + 4.0 * (T + 1) * (double)m * (double)n;
   if (approx > 4.0e18 || m > (int64_t{1} << 31) || n > (int64_t{1} << 31)) return false;
   size_t off = 0;
   L->ea = off;
@@ -418,6 +419,8 @@ bool layout_int8(int64_t m, int64_t n, int64_t k, int S, int T, LayoutI8* L) {
   L->da = off;
   off += align_up(static_cast<size_t>(m) * S * static_cast<size_t>(L->kp));
   L->db = off;
+  off += align_up(static_cast<size_t>(S) * static_cast<size_t>(L->kp) * static_cast<size_t>(L->np));
+  L->dbt = off;
   off += align_up(static_cast<size_t>(S) * static_cast<size_t>(L->kp) * static_cast<size_t>(L->np));
   L->g = off;
   off += align_up(sizeof(int32_t) * static_cast<size_t>(T + 1) * static_cast<size_t>(m) * static_cast<size_t>(n));
@@ -622,6 +625,7 @@ int run_int8(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const 
   int32_t* flag = reinterpret_cast<int32_t*>(ws + L.flag);
   int8_t* DA = reinterpret_cast<int8_t*>(ws + L.da);
   int8_t* DB = reinterpret_cast<int8_t*>(ws + L.db);
+  int8_t* DBt = reinterpret_cast<int8_t*>(ws + L.dbt);
   int32_t* G = reinterpret_cast<int32_t*>(ws + L.g);
   auto enqueue = [&]() -> int {
     if (r.flags & MDGEMM_CHECK_FINITE) MDG_TRY(check_finite(m, n, k, limbs, A, B, flag, s));
@@ -636,8 +640,9 @@ int run_int8(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const 
     if (timed) MDG_TRY(record(1, s));
     MDG_TRY(hip_status(mdg::launch_split_int8(m, k, limbs, r.S, r.w, 0, A, EA, DA, L.kp, L.np, s)));
     MDG_TRY(hip_status(mdg::launch_split_int8(k, n, limbs, r.S, r.w, 1, B, EB, DB, L.kp, L.np, s)));
+    MDG_TRY(hip_status(mdg::launch_transpose_bytes(DB, DBt, static_cast<int64_t>(r.S) * L.kp, L.np, s)));
     if (timed) MDG_TRY(record(2, s));
-    MDG_TRY(hip_status(mdg::launch_levels_int8(m, n, L.kp, L.np, r.S, r.T, DA, DB, G, s)));
+    MDG_TRY(hip_status(mdg::launch_levels_int8(m, n, L.kp, L.np, r.S, r.T, DA, DBt, G, s)));
     if (timed) MDG_TRY(record(3, s));
     MDG_TRY(hip_status(mdg::launch_accum_renorm_i32(m, n, limbs, r.T + 1, r.w, G, EA, EB, C, s)));
     if (timed) {

@@ -68,11 +68,16 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
 hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
                              const int32_t* E, int8_t* D, int64_t kp, int64_t np, hipStream_t stream);
 
-// a3 on the int8 matrix cores: levels t = 0..T of the layouts of
-// launch_split_int8 into int32 planes G [T+1][m][n], one hipBLASLt GEMM per
-// level; every level sum must stay below 2^31 (checked by the caller).
+// dst [C][R] = transpose of the byte matrix src [R][C]; R and C multiples of 16.
+hipError_t launch_transpose_bytes(const int8_t* src, int8_t* dst, int64_t R, int64_t C, hipStream_t stream);
+
+// a3 on the int8 matrix cores: levels t = 0..T into int32 planes G [T+1][m][n],
+// one hipBLASLt GEMM per level, from A's digits DA [m][S][kp] (launch_split_int8,
+// axis 0) and B's digits DBt [np][S kp], the transpose of launch_split_int8's
+// axis-1 layout (column j: digit q in k range (S-1-q) kp ..); every level sum
+// must stay below 2^31 (checked by the caller).
 hipError_t launch_levels_int8(int64_t m, int64_t n, int64_t kp, int64_t np, int S, int T, const int8_t* DA,
-                              const int8_t* DB, int32_t* G, hipStream_t stream);
+                              const int8_t* DBt, int32_t* G, hipStream_t stream);
 
 // a3: products of the combination panels DAt [*][panel_k(k)][panel_mn(m)] and
 // DBp [*][panel_k(k)][panel_mn(n)] (combinations 0..S-1 are the digits); one

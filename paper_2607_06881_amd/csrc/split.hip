@@ -354,6 +354,35 @@ hipError_t split_words(int words, int64_t rows, int64_t cols, int L, int S, int 
   return hipErrorInvalidValue;
 }
 
+// dst [C][R] = transpose of src [R][C] (bytes; R and C multiples of 16).  A block
+// moves a 64 x 64 tile through LDS: 16-byte rows in, 16-byte columns out.
+__global__ void __launch_bounds__(256) transpose_bytes_kernel(int64_t R, int64_t C, const int8_t* __restrict__ src,
+                                                              int8_t* __restrict__ dst) {
+  __shared__ int8_t tile[64][68];
+  const int t = threadIdx.x, a = t >> 2, q = t & 3;
+  for (int64_t ty = blockIdx.y; ty * 64 < C; ty += gridDim.y) {
+    for (int64_t tx = blockIdx.x; tx * 64 < R; tx += gridDim.x) {
+      const int64_t r0 = tx * 64, c0 = ty * 64;
+      // in: row r0 + a, columns c0 + 16q .. + 15
+      int4 v = make_int4(0, 0, 0, 0);
+      if (r0 + a < R && c0 + 16 * q < C) v = *reinterpret_cast<const int4*>(src + (r0 + a) * C + c0 + 16 * q);
+      const int8_t* vb = reinterpret_cast<const int8_t*>(&v);
+#pragma unroll
+      for (int b = 0; b < 16; ++b) tile[a][16 * q + b] = vb[b];
+      __syncthreads();
+      // out: row c0 + a of dst, columns r0 + 16q .. + 15
+      if (c0 + a < C && r0 + 16 * q < R) {
+        int4 o;
+        int8_t* ob = reinterpret_cast<int8_t*>(&o);
+#pragma unroll
+        for (int b = 0; b < 16; ++b) ob[b] = tile[16 * q + b][a];
+        *reinterpret_cast<int4*>(dst + (c0 + a) * R + r0 + 16 * q) = o;
+      }
+      __syncthreads();
+    }
+  }
+}
+
 template <int ML>
 hipError_t split_int8_words(int words, int64_t rows, int64_t cols, int64_t rows_p, int64_t cols_p, int L, int S,
                             int w, int axis, int64_t kp, const double* X, const int32_t* E, int8_t* D,
@@ -396,6 +425,16 @@ hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, in
   if (L <= 4) return split_int8_words<4>(words, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D, stream);
   if (L <= 8) return split_int8_words<8>(words, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D, stream);
   return split_int8_words<16>(words, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D, stream);
+}
+
+hipError_t launch_transpose_bytes(const int8_t* src, int8_t* dst, int64_t R, int64_t C, hipStream_t stream) {
+  if (R == 0 || C == 0) return hipSuccess;
+  if (R % 16 != 0 || C % 16 != 0) return hipErrorInvalidValue;
+  const int64_t gx = (R + 63) / 64, gy = (C + 63) / 64;
+  const dim3 grid(static_cast<unsigned>(gx < (int64_t{1} << 30) ? gx : (int64_t{1} << 30)),
+                  static_cast<unsigned>(gy < 65535 ? gy : 65535));
+  hipLaunchKernelGGL(transpose_bytes_kernel, grid, dim3(256), 0, stream, R, C, src, dst);
+  return hipGetLastError();
 }
 
 }  // namespace mdg
