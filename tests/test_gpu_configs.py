@@ -196,3 +196,34 @@ def test_workload_karatsuba(name):
     ref = pipeline.reference_entries(A_h, B_h, w.slices, w.cutoff, entries)
     for (i, j), r in ref.items():
         assert C_h[:, i, j].tolist() == r["limbs"], (i, j)
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5", "c7"])
+def test_workload_int8(name):
+    # The same workloads with the int8 level products (7-bit digits, exact int32
+    # sums): sampled entries bit-exact against the oracle's chain at that width
+    # and within the stated tolerance, and the whole C bit-identical to the FP64
+    # path run with the same digits (hexa-double needs more than 64 digits of
+    # 7 bits and is refused).
+    w = workloads.WORKLOADS[name]
+    rb = {"range_bits": w.range_bits} if w.range_bits else {}
+    bits, S, T = md.mdgemm_plan(w.m, w.n, w.k, w.limbs, flags=md.MDGEMM_INT8, **rb)
+    assert (bits, S, T) == exact.plan(w.limbs, w.k, int8=True, **rb)
+    print(f"[case] workload {name} int8: w={bits} S={S} T={T}", flush=True)
+    A_h, B_h = workloads.make_workload(w)
+    A, B = torch.from_numpy(A_h).to(DEV), torch.from_numpy(B_h).to(DEV)
+    C8 = md.mdgemm_ex(A, B, flags=md.MDGEMM_INT8, **rb).cpu().numpy()
+    torch.cuda.empty_cache()
+    D = -(-w.range_bits // bits) if w.range_bits else 0
+    C64 = md.mdgemm_ex(A, B, slice_bits=bits, slices=S - D, cutoff=T, **rb).cpu().numpy()
+    torch.cuda.empty_cache()
+    assert np.array_equal(C8, C64)
+    assert _nonoverlap_all(C8) and np.isfinite(C8).all()
+    EA, EB = coracle.exponents(A_h[0], 0), coracle.exponents(B_h[0], 1)
+    entries = _sample_entries(EA, EB, 12, w.seed + 95)
+    ref = pipeline.reference_entries(A_h, B_h, S, T, entries, bits)
+    for (i, j), r in ref.items():
+        assert C8[:, i, j].tolist() == r["limbs"], (i, j)
+        if w.limbs <= 4:
+            want, mag = exact.exact_product(A_h, B_h, i, j)
+            assert abs(exact.value(C8[:, i, j]) - want) <= exact.tolerance(w.k, w.limbs, mag), (i, j)
