@@ -26,7 +26,8 @@ Prints one JSON line:
 * ``int8``: the same workload with the level products on the int8 matrix
   cores (MDGEMM_INT8: digits of at most 7 bits, one int8 GEMM with exact int32
   sums per level, the same exact accumulation), its level GEMMs against the
-  5.0 POP/s dense int8 peak;
+  5.0 POP/s dense int8 peak (``--products int8`` times that mode as the main
+  line instead, its roofline against the int8 peak);
 * ``cpu_baseline``: the CPU oracle's classic multiple-double GEMM (one
   sequential inner product per element, all host cores) timed on a bounded
   sample of the same product's rows.
@@ -130,6 +131,9 @@ def main(argv=None) -> int:
     ap.add_argument("--adaptive-steps", type=int, default=5,
                     help="steps of each extra measurement (adaptive width, Karatsuba schedule) reported beside "
                          "the headline (0: none)")
+    ap.add_argument("--products", choices=("fp64", "int8"), default="fp64",
+                    help="level products on the FP64 matrix cores (the paper's, default) or on the int8 "
+                         "matrix cores (MDGEMM_INT8, 7-bit digits)")
     ap.add_argument("--schedule", choices=("pairs", "karatsuba"), default="pairs",
                     help="schedule of the level products of the timed product: the paper's digit pairs (default) "
                          "or the Karatsuba schedule")
@@ -141,6 +145,9 @@ def main(argv=None) -> int:
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only (the product has no multi-GPU path); use --gpus 1",
               file=sys.stderr)
+        return 2
+    if args.products == "int8" and (args.schedule != "pairs" or args.slice_bits != "13"):
+        print("bench.py: --products int8 takes its own digit width and the pair schedule", file=sys.stderr)
         return 2
 
     import numpy as np
@@ -195,7 +202,10 @@ def main(argv=None) -> int:
 
     bits_arg = md.MDGEMM_SLICE_BITS_AUTO if args.slice_bits == "auto" else int(args.slice_bits)
     sched_flags = md.MDGEMM_KARATSUBA if args.schedule == "karatsuba" else 0
-    opts = mode_opts(bits_arg)
+    int8 = args.products == "int8"
+    if int8:
+        sched_flags = md.MDGEMM_INT8
+    opts = {"range_bits": w.range_bits} if int8 and w.range_bits else ({} if int8 else mode_opts(bits_arg))
     bits, S, T = md.mdgemm_plan(w.m, w.n, w.k, w.limbs, flags=sched_flags, **opts)
     ms_per_step, stage_ms = measure(opts, args.steps, args.warmup, sched_flags)
 
@@ -209,7 +219,7 @@ def main(argv=None) -> int:
 
     m, n, k, L = w.m, w.n, w.k, w.limbs
     pairs = workloads.pair_count(S, T)
-    info = md.mdgemm_schedule_info(m, n, k, S, T, bits=bits, flags=sched_flags)
+    info = md.mdgemm_schedule_info(m, n, k, S, T, bits=bits, flags=0 if int8 else sched_flags)
     panels_f32 = bool(info["panels_f32"])  # digit panels kept in FP32 (every digit sum below 2^24)
     md_flops = w.md_flops()
     # the GEMMs actually run: one per digit pair, or the Karatsuba schedule's products
@@ -224,6 +234,10 @@ def main(argv=None) -> int:
     bytes_acc = 8.0 * info["planes"] * m * n + 8.0 * L * m * n + 4.0 * (m + n)
     gemm_ms = stage_ms[2]
     achieved = slice_flops / (gemm_ms * 1e-3) / 1e12
+    if int8:
+        # int8 digits (1 byte), B's also transposed once; int32 level planes
+        bytes_split = 8.0 * L * (m * k + k * n) + S * (m * k + 3.0 * k * n) + 4.0 * (m + n)
+        bytes_acc = 4.0 * info["planes"] * m * n + 8.0 * L * m * n + 4.0 * (m + n)
     roofline = {
         "bound": "mfma",
         "achieved": round(achieved, 3),
@@ -237,25 +251,37 @@ def main(argv=None) -> int:
         "flops_per_launch": slice_flops,
         "avg_launch_ms": round(gemm_ms, 4),
     }
+    if int8:
+        roofline.update({"peak": INT8_PEAK_TOPS, "unit": "TOP/s", "frac": round(achieved / INT8_PEAK_TOPS, 4),
+                         "traffic": None,
+                         "kernel": f"hipBLASLt int8 GEMMs, one per level ({T + 1}), int32 sums; duration of all "
+                                   "of them per step",
+                         "ops_per_step": roofline.pop("flops_per_launch"),
+                         "avg_step_ms": roofline.pop("avg_launch_ms")})
     stages = {
         "exponents": {"ms": round(stage_ms[0], 4), "GB/s": round(bytes_exp / (stage_ms[0] * 1e-3) / 1e9, 1),
                       "bytes": bytes_exp},
         "split": {"ms": round(stage_ms[1], 4), "GB/s": round(bytes_split / (stage_ms[1] * 1e-3) / 1e9, 1),
                   "bytes": bytes_split},
-        "slice_gemm": {"ms": round(stage_ms[2], 4), "TFLOP/s": round(achieved, 3)},
+        "slice_gemm": {"ms": round(stage_ms[2], 4), ("TOP/s" if int8 else "TFLOP/s"): round(achieved, 3)},
         "accum_renorm": {"ms": round(stage_ms[3], 4), "GB/s": round(bytes_acc / (stage_ms[3] * 1e-3) / 1e9, 1),
                          "bytes": bytes_acc},
         "hbm_peak_GB/s": HBM_PEAK_GBS,
     }
     config = {"workload": f"{w.name}: {w.description}", "m": m, "n": n, "k": k, "limbs": L, "slices": S,
               "cutoff": T, "pairs": pairs, "seed": w.seed, "panels": "f32" if panels_f32 else "f64"}
-    if sched_flags:
+    if sched_flags and not int8:
         config["schedule"] = "karatsuba"
         config["products"] = info["terms"]
         config["workload"] += f"; Karatsuba schedule: {info['terms']} digit-sum products for the {pairs} pairs"
     if w.range_bits:
         config["range_bits"] = w.range_bits
-    if bits != 13:
+    if int8:
+        config["products"] = "int8"
+        config["slice_bits"] = bits
+        config["panels"] = "int8"
+        config["workload"] += f"; int8 level products: {S} digits of {bits} bits, pairs p+q <= {T}"
+    elif bits != 13:
         config["slice_bits"] = bits
         config["workload"] += f"; adaptive width: {S} digits of {bits} bits, pairs p+q <= {T}"
     out = {
@@ -269,7 +295,7 @@ def main(argv=None) -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f64",
+        "dtype": "int8" if int8 else "f64",
         "data": "synthetic",
         "config": config,
         "roofline": roofline,
