@@ -397,17 +397,16 @@ bool resolved_exact(const Resolved& r, int64_t k) {
 }
 
 // Workspace of the int8 level products: EA | EB | flag | A's digits [m][S][kp] |
-// B's digits as split [S][kp][np] | B's digits transposed [np][S kp] | int32
-// levels [T+1][m][n], each aligned to 256 bytes; kp = k and np = n rounded up
-// to 16 (int8 operand columns of whole 16 bytes).
+// B's digits [np][S kp] | int32 levels [T+1][m][n], each aligned to 256 bytes;
+// kp = k and np = n rounded up to 16 (int8 operand columns of whole 16 bytes).
 struct LayoutI8 {
-  size_t ea = 0, eb = 0, flag = 0, da = 0, db = 0, dbt = 0, g = 0, total = 0;
+  size_t ea = 0, eb = 0, flag = 0, da = 0, dbt = 0, g = 0, total = 0;
   int64_t kp = 0, np = 0;
 };
 bool layout_int8(int64_t m, int64_t n, int64_t k, int S, int T, LayoutI8* L) {
   L->kp = (k + 15) / 16 * 16;
   L->np = (n + 15) / 16 * 16;
-  const double approx = (double)S * (double)L->kp * ((double)m + 2.0 * (double)L->np) + 4.0 * (T + 1) * (double)m * (double)n;
+  const double approx = (double)S * (double)L->kp * ((double)m + (double)L->np) + 4.0 * (T + 1) * (double)m * (double)n;
   if (approx > 4.0e18 || m > (int64_t{1} << 31) || n > (int64_t{1} << 31)) return false;
   size_t off = 0;
   L->ea = off;
@@ -418,8 +417,6 @@ bool layout_int8(int64_t m, int64_t n, int64_t k, int S, int T, LayoutI8* L) {
   off += align_up(sizeof(int32_t));
   L->da = off;
   off += align_up(static_cast<size_t>(m) * S * static_cast<size_t>(L->kp));
-  L->db = off;
-  off += align_up(static_cast<size_t>(S) * static_cast<size_t>(L->kp) * static_cast<size_t>(L->np));
   L->dbt = off;
   off += align_up(static_cast<size_t>(S) * static_cast<size_t>(L->kp) * static_cast<size_t>(L->np));
   L->g = off;
@@ -624,7 +621,6 @@ int run_int8(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const 
   int32_t* EB = reinterpret_cast<int32_t*>(ws + L.eb);
   int32_t* flag = reinterpret_cast<int32_t*>(ws + L.flag);
   int8_t* DA = reinterpret_cast<int8_t*>(ws + L.da);
-  int8_t* DB = reinterpret_cast<int8_t*>(ws + L.db);
   int8_t* DBt = reinterpret_cast<int8_t*>(ws + L.dbt);
   int32_t* G = reinterpret_cast<int32_t*>(ws + L.g);
   auto enqueue = [&]() -> int {
@@ -638,9 +634,8 @@ int run_int8(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const 
     MDG_TRY(hip_status(mdg::launch_exponents(m, k, 0, A, EA, s)));
     MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, EB, s)));
     if (timed) MDG_TRY(record(1, s));
-    MDG_TRY(hip_status(mdg::launch_split_int8(m, k, limbs, r.S, r.w, 0, A, EA, DA, L.kp, L.np, s)));
-    MDG_TRY(hip_status(mdg::launch_split_int8(k, n, limbs, r.S, r.w, 1, B, EB, DB, L.kp, L.np, s)));
-    MDG_TRY(hip_status(mdg::launch_transpose_bytes(DB, DBt, static_cast<int64_t>(r.S) * L.kp, L.np, s)));
+    MDG_TRY(hip_status(mdg::launch_split_int8(m, k, limbs, r.S, r.w, A, EA, DA, L.kp, s)));
+    MDG_TRY(hip_status(mdg::launch_split_int8t(k, n, limbs, r.S, r.w, B, EB, DBt, L.kp, L.np, s)));
     if (timed) MDG_TRY(record(2, s));
     MDG_TRY(hip_status(mdg::launch_levels_int8(m, n, L.kp, L.np, r.S, r.T, DA, DBt, G, s)));
     if (timed) MDG_TRY(record(3, s));

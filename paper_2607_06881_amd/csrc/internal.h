@@ -62,20 +62,21 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
                         void* D, bool panel, hipStream_t stream, const uint32_t* masks = nullptr,
                         int combos = 0, bool f32 = false);
 
-// a2 for the int8 level products: digits of at most 7 bits as int8, A (axis 0,
-// rows = m, cols = k) as D [m][S][kp], B (axis 1, rows = k, cols = n) as
-// D [S][kp][np] with digit q in plane S-1-q; zeros in the padding.
-hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
-                             const int32_t* E, int8_t* D, int64_t kp, int64_t np, hipStream_t stream);
+// a2 for the int8 level products: A's digits (at most 7 bits) as int8,
+// D [m][S][kp] (rows = m, cols = k), zeros for kk >= k.
+hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,
+                             int8_t* D, int64_t kp, hipStream_t stream);
 
-// dst [C][R] = transpose of the byte matrix src [R][C]; R and C multiples of 16.
-hipError_t launch_transpose_bytes(const int8_t* src, int8_t* dst, int64_t R, int64_t C, hipStream_t stream);
+// a2 for the int8 level products, B (rows = k, cols = n) straight into the
+// k-contiguous layout Dt [np][S kp]: Dt[j][(S-1-q) kp + kk] = digit q of B[kk][j].
+hipError_t launch_split_int8t(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,
+                              int8_t* Dt, int64_t kp, int64_t np, hipStream_t stream);
 
 // a3 on the int8 matrix cores: levels t = 0..T into int32 planes G [T+1][m][n],
 // one hipBLASLt GEMM per level, from A's digits DA [m][S][kp] (launch_split_int8,
-// axis 0) and B's digits DBt [np][S kp], the transpose of launch_split_int8's
-// axis-1 layout (column j: digit q in k range (S-1-q) kp ..); every level sum
-// must stay below 2^31 (checked by the caller).
+// axis 0) and B's digits DBt [np][S kp] (launch_split_int8t: column j, digit q
+// in k range (S-1-q) kp ..); every level sum must stay below 2^31 (checked by
+// the caller).
 hipError_t launch_levels_int8(int64_t m, int64_t n, int64_t kp, int64_t np, int S, int T, const int8_t* DA,
                               const int8_t* DBt, int32_t* G, hipStream_t stream);
 

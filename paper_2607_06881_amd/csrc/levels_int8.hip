@@ -9,7 +9,7 @@
 //
 // Layouts: A's digits D_A [m][S][kp] (launch_split_int8), B's digits D_Bt
 // [np][S kp] with digit q of column j at k range (S-1-q) kp .. (reverse order;
-// the transpose of the split's coalesced [S][kp][np]).  The pairs (p, t - p) of
+// launch_split_int8t).  The pairs (p, t - p) of
 // level t, p = p0 .. p1, are then the contiguous k range of length
 // K = (p1 - p0 + 1) kp starting at p0 kp in every row of D_A and at
 // (S-1-t+p0) kp in every column of D_Bt, so a level is one plain GEMM with

@@ -262,41 +262,62 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
   }
 }
 
-// Digit layouts of the int8 level products (digits of at most 7 bits):
-//   axis 0 (A, rows = m lines, cols = k):  D [m][S][kp],  D[i][s][kk] = digit s of A[i][kk]
-//   axis 1 (B, rows = k, cols = n lines):  D [S][kp][np], D[S-1-q][kk][j] = digit q of B[kk][j]
-// B's digits in reverse order, so that the pairs (p, t - p) of a level, p
-// ascending, are one contiguous k range of A's row and of B's column:
-// the level is a single int8 GEMM.  Zeros in the padding (kk >= k, j >= n).
-// One thread per element of the padded grid [rows_p][cols_p], consecutive
-// threads on consecutive columns: limb loads and digit stores are contiguous.
+// A's digits for the int8 level products (digits of at most 7 bits): D [m][S][kp],
+// D[i][s][kk] = digit s of A[i][kk], zeros for kk >= k.  A level's pairs
+// (p, t - p), p ascending, are then one contiguous k range of every row.  One
+// thread per element of the padded grid [m][kp], consecutive threads on
+// consecutive kk: limb loads and digit stores of a wave are contiguous.
 template <int NW, int ML>
-__global__ void __launch_bounds__(256) split_int8_kernel(int64_t rows, int64_t cols, int64_t rows_p, int64_t cols_p,
-                                                         int L, int S, int w, int axis, int64_t kp,
+__global__ void __launch_bounds__(256) split_int8_kernel(int64_t rows, int64_t cols, int64_t kp, int L, int S, int w,
                                                          const double* __restrict__ X,
                                                          const int32_t* __restrict__ E, int8_t* __restrict__ D) {
   const int64_t plane = rows * cols;
   const int64_t c = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (c >= cols_p) return;
-  for (int64_t r = blockIdx.y; r < rows_p; r += gridDim.y) {
-    int8_t* out;
-    int64_t stride;
-    if (axis == 0) {
-      out = D + r * S * kp + c;
-      stride = kp;
-    } else {
-      out = D + static_cast<int64_t>(S - 1) * kp * cols_p + r * cols_p + c;
-      stride = -kp * cols_p;
-    }
-    if (r < rows && c < cols) {
-      const int e = axis == 0 ? E[r] : E[c];
+  if (c >= kp) return;
+  for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
+    int8_t* out = D + r * S * kp + c;
+    if (c < cols) {
       double xs[ML];
       load_limbs<ML>(X, plane, L, r * cols + c, xs);
       uint64_t I[NW];
-      const bool neg = floor_on_grid<NW, ML>(xs, L, e - w * S, I);
-      store_digits<NW, int8_t>(I, S, w, neg, out, stride);
+      const bool neg = floor_on_grid<NW, ML>(xs, L, E[r] - w * S, I);
+      store_digits<NW, int8_t>(I, S, w, neg, out, kp);
     } else {
-      for (int q = 0; q < S; ++q) out[static_cast<int64_t>(q) * stride] = 0;
+      for (int q = 0; q < S; ++q) out[static_cast<int64_t>(q) * kp] = 0;
+    }
+  }
+}
+
+// B's int8 digits straight into the k-contiguous layout of the int8 level
+// GEMMs: Dt [np][S kp], Dt[j][(S-1-q) kp + kk] = digit q of B[kk][j], zeros in
+// the padding.  Lanes take consecutive kk, so every digit store of a wave is 64
+// contiguous bytes; a block covers 64 kk x 16 columns (each wave 4 columns), so
+// the 16 consecutive doubles of a row of B that one 128-byte line holds are all
+// read by the same block.
+template <int NW, int ML>
+__global__ void __launch_bounds__(256) split_int8t_kernel(int64_t rows, int64_t cols, int64_t kp, int64_t np, int L,
+                                                          int S, int w, const double* __restrict__ X,
+                                                          const int32_t* __restrict__ E, int8_t* __restrict__ Dt) {
+  const int64_t plane = rows * cols;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t ld = static_cast<int64_t>(S) * kp;
+  for (int64_t by = blockIdx.y; by * 16 < np; by += gridDim.y) {
+    const int64_t kk = static_cast<int64_t>(blockIdx.x) * 64 + lane;
+    if (kk >= kp) continue;
+#pragma unroll 1
+    for (int r = 0; r < 4; ++r) {
+      const int64_t j = by * 16 + 4 * wave + r;
+      if (j >= np) break;
+      int8_t* out = Dt + j * ld + static_cast<int64_t>(S - 1) * kp + kk;
+      if (kk < rows && j < cols) {
+        double xs[ML];
+        load_limbs<ML>(X, plane, L, kk * cols + j, xs);
+        uint64_t I[NW];
+        const bool neg = floor_on_grid<NW, ML>(xs, L, E[j] - w * S, I);
+        store_digits<NW, int8_t>(I, S, w, neg, out, -kp);
+      } else {
+        for (int q = 0; q < S; ++q) out[-static_cast<int64_t>(q) * kp] = 0;
+      }
     }
   }
 }
@@ -354,42 +375,29 @@ hipError_t split_words(int words, int64_t rows, int64_t cols, int L, int S, int 
   return hipErrorInvalidValue;
 }
 
-// dst [C][R] = transpose of src [R][C] (bytes; R and C multiples of 16).  A block
-// moves a 64 x 64 tile through LDS: 16-byte rows in, 16-byte columns out.
-__global__ void __launch_bounds__(256) transpose_bytes_kernel(int64_t R, int64_t C, const int8_t* __restrict__ src,
-                                                              int8_t* __restrict__ dst) {
-  __shared__ int8_t tile[64][68];
-  const int t = threadIdx.x, a = t >> 2, q = t & 3;
-  for (int64_t ty = blockIdx.y; ty * 64 < C; ty += gridDim.y) {
-    for (int64_t tx = blockIdx.x; tx * 64 < R; tx += gridDim.x) {
-      const int64_t r0 = tx * 64, c0 = ty * 64;
-      // in: row r0 + a, columns c0 + 16q .. + 15
-      int4 v = make_int4(0, 0, 0, 0);
-      if (r0 + a < R && c0 + 16 * q < C) v = *reinterpret_cast<const int4*>(src + (r0 + a) * C + c0 + 16 * q);
-      const int8_t* vb = reinterpret_cast<const int8_t*>(&v);
-#pragma unroll
-      for (int b = 0; b < 16; ++b) tile[a][16 * q + b] = vb[b];
-      __syncthreads();
-      // out: row c0 + a of dst, columns r0 + 16q .. + 15
-      if (c0 + a < C && r0 + 16 * q < R) {
-        int4 o;
-        int8_t* ob = reinterpret_cast<int8_t*>(&o);
-#pragma unroll
-        for (int b = 0; b < 16; ++b) ob[b] = tile[16 * q + b][a];
-        *reinterpret_cast<int4*>(dst + (c0 + a) * R + r0 + 16 * q) = o;
-      }
-      __syncthreads();
-    }
-  }
+template <int ML>
+hipError_t split_int8t_words(int words, int64_t rows, int64_t cols, int64_t kp, int64_t np, int L, int S, int w,
+                             const double* X, const int32_t* E, int8_t* Dt, hipStream_t stream) {
+  const int64_t gy = (np + 15) / 16;
+  const dim3 grid(static_cast<unsigned>((kp + 63) / 64), static_cast<unsigned>(gy < 65535 ? gy : 65535));
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, stream, rows, cols, kp, np, L, S, w, X, E, Dt);
+    return hipGetLastError();
+  };
+  if (words <= 2) return go(split_int8t_kernel<2, ML>);
+  if (words <= 3) return go(split_int8t_kernel<3, ML>);
+  if (words <= 4) return go(split_int8t_kernel<4, ML>);
+  if (words <= 6) return go(split_int8t_kernel<6, ML>);
+  if (words <= 8) return go(split_int8t_kernel<8, ML>);
+  return hipErrorInvalidValue;
 }
 
 template <int ML>
-hipError_t split_int8_words(int words, int64_t rows, int64_t cols, int64_t rows_p, int64_t cols_p, int L, int S,
-                            int w, int axis, int64_t kp, const double* X, const int32_t* E, int8_t* D,
-                            hipStream_t stream) {
-  const dim3 grid(static_cast<unsigned>((cols_p + 255) / 256), static_cast<unsigned>(rows_p < 65535 ? rows_p : 65535));
+hipError_t split_int8_words(int words, int64_t rows, int64_t cols, int64_t kp, int L, int S, int w, const double* X,
+                            const int32_t* E, int8_t* D, hipStream_t stream) {
+  const dim3 grid(static_cast<unsigned>((kp + 255) / 256), static_cast<unsigned>(rows < 65535 ? rows : 65535));
   auto go = [&](auto kernel) {
-    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, stream, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D);
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, stream, rows, cols, kp, L, S, w, X, E, D);
     return hipGetLastError();
   };
   // w <= 7 and S <= 64: w S + 52 <= 500 bits, at most 8 words
@@ -416,25 +424,24 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
   return split_words<16>(words, rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
 }
 
-hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
-                             const int32_t* E, int8_t* D, int64_t kp, int64_t np, hipStream_t stream) {
-  if (w < 1 || w > 7 || S < 1 || S > kMaxSlices) return hipErrorInvalidValue;
-  const int64_t rows_p = axis == 0 ? rows : kp, cols_p = axis == 0 ? kp : np;
-  if (rows_p == 0 || cols_p == 0) return hipSuccess;
+hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,
+                             int8_t* D, int64_t kp, hipStream_t stream) {
+  if (w < 1 || w > 7 || S < 1 || S > kMaxSlices || kp < cols) return hipErrorInvalidValue;
+  if (rows == 0 || kp == 0) return hipSuccess;
   const int words = (w * S + 52 + 63) / 64;
-  if (L <= 4) return split_int8_words<4>(words, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D, stream);
-  if (L <= 8) return split_int8_words<8>(words, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D, stream);
-  return split_int8_words<16>(words, rows, cols, rows_p, cols_p, L, S, w, axis, kp, X, E, D, stream);
+  if (L <= 4) return split_int8_words<4>(words, rows, cols, kp, L, S, w, X, E, D, stream);
+  if (L <= 8) return split_int8_words<8>(words, rows, cols, kp, L, S, w, X, E, D, stream);
+  return split_int8_words<16>(words, rows, cols, kp, L, S, w, X, E, D, stream);
 }
 
-hipError_t launch_transpose_bytes(const int8_t* src, int8_t* dst, int64_t R, int64_t C, hipStream_t stream) {
-  if (R == 0 || C == 0) return hipSuccess;
-  if (R % 16 != 0 || C % 16 != 0) return hipErrorInvalidValue;
-  const int64_t gx = (R + 63) / 64, gy = (C + 63) / 64;
-  const dim3 grid(static_cast<unsigned>(gx < (int64_t{1} << 30) ? gx : (int64_t{1} << 30)),
-                  static_cast<unsigned>(gy < 65535 ? gy : 65535));
-  hipLaunchKernelGGL(transpose_bytes_kernel, grid, dim3(256), 0, stream, R, C, src, dst);
-  return hipGetLastError();
+hipError_t launch_split_int8t(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,
+                              int8_t* Dt, int64_t kp, int64_t np, hipStream_t stream) {
+  if (w < 1 || w > 7 || S < 1 || S > kMaxSlices || kp < rows || np < cols) return hipErrorInvalidValue;
+  if (kp == 0 || np == 0) return hipSuccess;
+  const int words = (w * S + 52 + 63) / 64;
+  if (L <= 4) return split_int8t_words<4>(words, rows, cols, kp, np, L, S, w, X, E, Dt, stream);
+  if (L <= 8) return split_int8t_words<8>(words, rows, cols, kp, np, L, S, w, X, E, Dt, stream);
+  return split_int8t_words<16>(words, rows, cols, kp, np, L, S, w, X, E, Dt, stream);
 }
 
 }  // namespace mdg
