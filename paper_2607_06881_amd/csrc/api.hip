@@ -608,6 +608,11 @@ int run_int8(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const 
   LayoutI8 L;
   if (!layout_int8(m, n, k, r.S, r.T, &L)) return MDGEMM_EINVAL;
   hipStream_t s = r.stream;
+  // refused under graph capture: what hipBLASLt records (memset nodes of split-k
+  // forms, for instance) is not under this library's control
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cap) != hipSuccess) return MDGEMM_EHIP;
+  if (cap != hipStreamCaptureStatusNone) return MDGEMM_EINVAL;
   const bool timed = (r.flags & MDGEMM_TIME_STAGES) != 0;
   char* ws = nullptr;
   LibraryBuffer lib;

@@ -130,3 +130,23 @@ def test_int8_workspace_stream_and_stage_times():
         o = md.make_opts(flags=I8)
         assert md.lib().mdgemm_ex(m, n, k, L, Ag.data_ptr(), Bg.data_ptr(), C3.data_ptr(), ctypes.byref(o)) == 0
         assert np.array_equal(_host(C3), want)
+
+
+@pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")  # the refused call leaves the graph empty
+def test_int8_refused_under_graph_capture():
+    print("[case] int8 under graph capture", flush=True)
+    L, m, k, n = 2, 64, 64, 64
+    A, B = _operands(L, m, k, n, 80)
+    Ag, Bg = _gpu(A), _gpu(B)
+    C = torch.empty((L, m, n), dtype=torch.float64, device=DEV)
+    ws = torch.empty(md.mdgemm_workspace_bytes(m, n, k, L, flags=I8), dtype=torch.uint8, device=DEV)
+    s = torch.cuda.Stream()
+    o = md.make_opts(flags=I8, stream=s, workspace=ws)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        st = md.lib().mdgemm_ex(m, n, k, L, Ag.data_ptr(), Bg.data_ptr(), C.data_ptr(), ctypes.byref(o))
+    assert st == md.MDGEMM_EINVAL
+    # outside capture the same call works
+    want = _host(md.mdgemm_ex(Ag, Bg, flags=I8))
+    assert np.array_equal(want, pipeline.full_reference(A, B, 15, 14, 7)["C"])
