@@ -9,22 +9,23 @@
 //
 // Layouts: A's digits D_A [m][S][kp] (launch_split_int8), B's digits D_Bt
 // [np][S kp] with digit q of column j at k range (S-1-q) kp .. (reverse order;
-// launch_split_int8t).  The pairs (p, t - p) of
-// level t, p = p0 .. p1, are then the contiguous k range of length
-// K = (p1 - p0 + 1) kp starting at p0 kp in every row of D_A and at
-// (S-1-t+p0) kp in every column of D_Bt, so a level is one plain GEMM with
-// both operands k-contiguous (column-major, the first one transposed):
+// launch_split_int8t).  The pairs (p, t - p) of level t, p = p0 .. p1, are then
+// the contiguous k range of length K = (p1 - p0 + 1) kp starting at p0 kp in
+// every row of D_A and at (S-1-t+p0) kp in every column of D_Bt, so a level is
+// one plain GEMM with both operands k-contiguous (column-major, the first one
+// transposed):
 //     G_t^T (n x m, ld n) = op_T(D_Bt + (S-1-t+p0) kp: K x n, ld S kp) . (D_A + p0 kp: K x m, ld S kp)
 // G_t^T in column-major is the row-major plane G_t [m][n] that the
 // accumulation reads.  (With both operands k-contiguous hipBLASLt's int8 GEMMs
 // ran at 2.2-2.8 POP/s on MI355X at these shapes, against 1.8-2.4 with B's
-// digits n-contiguous.)  Each level is one hipBLASLt int8
-// GEMM; the handle, the operation descriptor and the algorithm per shape are
-// created once per device and kept.  The algorithm of a shape is chosen on its
-// first call: hipBLASLt's candidates (up to 8) are each timed on the call's
-// stream (two runs into the level's own output plane, which the chosen one
-// then overwrites) and the fastest is kept; while the stream captures a graph
-// nothing can be timed and the first candidate is taken.
+// digits n-contiguous.)
+//
+// The hipBLASLt handle, the operation descriptor and the algorithm per shape
+// are created once per device and kept.  The algorithm of a shape is chosen on
+// its first call: hipBLASLt's candidates (up to 8) are each timed on the call's
+// stream (two runs into the level's own output plane, which the chosen one then
+// overwrites) and the fastest is kept.  mdgemm_ex refuses int8 calls under graph
+// capture; a capturing stream here would get the first candidate, untimed.
 #include <hipblaslt/hipblaslt.h>
 
 #include <array>
