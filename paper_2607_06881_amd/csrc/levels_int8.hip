@@ -22,7 +22,7 @@
 //
 // The hipBLASLt handle, the operation descriptor and the algorithm per shape
 // are created once per device and kept.  The algorithm of a shape is chosen on
-// its first call: hipBLASLt's candidates (up to 8) are each timed on the call's
+// its first call: hipBLASLt's candidates (up to 32) are each timed on the call's
 // stream (two runs into the level's own output plane, which the chosen one then
 // overwrites) and the fastest is kept.  mdgemm_ex refuses int8 calls under graph
 // capture; a capturing stream here would get the first candidate, untimed.
@@ -125,7 +125,7 @@ hipError_t launch_levels_int8(int64_t m, int64_t n, int64_t kp, int64_t np, int 
     const std::array<int64_t, 5> key{n, m, K, ld, ld};
     auto it = b->algos.find(key);
     if (it == b->algos.end()) {
-      constexpr int kCandidates = 8;
+      constexpr int kCandidates = 32;
       hipblasLtMatmulHeuristicResult_t res[kCandidates];
       int nres = 0;
       if (hipblasLtMatmulAlgoGetHeuristic(b->handle, b->desc, l.a, l.b, l.d, l.d, b->pref, kCandidates, res,
