@@ -150,3 +150,35 @@ def test_int8_refused_under_graph_capture():
     # outside capture the same call works
     want = _host(md.mdgemm_ex(Ag, Bg, flags=I8))
     assert np.array_equal(want, pipeline.full_reference(A, B, 15, 14, 7)["C"])
+
+
+def test_int8_zero_lines_k0_and_extreme_magnitudes():
+    print("[case] int8 zero lines, k=0, extreme exponents, subnormal products", flush=True)
+    A, B = _operands(2, 50, 30, 40, 90)
+    A[:, 3, :] = 0.0
+    B[:, :, 5] = 0.0
+    A[:, 7, 4] = 0.0
+    A[:, 10:15] *= 2.0**-600  # rows far below 1
+    B[:, :, 20:24] *= 2.0**500  # columns far above 1
+    A[:, 30:33] *= 2.0**-520  # with columns 30..32 of B below: products far below 2^-1022
+    B[:, :, 30:33] *= 2.0**-520
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), flags=I8))
+    w, S, T = md.mdgemm_plan(50, 40, 30, 2, flags=I8)
+    assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])
+    assert np.array_equal(C, _fp64_same_digits(A, B, w, S, T, 0))
+    assert (C[:, 3, :] == 0).all() and (C[:, :, 5] == 0).all()
+    assert not np.signbit(C[:, 3, :]).any()
+    Z = md.mdgemm_ex(torch.empty((2, 5, 0), dtype=torch.float64, device=DEV),
+                     torch.empty((2, 0, 6), dtype=torch.float64, device=DEV),
+                     C=torch.full((2, 5, 6), 3.0, dtype=torch.float64, device=DEV), flags=I8)
+    z = _host(Z)
+    assert (z == 0).all() and not np.signbit(z).any()
+
+
+@pytest.mark.parametrize("m,k,n", [(1, 1, 1), (1, 700, 1), (300, 1, 17), (1, 64, 300), (17, 33, 1)])
+def test_int8_degenerate_shapes(m, k, n):
+    print(f"[case] int8 degenerate {m}x{k}x{n}", flush=True)
+    A, B = _operands(2, m, k, n, m + 3 * k + 7 * n)
+    w, S, T = md.mdgemm_plan(m, n, k, 2, flags=I8)
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), flags=I8))
+    assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])
