@@ -130,11 +130,12 @@ typedef struct mdgemm_opts {
  * or S > 64 (more than 8 limbs at w = 7) return MDGEMM_EINVAL, and no exact width
  * MDGEMM_EEXACT.  Digits, levels and C are bit-identical to the FP64 path run
  * with the same slice_bits, slices and cutoff.  Double-double at k = 4096:
- * w = 7, S = 15, T = 14 (120 pairs, 15 GEMMs).  The call allocates nothing
- * beyond the workspace; hipBLASLt's handle and chosen algorithms are created on
- * a device's first such call and kept until the process ends (the first call on
- * a new shape times hipBLASLt's candidate algorithms and synchronizes its stream).
- * Refused with MDGEMM_EINVAL while the stream captures a graph. */
+ * w = 7, S = 15, T = 14 (120 pairs, 15 GEMMs).  Besides the workspace the
+ * library keeps, per device, a hipBLASLt handle (with whatever hipBLASLt holds for
+ * it), created on the first such call, and the algorithm chosen per GEMM shape,
+ * until the process ends; the first call on a new shape times hipBLASLt's
+ * candidate algorithms and synchronizes its stream.  Refused with MDGEMM_EINVAL
+ * while the stream captures a graph. */
 
 /* Fill `opts` with the defaults: default stream, library workspace, 4 slices per
  * limb of 13 bits, cutoff T = S - 1, no range balancing, no flags. */
