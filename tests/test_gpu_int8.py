@@ -182,3 +182,35 @@ def test_int8_degenerate_shapes(m, k, n):
     w, S, T = md.mdgemm_plan(m, n, k, 2, flags=I8)
     C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), flags=I8))
     assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])
+
+
+@pytest.mark.parametrize("signs", ["same", "mixed"])
+def test_int8_at_the_int32_limit(signs):
+    # k = 8876 is the largest k with 15 pairs k 127^2 < 2^31 at w = 7 (checked
+    # on the CPU).  Elements of value 1 - 2^-105 (the double-double (1, -2^-105))
+    # have digits 63, 127, 127, ..., 127 on their grid, so the middle levels sum
+    # products of nearly maximal digits over the full k: the int32 sums come
+    # within a few percent of 2^31.
+    m, k, n = 8, 8876, 8
+    w, S, T = md.mdgemm_plan(m, n, k, 2, flags=I8)
+    assert (w, S, T) == (7, 15, 14)
+    print(f"[case] int8 at the int32 limit, {signs} signs", flush=True)
+    A = np.zeros((2, m, k))
+    B = np.zeros((2, k, n))
+    A[0], A[1] = 1.0, -(2.0**-105)
+    B[0], B[1] = 1.0, -(2.0**-105)
+    if signs == "mixed":
+        rng = np.random.default_rng(7)
+        sa = rng.choice([-1.0, 1.0], size=(m, k))
+        sb = rng.choice([-1.0, 1.0], size=(k, n))
+        A *= sa[None]
+        B *= sb[None]
+    ref = pipeline.full_reference(A, B, S, T, w)
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), flags=I8))
+    assert np.array_equal(C, ref["C"])
+    assert np.array_equal(C, _fp64_same_digits(A, B, w, S, T, 0))
+    if signs == "same":
+        # digits 63, 127, ..., 127; level 14 = k (2 63 127 + 13 127^2) = 0.93 2^31
+        assert ref["DA"][:, 0, 0].tolist() == [63] + [127] * 14
+        assert int(np.max(ref["G"])) == k * (2 * 63 * 127 + 13 * 127**2)
+        assert int(np.max(ref["G"])) > 0.9 * 2**31
