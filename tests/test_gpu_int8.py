@@ -214,3 +214,32 @@ def test_int8_at_the_int32_limit(signs):
         assert ref["DA"][:, 0, 0].tolist() == [63] + [127] * 14
         assert int(np.max(ref["G"])) == k * (2 * 63 * 127 + 13 * 127**2)
         assert int(np.max(ref["G"])) > 0.9 * 2**31
+
+
+def _sweep_cases(count, seed):
+    rng = random.Random(seed)
+    cases = []
+    for c in range(count):
+        L = rng.choice([1, 2, 2, 3, 4, 8])
+        m, k, n = rng.randint(1, 180), rng.randint(1, 300), rng.randint(1, 180)
+        rb = rng.choice([0, 0, 0, 13, 40])
+        if L == 8:
+            rb = 0  # 60 digits already; range digits would pass 64
+        cutoff = rng.choice([-1, -1, -2, "mid"])
+        cases.append((c, L, m, k, n, rb, cutoff))
+    return cases
+
+
+@pytest.mark.parametrize("case", _sweep_cases(14, 2026))
+def test_int8_random_sweep(case):
+    c, L, m, k, n, rb, cutoff = case
+    if cutoff == "mid":
+        w0, S0, _ = md.mdgemm_plan(m, n, k, L, flags=I8, range_bits=rb)
+        cutoff = max(0, S0 - 3)
+    w, S, T = md.mdgemm_plan(m, n, k, L, flags=I8, cutoff=cutoff, range_bits=rb)
+    assert (w, S, T) == exact.plan(L, k, int8=True, cutoff=cutoff, range_bits=rb)
+    print(f"[case] int8 sweep {c}: L={L} {m}x{k}x{n} range={rb} w={w} S={S} T={T}", flush=True)
+    A, B = _operands(L, m, k, n, 1000 + c, rb)
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), flags=I8, cutoff=cutoff, range_bits=rb))
+    assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])
+    assert np.array_equal(C, _fp64_same_digits(A, B, w, S, T, rb))
