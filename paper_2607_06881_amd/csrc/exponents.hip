@@ -44,7 +44,14 @@ __global__ void __launch_bounds__(256) row_exponents_kernel(int64_t rows, int64_
   if (row >= rows) return;  // whole wave leaves together
   const double* r = X0 + row * cols;
   int best = kNoExp;
-  for (int64_t c = lane; c < cols; c += 64) best = max(best, frexp_exp_or_min(r[c]));
+  int64_t c = lane;
+  // four independent loads per lane in flight, then the tail
+  for (; c + 192 < cols; c += 256) {
+    const double x0 = r[c], x1 = r[c + 64], x2 = r[c + 128], x3 = r[c + 192];
+    best = max(best, max(max(frexp_exp_or_min(x0), frexp_exp_or_min(x1)),
+                         max(frexp_exp_or_min(x2), frexp_exp_or_min(x3))));
+  }
+  for (; c < cols; c += 64) best = max(best, frexp_exp_or_min(r[c]));
   best = wave_max(best);
   if (lane == 0) E[row] = (best == kNoExp) ? 0 : best;
 }
