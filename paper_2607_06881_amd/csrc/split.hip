@@ -26,6 +26,8 @@
 // per element, consecutive threads on consecutive columns, so limb loads and
 // digit stores of a wave are contiguous 512-byte rows), and the k-major padded
 // panels the level GEMM reads (see split_panel_kernel).
+#include <type_traits>
+
 #include "internal.h"
 
 namespace mdg {
@@ -148,7 +150,13 @@ __device__ inline void store_digits(const uint64_t (&I)[NW], int S, int w, bool 
   for (int j = 0; j < S; ++j) {
     uint64_t f = cur >> b;
     if (b + w > 64) f |= nxt << (64 - b);  // b > 64 - w > 0 here
-    out[static_cast<int64_t>(S - 1 - j) * stride] = static_cast<OutT>(signed_digit(static_cast<uint32_t>(f & mask), neg));
+    const uint32_t d = static_cast<uint32_t>(f & mask);
+    if constexpr (std::is_integral<OutT>::value) {
+      const int32_t v = static_cast<int32_t>(d);  // int8 digits: the sign in integer arithmetic
+      out[static_cast<int64_t>(S - 1 - j) * stride] = static_cast<OutT>(neg ? -v : v);
+    } else {
+      out[static_cast<int64_t>(S - 1 - j) * stride] = static_cast<OutT>(signed_digit(d, neg));
+    }
     b += w;
     if (b >= 64) {
       b -= 64;
