@@ -396,18 +396,22 @@ bool resolved_exact(const Resolved& r, int64_t k) {
   return (r.flags & MDGEMM_INT8) ? exact_ok_i32(k, pairs, r.w) : exact_ok(k, pairs, r.w);
 }
 
-// Workspace of the int8 level products: EA | EB | flag | A's digits [m][S][kp] |
-// B's digits [np][S kp] | int32 levels [T+1][m][n], each aligned to 256 bytes;
-// kp = k and np = n rounded up to 16 (int8 operand columns of whole 16 bytes).
+// Workspace of the int8 level products: EA | EB | flag | A's digits
+// [mp][kI8Pad + S kp] | B's digits [np][kI8Pad + S kp] | int32 levels [T+1][m][n],
+// each aligned to 256 bytes; kp = k rounded up to 128, mp and np = m and n
+// rounded up to 256 (the layout of csrc/level_gemm_i8.hip).
 struct LayoutI8 {
   size_t ea = 0, eb = 0, flag = 0, da = 0, dbt = 0, g = 0, total = 0;
-  int64_t kp = 0, np = 0;
+  int64_t kp = 0, mp = 0, np = 0;
 };
 bool layout_int8(int64_t m, int64_t n, int64_t k, int S, int T, LayoutI8* L) {
-  L->kp = (k + 15) / 16 * 16;
-  L->np = (n + 15) / 16 * 16;
-  const double approx = (double)S * (double)L->kp * ((double)m + (double)L->np) + 4.0 * (T + 1) * (double)m * (double)n;
+  L->kp = mdg::i8_kp(k);
+  L->mp = mdg::i8_rows(m);
+  L->np = mdg::i8_rows(n);
+  const double ld = mdg::kI8Pad + (double)S * (double)L->kp;
+  const double approx = ld * ((double)L->mp + (double)L->np) + 4.0 * (T + 1) * (double)m * (double)n;
   if (approx > 4.0e18 || m > (int64_t{1} << 31) || n > (int64_t{1} << 31)) return false;
+  const size_t pitch = mdg::kI8Pad + static_cast<size_t>(S) * static_cast<size_t>(L->kp);
   size_t off = 0;
   L->ea = off;
   off += align_up(sizeof(int32_t) * static_cast<size_t>(m));
@@ -416,9 +420,9 @@ bool layout_int8(int64_t m, int64_t n, int64_t k, int S, int T, LayoutI8* L) {
   L->flag = off;
   off += align_up(sizeof(int32_t));
   L->da = off;
-  off += align_up(static_cast<size_t>(m) * S * static_cast<size_t>(L->kp));
+  off += align_up(static_cast<size_t>(L->mp) * pitch);
   L->dbt = off;
-  off += align_up(static_cast<size_t>(S) * static_cast<size_t>(L->kp) * static_cast<size_t>(L->np));
+  off += align_up(static_cast<size_t>(L->np) * pitch);
   L->g = off;
   off += align_up(sizeof(int32_t) * static_cast<size_t>(T + 1) * static_cast<size_t>(m) * static_cast<size_t>(n));
   L->total = off;
@@ -642,7 +646,7 @@ int run_int8(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const 
     MDG_TRY(hip_status(mdg::launch_split_int8(m, k, limbs, r.S, r.w, A, EA, DA, L.kp, s)));
     MDG_TRY(hip_status(mdg::launch_split_int8t(k, n, limbs, r.S, r.w, B, EB, DBt, L.kp, L.np, s)));
     if (timed) MDG_TRY(record(2, s));
-    MDG_TRY(hip_status(mdg::launch_levels_int8(m, n, L.kp, L.np, r.S, r.T, DA, DBt, G, s)));
+    MDG_TRY(hip_status(mdg::launch_levels_int8(m, n, L.kp, r.S, r.T, DA, DBt, G, s)));
     if (timed) MDG_TRY(record(3, s));
     MDG_TRY(hip_status(mdg::launch_accum_renorm_i32(m, n, limbs, r.T + 1, r.w, G, EA, EB, C, s)));
     if (timed) {

@@ -62,23 +62,38 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
                         void* D, bool panel, hipStream_t stream, const uint32_t* masks = nullptr,
                         int combos = 0, bool f32 = false);
 
+// Layout of the int8 digits: rows of pitch kI8Pad + S kp bytes (kp = k rounded
+// up to 128), the first kI8Pad bytes of every row zero, A's rows m rounded up to
+// 256, B's (columns of B) n rounded up to 256 (those extra rows are never
+// stored and only feed outputs that are not kept).
+constexpr int kI8Pad = 128;
+inline int64_t i8_kp(int64_t k) { return (k + 127) / 128 * 128; }
+inline int64_t i8_rows(int64_t x) { return (x + 255) / 256 * 256; }
+
 // a2 for the int8 level products: A's digits (at most 7 bits) as int8,
-// D [m][S][kp] (rows = m, cols = k), zeros for kk >= k.
+// D[i][kI8Pad + s kp + kk] = digit s of A[i][kk] (rows = m, cols = k), zeros for
+// kk >= k and in the pad.
 hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,
                              int8_t* D, int64_t kp, hipStream_t stream);
 
 // a2 for the int8 level products, B (rows = k, cols = n) straight into the
-// k-contiguous layout Dt [np][S kp]: Dt[j][(S-1-q) kp + kk] = digit q of B[kk][j].
+// k-contiguous layout: Dt[j][kI8Pad + (S-1-q) kp + kk] = digit q of B[kk][j], for
+// the np rows j (zeros for j >= n, kk >= k and in the pad).
 hipError_t launch_split_int8t(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,
                               int8_t* Dt, int64_t kp, int64_t np, hipStream_t stream);
 
 // a3 on the int8 matrix cores: levels t = 0..T into int32 planes G [T+1][m][n],
-// one hipBLASLt GEMM per level, from A's digits DA [m][S][kp] (launch_split_int8,
-// axis 0) and B's digits DBt [np][S kp] (launch_split_int8t: column j, digit q
-// in k range (S-1-q) kp ..); every level sum must stay below 2^31 (checked by
-// the caller).
-hipError_t launch_levels_int8(int64_t m, int64_t n, int64_t kp, int64_t np, int S, int T, const int8_t* DA,
-                              const int8_t* DBt, int32_t* G, hipStream_t stream);
+// from A's digits (launch_split_int8, i8_rows(m) rows) and B's (launch_split_int8t,
+// i8_rows(n) rows); every level sum must stay below 2^31 (checked by the caller).
+// Either the hand-written kernel (all levels in one launch) or one hipBLASLt
+// GEMM per level, whichever ran faster on the first call of the shape.
+hipError_t launch_levels_int8(int64_t m, int64_t n, int64_t kp, int S, int T, const int8_t* DA, const int8_t* DBt,
+                              int32_t* G, hipStream_t stream);
+
+// The hand-written int8 level kernel (csrc/level_gemm_i8.hip) and whether a shape fits it.
+bool level_gemm_i8_fits(int64_t kp, int S);
+hipError_t launch_level_gemm_i8(int64_t m, int64_t n, int64_t kp, int S, int T, const int8_t* DA, const int8_t* DBt,
+                                int32_t* G, hipStream_t stream);
 
 // a3: products of the combination panels DAt [*][panel_k(k)][panel_mn(m)] and
 // DBp [*][panel_k(k)][panel_mn(n)] (combinations 0..S-1 are the digits); one

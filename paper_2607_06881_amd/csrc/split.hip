@@ -270,20 +270,24 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
   }
 }
 
-// A's digits for the int8 level products (digits of at most 7 bits): D [m][S][kp],
-// D[i][s][kk] = digit s of A[i][kk], zeros for kk >= k.  A level's pairs
-// (p, t - p), p ascending, are then one contiguous k range of every row.  One
-// thread per element of the padded grid [m][kp], consecutive threads on
-// consecutive kk: limb loads and digit stores of a wave are contiguous.
+// A's digits for the int8 level products (digits of at most 7 bits), rows of
+// pitch kI8Pad + S kp: D[i][kI8Pad + s kp + kk] = digit s of A[i][kk], zeros for
+// kk >= k and in the first kI8Pad bytes.  A level's pairs (p, t - p), p
+// ascending, are then one contiguous k range of every row.  One thread per
+// element of the padded grid [m][kp], consecutive threads on consecutive kk:
+// limb loads and digit stores of a wave are contiguous.
 template <int NW, int ML>
 __global__ void __launch_bounds__(256) split_int8_kernel(int64_t rows, int64_t cols, int64_t kp, int L, int S, int w,
                                                          const double* __restrict__ X,
                                                          const int32_t* __restrict__ E, int8_t* __restrict__ D) {
   const int64_t plane = rows * cols;
+  const int64_t ld = kI8Pad + static_cast<int64_t>(S) * kp;
   const int64_t c = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (c >= kp) return;
   for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
-    int8_t* out = D + r * S * kp + c;
+    int8_t* row = D + r * ld;
+    if (c < kI8Pad) row[c] = 0;
+    int8_t* out = row + kI8Pad + c;
     if (c < cols) {
       double xs[ML];
       load_limbs<ML>(X, plane, L, r * cols + c, xs);
@@ -297,8 +301,9 @@ __global__ void __launch_bounds__(256) split_int8_kernel(int64_t rows, int64_t c
 }
 
 // B's int8 digits straight into the k-contiguous layout of the int8 level
-// GEMMs: Dt [np][S kp], Dt[j][(S-1-q) kp + kk] = digit q of B[kk][j], zeros in
-// the padding.  Lanes take consecutive kk, so every digit store of a wave is 64
+// products, rows of pitch kI8Pad + S kp: Dt[j][kI8Pad + (S-1-q) kp + kk] = digit q
+// of B[kk][j], zeros for j >= n, kk >= k and in the first kI8Pad bytes.  Lanes
+// take consecutive kk, so every digit store of a wave is 64
 // contiguous bytes; a block covers 64 kk x 16 columns (each wave 4 columns), so
 // the 16 consecutive doubles of a row of B that one 128-byte line holds are all
 // read by the same block.
@@ -308,7 +313,7 @@ __global__ void __launch_bounds__(256) split_int8t_kernel(int64_t rows, int64_t 
                                                           const int32_t* __restrict__ E, int8_t* __restrict__ Dt) {
   const int64_t plane = rows * cols;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t ld = static_cast<int64_t>(S) * kp;
+  const int64_t ld = kI8Pad + static_cast<int64_t>(S) * kp;
   for (int64_t by = blockIdx.y; by * 16 < np; by += gridDim.y) {
     const int64_t kk = static_cast<int64_t>(blockIdx.x) * 64 + lane;
     if (kk >= kp) continue;
@@ -316,7 +321,8 @@ __global__ void __launch_bounds__(256) split_int8t_kernel(int64_t rows, int64_t 
     for (int r = 0; r < 4; ++r) {
       const int64_t j = by * 16 + 4 * wave + r;
       if (j >= np) break;
-      int8_t* out = Dt + j * ld + static_cast<int64_t>(S - 1) * kp + kk;
+      if (kk < kI8Pad) Dt[j * ld + kk] = 0;
+      int8_t* out = Dt + j * ld + kI8Pad + static_cast<int64_t>(S - 1) * kp + kk;
       if (kk < rows && j < cols) {
         double xs[ML];
         load_limbs<ML>(X, plane, L, kk * cols + j, xs);
@@ -434,7 +440,7 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
 
 hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,
                              int8_t* D, int64_t kp, hipStream_t stream) {
-  if (w < 1 || w > 7 || S < 1 || S > kMaxSlices || kp < cols) return hipErrorInvalidValue;
+  if (w < 1 || w > 7 || S < 1 || S > kMaxSlices || kp < cols || kp % kI8Pad != 0) return hipErrorInvalidValue;
   if (rows == 0 || kp == 0) return hipSuccess;
   const int words = (w * S + 52 + 63) / 64;
   if (L <= 4) return split_int8_words<4>(words, rows, cols, kp, L, S, w, X, E, D, stream);
@@ -444,7 +450,8 @@ hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, co
 
 hipError_t launch_split_int8t(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,
                               int8_t* Dt, int64_t kp, int64_t np, hipStream_t stream) {
-  if (w < 1 || w > 7 || S < 1 || S > kMaxSlices || kp < rows || np < cols) return hipErrorInvalidValue;
+  if (w < 1 || w > 7 || S < 1 || S > kMaxSlices || kp < rows || np < cols || kp % kI8Pad != 0)
+    return hipErrorInvalidValue;
   if (kp == 0 || np == 0) return hipSuccess;
   const int words = (w * S + 52 + 63) / 64;
   if (L <= 4) return split_int8t_words<4>(words, rows, cols, kp, np, L, S, w, X, E, Dt, stream);

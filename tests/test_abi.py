@@ -255,12 +255,14 @@ def test_int8_plans(lib):
         md.mdgemm_plan(4, 4, 2**31, 1, flags=I8)
     assert ei.value.status == md.MDGEMM_EEXACT
     assert _ex(lib, 4, 4, 2**31, 1, flags=I8) == md.MDGEMM_EEXACT
-    # workspace: EA, EB, flag, int8 digits of A and of B, int32 levels, 256-byte aligned
+    # workspace: EA, EB, flag, int8 digits of A and of B (rows of 128 zero bytes + S kp,
+    # kp = k rounded up to 128, m and n rounded up to 256 rows), int32 levels, 256-byte aligned
     def al(x):
         return (x + 255) // 256 * 256
     m, n, k, S, T = 100, 70, 300, 15, 14
-    kp, np_ = 304, 80
-    want = al(4 * m) + al(4 * n) + al(4) + al(m * S * kp) + al(S * kp * np_) + al(4 * (T + 1) * m * n)
+    kp, mp, np_ = 384, 256, 256
+    ld = 128 + S * kp
+    want = al(4 * m) + al(4 * n) + al(4) + al(mp * ld) + al(np_ * ld) + al(4 * (T + 1) * m * n)
     assert md.mdgemm_workspace_bytes(m, n, k, 2, flags=I8) == want
 
 

@@ -5,7 +5,10 @@ int8 matrix products with int32 sums, so the digits, the levels and the limbs
 must equal the oracle's chain at the same width bit for bit, and equal the
 FP64 path run with the same width, digit count and cutoff.  Sizes span ragged
 shapes (n not a multiple of 16, k not a multiple of 16) and every limb count
-the option supports.
+the option supports.  The level products run on the hand-written int8 kernel or
+on hipBLASLt (chosen per shape by timing); the route tests force each one
+(MDGEMM_INT8_LEVELS) on shapes with odd stage counts, ragged tiles and many
+levels.
 """
 
 import ctypes
@@ -101,6 +104,23 @@ def test_int8_larger_products(L, m, k, n, seed):
         assert list(C[:, i, j]) == r["limbs"], (i, j)
 
 
+@pytest.mark.parametrize("route", ["mfma", "hipblaslt"])
+@pytest.mark.parametrize("L,m,k,n,seed", [(2, 300, 700, 257, 70), (3, 520, 1100, 300, 71), (2, 1000, 2000, 777, 60),
+                                          (8, 64, 128, 8192, 72), (4, 257, 129, 513, 73), (1, 3, 5, 2, 74)])
+def test_int8_both_routes(route, L, m, k, n, seed, monkeypatch):
+    monkeypatch.setenv("MDGEMM_INT8_LEVELS", route)
+    w, S, T = md.mdgemm_plan(m, n, k, L, flags=I8)
+    print(f"[case] int8 route={route} L={L} {m}x{k}x{n} w={w} S={S} T={T}", flush=True)
+    A, B = _operands(L, m, k, n, seed)
+    C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), flags=I8))
+    assert np.array_equal(C, _fp64_same_digits(A, B, w, S, T, 0))
+    pick = random.Random(seed)
+    entries = [(pick.randrange(m), pick.randrange(n)) for _ in range(4)] + [(m - 1, n - 1)]
+    ref = pipeline.reference_entries(A, B, S, T, entries, w)
+    for (i, j), r in ref.items():
+        assert list(C[:, i, j]) == r["limbs"], (i, j)
+
+
 def test_int8_workspace_stream_and_stage_times():
     L, m, k, n = 2, 200, 300, 130
     print("[case] int8 workspace / stream / timing / finite check", flush=True)
@@ -184,8 +204,11 @@ def test_int8_degenerate_shapes(m, k, n):
     assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])
 
 
+@pytest.mark.parametrize("route", ["auto", "mfma", "hipblaslt"])
 @pytest.mark.parametrize("signs", ["same", "mixed"])
-def test_int8_at_the_int32_limit(signs):
+def test_int8_at_the_int32_limit(signs, route, monkeypatch):
+    if route != "auto":
+        monkeypatch.setenv("MDGEMM_INT8_LEVELS", route)
     # k = 8876 is the largest k with 15 pairs k 127^2 < 2^31 at w = 7 (checked
     # on the CPU).  Elements of value 1 - 2^-105 (the double-double (1, -2^-105))
     # have digits 63, 127, 127, ..., 127 on their grid, so the middle levels sum
