@@ -121,20 +121,25 @@ typedef struct mdgemm_opts {
  *
  * MDGEMM_INT8.  The level sums of section 2 are exact integer sums, so with
  * digits of at most 7 bits (|d| <= 127) they are formed on the int8 matrix cores
- * with exact int32 sums: each level t is one int8 GEMM (hipBLASLt) of the
- * contiguous digit ranges of its pairs, which requires
- * max pairs of a level times k (2^w - 1)^2 < 2^31.  slice_bits 0 or
- * MDGEMM_SLICE_BITS_AUTO: the widest w <= 7 whose levels stay exact for this k,
+ * with exact int32 sums over the contiguous digit ranges of each level's pairs,
+ * which requires max pairs of a level times k (2^w - 1)^2 < 2^31.  slice_bits 0
+ * or MDGEMM_SLICE_BITS_AUTO: the widest w <= 7 whose levels stay exact for this k,
  * S = ceil(52 limbs / w) (plus the range digits), T by the cutoff rules above
  * (T = S - 1 by default); slice_bits 1..7: that width; wider, the Karatsuba flags,
  * or S > 64 (more than 8 limbs at w = 7) return MDGEMM_EINVAL, and no exact width
  * MDGEMM_EEXACT.  Digits, levels and C are bit-identical to the FP64 path run
  * with the same slice_bits, slices and cutoff.  Double-double at k = 4096:
- * w = 7, S = 15, T = 14 (120 pairs, 15 GEMMs).  Besides the workspace the
- * library keeps, per device, a hipBLASLt handle (with whatever hipBLASLt holds for
- * it), created on the first such call, and the algorithm chosen per GEMM shape,
- * until the process ends; the first call on a new shape times hipBLASLt's
- * candidate algorithms and synchronizes its stream.  Refused with MDGEMM_EINVAL
+ * w = 7, S = 15, T = 14 (120 pairs).  The level products run on the library's
+ * own int8 kernel (all levels in one launch) or as one hipBLASLt GEMM per level:
+ * the first call on a new shape (m, n, k, S, T) times both (hipBLASLt with the
+ * fastest of its candidate algorithms per level, also timed then) and keeps the
+ * own kernel unless hipBLASLt is more than 3% faster; that call synchronizes its
+ * stream.  The environment variable MDGEMM_INT8_LEVELS=mfma or =hipblaslt,
+ * read on every call, forces one route (the results are the same).  Besides the
+ * workspace the library keeps, per device, a hipBLASLt handle (with whatever
+ * hipBLASLt holds for it), created on the first such call, the algorithm per
+ * GEMM shape and the route per product shape, until the process ends.  Refused
+ * with MDGEMM_EINVAL
  * while the stream captures a graph. */
 
 /* Fill `opts` with the defaults: default stream, library workspace, 4 slices per
