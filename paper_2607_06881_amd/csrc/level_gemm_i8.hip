@@ -31,9 +31,14 @@
 // * k advances in stages of 128 bytes, two LDS stages (64 KB each: the A tile
 //   then the B tile, 128-byte rows).  Copies go global -> LDS directly with
 //   buffer_load_dwordx4 ... lds (counted on vmcnt only; the FLAT form would make
-//   the compiler wait for every LDS read).  16-byte granules of LDS row R are
-//   XOR-swizzled by (R & 7) ^ ((R >> 3) & 1): a fragment read (16 rows, one
-//   granule) then meets every bank group once.
+//   the compiler wait for every LDS read).  A ds_read_b128 is served 16 lanes at
+//   a time over 64 banks, lanes 8a .. 8a+7 together with 32+8a .. 32+8a+7 (the
+//   grouping that the bank-conflict counter confirms: a swizzle conflict-free
+//   for 16 consecutive lanes still doubled every read).  A fragment read meets
+//   8 rows twice there, at granules g and g ^ 2, so the 16-byte granules of LDS
+//   row R are XOR-swizzled by swz(R) = bit1(R) | (bit0(R) ^ bit3(R)) << 1 |
+//   bit2(R) << 2, which keeps all 16 accesses on distinct bank groups (and 16
+//   consecutive lanes too).
 // * A stage is two sub-steps of 64 MFMAs; the fragments of the next sub-step are
 //   read (four groups of four ds_read_b128) while the current one runs.  The
 //   barrier sits before a stage's last sub-step: it certifies the next stage's
@@ -64,6 +69,9 @@ static_assert(kI8Pad == kStage, "the zero pad is one stage");
 struct LevelOrder {
   uint8_t t[128];
 };
+
+// the granule swizzle of LDS row r (depends on r mod 16 only)
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) & 1) | ((((r & 1) ^ ((r >> 3) & 1))) << 1) | (r & 4); }
 
 struct Frag {
   v4i a[8], b[8];
@@ -178,17 +186,17 @@ __global__ void __launch_bounds__(256, 1) level_gemm_i8_kernel(int64_t m, int64_
 
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wr = wave >> 1, wc = wave & 1;
-  // copies: lane L of instruction q lands at tile row 64 wave + 8q + L/8, granule L%8,
-  // and fetches logical granule (L%8) ^ (L/8) ^ (q&1) of that row
+  // copies: lane L of instruction q lands at tile row 64 wave + 8q + L/8 (= 8 (q&1) + L/8
+  // mod 16), granule L%8, and fetches logical granule (L%8) ^ swz(row) of that row
   const int lr = 64 * wave + (lane >> 3);
-  const uint32_t lo0 = static_cast<uint32_t>(lr * ld + (((lane & 7) ^ (lane >> 3)) << 4));
-  const uint32_t lo1 = static_cast<uint32_t>(lr * ld + (((lane & 7) ^ (lane >> 3) ^ 1) << 4));
+  const uint32_t lo0 = static_cast<uint32_t>(lr * ld + (((lane & 7) ^ swz(lane >> 3)) << 4));
+  const uint32_t lo1 = static_cast<uint32_t>(lr * ld + (((lane & 7) ^ swz(8 + (lane >> 3))) << 4));
   // fragments: lane l reads row 16 i + l%16 of the wave's 128 rows, logical granule 4h + l/16
   int fa[2], fb[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int l = lane & 15, gl = 4 * h + (lane >> 4);
-    const int sw = ((gl ^ (l & 7) ^ (l >> 3)) << 4) + l * kStage;
+    const int sw = ((gl ^ swz(l)) << 4) + l * kStage;
     fa[h] = wr * 128 * kStage + sw;
     fb[h] = wc * 128 * kStage + sw;
   }
