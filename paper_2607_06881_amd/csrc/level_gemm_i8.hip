@@ -23,11 +23,13 @@
 // * v_mfma_i32_16x16x64_i8: lane l supplies 16 bytes of row l%16 of the A block
 //   and of column l%16 of the B block, at k granule l/16 (any k order works as
 //   long as A and B agree); register r of lane l holds D[4 (l/16) + r][l%16].
-// * One workgroup, four waves, owns a 256 x 256 output tile; each wave holds a
-//   128 x 128 sub-tile in 64 accumulator blocks (all 256 AGPRs).  The MFMAs are
-//   issued as inline instructions with AGPR accumulators: left to itself the
-//   register allocator permutes accumulators between AGPRs and VGPRs across the
-//   loop, dozens of copies per step that stall behind the MFMAs writing them.
+// * One workgroup, eight waves (two per SIMD), owns a 256 x 256 output tile;
+//   each wave holds a 128 x 64 sub-tile in 32 accumulator blocks (128 AGPRs,
+//   220 registers in all, so two waves fit a SIMD: one issues while the other
+//   waits; four waves of 128 x 128 ran 1-9% slower).  The MFMAs are issued as
+//   inline instructions with AGPR accumulators: left to itself the register
+//   allocator permutes accumulators between AGPRs and VGPRs across the loop,
+//   dozens of copies per step that stall behind the MFMAs writing them.
 // * k advances in stages of 128 bytes, two LDS stages (64 KB each: the A tile
 //   then the B tile, 128-byte rows).  Copies go global -> LDS directly with
 //   buffer_load_dwordx4 ... lds (counted on vmcnt only; the FLAT form would make
@@ -39,12 +41,12 @@
 //   row R are XOR-swizzled by swz(R) = bit1(R) | (bit0(R) ^ bit3(R)) << 1 |
 //   bit2(R) << 2, which keeps all 16 accesses on distinct bank groups (and 16
 //   consecutive lanes too).
-// * A stage is two sub-steps of 64 MFMAs; the fragments of the next sub-step are
-//   read (four groups of four ds_read_b128) while the current one runs.  The
-//   barrier sits before a stage's last sub-step: it certifies the next stage's
-//   copies and frees the current buffer, whose next copies (two stages ahead)
-//   are then issued one pair after every eighth MFMA: a burst of copies blocks
-//   the wave's in-order issue and starves the matrix pipe.
+// * A stage is two sub-steps of 32 MFMAs per wave; the fragments of the next
+//   sub-step are read (four groups of three ds_read_b128) while the current one
+//   runs.  The barrier sits before a stage's last sub-step: it certifies the
+//   next stage's copies and frees the current buffer, whose next copies (two
+//   stages ahead) are then issued one pair after every eighth MFMA: a burst of
+//   copies blocks the wave's in-order issue and starves the matrix pipe.
 //
 // Work decomposition: grid.x = output tiles (renumbered per XCD, as in the
 // FP64 kernel, in patches of `group` tile-rows), grid.y = levels, heaviest
@@ -74,7 +76,7 @@ struct LevelOrder {
 __device__ __forceinline__ int swz(int r) { return ((r >> 1) & 1) | ((((r & 1) ^ ((r >> 3) & 1))) << 1) | (r & 4); }
 
 struct Frag {
-  v4i a[8], b[8];
+  v4i a[8], b[4];
 };
 
 __device__ __forceinline__ void mfma(v4i& acc, const v4i& a, const v4i& b) {
@@ -87,35 +89,33 @@ __device__ __forceinline__ void mfma(v4i& acc, const v4i& a, const v4i& b) {
 __device__ __forceinline__ void tile_loop(int8_t* __restrict__ P0, int8_t* __restrict__ P1, const int8_t* a,
                                           const int8_t* b, uint32_t na, uint32_t nb, int nst, uint32_t qs,
                                           uint32_t lo0, uint32_t lo1, int fa0, int fa1, int fb0, int fb1, int wave,
-                                          v4i (&acc)[8][8]) {
+                                          v4i (&acc)[8][4]) {
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a), 0, na, 0x00020000);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(b), 0, nb, 0x00020000);
-  // copy q (0..7) of stage s into buffer P: tile rows 64 wave + 8q .. +7 of A and of B
+  // copy q (0..3) of stage s into buffer P: tile rows 32 wave + 8q .. +7 of A and of B
   auto copy = [&](int8_t* P, int s, int q) {
     const uint32_t so = static_cast<uint32_t>(s) * kStage + static_cast<uint32_t>(q) * qs;
     const uint32_t lo = (q & 1) ? lo1 : lo0;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(P + (64 * wave + 8 * q) * kStage), 16, lo, so, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(P + kTile * kStage + (64 * wave + 8 * q) * kStage), 16,
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(P + (32 * wave + 8 * q) * kStage), 16, lo, so, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(P + kTile * kStage + (32 * wave + 8 * q) * kStage), 16,
                                              lo, so, 0, 0);
   };
   auto read = [&](const int8_t* P, int h, Frag& f, int g) {
     const int oa = h ? fa1 : fa0, ob = h ? fb1 : fb0;
 #pragma unroll
-    for (int i = 2 * g; i < 2 * g + 2; ++i) {
-      f.a[i] = *reinterpret_cast<const v4i*>(P + oa + i * 16 * kStage);
-      f.b[i] = *reinterpret_cast<const v4i*>(P + kTile * kStage + ob + i * 16 * kStage);
-    }
+    for (int i = 2 * g; i < 2 * g + 2; ++i) f.a[i] = *reinterpret_cast<const v4i*>(P + oa + i * 16 * kStage);
+    f.b[g] = *reinterpret_cast<const v4i*>(P + kTile * kStage + ob + g * 16 * kStage);
   };
-  // rows 2g, 2g + 1 of the 8 x 8 blocks; with copies, copy pair q into P after each eighth MFMA
+  // rows 2g, 2g + 1 of the 8 x 4 blocks; with copies, copy pair g into P after the eighth MFMA
   auto run = [&](const Frag& f, int g, auto with_copies, int8_t* P, int s) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int i = 2 * g + (e >> 3), j = e & 7;
+    for (int e = 0; e < 8; ++e) {
+      const int i = 2 * g + (e >> 2), j = e & 3;
       mfma(acc[i][j], f.a[i], f.b[j]);
       if constexpr (decltype(with_copies)::value) {
-        if (j == 7) {
+        if (e == 7) {
           __builtin_amdgcn_sched_barrier(0);
-          copy(P, s, 2 * g + (e >> 3));
+          copy(P, s, g);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -141,9 +141,9 @@ __device__ __forceinline__ void tile_loop(int8_t* __restrict__ P0, int8_t* __res
     step(Q, 0, x, y, std::true_type{}, P, min(s + 2, nst - 1));  // copies of stage s + 2 (the last again near the end)
   };
 #pragma unroll
-  for (int q = 0; q < 8; ++q) copy(P0, 0, q);
+  for (int q = 0; q < 4; ++q) copy(P0, 0, q);
 #pragma unroll
-  for (int q = 0; q < 8; ++q) copy(P1, 1, q);
+  for (int q = 0; q < 4; ++q) copy(P1, 1, q);
   __builtin_amdgcn_s_waitcnt(kWaitVmLgkm0);
   __syncthreads();
   __builtin_amdgcn_sched_barrier(0);
@@ -157,7 +157,7 @@ __device__ __forceinline__ void tile_loop(int8_t* __restrict__ P0, int8_t* __res
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 }
 
-__global__ void __launch_bounds__(256, 1) level_gemm_i8_kernel(int64_t m, int64_t n, int64_t kp, int S, int tiles_n,
+__global__ void __launch_bounds__(512, 1) level_gemm_i8_kernel(int64_t m, int64_t n, int64_t kp, int S, int tiles_n,
                                                                int ntiles, int group, const int8_t* __restrict__ DA,
                                                                const int8_t* __restrict__ DBt,
                                                                int32_t* __restrict__ G, LevelOrder order) {
@@ -185,26 +185,27 @@ __global__ void __launch_bounds__(256, 1) level_gemm_i8_kernel(int64_t m, int64_
   const int64_t oa = kI8Pad + p0 * kp - odd * kStage, ob = kI8Pad + (S - 1 - t + p0) * kp - odd * kStage;
 
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wr = wave >> 1, wc = wave & 1;
-  // copies: lane L of instruction q lands at tile row 64 wave + 8q + L/8 (= 8 (q&1) + L/8
+  const int wr = wave >> 2, wc = wave & 3;
+  // copies: lane L of instruction q lands at tile row 32 wave + 8q + L/8 (= 8 (q&1) + L/8
   // mod 16), granule L%8, and fetches logical granule (L%8) ^ swz(row) of that row
-  const int lr = 64 * wave + (lane >> 3);
+  const int lr = 32 * wave + (lane >> 3);
   const uint32_t lo0 = static_cast<uint32_t>(lr * ld + (((lane & 7) ^ swz(lane >> 3)) << 4));
   const uint32_t lo1 = static_cast<uint32_t>(lr * ld + (((lane & 7) ^ swz(8 + (lane >> 3))) << 4));
-  // fragments: lane l reads row 16 i + l%16 of the wave's 128 rows, logical granule 4h + l/16
+  // fragments: lane l reads row 16 i + l%16 of the wave's 128 rows of A (64 columns of B),
+  // logical granule 4h + l/16
   int fa[2], fb[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int l = lane & 15, gl = 4 * h + (lane >> 4);
     const int sw = ((gl ^ swz(l)) << 4) + l * kStage;
     fa[h] = wr * 128 * kStage + sw;
-    fb[h] = wc * 128 * kStage + sw;
+    fb[h] = wc * 64 * kStage + sw;
   }
-  v4i acc[8][8];
+  v4i acc[8][4];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+    for (int j = 0; j < 4; ++j) acc[i][j] = v4i{0, 0, 0, 0};
   const int8_t* a = DA + m0 * ld + oa;
   const int8_t* b = DBt + n0 * ld + ob;
   tile_loop(P0, P1, a, b, static_cast<uint32_t>(kTile * ld - oa), static_cast<uint32_t>(kTile * ld - ob), nst,
@@ -214,11 +215,11 @@ __global__ void __launch_bounds__(256, 1) level_gemm_i8_kernel(int64_t m, int64_
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int64_t gi = m0 + wr * 128 + i * 16 + 4 * (lane >> 4) + r;
-        const int64_t gj = n0 + wc * 128 + j * 16 + (lane & 15);
+        const int64_t gj = n0 + wc * 64 + j * 16 + (lane & 15);
         if (gi < m && gj < n) o[gi * n + gj] = acc[i][j][r];
       }
 }
@@ -249,7 +250,7 @@ hipError_t launch_level_gemm_i8(int64_t m, int64_t n, int64_t kp, int S, int T, 
   // patches of 2 tile-rows for large outputs, 4 otherwise (measured on MI355X)
   const int group = ntiles >= 1024 ? 2 : 4;
   hipLaunchKernelGGL(level_gemm_i8_kernel, dim3(static_cast<unsigned>(ntiles), static_cast<unsigned>(T + 1)),
-                     dim3(256), 0, stream, m, n, kp, S, static_cast<int>(tiles_n), static_cast<int>(ntiles), group,
+                     dim3(512), 0, stream, m, n, kp, S, static_cast<int>(tiles_n), static_cast<int>(ntiles), group,
                      DA, DBt, G, order);
   return hipGetLastError();
 }
