@@ -302,3 +302,53 @@ def test_range_balancing_plans(lib):
     assert lib.mdgemm_line_spread(4, 4, 2, FA, FB, FC, None) == E
     assert lib.mdgemm_line_spread(4, 4, 0, FA, FB, FB, None) == E  # E and spread overlap
     assert lib.mdgemm_line_spread(0, 4, 0, None, None, None, None) == md.MDGEMM_OK
+
+
+def _swz(r):
+    # the int8 kernel's granule swizzle of LDS row r (level_gemm_i8.hip, swz)
+    return ((r >> 1) & 1) | (((r & 1) ^ ((r >> 3) & 1)) << 1) | (r & 4)
+
+
+def test_int8_kernel_lds_layout_model():
+    """The int8 level kernel's LDS addressing, modelled on the CPU.
+
+    Copies: lane L of copy instruction q of wave w lands at tile row
+    32 w + 8 q + L / 8, physical granule L % 8, and fetches logical granule
+    (L % 8) ^ swz(row).  Fragment reads: lane l of the wave at tile row
+    R = base + 16 i + l % 16 wants logical granule 4 h + l / 16 and reads
+    physical granule (4 h + l / 16) ^ swz(l % 16).  Checked: every logical
+    granule of every row is written exactly once and read from where it was
+    written; and a fragment read meets 16 distinct bank groups (64 banks of
+    4 bytes) in each group of lanes that the LDS serves together
+    (8a..8a+7 with 32+8a..32+8a+7, as the bank-conflict counter shows on
+    gfx950; also 16 and 8 consecutive lanes).
+    """
+    where = {}
+    for w in range(8):
+        for q in range(4):
+            for L in range(64):
+                row = 32 * w + 8 * q + L // 8
+                logical = (L % 8) ^ _swz(row)
+                assert (row, logical) not in where
+                where[(row, logical)] = L % 8
+    assert len(where) == 256 * 8
+    models = {
+        "halves": ([list(range(i, i + 8)) + list(range(i + 32, i + 40)) for i in range(0, 32, 8)], 64),
+        "consecutive 16": ([list(range(i, i + 16)) for i in range(0, 64, 16)], 64),
+        "consecutive 8": ([list(range(i, i + 8)) for i in range(0, 64, 8)], 32),
+    }
+    # A: a wave reads 8 blocks of 16 rows from row 0 or 128; B: 4 blocks from 0, 64, 128 or 192
+    for base, blocks in [(0, 8), (128, 8), (0, 4), (64, 4), (128, 4), (192, 4)]:
+        for i in range(blocks):
+            for h in range(2):
+                addr = []
+                for lane in range(64):
+                    R = base + 16 * i + lane % 16
+                    logical = 4 * h + lane // 16
+                    phys = logical ^ _swz(lane % 16)
+                    assert where[(R, logical)] == phys  # read where the copy wrote
+                    addr.append(R * 128 + 16 * phys)
+                for name, (groups, banks) in models.items():
+                    for grp in groups:
+                        hit = [(addr[l] // 4 + d) % banks for l in grp for d in range(4)]
+                        assert len(set(hit)) == len(hit), (name, base, i, h)
