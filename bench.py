@@ -254,8 +254,9 @@ def main(argv=None) -> int:
     if int8:
         roofline.update({"peak": INT8_PEAK_TOPS, "unit": "TOP/s", "frac": round(achieved / INT8_PEAK_TOPS, 4),
                          "traffic": None,
-                         "kernel": f"hipBLASLt int8 GEMMs, one per level ({T + 1}), int32 sums; duration of all "
-                                   "of them per step",
+                         "kernel": f"int8 level products ({T + 1} levels, int32 sums): level_gemm_i8_kernel in one "
+                                   "launch, or one hipBLASLt GEMM per level where that measured faster; duration "
+                                   "of all of them per step",
                          "ops_per_step": roofline.pop("flops_per_launch"),
                          "avg_step_ms": roofline.pop("avg_launch_ms")})
     stages = {

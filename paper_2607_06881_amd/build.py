@@ -9,8 +9,9 @@ Flags:
 * ``-Xclang -target-feature -Xclang -packed-fp32-ops``: no packed-FP32
   instructions are generated (none of these kernels needs them).
 
-The library links hipBLASLt, which runs the int8 level GEMMs of the
-MDGEMM_INT8 option (the FP64 path uses only the kernels built here).
+The library links hipBLASLt, the alternative route for the int8 level
+products of the MDGEMM_INT8 option (used where it measures faster than the
+int8 kernel built here; the FP64 path uses only the kernels built here).
 """
 
 from __future__ import annotations

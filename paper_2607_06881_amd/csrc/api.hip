@@ -612,8 +612,9 @@ int run_int8(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const 
   LayoutI8 L;
   if (!layout_int8(m, n, k, r.S, r.T, &L)) return MDGEMM_EINVAL;
   hipStream_t s = r.stream;
-  // refused under graph capture: what hipBLASLt records (memset nodes of split-k
-  // forms, for instance) is not under this library's control
+  // refused under graph capture: the first call on a shape times both routes of
+  // the level products and synchronizes, and what hipBLASLt records (memset nodes
+  // of split-k forms, for instance) is not under this library's control
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(s, &cap) != hipSuccess) return MDGEMM_EHIP;
   if (cap != hipStreamCaptureStatusNone) return MDGEMM_EINVAL;
