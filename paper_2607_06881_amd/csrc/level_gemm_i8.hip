@@ -17,7 +17,8 @@
 // row of DA and at (S-1-t+p0) kp in every row of DBt.  When K / 128 is odd the
 // range starts one 128-byte stage early: that stage is the zero pad of A's row
 // (p0 = 0) or of B's row (p0 > 0 means t >= S, so B's range starts at its pad),
-// and adds nothing.
+// and adds nothing.  (Levels are split into chunks of pairs only when a pair is
+// an even number of stages, so a chunk never needs that.)
 //
 // CDNA4 mapping:
 // * v_mfma_i32_16x16x64_i8: lane l supplies 16 bytes of row l%16 of the A block
@@ -49,8 +50,10 @@
 //   copies blocks the wave's in-order issue and starves the matrix pipe.
 //
 // Work decomposition: grid.x = output tiles (renumbered per XCD, as in the
-// FP64 kernel, in patches of `group` tile-rows), grid.y = levels, heaviest
-// first (a table in the kernel arguments).
+// FP64 kernel, in patches of `group` tile-rows), grid.y = jobs, heaviest first
+// (a table in the kernel arguments): whole levels, or, for small outputs whose
+// grid would hold few blocks, chunks of a level's pairs that add their partial
+// sums into zeroed planes with int32 atomics (exact in any order).
 #include <type_traits>
 
 #include "internal.h"
@@ -68,8 +71,10 @@ constexpr int kXcds = 8;
 constexpr unsigned kWaitVmLgkm0 = 0x0070;  // s_waitcnt vmcnt(0) lgkmcnt(0)
 static_assert(kI8Pad == kStage, "the zero pad is one stage");
 
-struct LevelOrder {
-  uint8_t t[128];
+// the jobs of one launch, heaviest first: level t[y], its pairs first[y] ..
+// first[y] + count[y] - 1 (indices into the level's pair range)
+struct Jobs {
+  uint8_t t[128], first[128], count[128];
 };
 
 // the granule swizzle of LDS row r (depends on r mod 16 only)
@@ -160,7 +165,7 @@ __device__ __forceinline__ void tile_loop(int8_t* __restrict__ P0, int8_t* __res
 __global__ void __launch_bounds__(512, 1) level_gemm_i8_kernel(int64_t m, int64_t n, int64_t kp, int S, int tiles_n,
                                                                int ntiles, int group, const int8_t* __restrict__ DA,
                                                                const int8_t* __restrict__ DBt,
-                                                               int32_t* __restrict__ G, LevelOrder order) {
+                                                               int32_t* __restrict__ G, Jobs jobs, int split) {
   __shared__ __attribute__((aligned(1024))) int8_t P0[kBuf];
   __shared__ __attribute__((aligned(1024))) int8_t P1[kBuf];
 
@@ -176,10 +181,10 @@ __global__ void __launch_bounds__(512, 1) level_gemm_i8_kernel(int64_t m, int64_
   const int rows_in = min(group, tiles_m - first), within = tt - g * gsz;
   const int64_t m0 = static_cast<int64_t>(first + within % rows_in) * kTile;
   const int64_t n0 = static_cast<int64_t>(within / rows_in) * kTile;
-  const int t = order.t[blockIdx.y];
-  const int p0 = t - (S - 1) > 0 ? t - (S - 1) : 0, p1 = t < S - 1 ? t : S - 1;
+  const int t = jobs.t[blockIdx.y];
+  const int p0 = (t - (S - 1) > 0 ? t - (S - 1) : 0) + jobs.first[blockIdx.y];
   const int64_t ld = kI8Pad + static_cast<int64_t>(S) * kp;
-  int nst = static_cast<int>((p1 - p0 + 1) * kp / kStage);
+  int nst = static_cast<int>(jobs.count[blockIdx.y] * kp / kStage);
   const int odd = nst & 1;  // start one (zero) stage early
   nst += odd;
   const int64_t oa = kI8Pad + p0 * kp - odd * kStage, ob = kI8Pad + (S - 1 - t + p0) * kp - odd * kStage;
@@ -220,8 +225,18 @@ __global__ void __launch_bounds__(512, 1) level_gemm_i8_kernel(int64_t m, int64_
       for (int r = 0; r < 4; ++r) {
         const int64_t gi = m0 + wr * 128 + i * 16 + 4 * (lane >> 4) + r;
         const int64_t gj = n0 + wc * 64 + j * 16 + (lane & 15);
-        if (gi < m && gj < n) o[gi * n + gj] = acc[i][j][r];
+        if (gi < m && gj < n) {
+          if (split)
+            atomicAdd(o + gi * n + gj, acc[i][j][r]);  // exact: the level's bound covers every partial sum
+          else
+            o[gi * n + gj] = acc[i][j][r];
+        }
       }
+}
+
+__global__ void __launch_bounds__(256) zero_i32_kernel(int32_t* __restrict__ p, int64_t count) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count; i += stride) p[i] = 0;
 }
 
 }  // namespace
@@ -238,20 +253,49 @@ hipError_t launch_level_gemm_i8(int64_t m, int64_t n, int64_t kp, int S, int T, 
   const int64_t tiles_m = (m + kTile - 1) / kTile, tiles_n = (n + kTile - 1) / kTile;
   const int64_t ntiles = tiles_m * tiles_n;
   if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
-  // levels by pair count, heaviest first (ties in level order)
-  LevelOrder order{};
-  int cnt = 0;
-  for (int pairs = S; pairs >= 1; --pairs)
-    for (int t = 0; t <= T; ++t) {
-      const int p0 = t - (S - 1) > 0 ? t - (S - 1) : 0, p1 = t < S - 1 ? t : S - 1;
-      if (p1 - p0 + 1 == pairs) order.t[cnt++] = static_cast<uint8_t>(t);
+  // Jobs: every level whole, or, when the grid would hold few blocks (small
+  // outputs) and every pair is an even number of stages, each level split into
+  // chunks of at most c pairs that add their sums into zeroed planes; heaviest
+  // first (ties in level order).
+  auto pairs_of = [&](int t) {
+    const int p0 = t - (S - 1) > 0 ? t - (S - 1) : 0, p1 = t < S - 1 ? t : S - 1;
+    return p1 - p0 + 1;
+  };
+  int chunk = S;
+  const bool even = (kp / kStage) % 2 == 0;
+  if (even && ntiles * (T + 1) < 512) {
+    chunk = (S + 1) / 2;  // halves: on c1 (1024^2, S = 15) +11%; thirds and quarters lose to the atomics
+    for (;; ++chunk) {
+      int njobs = 0;
+      for (int t = 0; t <= T; ++t) njobs += (pairs_of(t) + chunk - 1) / chunk;
+      if (njobs <= 128) break;
     }
-  if (cnt != T + 1) return hipErrorInvalidValue;
+  }
+  const bool split = chunk < S;
+  Jobs jobs{};
+  int cnt = 0;
+  for (int size = chunk; size >= 1; --size)
+    for (int t = 0; t <= T; ++t)
+      for (int f = 0; f < pairs_of(t); f += chunk) {
+        const int c = pairs_of(t) - f < chunk ? pairs_of(t) - f : chunk;
+        if (c != size) continue;
+        if (cnt == 128) return hipErrorInvalidValue;
+        jobs.t[cnt] = static_cast<uint8_t>(t);
+        jobs.first[cnt] = static_cast<uint8_t>(f);
+        jobs.count[cnt] = static_cast<uint8_t>(c);
+        ++cnt;
+      }
+  if (!split && cnt != T + 1) return hipErrorInvalidValue;
+  if (split) {
+    const int64_t count = static_cast<int64_t>(T + 1) * m * n;
+    const int64_t blocks = (count + 255) / 256 < 4096 ? (count + 255) / 256 : 4096;
+    hipLaunchKernelGGL(zero_i32_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, G, count);
+  }
   // patches of 2 tile-rows for large outputs, 4 otherwise (measured on MI355X)
   const int group = ntiles >= 1024 ? 2 : 4;
-  hipLaunchKernelGGL(level_gemm_i8_kernel, dim3(static_cast<unsigned>(ntiles), static_cast<unsigned>(T + 1)),
+  hipLaunchKernelGGL(level_gemm_i8_kernel, dim3(static_cast<unsigned>(ntiles), static_cast<unsigned>(cnt)),
                      dim3(512), 0, stream, m, n, kp, S, static_cast<int>(tiles_n), static_cast<int>(ntiles), group,
-                     DA, DBt, G, order);
+                     DA, DBt, G, jobs, split ? 1 : 0);
   return hipGetLastError();
 }
 
