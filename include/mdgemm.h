@@ -168,7 +168,10 @@ int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const do
  * to 16; mp and np = m and n rounded up to 128; the first S combinations are the
  * digits, CA = CB = S for the pair schedule), the GEMM output planes f64[P][m][n]
  * (P = T+1 levels for the pair schedule, the schedule's planes for
- * MDGEMM_KARATSUBA). */
+ * MDGEMM_KARATSUBA).  With MDGEMM_INT8: EA, EB, flag, A's int8 digits
+ * [mp][128 + S kp] and B's [np][128 + S kp] (rows of 128 zero bytes and the S
+ * digits' k ranges; kp = k rounded up to 128, mp and np = m and n rounded up
+ * to 256), the int32 level planes [T+1][m][n]. */
 size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts);
 
 /* C = A.B with explicit options (opts may be NULL for the defaults).  Runs, in
