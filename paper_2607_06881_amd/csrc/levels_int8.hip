@@ -129,7 +129,7 @@ hipError_t run_blas(Blt* b, int64_t m, int64_t n, int64_t kp, int S, int T, cons
     const int64_t ld = kI8Pad + static_cast<int64_t>(S) * kp;
     const int8_t* mat1 = DBt + kI8Pad + static_cast<int64_t>(S - 1 - t + p0) * kp;  // K x n, ld (used transposed)
     const int8_t* mat2 = DA + kI8Pad + static_cast<int64_t>(p0) * kp;               // K x m, ld
-    int32_t* out = G + static_cast<int64_t>(t) * m * n;                    // n x m, ld n
+    int32_t* out = G + static_cast<int64_t>(t) * m * n;                              // n x m, ld n
     Layouts l;
     if (hipblasLtMatrixLayoutCreate(&l.a, HIP_R_8I, K, n, ld) != HIPBLAS_STATUS_SUCCESS ||
         hipblasLtMatrixLayoutCreate(&l.b, HIP_R_8I, K, m, ld) != HIPBLAS_STATUS_SUCCESS ||
@@ -223,7 +223,13 @@ hipError_t launch_levels_int8(int64_t m, int64_t n, int64_t kp, int S, int T, co
   hipError_t e = timed([&] { return launch_level_gemm_i8(m, n, kp, S, T, DA, DBt, G, stream); }, &t_own);
   if (e != hipSuccess) return e;
   e = timed([&] { return run_blas(b, m, n, kp, S, T, DA, DBt, G, stream); }, &t_blas);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess) {
+    // hipBLASLt has no algorithm for a level shape (or one failed to launch):
+    // keep the hand-written kernel, and recompute the planes with it
+    (void)hipGetLastError();
+    b->own.emplace(key, true);
+    return launch_level_gemm_i8(m, n, kp, S, T, DA, DBt, G, stream);
+  }
   b->own.emplace(key, t_own <= 1.03f * t_blas);  // ties (within 3%) go to the hand-written kernel
   return hipSuccess;
 }
