@@ -9,9 +9,8 @@ Flags:
 * ``-Xclang -target-feature -Xclang -packed-fp32-ops``: no packed-FP32
   instructions are generated (none of these kernels needs them).
 
-The library links hipBLASLt, the alternative route for the int8 level
-products of the MDGEMM_INT8 option (used where it measures faster than the
-int8 kernel built here; the FP64 path uses only the kernels built here).
+Every kernel of the library is built here from its sources; it links no
+vendor BLAS.
 """
 
 from __future__ import annotations
@@ -70,7 +69,7 @@ def build(verbose: bool = False) -> str:
         for fut in [pool.submit(_run, cmd, verbose) for cmd in cmds]:
             fut.result()
     tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=gfx950", "-fPIC", "-shared", "-o", tmp, *objs, "-lhipblaslt"], verbose)
+    _run([HIPCC, "--offload-arch=gfx950", "-fPIC", "-shared", "-o", tmp, *objs], verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -5,10 +5,8 @@ int8 matrix products with int32 sums, so the digits, the levels and the limbs
 must equal the oracle's chain at the same width bit for bit, and equal the
 FP64 path run with the same width, digit count and cutoff.  Sizes span ragged
 shapes (n not a multiple of 16, k not a multiple of 16) and every limb count
-the option supports.  The level products run on the hand-written int8 kernel or
-on hipBLASLt (chosen per shape by timing); the route tests force each one
-(MDGEMM_INT8_LEVELS) on shapes with odd stage counts, ragged tiles and many
-levels.
+the option supports.  The level products run on the hand-written int8 kernel;
+the shape tests cover odd stage counts, ragged tiles and many levels.
 """
 
 import ctypes
@@ -104,13 +102,11 @@ def test_int8_larger_products(L, m, k, n, seed):
         assert list(C[:, i, j]) == r["limbs"], (i, j)
 
 
-@pytest.mark.parametrize("route", ["mfma", "hipblaslt"])
 @pytest.mark.parametrize("L,m,k,n,seed", [(2, 300, 700, 257, 70), (3, 520, 1100, 300, 71), (2, 1000, 2000, 777, 60),
                                           (8, 64, 128, 8192, 72), (4, 257, 129, 513, 73), (1, 3, 5, 2, 74)])
-def test_int8_both_routes(route, L, m, k, n, seed, monkeypatch):
-    monkeypatch.setenv("MDGEMM_INT8_LEVELS", route)
+def test_int8_shapes(L, m, k, n, seed):
     w, S, T = md.mdgemm_plan(m, n, k, L, flags=I8)
-    print(f"[case] int8 route={route} L={L} {m}x{k}x{n} w={w} S={S} T={T}", flush=True)
+    print(f"[case] int8 L={L} {m}x{k}x{n} w={w} S={S} T={T}", flush=True)
     A, B = _operands(L, m, k, n, seed)
     C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), flags=I8))
     assert np.array_equal(C, _fp64_same_digits(A, B, w, S, T, 0))
@@ -153,23 +149,40 @@ def test_int8_workspace_stream_and_stage_times():
 
 
 @pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")  # the refused call leaves the graph empty
-def test_int8_refused_under_graph_capture():
+def test_int8_graph_capture():
+    # With a caller workspace the int8 product (zeroing by kernel, no memsets,
+    # no synchronization) is captured into a HIP graph, and every replay, with
+    # eager work in between, equals the eager result; with the library's own
+    # buffer it is refused under capture like the FP64 path.
     print("[case] int8 under graph capture", flush=True)
     L, m, k, n = 2, 64, 64, 64
     A, B = _operands(L, m, k, n, 80)
     Ag, Bg = _gpu(A), _gpu(B)
-    C = torch.empty((L, m, n), dtype=torch.float64, device=DEV)
-    ws = torch.empty(md.mdgemm_workspace_bytes(m, n, k, L, flags=I8), dtype=torch.uint8, device=DEV)
-    s = torch.cuda.Stream()
-    o = md.make_opts(flags=I8, stream=s, workspace=ws)
-    torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g, stream=s):
-        st = md.lib().mdgemm_ex(m, n, k, L, Ag.data_ptr(), Bg.data_ptr(), C.data_ptr(), ctypes.byref(o))
-    assert st == md.MDGEMM_EINVAL
-    # outside capture the same call works
     want = _host(md.mdgemm_ex(Ag, Bg, flags=I8))
     assert np.array_equal(want, pipeline.full_reference(A, B, 15, 14, 7)["C"])
+    C = torch.empty((L, m, n), dtype=torch.float64, device=DEV)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    g0 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g0, stream=s):
+        o = md.make_opts(flags=I8, stream=s)
+        st = md.lib().mdgemm_ex(m, n, k, L, Ag.data_ptr(), Bg.data_ptr(), C.data_ptr(), ctypes.byref(o))
+    assert st == md.MDGEMM_EINVAL
+    ws = torch.empty(md.mdgemm_workspace_bytes(m, n, k, L, flags=I8), dtype=torch.uint8, device=DEV)
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        md.mdgemm_ex(Ag, Bg, C, workspace=ws, flags=I8)  # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        md.mdgemm_ex(Ag, Bg, C, workspace=ws, flags=I8)
+    for r in range(4):
+        C.fill_(7.0)
+        md.mdgemm_ex(Ag, Bg, workspace=ws, flags=I8)  # eager work between replays
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(C.cpu().numpy(), want), r
 
 
 def test_int8_zero_lines_k0_and_extreme_magnitudes():
@@ -204,11 +217,8 @@ def test_int8_degenerate_shapes(m, k, n):
     assert np.array_equal(C, pipeline.full_reference(A, B, S, T, w)["C"])
 
 
-@pytest.mark.parametrize("route", ["auto", "mfma", "hipblaslt"])
 @pytest.mark.parametrize("signs", ["same", "mixed"])
-def test_int8_at_the_int32_limit(signs, route, monkeypatch):
-    if route != "auto":
-        monkeypatch.setenv("MDGEMM_INT8_LEVELS", route)
+def test_int8_at_the_int32_limit(signs):
     # k = 8876 is the largest k with 15 pairs k 127^2 < 2^31 at w = 7 (checked
     # on the CPU).  Elements of value 1 - 2^-105 (the double-double (1, -2^-105))
     # have digits 63, 127, 127, ..., 127 on their grid, so the middle levels sum
