@@ -18,16 +18,17 @@ Prints one JSON line:
   wider digits whose level sums stay exact at this k; at least the digit bits of
   four 13-bit digits per limb), timed over a few steps; the headline ``value``
   keeps the workload's 13-bit digits unless ``--slice-bits`` says otherwise;
-* ``karatsuba`` and ``karatsuba_adaptive``: the same workload with the Karatsuba
-  schedule of the level products (fewer GEMMs of digit sums, the levels formed
-  exactly from their planes, bit-identical results), with the 13-bit digits and
-  with the adaptive width; the headline keeps the paper's pair schedule unless
-  ``--schedule karatsuba`` says otherwise;
-* ``int8``: the same workload with the level products on the int8 matrix
-  cores (MDGEMM_INT8: digits of at most 7 bits, one int8 GEMM with exact int32
-  sums per level, the same exact accumulation), its level GEMMs against the
-  5.0 POP/s dense int8 peak (``--products int8`` times that mode as the main
-  line instead, its roofline against the int8 peak);
+* ``calibration``: the FP64 MFMA rate and the HBM copy rate measured on the
+  same device in the same run (the library's probe kernels), beside the
+  published 78.6 TFLOP/s and 8 TB/s; ``roofline.frac_of_measured`` and each
+  stage's ``frac_of_copy`` are taken against them;
+* ``parity``: outside the timed region, the last timed step's C at sampled
+  entries (corners, the rows and columns of extreme exponents, random ones)
+  against the CPU oracle's chain (bit-exact limbs) and against the exact
+  rational product (largest error over the stated tolerance);
+* ``--extras`` adds ``karatsuba``, ``karatsuba_adaptive`` (the Karatsuba
+  schedule of the level products, bit-identical results) and ``int8`` (the
+  level products on the int8 matrix cores) lines;
 * ``cpu_baseline``: the CPU oracle's classic multiple-double GEMM (one
   sequential inner product per element, all host cores) timed on a bounded
   sample of the same product's rows.
@@ -50,16 +51,22 @@ MFMA_F64_PEAK_TFLOPS = 78.6  # MI355X dense FP64 matrix peak (published)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E (published)
 INT8_PEAK_TOPS = 5000.0  # MI355X dense int8 matrix peak (published)
 METRIC = "effective dd/qd GEMM GFLOP/s; % FP64 MFMA peak; bit-exact+tol vs CPU oracle"
-# the level-GEMM kernel is built from these sources (its job table is declared in internal.h)
-GEMM_SOURCES = [os.path.join(ROOT, "paper_2607_06881_amd", "csrc", f) for f in ("slice_gemm.hip", "internal.h")]
+# the level-GEMM kernel is built from its source and the tile constants of internal.h
+GEMM_SOURCE = os.path.join(ROOT, "paper_2607_06881_amd", "csrc", "slice_gemm.hip")
+GEMM_CONSTANTS = os.path.join(ROOT, "paper_2607_06881_amd", "csrc", "internal.h")
 DEFAULT_CONFIG = "c2"
 
 
-def kernel_source_hash(paths=GEMM_SOURCES) -> str:
+def kernel_source_hash() -> str:
+    """First 16 hex digits of the sha256 of the level-GEMM source followed by the
+    lines of internal.h that define its tile constants (``constexpr int kTile``)."""
     h = hashlib.sha256()
-    for path in paths:
-        with open(path, "rb") as fh:
-            h.update(fh.read())
+    with open(GEMM_SOURCE, "rb") as fh:
+        h.update(fh.read())
+    with open(GEMM_CONSTANTS, "rb") as fh:
+        for ln in fh:
+            if ln.lstrip().startswith(b"constexpr int kTile"):
+                h.update(ln)
     return h.hexdigest()[:16]
 
 
@@ -81,6 +88,83 @@ def stored_traffic(config: str):
         return float(vals["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def calibrate(md, torch, dev, stream):
+    """Measured FP64 MFMA rate (TFLOP/s) and copy rate (GB/s, read + write) of this device."""
+    sink = torch.empty(2048 * 256, dtype=torch.float64, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    md.mdgemm_probe_mfma_f64(sink, 200, stream=stream)  # warm-up
+    e0.record(stream)
+    flops = md.mdgemm_probe_mfma_f64(sink, 20000, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    mfma = flops / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    del sink
+    n = 1 << 28  # 2 GiB per buffer
+    src = torch.ones(n, dtype=torch.float64, device=dev)
+    dst = torch.empty_like(src)
+    md.mdgemm_probe_copy(src, dst, stream=stream)
+    e0.record(stream)
+    reps = 5
+    for _ in range(reps):
+        md.mdgemm_probe_copy(src, dst, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    copy = 2.0 * 8.0 * n * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    return {"mfma_f64_TFLOP/s": round(mfma, 2), "mfma_f64_published_TFLOP/s": MFMA_F64_PEAK_TFLOPS,
+            "copy_GB/s": round(copy, 1), "hbm_published_GB/s": HBM_PEAK_GBS,
+            "probes": "mdgemm_probe_mfma_f64 (2048 x 256 threads, 8 independent v_mfma_f64_16x16x4f64 chains per "
+                      "wave, 20000 rounds); mdgemm_probe_copy (2 GiB, read + write bytes, 5 copies)"}
+
+
+def parity(w, A_h, B_h, C_h, S, T, bits, count=32):
+    """The timed product's C at sampled entries against the CPU oracle (test
+    infrastructure, outside the timed region): bit-exact greedy limbs of the
+    oracle's chain, and the error against the exact rational product over the
+    stated tolerance 4 k 2^-(53L-4) (|A||B|)_ij."""
+    import numpy as np
+
+    from oracle import coracle, exact, pipeline
+
+    L, m, k = A_h.shape
+    n = B_h.shape[2]
+    EA, EB = coracle.exponents(A_h[0], 0), coracle.exponents(B_h[0], 1)
+    rng = np.random.default_rng(w.seed + 1000)
+    rows = {0, m - 1, int(np.argmin(EA)), int(np.argmax(EA))}
+    cols = {0, n - 1, int(np.argmin(EB)), int(np.argmax(EB))}
+    entries = {(i, j) for i in rows for j in cols}
+    while len(entries) < count:
+        entries.add((int(rng.integers(m)), int(rng.integers(n))))
+    entries = sorted(entries)
+    t0 = time.perf_counter()
+    ref = pipeline.reference_entries(A_h, B_h, S, T, entries, bits)
+    mismatch = [e for e in entries if C_h[:, e[0], e[1]].tolist() != ref[e]["limbs"]]
+    worst = 0.0
+    for (i, j) in entries:
+        want, mag = exact.exact_product(A_h, B_h, i, j)
+        err = abs(exact.value(C_h[:, i, j]) - want)
+        bound = exact.tolerance(k, L, mag)
+        if bound > 0:
+            worst = max(worst, float(err / bound))
+        elif err != 0:
+            worst = float("inf")
+    return {"entries": len(entries), "bit_exact_vs_oracle": not mismatch, "mismatches": len(mismatch),
+            "max_err_over_tolerance": worst, "within_tolerance": worst <= 1.0,
+            "tolerance": "4 k 2^-(53L-4) (|A||B|)_ij vs the exact rational product",
+            "seconds": round(time.perf_counter() - t0, 2)}
 
 
 def cpu_baseline(w, A, B, target_s: float):
@@ -110,6 +194,7 @@ def cpu_baseline(w, A, B, target_s: float):
         "value": flops / dt / 1e9,
         "unit": "GFLOP/s",
         "cores": int(used),
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "sample": f"classic {'double-double (Dekker/Hida-Li-Bailey add+mul)' if w.limbs == 2 else f'{w.limbs}-limb exact-expansion'}"
                   f" GEMM, rows 0..{rows - 1} of C ({rows} x {w.n} x {w.k}), {dt:.1f} s on {used} threads",
@@ -137,6 +222,10 @@ def main(argv=None) -> int:
     ap.add_argument("--schedule", choices=("pairs", "karatsuba"), default="pairs",
                     help="schedule of the level products of the timed product: the paper's digit pairs (default) "
                          "or the Karatsuba schedule")
+    ap.add_argument("--extras", action="store_true",
+                    help="also time the Karatsuba schedule and the int8 level products beside the headline")
+    ap.add_argument("--no-calibration", action="store_true", help="skip the MFMA and copy probes")
+    ap.add_argument("--no-parity", action="store_true", help="skip the sampled parity check of the timed C")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, run 3 device copies of this many MiB (calibrates the HBM byte "
                          "counters of a profiler run against a known size)")
@@ -208,6 +297,7 @@ def main(argv=None) -> int:
     opts = {"range_bits": w.range_bits} if int8 and w.range_bits else ({} if int8 else mode_opts(bits_arg))
     bits, S, T = md.mdgemm_plan(w.m, w.n, w.k, w.limbs, flags=sched_flags, **opts)
     ms_per_step, stage_ms = measure(opts, args.steps, args.warmup, sched_flags)
+    C_h = None if args.no_parity else C.cpu().numpy()  # the last timed step's product, for the parity check
 
     if args.copy_probe_mib > 0:
         src = torch.ones(args.copy_probe_mib * (1 << 20) // 8, dtype=torch.float64, device=dev)
@@ -254,9 +344,8 @@ def main(argv=None) -> int:
     if int8:
         roofline.update({"peak": INT8_PEAK_TOPS, "unit": "TOP/s", "frac": round(achieved / INT8_PEAK_TOPS, 4),
                          "traffic": None,
-                         "kernel": f"int8 level products ({T + 1} levels, int32 sums): level_gemm_i8_kernel in one "
-                                   "launch, or one hipBLASLt GEMM per level where that measured faster; duration "
-                                   "of all of them per step",
+                         "kernel": f"level_gemm_i8_kernel: int8 level products ({T + 1} levels, int32 sums) "
+                                   "in one launch",
                          "ops_per_step": roofline.pop("flops_per_launch"),
                          "avg_step_ms": roofline.pop("avg_launch_ms")})
     stages = {
@@ -337,13 +426,24 @@ def main(argv=None) -> int:
             "level_gemm_TOPS": round(tops, 1), "frac": round(tops / INT8_PEAK_TOPS, 4),
         }
 
+    if not args.no_parity:
+        out["parity"] = parity(w, A_h, B_h, C_h, S, T, bits)
+    if not args.no_calibration:
+        cal = calibrate(md, torch, dev, stream)
+        out["calibration"] = cal
+        roofline["peak_measured"] = cal["mfma_f64_TFLOP/s"]
+        roofline["frac_of_measured"] = round(achieved / cal["mfma_f64_TFLOP/s"], 4)
+        for key in ("exponents", "split", "accum_renorm"):
+            stages[key]["frac_of_copy"] = round(stages[key]["GB/s"] / cal["copy_GB/s"], 4)
     if bits_arg == 13 and not sched_flags and args.adaptive_steps > 0:
-        # the same workload with the adaptive width and with the Karatsuba
-        # schedule, reported beside the paper's 13-bit digit pairs
+        # the same workload with the adaptive width reported beside the paper's
+        # 13-bit digit pairs (and, on request, the Karatsuba schedule and the
+        # int8 level products)
         out["adaptive_width"] = extra(mode_opts(md.MDGEMM_SLICE_BITS_AUTO), 0)
-        out["karatsuba"] = extra(mode_opts(13), md.MDGEMM_KARATSUBA)
-        out["karatsuba_adaptive"] = extra(mode_opts(md.MDGEMM_SLICE_BITS_AUTO), md.MDGEMM_KARATSUBA)
-        out["int8"] = int8_mode()
+        if args.extras:
+            out["karatsuba"] = extra(mode_opts(13), md.MDGEMM_KARATSUBA)
+            out["karatsuba_adaptive"] = extra(mode_opts(md.MDGEMM_SLICE_BITS_AUTO), md.MDGEMM_KARATSUBA)
+            out["int8"] = int8_mode()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, A_h, B_h, args.cpu_seconds)
     print(json.dumps(out), flush=True)

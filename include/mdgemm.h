@@ -56,11 +56,11 @@ extern "C" {
 
 /* ---- limits ---------------------------------------------------------------- */
 #define MDGEMM_MAX_LIMBS 16   /* double (1), double-double (2), ... quad (4), octo (8), hexa double (16) */
-#define MDGEMM_MAX_SLICES 64  /* digits per element */
-#define MDGEMM_MAX_LEVELS 127 /* 2 * MDGEMM_MAX_SLICES - 1 */
+#define MDGEMM_MAX_SLICES 68  /* digits per element */
+#define MDGEMM_MAX_LEVELS 135 /* 2 * MDGEMM_MAX_SLICES - 1 */
 #define MDGEMM_SLICE_BITS 13      /* digit width of section 2 */
 #define MDGEMM_MAX_SLICE_BITS 26  /* widest digit: a product of two stays below 2^52 */
-#define MDGEMM_MAX_DIGIT_BITS 844 /* slices * slice_bits + 52 <= 14 64-bit words */
+#define MDGEMM_MAX_DIGIT_BITS 908 /* slices * slice_bits + 52 <= 15 64-bit words */
 #define MDGEMM_Z_WORDS 28         /* 64-bit words per element written by mdgemm_accumulate */
 
 /* slice_bits selector for mdgemm_opts.slice_bits (else an explicit width 1..26) */
@@ -82,7 +82,7 @@ typedef struct mdgemm_opts {
   void* stream;           /* hipStream_t to launch on; NULL = default stream */
   void* workspace;        /* caller-owned device buffer; NULL = library-owned buffer (see below) */
   size_t workspace_bytes; /* size of `workspace` in bytes */
-  int slices_per_limb;    /* 13-bit digits per limb, S = limbs * slices_per_limb <= 64; 0 = 4 */
+  int slices_per_limb;    /* 13-bit digits per limb, S = limbs * slices_per_limb; 0 = the default count (below) */
   int cutoff;             /* largest kept p + q; MDGEMM_CUTOFF_DEFAULT or _ALL or 0..2S-2 */
   unsigned flags;         /* MDGEMM_CHECK_FINITE, _SYNC, _TIME_STAGES, _KARATSUBA, _KARATSUBA_MIN_TERMS, _INT8 */
   int slice_bits;         /* digit width w: 0 = 13 (section 2), 1..26, or MDGEMM_SLICE_BITS_AUTO */
@@ -98,16 +98,22 @@ typedef struct mdgemm_opts {
  * would keep an address that a later, larger call may free). */
 
 /* Digit width and count.
- *  - slice_bits 0 or 13: w = 13 and S = slices, else limbs * slices_per_limb.
+ *  - The default count of 13-bit digits, S13(L): four per limb up to quad
+ *    doubles (section 2's quarters, 52 L bits, which cover the 53 L - 4 bits of
+ *    the tolerance 4 k 2^-(53 L - 4) (|A||B|)); for five or more limbs, where four
+ *    per limb fall short of those bits, ceil((53 L - 4) / 13) + 1 (one guard digit
+ *    for the levels dropped at T = S - 1): 34 for octo and 66 for hexa doubles.
+ *  - slice_bits 0 or 13: w = 13 and S = slices, else limbs * slices_per_limb,
+ *    else (slices_per_limb 0) S13(L).
  *  - slice_bits 1..26 (the adaptive width, wider digits and fewer of them): S =
- *    slices, else ceil(52 limbs / w), the digit bits of four 13-bit digits per limb.
+ *    slices, else ceil(13 S13(L) / w), at least the digit bits of the default.
  *  - MDGEMM_SLICE_BITS_AUTO (slices must be 0): among w = 13..26 with
- *    S = ceil(52 limbs / w) and the requested cutoff (T = S - 1 by default), those
+ *    S = ceil(13 S13(L) / w) and the requested cutoff (T = S - 1 by default), those
  *    whose levels stay exact (max pairs of a level times k (2^w - 1)^2 < 2^53), the
  *    one with the fewest pairs, the wider on a tie; MDGEMM_EEXACT when none
  *    qualifies.  Double-double at k = 4096 gets w = 19,
  *    S = 6 (21 pairs instead of 36); the digits cover at least as many bits as
- *    four 13-bit digits per limb, so the product is at least as accurate.
+ *    the default 13-bit digits, so the product is at least as accurate.
  * Range balancing (section 3, grouping by exponent so that smaller numbers keep
  * their bits): with range_bits > 0 every line keeps its one grid and gets
  * D = ceil(range_bits / w) more digits, S = S0 + D where S0 is the count above,
@@ -117,33 +123,25 @@ typedef struct mdgemm_opts {
  * its own leading level.  With MDGEMM_SLICE_BITS_AUTO the width is chosen for the
  * fewest pairs of (S, T) including D.  mdgemm_line_spread measures the range of
  * the data.
- * In every case S <= 64 and S w <= MDGEMM_MAX_DIGIT_BITS.
+ * In every case S <= MDGEMM_MAX_SLICES and S w <= MDGEMM_MAX_DIGIT_BITS; the Karatsuba
+ * schedules combine at most 64 digits (products with more keep the pair schedule).
  *
  * MDGEMM_INT8.  The level sums of section 2 are exact integer sums, so with
  * digits of at most 7 bits (|d| <= 127) they are formed on the int8 matrix cores
  * with exact int32 sums over the contiguous digit ranges of each level's pairs,
  * which requires max pairs of a level times k (2^w - 1)^2 < 2^31.  slice_bits 0
  * or MDGEMM_SLICE_BITS_AUTO: the widest w <= 7 whose levels stay exact for this k,
- * S = ceil(52 limbs / w) (plus the range digits), T by the cutoff rules above
+ * S = ceil(13 S13(L) / w) (plus the range digits), T by the cutoff rules above
  * (T = S - 1 by default); slice_bits 1..7: that width; wider, the Karatsuba flags,
  * or S > 64 (more than 8 limbs at w = 7) return MDGEMM_EINVAL, and no exact width
  * MDGEMM_EEXACT.  Digits, levels and C are bit-identical to the FP64 path run
  * with the same slice_bits, slices and cutoff.  Double-double at k = 4096:
  * w = 7, S = 15, T = 14 (120 pairs).  The level products run on the library's
- * own int8 kernel (all levels in one launch) or as one hipBLASLt GEMM per level:
- * the first call on a new shape (m, n, k, S, T) times both (hipBLASLt with the
- * fastest of its candidate algorithms per level, also timed then) and keeps the
- * own kernel unless hipBLASLt is more than 3% faster; that call synchronizes its
- * stream.  The environment variable MDGEMM_INT8_LEVELS=mfma or =hipblaslt,
- * read on every call, forces one route (the results are the same).  Besides the
- * workspace the library keeps, per device, a hipBLASLt handle (with whatever
- * hipBLASLt holds for it), created on the first such call, the algorithm per
- * GEMM shape and the route per product shape, until the process ends.  Refused
- * with MDGEMM_EINVAL
- * while the stream captures a graph. */
+ * own int8 kernel, all levels in one launch. */
 
-/* Fill `opts` with the defaults: default stream, library workspace, 4 slices per
- * limb of 13 bits, cutoff T = S - 1, no range balancing, no flags. */
+/* Fill `opts` with the defaults: default stream, library workspace, the default
+ * count S13(L) of 13-bit digits (slices_per_limb 0), cutoff T = S - 1, no range
+ * balancing, no flags. */
 void mdgemm_opts_init(mdgemm_opts* opts);
 
 /* The digit width, digit count and cutoff mdgemm_ex uses for this product and
@@ -152,8 +150,8 @@ void mdgemm_opts_init(mdgemm_opts* opts);
 int mdgemm_plan(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts, int* slice_bits, int* slices,
                 int* cutoff);
 
-/* C = A.B for L-limb operands (L = limbs in 1..16) with the default options (13-bit
- * digits, four per limb).
+/* C = A.B for L-limb operands (L = limbs in 1..16) with the default options (the
+ * default count S13(L) of 13-bit digits, T = S - 1).
  * m, n, k >= 0; m == 0 or n == 0 does nothing; k == 0 writes C = +0.0; m and n at
  * most 2^27 (MDGEMM_EINVAL beyond).
  * Returns MDGEMM_OK or a negative status. */
@@ -174,11 +172,33 @@ int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const do
  * to 256), the int32 level planes [T+1][m][n]. */
 size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts);
 
+#define MDGEMM_LAYOUT_INFO 12 /* entries written by mdgemm_workspace_layout */
+
+/* Where mdgemm_ex keeps each stage's output inside a caller workspace, for
+ * checking a product's intermediate results (the workspace is not cleared
+ * after the call, so after mdgemm_ex returns and its stream is synchronized
+ * the parts hold that call's exponents, digits and level products).  Host
+ * only.  Writes min(count, MDGEMM_LAYOUT_INFO) values:
+ *   info[0] byte offset of EA int32[m],   info[1] of EB int32[n],
+ *   info[2] of A's digit panels [CA][kp][mp] (A transposed: [s][kk][i] = digit s
+ *     of A[i][kk]), info[3] of B's digit panels [CB][kp][np] ([s][kk][j] = digit
+ *     s of B[kk][j]); the first S panels are the digits, zero padded,
+ *   info[4] of the output planes f64 [P][m][n] (the levels G_t, t = 0..T, when
+ *     info[10] == 1),
+ *   info[5] bytes per panel value (4: FP32, 8: FP64), info[6] kp, info[7] mp,
+ *   info[8] np, info[9] P, info[10] 1 for the pair schedule (planes = levels),
+ *   info[11] mdgemm_workspace_bytes().
+ * Returns the count written, MDGEMM_EEXACT, or MDGEMM_EINVAL (also for an empty
+ * product and with MDGEMM_INT8, whose layout is not described here). */
+int mdgemm_workspace_layout(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts, int64_t* info,
+                            int count);
+
 /* C = A.B with explicit options (opts may be NULL for the defaults).  Runs, in
  * stream order: row exponents of A and column exponents of B, the splits of A
  * and B into digits, the level GEMMs, and the exact accumulation and rounding
  * into C.  With a caller workspace smaller than mdgemm_workspace_bytes() it
- * returns MDGEMM_EWORKSPACE and launches nothing. */
+ * returns MDGEMM_EWORKSPACE, and with one that overlaps A, B or C it returns
+ * MDGEMM_EINVAL; in both cases it launches nothing. */
 int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
               const mdgemm_opts* opts);
 
@@ -346,6 +366,22 @@ int mdgemm_accumulate(int64_t m, int64_t n, int levels, int slice_bits, const do
  * EB int32[n], C [limbs][m][n] (limbs 1..16). */
 int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, int slice_bits, const double* G,
                         const int32_t* EA, const int32_t* EB, double* C, void* stream);
+
+/* ---- calibration (measurement aids, not part of the product) ---------------
+ * The rates the stages are measured against, on the caller's device. */
+
+/* Launches `blocks` workgroups of 256 threads that each run `iters` rounds of
+ * eight independent v_mfma_f64_16x16x4f64 per wave (no memory traffic in the
+ * loop) and write one double per thread to sink [blocks * 256] (device memory).
+ * Time it with events on `stream` to measure the sustainable FP64 MFMA rate.
+ * Returns the FP64 flops the launch performs (2 * 16 * 16 * 4 per instruction),
+ * or a negative status (blocks in 1 .. 2^24, iters >= 1). */
+int64_t mdgemm_probe_mfma_f64(int64_t blocks, int64_t iters, double* sink, void* stream);
+
+/* dst[0 .. count) = src[0 .. count) with 32-byte vector loads and stores
+ * (count a multiple of 4, both pointers 32-byte aligned, not overlapping):
+ * reads and writes 8 count bytes each, the HBM rate of a plain stream. */
+int mdgemm_probe_copy(const double* src, double* dst, int64_t count, void* stream);
 
 #ifdef __cplusplus
 }

@@ -219,16 +219,34 @@ def method_bound(A: np.ndarray, B: np.ndarray, i: int, j: int, S: int, T: int, E
     return trunc + dropped + 2 * two ** (-53 * L) * (mag + trunc + dropped)
 
 
-def adaptive_width(L: int, k: int, max_digit_bits: int = 844):
-    """(w, S) of the adaptive slice width: among w = 13..26 with S = ceil(52 L / w)
-    digits (the bits of four 13-bit digits per limb) such that every level with
-    T <= S - 1 stays exact, S k (2^w - 1)^2 < 2^53 (the bound (NBound) of
-    section 2 with w-bit digits), the fewest pairs S (S + 1) / 2, the wider digit
-    on a tie; S <= 64 and S w <= max_digit_bits.  None when no width qualifies."""
+MAX_SLICES = 68  # digits per element
+MAX_DIGIT_BITS = 908  # digits times width
+
+
+def default_slices(L: int) -> int:
+    """The default number of 13-bit digits of an L-limb element.  Up to four limbs
+    the paper's four quarters per limb (section 2), 52 L bits, at least the 53 L - 4
+    bits that the tolerance 4 k 2^-(53 L - 4) (|A||B|) asks for.  From five limbs
+    on, four quarters per limb give fewer bits than that; the count is then the
+    smallest number of 13-bit digits holding 53 L - 4 bits, plus one more for the
+    levels that the cutoff T = S - 1 leaves out."""
+    if L <= 4:
+        return 4 * L
+    return math.ceil((53 * L - 4) / 13) + 1
+
+
+def adaptive_width(L: int, k: int, max_digit_bits: int = MAX_DIGIT_BITS):
+    """(w, S) of the adaptive slice width: among w = 13..26 with S = ceil(13 S13 / w)
+    digits (S13 = default_slices(L): the bits of the default 13-bit digits) such
+    that every level with T <= S - 1 stays exact, S k (2^w - 1)^2 < 2^53 (the bound
+    (NBound) of section 2 with w-bit digits), the fewest pairs S (S + 1) / 2, the
+    wider digit on a tie; S <= 68 and S w <= max_digit_bits.  None when no width
+    qualifies."""
     best = None
+    bits = 13 * default_slices(L)
     for w in range(13, 27):
-        S = -(-52 * L // w)
-        if S > 64 or S * w > max_digit_bits or S * k * (2**w - 1) ** 2 >= 2**53:
+        S = -(-bits // w)
+        if S > MAX_SLICES or S * w > max_digit_bits or S * k * (2**w - 1) ** 2 >= 2**53:
             continue
         key = (S * (S + 1) // 2, -w)
         if best is None or key < best[0]:
@@ -258,13 +276,14 @@ def _max_pairs(S: int, T: int) -> int:
     return max(len(pairs_of_level(t, S)) for t in range(T + 1))
 
 
-def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_limb: int = 4, cutoff: int = -1,
+def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_limb: int = 0, cutoff: int = -1,
          range_bits: int = 0, int8: bool = False):
     """(w, S, T) of the product's digit width, digit count and cutoff, or None when
     the levels cannot stay exact.  Written from the options' definitions:
 
-    * w = 13 (slice_bits 0 or 13): S0 = slices or slices_per_limb L;
-      w explicit: S0 = slices or ceil(52 L / w);
+    * w = 13 (slice_bits 0 or 13): S0 = slices, or slices_per_limb L, or
+      (slices_per_limb 0) default_slices(L);
+      w explicit: S0 = slices or ceil(13 default_slices(L) / w);
       automatic (slice_bits -1): the width of 13..26 with the fewest pairs of the
       resulting (S, T) among those whose levels stay exact, the wider on a tie;
     * range balancing: D = ceil(range_bits / w) more digits, S = S0 + D, default
@@ -274,12 +293,15 @@ def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_lim
     * int8 (level sums in int32 on the int8 matrix cores): digits of at most 7
       bits; slice_bits 0 or -1 take the widest w = 7, 6, ..., 1 whose (S, T) is
       valid and whose level sums stay below 2^31 (the same bound with 2^31 in
-      place of 2^53), slice_bits 1..7 that width, S0 = slices or ceil(52 L / w).
-    Raises ValueError for invalid options (S > 64, S w > 844, ...)."""
+      place of 2^53), slice_bits 1..7 that width, S0 = slices or
+      ceil(13 default_slices(L) / w), at most 64 digits.
+    Raises ValueError for invalid options (S > 68, S w > 908, ...)."""
+    bits = 13 * default_slices(L)
+
     def finish(w, S0):
         D = -(-range_bits // w)
         S = S0 + D
-        if S < 1 or S > 64 or S * w > 844:
+        if S < 1 or S > (64 if int8 else MAX_SLICES) or S * w > MAX_DIGIT_BITS:
             raise ValueError("digit count")
         T = S0 - 1 + 2 * D if cutoff == -1 else (2 * S - 2 if cutoff == -2 else cutoff)
         if not 0 <= T <= 2 * S - 2:
@@ -301,7 +323,7 @@ def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_lim
             sized = False
             for w in range(7, 0, -1):
                 try:
-                    cand = finish(w, -(-52 * L // w))
+                    cand = finish(w, -(-bits // w))
                 except ValueError:
                     continue
                 sized = True
@@ -312,7 +334,7 @@ def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_lim
             return None
         if not 1 <= slice_bits <= 7:
             raise ValueError("width")
-        cand = finish(slice_bits, slices or -(-52 * L // slice_bits))
+        cand = finish(slice_bits, slices or -(-bits // slice_bits))
         return cand if exact32(*cand) else None
 
     if slice_bits == -1:
@@ -321,7 +343,7 @@ def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_lim
         best = None
         for w in range(13, 27):
             try:
-                cand = finish(w, -(-52 * L // w))
+                cand = finish(w, -(-bits // w))
             except ValueError:
                 continue
             if not exact_ok(*cand):
@@ -334,9 +356,9 @@ def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_lim
     if not 1 <= w <= 26:
         raise ValueError("width")
     if w == 13:
-        S0 = slices or slices_per_limb * L
+        S0 = slices or (slices_per_limb * L if slices_per_limb else default_slices(L))
     else:
-        S0 = slices or -(-52 * L // w)
+        S0 = slices or -(-bits // w)
     cand = finish(w, S0)
     return cand if exact_ok(*cand) else None
 

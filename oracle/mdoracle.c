@@ -412,7 +412,7 @@ static int split_one(const double* x, int64_t ls, int L, int E, int S, int w, do
  * (per row for axis 0, per column for axis 1), written to D [S][rows][cols]. */
 int oracle_split_bits(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
                       double* D) {
-  if (rows < 0 || cols < 0 || L < 1 || L > 16 || S < 1 || S > 64 || w < 1 || w > 26 || (axis != 0 && axis != 1))
+  if (rows < 0 || cols < 0 || L < 1 || L > 16 || S < 1 || S > 128 || w < 1 || w > 26 || (axis != 0 && axis != 1))
     return ORACLE_EINVAL;
   int64_t plane = rows * cols;
   int status = ORACLE_OK;

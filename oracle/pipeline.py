@@ -64,6 +64,30 @@ def levels_of_entry(da: np.ndarray, db: np.ndarray, T: int) -> list:
     return G
 
 
+def levels_rewritten(DA: np.ndarray, DB: np.ndarray, T: int) -> np.ndarray:
+    """Level products G [T+1][m][n] (float64, integer valued) of whole digit
+    planes DA [S][m][k], DB [S][k][n], one float64 matrix product per level.
+
+    Level t is block column t of the rewritten product of section 2 (the
+    stacked parts of A times the block-Toeplitz parts of B):
+    G_t = [DA_p0 .. DA_p1] . [DB_(t-p0); ..; DB_(t-p1)] over the pairs p + q = t.
+    Every product of two digits and every partial sum is an integer below 2^53
+    under the exactness condition pairs * k * (2^w - 1)^2 < 2^53, so the matrix
+    product (a library routine, any summation order) is exact."""
+    S, m, k = DA.shape
+    n = DB.shape[2]
+    G = np.empty((T + 1, m, n), dtype=np.float64)
+    for t in range(T + 1):
+        ps = [p for p, _ in exact.pairs_of_level(t, S)]
+        if not ps:
+            G[t] = 0.0
+            continue
+        abar = np.concatenate([DA[p] for p in ps], axis=1)  # m x (pairs k)
+        bbar = np.concatenate([DB[t - p] for p in ps], axis=0)  # (pairs k) x n
+        np.matmul(abar, bbar, out=G[t])
+    return G
+
+
 def reference_entries(A: np.ndarray, B: np.ndarray, S: int, T: int, entries, bits: int = 13):
     """For each (i, j): dict with exponents, level products, exact Z and the
     greedy L-limb rounding of Z (the product's expected limbs)."""

@@ -205,6 +205,20 @@ struct Resolved {
   Kind kind = Kind::kLevels;  // pair schedule, or Karatsuba (see kind_of)
 };
 
+// The default count of 13-bit digits for L limbs.  Up to quad doubles, four per
+// limb: section 2's quarters of each limb, 52 L bits, which cover the 53 L - 4
+// bits of the tolerance 4 k 2^-(53 L - 4) (|A||B|).  Beyond four limbs four
+// digits per limb fall short of those bits (by L - 4), so the count is the
+// 53 L - 4 bits in whole digits plus one guard digit for the levels dropped at
+// T = S - 1 (up to S - 1 products of the first dropped level): 34 for octo and
+// 66 for hexa doubles instead of 32 and 64.
+int default_digits(int limbs) {
+  return limbs <= 4 ? 4 * limbs : (53 * limbs - 4 + mdg::kSliceBits - 1) / mdg::kSliceBits + 1;
+}
+
+// The digit bits the other widths cover by default: those of the 13-bit default.
+int default_digit_bits(int limbs) { return mdg::kSliceBits * default_digits(limbs); }
+
 // Extra digits for elements down to range_bits below their line's exponent.
 inline int range_digits(int range_bits, int w) { return (range_bits + w - 1) / w; }
 
@@ -227,7 +241,7 @@ bool auto_width(int limbs, int64_t m, int64_t n, int64_t k, int range_bits, int 
   double best_cost = 0.0;
   bool found = false;
   for (int w = mdg::kSliceBits; w <= mdg::kMaxSliceBits; ++w) {
-    const int S0 = (4 * mdg::kSliceBits * limbs + w - 1) / w, D = range_digits(range_bits, w);
+    const int S0 = (default_digit_bits(limbs) + w - 1) / w, D = range_digits(range_bits, w);
     const int S = S0 + D, T = cutoff_for(cutoff, S0, D);
     if (!width_ok(S, w) || T < 0 || T > 2 * S - 2 || !levels_ok(T + 1, w) || !exact_ok(k, max_pairs(S, T), w))
       continue;
@@ -255,9 +269,9 @@ bool auto_width(int limbs, int64_t m, int64_t n, int64_t k, int range_bits, int 
 int int8_width(int limbs, int64_t k, int range_bits, int cutoff, int* w_out, int* S0_out) {
   bool sized = false;
   for (int w = kInt8MaxBits; w >= 1; --w) {
-    const int S0 = (4 * mdg::kSliceBits * limbs + w - 1) / w, D = range_digits(range_bits, w);
+    const int S0 = (default_digit_bits(limbs) + w - 1) / w, D = range_digits(range_bits, w);
     const int S = S0 + D, T = cutoff_for(cutoff, S0, D);
-    if (!width_ok(S, w) || T < 0 || T > 2 * S - 2 || !levels_ok(T + 1, w)) continue;
+    if (!width_ok(S, w) || S > mdg::kI8MaxSlices || T < 0 || T > 2 * S - 2 || !levels_ok(T + 1, w)) continue;
     sized = true;
     if (!exact_ok_i32(k, max_pairs(S, T), w)) continue;
     *w_out = w;
@@ -283,7 +297,7 @@ int resolve(int limbs, int64_t m, int64_t n, int64_t k, const mdgemm_opts* opts,
       MDG_TRY(int8_width(limbs, k, range_bits, opts->cutoff, &r->w, &r->S));
     } else if (bits >= 1 && bits <= kInt8MaxBits) {
       r->w = bits;
-      r->S = slices ? slices : (4 * mdg::kSliceBits * limbs + bits - 1) / bits;
+      r->S = slices ? slices : (default_digit_bits(limbs) + bits - 1) / bits;
     } else {
       return MDGEMM_EINVAL;
     }
@@ -292,13 +306,12 @@ int resolve(int limbs, int64_t m, int64_t n, int64_t k, const mdgemm_opts* opts,
     if (!auto_width(limbs, m, n, k, range_bits, opts->cutoff, r->kind, &r->w, &r->S)) return MDGEMM_EEXACT;
   } else if (bits == 0 || bits == mdg::kSliceBits) {
     r->w = mdg::kSliceBits;
-    int spl = opts ? opts->slices_per_limb : 0;
-    if (spl == 0) spl = 4;
+    const int spl = opts ? opts->slices_per_limb : 0;
     if (spl < 0) return MDGEMM_EINVAL;
-    r->S = slices ? slices : spl * limbs;
+    r->S = slices ? slices : (spl ? spl * limbs : default_digits(limbs));
   } else if (bits >= 1 && bits <= mdg::kMaxSliceBits) {
     r->w = bits;
-    r->S = slices ? slices : (4 * mdg::kSliceBits * limbs + bits - 1) / bits;
+    r->S = slices ? slices : (default_digit_bits(limbs) + bits - 1) / bits;
   } else {
     return MDGEMM_EINVAL;
   }
@@ -307,7 +320,7 @@ int resolve(int limbs, int64_t m, int64_t n, int64_t k, const mdgemm_opts* opts,
   // keeps its S0 leading levels
   const int S0 = r->S, D = range_digits(range_bits, r->w);
   r->S = S0 + D;
-  if (!width_ok(r->S, r->w)) return MDGEMM_EINVAL;
+  if (!width_ok(r->S, r->w) || (int8 && r->S > mdg::kI8MaxSlices)) return MDGEMM_EINVAL;
   const int cutoff = opts ? opts->cutoff : MDGEMM_CUTOFF_DEFAULT;
   if (cutoff < 0 && cutoff != MDGEMM_CUTOFF_DEFAULT && cutoff != MDGEMM_CUTOFF_ALL) return MDGEMM_EINVAL;
   r->T = cutoff_for(cutoff, S0, D);
@@ -408,6 +421,7 @@ bool layout_int8(int64_t m, int64_t n, int64_t k, int S, int T, LayoutI8* L) {
   L->kp = mdg::i8_kp(k);
   L->mp = mdg::i8_rows(m);
   L->np = mdg::i8_rows(n);
+  if (!mdg::level_gemm_i8_fits(L->kp, S)) return false;
   const double ld = mdg::kI8Pad + (double)S * (double)L->kp;
   const double approx = ld * ((double)L->mp + (double)L->np) + 4.0 * (T + 1) * (double)m * (double)n;
   if (approx > 4.0e18 || m > (int64_t{1} << 31) || n > (int64_t{1} << 31)) return false;
@@ -432,6 +446,17 @@ bool layout_int8(int64_t m, int64_t n, int64_t k, int S, int T, LayoutI8* L) {
 bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
   const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
   return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+// A caller workspace of `bytes` bytes that overlaps A [L][m][k], B [L][k][n] or
+// C [L][m][n] (the workspace is written while A and B are still read).
+bool workspace_overlaps(const void* ws, size_t bytes, int64_t m, int64_t n, int64_t k, int limbs, const double* A,
+                        const double* B, const double* C) {
+  const size_t L = static_cast<size_t>(limbs);
+  const size_t abytes = sizeof(double) * L * static_cast<size_t>(m) * static_cast<size_t>(k);
+  const size_t bbytes = sizeof(double) * L * static_cast<size_t>(k) * static_cast<size_t>(n);
+  const size_t cbytes = sizeof(double) * L * static_cast<size_t>(m) * static_cast<size_t>(n);
+  return overlaps(ws, bytes, A, abytes) || overlaps(ws, bytes, B, bbytes) || overlaps(ws, bytes, C, cbytes);
 }
 
 // ---- library-owned workspace (one per device) ---------------------------------
@@ -612,17 +637,12 @@ int run_int8(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const 
   LayoutI8 L;
   if (!layout_int8(m, n, k, r.S, r.T, &L)) return MDGEMM_EINVAL;
   hipStream_t s = r.stream;
-  // refused under graph capture: the first call on a shape times both routes of
-  // the level products and synchronizes, and what hipBLASLt records (memset nodes
-  // of split-k forms, for instance) is not under this library's control
-  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-  if (hipStreamIsCapturing(s, &cap) != hipSuccess) return MDGEMM_EHIP;
-  if (cap != hipStreamCaptureStatusNone) return MDGEMM_EINVAL;
   const bool timed = (r.flags & MDGEMM_TIME_STAGES) != 0;
   char* ws = nullptr;
   LibraryBuffer lib;
   if (opts && opts->workspace) {
     if (opts->workspace_bytes < L.total) return MDGEMM_EWORKSPACE;
+    if (workspace_overlaps(opts->workspace, L.total, m, n, k, limbs, A, B, C)) return MDGEMM_EINVAL;
     ws = static_cast<char*>(opts->workspace);
   } else {
     MDG_TRY(lib.acquire(L.total, s, &ws));
@@ -647,7 +667,7 @@ int run_int8(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const 
     MDG_TRY(hip_status(mdg::launch_split_int8(m, k, limbs, r.S, r.w, A, EA, DA, L.kp, s)));
     MDG_TRY(hip_status(mdg::launch_split_int8t(k, n, limbs, r.S, r.w, B, EB, DBt, L.kp, L.np, s)));
     if (timed) MDG_TRY(record(2, s));
-    MDG_TRY(hip_status(mdg::launch_levels_int8(m, n, L.kp, r.S, r.T, DA, DBt, G, s)));
+    MDG_TRY(hip_status(mdg::launch_level_gemm_i8(m, n, L.kp, r.S, r.T, DA, DBt, G, s)));
     if (timed) MDG_TRY(record(3, s));
     MDG_TRY(hip_status(mdg::launch_accum_renorm_i32(m, n, limbs, r.T + 1, r.w, G, EA, EB, C, s)));
     if (timed) {
@@ -669,7 +689,7 @@ extern "C" {
 void mdgemm_opts_init(mdgemm_opts* opts) {
   if (!opts) return;
   std::memset(opts, 0, sizeof *opts);
-  opts->slices_per_limb = 4;
+  opts->slices_per_limb = 0;
   opts->cutoff = MDGEMM_CUTOFF_DEFAULT;
   opts->slice_bits = 0;
   opts->slices = 0;
@@ -714,6 +734,33 @@ size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const 
   return L.total;
 }
 
+int mdgemm_workspace_layout(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts, int64_t* info,
+                            int count) {
+  Resolved r;
+  if (m < 0 || n < 0 || k < 0 || count < 0 || (count > 0 && !info)) return MDGEMM_EINVAL;
+  MDG_TRY(resolve(limbs, m, n, k, opts, &r));
+  if (m == 0 || n == 0 || k == 0 || (r.flags & MDGEMM_INT8)) return MDGEMM_EINVAL;
+  if (!resolved_exact(r, k)) return MDGEMM_EEXACT;
+  const auto pl = planned_for(r.S, r.T, m, n, k, r.w, r.kind);
+  Layout L;
+  if (!layout(m, n, k, *pl, r.w, &L)) return MDGEMM_EINVAL;
+  const int64_t v[MDGEMM_LAYOUT_INFO] = {static_cast<int64_t>(L.ea),
+                                         static_cast<int64_t>(L.eb),
+                                         static_cast<int64_t>(L.da),
+                                         static_cast<int64_t>(L.db),
+                                         static_cast<int64_t>(L.g),
+                                         L.f32 ? 4 : 8,
+                                         L.f32 ? mdg::panel_k32(k) : mdg::panel_k(k),
+                                         mdg::panel_mn(m),
+                                         mdg::panel_mn(n),
+                                         pl->s.planes,
+                                         pl->s.direct_levels ? 1 : 0,
+                                         static_cast<int64_t>(L.total)};
+  const int nw = std::min(count, MDGEMM_LAYOUT_INFO);
+  for (int i = 0; i < nw; ++i) info[i] = v[i];
+  return nw;
+}
+
 int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
               const mdgemm_opts* opts) {
   Resolved r;
@@ -744,6 +791,7 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   LibraryBuffer lib;
   if (opts && opts->workspace) {
     if (opts->workspace_bytes < L.total) return MDGEMM_EWORKSPACE;
+    if (workspace_overlaps(opts->workspace, L.total, m, n, k, limbs, A, B, C)) return MDGEMM_EINVAL;
     ws = static_cast<char*>(opts->workspace);
   } else {
     MDG_TRY(lib.acquire(L.total, s, &ws));

@@ -13,13 +13,13 @@ namespace mdg {
 
 constexpr int kSliceBits = 13;
 constexpr int kDigitMax = (1 << kSliceBits) - 1;  // 8191
-constexpr int kMaxSlices = 64;  // 4 digits per limb of a hexa double
+constexpr int kMaxSlices = 68;  // the 66 default digits of a hexa double, and a little room
 constexpr int kMaxLimbs = 16;   // hexa double
 constexpr int kMaxLevels = 2 * kMaxSlices - 1;
-constexpr int kZWords = 28;     // 64-bit words of an exact level sum (13 (kMaxLevels - 1) + 55 bits)
+constexpr int kZWords = 28;     // 64-bit words of an exact level sum (w (levels - 1) + 55 bits <= 1792)
 constexpr int kMaxJobs = 65535;  // jobs of one level-GEMM launch (grid.y)
 constexpr int kMaxSliceBits = 26;                  // widest digit: products of two stay below 2^52
-constexpr int kMaxDigitBits = 64 * 14 - 52;  // w S + 52 <= 896: the split's integer fits 14 words
+constexpr int kMaxDigitBits = 64 * 15 - 52;  // w S + 52 <= 960: the split's integer fits 15 words
 constexpr int kTileMN = 128;  // level-GEMM tile rows / columns
 constexpr int kTileK = 16;    // level-GEMM k step
 
@@ -67,6 +67,7 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
 // 256, B's (columns of B) n rounded up to 256 (those extra rows are never
 // stored and only feed outputs that are not kept).
 constexpr int kI8Pad = 128;
+constexpr int kI8MaxSlices = 64;  // int8 digits per element (w S + 52 <= 500 bits at w <= 7)
 inline int64_t i8_kp(int64_t k) { return (k + 127) / 128 * 128; }
 inline int64_t i8_rows(int64_t x) { return (x + 255) / 256 * 256; }
 
@@ -84,13 +85,9 @@ hipError_t launch_split_int8t(int64_t rows, int64_t cols, int L, int S, int w, c
 
 // a3 on the int8 matrix cores: levels t = 0..T into int32 planes G [T+1][m][n],
 // from A's digits (launch_split_int8, i8_rows(m) rows) and B's (launch_split_int8t,
-// i8_rows(n) rows); every level sum must stay below 2^31 (checked by the caller).
-// Either the hand-written kernel (all levels in one launch) or one hipBLASLt
-// GEMM per level, whichever ran faster on the first call of the shape.
-hipError_t launch_levels_int8(int64_t m, int64_t n, int64_t kp, int S, int T, const int8_t* DA, const int8_t* DBt,
-                              int32_t* G, hipStream_t stream);
-
-// The hand-written int8 level kernel (csrc/level_gemm_i8.hip) and whether a shape fits it.
+// i8_rows(n) rows), all levels in one launch of the hand-written kernel of
+// level_gemm_i8.hip; every level sum must stay below 2^31 (checked by the caller).
+// level_gemm_i8_fits tells whether a digit layout fits that kernel.
 bool level_gemm_i8_fits(int64_t kp, int S);
 hipError_t launch_level_gemm_i8(int64_t m, int64_t n, int64_t kp, int S, int T, const int8_t* DA, const int8_t* DBt,
                                 int32_t* G, hipStream_t stream);

@@ -25,6 +25,10 @@
 
 namespace mdg {
 
+// Digits a Karatsuba combination may draw on (digit sets are 64-bit masks);
+// products with more digits per element keep the pair schedule.
+constexpr int kMaxComboDigits = 64;
+
 struct Schedule {
   int S = 0, T = 0;
   bool direct_levels = true;  // plane j of the GEMM output is level job_out[j] (pair schedule)

@@ -235,8 +235,9 @@ Schedule pair_schedule(int S, int T) {
   s.T = T;
   s.direct_levels = true;
   for (int c = 0; c < S; ++c) {
-    s.mask_a.push_back(1ull << c);
-    s.mask_b.push_back(1ull << c);
+    // digit sets are read only for combinations, which take digits 0..63
+    s.mask_a.push_back(c < kMaxComboDigits ? 1ull << c : 0ull);
+    s.mask_b.push_back(c < kMaxComboDigits ? 1ull << c : 0ull);
     s.par1_a.push_back(-1);
     s.par2_a.push_back(-1);
     s.par1_b.push_back(-1);
@@ -308,6 +309,8 @@ double schedule_cost(const Schedule& s, const ScheduleCosts& costs) {
 }
 
 Schedule karatsuba_schedule(int S, int T, int64_t budget, const ScheduleCosts& costs, bool fallback) {
+  // combinations carry their digit sets in 64-bit masks: more digits keep the pair schedule
+  if (S > kMaxComboDigits) return pair_schedule(S, T);
   Planner planner(budget, costs);
   const Terms terms = planner.build(S, S, T);
   Schedule pairs = pair_schedule(S, T);

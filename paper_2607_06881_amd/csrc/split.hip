@@ -373,7 +373,7 @@ hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int w, int axis, 
   return hipGetLastError();
 }
 
-// Word counts instantiated for w S up to 844 digit bits (896 bits).
+// Word counts instantiated for w S up to 908 digit bits (960 bits).
 template <int ML>
 hipError_t split_words(int words, int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
                        const int32_t* E, void* D, bool panel, bool f32, const uint32_t* masks, int C,
@@ -386,6 +386,7 @@ hipError_t split_words(int words, int64_t rows, int64_t cols, int L, int S, int 
   if (words <= 8) return launch_nw<8, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
   if (words <= 10) return launch_nw<10, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
   if (words <= 14) return launch_nw<14, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+  if (words <= 15) return launch_nw<15, ML>(rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
   return hipErrorInvalidValue;
 }
 
@@ -440,7 +441,7 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
 
 hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,
                              int8_t* D, int64_t kp, hipStream_t stream) {
-  if (w < 1 || w > 7 || S < 1 || S > kMaxSlices || kp < cols || kp % kI8Pad != 0) return hipErrorInvalidValue;
+  if (w < 1 || w > 7 || S < 1 || S > kI8MaxSlices || kp < cols || kp % kI8Pad != 0) return hipErrorInvalidValue;
   if (rows == 0 || kp == 0) return hipSuccess;
   const int words = (w * S + 52 + 63) / 64;
   if (L <= 4) return split_int8_words<4>(words, rows, cols, kp, L, S, w, X, E, D, stream);
@@ -450,7 +451,7 @@ hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, co
 
 hipError_t launch_split_int8t(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,
                               int8_t* Dt, int64_t kp, int64_t np, hipStream_t stream) {
-  if (w < 1 || w > 7 || S < 1 || S > kMaxSlices || kp < rows || np < cols || kp % kI8Pad != 0)
+  if (w < 1 || w > 7 || S < 1 || S > kI8MaxSlices || kp < rows || np < cols || kp % kI8Pad != 0)
     return hipErrorInvalidValue;
   if (kp == 0 || np == 0) return hipSuccess;
   const int words = (w * S + 52 + 63) / 64;

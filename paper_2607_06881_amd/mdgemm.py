@@ -33,15 +33,16 @@ MDGEMM_KARATSUBA = 8
 MDGEMM_KARATSUBA_MIN_TERMS = 16
 MDGEMM_INT8 = 32
 MDGEMM_SCHEDULE_INFO = 12
+MDGEMM_LAYOUT_INFO = 12
 
 MDGEMM_CUTOFF_DEFAULT = -1
 MDGEMM_CUTOFF_ALL = -2
 MDGEMM_MAX_LIMBS = 16
-MDGEMM_MAX_SLICES = 64
-MDGEMM_MAX_LEVELS = 127
+MDGEMM_MAX_SLICES = 68
+MDGEMM_MAX_LEVELS = 135
 MDGEMM_SLICE_BITS = 13
 MDGEMM_MAX_SLICE_BITS = 26
-MDGEMM_MAX_DIGIT_BITS = 844
+MDGEMM_MAX_DIGIT_BITS = 908
 MDGEMM_SLICE_BITS_AUTO = -1
 MDGEMM_Z_WORDS = 28
 PANEL_K = 16  # level-GEMM panels: k rounded up to 16,
@@ -66,6 +67,7 @@ EXPORTED = (
     "mdgemm",
     "mdgemm_workspace_bytes",
     "mdgemm_ex",
+    "mdgemm_workspace_layout",
     "mdgemm_stage_times",
     "mdgemm_status_string",
     "mdgemm_release",
@@ -80,6 +82,8 @@ EXPORTED = (
     "mdgemm_schedule_export",
     "mdgemm_schedule_workspace_bytes",
     "mdgemm_schedule_levels",
+    "mdgemm_probe_mfma_f64",
+    "mdgemm_probe_copy",
 )
 
 
@@ -127,6 +131,9 @@ def lib() -> ctypes.CDLL:
         L.mdgemm_workspace_bytes.restype = ctypes.c_size_t
         L.mdgemm_ex.argtypes = [_i64, _i64, _i64, ctypes.c_int, _vp, _vp, _vp, ctypes.POINTER(mdgemm_opts)]
         L.mdgemm_ex.restype = ctypes.c_int
+        L.mdgemm_workspace_layout.argtypes = [_i64, _i64, _i64, ctypes.c_int, ctypes.POINTER(mdgemm_opts),
+                                              ctypes.POINTER(ctypes.c_int64), ctypes.c_int]
+        L.mdgemm_workspace_layout.restype = ctypes.c_int
         L.mdgemm_stage_times.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_int]
         L.mdgemm_stage_times.restype = ctypes.c_int
         L.mdgemm_status_string.argtypes = [ctypes.c_int]
@@ -158,6 +165,10 @@ def lib() -> ctypes.CDLL:
         L.mdgemm_schedule_levels.argtypes = [_i64, _i64, _i64, _c, _c, _c, _u, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                              _vp]
         L.mdgemm_schedule_levels.restype = ctypes.c_int
+        L.mdgemm_probe_mfma_f64.argtypes = [_i64, _i64, _vp, _vp]
+        L.mdgemm_probe_mfma_f64.restype = ctypes.c_int64
+        L.mdgemm_probe_copy.argtypes = [_vp, _vp, _i64, _vp]
+        L.mdgemm_probe_copy.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -192,7 +203,7 @@ def _stream(stream) -> int:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def make_opts(*, slices_per_limb: int = 4, cutoff: int = MDGEMM_CUTOFF_DEFAULT, flags: int = 0, stream=None,
+def make_opts(*, slices_per_limb: int = 0, cutoff: int = MDGEMM_CUTOFF_DEFAULT, flags: int = 0, stream=None,
               workspace: Optional[torch.Tensor] = None, slice_bits: int = 0, slices: int = 0,
               range_bits: int = 0) -> mdgemm_opts:
     o = mdgemm_opts()
@@ -210,7 +221,7 @@ def make_opts(*, slices_per_limb: int = 4, cutoff: int = MDGEMM_CUTOFF_DEFAULT, 
     return o
 
 
-def mdgemm_workspace_bytes(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
+def mdgemm_workspace_bytes(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 0,
                            cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0,
                            range_bits: int = 0, flags: int = 0) -> int:
     o = mdgemm_opts()
@@ -224,7 +235,7 @@ def mdgemm_workspace_bytes(m: int, n: int, k: int, limbs: int, *, slices_per_lim
     return int(lib().mdgemm_workspace_bytes(m, n, k, limbs, ctypes.byref(o)))
 
 
-def mdgemm_plan(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
+def mdgemm_plan(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 0,
                 cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0, range_bits: int = 0,
                 flags: int = 0):
     """(digit width w, digit count S, cutoff T) that mdgemm_ex uses for these options."""
@@ -242,7 +253,7 @@ def mdgemm_plan(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 4,
     return w.value, S.value, T.value
 
 
-def mdgemm_ex(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None, *, slices_per_limb: int = 4,
+def mdgemm_ex(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None, *, slices_per_limb: int = 0,
               cutoff: int = MDGEMM_CUTOFF_DEFAULT, flags: int = 0, workspace: Optional[torch.Tensor] = None,
               stream=None, slice_bits: int = 0, slices: int = 0, range_bits: int = 0) -> torch.Tensor:
     """C = A.B for limb-major float64 tensors A [L, m, k] and B [L, k, n] on the GPU.
@@ -271,6 +282,49 @@ def mdgemm_ex(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None
                   slice_bits=slice_bits, slices=slices, range_bits=range_bits)
     _check(lib().mdgemm_ex(m, n, k, L, _ptr(A), _ptr(B), _ptr(C), ctypes.byref(o)), "mdgemm_ex")
     return C
+
+
+LAYOUT_INFO_KEYS = ("ea", "eb", "da", "db", "planes_off", "panel_bytes", "kp", "mp", "np", "planes",
+                    "direct_levels", "total")
+
+
+def mdgemm_workspace_layout(m: int, n: int, k: int, limbs: int, *, slices_per_limb: int = 0,
+                            cutoff: int = MDGEMM_CUTOFF_DEFAULT, slice_bits: int = 0, slices: int = 0,
+                            range_bits: int = 0, flags: int = 0) -> dict:
+    """Byte offsets and sizes of the parts mdgemm_ex writes into a caller workspace (host only)."""
+    o = make_opts(slices_per_limb=slices_per_limb, cutoff=cutoff, flags=flags, slice_bits=slice_bits, slices=slices,
+                  range_bits=range_bits, stream=0)
+    buf = (ctypes.c_int64 * MDGEMM_LAYOUT_INFO)()
+    cnt = lib().mdgemm_workspace_layout(m, n, k, limbs, ctypes.byref(o), buf, MDGEMM_LAYOUT_INFO)
+    if cnt < 0:
+        _check(cnt, "mdgemm_workspace_layout")
+    return {key: int(buf[i]) for i, key in enumerate(LAYOUT_INFO_KEYS[:cnt])}
+
+
+def workspace_parts(ws: torch.Tensor, m: int, n: int, k: int, limbs: int, **opts) -> dict:
+    """Views of a caller workspace after mdgemm_ex: EA [m], EB [n] (int32), the digit
+    panels DA [CA, kp, mp], DB [CB, kp, np] (float32 or float64) and the output
+    planes G [P, m, n] (float64).  Argument marshalling only (offsets from the library)."""
+    lay = mdgemm_workspace_layout(m, n, k, limbs, **opts)
+    if ws.numel() < lay["total"]:
+        raise ValueError("workspace smaller than the layout")
+    pdt = torch.float32 if lay["panel_bytes"] == 4 else torch.float64
+    kp, mp, np_ = lay["kp"], lay["mp"], lay["np"]
+    ca = (lay["db"] - lay["da"]) // (lay["panel_bytes"] * kp * mp)
+    cb = (lay["planes_off"] - lay["db"]) // (lay["panel_bytes"] * kp * np_)
+
+    def view(off, count, dtype, shape):
+        size = torch.empty(0, dtype=dtype).element_size()
+        return ws[off:off + count * size].view(dtype).view(shape)
+
+    return {
+        "layout": lay,
+        "EA": view(lay["ea"], m, torch.int32, (m,)),
+        "EB": view(lay["eb"], n, torch.int32, (n,)),
+        "DA": view(lay["da"], ca * kp * mp, pdt, (ca, kp, mp)),
+        "DB": view(lay["db"], cb * kp * np_, pdt, (cb, kp, np_)),
+        "G": view(lay["planes_off"], lay["planes"] * m * n, torch.float64, (lay["planes"], m, n)),
+    }
 
 
 def mdgemm(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None) -> torch.Tensor:
@@ -462,3 +516,23 @@ def mdgemm_schedule_levels(DAt: torch.Tensor, DBp: torch.Tensor, m: int, n: int,
                                         _ptr(workspace), workspace.numel(), _stream(stream)),
            "mdgemm_schedule_levels")
     return out
+
+
+def mdgemm_probe_mfma_f64(sink: torch.Tensor, iters: int, stream=None) -> int:
+    """Launch the FP64 MFMA throughput probe with sink.numel() // 256 blocks;
+    returns the flops of the launch (time it with events on the same stream)."""
+    _dev_tensor(sink, torch.float64, "sink")
+    blocks = sink.numel() // 256
+    flops = lib().mdgemm_probe_mfma_f64(blocks, iters, _ptr(sink), _stream(stream))
+    if flops < 0:
+        _check(int(flops), "mdgemm_probe_mfma_f64")
+    return int(flops)
+
+
+def mdgemm_probe_copy(src: torch.Tensor, dst: torch.Tensor, stream=None) -> None:
+    """dst = src (float64, same size) through the library's copy probe."""
+    _dev_tensor(src, torch.float64, "src")
+    _dev_tensor(dst, torch.float64, "dst")
+    if src.numel() != dst.numel():
+        raise ValueError("src and dst differ in size")
+    _check(lib().mdgemm_probe_copy(_ptr(src), _ptr(dst), src.numel(), _stream(stream)), "mdgemm_probe_copy")

@@ -74,7 +74,7 @@ class Workload:
             return opts
         if self.range_bits:
             return {"range_bits": self.range_bits}
-        return {"slices_per_limb": self.slices // self.limbs, "cutoff": self.cutoff}
+        return {"slices": self.slices, "cutoff": self.cutoff}
 
     @property
     def pairs(self) -> int:
@@ -113,13 +113,14 @@ WORKLOADS = {
     # More limbs: the octo- and hexa-double shapes of the top-down method (section 4,
     # the table of dimensions adapted for dd, qd, od and hd), A 256 x 128 (od) and
     # 128 x 64 (hd), B with the 8192 columns of the rewritten second operand;
-    # the paper's four digits per limb.
+    # the default digit count for more than four limbs (the 53 L - 4 bits of the
+    # tolerance in whole 13-bit digits plus one guard digit: 34 and 66).
     "c5": Workload(
-        "c5", 8, 256, 8192, 128, 32, 31, 5, "normal",
-        description="octo-double 256x8192x128, limb 0 ~ N(0,1), pairs p+q <= 31"),
+        "c5", 8, 256, 8192, 128, 34, 33, 5, "normal",
+        description="octo-double 256x8192x128, limb 0 ~ N(0,1), 34 digits, pairs p+q <= 33"),
     "c6": Workload(
-        "c6", 16, 128, 8192, 64, 64, 63, 6, "normal",
-        description="hexa-double 128x8192x64, limb 0 ~ N(0,1), pairs p+q <= 63"),
+        "c6", 16, 128, 8192, 64, 66, 65, 6, "normal",
+        description="hexa-double 128x8192x64, limb 0 ~ N(0,1), 66 digits, pairs p+q <= 65"),
     # A wide range inside every line (section 3, balancing): the inner dimension is
     # scaled oppositely in A and B, so each row of A and column of B spans 60
     # bits while every term a_ik b_kj has the same size; one shared grid per line

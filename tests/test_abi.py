@@ -51,7 +51,7 @@ def test_opts_init_defaults(lib):
     o = md.mdgemm_opts()
     o.flags = 77
     lib.mdgemm_opts_init(ctypes.byref(o))
-    assert (o.stream, o.workspace, o.workspace_bytes, o.slices_per_limb, o.cutoff, o.flags) == (None, None, 0, 4, -1,
+    assert (o.stream, o.workspace, o.workspace_bytes, o.slices_per_limb, o.cutoff, o.flags) == (None, None, 0, 0, -1,
                                                                                               0)
 
 
@@ -69,8 +69,8 @@ def test_invalid_arguments(lib):
     assert _ex(lib, 4, 4, -3, 2) == E
     assert _ex(lib, 4, 4, 4, 0) == E
     assert _ex(lib, 4, 4, 4, md.MDGEMM_MAX_LIMBS + 1) == E
-    assert _ex(lib, 4, 4, 4, 2, slices_per_limb=33) == E  # S = 66 > 64
-    assert _ex(lib, 4, 4, 4, 16, slices_per_limb=5) == E  # S = 80 > 64
+    assert _ex(lib, 4, 4, 4, 2, slices_per_limb=35) == E  # S = 70 > 68
+    assert _ex(lib, 4, 4, 4, 16, slices_per_limb=5) == E  # S = 80 > 68
     assert _ex(lib, 4, 4, 4, 2, cutoff=15) == E  # > 2S - 2
     assert _ex(lib, 4, 4, 4, 2, cutoff=-3) == E
     assert _ex(lib, 4, 4, 4, 2, A=None) == E
@@ -82,7 +82,7 @@ def test_invalid_arguments(lib):
     assert lib.mdgemm_split(4, 4, 2, 8, 13, 2, FA, FB, FC, None) == E
     assert lib.mdgemm_split(4, 4, 2, 8, 27, 0, FA, FB, FC, None) == E  # digits wider than 26 bits
     assert lib.mdgemm_split(4, 4, 2, 8, 0, 0, FA, FB, FC, None) == E
-    assert lib.mdgemm_split(4, 4, 2, 33, 26, 0, FA, FB, FC, None) == E  # 33 x 26 > 844 digit bits
+    assert lib.mdgemm_split(4, 4, 2, 35, 26, 0, FA, FB, FC, None) == E  # 35 x 26 > 908 digit bits
     assert lib.mdgemm_split_panel(4, 4, 2, 0, 13, 0, FA, FB, FC, None) == E
     assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 13, 7, 0, FA + 8, FB, FC, None) == E  # panels must be 16-byte aligned
     assert lib.mdgemm_slice_gemm(4, 4, 4, 8, 13, 15, 0, FA, FB, FC, None) == E
@@ -96,7 +96,7 @@ def test_invalid_arguments(lib):
     assert _ex(lib, 4, 4, 4, 2, slice_bits=27) == E
     assert _ex(lib, 4, 4, 4, 2, slice_bits=-2) == E
     assert _ex(lib, 4, 4, 4, 2, slice_bits=md.MDGEMM_SLICE_BITS_AUTO, slices=6) == E
-    assert _ex(lib, 4, 4, 4, 16, slice_bits=23) == E  # S = ceil(832 / 23) = 37, 37 x 23 > 844
+    assert _ex(lib, 4, 4, 4, 16, slice_bits=23, slices=40) == E  # 40 x 23 > 908
     assert lib.mdgemm_exponents(4, 4, 3, FA, FB, None) == E
     # m, n at most 2^27 (the level GEMM's 32-bit panel row offsets)
     assert _ex(lib, 2**27 + 1, 4, 4, 2, C=FC + (1 << 44)) == E
@@ -118,14 +118,15 @@ def _max_k(pairs):
 
 
 @pytest.mark.parametrize("limbs,cutoff,pairs", [(2, -1, 8), (2, -2, 8), (4, -1, 16), (1, 0, 1), (3, 5, 6),
-                                                (8, -1, 32), (16, -1, 64), (16, -2, 64)])
+                                                (8, -1, 34), (16, -1, 66), (16, -2, 66)])
 def test_exactness_bound(lib, limbs, cutoff, pairs):
+    S = exact.default_slices(limbs)
     kmax = _max_k(pairs)
     assert _ex(lib, 4, 4, kmax + 1, limbs, cutoff=cutoff) == md.MDGEMM_EEXACT
     # at kmax the check passes and the call goes on to the workspace check
     assert _ex(lib, 4, 4, kmax, limbs, cutoff=cutoff, workspace=FC + (1 << 40),
                workspace_bytes=16) == md.MDGEMM_EWORKSPACE
-    assert lib.mdgemm_slice_gemm(4, 4, kmax + 1, 4 * limbs, 13, cutoff if cutoff >= 0 else 4 * limbs - 1, 0, FA, FB, FC,
+    assert lib.mdgemm_slice_gemm(4, 4, kmax + 1, S, 13, cutoff if cutoff >= 0 else S - 1, 0, FA, FB, FC,
                                  None) == md.MDGEMM_EEXACT
 
 
@@ -147,14 +148,36 @@ def test_workspace_bytes_layout(lib):
     assert md.mdgemm_workspace_bytes(100, 70, 33, 2, cutoff=-2) == expect(100, 70, 33, 2, 8, 14)
     assert md.mdgemm_workspace_bytes(64, 64, 64, 4, slices_per_limb=3, cutoff=5) == expect(64, 64, 64, 4, 12, 5)
     assert md.mdgemm_workspace_bytes(0, 64, 64, 2) == 0
-    assert md.mdgemm_workspace_bytes(256, 8192, 128, 8) == expect(256, 8192, 128, 8, 32, 31)
-    assert md.mdgemm_workspace_bytes(128, 8192, 64, 16) == expect(128, 8192, 64, 16, 64, 63)
+    assert md.mdgemm_workspace_bytes(256, 8192, 128, 8) == expect(256, 8192, 128, 8, 34, 33)
+    assert md.mdgemm_workspace_bytes(128, 8192, 64, 16) == expect(128, 8192, 64, 16, 66, 65)
     assert md.mdgemm_workspace_bytes(4, 4, 4, md.MDGEMM_MAX_LIMBS + 1) == 2**64 - 1
 
 
 def test_workspace_too_small_is_reported_before_any_launch(lib):
     need = md.mdgemm_workspace_bytes(40, 30, 20, 3)
     assert _ex(lib, 40, 30, 20, 3, workspace=FC + (1 << 40), workspace_bytes=need - 1) == md.MDGEMM_EWORKSPACE
+
+
+@pytest.mark.parametrize("flags", [0, md.MDGEMM_INT8])
+def test_workspace_overlapping_an_operand_is_refused_before_any_launch(lib, flags):
+    m, n, k, L = 40, 30, 20, 3
+    need = md.mdgemm_workspace_bytes(m, n, k, L, flags=flags)
+    abytes, bbytes, cbytes = 8 * L * m * k, 8 * L * k * n, 8 * L * m * n
+    far = FC + (1 << 40)
+    # each operand's first and last byte inside the workspace, and the workspace
+    # starting inside each operand
+    for ws in (FA - need + 1, FA + abytes - 1, FB - need + 8, FB + bbytes - 8, FC - need + 1, FC + cbytes - 1):
+        assert _ex(lib, m, n, k, L, workspace=ws, workspace_bytes=need, flags=flags) == md.MDGEMM_EINVAL, hex(ws)
+    # adjacent on both sides is fine: the call goes on to the HIP calls, which
+    # without a device return MDGEMM_EHIP (never run with a device: the fake
+    # addresses would then reach a kernel)
+    import torch
+
+    if torch.cuda.is_available():
+        return
+    for ws in (FA - need, FA + abytes):
+        assert _ex(lib, m, n, k, L, workspace=ws, workspace_bytes=need, flags=flags) != md.MDGEMM_EINVAL
+    assert _ex(lib, m, n, k, L, workspace=far, workspace_bytes=need, flags=flags) != md.MDGEMM_EINVAL
 
 
 def test_binding_refuses_cpu_tensors(lib):
@@ -169,11 +192,17 @@ def test_binding_refuses_cpu_tensors(lib):
 
 def test_plan_digit_width_and_count(lib):
     auto = md.MDGEMM_SLICE_BITS_AUTO
-    # 13-bit digits: four per limb, or slices_per_limb, or an explicit count
+    # 13-bit digits: four per limb up to four limbs, ceil((53 L - 4) / 13) + 1 beyond,
+    # or slices_per_limb, or an explicit count
     assert md.mdgemm_plan(64, 64, 64, 2) == (13, 8, 7)
+    assert md.mdgemm_plan(64, 64, 64, 4) == (13, 16, 15)
+    assert md.mdgemm_plan(64, 64, 64, 5) == (13, 22, 21)  # 261 bits: 21 digits + 1
+    assert md.mdgemm_plan(64, 64, 64, 8) == (13, 34, 33)  # 420 bits: 33 digits + 1
+    assert md.mdgemm_plan(64, 64, 64, 16) == (13, 66, 65)  # 844 bits: 65 digits + 1
+    assert md.mdgemm_plan(64, 64, 64, 8, slices_per_limb=4) == (13, 32, 31)
     assert md.mdgemm_plan(64, 64, 64, 3, slices_per_limb=3, cutoff=-2) == (13, 9, 16)
     assert md.mdgemm_plan(64, 64, 64, 2, slices=9, cutoff=4) == (13, 9, 4)
-    # explicit width: ceil(52 L / w) digits unless given
+    # explicit width: ceil(13 S13(L) / w) digits unless given
     assert md.mdgemm_plan(64, 64, 64, 2, slice_bits=19) == (19, 6, 5)
     assert md.mdgemm_plan(64, 64, 4, 4, slice_bits=21) == (21, 10, 9)
     assert md.mdgemm_plan(64, 64, 64, 2, slice_bits=17, slices=5, cutoff=-2) == (17, 5, 8)
@@ -181,7 +210,7 @@ def test_plan_digit_width_and_count(lib):
     assert md.mdgemm_plan(4096, 4096, 4096, 2, slice_bits=auto) == (19, 6, 5)  # 21 pairs instead of 36
     assert md.mdgemm_plan(2048, 2048, 1024, 4, slice_bits=auto) == (19, 11, 10)  # 66 instead of 136
     assert md.mdgemm_plan(8192, 8192, 512, 3, slice_bits=auto) == (20, 8, 7)  # 36 instead of 78
-    assert md.mdgemm_plan(128, 8192, 64, 16, slice_bits=auto) == (20, 42, 41)  # 903 instead of 2080
+    assert md.mdgemm_plan(128, 8192, 64, 16, slice_bits=auto) == (20, 43, 42)  # 946 instead of 2211
     for L in (1, 2, 3, 4, 8, 16):
         for k in (1, 7, 64, 512, 1000, 4096, 2**16, 2**20, 2**22):
             want = exact.adaptive_width(L, k)
@@ -238,7 +267,7 @@ def test_int8_plans(lib):
     assert md.mdgemm_plan(64, 64, 8876, 2, flags=I8) == (7, 15, 14)
     assert md.mdgemm_plan(64, 64, 8877, 2, flags=I8) == (6, 18, 17)
     assert md.mdgemm_plan(64, 64, 65536, 2, flags=I8) == (5, 21, 20)
-    assert md.mdgemm_plan(64, 64, 64, 8, flags=I8) == (7, 60, 59)
+    assert md.mdgemm_plan(64, 64, 64, 8, flags=I8) == (7, 64, 63)  # ceil(442 / 7)
     assert md.mdgemm_plan(64, 64, 64, 2, flags=I8, slice_bits=4) == (4, 26, 25)
     assert md.mdgemm_plan(64, 64, 2048, 2, flags=I8, range_bits=60) == (7, 24, 32)
     E = md.MDGEMM_EINVAL
@@ -248,7 +277,7 @@ def test_int8_plans(lib):
         with pytest.raises(md.MdgemmError) as ei:
             md.mdgemm_plan(64, 64, 64, 2, **kw)
         assert ei.value.status == E, kw
-    with pytest.raises(md.MdgemmError) as ei:  # hexa-double: ceil(832 / 7) = 119 digits > 64
+    with pytest.raises(md.MdgemmError) as ei:  # hexa-double: ceil(858 / 7) = 123 digits > 64
         md.mdgemm_plan(64, 64, 64, 16, flags=I8)
     assert ei.value.status == E
     with pytest.raises(md.MdgemmError) as ei:  # even 1-bit digits overflow int32 sums
@@ -297,7 +326,7 @@ def test_range_balancing_plans(lib):
     assert md.mdgemm_plan(64, 64, 2048, 2, range_bits=60, slice_bits=md.MDGEMM_SLICE_BITS_AUTO) == (19, 10, 13)
     assert md.mdgemm_plan(64, 64, 2048, 2, range_bits=60, cutoff=-2) == (13, 13, 24)
     assert _ex(lib, 4, 4, 4, 2, range_bits=-1) == md.MDGEMM_EINVAL
-    assert _ex(lib, 4, 4, 4, 16, range_bits=13) == md.MDGEMM_EINVAL  # 65 digits
+    assert _ex(lib, 4, 4, 4, 16, range_bits=40) == md.MDGEMM_EINVAL  # 66 + 4 = 70 digits
     E = md.MDGEMM_EINVAL
     assert lib.mdgemm_line_spread(4, 4, 2, FA, FB, FC, None) == E
     assert lib.mdgemm_line_spread(4, 4, 0, FA, FB, FB, None) == E  # E and spread overlap

@@ -103,7 +103,7 @@ def test_mdgemm_karatsuba_end_to_end(L, m, k, n, cutoff, seed):
     base = "normal" if seed % 2 else "uniform"
     A = workloads.make_operand(rng, L, m, k, base, row_exp=15)
     B = workloads.make_operand(rng, L, k, n, base, col_exp=15)
-    S = 4 * L
+    S = exact.default_slices(L)
     T = {-1: S - 1, -2: 2 * S - 2}.get(cutoff, cutoff)
     C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), cutoff=cutoff, flags=KMIN))
     ref = pipeline.full_reference(A, B, S, T)
@@ -141,7 +141,7 @@ def test_mdgemm_karatsuba_workspace_stream_and_graph():
     rng = np.random.default_rng(99)
     A_h = workloads.make_operand(rng, L, m, k, "normal", row_exp=10)
     B_h = workloads.make_operand(rng, L, k, n, "normal", col_exp=10)
-    want = pipeline.full_reference(A_h, B_h, 4 * L, 4 * L - 1)["C"]
+    want = pipeline.full_reference(A_h, B_h, exact.default_slices(L), exact.default_slices(L) - 1)["C"]
     A, B = _gpu(A_h), _gpu(B_h)
     need = md.mdgemm_workspace_bytes(m, n, k, L, flags=KMIN)
     assert need > md.mdgemm_workspace_bytes(m, n, k, L)
@@ -175,7 +175,7 @@ def test_mdgemm_karatsuba_cost_model_shapes(L, m, k, n, cutoff):
     # shapes where the cost model takes the Karatsuba schedule; sampled
     # entries against the oracle's chain (bit-exact) and every entry against
     # the pair schedule's product (bit-identical)
-    S = 4 * L
+    S = exact.default_slices(L)
     T = S - 1 if cutoff == -1 else 2 * S - 2
     info = md.mdgemm_schedule_info(m, n, k, S, T, flags=KARA)
     print(f"[case] mdgemm karatsuba (cost model) L={L} {m}x{k}x{n}: {info}", flush=True)

@@ -394,7 +394,7 @@ def test_accum_renorm_wide_digits(L, levels, bits):
 def test_mdgemm_end_to_end(L, m, k, n, cutoff, seed):
     print(f"[case] mdgemm L={L} {m}x{k}x{n} cutoff={cutoff}", flush=True)
     A, B = _operands(L, m, k, n, seed, base="normal" if seed % 2 else "uniform", row_exp=15, col_exp=15)
-    S = 4 * L
+    S = exact.default_slices(L)
     T = S - 1 if cutoff == -1 else 2 * S - 2
     C = _host(md.mdgemm_ex(_gpu(A), _gpu(B), cutoff=cutoff))
     ref = pipeline.full_reference(A, B, S, T)
@@ -583,9 +583,7 @@ def test_mdgemm_adaptive_width_end_to_end(L, m, k, n, seed):
         for j in range(0, n, max(1, n // 3)):
             want, mag = exact.exact_product(A, B, i, j)
             err = abs(exact.value(C[:, i, j]) - want)
-            bound = exact.tolerance(k, L, mag) if L <= 4 else \
-                exact.method_bound(A, B, i, j, S, T, int(ref["EA"][i]), int(ref["EB"][j]), w)
-            assert err <= bound, (i, j)
+            assert err <= exact.tolerance(k, L, mag), (i, j)
 
 
 @pytest.mark.parametrize("L,bits,slices,cutoff", [(2, 17, 0, -2), (3, 22, 8, -1), (2, 20, 6, 3), (4, 13, 12, -1)])
@@ -623,6 +621,5 @@ def test_mdgemm_range_balancing_end_to_end(L, m, k, n, range_bits, auto):
         for j in range(0, n, max(1, n // 3)):
             want, mag = exact.exact_product(A, B, i, j)
             err = abs(exact.value(C[:, i, j]) - want)
-            bound = exact.tolerance(k, L, mag) if L <= 4 else \
-                exact.method_bound(A, B, i, j, S, T, int(ref["EA"][i]), int(ref["EB"][j]), w)
+            bound = exact.tolerance(k, L, mag)
             assert err <= bound, (i, j, float(err / bound))

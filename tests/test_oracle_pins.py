@@ -15,6 +15,7 @@ from fractions import Fraction
 import numpy as np
 import pytest
 
+from checks import nonoverlap_all
 from oracle import coracle, exact, pipeline
 from paper_2607_06881_amd import workloads
 
@@ -289,6 +290,25 @@ def test_levels_against_float_matmul_and_per_pair():
         assert np.array_equal(G[t], acc.astype(np.int64))
 
 
+@pytest.mark.parametrize("S,T,m,k,n", [(8, 7, 37, 64, 29), (12, 11, 16, 32, 40), (5, 8, 3, 1, 2), (4, 0, 6, 9, 5)])
+def test_levels_rewritten_matches_int64_and_python_ints(S, T, m, k, n):
+    # The rewritten-product form of the levels (one float64 matrix product per
+    # level) against the int64 loops of the C oracle on maximal digits of both
+    # signs, and against Python ints on a small corner.
+    rng = np.random.default_rng(S * 100 + T)
+    DA = rng.choice([-8191.0, 8191.0, -1.0, 0.0, 4096.0], size=(S, m, k))
+    DB = rng.choice([-8191.0, 8191.0, 7.0, 0.0, -4095.0], size=(S, k, n))
+    G = pipeline.levels_rewritten(DA, DB, T)
+    assert G.shape == (T + 1, m, n)
+    assert np.array_equal(G.astype(np.int64), coracle.levels(DA, DB, T))
+    small = exact.level_products(DA[:, :3, :], DB[:, :, :2], T)
+    for t in range(T + 1):
+        assert G[t, :3, :2].astype(np.int64).tolist() == small[t]
+    # dropping one pair of the last level changes it (the check is not vacuous)
+    if T < S:
+        assert not np.array_equal(G[T] - DA[0] @ DB[T], G[T])
+
+
 @pytest.mark.parametrize("bits", [13, 19, 24])
 def test_all_pairs_identity_with_truncated_operands(bits):
     # With every pair kept (T = 2S - 2), the weighted levels are exactly the
@@ -344,6 +364,65 @@ def test_round_to_limbs_properties():
             assert err <= Fraction(math.ulp(c[-1])) / 2
         else:
             assert err == 0
+
+
+def test_default_digit_count_closed_forms():
+    # four 13-bit quarters per limb up to quad doubles (52 L >= 53 L - 4 bits);
+    # beyond, the 53 L - 4 bits of the tolerance in whole digits plus one
+    assert [exact.default_slices(L) for L in (1, 2, 3, 4)] == [4, 8, 12, 16]
+    assert [52 * L >= 53 * L - 4 for L in (1, 2, 3, 4, 5)] == [True, True, True, True, False]
+    assert exact.default_slices(5) == 22 and exact.default_slices(8) == 34 and exact.default_slices(16) == 66
+    for L in range(5, 17):
+        S = exact.default_slices(L)
+        assert 13 * (S - 2) < 53 * L - 4 <= 13 * (S - 1)
+
+
+@pytest.mark.parametrize("L,k", [(5, 128), (8, 128), (16, 64)])
+def test_default_digit_count_meets_the_tolerance_beyond_four_limbs(L, k):
+    # The sliced chain with the default digit count meets 4 k 2^-(53L-4) (|A||B|)
+    # on N(0,1) octo/hexa-double data (the shapes' k of the od/hd workloads),
+    # while four digits per limb miss it for octo and hexa doubles.
+    rng = np.random.default_rng(L)
+    A = workloads.make_operand(rng, L, 6, k, "normal")
+    B = workloads.make_operand(rng, L, k, 5, "normal")
+    worst = {}
+    for S in (4 * L, exact.default_slices(L)):
+        C = pipeline.full_reference(A, B, S, S - 1)["C"]
+        r = 0.0
+        for i in range(6):
+            for j in range(5):
+                want, mag = exact.exact_product(A, B, i, j)
+                r = max(r, float(abs(exact.value(C[:, i, j]) - want) / exact.tolerance(k, L, mag)))
+        worst[S] = r
+    assert worst[exact.default_slices(L)] < 1e-3
+    if L >= 8:
+        assert worst[4 * L] > 1.0
+
+
+@pytest.mark.parametrize("x0", [1.0, 1.5, -0.75, 3.0 * 2.0**-600, -(2.0**900) * 1.125, 2.0**-1000 * 1.25])
+def test_nonoverlap_checkers_accept_the_boundary_and_reject_overlap(x0):
+    """Both nonoverlap checkers (the oracle's per element and the tests' whole-array
+    one) take section 1's nonoverlapping in the half-ulp sense.  The boundary
+    |x1| = ulp(x0)/2 is accepted; one ulp of x1 beyond it, |x1| = ulp(x0)/2 +
+    ulp(x1), is rejected, which a checker loosened to a whole ulp would accept;
+    a nonzero limb after a zero limb is rejected, which a checker without the
+    zero rule would accept."""
+    h = 0.5 * math.ulp(x0)
+    over = h + math.ulp(h)
+    assert Fraction(over) - Fraction(h) == Fraction(math.ulp(h)) and over < math.ulp(x0)
+    accepted = [[x0, h], [x0, -h], [x0, h, 0.5 * math.ulp(h)], [x0, 0.0, 0.0], [0.0, 0.0, 0.0]]
+    rejected = [[x0, over], [x0, -over], [x0, h, 0.5 * math.ulp(h) + math.ulp(0.5 * math.ulp(h))],
+                [0.0, h], [x0, 0.0, 2.0**-1074], [0.0, 0.0, -x0]]
+    for limbs in accepted:
+        assert exact.is_nonoverlapping(limbs), limbs
+        assert nonoverlap_all(np.array(limbs)[:, None]), limbs
+    for limbs in rejected:
+        assert not exact.is_nonoverlapping(limbs), limbs
+        assert not nonoverlap_all(np.array(limbs)[:, None]), limbs
+    # the array checker rejects a whole array when one element overlaps
+    many = np.array([[x0, h]] * 5 + [[x0, over]] + [[x0, -h]] * 3).T.reshape(2, 3, 3)
+    assert not nonoverlap_all(many)
+    assert nonoverlap_all(np.array([[x0, h]] * 9).T.reshape(2, 3, 3))
 
 
 # --------------------------------------------------------------------------
