@@ -202,6 +202,26 @@ int mdgemm_workspace_layout(int64_t m, int64_t n, int64_t k, int limbs, const md
 int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
               const mdgemm_opts* opts);
 
+/* ---- allocation-free entry point ---------------------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): mdgemm_ex on a fixed
+ * device scratch array of MDGEMM_NOALLOC_MAX_BYTES bytes that the library holds,
+ * one per device it runs on, from when the library is loaded on that device
+ * until the process ends.  The caller passes A, B and C as for mdgemm_ex and
+ * opts with no workspace (workspace NULL, workspace_bytes 0); MDGEMM_TIME_STAGES
+ * and MDGEMM_CHECK_FINITE are refused (MDGEMM_EINVAL).  A product whose
+ * mdgemm_workspace_bytes() exceeds MDGEMM_NOALLOC_MAX_BYTES returns
+ * MDGEMM_EWORKSPACE and launches nothing.  The call allocates no device memory
+ * (no hipMalloc, hipFree or allocating library routine).  Every call on one
+ * device shares that device's scratch array, which keeps the last call's
+ * contents: calls that may overlap in time on one device (other streams, other
+ * host threads) race and must be ordered by the caller.  Results equal
+ * mdgemm_ex's bit for bit. */
+#define MDGEMM_NOALLOC_MAX_BYTES 67108864 /* 64 MiB of scratch per device */
+
+int mdgemm_ex_noalloc(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
+                      const mdgemm_opts* opts);
+
 /* Milliseconds spent in each stage of the last mdgemm_ex call that set
  * MDGEMM_TIME_STAGES on this process: ms[0] exponents, ms[1] splits,
  * ms[2] level GEMMs, ms[3] accumulation and rounding.  Waits for that call's

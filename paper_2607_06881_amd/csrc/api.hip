@@ -24,6 +24,13 @@
 #include "internal.h"
 #include "mdgemm.h"
 
+// Device scratch of mdgemm_ex_noalloc: one fixed array per device, allocated
+// with the code object when the library is loaded on that device and held until
+// the process ends.  On the host, `scratch` is only a stand-in for the symbol,
+// not a device address: host code resolves the address of each device's copy
+// with hipGetSymbolAddress (noalloc_scratch below) and passes that to kernels.
+static __device__ __align__(256) unsigned char scratch[MDGEMM_NOALLOC_MAX_BYTES];
+
 static_assert(MDGEMM_MAX_LIMBS == mdg::kMaxLimbs && MDGEMM_MAX_SLICES == mdg::kMaxSlices &&
                   MDGEMM_Z_WORDS == mdg::kZWords && MDGEMM_SLICE_BITS == mdg::kSliceBits &&
                   MDGEMM_MAX_LEVELS == mdg::kMaxLevels && MDGEMM_MAX_SLICE_BITS == mdg::kMaxSliceBits &&
@@ -847,6 +854,69 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
 
 int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C) {
   return mdgemm_ex(m, n, k, limbs, A, B, C, nullptr);
+}
+
+}  // extern "C"
+
+namespace {
+
+// The device address of `scratch` on the current device, resolved once per
+// device (with that device current) and kept.
+struct NoallocScratch {
+  std::mutex mu;
+  std::vector<void*> ptr;
+};
+NoallocScratch& noalloc_state() {
+  static NoallocScratch s;
+  return s;
+}
+
+int noalloc_scratch(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MDGEMM_EHIP;
+  NoallocScratch& s = noalloc_state();
+  std::lock_guard<std::mutex> lock(s.mu);
+  if (static_cast<size_t>(dev) >= s.ptr.size()) s.ptr.resize(dev + 1, nullptr);
+  if (!s.ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return MDGEMM_EHIP;
+    }
+    s.ptr[dev] = p;
+  }
+  *out = s.ptr[dev];
+  return MDGEMM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mdgemm_ex_noalloc(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
+                      const mdgemm_opts* opts) {
+  mdgemm_opts o;
+  if (opts) {
+    o = *opts;
+  } else {
+    mdgemm_opts_init(&o);
+  }
+  // the scratch array is the workspace; timing events and the finiteness
+  // check's host copy are left out so that nothing is allocated on the way
+  if (o.workspace || o.workspace_bytes || (o.flags & (MDGEMM_TIME_STAGES | MDGEMM_CHECK_FINITE)))
+    return MDGEMM_EINVAL;
+  Resolved r;
+  if (m < 0 || n < 0 || k < 0) return MDGEMM_EINVAL;
+  MDG_TRY(resolve(limbs, m, n, k, &o, &r));
+  if (m == 0 || n == 0) return MDGEMM_OK;
+  const size_t need = mdgemm_workspace_bytes(m, n, k, limbs, &o);
+  if (need == SIZE_MAX) return MDGEMM_EINVAL;
+  if (need > MDGEMM_NOALLOC_MAX_BYTES) return MDGEMM_EWORKSPACE;
+  void* p = nullptr;
+  MDG_TRY(noalloc_scratch(&p));
+  o.workspace = p;
+  o.workspace_bytes = MDGEMM_NOALLOC_MAX_BYTES;
+  return mdgemm_ex(m, n, k, limbs, A, B, C, &o);
 }
 
 int mdgemm_stage_times(float* ms, int count) {

@@ -34,6 +34,7 @@ MDGEMM_KARATSUBA_MIN_TERMS = 16
 MDGEMM_INT8 = 32
 MDGEMM_SCHEDULE_INFO = 12
 MDGEMM_LAYOUT_INFO = 12
+MDGEMM_NOALLOC_MAX_BYTES = 64 << 20
 
 MDGEMM_CUTOFF_DEFAULT = -1
 MDGEMM_CUTOFF_ALL = -2
@@ -67,6 +68,7 @@ EXPORTED = (
     "mdgemm",
     "mdgemm_workspace_bytes",
     "mdgemm_ex",
+    "mdgemm_ex_noalloc",
     "mdgemm_workspace_layout",
     "mdgemm_stage_times",
     "mdgemm_status_string",
@@ -131,6 +133,8 @@ def lib() -> ctypes.CDLL:
         L.mdgemm_workspace_bytes.restype = ctypes.c_size_t
         L.mdgemm_ex.argtypes = [_i64, _i64, _i64, ctypes.c_int, _vp, _vp, _vp, ctypes.POINTER(mdgemm_opts)]
         L.mdgemm_ex.restype = ctypes.c_int
+        L.mdgemm_ex_noalloc.argtypes = [_i64, _i64, _i64, ctypes.c_int, _vp, _vp, _vp, ctypes.POINTER(mdgemm_opts)]
+        L.mdgemm_ex_noalloc.restype = ctypes.c_int
         L.mdgemm_workspace_layout.argtypes = [_i64, _i64, _i64, ctypes.c_int, ctypes.POINTER(mdgemm_opts),
                                               ctypes.POINTER(ctypes.c_int64), ctypes.c_int]
         L.mdgemm_workspace_layout.restype = ctypes.c_int
@@ -325,6 +329,24 @@ def workspace_parts(ws: torch.Tensor, m: int, n: int, k: int, limbs: int, **opts
         "DB": view(lay["db"], cb * kp * np_, pdt, (cb, kp, np_)),
         "G": view(lay["planes_off"], lay["planes"] * m * n, torch.float64, (lay["planes"], m, n)),
     }
+
+
+def mdgemm_ex_noalloc(A: torch.Tensor, B: torch.Tensor, C: torch.Tensor, *, slices_per_limb: int = 0,
+                      cutoff: int = MDGEMM_CUTOFF_DEFAULT, flags: int = 0, stream=None, slice_bits: int = 0,
+                      slices: int = 0, range_bits: int = 0) -> torch.Tensor:
+    """C = A.B through the allocation-free entry point (the library's fixed device
+    scratch instead of a workspace); C must be given."""
+    _dev_tensor(A, torch.float64, "A")
+    _dev_tensor(B, torch.float64, "B")
+    _dev_tensor(C, torch.float64, "C")
+    L, m, k = A.shape
+    n = B.shape[2]
+    if tuple(B.shape) != (L, k, n) or tuple(C.shape) != (L, m, n):
+        raise ValueError("shapes do not form a product [L,m,k].[L,k,n] -> [L,m,n]")
+    o = make_opts(slices_per_limb=slices_per_limb, cutoff=cutoff, flags=flags, stream=stream, slice_bits=slice_bits,
+                  slices=slices, range_bits=range_bits)
+    _check(lib().mdgemm_ex_noalloc(m, n, k, L, _ptr(A), _ptr(B), _ptr(C), ctypes.byref(o)), "mdgemm_ex_noalloc")
+    return C
 
 
 def mdgemm(A: torch.Tensor, B: torch.Tensor, C: Optional[torch.Tensor] = None) -> torch.Tensor:
