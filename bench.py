@@ -37,6 +37,7 @@ Prints one JSON line:
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -268,26 +269,43 @@ def main(argv=None) -> int:
         return opts
 
     def measure(opts, steps, warmup, base_flags=0):
-        """ms per step and per-stage ms of mdgemm_ex with these options."""
-        ws = torch.empty(md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, flags=base_flags, **opts),
+        """ms per step and per-stage ms of mdgemm_ex with these options: K steps
+        back to back (torch events around them; the options are marshalled once
+        and the C entry point called directly, so that a small product is not
+        bound by the host), then K steps with the library's stage events
+        (MDGEMM_TIME_STAGES, each step read back before the next)."""
+        ws = torch.empty(max(1, md.mdgemm_workspace_bytes(w.m, w.n, w.k, w.limbs, flags=base_flags, **opts)),
                          dtype=torch.uint8, device=dev)
+        o_plain = md.make_opts(flags=base_flags, stream=stream, workspace=ws, **opts)
+        o_timed = md.make_opts(flags=base_flags | md.MDGEMM_TIME_STAGES, stream=stream, workspace=ws, **opts)
+        lib = md.lib()
+        L_, m_, k_ = A.shape
+        n_ = B.shape[2]
+        pa, pb, pc = A.data_ptr(), B.data_ptr(), C.data_ptr()
+        ref_plain, ref_timed = ctypes.byref(o_plain), ctypes.byref(o_timed)
 
-        def step(flags=0):
-            md.mdgemm_ex(A, B, C, workspace=ws, flags=flags | base_flags, stream=stream, **opts)
+        def step(o):
+            st = lib.mdgemm_ex(m_, n_, k_, L_, pa, pb, pc, o)
+            if st != md.MDGEMM_OK:
+                raise md.MdgemmError(st, "mdgemm_ex")
 
         for _ in range(warmup):
-            step()
+            step(ref_plain)
         torch.cuda.synchronize()
-        stage_sum = np.zeros(4)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for _ in range(steps):
-            step(md.MDGEMM_TIME_STAGES)
-            stage_sum += np.array(md.mdgemm_stage_times())  # waits for this step's last event
+            step(ref_plain)
         e1.record(stream)
         torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        stage_sum = np.zeros(4)
+        for _ in range(steps):
+            step(ref_timed)
+            stage_sum += np.array(md.mdgemm_stage_times())  # waits for this step's last event
+        torch.cuda.synchronize()
         del ws
-        return e0.elapsed_time(e1) / steps, stage_sum / steps
+        return ms, stage_sum / steps
 
     bits_arg = md.MDGEMM_SLICE_BITS_AUTO if args.slice_bits == "auto" else int(args.slice_bits)
     sched_flags = md.MDGEMM_KARATSUBA if args.schedule == "karatsuba" else 0
@@ -311,6 +329,15 @@ def main(argv=None) -> int:
     pairs = workloads.pair_count(S, T)
     info = md.mdgemm_schedule_info(m, n, k, S, T, bits=bits, flags=0 if int8 else sched_flags)
     panels_f32 = bool(info["panels_f32"])  # digit panels kept in FP32 (every digit sum below 2^24)
+    # small outputs run the fused small-product kernel (all five steps in one
+    # launch), whose stages leave nothing in the workspace: the library refuses
+    # to describe a workspace layout for them
+    fused = False
+    if not int8 and not sched_flags:
+        try:
+            md.mdgemm_workspace_layout(w.m, w.n, w.k, w.limbs, **opts)
+        except md.MdgemmError:
+            fused = True
     md_flops = w.md_flops()
     # the GEMMs actually run: one per digit pair, or the Karatsuba schedule's products
     slice_flops = 2.0 * m * n * k * info["terms"]
@@ -348,6 +375,9 @@ def main(argv=None) -> int:
                                    "in one launch",
                          "ops_per_step": roofline.pop("flops_per_launch"),
                          "avg_step_ms": roofline.pop("avg_launch_ms")})
+    if fused:
+        roofline.update({"kernel": "small_product_kernel (the five steps fused per 16 x 16 tile of C, "
+                                   "v_mfma_f64_16x16x4f64)", "traffic": None})
     stages = {
         "exponents": {"ms": round(stage_ms[0], 4), "GB/s": round(bytes_exp / (stage_ms[0] * 1e-3) / 1e9, 1),
                       "bytes": bytes_exp},
@@ -358,6 +388,9 @@ def main(argv=None) -> int:
                          "bytes": bytes_acc},
         "hbm_peak_GB/s": HBM_PEAK_GBS,
     }
+    if fused:  # one kernel: its time is the level-product stage's, the others are event gaps
+        stages = {"fused_small_product": {"ms": round(stage_ms[2], 4), "TFLOP/s": round(achieved, 3)},
+                  "event_gaps_ms": [round(float(x), 4) for x in (stage_ms[0], stage_ms[1], stage_ms[3])]}
     config = {"workload": f"{w.name}: {w.description}", "m": m, "n": n, "k": k, "limbs": L, "slices": S,
               "cutoff": T, "pairs": pairs, "seed": w.seed, "panels": "f32" if panels_f32 else "f64"}
     if sched_flags and not int8:
@@ -434,7 +467,8 @@ def main(argv=None) -> int:
         roofline["peak_measured"] = cal["mfma_f64_TFLOP/s"]
         roofline["frac_of_measured"] = round(achieved / cal["mfma_f64_TFLOP/s"], 4)
         for key in ("exponents", "split", "accum_renorm"):
-            stages[key]["frac_of_copy"] = round(stages[key]["GB/s"] / cal["copy_GB/s"], 4)
+            if key in stages:
+                stages[key]["frac_of_copy"] = round(stages[key]["GB/s"] / cal["copy_GB/s"], 4)
     if bits_arg == 13 and not sched_flags and args.adaptive_steps > 0:
         # the same workload with the adaptive width reported beside the paper's
         # 13-bit digit pairs (and, on request, the Karatsuba schedule and the

@@ -73,6 +73,7 @@ extern "C" {
 #define MDGEMM_KARATSUBA 8u    /* level products by the Karatsuba schedule where it pays (see below) */
 #define MDGEMM_KARATSUBA_MIN_TERMS 16u /* the Karatsuba schedule with the fewest GEMMs, always */
 #define MDGEMM_INT8 32u        /* level products on the int8 matrix cores, digits of at most 7 bits (see below) */
+#define MDGEMM_STAGED 64u      /* always the staged kernels, never the fused small-product kernel (see below) */
 
 /* cutoff selectors for mdgemm_opts.cutoff (else an explicit T in 0 .. 2S-2) */
 #define MDGEMM_CUTOFF_DEFAULT -1  /* T = S - 1: the pair set of the rewritten product */
@@ -84,7 +85,8 @@ typedef struct mdgemm_opts {
   size_t workspace_bytes; /* size of `workspace` in bytes */
   int slices_per_limb;    /* 13-bit digits per limb, S = limbs * slices_per_limb; 0 = the default count (below) */
   int cutoff;             /* largest kept p + q; MDGEMM_CUTOFF_DEFAULT or _ALL or 0..2S-2 */
-  unsigned flags;         /* MDGEMM_CHECK_FINITE, _SYNC, _TIME_STAGES, _KARATSUBA, _KARATSUBA_MIN_TERMS, _INT8 */
+  unsigned flags;         /* MDGEMM_CHECK_FINITE, _SYNC, _TIME_STAGES, _KARATSUBA, _KARATSUBA_MIN_TERMS, _INT8,
+                             _STAGED */
   int slice_bits;         /* digit width w: 0 = 13 (section 2), 1..26, or MDGEMM_SLICE_BITS_AUTO */
   int slices;             /* digits per element S; 0 = derived (see below) */
   int range_bits;         /* range balancing: full precision down to 2^-range_bits of the line; 0 = off */
@@ -139,6 +141,20 @@ typedef struct mdgemm_opts {
  * w = 7, S = 15, T = 14 (120 pairs).  The level products run on the library's
  * own int8 kernel, all levels in one launch. */
 
+/* Small products.  For an output of at most 256 tiles of 16 x 16 (up to 4
+ * limbs, digits of at most 24 bits, at most 32 levels, the level sum of an
+ * element within 448 bits and the split's integer within 320 bits), whose level
+ * products are short enough (the
+ * levels dealt to four waves, the most loaded one at most 2048 MFMA
+ * instructions of 16 x 16 x 4), mdgemm_ex runs all five steps in one launch of a
+ * fused kernel per 16 x 16 tile of C instead of the staged kernels: the same
+ * digits, levels and limbs bit for bit, without launches in between and
+ * without the workspace (a caller workspace is still checked but not written;
+ * the library buffer is not used, so such calls can be captured in a HIP graph
+ * without a workspace).  Not with MDGEMM_INT8, the Karatsuba flags or
+ * MDGEMM_CHECK_FINITE; MDGEMM_STAGED turns it off.  With MDGEMM_TIME_STAGES the
+ * whole kernel counts as the level-product stage. */
+
 /* Fill `opts` with the defaults: default stream, library workspace, the default
  * count S13(L) of 13-bit digits (slices_per_limb 0), cutoff T = S - 1, no range
  * balancing, no flags. */
@@ -189,7 +205,9 @@ size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const 
  *   info[8] np, info[9] P, info[10] 1 for the pair schedule (planes = levels),
  *   info[11] mdgemm_workspace_bytes().
  * Returns the count written, MDGEMM_EEXACT, or MDGEMM_EINVAL (also for an empty
- * product and with MDGEMM_INT8, whose layout is not described here). */
+ * product, with MDGEMM_INT8, whose layout is not described here, and for a
+ * product that runs the fused small-product kernel, which leaves nothing in the
+ * workspace; MDGEMM_STAGED selects the staged kernels). */
 int mdgemm_workspace_layout(int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts, int64_t* info,
                             int count);
 

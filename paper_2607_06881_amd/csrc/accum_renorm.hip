@@ -22,65 +22,11 @@
 // so the T + 1 level loads and the L limb stores are contiguous 512-byte rows.
 #include <type_traits>
 
+#include "digits.h"
 #include "internal.h"
 
 namespace mdg {
 namespace {
-
-// N += g 2^sh (g sign-extended), modulo 2^(64 NW).
-template <int NW>
-__device__ inline void add_shifted_signed(uint64_t (&N)[NW], int64_t g, int sh) {
-  const int w = sh >> 6, b = sh & 63;
-  const uint64_t lo = static_cast<uint64_t>(g) << b;
-  const uint64_t hi = b ? static_cast<uint64_t>(g >> (64 - b)) : static_cast<uint64_t>(g >> 63);
-  const uint64_t ext = static_cast<uint64_t>(g >> 63);  // 0 or all ones
-  uint64_t carry = 0;
-#pragma unroll
-  for (int i = 0; i < NW; ++i) {
-    const uint64_t t = (i < w) ? 0ull : ((i == w) ? lo : ((i == w + 1) ? hi : ext));
-    const uint64_t s = N[i] + t;
-    const uint64_t c1 = s < t;
-    const uint64_t s2 = s + carry;
-    const uint64_t c2 = s2 < s;
-    N[i] = s2;
-    carry = c1 | c2;
-  }
-}
-
-// N = sum_t G_t 2^(w (T - t)) exactly.  Level t is column j = T - t of weight
-// 2^(w j); the columns are visited in increasing significance (t = T down to
-// 0) with a running carry in base 2^w: v = G_t + carry, the low w bits of v
-// are the digit of column j (placed into N, whose bits there are still zero)
-// and carry = floor(v / 2^w).  |G_t| < 2^53 keeps |v| < 2^54, so int64 never
-// overflows; the last carry, signed, is added above column T.
-// The digits fill N from bit 0 upward: `word` collects the bits of word wi of
-// N, `fill` of them so far; a full word is placed with one select over the words.
-template <int NW>
-struct CarryChain {
-  uint64_t word = 0;
-  int fill = 0, wi = 0;
-  int64_t carry = 0;
-
-  __device__ inline void step(uint64_t (&N)[NW], int64_t g, int w, uint64_t mask) {
-    const int64_t v = g + carry;
-    const uint64_t d = static_cast<uint64_t>(v) & mask;
-    carry = v >> w;  // arithmetic shift: floor division
-    word |= d << fill;
-    fill += w;
-    if (fill >= 64) {
-#pragma unroll
-      for (int i = 0; i < NW; ++i) N[i] = (i == wi) ? word : N[i];
-      ++wi;
-      fill -= 64;
-      word = fill ? d >> (w - fill) : 0ull;  // the bits of d beyond the full word
-    }
-  }
-  __device__ inline void finish(uint64_t (&N)[NW], int w, int T) {
-#pragma unroll
-    for (int i = 0; i < NW; ++i) N[i] = (i == wi) ? word : N[i];
-    if (carry != 0) add_shifted_signed<NW>(N, carry, w * (T + 1));
-  }
-};
 
 // The chain over levels read from G [levels][m][n] (integer-valued doubles, or
 // int32 planes of the int8 level products).  Loads are issued eight levels at a
@@ -110,90 +56,6 @@ __device__ inline void accumulate_levels(uint64_t (&N)[NW], const PT* __restrict
     }
   }
   chain.finish(N, w, T);
-}
-
-// Bit `pos` (0 <= pos < 64 NW) of v.
-template <int NW>
-__device__ inline uint64_t word_at(const uint64_t (&v)[NW], int w) {
-  uint64_t r = 0;
-#pragma unroll
-  for (int i = 0; i < NW; ++i) r = (i == w) ? v[i] : r;
-  return r;
-}
-
-template <int NW>
-__device__ inline void round_limbs(uint64_t (&N)[NW], int L, int scale, double* __restrict__ C, int64_t plane,
-                                   int64_t idx) {
-  // sign and magnitude
-  bool neg = (N[NW - 1] >> 63) != 0;
-  if (neg) {
-    uint64_t carry = 1;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const uint64_t v = ~N[i] + carry;
-      carry = (carry && v == 0) ? 1ull : 0ull;
-      N[i] = v;
-    }
-  }
-  for (int l = 0; l < L; ++l) {
-    // position of the leading one
-    int h = -1;
-#pragma unroll
-    for (int i = 0; i < NW; ++i)
-      if (N[i] != 0) h = 64 * i + 63 - __clzll(static_cast<long long>(N[i]));
-    double c;
-    if (h < 0) {
-      c = 0.0;
-    } else if (h <= 52) {
-      const double v = static_cast<double>(N[0]);  // below 2^53: exact
-      c = ldexp(neg ? -v : v, scale);
-#pragma unroll
-      for (int i = 0; i < NW; ++i) N[i] = 0;
-    } else {
-      const int sh = h - 52;  // the 53 leading bits start at bit sh
-      const int w = sh >> 6, b = sh & 63;
-      const uint64_t lo = word_at<NW>(N, w), hi = word_at<NW>(N, w + 1);
-      uint64_t M = (lo >> b) | (b ? (hi << (64 - b)) : 0ull);
-      M &= 0x001fffffffffffffull;
-      // round bit (bit sh-1) and sticky (any bit below sh-1)
-      const int rpos = sh - 1, rw = rpos >> 6, rb = rpos & 63;
-      const uint64_t rword = word_at<NW>(N, rw);
-      const bool round_bit = ((rword >> rb) & 1ull) != 0;
-      bool sticky = (rword & ((1ull << rb) - 1ull)) != 0;
-#pragma unroll
-      for (int i = 0; i < NW; ++i) sticky |= (i < rw) && (N[i] != 0);
-      const bool up = round_bit && (sticky || (M & 1ull));
-      const double v = static_cast<double>(M + (up ? 1ull : 0ull));  // <= 2^53: exact
-      c = ldexp(neg ? -v : v, scale + sh);
-      // remainder: the bits below sh, or 2^sh minus them (and the sign flips)
-#pragma unroll
-      for (int i = 0; i < NW; ++i) {
-        const int lo_bit = 64 * i;
-        uint64_t keep;
-        if (lo_bit + 64 <= sh) keep = ~0ull;
-        else if (lo_bit >= sh) keep = 0ull;
-        else keep = (1ull << (sh - lo_bit)) - 1ull;
-        N[i] &= keep;
-      }
-      if (up) {
-        uint64_t carry = 1;
-#pragma unroll
-        for (int i = 0; i < NW; ++i) {
-          const int lo_bit = 64 * i;
-          uint64_t keep;
-          if (lo_bit + 64 <= sh) keep = ~0ull;
-          else if (lo_bit >= sh) keep = 0ull;
-          else keep = (1ull << (sh - lo_bit)) - 1ull;
-          const uint64_t v = ~N[i] + carry;
-          carry = (carry && v == 0) ? 1ull : 0ull;
-          N[i] = v & keep;
-        }
-        neg = !neg;
-      }
-    }
-    // a limb that underflows in the final scaling is +0.0, like every zero limb
-    C[static_cast<int64_t>(l) * plane + idx] = c == 0.0 ? 0.0 : c;
-  }
 }
 
 template <int NW, class PT>

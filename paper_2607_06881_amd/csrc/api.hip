@@ -368,6 +368,54 @@ std::shared_ptr<const Planned> planned_for(int S, int T, int64_t m, int64_t n, i
   return sigma > 1 ? schedule_for(S, T, m, n, k, w, kind, sigma) : base;
 }
 
+// The fused small-product kernel (one block per 16 x 16 tile of C runs all five
+// steps) instead of the staged path, for outputs of at most 256 such tiles whose
+// levels fit its limits: there the staged path is bound by launch latency and
+// by its level GEMM's 128 x 128 tiles (one block per tile and level, the
+// heaviest level's pairs in series).  Each level belongs to one of the four
+// waves, levels dealt heaviest first to the least loaded wave; the product
+// qualifies while the most loaded wave runs at most 2048 MFMAs (about 55 us at
+// the matrix pipe's rate).  kc: the largest k chunk (a multiple of 4, at most
+// 256) whose digits fit the kernel's LDS beside the levels.
+constexpr int64_t kSmallMaxTiles = 256;
+constexpr int64_t kSmallMaxWaveMfma = 2048;
+
+bool small_plan(int64_t m, int64_t n, int64_t k, int limbs, const Resolved& r, int* kc_out,
+                mdg::SmallLevelOwners* owners) {
+  if (r.flags & (MDGEMM_INT8 | MDGEMM_KARATSUBA | MDGEMM_KARATSUBA_MIN_TERMS | MDGEMM_STAGED | MDGEMM_CHECK_FINITE))
+    return false;
+  // digits are held in LDS as FP32 values: exact while below 2^24
+  if (limbs > mdg::kSmallMaxLimbs || r.T + 1 > mdg::kSmallMaxLevels || k < 1 || r.w > 24) return false;
+  if (r.w * r.S + 52 > 64 * mdg::kSmallSplitWords || r.w * r.T + 55 > 64 * mdg::kSmallAccumWords) return false;
+  if (((m + 15) / 16) * ((n + 15) / 16) > kSmallMaxTiles) return false;
+  int load[4] = {0, 0, 0, 0};
+  bool done[mdg::kSmallMaxLevels] = {};
+  for (int rep = 0; rep <= r.T; ++rep) {
+    int best = -1, bp = -1;
+    for (int t = 0; t <= r.T; ++t) {
+      const int lo = t - (r.S - 1) > 0 ? t - (r.S - 1) : 0, hi = t < r.S - 1 ? t : r.S - 1;
+      const int p = hi - lo + 1;
+      if (!done[t] && p > bp) {
+        bp = p;
+        best = t;
+      }
+    }
+    int wv = 0;
+    for (int v = 1; v < 4; ++v)
+      if (load[v] < load[wv]) wv = v;
+    done[best] = true;
+    load[wv] += bp;
+    owners->wave[best] = static_cast<int8_t>(wv);
+  }
+  const int maxload = std::max(std::max(load[0], load[1]), std::max(load[2], load[3]));
+  if (static_cast<int64_t>(maxload) * ((k + 3) / 4) > kSmallMaxWaveMfma) return false;
+  int kc = static_cast<int>(std::min<int64_t>(256, (k + 3) / 4 * 4));
+  while (kc > 4 && mdg::small_product_lds(r.S, r.T, kc) > mdg::kSmallMaxLds) kc -= 4;
+  if (mdg::small_product_lds(r.S, r.T, kc) > mdg::kSmallMaxLds) return false;
+  *kc_out = kc;
+  return true;
+}
+
 struct Layout {
   size_t ea = 0, eb = 0, flag = 0, table = 0, da = 0, db = 0, g = 0, total = 0;
   bool f32 = false;  // FP32 panels with panel_k32 rows, else FP64 with panel_k rows
@@ -748,6 +796,9 @@ int mdgemm_workspace_layout(int64_t m, int64_t n, int64_t k, int limbs, const md
   MDG_TRY(resolve(limbs, m, n, k, opts, &r));
   if (m == 0 || n == 0 || k == 0 || (r.flags & MDGEMM_INT8)) return MDGEMM_EINVAL;
   if (!resolved_exact(r, k)) return MDGEMM_EEXACT;
+  int kc = 0;
+  mdg::SmallLevelOwners owners{};
+  if (small_plan(m, n, k, limbs, r, &kc, &owners)) return MDGEMM_EINVAL;
   const auto pl = planned_for(r.S, r.T, m, n, k, r.w, r.kind);
   Layout L;
   if (!layout(m, n, k, *pl, r.w, &L)) return MDGEMM_EINVAL;
@@ -794,11 +845,32 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   if (!schedule_exact(pl->s, k, r.w)) return MDGEMM_EEXACT;
   Layout L;
   if (!layout(m, n, k, *pl, r.w, &L)) return MDGEMM_EINVAL;
-  char* ws = nullptr;
-  LibraryBuffer lib;
   if (opts && opts->workspace) {
     if (opts->workspace_bytes < L.total) return MDGEMM_EWORKSPACE;
     if (workspace_overlaps(opts->workspace, L.total, m, n, k, limbs, A, B, C)) return MDGEMM_EINVAL;
+  }
+  int kc = 0;
+  mdg::SmallLevelOwners owners{};
+  if (small_plan(m, n, k, limbs, r, &kc, &owners)) {
+    // the fused small-product kernel: no workspace
+    std::unique_lock<std::mutex> tlock(timing().mu, std::defer_lock);
+    if (timed) {
+      tlock.lock();
+      timing().valid = false;
+      for (int i = 0; i < 3; ++i) MDG_TRY(record(i, s));
+    }
+    MDG_TRY(hip_status(mdg::launch_small_product(m, n, k, limbs, r.S, r.T, r.w, kc, owners, A, B, C, s)));
+    if (timed) {
+      MDG_TRY(record(3, s));
+      MDG_TRY(record(4, s));
+      timing().valid = true;
+    }
+    if (r.flags & MDGEMM_SYNC) MDG_TRY(hip_status(hipStreamSynchronize(s)));
+    return MDGEMM_OK;
+  }
+  char* ws = nullptr;
+  LibraryBuffer lib;
+  if (opts && opts->workspace) {
     ws = static_cast<char*>(opts->workspace);
   } else {
     MDG_TRY(lib.acquire(L.total, s, &ws));

@@ -14,22 +14,11 @@
 // memory through a vector atomic max; a last pass maps "no nonzero" to 0.
 #include <climits>
 
+#include "digits.h"
 #include "internal.h"
 
 namespace mdg {
 namespace {
-
-constexpr int kNoExp = INT_MIN;
-
-// frexp exponent of x; INT_MIN for +-0.  Subnormals: bit length of the
-// significand minus 1074.
-__device__ inline int frexp_exp_or_min(double x) {
-  uint64_t mag = static_cast<uint64_t>(__double_as_longlong(x)) & 0x7fffffffffffffffull;
-  if (mag == 0) return kNoExp;
-  int be = static_cast<int>(mag >> 52);
-  if (be == 0) return (64 - __clzll(static_cast<long long>(mag))) - 1074;
-  return be - 1022;
-}
 
 __device__ inline int wave_max(int v) {
 #pragma unroll

@@ -103,6 +103,26 @@ hipError_t launch_slice_gemm(int64_t m, int64_t n, int64_t k, const double* DAt,
 hipError_t launch_slice_gemm32(int64_t m, int64_t n, int64_t k, const float* DAt, const float* DBp, double* out,
                                const GemmJobs& jobs, hipStream_t stream);
 
+// The fused small-product kernel (small_product.hip): one block per 16 x 16
+// tile of C runs all five steps.  Limits: up to 4 limbs, digits below 2^24
+// (held in LDS as FP32), w S + 52 <= 320 bits
+// (the split's integer in 5 words), w T + 55 <= 448 bits (the level sum in 7
+// words), up to 32 levels; its dynamic LDS holds the levels of the tile and the
+// digits of one k chunk of kc (a multiple of 4).  wave[t] is the wave (0..3) that
+// forms level t.
+constexpr int kSmallMaxLimbs = 4;
+constexpr int kSmallSplitWords = 5;
+constexpr int kSmallAccumWords = 7;
+constexpr int kSmallMaxLevels = 32;
+constexpr size_t kSmallMaxLds = 150 * 1024;
+struct SmallLevelOwners {
+  int8_t wave[kSmallMaxLevels];
+};
+size_t small_product_lds(int S, int T, int kc);
+hipError_t launch_small_product(int64_t m, int64_t n, int64_t k, int L, int S, int T, int w, int kc,
+                                const SmallLevelOwners& owners, const double* A, const double* B, double* C,
+                                hipStream_t stream);
+
 // Copies `words` into the device array dst (stream-ordered kernel launches that
 // carry the words as arguments, so that no host memory is read later).
 hipError_t launch_upload(const std::vector<uint32_t>& words, uint32_t* dst, hipStream_t stream);

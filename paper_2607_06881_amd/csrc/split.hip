@@ -28,144 +28,11 @@
 // panels the level GEMM reads (see split_panel_kernel).
 #include <type_traits>
 
+#include "digits.h"
 #include "internal.h"
 
 namespace mdg {
 namespace {
-
-// acc += M 2^sh (neg == false) or acc -= M 2^sh (neg == true), modulo 2^(64 NW);
-// M < 2^53 and sh + 53 <= 64 NW.
-template <int NW>
-__device__ inline void add_shifted(uint64_t (&acc)[NW], uint64_t M, int sh, bool neg) {
-  const int w = sh >> 6, b = sh & 63;
-  const uint64_t lo = M << b;
-  const uint64_t hi = b ? (M >> (64 - b)) : 0ull;
-  uint64_t carry = 0;
-#pragma unroll
-  for (int i = 0; i < NW; ++i) {
-    const uint64_t t = (i == w) ? lo : ((i == w + 1) ? hi : 0ull);
-    const uint64_t a = acc[i];
-    if (!neg) {
-      const uint64_t s = a + t;
-      const uint64_t c1 = s < a;
-      const uint64_t s2 = s + carry;
-      const uint64_t c2 = s2 < s;
-      acc[i] = s2;
-      carry = c1 | c2;
-    } else {
-      const uint64_t s = a - t;
-      const uint64_t b1 = a < t;
-      const uint64_t s2 = s - carry;
-      const uint64_t b2 = s < carry;
-      acc[i] = s2;
-      carry = b1 | b2;
-    }
-  }
-}
-
-// D = floor(|V| / u) for one element with limbs xs[0..L-1] (L <= ML) on the
-// grid unit 2^g, as an NW-word integer; returns true when V < 0.
-template <int NW, int ML>
-__device__ inline bool floor_on_grid(const double (&xs)[ML], int L, int g, uint64_t (&I)[NW]) {
-  const double x0 = xs[0];
-  const bool neg = x0 < 0.0;
-  uint64_t acc[NW];
-#pragma unroll
-  for (int i = 0; i < NW; ++i) acc[i] = 0;
-  int tail = 0;  // +1 / -1: sign, relative to V, of the part of V below u that is not in acc
-  if (x0 != 0.0) {
-#pragma unroll
-    for (int l = 0; l < ML; ++l) {
-      const double xl = xs[l];
-      if (l >= L || xl == 0.0) break;  // normalized: every later limb is zero too
-      const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(xl));
-      const bool lneg = (bits >> 63) != 0;
-      const uint64_t mag = bits & 0x7fffffffffffffffull;
-      const int be = static_cast<int>(mag >> 52);
-      uint64_t M;
-      int ex;  // |xl| = M 2^ex
-      if (be != 0) {
-        M = (mag & 0x000fffffffffffffull) | 0x0010000000000000ull;
-        ex = be - 1075;
-      } else {
-        M = mag;
-        ex = -1074;
-      }
-      const int fe = ex + (64 - __clzll(static_cast<long long>(M)));  // frexp exponent of xl
-      if (fe <= g) {  // |xl| < u: xl and the rest of the limbs lie below the grid unit
-        tail = (lneg == neg) ? 1 : -1;
-        break;
-      }
-      add_shifted<NW>(acc, M, ex - g + 52, lneg != neg);
-    }
-  }
-  // I = floor(acc / 2^52), lowered by one when the fraction is zero and the
-  // part below u is negative (relative to the sign of V).
-  const bool frac_zero = (acc[0] & 0x000fffffffffffffull) == 0;
-#pragma unroll
-  for (int i = 0; i < NW; ++i) I[i] = (acc[i] >> 52) | (i + 1 < NW ? acc[i + 1] << 12 : 0ull);
-  if (frac_zero && tail < 0) {
-    uint64_t borrow = 1;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const uint64_t v = I[i];
-      I[i] = v - borrow;
-      borrow = (v < borrow) ? 1ull : 0ull;
-    }
-  }
-  return neg;
-}
-
-// The L limbs of the element at idx (limb stride ls), all loads issued together;
-// limbs beyond L are +0.0 (L is the same for every thread).
-template <int ML>
-__device__ inline void load_limbs(const double* __restrict__ X, int64_t ls, int L, int64_t idx, double (&xs)[ML]) {
-#pragma unroll
-  for (int l = 0; l < ML; ++l) xs[l] = l < L ? X[static_cast<int64_t>(l) * ls + idx] : 0.0;
-}
-
-__device__ inline double signed_digit(uint32_t d, bool neg) {
-  const double v = static_cast<double>(d);
-  return (d == 0u) ? 0.0 : (neg ? -v : v);  // zero digits are +0.0
-}
-
-// Word i of v (0 beyond the top), by an unrolled select: no dynamic register indexing.
-template <int NW>
-__device__ inline uint64_t word_or_zero(const uint64_t (&v)[NW], int i) {
-  uint64_t r = 0;
-#pragma unroll
-  for (int j = 0; j < NW; ++j) r = (j == i) ? v[j] : r;
-  return r;
-}
-
-// Digit s of I (bits w(S-1-s) .. w(S-s)-1) to out[s * stride] for every s, read
-// upward from bit 0 through a two-word window: one select over the words per
-// 64 bits consumed instead of one per digit.
-template <int NW, class OutT>
-__device__ inline void store_digits(const uint64_t (&I)[NW], int S, int w, bool neg, OutT* __restrict__ out,
-                                    int64_t stride) {
-  const uint64_t mask = (1ull << w) - 1ull;
-  uint64_t cur = I[0], nxt = NW > 1 ? I[1] : 0ull;
-  int wi = 0, b = 0;  // cur = word wi of I; b = next unread bit of cur
-  for (int j = 0; j < S; ++j) {
-    uint64_t f = cur >> b;
-    if (b + w > 64) f |= nxt << (64 - b);  // b > 64 - w > 0 here
-    const uint32_t d = static_cast<uint32_t>(f & mask);
-    if constexpr (std::is_integral<OutT>::value) {
-      const int32_t v = static_cast<int32_t>(d);  // int8 digits: the sign in integer arithmetic
-      out[static_cast<int64_t>(S - 1 - j) * stride] = static_cast<OutT>(neg ? -v : v);
-    } else {
-      out[static_cast<int64_t>(S - 1 - j) * stride] = static_cast<OutT>(signed_digit(d, neg));
-    }
-    b += w;
-    if (b >= 64) {
-      b -= 64;
-      cur = nxt;
-      ++wi;
-      nxt = word_or_zero<NW>(I, wi + 1);
-    }
-  }
-}
 
 // The combinations c = S .. C-1 of the Karatsuba schedule (sums of digits of
 // this element, digit set masks[c] as two 32-bit words) to out[c * stride]:

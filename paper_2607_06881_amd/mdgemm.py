@@ -32,6 +32,7 @@ MDGEMM_TIME_STAGES = 4
 MDGEMM_KARATSUBA = 8
 MDGEMM_KARATSUBA_MIN_TERMS = 16
 MDGEMM_INT8 = 32
+MDGEMM_STAGED = 64
 MDGEMM_SCHEDULE_INFO = 12
 MDGEMM_LAYOUT_INFO = 12
 MDGEMM_NOALLOC_MAX_BYTES = 64 << 20

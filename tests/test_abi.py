@@ -180,6 +180,24 @@ def test_workspace_overlapping_an_operand_is_refused_before_any_launch(lib, flag
     assert _ex(lib, m, n, k, L, workspace=far, workspace_bytes=need, flags=flags) != md.MDGEMM_EINVAL
 
 
+def test_workspace_layout_of_staged_and_fused_products(lib):
+    # small outputs run the fused kernel, which leaves nothing in the workspace:
+    # the layout is refused for them unless MDGEMM_STAGED selects the stages
+    with pytest.raises(md.MdgemmError) as ei:
+        md.mdgemm_workspace_layout(64, 64, 64, 2)
+    assert ei.value.status == md.MDGEMM_EINVAL
+    lay = md.mdgemm_workspace_layout(64, 64, 64, 2, flags=md.MDGEMM_STAGED)
+    assert lay["total"] == md.mdgemm_workspace_bytes(64, 64, 64, 2) and lay["planes"] == 8
+    # beyond 256 tiles of 16 x 16, or with too many MFMAs for one wave, the stages run
+    lay = md.mdgemm_workspace_layout(257, 256, 64, 2)
+    assert lay["direct_levels"] == 1 and lay["panel_bytes"] == 4 and lay["planes"] == 8
+    assert md.mdgemm_workspace_layout(64, 64, 4096, 2)["planes"] >= 8
+    a = lambda x: (x + 255) // 256 * 256
+    lay = md.mdgemm_workspace_layout(300, 270, 100, 3)
+    assert lay["ea"] == 0 and lay["eb"] == a(4 * 300) and lay["kp"] == 128 and lay["mp"] == 384
+    assert lay["np"] == 384 and lay["planes"] == 12 and lay["total"] == md.mdgemm_workspace_bytes(300, 270, 100, 3)
+
+
 def test_binding_refuses_cpu_tensors(lib):
     import torch
 

@@ -492,9 +492,10 @@ def test_mdgemm_library_workspace_grows():
     md.mdgemm_release()
 
 
-def _library_ex(A, B, C, stream):
-    """mdgemm_ex through the C ABI with the library-owned workspace on `stream`."""
-    o = md.make_opts(stream=stream)
+def _library_ex(A, B, C, stream, flags=md.MDGEMM_STAGED):
+    """mdgemm_ex through the C ABI with the library-owned workspace on `stream`
+    (the staged kernels: the fused small-product kernel uses no workspace)."""
+    o = md.make_opts(stream=stream, flags=flags)
     o.workspace, o.workspace_bytes = None, 0
     L, m, k = A.shape
     n = B.shape[2]
