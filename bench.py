@@ -26,9 +26,13 @@ Prints one JSON line:
   entries (corners, the rows and columns of extreme exponents, random ones)
   against the CPU oracle's chain (bit-exact limbs) and against the exact
   rational product (largest error over the stated tolerance);
+* ``exponent_classes`` (workloads with a range, c7): the same product grouped
+  by exponent class over that range (section 3's balancing), timed over a few
+  steps, with a sampled parity check against the oracle's grouped chain;
 * ``--extras`` adds ``karatsuba``, ``karatsuba_adaptive`` (the Karatsuba
-  schedule of the level products, bit-identical results) and ``int8`` (the
-  level products on the int8 matrix cores) lines;
+  schedule of the level products, bit-identical results), ``int8`` (the
+  level products on the int8 matrix cores) and ``sign_groups`` (section 3's
+  sign grouping, four products, the same limbs) lines;
 * ``cpu_baseline``: the CPU oracle's classic multiple-double GEMM (one
   sequential inner product per element, all host cores) timed on a bounded
   sample of the same product's rows.
@@ -478,6 +482,45 @@ def main(argv=None) -> int:
             out["karatsuba"] = extra(mode_opts(13), md.MDGEMM_KARATSUBA)
             out["karatsuba_adaptive"] = extra(mode_opts(md.MDGEMM_SLICE_BITS_AUTO), md.MDGEMM_KARATSUBA)
             out["int8"] = int8_mode()
+    def grouped(g_flags):
+        """A few timed steps of the same workload as a grouped product (section 3's
+        exponent classes over the workload's range, or sign groups), with a
+        sampled parity check against the oracle's grouped chain."""
+        from oracle import exact as ex
+        from oracle import pipeline as pl
+
+        g_opts = {"range_bits": w.range_bits} if w.range_bits else {}
+        g_bits, g_S, g_T = md.mdgemm_plan(m, n, k, L, flags=g_flags, **g_opts)
+        classes = 1 + -(-w.range_bits // g_bits) if (g_flags & md.MDGEMM_GROUP_EXPONENT) and w.range_bits else 1
+        groups = classes * (2 if g_flags & md.MDGEMM_GROUP_SIGN else 1)
+        g_ms, g_stage = measure(g_opts, args.adaptive_steps, 1, g_flags)
+        terms = groups * groups * workloads.pair_count(g_S, g_T)
+        tflops = 2.0 * m * n * k * terms / (g_stage[2] * 1e-3) / 1e12
+        res = {"classes": classes, "groups": groups, "slices": g_S, "cutoff": g_T, "levels": g_T + 1 + 2 * (classes - 1),
+               "pairs": terms, "steps": args.adaptive_steps, "ms_per_step": round(g_ms, 4),
+               "value": round(md_flops / (g_ms * 1e-3) / 1e9, 3), "stage_ms": [round(float(x), 4) for x in g_stage],
+               "slice_gemm_TFLOP/s": round(tflops, 3), "frac": round(tflops / MFMA_F64_PEAK_TFLOPS, 4)}
+        if not args.no_parity:
+            Cg = C.cpu().numpy()
+            rng = np.random.default_rng(w.seed + 2000)
+            entries = sorted({(int(rng.integers(m)), int(rng.integers(n))) for _ in range(8)})
+            ref = pl.reference_entries_groups(A_h, B_h, g_S, g_T, classes, bool(g_flags & md.MDGEMM_GROUP_SIGN),
+                                              entries, g_bits)
+            worst = 0.0
+            for (i, j) in entries:
+                want, mag = ex.exact_product(A_h, B_h, i, j)
+                worst = max(worst, float(abs(ex.value(Cg[:, i, j]) - want) / ex.tolerance(k, L, mag)))
+            res["parity"] = {"entries": len(entries),
+                             "bit_exact_vs_oracle": all(Cg[:, i, j].tolist() == ref[(i, j)]["limbs"]
+                                                        for (i, j) in entries),
+                             "max_err_over_tolerance": worst}
+        return res
+
+    if w.range_bits and bits_arg == 13 and not sched_flags and args.adaptive_steps > 0:
+        # the paper's own balancing (exponent classes) beside the range balancing of the headline
+        out["exponent_classes"] = grouped(md.MDGEMM_GROUP_EXPONENT)
+    if args.extras and bits_arg == 13 and not sched_flags and args.adaptive_steps > 0:
+        out["sign_groups"] = grouped(md.MDGEMM_GROUP_SIGN)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, A_h, B_h, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -74,6 +74,8 @@ extern "C" {
 #define MDGEMM_KARATSUBA_MIN_TERMS 16u /* the Karatsuba schedule with the fewest GEMMs, always */
 #define MDGEMM_INT8 32u        /* level products on the int8 matrix cores, digits of at most 7 bits (see below) */
 #define MDGEMM_STAGED 64u      /* always the staged kernels, never the fused small-product kernel (see below) */
+#define MDGEMM_GROUP_SIGN 128u      /* section 3's sign groups: A = A+ + A-, B likewise, four products (see below) */
+#define MDGEMM_GROUP_EXPONENT 256u  /* section 3's exponent classes over range_bits (see below) */
 
 /* cutoff selectors for mdgemm_opts.cutoff (else an explicit T in 0 .. 2S-2) */
 #define MDGEMM_CUTOFF_DEFAULT -1  /* T = S - 1: the pair set of the rewritten product */
@@ -86,7 +88,7 @@ typedef struct mdgemm_opts {
   int slices_per_limb;    /* 13-bit digits per limb, S = limbs * slices_per_limb; 0 = the default count (below) */
   int cutoff;             /* largest kept p + q; MDGEMM_CUTOFF_DEFAULT or _ALL or 0..2S-2 */
   unsigned flags;         /* MDGEMM_CHECK_FINITE, _SYNC, _TIME_STAGES, _KARATSUBA, _KARATSUBA_MIN_TERMS, _INT8,
-                             _STAGED */
+                             _STAGED, _GROUP_SIGN, _GROUP_EXPONENT */
   int slice_bits;         /* digit width w: 0 = 13 (section 2), 1..26, or MDGEMM_SLICE_BITS_AUTO */
   int slices;             /* digits per element S; 0 = derived (see below) */
   int range_bits;         /* range balancing: full precision down to 2^-range_bits of the line; 0 = off */
@@ -140,6 +142,30 @@ typedef struct mdgemm_opts {
  * with the same slice_bits, slices and cutoff.  Double-double at k = 4096:
  * w = 7, S = 15, T = 14 (120 pairs).  The level products run on the library's
  * own int8 kernel, all levels in one launch. */
+
+/* Grouped products (section 3, the balancing problems: numbers grouped by sign,
+ * A = A+ + A-, and by the exponent of their leading part, A = A_0 + A_1 + ...,
+ * each group multiplied with each group of the other operand).
+ *  - MDGEMM_GROUP_EXPONENT: every line keeps its grid exponent E; an element
+ *    whose leading limb has frexp exponent e is in class
+ *    c = min(Ge - 1, floor((E - e) / w)), with Ge = 1 + ceil(range_bits / w)
+ *    classes, and its digits are taken on the class grid E - c w (so it keeps
+ *    its leading bits); range_bits then sets the classes instead of adding
+ *    digits: S = S0 + 1 (the element lies up to one digit below its class
+ *    grid) and the default cutoff T = S0 + 1 (S0 the digit count without range
+ *    balancing), applied to every class pair.
+ *  - MDGEMM_GROUP_SIGN: positive and negative elements in separate groups on the
+ *    same grid (both flags: 2 Ge groups).
+ * Every group pair (g, h) contributes its pairs p + q <= T at level
+ * p + q + c(g) + c(h), so the product has T + 1 + 2 (Ge - 1) levels, and every
+ * element belongs to one group, so a level's sums keep the bound of the pair
+ * schedule (pairs_t k (2^w - 1)^2 < 2^53 over the pairs of one group pair).
+ * mdgemm_plan reports S (digits per group) and T (per group pair).  Sign groups
+ * give the same digits summed in a different grouping: the limbs equal the
+ * ungrouped product's bit for bit, at four times the pairs.  Up to 4 limbs and
+ * w S + 52 <= 384; not with MDGEMM_INT8, the Karatsuba flags or
+ * MDGEMM_SLICE_BITS_AUTO (MDGEMM_EINVAL).  The workspace holds G S digit panels
+ * of each operand and the T + 1 + 2 (Ge - 1) level planes. */
 
 /* Small products.  For an output of at most 256 tiles of 16 x 16 (up to 4
  * limbs, digits of at most 24 bits, at most 32 levels, the level sum of an

@@ -277,7 +277,7 @@ def _max_pairs(S: int, T: int) -> int:
 
 
 def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_limb: int = 0, cutoff: int = -1,
-         range_bits: int = 0, int8: bool = False):
+         range_bits: int = 0, int8: bool = False, group_exponent: bool = False, group_sign: bool = False):
     """(w, S, T) of the product's digit width, digit count and cutoff, or None when
     the levels cannot stay exact.  Written from the options' definitions:
 
@@ -294,20 +294,41 @@ def plan(L: int, k: int, *, slice_bits: int = 0, slices: int = 0, slices_per_lim
       bits; slice_bits 0 or -1 take the widest w = 7, 6, ..., 1 whose (S, T) is
       valid and whose level sums stay below 2^31 (the same bound with 2^31 in
       place of 2^53), slice_bits 1..7 that width, S0 = slices or
-      ceil(13 default_slices(L) / w), at most 64 digits.
+      ceil(13 default_slices(L) / w), at most 64 digits;
+    * exponent classes (group_exponent, section 3): range_bits sets
+      1 + ceil(range_bits / w) classes instead of extra digits, one more digit
+      per element (S = S0 + 1 when there is more than one class), default cutoff
+      S0 + 1 per class pair; the levels reach T + 2 (classes - 1); sign groups
+      (group_sign) change no count; grouped products take up to 4 limbs and no
+      automatic width.
     Raises ValueError for invalid options (S > 68, S w > 908, ...)."""
     bits = 13 * default_slices(L)
+    if ((group_exponent and range_bits > 0) or group_sign) and slice_bits == -1:
+        raise ValueError("groups with the automatic width")
 
     def finish(w, S0):
-        D = -(-range_bits // w)
+        if group_exponent:
+            # exponent classes (section 3): range_bits sets 1 + ceil(range_bits / w)
+            # classes; one more digit per element (it lies up to one digit below
+            # its class grid) when there is more than one class
+            D = 1 if range_bits > 0 else 0
+            classes = 1 + -(-range_bits // w)
+        else:
+            D = -(-range_bits // w)
+            classes = 1
         S = S0 + D
         if S < 1 or S > (64 if int8 else MAX_SLICES) or S * w > MAX_DIGIT_BITS:
             raise ValueError("digit count")
         T = S0 - 1 + 2 * D if cutoff == -1 else (2 * S - 2 if cutoff == -2 else cutoff)
         if not 0 <= T <= 2 * S - 2:
             raise ValueError("cutoff")
-        if w * T + 55 > 64 * 28:  # the exact level sum fits 28 words
+        if w * (T + 2 * (classes - 1)) + 55 > 64 * 28:  # the exact level sum fits 28 words
             raise ValueError("levels")
+        if (group_exponent and classes > 1) or group_sign:
+            # grouped products: up to 4 limbs, the split's integer in 6 words, 4096 panels
+            if int8 or slice_bits == -1 or L > 4 or -(-(w * S + 52) // 64) > 6 or \
+                    (2 if group_sign else 1) * classes * S > 4096:
+                raise ValueError("groups")
         return w, S, T
 
     def exact_ok(w, S, T):

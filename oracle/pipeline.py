@@ -126,3 +126,108 @@ def full_reference(A: np.ndarray, B: np.ndarray, S: int, T: int, bits: int = 13)
             z = exact.accumulate([int(G[t, i, j]) for t in range(T + 1)], int(EA[i]), int(EB[j]), bits)
             C[:, i, j] = exact.round_to_limbs(z, L)
     return {"EA": EA, "EB": EB, "DA": DA, "DB": DB, "G": G, "C": C}
+
+
+# --------------------------------------------------------------------------
+# Grouped products (section 3: numbers grouped by sign, A = A+ + A-, and by the
+# exponent of their leading part, A = A_0 + A_1 + ...; every group of A is
+# multiplied with every group of B)
+# --------------------------------------------------------------------------
+
+def element_groups(X0: np.ndarray, E: np.ndarray, axis: int, classes: int, sign: bool, bits: int = 13) -> np.ndarray:
+    """Group of every element of a leading-limb plane [rows][cols]: exponent class
+    c = min(classes - 1, floor((E - e) / bits)) with e the frexp exponent of the
+    element (0 for a zero element) and E its line's grid exponent, plus
+    `classes` for a negative element when grouping by sign."""
+    X0 = np.asarray(X0, dtype=np.float64)
+    Eb = (E[:, None] if axis == 0 else E[None, :]).astype(np.int64)
+    e = np.frexp(X0)[1].astype(np.int64)
+    c = np.minimum(classes - 1, (Eb - e) // bits)
+    c = np.where(X0 == 0.0, 0, c)
+    if sign:
+        c = c + np.where(X0 < 0.0, classes, 0)
+    return c
+
+
+def group_digits(X: np.ndarray, E: np.ndarray, S: int, axis: int, classes: int, sign: bool,
+                 bits: int = 13) -> np.ndarray:
+    """Digits [G][S][rows][cols] of the groups of X [L][rows][cols]: group g holds
+    the digits of its own elements (zeros elsewhere), taken on the grid of its
+    exponent class, E - (g mod classes) bits."""
+    grp = element_groups(X[0], E, axis, classes, sign, bits)
+    G = classes * (2 if sign else 1)
+    out = np.zeros((G, S) + X.shape[1:], dtype=np.float64)
+    for g in range(G):
+        mask = grp == g
+        if not mask.any():
+            continue
+        Xg = np.where(mask[None], X, 0.0)
+        Eg = (np.asarray(E, dtype=np.int64) - (g % classes) * bits).astype(np.int32)
+        out[g] = coracle.split(Xg, Eg, S, axis, bits)
+    return out
+
+
+def group_levels(DA: np.ndarray, DB: np.ndarray, T: int, classes: int) -> np.ndarray:
+    """Levels of a grouped product: group pair (g, h) contributes DA[g][p] . DB[h][q]
+    for p + q <= T at level p + q + (g mod classes) + (h mod classes); levels
+    0 .. T + 2 (classes - 1), float64 matrix products (exact: integers < 2^53)."""
+    G, S, m, k = DA.shape
+    n = DB.shape[3]
+    Tg = T + 2 * (classes - 1)
+    out = np.zeros((Tg + 1, m, n), dtype=np.float64)
+    for g in range(G):
+        for h in range(G):
+            o = g % classes + h % classes
+            if not DA[g].any() or not DB[h].any():
+                continue
+            for t in range(T + 1):
+                for p, q in exact.pairs_of_level(t, S):
+                    out[t + o] += DA[g][p] @ DB[h][q]
+    return out
+
+
+def full_reference_groups(A: np.ndarray, B: np.ndarray, S: int, T: int, classes: int, sign: bool,
+                          bits: int = 13) -> np.ndarray:
+    """C [L][m][n] of the grouped product: group digits, levels, exact sum and
+    greedy rounding (the sum uses the level weights of the shared line grids)."""
+    L, m, k = A.shape
+    n = B.shape[2]
+    EA, EB = exponents(A, B)
+    DA = group_digits(A, EA, S, 0, classes, sign, bits)
+    DB = group_digits(B, EB, S, 1, classes, sign, bits)
+    G = group_levels(DA, DB, T, classes)
+    C = np.zeros((L, m, n), dtype=np.float64)
+    for i in range(m):
+        for j in range(n):
+            z = exact.accumulate([int(G[t, i, j]) for t in range(G.shape[0])], int(EA[i]), int(EB[j]), bits)
+            C[:, i, j] = exact.round_to_limbs(z, L)
+    return C
+
+
+def reference_entries_groups(A: np.ndarray, B: np.ndarray, S: int, T: int, classes: int, sign: bool, entries,
+                             bits: int = 13) -> dict:
+    """The grouped chain for chosen output entries: {(i, j): {"levels", "limbs"}}."""
+    L = A.shape[0]
+    EA, EB = exponents(A, B)
+    G = classes * (2 if sign else 1)
+    rows = sorted({i for i, _ in entries})
+    cols = sorted({j for _, j in entries})
+    dA = {i: group_digits(np.ascontiguousarray(A[:, i:i + 1, :]), EA[i:i + 1], S, 0, classes, sign, bits)[:, :, 0, :]
+          for i in rows}
+    dB = {j: group_digits(np.ascontiguousarray(B[:, :, j:j + 1]), EB[j:j + 1], S, 1, classes, sign, bits)[:, :, :, 0]
+          for j in cols}
+    out = {}
+    Tg = T + 2 * (classes - 1)
+    for i, j in entries:
+        lv = [0] * (Tg + 1)
+        a = dA[i].astype(np.int64)
+        b = dB[j].astype(np.int64)
+        for g in range(G):
+            for h in range(G):
+                o = g % classes + h % classes
+                for t in range(T + 1):
+                    for p, q in exact.pairs_of_level(t, S):
+                        lv[t + o] += int(np.dot(a[g][p], b[h][q]))
+        z = exact.accumulate(lv, int(EA[i]), int(EB[j]), bits)
+        out[(i, j)] = {"levels": lv, "limbs": exact.round_to_limbs(z, L)}
+    return out

@@ -159,7 +159,8 @@ ScheduleCache& schedule_cache() {
 
 // kKaratsuba: the cost model's choice (may be the pair schedule);
 // kKaratsubaMin: the Karatsuba schedule with the fewest GEMM terms.
-enum class Kind { kLevels = 0, kPerPair = 1, kKaratsuba = 2, kKaratsubaMin = 3 };
+// kGroups: the grouped pair schedule (exponent classes and / or sign groups).
+enum class Kind { kLevels = 0, kPerPair = 1, kKaratsuba = 2, kKaratsubaMin = 3, kGroups = 4 };
 
 Kind kind_of(unsigned flags) {
   if (flags & MDGEMM_KARATSUBA_MIN_TERMS) return Kind::kKaratsubaMin;
@@ -169,11 +170,12 @@ Kind kind_of(unsigned flags) {
 // The schedule of the level products for S digits, cutoff T, an m x k by k x n
 // product and width w, its jobs split into `sigma` k chunks; built once per key
 // and kept for the life of the process.
+// group: 2 Ge + sign for Kind::kGroups (Ge exponent classes, sign groups or not).
 std::shared_ptr<const Planned> schedule_for(int S, int T, int64_t m, int64_t n, int64_t k, int w, Kind kind,
-                                            int sigma = 1) {
+                                            int sigma = 1, int group = 0) {
   const bool kara = kind == Kind::kKaratsuba || kind == Kind::kKaratsubaMin;
   const bool model = kind == Kind::kKaratsuba;
-  const int64_t budget = kara ? job_budget(k, w) : 0;
+  const int64_t budget = kara ? job_budget(k, w) : (kind == Kind::kGroups ? group : 0);
   const int mc = model ? size_code(m) : 0, nc = model ? size_code(n) : 0, kc = model ? size_code(k) : 0;
   const auto key = std::make_tuple(S, T, budget, mc, nc, kc, static_cast<int>(kind), sigma);
   ScheduleCache& c = schedule_cache();
@@ -183,8 +185,9 @@ std::shared_ptr<const Planned> schedule_for(int S, int T, int64_t m, int64_t n, 
     if (it != c.map.end()) return it->second;
   }
   auto pl = std::make_shared<Planned>();
-  if (sigma > 1) pl->s = mdg::split_k(schedule_for(S, T, m, n, k, w, kind, 1)->s, sigma);
+  if (sigma > 1) pl->s = mdg::split_k(schedule_for(S, T, m, n, k, w, kind, 1, group)->s, sigma);
   else if (kind == Kind::kLevels) pl->s = mdg::pair_schedule(S, T);
+  else if (kind == Kind::kGroups) pl->s = mdg::group_schedule(S, T, group / 2, (group & 1) != 0);
   else if (kind == Kind::kPerPair) pl->s = mdg::per_pair_schedule(S, T);
   else if (kind == Kind::kKaratsuba)
     pl->s = mdg::karatsuba_schedule(S, T, budget, schedule_costs(mc, nc, kc, T + 1), true);
@@ -207,10 +210,18 @@ bool schedule_exact(const mdg::Schedule& s, int64_t k, int w) {
 
 struct Resolved {
   int S = 0, T = 0, w = mdg::kSliceBits;
+  int Ge = 1;         // exponent classes (MDGEMM_GROUP_EXPONENT)
+  bool sign = false;  // sign groups (MDGEMM_GROUP_SIGN)
   hipStream_t stream = nullptr;
   unsigned flags = 0;
-  Kind kind = Kind::kLevels;  // pair schedule, or Karatsuba (see kind_of)
+  Kind kind = Kind::kLevels;  // pair schedule, or Karatsuba (see kind_of), or groups
 };
+
+// The group parameters of a grouped schedule (0 for the others) and the levels
+// of the product: T + 1, and 2 (Ge - 1) more with exponent classes (the class
+// pairs' levels start up to 2 (Ge - 1) digits further down).
+int group_code(const Resolved& r) { return r.kind == Kind::kGroups ? 2 * r.Ge + (r.sign ? 1 : 0) : 0; }
+int total_levels(const Resolved& r) { return r.T + 1 + 2 * (r.Ge - 1); }
 
 // The default count of 13-bit digits for L limbs.  Up to quad doubles, four per
 // limb: section 2's quarters of each limb, 52 L bits, which cover the 53 L - 4
@@ -324,15 +335,31 @@ int resolve(int limbs, int64_t m, int64_t n, int64_t k, const mdgemm_opts* opts,
   }
   // range balancing: D more digits on the same line grid, and the cutoff raised by
   // 2D so that a product of two elements D digits below their lines' exponents
-  // keeps its S0 leading levels
-  const int S0 = r->S, D = range_digits(range_bits, r->w);
+  // keeps its S0 leading levels.  With exponent classes the range sets the
+  // number of classes instead, Ge = 1 + ceil(range_bits / w), and each class
+  // element gets one more digit (it lies up to one digit below its class grid),
+  // with the cutoff of one such digit per factor.
+  const unsigned flags = opts ? opts->flags : 0u;
+  const bool gexp = (flags & MDGEMM_GROUP_EXPONENT) != 0;
+  const int S0 = r->S, D = gexp ? (range_bits > 0 ? 1 : 0) : range_digits(range_bits, r->w);
+  r->Ge = gexp ? 1 + range_digits(range_bits, r->w) : 1;
+  r->sign = (flags & MDGEMM_GROUP_SIGN) != 0;
   r->S = S0 + D;
   if (!width_ok(r->S, r->w) || (int8 && r->S > mdg::kI8MaxSlices)) return MDGEMM_EINVAL;
   const int cutoff = opts ? opts->cutoff : MDGEMM_CUTOFF_DEFAULT;
   if (cutoff < 0 && cutoff != MDGEMM_CUTOFF_DEFAULT && cutoff != MDGEMM_CUTOFF_ALL) return MDGEMM_EINVAL;
   r->T = cutoff_for(cutoff, S0, D);
   if (r->T < 0 || r->T > 2 * r->S - 2) return MDGEMM_EINVAL;
-  if (!levels_ok(r->T + 1, r->w)) return MDGEMM_EINVAL;
+  if (!levels_ok(r->T + 1 + 2 * (r->Ge - 1), r->w)) return MDGEMM_EINVAL;
+  if (r->Ge > 1 || r->sign) {
+    // grouped products: the pair schedule over group pairs, up to 4 limbs, the
+    // split's integer in kGroupSplitWords words, at most 4096 panels (G S)
+    if (int8 || (flags & (MDGEMM_KARATSUBA | MDGEMM_KARATSUBA_MIN_TERMS)) || bits == MDGEMM_SLICE_BITS_AUTO ||
+        limbs > 4 || (r->w * r->S + 52 + 63) / 64 > mdg::kGroupSplitWords ||
+        (r->sign ? 2 : 1) * r->Ge * r->S > 4096)
+      return MDGEMM_EINVAL;
+    r->kind = Kind::kGroups;
+  }
   r->stream = opts ? static_cast<hipStream_t>(opts->stream) : nullptr;
   r->flags = opts ? opts->flags : 0u;
   return MDGEMM_OK;
@@ -362,10 +389,11 @@ int ksplit_for(int64_t m, int64_t n, int64_t k, const Planned& pl, bool f32) {
 }
 
 // The schedule a product runs: the planned one, split in k when it is small.
-std::shared_ptr<const Planned> planned_for(int S, int T, int64_t m, int64_t n, int64_t k, int w, Kind kind) {
-  auto base = schedule_for(S, T, m, n, k, w, kind);
+std::shared_ptr<const Planned> planned_for(int S, int T, int64_t m, int64_t n, int64_t k, int w, Kind kind,
+                                           int group = 0) {
+  auto base = schedule_for(S, T, m, n, k, w, kind, 1, group);
   const int sigma = ksplit_for(m, n, k, *base, panels_f32(*base, w));
-  return sigma > 1 ? schedule_for(S, T, m, n, k, w, kind, sigma) : base;
+  return sigma > 1 ? schedule_for(S, T, m, n, k, w, kind, sigma, group) : base;
 }
 
 // The fused small-product kernel (one block per 16 x 16 tile of C runs all five
@@ -382,7 +410,8 @@ constexpr int64_t kSmallMaxWaveMfma = 2048;
 
 bool small_plan(int64_t m, int64_t n, int64_t k, int limbs, const Resolved& r, int* kc_out,
                 mdg::SmallLevelOwners* owners) {
-  if (r.flags & (MDGEMM_INT8 | MDGEMM_KARATSUBA | MDGEMM_KARATSUBA_MIN_TERMS | MDGEMM_STAGED | MDGEMM_CHECK_FINITE))
+  if (r.kind == Kind::kGroups ||
+      (r.flags & (MDGEMM_INT8 | MDGEMM_KARATSUBA | MDGEMM_KARATSUBA_MIN_TERMS | MDGEMM_STAGED | MDGEMM_CHECK_FINITE)))
     return false;
   // digits are held in LDS as FP32 values: exact while below 2^24
   if (limbs > mdg::kSmallMaxLimbs || r.T + 1 > mdg::kSmallMaxLevels || k < 1 || r.w > 24) return false;
@@ -785,7 +814,7 @@ size_t mdgemm_workspace_bytes(int64_t m, int64_t n, int64_t k, int limbs, const 
     return layout_int8(m, n, k, r.S, r.T, &L8) ? L8.total : SIZE_MAX;
   }
   Layout L;
-  if (!layout(m, n, k, *planned_for(r.S, r.T, m, n, k, r.w, r.kind), r.w, &L)) return SIZE_MAX;
+  if (!layout(m, n, k, *planned_for(r.S, r.T, m, n, k, r.w, r.kind, group_code(r)), r.w, &L)) return SIZE_MAX;
   return L.total;
 }
 
@@ -799,7 +828,7 @@ int mdgemm_workspace_layout(int64_t m, int64_t n, int64_t k, int limbs, const md
   int kc = 0;
   mdg::SmallLevelOwners owners{};
   if (small_plan(m, n, k, limbs, r, &kc, &owners)) return MDGEMM_EINVAL;
-  const auto pl = planned_for(r.S, r.T, m, n, k, r.w, r.kind);
+  const auto pl = planned_for(r.S, r.T, m, n, k, r.w, r.kind, group_code(r));
   Layout L;
   if (!layout(m, n, k, *pl, r.w, &L)) return MDGEMM_EINVAL;
   const int64_t v[MDGEMM_LAYOUT_INFO] = {static_cast<int64_t>(L.ea),
@@ -841,7 +870,7 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   }
 
   if (r.flags & MDGEMM_INT8) return run_int8(m, n, k, limbs, A, B, C, opts, r);
-  const auto pl = planned_for(r.S, r.T, m, n, k, r.w, r.kind);
+  const auto pl = planned_for(r.S, r.T, m, n, k, r.w, r.kind, group_code(r));
   if (!schedule_exact(pl->s, k, r.w)) return MDGEMM_EEXACT;
   Layout L;
   if (!layout(m, n, k, *pl, r.w, &L)) return MDGEMM_EINVAL;
@@ -892,21 +921,27 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
     // a2: exact splits into S digit panels and, beside them, the schedule's
     // combinations (digit sums) from the same integers
     MDG_TRY(hip_status(mdg::launch_upload(pl->t.words, w.table, s)));
-    MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, r.w, 0, A, w.EA, w.DA, true, s,
-                                         w.table + pl->t.masks_a_off, static_cast<int>(pl->s.mask_a.size()),
-                                         w.f32)));
-    MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, r.w, 1, B, w.EB, w.DB, true, s,
-                                         w.table + pl->t.masks_b_off, static_cast<int>(pl->s.mask_b.size()),
-                                         w.f32)));
+    if (r.kind == Kind::kGroups) {
+      // grouped digits: each element's S digits in its group's panels, on its class grid
+      MDG_TRY(hip_status(mdg::launch_split_groups(m, k, limbs, r.S, r.w, 0, A, w.EA, w.DA, w.f32, r.Ge, r.sign, s)));
+      MDG_TRY(hip_status(mdg::launch_split_groups(k, n, limbs, r.S, r.w, 1, B, w.EB, w.DB, w.f32, r.Ge, r.sign, s)));
+    } else {
+      MDG_TRY(hip_status(mdg::launch_split(m, k, limbs, r.S, r.w, 0, A, w.EA, w.DA, true, s,
+                                           w.table + pl->t.masks_a_off, static_cast<int>(pl->s.mask_a.size()),
+                                           w.f32)));
+      MDG_TRY(hip_status(mdg::launch_split(k, n, limbs, r.S, r.w, 1, B, w.EB, w.DB, true, s,
+                                           w.table + pl->t.masks_b_off, static_cast<int>(pl->s.mask_b.size()),
+                                           w.f32)));
+    }
     if (timed) MDG_TRY(record(2, s));
     // a3: level GEMMs (or the Karatsuba products) on the FP64 matrix cores
     MDG_TRY(enqueue_gemm(*pl, m, n, k, w, w.G, s));
     if (timed) MDG_TRY(record(3, s));
     // a4 + a5: exact accumulation and greedy rounding into L limbs
     if (pl->s.direct_levels) {
-      MDG_TRY(hip_status(mdg::launch_accum_renorm(m, n, limbs, r.T + 1, r.w, w.G, w.EA, w.EB, C, s)));
+      MDG_TRY(hip_status(mdg::launch_accum_renorm(m, n, limbs, total_levels(r), r.w, w.G, w.EA, w.EB, C, s)));
     } else {
-      MDG_TRY(hip_status(mdg::launch_plan_accum(m, n, limbs, r.T + 1, r.w, pl->s.planes, w.G,
+      MDG_TRY(hip_status(mdg::launch_plan_accum(m, n, limbs, total_levels(r), r.w, pl->s.planes, w.G,
                                                 w.table + pl->t.chunk_first_off, w.table + pl->t.chunks_off, w.EA,
                                                 w.EB, C, nullptr, s)));
     }

@@ -62,6 +62,16 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
                         void* D, bool panel, hipStream_t stream, const uint32_t* masks = nullptr,
                         int combos = 0, bool f32 = false);
 
+// a2 for grouped products (section 3's grouping by sign and by exponent class):
+// panels as launch_split (panel == true), G = (sign ? 2 : 1) Ge groups of S
+// panels each; element in group g = sign group * Ge + class, class c =
+// min(Ge - 1, floor((E - e) / w)) (e: the frexp exponent of its leading limb, 0
+// for a zero element), split on the grid E - c w into panels g S .. g S + S - 1,
+// zeros in the other groups' panels.  Up to 4 limbs and w S + 52 <= 384 bits.
+constexpr int kGroupSplitWords = 6;
+hipError_t launch_split_groups(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
+                               const int32_t* E, void* D, bool f32, int Ge, bool sign, hipStream_t stream);
+
 // Layout of the int8 digits: rows of pitch kI8Pad + S kp bytes (kp = k rounded
 // up to 128), the first kI8Pad bytes of every row zero, A's rows m rounded up to
 // 256, B's (columns of B) n rounded up to 256 (those extra rows are never

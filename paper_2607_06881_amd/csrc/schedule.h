@@ -59,6 +59,16 @@ struct Schedule {
 // pairs (p, t - p) of the level in increasing p, plane = level.
 Schedule pair_schedule(int S, int T);
 
+// Grouped products (section 3: the numbers grouped by exponent class and, with
+// sign, by sign; every group pair multiplied): G = (sign ? 2 : 1) Ge groups of S
+// digit panels (group g's digits are combinations g S .. g S + S - 1, on a grid
+// g % Ge digits below the line's), every group pair (g, h) keeps its pairs
+// p + q <= T at level p + q + g % Ge + h % Ge; one job per level
+// t <= T + 2 (Ge - 1), heaviest first, plane = level.  The schedule's S is G S
+// and its T is T + 2 (Ge - 1).  Every element lies in one group, so a level sums
+// at most max_pairs(S, T) products per k index: the pair schedule's bound.
+Schedule group_schedule(int S, int T, int Ge, bool sign);
+
 // One job per pair (p, q) with p + q <= T, written to plane p S + q.
 Schedule per_pair_schedule(int S, int T);
 

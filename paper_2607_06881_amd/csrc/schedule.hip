@@ -272,6 +272,54 @@ Schedule pair_schedule(int S, int T) {
   return s;
 }
 
+Schedule group_schedule(int S, int T, int Ge, bool sign) {
+  const int G = (sign ? 2 : 1) * Ge;
+  auto off = [Ge](int g) { return g % Ge; };  // exponent class of group g, in digits
+  const int Tg = T + 2 * (Ge - 1);
+  Schedule s;
+  s.S = G * S;
+  s.T = Tg;
+  s.direct_levels = true;
+  for (int c = 0; c < G * S; ++c) {
+    s.mask_a.push_back(0ull);  // no combinations: digit sets are never read
+    s.mask_b.push_back(0ull);
+    s.par1_a.push_back(-1);
+    s.par2_a.push_back(-1);
+    s.par1_b.push_back(-1);
+    s.par2_b.push_back(-1);
+    s.depth_a.push_back(0);
+    s.depth_b.push_back(0);
+  }
+  std::vector<std::vector<std::pair<int, int>>> lv(Tg + 1);
+  for (int g = 0; g < G; ++g)
+    for (int h = 0; h < G; ++h)
+      for (int p = 0; p < S; ++p)
+        for (int q = 0; q < S && p + q <= T; ++q) lv[p + q + off(g) + off(h)].push_back({g * S + p, h * S + q});
+  std::vector<int> order;
+  for (int t = 0; t <= Tg; ++t) order.push_back(t);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return lv[x].size() > lv[y].size(); });
+  for (int t : order) {
+    if (lv[t].empty()) continue;  // (cannot happen: level t always has the pair (0, t) of some class pair)
+    s.job_first.push_back(static_cast<int>(s.pair_a.size()));
+    s.job_count.push_back(static_cast<int>(lv[t].size()));
+    s.job_out.push_back(t);
+    for (const auto& pq : lv[t]) {
+      s.pair_a.push_back(pq.first);
+      s.pair_b.push_back(pq.second);
+    }
+    s.max_job_weight = std::max<int64_t>(s.max_job_weight, static_cast<int64_t>(lv[t].size()));
+  }
+  s.terms = static_cast<int>(s.pair_a.size());
+  s.planes = Tg + 1;
+  for (int t = 0; t <= Tg; ++t) {
+    s.plane_first.push_back(t);
+    s.entry_level.push_back(t);
+    s.entry_coef.push_back(1);
+  }
+  s.plane_first.push_back(Tg + 1);
+  return s;
+}
+
 Schedule per_pair_schedule(int S, int T) {
   Schedule s = pair_schedule(S, T);
   s.job_first.clear();

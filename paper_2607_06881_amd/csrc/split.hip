@@ -203,6 +203,56 @@ __global__ void __launch_bounds__(256) split_int8t_kernel(int64_t rows, int64_t 
   }
 }
 
+// Grouped panels (section 3: numbers grouped by sign and by the exponent of
+// their leading part, each group multiplied separately).  Every element belongs
+// to one of G = (sign ? 2 : 1) Ge groups: exponent class c = 0 for a zero
+// element, else min(Ge - 1, floor((E - e) / w)) where e is the frexp exponent of
+// its leading limb (the class of elements whose leading digit falls c digits
+// below the line's grid), and sign group 1 for a negative element with sign
+// grouping, else 0; g = sign group * Ge + c.  Its S digits are taken on the
+// class grid E - c w (so the element keeps its leading bits) and written to
+// panels g S .. g S + S - 1; the S digits of the other G - 1 groups are zero.
+// (e <= E - c w, so |V| < 2^(E - c w): the split's precondition holds.)
+// One element per thread, the panel layout of split_panel_kernel.
+template <int NW, int ML, class OutT>
+__global__ void __launch_bounds__(256) split_groups_kernel(int64_t rows, int64_t cols, int L, int S, int w, int axis,
+                                                           int64_t kp, int64_t cp, int Ge, int G,
+                                                           const double* __restrict__ X,
+                                                           const int32_t* __restrict__ E, OutT* __restrict__ D) {
+  const int64_t plane = rows * cols, pplane = kp * cp;
+  const int64_t K = axis == 0 ? cols : rows;
+  const int64_t Cn = axis == 0 ? rows : cols;
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * 64 + (threadIdx.x & 63);
+  if (c >= cp) return;
+  const int64_t cc = c < Cn ? c : 0;
+  const int e = E[cc];
+  for (int64_t kb = blockIdx.y; kb * 4 < kp; kb += gridDim.y) {
+    const int64_t kk = kb * 4 + (threadIdx.x >> 6);
+    OutT* out = D + kk * cp + c;
+    const bool valid = c < Cn && kk < K;
+    const int64_t kc = kk < K ? kk : 0;
+    double xs[ML];
+    load_limbs<ML>(X, plane, valid ? L : 0, axis == 0 ? cc * cols + kc : kc * cols + cc, xs);
+    int g = 0, cls = 0;
+    if (xs[0] != 0.0) {
+      const int fe = frexp_exp_or_min(xs[0]);
+      cls = (e - fe) / w;
+      cls = cls < Ge - 1 ? cls : Ge - 1;
+      g = (G > Ge && xs[0] < 0.0 ? Ge : 0) + cls;
+    }
+    uint64_t I[NW];
+    const bool neg = floor_on_grid<NW, ML>(xs, L, e - cls * w - w * S, I);
+    for (int h = 0; h < G; ++h) {
+      OutT* o = out + static_cast<int64_t>(h) * S * pplane;
+      if (h == g) {
+        store_digits<NW, OutT>(I, S, w, neg, o, pplane);
+      } else {
+        for (int q = 0; q < S; ++q) o[static_cast<int64_t>(q) * pplane] = OutT(0);
+      }
+    }
+  }
+}
+
 template <int NW, int ML>
 hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X, const int32_t* E,
                      void* D, bool panel, bool f32, const uint32_t* masks, int C, hipStream_t stream) {
@@ -304,6 +354,24 @@ hipError_t launch_split(int64_t rows, int64_t cols, int L, int S, int w, int axi
   if (L <= 4) return split_words<4>(words, rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
   if (L <= 8) return split_words<8>(words, rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
   return split_words<16>(words, rows, cols, L, S, w, axis, X, E, D, panel, f32, masks, C, stream);
+}
+
+hipError_t launch_split_groups(int64_t rows, int64_t cols, int L, int S, int w, int axis, const double* X,
+                               const int32_t* E, void* D, bool f32, int Ge, bool sign, hipStream_t stream) {
+  if (L < 1 || L > 4 || Ge < 1 || (w * S + 52 + 63) / 64 > kGroupSplitWords) return hipErrorInvalidValue;
+  if (rows == 0 || cols == 0) return hipSuccess;
+  const int G = (sign ? 2 : 1) * Ge;
+  const int64_t K = axis == 0 ? cols : rows, Cn = axis == 0 ? rows : cols;
+  const int64_t kp = f32 ? panel_k32(K) : panel_k(K), cp = panel_mn(Cn);
+  const int64_t nkb = kp / 4;
+  const dim3 grid(static_cast<unsigned>(cp / 64), static_cast<unsigned>(nkb < 65535 ? nkb : 65535));
+  if (f32)
+    hipLaunchKernelGGL((split_groups_kernel<kGroupSplitWords, 4, float>), grid, dim3(256), 0, stream, rows, cols, L, S,
+                       w, axis, kp, cp, Ge, G, X, E, static_cast<float*>(D));
+  else
+    hipLaunchKernelGGL((split_groups_kernel<kGroupSplitWords, 4, double>), grid, dim3(256), 0, stream, rows, cols, L,
+                       S, w, axis, kp, cp, Ge, G, X, E, static_cast<double*>(D));
+  return hipGetLastError();
 }
 
 hipError_t launch_split_int8(int64_t rows, int64_t cols, int L, int S, int w, const double* X, const int32_t* E,

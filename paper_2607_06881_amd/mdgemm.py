@@ -33,6 +33,8 @@ MDGEMM_KARATSUBA = 8
 MDGEMM_KARATSUBA_MIN_TERMS = 16
 MDGEMM_INT8 = 32
 MDGEMM_STAGED = 64
+MDGEMM_GROUP_SIGN = 128
+MDGEMM_GROUP_EXPONENT = 256
 MDGEMM_SCHEDULE_INFO = 12
 MDGEMM_LAYOUT_INFO = 12
 MDGEMM_NOALLOC_MAX_BYTES = 64 << 20

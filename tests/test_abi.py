@@ -336,6 +336,43 @@ def test_int8_plans_match_the_oracle_reading(lib):
     assert combos == 6 * 5 * 4 * 3 * 2
 
 
+def test_group_plans_match_the_oracle_reading(lib):
+    # exponent classes / sign groups: the library's option resolution against
+    # exact.plan's restatement, refusals included
+    GE, GS = md.MDGEMM_GROUP_EXPONENT, md.MDGEMM_GROUP_SIGN
+    assert md.mdgemm_plan(64, 64, 2048, 2, range_bits=60, flags=GE) == (13, 9, 9)  # 6 classes
+    assert md.mdgemm_plan(64, 64, 2048, 2, flags=GS) == (13, 8, 7)
+    combos = 0
+    for L in (1, 2, 3, 4, 8):
+        for k in (64, 2048):
+            for flags in (GE, GS, GE | GS):
+                for slice_bits in (0, 17, md.MDGEMM_SLICE_BITS_AUTO):
+                    for cutoff in (-1, -2, 5):
+                        for range_bits in (0, 13, 60):
+                            kw = dict(slice_bits=slice_bits, cutoff=cutoff, range_bits=range_bits)
+                            try:
+                                want = exact.plan(L, k, group_exponent=bool(flags & GE), group_sign=bool(flags & GS),
+                                                  **kw)
+                                err = None if want is not None else md.MDGEMM_EEXACT
+                            except ValueError:
+                                want, err = None, md.MDGEMM_EINVAL
+                            if err is None:
+                                assert md.mdgemm_plan(8, 8, k, L, flags=flags, **kw) == want, (L, k, flags, kw)
+                            else:
+                                with pytest.raises(md.MdgemmError) as ei:
+                                    md.mdgemm_plan(8, 8, k, L, flags=flags, **kw)
+                                assert ei.value.status == err, (L, k, flags, kw)
+                            combos += 1
+    assert combos == 5 * 2 * 3 * 3 * 3 * 3
+    for extra in (md.MDGEMM_INT8, md.MDGEMM_KARATSUBA):
+        with pytest.raises(md.MdgemmError):
+            md.mdgemm_plan(64, 64, 64, 2, flags=GS | extra)
+    # the staged workspace: G S panels per operand and T + 1 + 2 (Ge - 1) level planes
+    lay = md.mdgemm_workspace_layout(300, 270, 100, 2, range_bits=60, flags=GE | GS)
+    assert lay["planes"] == 9 + 1 + 2 * 5 and lay["panel_bytes"] == 4
+    assert (lay["db"] - lay["da"]) // (4 * lay["kp"] * lay["mp"]) == 12 * 9
+
+
 def test_range_balancing_plans(lib):
     # D = ceil(range / w) more digits, default cutoff S0 - 1 + 2D
     assert md.mdgemm_plan(64, 64, 2048, 2, range_bits=60) == (13, 13, 17)

@@ -664,6 +664,88 @@ def test_range_balancing_restores_the_tolerance():
             assert abs(exact.value(adaptive["C"][:, i, j]) - want) <= exact.tolerance(k, L, mag)
 
 
+# --------------------------------------------------------------------------
+# grouped products (section 3: by sign and by exponent class)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("L,m,k,n,seed", [(2, 7, 40, 6, 1), (3, 5, 17, 9, 2), (1, 4, 64, 4, 3)])
+def test_sign_groups_sum_to_the_ungrouped_levels(L, m, k, n, seed):
+    # A = A+ + A-, B = B+ + B-: the digits of the sign groups add up to the
+    # digits of the whole operand, so the four group products give the levels
+    # of the ungrouped product exactly (the int64 loops of the C oracle)
+    rng = np.random.default_rng(seed)
+    A = workloads.make_operand(rng, L, m, k, "normal", row_exp=6)
+    B = workloads.make_operand(rng, L, k, n, "normal", col_exp=6)
+    S = 4 * L
+    EA, EB = pipeline.exponents(A, B)
+    DA = pipeline.group_digits(A, EA, S, 0, 1, True)
+    DB = pipeline.group_digits(B, EB, S, 1, 1, True)
+    assert DA.shape == (2, S, m, k)
+    assert np.array_equal(DA[0] + DA[1], coracle.split(A, EA.astype(np.int32), S, 0))
+    assert not (DA[0] < 0).any() and not (DA[1] > 0).any()
+    G = pipeline.group_levels(DA, DB, S - 1, 1)
+    want = coracle.levels(coracle.split(A, EA.astype(np.int32), S, 0), coracle.split(B, EB.astype(np.int32), S, 1),
+                          S - 1)
+    assert np.array_equal(G.astype(np.int64), want)
+
+
+@pytest.mark.parametrize("L,S", [(1, 6), (2, 10)])
+def test_exponent_classes_are_exact_when_the_digits_cover_every_element(L, S):
+    # Elements spread over 39 bits below their line's exponent, 4 classes of 13
+    # bits: on its class grid every element has its leading bit within one digit
+    # of the top, so S digits of 13 bits hold it exactly (53 L bits + 13), and
+    # with every pair kept the grouped product is the exact product, rounded
+    # greedily.  A class offset one digit off changes the value.
+    rng = np.random.default_rng(L)
+    m, k, n = 4, 12, 3
+    A = workloads.make_operand(rng, L, m, k, "uniform")
+    B = workloads.make_operand(rng, L, k, n, "uniform")
+    A *= np.ldexp(1.0, -rng.integers(0, 40, (m, k)))[None]
+    B *= np.ldexp(1.0, -rng.integers(0, 40, (k, n)))[None]
+    classes, T = 4, 2 * S - 2
+    C = pipeline.full_reference_groups(A, B, S, T, classes, False)
+    EA, EB = pipeline.exponents(A, B)
+    grp = pipeline.element_groups(A[0], EA, 0, classes, False)
+    assert set(np.unique(grp)) >= {0, 1, 2}  # several classes in use
+    for i in range(m):
+        for j in range(n):
+            want, _ = exact.exact_product(A, B, i, j)
+            assert C[:, i, j].tolist() == exact.round_to_limbs(want, L), (i, j)
+    # planted mistake: the levels of every group pair one level too low
+    DA = pipeline.group_digits(A, EA, S, 0, classes, False)
+    DB = pipeline.group_digits(B, EB, S, 1, classes, False)
+    good = pipeline.group_levels(DA, DB, T, classes)
+    bad = np.zeros_like(good)
+    for g in range(classes):
+        for h in range(classes):
+            for t in range(T + 1):
+                for p, q in exact.pairs_of_level(t, S):
+                    bad[min(t + g + h + 1, bad.shape[0] - 1)] += DA[g][p] @ DB[h][q]
+    z_good = exact.accumulate([int(good[t, 0, 0]) for t in range(good.shape[0])], int(EA[0]), int(EB[0]))
+    z_bad = exact.accumulate([int(bad[t, 0, 0]) for t in range(bad.shape[0])], int(EA[0]), int(EB[0]))
+    assert z_good == exact.exact_product(A, B, 0, 0)[0] and z_bad != z_good
+
+
+def test_exponent_classes_restore_the_tolerance():
+    # workload c7's recipe, small: the shared grid misses the tolerance by far,
+    # exponent classes over the 60 bits meet it (as range balancing does)
+    w = workloads.WORKLOADS["c7"]
+    A, B = workloads.make_workload(w, m=3, n=3, k=48, seed=3)
+    L, k = 2, 48
+    wg, Sg, Tg = exact.plan(L, k, range_bits=60, group_exponent=True)
+    assert (wg, Sg, Tg) == (13, 9, 9)
+    classes = 1 + -(-60 // 13)
+    C = pipeline.full_reference_groups(A, B, Sg, Tg, classes, False)
+    Cs = pipeline.full_reference_groups(A, B, Sg, Tg, classes, True)  # with sign groups too: the same limbs
+    assert np.array_equal(C, Cs)
+    for i in range(3):
+        for j in range(3):
+            want, mag = exact.exact_product(A, B, i, j)
+            assert abs(exact.value(C[:, i, j]) - want) <= exact.tolerance(k, L, mag)
+    ref = pipeline.reference_entries_groups(A, B, Sg, Tg, classes, False, [(0, 0), (2, 1)])
+    assert ref[(0, 0)]["limbs"] == C[:, 0, 0].tolist() and ref[(2, 1)]["limbs"] == C[:, 2, 1].tolist()
+
+
 def test_method_bound_catches_a_dropped_kept_pair():
     # Planted in the oracle's chain: leave out pair (0, T) of the last kept level.
     L, S, T, k = 8, 32, 31, 16
