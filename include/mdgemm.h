@@ -431,6 +431,29 @@ int mdgemm_accumulate(int64_t m, int64_t n, int levels, int slice_bits, const do
 int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, int slice_bits, const double* G,
                         const int32_t* EA, const int32_t* EB, double* C, void* stream);
 
+/* ---- application: blocked Householder QR in double-double --------------------
+ * The downstream use the paper names as future work (section 5): A = Q R for a
+ * double-double matrix, with the trailing updates of each panel on mdgemm_ex. */
+
+/* Workspace bytes of mdgemm_qr_dd (SIZE_MAX for invalid arguments: m >= n >= 1,
+ * nb in 1..32, m and n at most 2^20). */
+size_t mdgemm_qr_dd_workspace_bytes(int64_t m, int64_t n, int nb);
+
+/* Householder QR of A [2][m][n] (double-double, limb-major, m >= n), in place:
+ * A = Q R with Q = H_0 ... H_{n-1}, H_j = I - tau_j v_j v_j^T, v_j(j) = 1 and
+ * v_j zero above row j.  On return A holds R on and above the diagonal (R(j, j)
+ * >= 0) and v_j below it (LAPACK's convention), tau [2][n] the tau_j (all in
+ * double-double).  Panels of nb columns (1..32) are factored by one workgroup in
+ * double-double arithmetic (Golub and Van Loan's Householder vector); each
+ * panel's reflections are accumulated as I - V T V^T (T upper triangular) and
+ * the columns to its right updated as A2 - V (T^T (V^T A2)), three products on
+ * mdgemm_ex with the default options.  workspace: caller-owned device buffer of
+ * mdgemm_qr_dd_workspace_bytes() bytes, not overlapping A or tau.  Stream
+ * ordered; returns MDGEMM_OK, MDGEMM_EINVAL, MDGEMM_EWORKSPACE or a status of
+ * mdgemm_ex.  Inputs must be finite and normalized double-doubles. */
+int mdgemm_qr_dd(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspace, size_t workspace_bytes,
+                 void* stream);
+
 /* ---- calibration (measurement aids, not part of the product) ---------------
  * The rates the stages are measured against, on the caller's device. */
 

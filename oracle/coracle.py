@@ -47,6 +47,10 @@ def lib():
         L.oracle_levels.argtypes = [_i64, _i64, _i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _dp, _dp, _lp]
         L.oracle_levels.restype = ctypes.c_int
         L.oracle_num_threads.restype = ctypes.c_int
+        L.oracle_qr_dd.argtypes = [_i64, _i64, _dp, _dp]
+        L.oracle_qr_dd.restype = ctypes.c_int
+        L.oracle_qr_dd_check.argtypes = [_i64, _i64, _dp, _dp, _dp, _dp, _dp]
+        L.oracle_qr_dd_check.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -162,3 +166,29 @@ def levels(DA, DB, T, per_pair=False):
 
 def num_threads() -> int:
     return lib().oracle_num_threads()
+
+
+def qr_dd(A):
+    """Householder QR of a double-double matrix A [2][m][n] (m >= n) in classic
+    double-double arithmetic: (QR [2][m][n] with R on and above the diagonal and
+    the vectors below, tau [2][n])."""
+    QR = np.array(A, dtype=np.float64, order="C", copy=True)
+    _, m, n = QR.shape
+    tau = np.zeros((2, n), dtype=np.float64)
+    st = lib().oracle_qr_dd(m, n, _d(QR), _d(tau))
+    if st:
+        raise ValueError(f"oracle_qr_dd failed: {st}")
+    return QR, tau
+
+
+def qr_dd_check(A0, QR, tau):
+    """(max |A0 - Q R| / max |A0|, max |Q^T Q - I|, Q [2][m][n]) of a factorization
+    stored as qr_dd leaves it, every entry formed in double-double."""
+    A0, QR, tau = _f64(A0), _f64(QR), _f64(tau)
+    _, m, n = A0.shape
+    out = np.zeros(2, dtype=np.float64)
+    Q = np.zeros((2, m, n), dtype=np.float64)
+    st = lib().oracle_qr_dd_check(m, n, _d(A0), _d(QR), _d(tau), _d(out), _d(Q))
+    if st:
+        raise ValueError(f"oracle_qr_dd_check failed: {st}")
+    return float(out[0]), float(out[1]), Q

@@ -495,3 +495,214 @@ int oracle_num_threads(void) {
   return 1;
 #endif
 }
+
+/* ------------------------------------------------------------------------- */
+/* 5. Householder QR in double-double arithmetic (the downstream application  */
+/*    of multiple-double products that the paper names as future work)        */
+/* ------------------------------------------------------------------------- */
+
+/* Double-double quotient by long division (Hida, Li and Bailey): q1 = a0 / b0,
+ * the remainder a - q1 b in double-double, q2 and q3 from the next remainders. */
+static void dd_mul_d(const double* a, double b, double* r) {
+  double p1, p2;
+  two_prod(a[0], b, &p1, &p2);
+  p2 += a[1] * b;
+  fast_two_sum(p1, p2, &r[0], &r[1]);
+}
+
+static void dd_sub(const double* a, const double* b, double* r) {
+  double nb[2] = {-b[0], -b[1]};
+  dd_add(a, nb, r);
+}
+
+static void dd_div(const double* a, const double* b, double* q) {
+  double t[2], r[2], r2[2];
+  double q1 = a[0] / b[0];
+  dd_mul_d(b, q1, t);
+  dd_sub(a, t, r);
+  double q2 = r[0] / b[0];
+  dd_mul_d(b, q2, t);
+  dd_sub(r, t, r2);
+  double q3 = r2[0] / b[0];
+  double s[2], e3[2] = {q3, 0.0};
+  fast_two_sum(q1, q2, &s[0], &s[1]);
+  dd_add(s, e3, q);
+}
+
+/* Double-double square root by one Newton step on the double root (Karp):
+ * x = 1/sqrt(a0), y = a0 x, sqrt(a) = y + x (a - y^2) / 2. */
+static void dd_sqrt(const double* a, double* r) {
+  if (a[0] <= 0.0) {
+    r[0] = r[1] = 0.0;
+    return;
+  }
+  double x = 1.0 / sqrt(a[0]);
+  double y = a[0] * x;
+  double y2[2], d[2];
+  two_prod(y, y, &y2[0], &y2[1]);
+  dd_sub(a, y2, d);
+  two_sum(y, d[0] * x * 0.5, &r[0], &r[1]);
+}
+
+/* A = Q R for A [2][m][n] (double-double, m >= n), unblocked: for each column j
+ * the Householder vector of x = A(j:m, j) after Golub and Van Loan (v_1 without
+ * cancellation, R(j, j) = ||x|| >= 0), then H_j applied to the columns right of
+ * j, each by w = v^T a, a <- a - tau w v.  On return A holds R on and above the
+ * diagonal and v (v_1 = 1 implicit) below it; tau [2][n]. */
+int oracle_qr_dd(int64_t m, int64_t n, double* A, double* tau) {
+  if (m < 1 || n < 1 || m < n) return ORACLE_EINVAL;
+  const int64_t P = m * n;
+#define AT(r, c, l) A[(l) * P + (r) * n + (c)]
+  for (int64_t j = 0; j < n; ++j) {
+    double sigma[2] = {0.0, 0.0}, t[2];
+    for (int64_t r = j + 1; r < m; ++r) {
+      double a[2] = {AT(r, j, 0), AT(r, j, 1)};
+      dd_mul(a, a, t);
+      dd_add(sigma, t, sigma);
+    }
+    double x1[2] = {AT(j, j, 0), AT(j, j, 1)}, tj[2], diag[2];
+    int mode;
+    double v1[2] = {1.0, 0.0};
+    if (sigma[0] == 0.0) {
+      mode = x1[0] < 0.0 ? 1 : 0;
+      tj[0] = mode ? 2.0 : 0.0;
+      tj[1] = 0.0;
+      diag[0] = mode ? -x1[0] : x1[0];
+      diag[1] = mode ? -x1[1] : x1[1];
+    } else {
+      double s2[2], mu[2], v1sq[2], num[2], den[2];
+      dd_mul(x1, x1, s2);
+      dd_add(s2, sigma, s2);
+      dd_sqrt(s2, mu);
+      if (x1[0] <= 0.0) {
+        dd_sub(x1, mu, v1);
+      } else {
+        double xs[2], q[2];
+        dd_add(x1, mu, xs);
+        dd_div(sigma, xs, q);
+        v1[0] = -q[0];
+        v1[1] = -q[1];
+      }
+      dd_mul(v1, v1, v1sq);
+      dd_mul_d(v1sq, 2.0, num);
+      dd_add(sigma, v1sq, den);
+      dd_div(num, den, tj);
+      diag[0] = mu[0];
+      diag[1] = mu[1];
+      mode = 2;
+    }
+    AT(j, j, 0) = diag[0];
+    AT(j, j, 1) = diag[1];
+    tau[j] = tj[0];
+    tau[n + j] = tj[1];
+    if (mode == 2)
+      for (int64_t r = j + 1; r < m; ++r) {
+        double a[2] = {AT(r, j, 0), AT(r, j, 1)}, q[2];
+        dd_div(a, v1, q);
+        AT(r, j, 0) = q[0];
+        AT(r, j, 1) = q[1];
+      }
+    if (mode == 0) continue;
+    for (int64_t c = j + 1; c < n; ++c) {
+      double w[2] = {AT(j, c, 0), AT(j, c, 1)};
+      if (mode == 2)
+        for (int64_t r = j + 1; r < m; ++r) {
+          double v[2] = {AT(r, j, 0), AT(r, j, 1)}, a[2] = {AT(r, c, 0), AT(r, c, 1)};
+          dd_mul(v, a, t);
+          dd_add(w, t, w);
+        }
+      double tw[2], a0[2] = {AT(j, c, 0), AT(j, c, 1)};
+      dd_mul(tj, w, tw);
+      dd_sub(a0, tw, a0);
+      AT(j, c, 0) = a0[0];
+      AT(j, c, 1) = a0[1];
+      if (mode == 2)
+        for (int64_t r = j + 1; r < m; ++r) {
+          double v[2] = {AT(r, j, 0), AT(r, j, 1)}, a[2] = {AT(r, c, 0), AT(r, c, 1)};
+          dd_mul(tw, v, t);
+          dd_sub(a, t, a);
+          AT(r, c, 0) = a[0];
+          AT(r, c, 1) = a[1];
+        }
+    }
+  }
+#undef AT
+  return ORACLE_OK;
+}
+
+/* Check a factorization in double-double arithmetic: QR [2][m][n] holds R and
+ * the vectors as oracle_qr_dd leaves them, tau [2][n].  Forms the thin Q (m x n:
+ * the reflections applied, last to first, to the first n columns of I), then
+ * out[0] = max |A0 - Q R| / max |A0| and out[1] = max |Q^T Q - I|, each entry
+ * formed in double-double.  Q [2][m][n] is returned as well (may be NULL). */
+int oracle_qr_dd_check(int64_t m, int64_t n, const double* A0, const double* QR, const double* tau, double* out,
+                       double* Qout) {
+  if (m < 1 || n < 1 || m < n) return ORACLE_EINVAL;
+  const int64_t P = m * n;
+  double* Q = (double*)malloc(sizeof(double) * 2 * (size_t)P);
+  if (!Q) return ORACLE_EINVAL;
+#define QV(r, c, l) QR[(l) * P + (r) * n + (c)]
+#define QQ(r, c, l) Q[(l) * P + (r) * n + (c)]
+  for (int64_t r = 0; r < m; ++r)
+    for (int64_t c = 0; c < n; ++c) {
+      QQ(r, c, 0) = r == c ? 1.0 : 0.0;
+      QQ(r, c, 1) = 0.0;
+    }
+  for (int64_t j = n - 1; j >= 0; --j) {
+    double tj[2] = {tau[j], tau[n + j]}, t[2];
+    if (tj[0] == 0.0) continue;
+    for (int64_t c = 0; c < n; ++c) {
+      double w[2] = {QQ(j, c, 0), QQ(j, c, 1)};
+      for (int64_t r = j + 1; r < m; ++r) {
+        double v[2] = {QV(r, j, 0), QV(r, j, 1)}, q[2] = {QQ(r, c, 0), QQ(r, c, 1)};
+        dd_mul(v, q, t);
+        dd_add(w, t, w);
+      }
+      double tw[2], q0[2] = {QQ(j, c, 0), QQ(j, c, 1)};
+      dd_mul(tj, w, tw);
+      dd_sub(q0, tw, q0);
+      QQ(j, c, 0) = q0[0];
+      QQ(j, c, 1) = q0[1];
+      for (int64_t r = j + 1; r < m; ++r) {
+        double v[2] = {QV(r, j, 0), QV(r, j, 1)}, q[2] = {QQ(r, c, 0), QQ(r, c, 1)};
+        dd_mul(tw, v, t);
+        dd_sub(q, t, q);
+        QQ(r, c, 0) = q[0];
+        QQ(r, c, 1) = q[1];
+      }
+    }
+  }
+  double amax = 0.0, res = 0.0, orth = 0.0;
+  for (int64_t e = 0; e < P; ++e) amax = fmax(amax, fabs(A0[e]));
+#pragma omp parallel for reduction(max : res) schedule(static)
+  for (int64_t r = 0; r < m; ++r)
+    for (int64_t c = 0; c < n; ++c) {
+      double s[2] = {0.0, 0.0}, t[2];
+      for (int64_t l = 0; l <= c; ++l) {
+        double q[2] = {QQ(r, l, 0), QQ(r, l, 1)}, rr[2] = {QV(l, c, 0), QV(l, c, 1)};
+        dd_mul(q, rr, t);
+        dd_add(s, t, s);
+      }
+      double a[2] = {A0[r * n + c], A0[P + r * n + c]}, d[2];
+      dd_sub(a, s, d);
+      res = fmax(res, fabs(d[0]));
+    }
+#pragma omp parallel for reduction(max : orth) schedule(static)
+  for (int64_t i = 0; i < n; ++i)
+    for (int64_t c = 0; c < n; ++c) {
+      double s[2] = {i == c ? -1.0 : 0.0, 0.0}, t[2];
+      for (int64_t r = 0; r < m; ++r) {
+        double a[2] = {QQ(r, i, 0), QQ(r, i, 1)}, b[2] = {QQ(r, c, 0), QQ(r, c, 1)};
+        dd_mul(a, b, t);
+        dd_add(s, t, s);
+      }
+      orth = fmax(orth, fabs(s[0]));
+    }
+#undef QV
+#undef QQ
+  out[0] = amax > 0.0 ? res / amax : res;
+  out[1] = orth;
+  if (Qout) memcpy(Qout, Q, sizeof(double) * 2 * (size_t)P);
+  free(Q);
+  return ORACLE_OK;
+}

@@ -1,0 +1,316 @@
+// Blocked Householder QR of a double-double matrix: the downstream
+// application the paper names as future work (section 5), with its trailing
+// updates on the multiple-double product of this library.
+//
+// A [2][m][n] (limb-major double-double, m >= n) is factored as A = Q R with
+// Q = H_0 H_1 ... H_{n-1}, H_j = I - tau_j v_j v_j^T (Householder reflections,
+// v_j(j) = 1, v_j zero above row j).  Panels of nb <= 32 columns are factored by
+// one workgroup in double-double arithmetic (dd.h); the panel's reflections are
+// accumulated in the compact form I - V T V^T (T upper triangular, the forward
+// recurrence of Schreiber and Van Loan), and the trailing columns are updated as
+//     A2 <- A2 - V (T^T (V^T A2))
+// with three products on mdgemm_ex (double-double in, double-double out).  On
+// return A holds R on and above the diagonal and the vectors v_j below it
+// (LAPACK's convention), tau the scalars tau_j.
+//
+// Householder vector of x = A(j:m, j) (Golub and Van Loan, the algorithm that
+// keeps v_1 free of cancellation): sigma = x(2:)^T x(2:), mu = sqrt(x_1^2 +
+// sigma); v_1 = x_1 - mu if x_1 <= 0, else -sigma / (x_1 + mu); tau = 2 v_1^2 /
+// (sigma + v_1^2); v = x / v_1; then H x = mu e_1, so the diagonal of R is
+// nonnegative.  sigma = 0: tau = 0 (x_1 >= 0) or tau = 2 with v = e_1 (x_1 < 0).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+
+#include "dd.h"
+#include "internal.h"
+#include "mdgemm.h"
+
+namespace mdg {
+namespace {
+
+constexpr int kPanelThreads = 1024;
+constexpr int kMaxNb = 32;
+
+__device__ inline dd ldd(const double* P, int64_t plane, int64_t idx) { return {P[idx], P[plane + idx]}; }
+__device__ inline void std_(double* P, int64_t plane, int64_t idx, dd v) {
+  P[idx] = v.hi;
+  P[plane + idx] = v.lo;
+}
+
+// Sum of one dd per thread over the workgroup (tree in LDS); the result in red[0].
+__device__ inline dd block_sum(dd v, dd* red) {
+  const int tid = threadIdx.x;
+  red[tid] = v;
+  __syncthreads();
+  for (int s = kPanelThreads / 2; s > 0; s >>= 1) {
+    if (tid < s) red[tid] = dd_add(red[tid], red[tid + s]);
+    __syncthreads();
+  }
+  const dd r = red[0];
+  __syncthreads();
+  return r;
+}
+
+// Factor the panel A(j0:m, j0:j0+jb) in place.  Thread layout for the updates:
+// column cc = tid % 32 of the remaining panel columns, row group rg = tid / 32.
+__global__ void __launch_bounds__(kPanelThreads) qr_panel_kernel(int64_t m, int64_t n, int64_t j0, int jb,
+                                                                 double* __restrict__ A, double* __restrict__ tau) {
+  __shared__ dd red[kPanelThreads];
+  __shared__ dd wv[kMaxNb];
+  __shared__ dd s_scale, s_tau;
+  __shared__ int s_mode;  // 0: H = I, 1: v = e_1 (tau = 2), 2: general
+  const int64_t plane = m * n;
+  const int tid = threadIdx.x, cc = tid & 31, rg = tid >> 5;
+  for (int j = 0; j < jb; ++j) {
+    const int64_t r0 = j0 + j, cj = j0 + j;
+    // sigma = sum of squares below the pivot
+    dd part = {0.0, 0.0};
+    for (int64_t r = r0 + 1 + tid; r < m; r += kPanelThreads) {
+      const dd a = ldd(A, plane, r * n + cj);
+      part = dd_add(part, dd_mul(a, a));
+    }
+    const dd sigma = block_sum(part, red);
+    if (tid == 0) {
+      const dd x1 = ldd(A, plane, r0 * n + cj);
+      dd diag;
+      if (sigma.hi == 0.0) {
+        s_mode = x1.hi < 0.0 ? 1 : 0;
+        s_tau = s_mode ? dd{2.0, 0.0} : dd{0.0, 0.0};
+        diag = s_mode ? dd_neg(x1) : x1;
+      } else {
+        const dd mu = dd_sqrt(dd_add(dd_mul(x1, x1), sigma));
+        const dd v1 = x1.hi <= 0.0 ? dd_sub(x1, mu) : dd_neg(dd_div(sigma, dd_add(x1, mu)));
+        const dd v1sq = dd_mul(v1, v1);
+        s_tau = dd_div(dd_mul_d(v1sq, 2.0), dd_add(sigma, v1sq));
+        s_scale = v1;
+        s_mode = 2;
+        diag = mu;
+      }
+      std_(A, plane, r0 * n + cj, diag);
+      std_(tau, n, cj, s_tau);
+    }
+    __syncthreads();
+    const int mode = s_mode;
+    if (mode == 2) {
+      const dd v1 = s_scale;
+      for (int64_t r = r0 + 1 + tid; r < m; r += kPanelThreads)
+        std_(A, plane, r * n + cj, dd_div(ldd(A, plane, r * n + cj), v1));
+    }
+    __syncthreads();
+    if (mode == 0) continue;  // H_j = I
+    const dd t = s_tau;
+    // w_c = v^T a_c for the remaining columns c = j + 1 + cc (v(r0) = 1)
+    const int c = j + 1 + cc;
+    dd acc = {0.0, 0.0};
+    if (c < jb && mode == 2) {
+      for (int64_t r = r0 + 1 + rg; r < m; r += 32)
+        acc = dd_add(acc, dd_mul(ldd(A, plane, r * n + cj), ldd(A, plane, r * n + j0 + c)));
+    }
+    red[tid] = acc;
+    __syncthreads();
+    if (rg == 0 && c < jb) {
+      dd w = ldd(A, plane, r0 * n + j0 + c);
+      for (int g = 0; g < 32; ++g) w = dd_add(w, red[g * 32 + cc]);
+      wv[cc] = dd_mul(t, w);
+    }
+    __syncthreads();
+    // a_c <- a_c - tau w_c v
+    if (c < jb) {
+      const dd tw = wv[cc];
+      if (rg == 0) std_(A, plane, r0 * n + j0 + c, dd_sub(ldd(A, plane, r0 * n + j0 + c), tw));
+      if (mode == 2) {
+        for (int64_t r = r0 + 1 + rg; r < m; r += 32) {
+          const int64_t idx = r * n + j0 + c;
+          std_(A, plane, idx, dd_sub(ldd(A, plane, idx), dd_mul(tw, ldd(A, plane, r * n + cj))));
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// V (mp x jb, dense: 1 on the diagonal, the stored vectors below, 0 above) and
+// its transpose Vt (jb x mp), from the factored panel; rows of the panel start
+// at row j0 of A.
+__global__ void __launch_bounds__(256) qr_pack_v_kernel(int64_t m, int64_t n, int64_t j0, int jb,
+                                                        const double* __restrict__ A, double* __restrict__ V,
+                                                        double* __restrict__ Vt) {
+  const int64_t mp = m - j0, planeA = m * n, planeV = mp * jb;
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= planeV) return;
+  const int64_t i = e / jb;
+  const int c = static_cast<int>(e - i * jb);
+  dd v = {0.0, 0.0};
+  if (i == c) v = {1.0, 0.0};
+  else if (i > c) v = ldd(A, planeA, (j0 + i) * n + j0 + c);
+  std_(V, planeV, i * jb + c, v);
+  std_(Vt, planeV, static_cast<int64_t>(c) * mp + i, v);
+}
+
+// T (upper triangular, jb x jb) of I - V T V^T = H_0 ... H_{jb-1} from
+// G = V^T V and tau: T(j, j) = tau_j, T(0:j, j) = -tau_j T(0:j, 0:j) G(0:j, j);
+// writes the transpose Tt.  One wave, serial in j.
+__global__ void __launch_bounds__(64) qr_t_kernel(int jb, int64_t n, int64_t j0, const double* __restrict__ G,
+                                                  const double* __restrict__ tau, double* __restrict__ Tt) {
+  __shared__ dd T[kMaxNb][kMaxNb];
+  const int i = threadIdx.x;
+  const int64_t pg = static_cast<int64_t>(jb) * jb;
+  if (i < kMaxNb)
+    for (int c = 0; c < kMaxNb; ++c) T[i][c] = {0.0, 0.0};
+  __syncthreads();
+  for (int j = 0; j < jb; ++j) {
+    const dd tj = ldd(tau, n, j0 + j);
+    dd s = {0.0, 0.0};
+    if (i < j) {
+      for (int l = i; l < j; ++l) s = dd_add(s, dd_mul(T[i][l], ldd(G, pg, static_cast<int64_t>(l) * jb + j)));
+    }
+    __syncthreads();
+    if (i < j) T[i][j] = dd_neg(dd_mul(tj, s));
+    if (i == j) T[j][j] = tj;
+    __syncthreads();
+  }
+  if (i < jb)
+    for (int c = 0; c < jb; ++c) std_(Tt, pg, static_cast<int64_t>(c) * jb + i, T[i][c]);
+}
+
+// Copy the trailing block A(j0:m, c0:n) into a contiguous [2][mp][nc] array.
+__global__ void __launch_bounds__(256) qr_pack_block_kernel(int64_t m, int64_t n, int64_t j0, int64_t c0,
+                                                            const double* __restrict__ A, double* __restrict__ X) {
+  const int64_t mp = m - j0, nc = n - c0, planeX = mp * nc;
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= planeX) return;
+  const int64_t i = e / nc, c = e - i * nc;
+  std_(X, planeX, e, ldd(A, m * n, (j0 + i) * n + c0 + c));
+}
+
+// A(j0:m, c0:n) <- X - P (double-double difference).
+__global__ void __launch_bounds__(256) qr_update_kernel(int64_t m, int64_t n, int64_t j0, int64_t c0,
+                                                        const double* __restrict__ X, const double* __restrict__ P,
+                                                        double* __restrict__ A) {
+  const int64_t mp = m - j0, nc = n - c0, planeX = mp * nc;
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= planeX) return;
+  const int64_t i = e / nc, c = e - i * nc;
+  std_(A, m * n, (j0 + i) * n + c0 + c, dd_sub(ldd(X, planeX, e), ldd(P, planeX, e)));
+}
+
+inline unsigned blocks_for(int64_t count) { return static_cast<unsigned>((count + 255) / 256); }
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// Workspace parts of the QR: V, Vt, G (V^T V), Tt, X (trailing block), W, W2, P,
+// then the workspace of the largest mdgemm_ex call.
+struct QrLayout {
+  size_t v = 0, vt = 0, g = 0, tt = 0, x = 0, w = 0, w2 = 0, p = 0, gemm = 0, gemm_bytes = 0, total = 0;
+};
+
+bool qr_layout(int64_t m, int64_t n, int nb, QrLayout* L) {
+  const size_t dd_bytes = 2 * sizeof(double);
+  const size_t vbytes = align256(dd_bytes * static_cast<size_t>(m) * nb);
+  const size_t xbytes = align256(dd_bytes * static_cast<size_t>(m) * static_cast<size_t>(n));
+  const size_t wbytes = align256(dd_bytes * static_cast<size_t>(nb) * static_cast<size_t>(n));
+  const size_t gbytes = align256(dd_bytes * nb * nb);
+  size_t off = 0;
+  L->v = off;
+  off += vbytes;
+  L->vt = off;
+  off += vbytes;
+  L->g = off;
+  off += gbytes;
+  L->tt = off;
+  off += gbytes;
+  L->x = off;
+  off += xbytes;
+  L->w = off;
+  off += wbytes;
+  L->w2 = off;
+  off += wbytes;
+  L->p = off;
+  off += xbytes;
+  // the largest workspace of the four products of any panel: V^T V, V^T X, T^T W, V W2
+  size_t need = 0;
+  for (int64_t j0 = 0; j0 < n; j0 += nb) {
+    const int64_t jb = std::min<int64_t>(nb, n - j0), mp = m - j0, nc = n - j0 - jb;
+    const size_t c[4] = {mdgemm_workspace_bytes(jb, jb, mp, 2, nullptr),
+                         nc ? mdgemm_workspace_bytes(jb, nc, mp, 2, nullptr) : 0,
+                         nc ? mdgemm_workspace_bytes(jb, nc, jb, 2, nullptr) : 0,
+                         nc ? mdgemm_workspace_bytes(mp, nc, jb, 2, nullptr) : 0};
+    for (size_t x : c) {
+      if (x == SIZE_MAX) return false;
+      need = std::max(need, x);
+    }
+  }
+  L->gemm = off;
+  L->gemm_bytes = std::max<size_t>(need, 256);
+  off += align256(L->gemm_bytes);
+  L->total = off;
+  return true;
+}
+
+}  // namespace
+}  // namespace mdg
+
+extern "C" {
+
+size_t mdgemm_qr_dd_workspace_bytes(int64_t m, int64_t n, int nb) {
+  if (m < 1 || n < 1 || m < n || nb < 1 || nb > mdg::kMaxNb || m > (int64_t{1} << 20) || n > (int64_t{1} << 20))
+    return SIZE_MAX;
+  mdg::QrLayout L;
+  return mdg::qr_layout(m, n, nb, &L) ? L.total : SIZE_MAX;
+}
+
+int mdgemm_qr_dd(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspace, size_t workspace_bytes,
+                 void* stream) {
+  if (m < 1 || n < 1 || m < n || nb < 1 || nb > mdg::kMaxNb || !A || !tau || !workspace) return MDGEMM_EINVAL;
+  if (m > (int64_t{1} << 20) || n > (int64_t{1} << 20)) return MDGEMM_EINVAL;
+  mdg::QrLayout L;
+  if (!mdg::qr_layout(m, n, nb, &L)) return MDGEMM_EINVAL;
+  if (workspace_bytes < L.total) return MDGEMM_EWORKSPACE;
+  const uintptr_t w0 = reinterpret_cast<uintptr_t>(workspace), a0 = reinterpret_cast<uintptr_t>(A),
+                  t0 = reinterpret_cast<uintptr_t>(tau);
+  const uintptr_t abytes = sizeof(double) * 2 * static_cast<uintptr_t>(m) * n, tbytes = sizeof(double) * 2 * n;
+  if ((w0 < a0 + abytes && a0 < w0 + L.total) || (w0 < t0 + tbytes && t0 < w0 + L.total) ||
+      (a0 < t0 + tbytes && t0 < a0 + abytes))
+    return MDGEMM_EINVAL;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  double* V = reinterpret_cast<double*>(ws + L.v);
+  double* Vt = reinterpret_cast<double*>(ws + L.vt);
+  double* G = reinterpret_cast<double*>(ws + L.g);
+  double* Tt = reinterpret_cast<double*>(ws + L.tt);
+  double* X = reinterpret_cast<double*>(ws + L.x);
+  double* W = reinterpret_cast<double*>(ws + L.w);
+  double* W2 = reinterpret_cast<double*>(ws + L.w2);
+  double* P = reinterpret_cast<double*>(ws + L.p);
+  mdgemm_opts o;
+  mdgemm_opts_init(&o);
+  o.stream = stream;
+  o.workspace = ws + L.gemm;
+  o.workspace_bytes = L.gemm_bytes;
+  for (int64_t j0 = 0; j0 < n; j0 += nb) {
+    const int jb = static_cast<int>(std::min<int64_t>(nb, n - j0));
+    const int64_t mp = m - j0, c0 = j0 + jb, nc = n - c0;
+    hipLaunchKernelGGL(mdg::qr_panel_kernel, dim3(1), dim3(mdg::kPanelThreads), 0, s, m, n, j0, jb, A, tau);
+    if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
+    if (nc == 0) break;
+    hipLaunchKernelGGL(mdg::qr_pack_v_kernel, dim3(mdg::blocks_for(mp * jb)), dim3(256), 0, s, m, n, j0, jb, A, V,
+                       Vt);
+    hipLaunchKernelGGL(mdg::qr_pack_block_kernel, dim3(mdg::blocks_for(mp * nc)), dim3(256), 0, s, m, n, j0, c0, A,
+                       X);
+    if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
+    int st = mdgemm_ex(jb, jb, mp, 2, Vt, V, G, &o);  // G = V^T V
+    if (st != MDGEMM_OK) return st;
+    hipLaunchKernelGGL(mdg::qr_t_kernel, dim3(1), dim3(64), 0, s, jb, n, j0, G, tau, Tt);
+    if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
+    if ((st = mdgemm_ex(jb, nc, mp, 2, Vt, X, W, &o)) != MDGEMM_OK) return st;   // W = V^T X
+    if ((st = mdgemm_ex(jb, nc, jb, 2, Tt, W, W2, &o)) != MDGEMM_OK) return st;  // W2 = T^T W
+    if ((st = mdgemm_ex(mp, nc, jb, 2, V, W2, P, &o)) != MDGEMM_OK) return st;   // P = V W2
+    hipLaunchKernelGGL(mdg::qr_update_kernel, dim3(mdg::blocks_for(mp * nc)), dim3(256), 0, s, m, n, j0, c0, X, P, A);
+    if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
+  }
+  return MDGEMM_OK;
+}
+
+}  // extern "C"

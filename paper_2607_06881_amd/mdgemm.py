@@ -87,6 +87,8 @@ EXPORTED = (
     "mdgemm_schedule_export",
     "mdgemm_schedule_workspace_bytes",
     "mdgemm_schedule_levels",
+    "mdgemm_qr_dd_workspace_bytes",
+    "mdgemm_qr_dd",
     "mdgemm_probe_mfma_f64",
     "mdgemm_probe_copy",
 )
@@ -172,6 +174,10 @@ def lib() -> ctypes.CDLL:
         L.mdgemm_schedule_levels.argtypes = [_i64, _i64, _i64, _c, _c, _c, _u, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                              _vp]
         L.mdgemm_schedule_levels.restype = ctypes.c_int
+        L.mdgemm_qr_dd_workspace_bytes.argtypes = [_i64, _i64, ctypes.c_int]
+        L.mdgemm_qr_dd_workspace_bytes.restype = ctypes.c_size_t
+        L.mdgemm_qr_dd.argtypes = [_i64, _i64, ctypes.c_int, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+        L.mdgemm_qr_dd.restype = ctypes.c_int
         L.mdgemm_probe_mfma_f64.argtypes = [_i64, _i64, _vp, _vp]
         L.mdgemm_probe_mfma_f64.restype = ctypes.c_int64
         L.mdgemm_probe_copy.argtypes = [_vp, _vp, _i64, _vp]
@@ -561,3 +567,22 @@ def mdgemm_probe_copy(src: torch.Tensor, dst: torch.Tensor, stream=None) -> None
     if src.numel() != dst.numel():
         raise ValueError("src and dst differ in size")
     _check(lib().mdgemm_probe_copy(_ptr(src), _ptr(dst), src.numel(), _stream(stream)), "mdgemm_probe_copy")
+
+
+def mdgemm_qr_dd(A: torch.Tensor, nb: int = 32, workspace: Optional[torch.Tensor] = None, stream=None):
+    """Householder QR of a double-double matrix A [2, m, n] (m >= n) in place:
+    returns (A, tau) with R on and above the diagonal of A, the Householder
+    vectors below it, and tau [2, n]."""
+    _dev_tensor(A, torch.float64, "A")
+    if A.dim() != 3 or A.shape[0] != 2:
+        raise ValueError("A must be a double-double matrix [2, m, n]")
+    _, m, n = A.shape
+    tau = torch.empty((2, n), dtype=torch.float64, device=A.device)
+    if workspace is None:
+        need = int(lib().mdgemm_qr_dd_workspace_bytes(m, n, nb))
+        if need == 2**64 - 1:
+            _check(MDGEMM_EINVAL, "mdgemm_qr_dd_workspace_bytes")
+        workspace = torch.empty(need, dtype=torch.uint8, device=A.device)
+    _check(lib().mdgemm_qr_dd(m, n, nb, _ptr(A), _ptr(tau), _ptr(workspace), workspace.numel(), _stream(stream)),
+           "mdgemm_qr_dd")
+    return A, tau

@@ -746,6 +746,72 @@ def test_exponent_classes_restore_the_tolerance():
     assert ref[(0, 0)]["limbs"] == C[:, 0, 0].tolist() and ref[(2, 1)]["limbs"] == C[:, 2, 1].tolist()
 
 
+# --------------------------------------------------------------------------
+# the downstream application: Householder QR in double-double
+# --------------------------------------------------------------------------
+
+def test_qr_oracle_closed_form():
+    # x = (3, 4): ||x|| = 5, v_1 = -sigma / (x_1 + mu) = -16 / 8 = -2, so the stored
+    # vector is 4 / -2 = -2 and tau = 2 v_1^2 / (sigma + v_1^2) = 8 / 20 = 0.4
+    A = np.zeros((2, 2, 1))
+    A[0, :, 0] = [3.0, 4.0]
+    QR, tau = coracle.qr_dd(A)
+    assert QR[:, 0, 0].tolist() == [5.0, 0.0] and QR[:, 1, 0].tolist() == [-2.0, 0.0]
+    assert abs(exact.value(tau[:, 0]) - Fraction(2, 5)) < Fraction(1, 2**105)  # 0.4 to double-double precision
+
+
+def _exact_q(QR, tau):
+    """Thin Q as Fractions from the stored vectors and tau (reflections applied to I)."""
+    _, m, n = QR.shape
+    Q = [[Fraction(int(r == c)) for c in range(n)] for r in range(m)]
+    for j in range(n - 1, -1, -1):
+        t = exact.value(tau[:, j])
+        v = [Fraction(0)] * j + [Fraction(1)] + [exact.value(QR[:, r, j]) for r in range(j + 1, m)]
+        for c in range(n):
+            w = sum(v[r] * Q[r][c] for r in range(j, m))
+            for r in range(j, m):
+                Q[r][c] -= t * w * v[r]
+    return Q
+
+
+def test_qr_oracle_exact_residual_and_orthogonality():
+    # the oracle's factorization checked in exact rational arithmetic (no
+    # double-double on the checking side): A - Q R and Q^T Q - I at the level of
+    # double-double rounding, and the oracle's own check agrees with it
+    rng = np.random.default_rng(4)
+    A = workloads.make_operand(rng, 2, 6, 4, "normal")
+    QR, tau = coracle.qr_dd(A)
+    Q = _exact_q(QR, tau)
+    m, n = 6, 4
+    amax = max(abs(exact.value(A[:, r, c])) for r in range(m) for c in range(n))
+    res = max(abs(exact.value(A[:, r, c]) - sum(Q[r][l] * exact.value(QR[:, l, c]) for l in range(c + 1)))
+              for r in range(m) for c in range(n)) / amax
+    orth = max(abs(sum(Q[r][i] * Q[r][c] for r in range(m)) - int(i == c)) for i in range(n) for c in range(n))
+    assert res < Fraction(1, 2**100) and orth < Fraction(1, 2**100)
+    r2, o2, _ = coracle.qr_dd_check(A, QR, tau)
+    assert r2 < 2.0**-100 and o2 < 2.0**-100
+    assert all(QR[0, j, j] >= 0.0 for j in range(n))
+    # a wrong tau (one part in 2^60) is visible to both checks
+    bad = tau.copy()
+    bad[1, 1] += bad[0, 1] * 2.0**-60
+    Qb = _exact_q(QR, bad)
+    orth_b = max(abs(sum(Qb[r][i] * Qb[r][c] for r in range(m)) - int(i == c)) for i in range(n) for c in range(n))
+    assert orth_b > Fraction(1, 2**70)
+    assert coracle.qr_dd_check(A, QR, bad)[1] > 2.0**-70
+
+
+def test_qr_oracle_agrees_with_float64_qr():
+    # R of the double-double factorization rounded to doubles against LAPACK's
+    # float64 QR (numpy), rows' signs normalized to a nonnegative diagonal
+    rng = np.random.default_rng(5)
+    A = workloads.make_operand(rng, 2, 50, 30, "normal")
+    QR, _ = coracle.qr_dd(A)
+    R = np.triu(QR[0])[:30]
+    Rn = np.linalg.qr(A[0] + A[1])[1]
+    Rn *= np.sign(np.diag(Rn))[:, None]
+    assert np.abs(R - Rn).max() <= 1e-12 * np.abs(Rn).max()
+
+
 def test_method_bound_catches_a_dropped_kept_pair():
     # Planted in the oracle's chain: leave out pair (0, T) of the last kept level.
     L, S, T, k = 8, 32, 31, 16
