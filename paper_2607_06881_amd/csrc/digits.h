@@ -119,6 +119,105 @@ __device__ inline bool floor_on_grid(const double (&xs)[ML], int L, int g, uint6
   return neg;
 }
 
+// The same floor for digit windows of at most 128 bits (w S <= 128), held in one
+// 128-bit integer without fraction bits.  By nonoverlap (|x_{l+1}| <= ulp(x_l)/2)
+// only the first limb with bits below the grid unit matters below it: the
+// limbs after it are smaller than one unit of its last place, so the fraction
+// of |V| / u has that limb's sign relative to V and lies strictly between -1 and
+// 1.  Hence D = sum over the limbs up to it of +-floor(|x_l| / u), lowered by
+// one when that limb has the opposite sign of V.  Every partial sum stays in
+// [0, 2^(w S)) and |x_0| < 2^(g + w S) keeps each shift below 128 - 53.
+template <int ML>
+__device__ inline bool floor_on_grid_128(const double (&xs)[ML], int L, int g, uint64_t (&I)[2]) {
+  const bool neg = xs[0] < 0.0;
+  unsigned __int128 acc = 0;
+  bool lower = false;
+#pragma unroll
+  for (int l = 0; l < ML; ++l) {
+    const double xl = xs[l];
+    if (l >= L || xl == 0.0) break;  // normalized: every later limb is zero too
+    const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(xl));
+    const bool sub = ((bits >> 63) != 0) != neg;
+    const uint64_t mag = bits & 0x7fffffffffffffffull;
+    const int be = static_cast<int>(mag >> 52);
+    const uint64_t M = be != 0 ? ((mag & 0x000fffffffffffffull) | 0x0010000000000000ull) : mag;
+    int k = (be != 0 ? be - 1075 : -1074) - g;  // |x_l| / u = M 2^k
+    if (k <= -53) {  // the whole limb lies below the grid unit
+      lower = sub;
+      break;
+    }
+    k = k < 127 ? k : 127;  // only for exponents that are not the line's maximum
+    const unsigned __int128 part = k >= 0 ? static_cast<unsigned __int128>(M) << k : M >> -k;
+    acc = sub ? acc - part : acc + part;
+    if (k < 0 && (M & ((1ull << -k) - 1ull)) != 0) {  // bits below the unit: the last limb that counts
+      lower = sub;
+      break;
+    }
+  }
+  if (lower) acc -= 1;
+  I[0] = static_cast<uint64_t>(acc);
+  I[1] = static_cast<uint64_t>(acc >> 64);
+  return neg;
+}
+
+// The same floor for windows of at most 256 bits, in two 128-bit halves with the
+// carry (or borrow) between them formed by comparison.
+template <int ML>
+__device__ inline bool floor_on_grid_256(const double (&xs)[ML], int L, int g, uint64_t (&I)[4]) {
+  typedef unsigned __int128 u128;
+  const bool neg = xs[0] < 0.0;
+  u128 lo = 0, hi = 0;
+  bool lower = false;
+#pragma unroll
+  for (int l = 0; l < ML; ++l) {
+    const double xl = xs[l];
+    if (l >= L || xl == 0.0) break;
+    const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(xl));
+    const bool sub = ((bits >> 63) != 0) != neg;
+    const uint64_t mag = bits & 0x7fffffffffffffffull;
+    const int be = static_cast<int>(mag >> 52);
+    const uint64_t M = be != 0 ? ((mag & 0x000fffffffffffffull) | 0x0010000000000000ull) : mag;
+    int k = (be != 0 ? be - 1075 : -1074) - g;
+    if (k <= -53) {
+      lower = sub;
+      break;
+    }
+    k = k < 255 ? k : 255;
+    u128 plo, phi;  // M 2^k (integer part) as two halves
+    if (k < 0) {
+      plo = M >> -k;
+      phi = 0;
+    } else if (k < 128) {
+      plo = static_cast<u128>(M) << k;
+      phi = k > 75 ? static_cast<u128>(M) >> (128 - k) : 0;  // the bits that pass bit 127
+    } else {
+      plo = 0;
+      phi = static_cast<u128>(M) << (k - 128);
+    }
+    if (sub) {
+      const u128 borrow = lo < plo ? 1 : 0;
+      lo -= plo;
+      hi = hi - phi - borrow;
+    } else {
+      lo += plo;
+      hi = hi + phi + (lo < plo ? 1 : 0);
+    }
+    if (k < 0 && (M & ((1ull << -k) - 1ull)) != 0) {
+      lower = sub;
+      break;
+    }
+  }
+  if (lower) {
+    hi -= lo == 0 ? 1 : 0;
+    lo -= 1;
+  }
+  I[0] = static_cast<uint64_t>(lo);
+  I[1] = static_cast<uint64_t>(lo >> 64);
+  I[2] = static_cast<uint64_t>(hi);
+  I[3] = static_cast<uint64_t>(hi >> 64);
+  return neg;
+}
+
 // The L limbs of the element at idx (limb stride ls), all loads issued together;
 // limbs beyond L are +0.0 (L is the same for every thread).
 template <int ML>

@@ -20,12 +20,16 @@
 // double every limb whose top bit is at or above u has its ulp at or above
 // 2^-52 u, so those limbs add exactly; the first limb entirely below u (and
 // everything after it, of smaller magnitude) only decides the floor through its
-// sign, when the fraction of the accumulated part is exactly zero.
+// sign, when the fraction of the accumulated part is exactly zero.  For digit
+// windows of up to 256 bits (multiple doubles of up to four limbs at the
+// default digits) the panel kernel uses the equivalent integer-only form
+// without fraction bits (floor_on_grid_128 / _256: by nonoverlap only the first
+// limb with bits below u acts below it), in 128-bit arithmetic.
 //
 // Two output layouts share this arithmetic: row-major digit planes (one thread
 // per element, consecutive threads on consecutive columns, so limb loads and
 // digit stores of a wave are contiguous 512-byte rows), and the k-major padded
-// panels the level GEMM reads (see split_panel_kernel).
+// panels the level GEMM reads (see split_panel_kernel and split_tile_kernel).
 #include <type_traits>
 
 #include "digits.h"
@@ -131,6 +135,127 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
           if (C > S) store_combos<NW, OutT>(I, S, C, w, neg, masks, out, pplane);
         } else {
           for (int s = 0; s < (C > S ? C : S); ++s) out[static_cast<int64_t>(s) * pplane] = OutT(0);
+        }
+      }
+    }
+  }
+}
+
+// The panel layout of split_panel_kernel for multiple doubles of up to four
+// limbs, a block per tile of 64 lines x 16 k values, in two phases:
+//  - load: the tile's limbs go through LDS, so that every global load of a wave
+//    reads whole 128-byte lines whichever operand it is (A's lines are rows, 16
+//    consecutive k values of a row per 16 lanes; B's lines are columns, 64
+//    consecutive columns per wave), the padding positions loading +0.0;
+//  - split: each thread takes 4 consecutive lines of one k value, so that every
+//    digit store is one 16-byte vector (a wave writes 1 KiB of a panel row).
+// kFast selects floor_on_grid_128 (digit windows w S <= 128, NW = 2) or
+// floor_on_grid_256 (w S <= 256, NW = 4); otherwise floor_on_grid with NW words.  The digit fields are read upward from bit 0 in a
+// two-word window as in store_digits; the window position is the same for all
+// four elements (and all lanes), so only the words differ.
+constexpr int kTileLines = 64, kTileK = 16, kTilePitch = kTileLines + 4;  // LDS row pitch in doubles
+
+__host__ __device__ constexpr size_t split_tile_lds(int L) {
+  return sizeof(double) * static_cast<size_t>(L) * kTileK * kTilePitch;
+}
+
+template <class OutT>
+__device__ inline OutT digit_value(uint64_t f, uint64_t mask, bool neg);
+template <>
+__device__ inline float digit_value<float>(uint64_t f, uint64_t mask, bool neg) {
+  const uint32_t d = static_cast<uint32_t>(f & mask);  // below 2^24 for FP32 panels: exact
+  const uint32_t b = __float_as_uint(static_cast<float>(d));
+  return __uint_as_float(b | ((neg && d) ? 0x80000000u : 0u));  // zero digits are +0.0
+}
+template <>
+__device__ inline double digit_value<double>(uint64_t f, uint64_t mask, bool neg) {
+  return signed_digit(static_cast<uint32_t>(f & mask), neg);
+}
+
+__device__ inline void store4(float* p, const float (&v)[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ inline void store4(double* p, const double (&v)[4]) {
+  reinterpret_cast<double2*>(p)[0] = make_double2(v[0], v[1]);
+  reinterpret_cast<double2*>(p)[1] = make_double2(v[2], v[3]);
+}
+
+template <int NW, int ML, class OutT, bool kFast>
+__global__ void __launch_bounds__(256) split_tile_kernel(int64_t rows, int64_t cols, int L, int S, int w, int axis,
+                                                         int64_t kp, int64_t cp, const double* __restrict__ X,
+                                                         const int32_t* __restrict__ E, OutT* __restrict__ D) {
+  static_assert(!kFast || NW == 2 || NW == 4, "the fast floors fill two or four words");
+  extern __shared__ double tile[];  // [L][kTileK][kTilePitch]
+  const int64_t plane = rows * cols, pplane = kp * cp;
+  const int64_t K = axis == 0 ? cols : rows;   // reduction length
+  const int64_t Cn = axis == 0 ? rows : cols;  // lines
+  const int t = threadIdx.x;
+  const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kTileLines;
+  const int qk = t >> 4, qc = 4 * (t & 15);  // split phase: lines qc .. qc + 3 of k row qk
+  int e[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) e[i] = c0 + qc + i < Cn ? E[c0 + qc + i] : 0;
+  const uint64_t mask = (1ull << w) - 1ull;
+  for (int64_t kb = blockIdx.y; kb * kTileK < kp; kb += gridDim.y) {
+    const int64_t k0 = kb * kTileK;
+    double v[ML][4];
+    int lk[4], lc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      lk[i] = axis == 0 ? (t & 15) : (t >> 6) + 4 * i;
+      lc[i] = axis == 0 ? (t >> 4) + 16 * i : (t & 63);
+      const int64_t c = c0 + lc[i], kk = k0 + lk[i];
+      const bool ok = c < Cn && kk < K;
+      const int64_t idx = ok ? (axis == 0 ? c * cols + kk : kk * cols + c) : 0;
+#pragma unroll
+      for (int l = 0; l < ML; ++l) v[l][i] = (ok && l < L) ? X[static_cast<int64_t>(l) * plane + idx] : 0.0;
+    }
+    __syncthreads();  // the previous tile's readers are done
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int l = 0; l < ML; ++l)
+        if (l < L) tile[(l * kTileK + lk[i]) * kTilePitch + lc[i]] = v[l][i];
+    __syncthreads();
+    uint64_t I[4][NW];
+    bool neg[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      double xs[ML];
+#pragma unroll
+      for (int l = 0; l < ML; ++l) xs[l] = l < L ? tile[(l * kTileK + qk) * kTilePitch + qc + i] : 0.0;
+      if constexpr (kFast && NW == 2)
+        neg[i] = floor_on_grid_128<ML>(xs, L, e[i] - w * S, I[i]);
+      else if constexpr (kFast)
+        neg[i] = floor_on_grid_256<ML>(xs, L, e[i] - w * S, I[i]);
+      else
+        neg[i] = floor_on_grid<NW, ML>(xs, L, e[i] - w * S, I[i]);
+    }
+    OutT* out = D + (k0 + qk) * cp + c0 + qc + static_cast<int64_t>(S - 1) * pplane;
+    uint64_t cur[4], nxt[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      cur[i] = I[i][0];
+      nxt[i] = NW > 1 ? I[i][1] : 0ull;
+    }
+    int b = 0, wi = 0;  // the window: word wi of every I, next unread bit b
+    for (int j = 0; j < S; ++j) {
+      OutT d[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint64_t f = cur[i] >> b;
+        if (b + w > 64) f |= nxt[i] << (64 - b);
+        d[i] = digit_value<OutT>(f, mask, neg[i]);
+      }
+      store4(out - static_cast<int64_t>(j) * pplane, d);
+      b += w;
+      if (b >= 64) {
+        b -= 64;
+        ++wi;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          cur[i] = nxt[i];
+          nxt[i] = word_or_zero<NW>(I[i], wi + 1);
         }
       }
     }
@@ -272,6 +397,28 @@ hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int w, int axis, 
   const int64_t nkb = kp / (wide ? 16 : 4);
   const unsigned gy = static_cast<unsigned>(nkb < 65535 ? nkb : 65535);
   const dim3 grid(gx, gy);
+  if constexpr (ML == 4) {
+    // tiles of 64 lines x 16 k through LDS, 16-byte digit stores (the panel base
+    // must be 16-byte aligned; kp is a multiple of 16 and cp of 64)
+    if (wide && C == S && (reinterpret_cast<uintptr_t>(D) & 15u) == 0) {
+      const size_t lds = split_tile_lds(L);
+      auto go = [&](auto kernel, auto* out) {
+        hipLaunchKernelGGL(kernel, grid, dim3(256), lds, stream, rows, cols, L, S, w, axis, kp, cp, X, E, out);
+        return hipGetLastError();
+      };
+      const int bits = w * S;
+      if (f32) {
+        float* out = static_cast<float*>(D);
+        if (bits <= 128) return go(split_tile_kernel<2, 4, float, true>, out);
+        if (bits <= 256) return go(split_tile_kernel<4, 4, float, true>, out);
+        return go(split_tile_kernel<NW, 4, float, false>, out);
+      }
+      double* out = static_cast<double*>(D);
+      if (bits <= 128) return go(split_tile_kernel<2, 4, double, true>, out);
+      if (bits <= 256) return go(split_tile_kernel<4, 4, double, true>, out);
+      return go(split_tile_kernel<NW, 4, double, false>, out);
+    }
+  }
   if (f32) {
     if (wide)
       hipLaunchKernelGGL((split_panel_kernel<NW, ML, float, 4>), grid, dim3(256), 0, stream, rows, cols, L, S, w, axis,
