@@ -914,9 +914,9 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
       timing().valid = false;
       MDG_TRY(record(0, s));
     }
-    // a1: grid exponents per row of A and per column of B
-    MDG_TRY(hip_status(mdg::launch_exponents(m, k, 0, A, w.EA, s)));
-    MDG_TRY(hip_status(mdg::launch_exponents(k, n, 1, B, w.EB, s)));
+    // a1: grid exponents per row of A and per column of B (partial column maxima
+    // in B's panel region, which the split overwrites next)
+    MDG_TRY(hip_status(mdg::launch_exponents_ab(m, k, n, A, B, w.EA, w.EB, w.DB, L.g - L.db, s)));
     if (timed) MDG_TRY(record(1, s));
     // a2: exact splits into S digit panels and, beside them, the schedule's
     // combinations (digit sums) from the same integers

@@ -64,6 +64,91 @@ __global__ void __launch_bounds__(256) col_exponents_kernel(int64_t rows, int64_
   }
 }
 
+// Both operands in one launch, without an initial fill or a final pass over
+// atomics: blocks [0, ra) take four rows of A each (one wave per row); blocks
+// [ra, ra + cx cy) take 64 columns of B over one chunk of chunk_rows rows (lanes
+// on consecutive columns, the four waves on interleaved rows) and write the
+// chunk's maxima to P[chunk][column] (kNoExp where the chunk has no nonzero), or,
+// with a single chunk (cy = 1), the final exponents straight to EB.  Every lane
+// issues its loads in predicated batches of eight before reducing them; with
+// kVec, A's rows are read as 16-byte pairs (k even and A 16-byte aligned).
+template <bool kVec>
+__global__ void __launch_bounds__(256) exponents_ab_kernel(int64_t m, int64_t k, int64_t n,
+                                                           const double* __restrict__ A0,
+                                                           const double* __restrict__ B0, int32_t* __restrict__ EA,
+                                                           int32_t* __restrict__ EB, int32_t* __restrict__ P,
+                                                           int64_t ra, int64_t cx, int64_t cy, int64_t chunk_rows) {
+  __shared__ int part[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t b = blockIdx.x;
+  if (b < ra) {  // block-uniform: A's rows
+    const int64_t row = b * 4 + wave;
+    if (row >= m) return;
+    int best = kNoExp;
+    if constexpr (kVec) {
+      const double2* r = reinterpret_cast<const double2*>(A0 + row * k);
+      const int64_t k2 = k / 2;
+      for (int64_t c = lane; c < k2; c += 64 * 8) {
+        double2 x[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = c + 64 * j < k2 ? r[c + 64 * j] : make_double2(0.0, 0.0);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) best = max(best, max(frexp_exp_or_min(x[j].x), frexp_exp_or_min(x[j].y)));
+      }
+    } else {
+      const double* r = A0 + row * k;
+      for (int64_t c = lane; c < k; c += 64 * 8) {
+        double x[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = c + 64 * j < k ? r[c + 64 * j] : 0.0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) best = max(best, frexp_exp_or_min(x[j]));
+      }
+    }
+    best = wave_max(best);
+    if (lane == 0) EA[row] = best == kNoExp ? 0 : best;
+    return;
+  }
+  const int64_t bb = b - ra, chunk = bb / cx;
+  const int64_t col = (bb - chunk * cx) * 64 + lane;
+  int best = kNoExp;
+  if (col < n) {
+    const int64_t r1 = min(k, (chunk + 1) * chunk_rows);
+    for (int64_t r = chunk * chunk_rows + wave; r < r1; r += 4 * 8) {
+      double x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = r + 4 * j < r1 ? B0[(r + 4 * j) * n + col] : 0.0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) best = max(best, frexp_exp_or_min(x[j]));
+    }
+  }
+  part[wave][lane] = best;
+  __syncthreads();
+  if (wave == 0 && col < n) {
+    best = max(max(part[0][lane], part[1][lane]), max(part[2][lane], part[3][lane]));
+    if (cy == 1)
+      EB[col] = best == kNoExp ? 0 : best;
+    else
+      P[chunk * n + col] = best;
+  }
+}
+
+// EB[j] = the largest of the cy chunk maxima of column j, 0 for a zero column.
+__global__ void __launch_bounds__(256) reduce_col_chunks_kernel(int64_t n, int64_t cy, const int32_t* __restrict__ P,
+                                                                int32_t* __restrict__ EB) {
+  const int64_t col = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (col >= n) return;
+  int best = kNoExp;
+  for (int64_t c = 0; c < cy; c += 8) {
+    int v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = c + j < cy ? P[(c + j) * n + col] : kNoExp;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) best = max(best, v[j]);
+  }
+  EB[col] = best == kNoExp ? 0 : best;
+}
+
 // Smallest frexp exponent of a nonzero entry of every row (one wave per row) or
 // column (64 columns per block, as col_exponents_kernel, vector atomic min);
 // INT_MAX for a line without a nonzero entry.
@@ -178,6 +263,38 @@ hipError_t launch_exponents(int64_t rows, int64_t cols, int axis, const double* 
     if (err != hipSuccess) return err;
   }
   hipLaunchKernelGGL(finalize_exponents_kernel, dim3(grid_for(cols, 256, 1ll << 30)), dim3(256), 0, stream, cols, E);
+  return hipGetLastError();
+}
+
+hipError_t launch_exponents_ab(int64_t m, int64_t k, int64_t n, const double* A0, const double* B0, int32_t* EA,
+                               int32_t* EB, void* scratch, size_t scratch_bytes, hipStream_t stream) {
+  const int64_t ra = (m + 3) / 4, cx = (n + 63) / 64;
+  // 16 column chunks: a wave of B's blocks then reads 64 columns x k / 64 rows,
+  // as many elements as a wave of A's rows (both kinds of blocks take about the
+  // same time); chunks of at least 64 rows
+  int64_t cy = 16;
+  const int64_t max_cy = (k + 63) / 64;
+  if (cy > max_cy) cy = max_cy;
+  if (cy < 1) cy = 1;
+  if (cy > 1 && static_cast<size_t>(cy) * static_cast<size_t>(n) * sizeof(int32_t) > scratch_bytes) {
+    hipError_t err = launch_exponents(m, k, 0, A0, EA, stream);
+    return err != hipSuccess ? err : launch_exponents(k, n, 1, B0, EB, stream);
+  }
+  const int64_t chunk_rows = cy > 1 ? (k + cy - 1) / cy : (k > 0 ? k : 1);
+  const int64_t blocks = ra + cx * cy;
+  if (blocks == 0) return hipSuccess;
+  if (blocks > INT_MAX) return hipErrorInvalidValue;
+  int32_t* P = static_cast<int32_t*>(scratch);
+  const bool vec = k % 2 == 0 && (reinterpret_cast<uintptr_t>(A0) & 15u) == 0;
+  if (vec)
+    hipLaunchKernelGGL(exponents_ab_kernel<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, m, k, n,
+                       A0, B0, EA, EB, P, ra, cx, cy, chunk_rows);
+  else
+    hipLaunchKernelGGL(exponents_ab_kernel<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, m, k, n,
+                       A0, B0, EA, EB, P, ra, cx, cy, chunk_rows);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || cy == 1 || n == 0) return err;
+  hipLaunchKernelGGL(reduce_col_chunks_kernel, dim3(grid_for(n, 256, 1ll << 30)), dim3(256), 0, stream, n, cy, P, EB);
   return hipGetLastError();
 }
 

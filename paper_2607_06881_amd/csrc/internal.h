@@ -44,6 +44,11 @@ struct GemmJobs {
 
 // a1: per-row (axis 0) or per-column (axis 1) grid exponents of a [rows][cols] plane.
 hipError_t launch_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, hipStream_t stream);
+// The exponents of A's rows (EA) and of B's columns (EB) in one pass over both
+// leading limbs; scratch (cy n int32 partial maxima, cy <= ceil(k / 64)) is
+// device memory that is free until the pass ends (too small: the two launches above).
+hipError_t launch_exponents_ab(int64_t m, int64_t k, int64_t n, const double* A0, const double* B0, int32_t* EA,
+                               int32_t* EB, void* scratch, size_t scratch_bytes, hipStream_t stream);
 
 // Exponent spread of every line: E as launch_exponents, spread = E - (smallest
 // frexp exponent of a nonzero entry of the line), 0 for an all-zero line.
