@@ -20,8 +20,10 @@ Prints one JSON line:
   keeps the workload's 13-bit digits unless ``--slice-bits`` says otherwise;
 * ``calibration``: the FP64 MFMA rate and the HBM copy rate measured on the
   same device in the same run (the library's probe kernels), beside the
-  published 78.6 TFLOP/s and 8 TB/s; ``roofline.frac_of_measured`` and each
-  stage's ``frac_of_copy`` are taken against them;
+  published 78.6 TFLOP/s and 8 TB/s; ``roofline.frac_of_measured`` is taken
+  against the former; every memory-bound stage gets ``frac_of_peak`` (against
+  8 TB/s) and ``frac_of_probe``, against the library's plain stream probe run
+  at the stage's own size and read/write mix (``probe_GB/s``, ``probe_mix``);
 * ``parity``: outside the timed region, the last timed step's C at sampled
   entries (corners, the rows and columns of extreme exponents, random ones)
   against the CPU oracle's chain (bit-exact limbs) and against the exact
@@ -133,6 +135,26 @@ def calibrate(md, torch, dev, stream):
             "copy_GB/s": round(copy, 1), "hbm_published_GB/s": HBM_PEAK_GBS,
             "probes": "mdgemm_probe_mfma_f64 (2048 x 256 threads, 8 independent v_mfma_f64_16x16x4f64 chains per "
                       "wave, 20000 rounds); mdgemm_probe_copy (2 GiB, read + write bytes, 5 copies)"}
+
+
+def stage_probes(md, torch, dev, stream, mixes, reps=3):
+    """The library's plain stream probe at each memory-bound stage's own size and
+    read/write mix (count elements, reads and writes planes of doubles each)."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {}
+    for key, (count, reads, writes) in mixes.items():
+        src = torch.ones(reads * count, dtype=torch.float64, device=dev)
+        dst = torch.empty(writes * count, dtype=torch.float64, device=dev) if writes else None
+        md.mdgemm_probe_stream(src, reads, dst, writes, count, stream=stream)  # warm-up
+        e0.record(stream)
+        for _ in range(reps):
+            md.mdgemm_probe_stream(src, reads, dst, writes, count, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        gbs = 8.0 * count * (reads + writes) * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        out[key] = {"GB/s": round(gbs, 1), "count": count, "reads": reads, "writes": writes}
+        del src, dst
+    return out
 
 
 def parity(w, A_h, B_h, C_h, S, T, bits, count=32):
@@ -470,9 +492,22 @@ def main(argv=None) -> int:
         out["calibration"] = cal
         roofline["peak_measured"] = cal["mfma_f64_TFLOP/s"]
         roofline["frac_of_measured"] = round(achieved / cal["mfma_f64_TFLOP/s"], 4)
-        for key in ("exponents", "split", "accum_renorm"):
-            if key in stages:
-                stages[key]["frac_of_copy"] = round(stages[key]["GB/s"] / cal["copy_GB/s"], 4)
+        # every memory-bound stage against the published 8 TB/s and against a
+        # plain stream of its own size and read/write mix (planes of doubles,
+        # the stage's read and write bytes per element rounded to whole planes)
+        if "split" in stages:
+            cnt_s = m * k + k * n
+            w_split = bytes_split - 8.0 * L * cnt_s - 4.0 * (m + n)
+            mixes = {"exponents": (cnt_s, 1, 0),
+                     "split": (cnt_s, L, max(1, round(w_split / (8.0 * cnt_s)))),
+                     "accum_renorm": (m * n, max(1, round((bytes_acc - 8.0 * L * m * n - 4.0 * (m + n)) /
+                                                          (8.0 * m * n))), L)}
+            probes = stage_probes(md, torch, dev, stream, mixes)
+            for key, pr in probes.items():
+                stages[key]["frac_of_peak"] = round(stages[key]["GB/s"] / HBM_PEAK_GBS, 4)
+                stages[key]["probe_GB/s"] = pr["GB/s"]
+                stages[key]["frac_of_probe"] = round(stages[key]["GB/s"] / pr["GB/s"], 4)
+                stages[key]["probe_mix"] = f"{pr['reads']} read + {pr['writes']} write planes of {pr['count']}"
     if bits_arg == 13 and not sched_flags and args.adaptive_steps > 0:
         # the same workload with the adaptive width reported beside the paper's
         # 13-bit digit pairs (and, on request, the Karatsuba schedule and the

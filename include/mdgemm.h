@@ -470,6 +470,14 @@ int64_t mdgemm_probe_mfma_f64(int64_t blocks, int64_t iters, double* sink, void*
  * reads and writes 8 count bytes each, the HBM rate of a plain stream. */
 int mdgemm_probe_copy(const double* src, double* dst, int64_t count, void* stream);
 
+/* Plain streaming rate for a read/write mix: out of src [reads][count] (doubles,
+ * plane stride count) every element's planes are read and [writes][count]
+ * doubles written to dst.  reads 1..256, writes 0..256; the two regions must not
+ * overlap.  Stream ordered; returns MDGEMM_OK, MDGEMM_EINVAL or MDGEMM_EHIP.
+ * bench.py times it at the size and mix of the exponent, split and
+ * accumulation stages. */
+int mdgemm_probe_stream(const double* src, int reads, double* dst, int writes, int64_t count, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -196,20 +196,29 @@ __global__ void __launch_bounds__(256) split_tile_kernel(int64_t rows, int64_t c
 #pragma unroll
   for (int i = 0; i < 4; ++i) e[i] = c0 + qc + i < Cn ? E[c0 + qc + i] : 0;
   const uint64_t mask = (1ull << w) - 1ull;
-  for (int64_t kb = blockIdx.y; kb * kTileK < kp; kb += gridDim.y) {
-    const int64_t k0 = kb * kTileK;
-    double v[ML][4];
-    int lk[4], lc[4];
+  // load-phase positions (fixed per thread) and the tile's limbs in registers;
+  // the next tile's loads are issued before the current tile is split
+  int lk[4], lc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    lk[i] = axis == 0 ? (t & 15) : (t >> 6) + 4 * i;
+    lc[i] = axis == 0 ? (t >> 4) + 16 * i : (t & 63);
+  }
+  double v[ML][4];
+  auto load_tile = [&](int64_t k0) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      lk[i] = axis == 0 ? (t & 15) : (t >> 6) + 4 * i;
-      lc[i] = axis == 0 ? (t >> 4) + 16 * i : (t & 63);
       const int64_t c = c0 + lc[i], kk = k0 + lk[i];
       const bool ok = c < Cn && kk < K;
       const int64_t idx = ok ? (axis == 0 ? c * cols + kk : kk * cols + c) : 0;
 #pragma unroll
       for (int l = 0; l < ML; ++l) v[l][i] = (ok && l < L) ? X[static_cast<int64_t>(l) * plane + idx] : 0.0;
     }
+  };
+  int64_t kb = blockIdx.y;
+  if (kb * kTileK < kp) load_tile(kb * kTileK);
+  for (; kb * kTileK < kp; kb += gridDim.y) {
+    const int64_t k0 = kb * kTileK;
     __syncthreads();  // the previous tile's readers are done
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -217,6 +226,7 @@ __global__ void __launch_bounds__(256) split_tile_kernel(int64_t rows, int64_t c
       for (int l = 0; l < ML; ++l)
         if (l < L) tile[(l * kTileK + lk[i]) * kTilePitch + lc[i]] = v[l][i];
     __syncthreads();
+    if ((kb + gridDim.y) * kTileK < kp) load_tile((kb + gridDim.y) * kTileK);
     uint64_t I[4][NW];
     bool neg[4];
 #pragma unroll
@@ -402,6 +412,12 @@ hipError_t launch_nw(int64_t rows, int64_t cols, int L, int S, int w, int axis, 
     // must be 16-byte aligned; kp is a multiple of 16 and cp of 64)
     if (wide && C == S && (reinterpret_cast<uintptr_t>(D) & 15u) == 0) {
       const size_t lds = split_tile_lds(L);
+      // up to four tiles per block (each block's next loads overlap its split)
+      // while at least 2048 blocks remain
+      int64_t tiles = kp / kTileK, per = 1;
+      while (per < 4 && gx * ((tiles + 2 * per - 1) / (2 * per)) >= 2048) per *= 2;
+      const int64_t gyt = (tiles + per - 1) / per;
+      const dim3 grid(gx, static_cast<unsigned>(gyt < 65535 ? gyt : 65535));
       auto go = [&](auto kernel, auto* out) {
         hipLaunchKernelGGL(kernel, grid, dim3(256), lds, stream, rows, cols, L, S, w, axis, kp, cp, X, E, out);
         return hipGetLastError();

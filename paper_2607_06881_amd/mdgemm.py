@@ -91,6 +91,7 @@ EXPORTED = (
     "mdgemm_qr_dd",
     "mdgemm_probe_mfma_f64",
     "mdgemm_probe_copy",
+    "mdgemm_probe_stream",
 )
 
 
@@ -182,6 +183,8 @@ def lib() -> ctypes.CDLL:
         L.mdgemm_probe_mfma_f64.restype = ctypes.c_int64
         L.mdgemm_probe_copy.argtypes = [_vp, _vp, _i64, _vp]
         L.mdgemm_probe_copy.restype = ctypes.c_int
+        L.mdgemm_probe_stream.argtypes = [_vp, ctypes.c_int, _vp, ctypes.c_int, _i64, _vp]
+        L.mdgemm_probe_stream.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -567,6 +570,21 @@ def mdgemm_probe_copy(src: torch.Tensor, dst: torch.Tensor, stream=None) -> None
     if src.numel() != dst.numel():
         raise ValueError("src and dst differ in size")
     _check(lib().mdgemm_probe_copy(_ptr(src), _ptr(dst), src.numel(), _stream(stream)), "mdgemm_probe_copy")
+
+
+def mdgemm_probe_stream(src: torch.Tensor, reads: int, dst: Optional[torch.Tensor], writes: int, count: int,
+                        stream=None) -> None:
+    """Read `reads` planes of `count` doubles from src and write `writes` planes
+    to dst through the library's stream probe."""
+    _dev_tensor(src, torch.float64, "src")
+    if src.numel() < reads * count:
+        raise ValueError("src holds fewer than reads x count doubles")
+    if writes > 0:
+        _dev_tensor(dst, torch.float64, "dst")
+        if dst.numel() < writes * count:
+            raise ValueError("dst holds fewer than writes x count doubles")
+    _check(lib().mdgemm_probe_stream(_ptr(src), reads, _ptr(dst) if writes > 0 else None, writes, count,
+                                     _stream(stream)), "mdgemm_probe_stream")
 
 
 def mdgemm_qr_dd(A: torch.Tensor, nb: int = 32, workspace: Optional[torch.Tensor] = None, stream=None):
