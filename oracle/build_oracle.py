@@ -31,6 +31,25 @@ def build(verbose: bool = False) -> str:
     return OUT
 
 
+# The oracle under AddressSanitizer + UndefinedBehaviorSanitizer, built by clang
+# so that it shares one sanitizer runtime with the library's sanitized build;
+# without OpenMP (its loops then run on one thread).
+SAN_OUT = os.path.join(os.path.dirname(HERE), "_build_san", "libmdoracle.so")
+CLANG = "/opt/rocm/llvm/bin/clang"
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    os.makedirs(os.path.dirname(SAN_OUT), exist_ok=True)
+    flags = [f for f in CFLAGS if f not in ("-O2", "-fopenmp")] + [
+        "-O1", "-g", "-Wno-unknown-pragmas", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+        "-fno-omit-frame-pointer", "-shared-libasan"]
+    cmd = [CLANG, *flags, "-o", SAN_OUT, SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return SAN_OUT
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build_sanitized(verbose=True) if "--sanitize" in sys.argv[1:] else build(verbose=True))
     sys.exit(0)

@@ -74,6 +74,34 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# AddressSanitizer and UndefinedBehaviorSanitizer on the host code only (the
+# device code is built as usual, unsanitized); run under the clang runtime
+# preloaded (tests/run_sanitized.py does this for the CPU tests).
+SAN_DIR = os.path.join(ROOT, "_build_san")
+SAN_LIB = os.path.join(SAN_DIR, "libmdgemm.so")
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-Xarch_host",
+             "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=undefined", "-g"]
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """The library with its host code under ASan + UBSan, in _build_san/."""
+    objdir = os.path.join(SAN_DIR, "obj")
+    os.makedirs(objdir, exist_ok=True)
+    compile_flags = [f for f in FLAGS if f not in ("-shared", "-O3")] + ["-O1", *SAN_FLAGS]
+    objs = [os.path.join(objdir, os.path.basename(src) + ".o") for src in SOURCES]
+    cmds = [[HIPCC, *compile_flags, "-I", INCLUDE, "-I", os.path.join(HERE, "csrc"), "-c", "-o", obj, src]
+            for src, obj in zip(SOURCES, objs)]
+    with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 1)) as pool:
+        for fut in [pool.submit(_run, cmd, verbose) for cmd in cmds]:
+            fut.result()
+    _run([HIPCC, "--offload-arch=gfx950", "-fPIC", "-shared", "-Xarch_host", "-fsanitize=address", "-Xarch_host",
+          "-fsanitize=undefined", "-shared-libasan", "-o", SAN_LIB, *objs], verbose)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    if "--sanitize" in sys.argv[1:]:
+        print(build_sanitized(verbose=True))
+    else:
+        print(build(verbose=True))
     sys.exit(0)
