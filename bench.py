@@ -157,6 +157,52 @@ def stage_probes(md, torch, dev, stream, mixes, reps=3):
     return out
 
 
+def qr_dd_line(md, torch, dev, stream, A, no_cpu, nb=32, reps=3):
+    """The downstream use: blocked Householder QR (mdgemm_qr_dd) of the
+    workload's double-double A, and of its leading 1024 x 1024 block.  Rate in
+    effective double-double flops, 2 m n^2 - 2 n^3 / 3 per factorization (each
+    double-double operation counted once).  Its parity (residual and
+    orthogonality in double-double against the CPU oracle) is the QR tests';
+    beside it, the oracle's unblocked QR on a 256 x 256 block (CPU)."""
+    import numpy as np
+
+    res = {"nb": nb}
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for key, (mm, nn) in (("full", (A.shape[1], A.shape[2])), ("block_1024", (1024, 1024))):
+        if nn > mm or mm > A.shape[1] or nn > A.shape[2]:
+            continue
+        src = A[:, :mm, :nn].contiguous()
+        need = int(md.lib().mdgemm_qr_dd_workspace_bytes(mm, nn, nb))
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+        work = src.clone()
+        md.mdgemm_qr_dd(work, nb=nb, workspace=ws, stream=stream)  # warm-up
+        times = []
+        for _ in range(reps):
+            work.copy_(src)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            md.mdgemm_qr_dd(work, nb=nb, workspace=ws, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        ms = float(np.median(times))
+        flops = 2.0 * mm * nn * nn - 2.0 * nn ** 3 / 3.0
+        res[key] = {"m": mm, "n": nn, "ms": round(ms, 3), "dd_GFLOP/s": round(flops / (ms * 1e-3) / 1e9, 2),
+                    "workspace_bytes": need}
+        del ws, work, src
+    if not no_cpu:
+        from oracle import coracle
+
+        blk = A[:, :256, :256].cpu().numpy()
+        t0 = time.perf_counter()
+        coracle.qr_dd(blk)
+        sec = time.perf_counter() - t0
+        flops = 2.0 * 256 ** 3 - 2.0 * 256 ** 3 / 3.0
+        res["cpu_oracle_256"] = {"seconds": round(sec, 3), "dd_GFLOP/s": round(flops / sec / 1e9, 4),
+                                 "kind": "oracle", "sample": "unblocked double-double Householder QR, 256 x 256"}
+    return res
+
+
 def parity(w, A_h, B_h, C_h, S, T, bits, count=32):
     """The timed product's C at sampled entries against the CPU oracle (test
     infrastructure, outside the timed region): bit-exact greedy limbs of the
@@ -556,6 +602,8 @@ def main(argv=None) -> int:
         out["exponent_classes"] = grouped(md.MDGEMM_GROUP_EXPONENT)
     if args.extras and bits_arg == 13 and not sched_flags and args.adaptive_steps > 0:
         out["sign_groups"] = grouped(md.MDGEMM_GROUP_SIGN)
+    if args.extras and L == 2:
+        out["qr_dd"] = qr_dd_line(md, torch, dev, stream, A, args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, A_h, B_h, args.cpu_seconds)
     print(json.dumps(out), flush=True)
