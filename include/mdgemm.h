@@ -443,11 +443,12 @@ size_t mdgemm_qr_dd_workspace_bytes(int64_t m, int64_t n, int nb);
  * A = Q R with Q = H_0 ... H_{n-1}, H_j = I - tau_j v_j v_j^T, v_j(j) = 1 and
  * v_j zero above row j.  On return A holds R on and above the diagonal (R(j, j)
  * >= 0) and v_j below it (LAPACK's convention), tau [2][n] the tau_j (all in
- * double-double).  Panels of nb columns (1..32) are factored by one workgroup in
- * double-double arithmetic (Golub and Van Loan's Householder vector); each
- * panel's reflections are accumulated as I - V T V^T (T upper triangular) and
- * the columns to its right updated as A2 - V (T^T (V^T A2)), three products on
- * mdgemm_ex with the default options.  workspace: caller-owned device buffer of
+ * double-double).  Panels of nb columns (1..32) are factored in double-double
+ * arithmetic (Golub and Van Loan's Householder vector; one workgroup for panels
+ * of at most 256 rows, else workgroups of 64 rows with two launches per column);
+ * each panel's reflections are accumulated as I - V T V^T (T upper triangular)
+ * and the columns to its right updated as A2 - V (T^T (V^T A2)), three products
+ * on mdgemm_ex at the adaptive digit width.  workspace: caller-owned device buffer of
  * mdgemm_qr_dd_workspace_bytes() bytes, not overlapping A or tau.  Stream
  * ordered; returns MDGEMM_OK, MDGEMM_EINVAL, MDGEMM_EWORKSPACE or a status of
  * mdgemm_ex.  Inputs must be finite and normalized double-doubles. */

@@ -4,20 +4,24 @@
 //
 // A [2][m][n] (limb-major double-double, m >= n) is factored as A = Q R with
 // Q = H_0 H_1 ... H_{n-1}, H_j = I - tau_j v_j v_j^T (Householder reflections,
-// v_j(j) = 1, v_j zero above row j).  Panels of nb <= 32 columns are factored by
-// one workgroup in double-double arithmetic (dd.h); the panel's reflections are
+// v_j(j) = 1, v_j zero above row j).  Panels of nb <= 32 columns are factored in
+// double-double arithmetic (dd.h), by one workgroup for short panels and by many
+// for tall ones (see qr_col_update_kernel); the panel's reflections are
 // accumulated in the compact form I - V T V^T (T upper triangular, the forward
 // recurrence of Schreiber and Van Loan), and the trailing columns are updated as
 //     A2 <- A2 - V (T^T (V^T A2))
-// with three products on mdgemm_ex (double-double in, double-double out).  On
-// return A holds R on and above the diagonal and the vectors v_j below it
-// (LAPACK's convention), tau the scalars tau_j.
+// with three products on mdgemm_ex (double-double in, double-double out, at the
+// adaptive digit width).  On return A holds R on and above the diagonal and the
+// vectors v_j below it (LAPACK's convention), tau the scalars tau_j.
 //
 // Householder vector of x = A(j:m, j) (Golub and Van Loan, the algorithm that
 // keeps v_1 free of cancellation): sigma = x(2:)^T x(2:), mu = sqrt(x_1^2 +
 // sigma); v_1 = x_1 - mu if x_1 <= 0, else -sigma / (x_1 + mu); tau = 2 v_1^2 /
 // (sigma + v_1^2); v = x / v_1; then H x = mu e_1, so the diagonal of R is
-// nonnegative.  sigma = 0: tau = 0 (x_1 >= 0) or tau = 2 with v = e_1 (x_1 < 0).
+// nonnegative.  sigma = 0: tau = 0 (x_1 >= 0) or tau = 2 (x_1 < 0), v = e_1 (the
+// stored entries below the pivot are set to zero).  Squares that underflow
+// (|a| below about 1e-154) count as zero: columns of such entries only are
+// outside the range of this factorization.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -97,6 +101,8 @@ __global__ void __launch_bounds__(kPanelThreads) qr_panel_kernel(int64_t m, int6
       const dd v1 = s_scale;
       for (int64_t r = r0 + 1 + tid; r < m; r += kPanelThreads)
         std_(A, plane, r * n + cj, dd_div(ldd(A, plane, r * n + cj), v1));
+    } else {  // v = e_1: the stored vector is zero below the pivot
+      for (int64_t r = r0 + 1 + tid; r < m; r += kPanelThreads) std_(A, plane, r * n + cj, dd{0.0, 0.0});
     }
     __syncthreads();
     if (mode == 0) continue;  // H_j = I
@@ -131,6 +137,156 @@ __global__ void __launch_bounds__(kPanelThreads) qr_panel_kernel(int64_t m, int6
   }
 }
 
+// Tall panels (more than kSmallPanel rows) are factored by many workgroups, two
+// launches per column, each workgroup owning kPanelRows consecutive panel rows:
+//   qr_col_update_kernel(j): apply H_{j-1} to columns j .. jb-1 of the block's
+//     rows (w from the partial dot products of the previous launch), then write
+//     the block's part of sigma_j (rows below the pivot) and, from the block
+//     that holds the pivot row, x1 = a(r0, j);
+//   qr_col_reflect_kernel(j): every block forms sigma_j from all partials in the
+//     same order and the Householder scalars from it (so all blocks agree bit for
+//     bit), block 0 writes the diagonal and tau_j, each block scales its rows of
+//     column j into v and writes its partial dot products v^T a_c (c > j), the
+//     pivot row entering with v = 1.
+// Every block writes all of its partial slots (zeros when it holds no row at or
+// below the pivot), so the sums never read a stale slot.
+constexpr int kPanelRows = 64;
+constexpr int kColThreads = 256;  // 32 column lanes x 8 row groups
+constexpr int64_t kSmallPanel = 256;
+
+__device__ inline dd block_sum256(dd v, dd* red) {
+  const int tid = threadIdx.x;
+  red[tid] = v;
+  __syncthreads();
+  for (int s = kColThreads / 2; s > 0; s >>= 1) {
+    if (tid < s) red[tid] = dd_add(red[tid], red[tid + s]);
+    __syncthreads();
+  }
+  const dd r = red[0];
+  __syncthreads();
+  return r;
+}
+
+__global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, int64_t n, int64_t j0, int jb, int j,
+                                                                    double* __restrict__ A,
+                                                                    const double* __restrict__ tau,
+                                                                    double* __restrict__ psig,
+                                                                    const double* __restrict__ pw,
+                                                                    double* __restrict__ px1) {
+  __shared__ dd red[kColThreads];
+  __shared__ dd tw[kMaxNb];
+  const int64_t plane = m * n;
+  const int tid = threadIdx.x, cc = tid & 31, rg = tid >> 5;
+  const int64_t G = gridDim.x;
+  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kPanelRows, re = min(m, rb + kPanelRows);
+  if (j > 0) {
+    // w_c = tau_{j-1} sum_b pw[b][c - j] for c = j + cc: the same order in every block
+    dd s = {0.0, 0.0};
+    for (int64_t b = rg; b < G; b += 8) s = dd_add(s, ldd(pw, G * kMaxNb, b * kMaxNb + cc));
+    red[tid] = s;
+    __syncthreads();
+    if (rg == 0) {
+      dd w = red[cc];
+      for (int g = 1; g < 8; ++g) w = dd_add(w, red[g * 32 + cc]);
+      tw[cc] = dd_mul(ldd(tau, n, j0 + j - 1), w);
+    }
+    __syncthreads();
+    const int64_t rp = j0 + j - 1;  // the previous pivot row (v = 1 there)
+    const int c = j + cc;
+    if (c < jb) {
+      const dd t = tw[cc];
+      for (int64_t r = rb + rg; r < re; r += 8) {
+        if (r < rp) continue;
+        const dd v = r == rp ? dd{1.0, 0.0} : ldd(A, plane, r * n + j0 + j - 1);
+        const int64_t idx = r * n + j0 + c;
+        std_(A, plane, idx, dd_sub(ldd(A, plane, idx), dd_mul(t, v)));
+      }
+    }
+    __syncthreads();  // the block's writes of column j before its sum of squares
+  }
+  const int64_t r0 = j0 + j;
+  dd part = {0.0, 0.0};
+  if (tid < kPanelRows) {
+    const int64_t r = rb + tid;
+    if (r > r0 && r < re) {
+      const dd a = ldd(A, plane, r * n + j0 + j);
+      part = dd_mul(a, a);
+    }
+    if (r == r0) std_(px1, kMaxNb, j, ldd(A, plane, r * n + j0 + j));
+  }
+  const dd sig = block_sum256(part, red);
+  if (tid == 0) std_(psig, G, blockIdx.x, sig);
+}
+
+__global__ void __launch_bounds__(kColThreads) qr_col_reflect_kernel(int64_t m, int64_t n, int64_t j0, int jb, int j,
+                                                                     double* __restrict__ A, double* __restrict__ tau,
+                                                                     const double* __restrict__ psig,
+                                                                     double* __restrict__ pw,
+                                                                     const double* __restrict__ px1) {
+  __shared__ dd red[kColThreads];
+  __shared__ dd vs[kPanelRows];
+  __shared__ dd s_scale, s_tau;
+  __shared__ int s_mode;
+  const int64_t plane = m * n;
+  const int tid = threadIdx.x, cc = tid & 31, rg = tid >> 5;
+  const int64_t G = gridDim.x;
+  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kPanelRows, re = min(m, rb + kPanelRows);
+  const int64_t r0 = j0 + j;
+  dd part = {0.0, 0.0};
+  for (int64_t b = tid; b < G; b += kColThreads) part = dd_add(part, ldd(psig, G, b));
+  const dd sigma = block_sum256(part, red);
+  if (tid == 0) {
+    const dd x1 = ldd(px1, kMaxNb, j);
+    dd diag;
+    if (sigma.hi == 0.0) {
+      s_mode = x1.hi < 0.0 ? 1 : 0;
+      s_tau = s_mode ? dd{2.0, 0.0} : dd{0.0, 0.0};
+      diag = s_mode ? dd_neg(x1) : x1;
+    } else {
+      const dd mu = dd_sqrt(dd_add(dd_mul(x1, x1), sigma));
+      const dd v1 = x1.hi <= 0.0 ? dd_sub(x1, mu) : dd_neg(dd_div(sigma, dd_add(x1, mu)));
+      const dd v1sq = dd_mul(v1, v1);
+      s_tau = dd_div(dd_mul_d(v1sq, 2.0), dd_add(sigma, v1sq));
+      s_scale = v1;
+      s_mode = 2;
+      diag = mu;
+    }
+    if (blockIdx.x == 0) {
+      std_(A, plane, r0 * n + j0 + j, diag);
+      std_(tau, n, j0 + j, s_tau);
+    }
+  }
+  __syncthreads();
+  const int mode = s_mode;
+  if (tid < kPanelRows) {
+    const int64_t r = rb + tid;
+    dd v = {0.0, 0.0};
+    if (r == r0) {
+      v = {1.0, 0.0};
+    } else if (r > r0 && r < re) {
+      // mode 2: v = x / v1; otherwise v = e_1, zero below the pivot
+      v = mode == 2 ? dd_div(ldd(A, plane, r * n + j0 + j), s_scale) : dd{0.0, 0.0};
+      std_(A, plane, r * n + j0 + j, v);
+    }
+    vs[tid] = v;
+  }
+  __syncthreads();
+  // partial w_c = v^T a_c over the block's rows at or below the pivot, c = j + 1 + cc
+  const int c = j + 1 + cc;
+  dd acc = {0.0, 0.0};
+  if (c < jb) {
+    for (int64_t r = rb + rg; r < re; r += 8)
+      if (r >= r0) acc = dd_add(acc, dd_mul(vs[r - rb], ldd(A, plane, r * n + j0 + c)));
+  }
+  red[tid] = acc;
+  __syncthreads();
+  if (rg == 0) {
+    dd w = red[cc];
+    for (int g = 1; g < 8; ++g) w = dd_add(w, red[g * 32 + cc]);
+    std_(pw, G * kMaxNb, static_cast<int64_t>(blockIdx.x) * kMaxNb + cc, w);
+  }
+}
+
 // V (mp x jb, dense: 1 on the diagonal, the stored vectors below, 0 above) and
 // its transpose Vt (jb x mp), from the factored panel; rows of the panel start
 // at row j0 of A.
@@ -151,20 +307,24 @@ __global__ void __launch_bounds__(256) qr_pack_v_kernel(int64_t m, int64_t n, in
 
 // T (upper triangular, jb x jb) of I - V T V^T = H_0 ... H_{jb-1} from
 // G = V^T V and tau: T(j, j) = tau_j, T(0:j, j) = -tau_j T(0:j, 0:j) G(0:j, j);
-// writes the transpose Tt.  One wave, serial in j.
+// writes the transpose Tt.  One wave, serial in j, G staged in LDS.
 __global__ void __launch_bounds__(64) qr_t_kernel(int jb, int64_t n, int64_t j0, const double* __restrict__ G,
                                                   const double* __restrict__ tau, double* __restrict__ Tt) {
   __shared__ dd T[kMaxNb][kMaxNb];
+  __shared__ dd Gs[kMaxNb][kMaxNb];
   const int i = threadIdx.x;
   const int64_t pg = static_cast<int64_t>(jb) * jb;
   if (i < kMaxNb)
-    for (int c = 0; c < kMaxNb; ++c) T[i][c] = {0.0, 0.0};
+    for (int c = 0; c < kMaxNb; ++c) {
+      T[i][c] = {0.0, 0.0};
+      Gs[i][c] = (i < jb && c < jb) ? ldd(G, pg, static_cast<int64_t>(i) * jb + c) : dd{0.0, 0.0};
+    }
   __syncthreads();
   for (int j = 0; j < jb; ++j) {
     const dd tj = ldd(tau, n, j0 + j);
     dd s = {0.0, 0.0};
     if (i < j) {
-      for (int l = i; l < j; ++l) s = dd_add(s, dd_mul(T[i][l], ldd(G, pg, static_cast<int64_t>(l) * jb + j)));
+      for (int l = i; l < j; ++l) s = dd_add(s, dd_mul(T[i][l], Gs[l][j]));
     }
     __syncthreads();
     if (i < j) T[i][j] = dd_neg(dd_mul(tj, s));
@@ -203,8 +363,18 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // Workspace parts of the QR: V, Vt, G (V^T V), Tt, X (trailing block), W, W2, P,
 // then the workspace of the largest mdgemm_ex call.
 struct QrLayout {
-  size_t v = 0, vt = 0, g = 0, tt = 0, x = 0, w = 0, w2 = 0, p = 0, gemm = 0, gemm_bytes = 0, total = 0;
+  size_t v = 0, vt = 0, g = 0, tt = 0, x = 0, w = 0, w2 = 0, p = 0, psig = 0, pw = 0, px1 = 0, gemm = 0,
+         gemm_bytes = 0, total = 0;
 };
+
+// The options of the trailing products: the adaptive digit width (fewer, wider
+// digits whose level sums stay exact at the product's k), default cutoff.
+mdgemm_opts qr_gemm_opts() {
+  mdgemm_opts o;
+  mdgemm_opts_init(&o);
+  o.slice_bits = MDGEMM_SLICE_BITS_AUTO;
+  return o;
+}
 
 bool qr_layout(int64_t m, int64_t n, int nb, QrLayout* L) {
   const size_t dd_bytes = 2 * sizeof(double);
@@ -229,14 +399,23 @@ bool qr_layout(int64_t m, int64_t n, int nb, QrLayout* L) {
   off += wbytes;
   L->p = off;
   off += xbytes;
+  // partial sums of the multi-workgroup panel: sigma [G], w [G][32], x1 [32]
+  const size_t groups = static_cast<size_t>((m + kPanelRows - 1) / kPanelRows);
+  L->psig = off;
+  off += align256(dd_bytes * groups);
+  L->pw = off;
+  off += align256(dd_bytes * groups * kMaxNb);
+  L->px1 = off;
+  off += align256(dd_bytes * kMaxNb);
   // the largest workspace of the four products of any panel: V^T V, V^T X, T^T W, V W2
+  mdgemm_opts o = qr_gemm_opts();
   size_t need = 0;
   for (int64_t j0 = 0; j0 < n; j0 += nb) {
     const int64_t jb = std::min<int64_t>(nb, n - j0), mp = m - j0, nc = n - j0 - jb;
-    const size_t c[4] = {mdgemm_workspace_bytes(jb, jb, mp, 2, nullptr),
-                         nc ? mdgemm_workspace_bytes(jb, nc, mp, 2, nullptr) : 0,
-                         nc ? mdgemm_workspace_bytes(jb, nc, jb, 2, nullptr) : 0,
-                         nc ? mdgemm_workspace_bytes(mp, nc, jb, 2, nullptr) : 0};
+    const size_t c[4] = {mdgemm_workspace_bytes(jb, jb, mp, 2, &o),
+                         nc ? mdgemm_workspace_bytes(jb, nc, mp, 2, &o) : 0,
+                         nc ? mdgemm_workspace_bytes(jb, nc, jb, 2, &o) : 0,
+                         nc ? mdgemm_workspace_bytes(mp, nc, jb, 2, &o) : 0};
     for (size_t x : c) {
       if (x == SIZE_MAX) return false;
       need = std::max(need, x);
@@ -284,15 +463,27 @@ int mdgemm_qr_dd(int64_t m, int64_t n, int nb, double* A, double* tau, void* wor
   double* W = reinterpret_cast<double*>(ws + L.w);
   double* W2 = reinterpret_cast<double*>(ws + L.w2);
   double* P = reinterpret_cast<double*>(ws + L.p);
-  mdgemm_opts o;
-  mdgemm_opts_init(&o);
+  double* psig = reinterpret_cast<double*>(ws + L.psig);
+  double* pw = reinterpret_cast<double*>(ws + L.pw);
+  double* px1 = reinterpret_cast<double*>(ws + L.px1);
+  mdgemm_opts o = mdg::qr_gemm_opts();
   o.stream = stream;
   o.workspace = ws + L.gemm;
   o.workspace_bytes = L.gemm_bytes;
   for (int64_t j0 = 0; j0 < n; j0 += nb) {
     const int jb = static_cast<int>(std::min<int64_t>(nb, n - j0));
     const int64_t mp = m - j0, c0 = j0 + jb, nc = n - c0;
-    hipLaunchKernelGGL(mdg::qr_panel_kernel, dim3(1), dim3(mdg::kPanelThreads), 0, s, m, n, j0, jb, A, tau);
+    if (mp <= mdg::kSmallPanel) {
+      hipLaunchKernelGGL(mdg::qr_panel_kernel, dim3(1), dim3(mdg::kPanelThreads), 0, s, m, n, j0, jb, A, tau);
+    } else {
+      const unsigned groups = static_cast<unsigned>((mp + mdg::kPanelRows - 1) / mdg::kPanelRows);
+      for (int j = 0; j < jb; ++j) {
+        hipLaunchKernelGGL(mdg::qr_col_update_kernel, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0, jb, j, A,
+                           tau, psig, pw, px1);
+        hipLaunchKernelGGL(mdg::qr_col_reflect_kernel, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0, jb, j,
+                           A, tau, psig, pw, px1);
+      }
+    }
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     if (nc == 0) break;
     hipLaunchKernelGGL(mdg::qr_pack_v_kernel, dim3(mdg::blocks_for(mp * jb)), dim3(256), 0, s, m, n, j0, jb, A, V,

@@ -25,7 +25,8 @@ DEV = torch.device("cuda:0")
 
 
 @pytest.mark.parametrize("m,n,nb,seed", [(256, 128, 32, 1), (300, 173, 32, 2), (64, 64, 16, 3), (129, 1, 8, 4),
-                                         (100, 37, 7, 5), (520, 96, 32, 6)])
+                                         (100, 37, 7, 5), (520, 96, 32, 6), (1100, 300, 32, 7), (700, 700, 32, 8),
+                                         (1000, 61, 13, 9)])
 def test_qr_dd_against_the_oracle(m, n, nb, seed):
     print(f"[case] qr dd {m}x{n} nb={nb}", flush=True)
     rng = np.random.default_rng(seed)
