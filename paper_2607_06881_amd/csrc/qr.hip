@@ -305,6 +305,46 @@ __global__ void __launch_bounds__(256) qr_pack_v_kernel(int64_t m, int64_t n, in
   std_(Vt, planeV, static_cast<int64_t>(c) * mp + i, v);
 }
 
+// G = V^T V (jb x jb) of the factored panel, in double-double arithmetic, in
+// two launches: workgroups of kPanelRows rows stage their rows of V (1 on the
+// diagonal, the stored vectors below, 0 above) in LDS and write the partial sums
+// of all 32 x 32 entries (four per thread); one workgroup of 1024 threads then
+// adds the partials of each entry in workgroup order and writes G [2][jb][jb].
+__global__ void __launch_bounds__(kColThreads) qr_gram_partial_kernel(int64_t m, int64_t n, int64_t j0, int jb,
+                                                                      const double* __restrict__ A,
+                                                                      double* __restrict__ pg) {
+  __shared__ dd Vs[kPanelRows][kMaxNb + 1];
+  const int64_t plane = m * n, G = gridDim.x;
+  const int tid = threadIdx.x;
+  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kPanelRows;
+  for (int e = tid; e < kPanelRows * kMaxNb; e += kColThreads) {
+    const int rr = e >> 5, c = e & 31;
+    const int64_t r = rb + rr;
+    dd v = {0.0, 0.0};
+    if (r < m && c < jb) {
+      if (r == j0 + c) v = {1.0, 0.0};
+      else if (r > j0 + c) v = ldd(A, plane, r * n + j0 + c);
+    }
+    Vs[rr][c] = v;
+  }
+  __syncthreads();
+  for (int q = 0; q < 4; ++q) {
+    const int e = tid + kColThreads * q, l = e >> 5, c = e & 31;
+    dd s = {0.0, 0.0};
+    for (int rr = 0; rr < kPanelRows; ++rr) s = dd_add(s, dd_mul(Vs[rr][l], Vs[rr][c]));
+    std_(pg, G * kMaxNb * kMaxNb, static_cast<int64_t>(blockIdx.x) * kMaxNb * kMaxNb + e, s);
+  }
+}
+
+__global__ void __launch_bounds__(kMaxNb * kMaxNb) qr_gram_reduce_kernel(int jb, int64_t groups,
+                                                                         const double* __restrict__ pg,
+                                                                         double* __restrict__ Gout) {
+  const int e = threadIdx.x, l = e >> 5, c = e & 31;
+  dd s = {0.0, 0.0};
+  for (int64_t b = 0; b < groups; ++b) s = dd_add(s, ldd(pg, groups * kMaxNb * kMaxNb, b * kMaxNb * kMaxNb + e));
+  if (l < jb && c < jb) std_(Gout, static_cast<int64_t>(jb) * jb, static_cast<int64_t>(l) * jb + c, s);
+}
+
 // T (upper triangular, jb x jb) of I - V T V^T = H_0 ... H_{jb-1} from
 // G = V^T V and tau: T(j, j) = tau_j, T(0:j, j) = -tau_j T(0:j, 0:j) G(0:j, j);
 // writes the transpose Tt.  One wave, serial in j, G staged in LDS.
@@ -363,7 +403,7 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // Workspace parts of the QR: V, Vt, G (V^T V), Tt, X (trailing block), W, W2, P,
 // then the workspace of the largest mdgemm_ex call.
 struct QrLayout {
-  size_t v = 0, vt = 0, g = 0, tt = 0, x = 0, w = 0, w2 = 0, p = 0, psig = 0, pw = 0, px1 = 0, gemm = 0,
+  size_t v = 0, vt = 0, g = 0, tt = 0, x = 0, w = 0, w2 = 0, p = 0, psig = 0, pw = 0, px1 = 0, pgram = 0, gemm = 0,
          gemm_bytes = 0, total = 0;
 };
 
@@ -407,13 +447,14 @@ bool qr_layout(int64_t m, int64_t n, int nb, QrLayout* L) {
   off += align256(dd_bytes * groups * kMaxNb);
   L->px1 = off;
   off += align256(dd_bytes * kMaxNb);
-  // the largest workspace of the four products of any panel: V^T V, V^T X, T^T W, V W2
+  L->pgram = off;
+  off += align256(dd_bytes * groups * kMaxNb * kMaxNb);
+  // the largest workspace of the three products of any panel: V^T X, T^T W, V W2
   mdgemm_opts o = qr_gemm_opts();
   size_t need = 0;
   for (int64_t j0 = 0; j0 < n; j0 += nb) {
     const int64_t jb = std::min<int64_t>(nb, n - j0), mp = m - j0, nc = n - j0 - jb;
-    const size_t c[4] = {mdgemm_workspace_bytes(jb, jb, mp, 2, &o),
-                         nc ? mdgemm_workspace_bytes(jb, nc, mp, 2, &o) : 0,
+    const size_t c[3] = {nc ? mdgemm_workspace_bytes(jb, nc, mp, 2, &o) : 0,
                          nc ? mdgemm_workspace_bytes(jb, nc, jb, 2, &o) : 0,
                          nc ? mdgemm_workspace_bytes(mp, nc, jb, 2, &o) : 0};
     for (size_t x : c) {
@@ -466,6 +507,7 @@ int mdgemm_qr_dd(int64_t m, int64_t n, int nb, double* A, double* tau, void* wor
   double* psig = reinterpret_cast<double*>(ws + L.psig);
   double* pw = reinterpret_cast<double*>(ws + L.pw);
   double* px1 = reinterpret_cast<double*>(ws + L.px1);
+  double* pgram = reinterpret_cast<double*>(ws + L.pgram);
   mdgemm_opts o = mdg::qr_gemm_opts();
   o.stream = stream;
   o.workspace = ws + L.gemm;
@@ -491,8 +533,14 @@ int mdgemm_qr_dd(int64_t m, int64_t n, int nb, double* A, double* tau, void* wor
     hipLaunchKernelGGL(mdg::qr_pack_block_kernel, dim3(mdg::blocks_for(mp * nc)), dim3(256), 0, s, m, n, j0, c0, A,
                        X);
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
-    int st = mdgemm_ex(jb, jb, mp, 2, Vt, V, G, &o);  // G = V^T V
-    if (st != MDGEMM_OK) return st;
+    // G = V^T V (double-double dot products over the panel's rows)
+    const unsigned groups = static_cast<unsigned>((mp + mdg::kPanelRows - 1) / mdg::kPanelRows);
+    hipLaunchKernelGGL(mdg::qr_gram_partial_kernel, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0, jb, A,
+                       pgram);
+    hipLaunchKernelGGL(mdg::qr_gram_reduce_kernel, dim3(1), dim3(mdg::kMaxNb * mdg::kMaxNb), 0, s, jb,
+                       static_cast<int64_t>(groups), pgram, G);
+    if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
+    int st = MDGEMM_OK;
     hipLaunchKernelGGL(mdg::qr_t_kernel, dim3(1), dim3(64), 0, s, jb, n, j0, G, tau, Tt);
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     if ((st = mdgemm_ex(jb, nc, mp, 2, Vt, X, W, &o)) != MDGEMM_OK) return st;   // W = V^T X
