@@ -31,10 +31,14 @@ Prints one JSON line:
 * ``exponent_classes`` (workloads with a range, c7): the same product grouped
   by exponent class over that range (section 3's balancing), timed over a few
   steps, with a sampled parity check against the oracle's grouped chain;
-* ``--extras`` adds ``karatsuba``, ``karatsuba_adaptive`` (the Karatsuba
-  schedule of the level products, bit-identical results), ``int8`` (the
-  level products on the int8 matrix cores) and ``sign_groups`` (section 3's
-  sign grouping, four products, the same limbs) lines;
+* ``karatsuba`` (the Karatsuba schedule of the level products: fewer
+  products, bit-identical limbs) and ``int8`` (the level products of 7-bit
+  digits on the int8 matrix cores, within the same error bound), a few timed
+  steps each beside the headline, which keeps the paper's separate pair
+  products on the FP64 matrix cores;
+* ``--extras`` adds ``karatsuba_adaptive``, ``sign_groups`` (section 3's
+  sign grouping, four products, the same limbs) and ``qr_dd`` (the
+  double-double Householder QR built on the product) lines;
 * ``cpu_baseline``: the CPU oracle's classic multiple-double GEMM (one
   sequential inner product per element, all host cores) timed on a bounded
   sample of the same product's rows.
@@ -559,10 +563,10 @@ def main(argv=None) -> int:
         # 13-bit digit pairs (and, on request, the Karatsuba schedule and the
         # int8 level products)
         out["adaptive_width"] = extra(mode_opts(md.MDGEMM_SLICE_BITS_AUTO), 0)
+        out["karatsuba"] = extra(mode_opts(13), md.MDGEMM_KARATSUBA)
+        out["int8"] = int8_mode()
         if args.extras:
-            out["karatsuba"] = extra(mode_opts(13), md.MDGEMM_KARATSUBA)
             out["karatsuba_adaptive"] = extra(mode_opts(md.MDGEMM_SLICE_BITS_AUTO), md.MDGEMM_KARATSUBA)
-            out["int8"] = int8_mode()
     def grouped(g_flags):
         """A few timed steps of the same workload as a grouped product (section 3's
         exponent classes over the workload's range, or sign groups), with a
