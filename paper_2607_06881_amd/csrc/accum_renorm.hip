@@ -208,6 +208,7 @@ hipError_t with_words(int words, F&& f) {
   else if (words <= 10) f(Words<10>{});
   else if (words <= 12) f(Words<12>{});
   else if (words <= 14) f(Words<14>{});
+  else if (words <= 15) f(Words<15>{});  // sixteen limbs at the default digits: 13 x 65 + 55 bits
   else if (words <= 20) f(Words<20>{});
   else if (words <= kZWords) f(Words<kZWords>{});
   else return hipErrorInvalidValue;
