@@ -181,6 +181,14 @@ typedef struct mdgemm_opts {
  * MDGEMM_CHECK_FINITE; MDGEMM_STAGED turns it off.  With MDGEMM_TIME_STAGES the
  * whole kernel counts as the level-product stage. */
 
+/* Logging.  With the environment variable MDGEMM_LOG=1 (read once per process)
+ * every call of mdgemm, mdgemm_ex, mdgemm_ex_noalloc and mdgemm_qr_dd writes one
+ * line to stderr when it returns: its sizes, the plan (w, S, T; "unplanned" for
+ * arguments that do not resolve), the flags, the workspace kind, the stream, the
+ * path taken (refused, empty, zero (k = 0), fused small product, staged: pair
+ * levels / karatsuba / grouped products, int8 levels) and the status string.
+ * MDGEMM_LOG=2 also logs the products a QR makes.  Unset or 0: silent. */
+
 /* Fill `opts` with the defaults: default stream, library workspace, the default
  * count S13(L) of 13-bit digits (slices_per_limb 0), cutoff T = S - 1, no range
  * balancing, no flags. */

@@ -14,6 +14,9 @@
 #include <climits>
 #include <cmath>
 #include <cstdint>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <memory>
@@ -848,12 +851,20 @@ int mdgemm_workspace_layout(int64_t m, int64_t n, int64_t k, int limbs, const md
   return nw;
 }
 
-int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
-              const mdgemm_opts* opts) {
+}  // extern "C"
+
+namespace {
+
+// The product; *path names the branch taken (for MDGEMM_LOG).
+int ex_impl(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
+            const mdgemm_opts* opts, const char** path) {
   Resolved r;
+  *path = "refused";
   if (m < 0 || n < 0 || k < 0) return MDGEMM_EINVAL;
   MDG_TRY(resolve(limbs, m, n, k, opts, &r));
+  *path = "empty";
   if (m == 0 || n == 0) return MDGEMM_OK;
+  *path = "refused";
   if (!C || (k > 0 && (!A || !B))) return MDGEMM_EINVAL;
   const size_t abytes = sizeof(double) * limbs * static_cast<size_t>(m) * static_cast<size_t>(k);
   const size_t bbytes = sizeof(double) * limbs * static_cast<size_t>(k) * static_cast<size_t>(n);
@@ -864,12 +875,16 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   const bool timed = (r.flags & MDGEMM_TIME_STAGES) != 0;
 
   if (k == 0) {
+    *path = "zero (k = 0)";
     MDG_TRY(hip_status(mdg::launch_zero_f64(C, static_cast<int64_t>(limbs) * m * n, s)));
     if (r.flags & MDGEMM_SYNC) MDG_TRY(hip_status(hipStreamSynchronize(s)));
     return MDGEMM_OK;
   }
 
-  if (r.flags & MDGEMM_INT8) return run_int8(m, n, k, limbs, A, B, C, opts, r);
+  if (r.flags & MDGEMM_INT8) {
+    *path = "int8 levels";
+    return run_int8(m, n, k, limbs, A, B, C, opts, r);
+  }
   const auto pl = planned_for(r.S, r.T, m, n, k, r.w, r.kind, group_code(r));
   if (!schedule_exact(pl->s, k, r.w)) return MDGEMM_EEXACT;
   Layout L;
@@ -882,6 +897,7 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   mdg::SmallLevelOwners owners{};
   if (small_plan(m, n, k, limbs, r, &kc, &owners)) {
     // the fused small-product kernel: no workspace
+    *path = "fused small product";
     std::unique_lock<std::mutex> tlock(timing().mu, std::defer_lock);
     if (timed) {
       tlock.lock();
@@ -897,6 +913,9 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
     if (r.flags & MDGEMM_SYNC) MDG_TRY(hip_status(hipStreamSynchronize(s)));
     return MDGEMM_OK;
   }
+  *path = r.kind == Kind::kGroups ? "staged: grouped products"
+          : (r.kind == Kind::kLevels ? "staged: pair levels"
+                                     : (r.kind == Kind::kPerPair ? "staged: per pair" : "staged: karatsuba"));
   char* ws = nullptr;
   LibraryBuffer lib;
   if (opts && opts->workspace) {
@@ -959,6 +978,55 @@ int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const
   return MDGEMM_OK;
 }
 
+// One line per call on stderr: the arguments, the plan, the branch and the status.
+void log_product(const char* entry, int64_t m, int64_t n, int64_t k, int limbs, const mdgemm_opts* opts,
+                 const char* ws, const char* path, int status) {
+  int w = 0, S = 0, T = 0;
+  const bool planned = mdgemm_plan(m, n, k, limbs, opts, &w, &S, &T) == MDGEMM_OK;
+  const unsigned flags = opts ? opts->flags : 0u;
+  char plan[64] = "unplanned";
+  if (planned) std::snprintf(plan, sizeof plan, "w=%d S=%d T=%d", w, S, T);
+  mdg::log_line("%s m=%lld n=%lld k=%lld limbs=%d %s flags=0x%x workspace=%s stream=%p path=%s -> %s", entry,
+                static_cast<long long>(m), static_cast<long long>(n), static_cast<long long>(k), limbs, plan, flags,
+                ws, opts ? opts->stream : nullptr, path, mdgemm_status_string(status));
+}
+
+}  // namespace
+
+namespace mdg {
+
+int log_level() {
+  static const int level = [] {
+    const char* v = std::getenv("MDGEMM_LOG");
+    return v ? std::atoi(v) : 0;
+  }();
+  return level;
+}
+
+thread_local int log_depth = 0;
+
+void log_line(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  std::fprintf(stderr, "[mdgemm] %s\n", buf);
+}
+
+}  // namespace mdg
+
+extern "C" {
+
+int mdgemm_ex(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
+              const mdgemm_opts* opts) {
+  const char* path = "refused";
+  const int st = ex_impl(m, n, k, limbs, A, B, C, opts, &path);
+  if (mdg::log_level() > mdg::log_depth)
+    log_product("mdgemm_ex", m, n, k, limbs, opts, opts && opts->workspace ? "caller" : "library", path, st);
+  return st;
+}
+
 int mdgemm(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C) {
   return mdgemm_ex(m, n, k, limbs, A, B, C, nullptr);
 }
@@ -998,10 +1066,11 @@ int noalloc_scratch(void** out) {
 
 }  // namespace
 
-extern "C" {
+namespace {
 
-int mdgemm_ex_noalloc(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
-                      const mdgemm_opts* opts) {
+int noalloc_impl(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
+                 const mdgemm_opts* opts, const char** path) {
+  *path = "refused";
   mdgemm_opts o;
   if (opts) {
     o = *opts;
@@ -1023,7 +1092,20 @@ int mdgemm_ex_noalloc(int64_t m, int64_t n, int64_t k, int limbs, const double* 
   MDG_TRY(noalloc_scratch(&p));
   o.workspace = p;
   o.workspace_bytes = MDGEMM_NOALLOC_MAX_BYTES;
-  return mdgemm_ex(m, n, k, limbs, A, B, C, &o);
+  return ex_impl(m, n, k, limbs, A, B, C, &o, path);
+}
+
+}  // namespace
+
+extern "C" {
+
+int mdgemm_ex_noalloc(int64_t m, int64_t n, int64_t k, int limbs, const double* A, const double* B, double* C,
+                      const mdgemm_opts* opts) {
+  const char* path = "refused";
+  const int st = noalloc_impl(m, n, k, limbs, A, B, C, opts, &path);
+  if (mdg::log_level() > mdg::log_depth)
+    log_product("mdgemm_ex_noalloc", m, n, k, limbs, opts, "scratch array", path, st);
+  return st;
 }
 
 int mdgemm_stage_times(float* ms, int count) {

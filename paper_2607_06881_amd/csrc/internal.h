@@ -43,6 +43,13 @@ struct GemmJobs {
 };
 
 // a1: per-row (axis 0) or per-column (axis 1) grid exponents of a [rows][cols] plane.
+// MDGEMM_LOG (environment, read once): 0 or unset, silent; 1, one stderr line per
+// call of mdgemm_ex, mdgemm_ex_noalloc and mdgemm_qr_dd; 2, also the products a
+// QR makes.  log_depth is the nesting of the calling thread (the QR raises it).
+int log_level();
+extern thread_local int log_depth;
+void log_line(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
+
 hipError_t launch_exponents(int64_t rows, int64_t cols, int axis, const double* X0, int32_t* E, hipStream_t stream);
 // The exponents of A's rows (EA) and of B's columns (EB) in one pass over both
 // leading limbs; scratch (cy n int32 partial maxima, cy <= ceil(k / 64)) is

@@ -481,8 +481,12 @@ size_t mdgemm_qr_dd_workspace_bytes(int64_t m, int64_t n, int nb) {
   return mdg::qr_layout(m, n, nb, &L) ? L.total : SIZE_MAX;
 }
 
-int mdgemm_qr_dd(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspace, size_t workspace_bytes,
-                 void* stream) {
+}  // extern "C"
+
+namespace {
+
+int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspace, size_t workspace_bytes,
+            void* stream) {
   if (m < 1 || n < 1 || m < n || nb < 1 || nb > mdg::kMaxNb || !A || !tau || !workspace) return MDGEMM_EINVAL;
   if (m > (int64_t{1} << 20) || n > (int64_t{1} << 20)) return MDGEMM_EINVAL;
   mdg::QrLayout L;
@@ -550,6 +554,22 @@ int mdgemm_qr_dd(int64_t m, int64_t n, int nb, double* A, double* tau, void* wor
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
   }
   return MDGEMM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mdgemm_qr_dd(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspace, size_t workspace_bytes,
+                 void* stream) {
+  // the products inside log at MDGEMM_LOG=2 only
+  ++mdg::log_depth;
+  const int st = qr_impl(m, n, nb, A, tau, workspace, workspace_bytes, stream);
+  --mdg::log_depth;
+  if (mdg::log_level() > mdg::log_depth)
+    mdg::log_line("mdgemm_qr_dd m=%lld n=%lld nb=%d workspace=%zu stream=%p -> %s", static_cast<long long>(m),
+                  static_cast<long long>(n), nb, workspace_bytes, stream, mdgemm_status_string(st));
+  return st;
 }
 
 }  // extern "C"
