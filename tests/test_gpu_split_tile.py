@@ -92,3 +92,30 @@ def test_split_tile_fp32_panels_of_mdgemm_ex(L, bits):
     wantB = _panel_from_oracle(coracle.split(B, EB, S, 1, bits=w), 1, kp, np_)
     assert np.array_equal(parts["DA"][:S].cpu().numpy().astype(np.float64), wantA)
     assert np.array_equal(parts["DB"][:S].cpu().numpy().astype(np.float64), wantB)
+
+
+@pytest.mark.parametrize("k", [2100, 64])
+def test_staged_path_with_operands_off_16_byte_alignment(k):
+    # the same product through views of A and B that start 8 bytes into their
+    # buffers (the exponent pass then reads A's rows with 8-byte loads): the
+    # exponents equal the oracle's and C equals the aligned product's bit for bit
+    m, n, L = 1000, 1000, 2
+    print(f"[case] staged product on operands 8 bytes off alignment, k={k}", flush=True)
+    A = _operand(L, m, k, 31)
+    B = _operand(L, k, n, 32)
+    Ag, Bg = torch.from_numpy(A).to(DEV), torch.from_numpy(B).to(DEV)
+    bufA = torch.empty(A.size + 1, dtype=torch.float64, device=DEV)
+    bufB = torch.empty(B.size + 1, dtype=torch.float64, device=DEV)
+    Au, Bu = bufA[1:].view(L, m, k), bufB[1:].view(L, k, n)
+    Au.copy_(Ag)
+    Bu.copy_(Bg)
+    assert Au.data_ptr() % 16 == 8 and Bu.data_ptr() % 16 == 8
+    ws = torch.empty(md.mdgemm_workspace_bytes(m, n, k, L), dtype=torch.uint8, device=DEV)
+    C = md.mdgemm_ex(Au, Bu, workspace=ws, flags=md.MDGEMM_STAGED)
+    torch.cuda.synchronize()
+    parts = md.workspace_parts(ws, m, n, k, L, flags=md.MDGEMM_STAGED)
+    assert np.array_equal(parts["EA"].cpu().numpy(), coracle.exponents(A[0], 0))
+    assert np.array_equal(parts["EB"].cpu().numpy(), coracle.exponents(B[0], 1))
+    C0 = md.mdgemm_ex(Ag, Bg, flags=md.MDGEMM_STAGED)
+    torch.cuda.synchronize()
+    assert torch.equal(C, C0)
