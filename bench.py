@@ -161,7 +161,7 @@ def stage_probes(md, torch, dev, stream, mixes, reps=3):
     return out
 
 
-def qr_dd_line(md, torch, dev, stream, A, no_cpu, nb=32, reps=3):
+def qr_dd_line(md, torch, dev, stream, A, no_cpu, nb=64, reps=3):
     """The downstream use: blocked Householder QR (mdgemm_qr_dd) of the
     workload's double-double A, and of its leading 1024 x 1024 block.  Rate in
     effective double-double flops, 2 m n^2 - 2 n^3 / 3 per factorization (each

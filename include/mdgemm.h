@@ -444,14 +444,14 @@ int mdgemm_accum_renorm(int64_t m, int64_t n, int limbs, int levels, int slice_b
  * double-double matrix, with the trailing updates of each panel on mdgemm_ex. */
 
 /* Workspace bytes of mdgemm_qr_dd (SIZE_MAX for invalid arguments: m >= n >= 1,
- * nb in 1..32, m and n at most 2^20). */
+ * nb in 1..64, m and n at most 2^20). */
 size_t mdgemm_qr_dd_workspace_bytes(int64_t m, int64_t n, int nb);
 
 /* Householder QR of A [2][m][n] (double-double, limb-major, m >= n), in place:
  * A = Q R with Q = H_0 ... H_{n-1}, H_j = I - tau_j v_j v_j^T, v_j(j) = 1 and
  * v_j zero above row j.  On return A holds R on and above the diagonal (R(j, j)
  * >= 0) and v_j below it (LAPACK's convention), tau [2][n] the tau_j (all in
- * double-double).  Panels of nb columns (1..32) are factored in double-double
+ * double-double).  Panels of nb columns (1..64) are factored in double-double
  * arithmetic (Golub and Van Loan's Householder vector; one workgroup for panels
  * of at most 256 rows, else workgroups of 64 rows with two launches per column);
  * each panel's reflections are accumulated as I - V T V^T (T upper triangular)

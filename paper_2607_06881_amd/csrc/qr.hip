@@ -4,7 +4,7 @@
 //
 // A [2][m][n] (limb-major double-double, m >= n) is factored as A = Q R with
 // Q = H_0 H_1 ... H_{n-1}, H_j = I - tau_j v_j v_j^T (Householder reflections,
-// v_j(j) = 1, v_j zero above row j).  Panels of nb <= 32 columns are factored in
+// v_j(j) = 1, v_j zero above row j).  Panels of nb <= 64 columns are factored in
 // double-double arithmetic (dd.h), by one workgroup for short panels and by many
 // for tall ones (see qr_col_update_kernel); the panel's reflections are
 // accumulated in the compact form I - V T V^T (T upper triangular, the forward
@@ -26,6 +26,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <mutex>
 
 #include "dd.h"
 #include "internal.h"
@@ -35,7 +36,7 @@ namespace mdg {
 namespace {
 
 constexpr int kPanelThreads = 1024;
-constexpr int kMaxNb = 32;
+constexpr int kMaxNb = 64;  // panel width; the kernels take its columns 32 at a time
 
 __device__ inline dd ldd(const double* P, int64_t plane, int64_t idx) { return {P[idx], P[plane + idx]}; }
 __device__ inline void std_(double* P, int64_t plane, int64_t idx, dd v) {
@@ -107,29 +108,34 @@ __global__ void __launch_bounds__(kPanelThreads) qr_panel_kernel(int64_t m, int6
     __syncthreads();
     if (mode == 0) continue;  // H_j = I
     const dd t = s_tau;
-    // w_c = v^T a_c for the remaining columns c = j + 1 + cc (v(r0) = 1)
-    const int c = j + 1 + cc;
-    dd acc = {0.0, 0.0};
-    if (c < jb && mode == 2) {
-      for (int64_t r = r0 + 1 + rg; r < m; r += 32)
-        acc = dd_add(acc, dd_mul(ldd(A, plane, r * n + cj), ldd(A, plane, r * n + j0 + c)));
+    // w_c = v^T a_c for the remaining columns c = j + 1 + g0 + cc, 32 at a time (v(r0) = 1)
+    for (int g0 = 0; g0 < jb - j - 1; g0 += 32) {
+      const int c = j + 1 + g0 + cc;
+      dd acc = {0.0, 0.0};
+      if (c < jb && mode == 2) {
+        for (int64_t r = r0 + 1 + rg; r < m; r += 32)
+          acc = dd_add(acc, dd_mul(ldd(A, plane, r * n + cj), ldd(A, plane, r * n + j0 + c)));
+      }
+      red[tid] = acc;
+      __syncthreads();
+      if (rg == 0 && c < jb) {
+        dd w = ldd(A, plane, r0 * n + j0 + c);
+        for (int g = 0; g < 32; ++g) w = dd_add(w, red[g * 32 + cc]);
+        wv[g0 + cc] = dd_mul(t, w);
+      }
+      __syncthreads();
     }
-    red[tid] = acc;
-    __syncthreads();
-    if (rg == 0 && c < jb) {
-      dd w = ldd(A, plane, r0 * n + j0 + c);
-      for (int g = 0; g < 32; ++g) w = dd_add(w, red[g * 32 + cc]);
-      wv[cc] = dd_mul(t, w);
-    }
-    __syncthreads();
     // a_c <- a_c - tau w_c v
-    if (c < jb) {
-      const dd tw = wv[cc];
-      if (rg == 0) std_(A, plane, r0 * n + j0 + c, dd_sub(ldd(A, plane, r0 * n + j0 + c), tw));
-      if (mode == 2) {
-        for (int64_t r = r0 + 1 + rg; r < m; r += 32) {
-          const int64_t idx = r * n + j0 + c;
-          std_(A, plane, idx, dd_sub(ldd(A, plane, idx), dd_mul(tw, ldd(A, plane, r * n + cj))));
+    for (int g0 = 0; g0 < jb - j - 1; g0 += 32) {
+      const int c = j + 1 + g0 + cc;
+      if (c < jb) {
+        const dd tw = wv[g0 + cc];
+        if (rg == 0) std_(A, plane, r0 * n + j0 + c, dd_sub(ldd(A, plane, r0 * n + j0 + c), tw));
+        if (mode == 2) {
+          for (int64_t r = r0 + 1 + rg; r < m; r += 32) {
+            const int64_t idx = r * n + j0 + c;
+            std_(A, plane, idx, dd_sub(ldd(A, plane, idx), dd_mul(tw, ldd(A, plane, r * n + cj))));
+          }
         }
       }
     }
@@ -180,26 +186,32 @@ __global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, i
   const int64_t G = gridDim.x;
   const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kPanelRows, re = min(m, rb + kPanelRows);
   if (j > 0) {
-    // w_c = tau_{j-1} sum_b pw[b][c - j] for c = j + cc: the same order in every block
-    dd s = {0.0, 0.0};
-    for (int64_t b = rg; b < G; b += 8) s = dd_add(s, ldd(pw, G * kMaxNb, b * kMaxNb + cc));
-    red[tid] = s;
-    __syncthreads();
-    if (rg == 0) {
-      dd w = red[cc];
-      for (int g = 1; g < 8; ++g) w = dd_add(w, red[g * 32 + cc]);
-      tw[cc] = dd_mul(ldd(tau, n, j0 + j - 1), w);
+    // w_c = tau_{j-1} sum_b pw[b][c - j] for c = j + g0 + cc, 32 columns at a time:
+    // the same order in every block
+    const dd tprev = ldd(tau, n, j0 + j - 1);
+    for (int g0 = 0; g0 < jb - j; g0 += 32) {
+      dd s = {0.0, 0.0};
+      for (int64_t b = rg; b < G; b += 8) s = dd_add(s, ldd(pw, G * kMaxNb, b * kMaxNb + g0 + cc));
+      red[tid] = s;
+      __syncthreads();
+      if (rg == 0) {
+        dd w = red[cc];
+        for (int g = 1; g < 8; ++g) w = dd_add(w, red[g * 32 + cc]);
+        tw[g0 + cc] = dd_mul(tprev, w);
+      }
+      __syncthreads();
     }
-    __syncthreads();
     const int64_t rp = j0 + j - 1;  // the previous pivot row (v = 1 there)
-    const int c = j + cc;
-    if (c < jb) {
-      const dd t = tw[cc];
-      for (int64_t r = rb + rg; r < re; r += 8) {
-        if (r < rp) continue;
-        const dd v = r == rp ? dd{1.0, 0.0} : ldd(A, plane, r * n + j0 + j - 1);
-        const int64_t idx = r * n + j0 + c;
-        std_(A, plane, idx, dd_sub(ldd(A, plane, idx), dd_mul(t, v)));
+    for (int g0 = 0; g0 < jb - j; g0 += 32) {
+      const int c = j + g0 + cc;
+      if (c < jb) {
+        const dd t = tw[g0 + cc];
+        for (int64_t r = rb + rg; r < re; r += 8) {
+          if (r < rp) continue;
+          const dd v = r == rp ? dd{1.0, 0.0} : ldd(A, plane, r * n + j0 + j - 1);
+          const int64_t idx = r * n + j0 + c;
+          std_(A, plane, idx, dd_sub(ldd(A, plane, idx), dd_mul(t, v)));
+        }
       }
     }
     __syncthreads();  // the block's writes of column j before its sum of squares
@@ -271,19 +283,23 @@ __global__ void __launch_bounds__(kColThreads) qr_col_reflect_kernel(int64_t m, 
     vs[tid] = v;
   }
   __syncthreads();
-  // partial w_c = v^T a_c over the block's rows at or below the pivot, c = j + 1 + cc
-  const int c = j + 1 + cc;
-  dd acc = {0.0, 0.0};
-  if (c < jb) {
-    for (int64_t r = rb + rg; r < re; r += 8)
-      if (r >= r0) acc = dd_add(acc, dd_mul(vs[r - rb], ldd(A, plane, r * n + j0 + c)));
-  }
-  red[tid] = acc;
-  __syncthreads();
-  if (rg == 0) {
-    dd w = red[cc];
-    for (int g = 1; g < 8; ++g) w = dd_add(w, red[g * 32 + cc]);
-    std_(pw, G * kMaxNb, static_cast<int64_t>(blockIdx.x) * kMaxNb + cc, w);
+  // partial w_c = v^T a_c over the block's rows at or below the pivot, for
+  // c = j + 1 + g0 + cc, 32 columns at a time (slot g0 + cc)
+  for (int g0 = 0; g0 < jb - j - 1; g0 += 32) {
+    const int c = j + 1 + g0 + cc;
+    dd acc = {0.0, 0.0};
+    if (c < jb) {
+      for (int64_t r = rb + rg; r < re; r += 8)
+        if (r >= r0) acc = dd_add(acc, dd_mul(vs[r - rb], ldd(A, plane, r * n + j0 + c)));
+    }
+    red[tid] = acc;
+    __syncthreads();
+    if (rg == 0) {
+      dd w = red[cc];
+      for (int g = 1; g < 8; ++g) w = dd_add(w, red[g * 32 + cc]);
+      std_(pw, G * kMaxNb, static_cast<int64_t>(blockIdx.x) * kMaxNb + g0 + cc, w);
+    }
+    __syncthreads();
   }
 }
 
@@ -306,19 +322,21 @@ __global__ void __launch_bounds__(256) qr_pack_v_kernel(int64_t m, int64_t n, in
 }
 
 // G = V^T V (jb x jb) of the factored panel, in double-double arithmetic, in
-// two launches: workgroups of kPanelRows rows stage their rows of V (1 on the
+// two launches: workgroups of kGramRows rows stage their rows of V (1 on the
 // diagonal, the stored vectors below, 0 above) in LDS and write the partial sums
-// of all 32 x 32 entries (four per thread); one workgroup of 1024 threads then
-// adds the partials of each entry in workgroup order and writes G [2][jb][jb].
+// of all kMaxNb x kMaxNb entries; one workgroup of 1024 threads then adds the
+// partials of each entry in workgroup order and writes G [2][jb][jb].
+constexpr int kGramRows = 32;
+
 __global__ void __launch_bounds__(kColThreads) qr_gram_partial_kernel(int64_t m, int64_t n, int64_t j0, int jb,
                                                                       const double* __restrict__ A,
                                                                       double* __restrict__ pg) {
-  __shared__ dd Vs[kPanelRows][kMaxNb + 1];
+  __shared__ dd Vs[kGramRows][kMaxNb + 1];
   const int64_t plane = m * n, G = gridDim.x;
   const int tid = threadIdx.x;
-  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kPanelRows;
-  for (int e = tid; e < kPanelRows * kMaxNb; e += kColThreads) {
-    const int rr = e >> 5, c = e & 31;
+  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kGramRows;
+  for (int e = tid; e < kGramRows * kMaxNb; e += kColThreads) {
+    const int rr = e / kMaxNb, c = e % kMaxNb;
     const int64_t r = rb + rr;
     dd v = {0.0, 0.0};
     if (r < m && c < jb) {
@@ -328,51 +346,61 @@ __global__ void __launch_bounds__(kColThreads) qr_gram_partial_kernel(int64_t m,
     Vs[rr][c] = v;
   }
   __syncthreads();
-  for (int q = 0; q < 4; ++q) {
-    const int e = tid + kColThreads * q, l = e >> 5, c = e & 31;
+  for (int e = tid; e < kMaxNb * kMaxNb; e += kColThreads) {
+    const int l = e / kMaxNb, c = e % kMaxNb;
     dd s = {0.0, 0.0};
-    for (int rr = 0; rr < kPanelRows; ++rr) s = dd_add(s, dd_mul(Vs[rr][l], Vs[rr][c]));
+    if (l < jb && c < jb)
+      for (int rr = 0; rr < kGramRows; ++rr) s = dd_add(s, dd_mul(Vs[rr][l], Vs[rr][c]));
     std_(pg, G * kMaxNb * kMaxNb, static_cast<int64_t>(blockIdx.x) * kMaxNb * kMaxNb + e, s);
   }
 }
 
-__global__ void __launch_bounds__(kMaxNb * kMaxNb) qr_gram_reduce_kernel(int jb, int64_t groups,
-                                                                         const double* __restrict__ pg,
-                                                                         double* __restrict__ Gout) {
-  const int e = threadIdx.x, l = e >> 5, c = e & 31;
-  dd s = {0.0, 0.0};
-  for (int64_t b = 0; b < groups; ++b) s = dd_add(s, ldd(pg, groups * kMaxNb * kMaxNb, b * kMaxNb * kMaxNb + e));
-  if (l < jb && c < jb) std_(Gout, static_cast<int64_t>(jb) * jb, static_cast<int64_t>(l) * jb + c, s);
+constexpr int kGramThreads = 1024;
+
+__global__ void __launch_bounds__(kGramThreads) qr_gram_reduce_kernel(int jb, int64_t groups,
+                                                                      const double* __restrict__ pg,
+                                                                      double* __restrict__ Gout) {
+  for (int e = threadIdx.x; e < kMaxNb * kMaxNb; e += kGramThreads) {
+    const int l = e / kMaxNb, c = e % kMaxNb;
+    if (l >= jb || c >= jb) continue;
+    dd s = {0.0, 0.0};
+    for (int64_t b = 0; b < groups; ++b) s = dd_add(s, ldd(pg, groups * kMaxNb * kMaxNb, b * kMaxNb * kMaxNb + e));
+    std_(Gout, static_cast<int64_t>(jb) * jb, static_cast<int64_t>(l) * jb + c, s);
+  }
 }
 
 // T (upper triangular, jb x jb) of I - V T V^T = H_0 ... H_{jb-1} from
 // G = V^T V and tau: T(j, j) = tau_j, T(0:j, j) = -tau_j T(0:j, 0:j) G(0:j, j);
-// writes the transpose Tt.  One wave, serial in j, G staged in LDS.
+// writes the transpose Tt.  One wave, serial in j; T and G in dynamic LDS,
+// 2 jb^2 double-doubles (128 KB at jb = 64).
+__host__ __device__ constexpr size_t qr_t_lds(int jb) { return 2 * sizeof(dd) * static_cast<size_t>(jb) * jb; }
+
 __global__ void __launch_bounds__(64) qr_t_kernel(int jb, int64_t n, int64_t j0, const double* __restrict__ G,
                                                   const double* __restrict__ tau, double* __restrict__ Tt) {
-  __shared__ dd T[kMaxNb][kMaxNb];
-  __shared__ dd Gs[kMaxNb][kMaxNb];
+  extern __shared__ dd tsm[];
+  dd* T = tsm;             // T[i * jb + c]
+  dd* Gs = tsm + jb * jb;  // G[l * jb + c]
   const int i = threadIdx.x;
   const int64_t pg = static_cast<int64_t>(jb) * jb;
-  if (i < kMaxNb)
-    for (int c = 0; c < kMaxNb; ++c) {
-      T[i][c] = {0.0, 0.0};
-      Gs[i][c] = (i < jb && c < jb) ? ldd(G, pg, static_cast<int64_t>(i) * jb + c) : dd{0.0, 0.0};
+  if (i < jb)
+    for (int c = 0; c < jb; ++c) {
+      T[i * jb + c] = {0.0, 0.0};
+      Gs[i * jb + c] = ldd(G, pg, static_cast<int64_t>(i) * jb + c);
     }
   __syncthreads();
   for (int j = 0; j < jb; ++j) {
     const dd tj = ldd(tau, n, j0 + j);
     dd s = {0.0, 0.0};
     if (i < j) {
-      for (int l = i; l < j; ++l) s = dd_add(s, dd_mul(T[i][l], Gs[l][j]));
+      for (int l = i; l < j; ++l) s = dd_add(s, dd_mul(T[i * jb + l], Gs[l * jb + j]));
     }
     __syncthreads();
-    if (i < j) T[i][j] = dd_neg(dd_mul(tj, s));
-    if (i == j) T[j][j] = tj;
+    if (i < j) T[i * jb + j] = dd_neg(dd_mul(tj, s));
+    if (i == j) T[j * jb + j] = tj;
     __syncthreads();
   }
   if (i < jb)
-    for (int c = 0; c < jb; ++c) std_(Tt, pg, static_cast<int64_t>(c) * jb + i, T[i][c]);
+    for (int c = 0; c < jb; ++c) std_(Tt, pg, static_cast<int64_t>(c) * jb + i, T[i * jb + c]);
 }
 
 // Copy the trailing block A(j0:m, c0:n) into a contiguous [2][mp][nc] array.
@@ -448,7 +476,7 @@ bool qr_layout(int64_t m, int64_t n, int nb, QrLayout* L) {
   L->px1 = off;
   off += align256(dd_bytes * kMaxNb);
   L->pgram = off;
-  off += align256(dd_bytes * groups * kMaxNb * kMaxNb);
+  off += align256(dd_bytes * static_cast<size_t>((m + kGramRows - 1) / kGramRows) * kMaxNb * kMaxNb);
   // the largest workspace of the three products of any panel: V^T X, T^T W, V W2
   mdgemm_opts o = qr_gemm_opts();
   size_t need = 0;
@@ -499,6 +527,15 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
       (a0 < t0 + tbytes && t0 < a0 + abytes))
     return MDGEMM_EINVAL;
   const hipStream_t s = static_cast<hipStream_t>(stream);
+  // the T kernel's dynamic LDS beyond 64 KB (panels wider than 45 columns):
+  // allowed once for the kernel (a failure shows up as a launch error below)
+  static std::once_flag once;
+  std::call_once(once, [] {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&mdg::qr_t_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              static_cast<int>(mdg::qr_t_lds(mdg::kMaxNb)));
+    (void)hipGetLastError();
+  });
   char* ws = static_cast<char*>(workspace);
   double* V = reinterpret_cast<double*>(ws + L.v);
   double* Vt = reinterpret_cast<double*>(ws + L.vt);
@@ -538,14 +575,14 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
                        X);
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     // G = V^T V (double-double dot products over the panel's rows)
-    const unsigned groups = static_cast<unsigned>((mp + mdg::kPanelRows - 1) / mdg::kPanelRows);
-    hipLaunchKernelGGL(mdg::qr_gram_partial_kernel, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0, jb, A,
+    const unsigned ggroups = static_cast<unsigned>((mp + mdg::kGramRows - 1) / mdg::kGramRows);
+    hipLaunchKernelGGL(mdg::qr_gram_partial_kernel, dim3(ggroups), dim3(mdg::kColThreads), 0, s, m, n, j0, jb, A,
                        pgram);
-    hipLaunchKernelGGL(mdg::qr_gram_reduce_kernel, dim3(1), dim3(mdg::kMaxNb * mdg::kMaxNb), 0, s, jb,
-                       static_cast<int64_t>(groups), pgram, G);
+    hipLaunchKernelGGL(mdg::qr_gram_reduce_kernel, dim3(1), dim3(mdg::kGramThreads), 0, s, jb,
+                       static_cast<int64_t>(ggroups), pgram, G);
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     int st = MDGEMM_OK;
-    hipLaunchKernelGGL(mdg::qr_t_kernel, dim3(1), dim3(64), 0, s, jb, n, j0, G, tau, Tt);
+    hipLaunchKernelGGL(mdg::qr_t_kernel, dim3(1), dim3(64), mdg::qr_t_lds(jb), s, jb, n, j0, G, tau, Tt);
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     if ((st = mdgemm_ex(jb, nc, mp, 2, Vt, X, W, &o)) != MDGEMM_OK) return st;   // W = V^T X
     if ((st = mdgemm_ex(jb, nc, jb, 2, Tt, W, W2, &o)) != MDGEMM_OK) return st;  // W2 = T^T W

@@ -587,7 +587,7 @@ def mdgemm_probe_stream(src: torch.Tensor, reads: int, dst: Optional[torch.Tenso
                                      _stream(stream)), "mdgemm_probe_stream")
 
 
-def mdgemm_qr_dd(A: torch.Tensor, nb: int = 32, workspace: Optional[torch.Tensor] = None, stream=None):
+def mdgemm_qr_dd(A: torch.Tensor, nb: int = 64, workspace: Optional[torch.Tensor] = None, stream=None):
     """Householder QR of a double-double matrix A [2, m, n] (m >= n) in place:
     returns (A, tau) with R on and above the diagonal of A, the Householder
     vectors below it, and tau [2, n]."""

@@ -26,7 +26,8 @@ DEV = torch.device("cuda:0")
 
 @pytest.mark.parametrize("m,n,nb,seed", [(256, 128, 32, 1), (300, 173, 32, 2), (64, 64, 16, 3), (129, 1, 8, 4),
                                          (100, 37, 7, 5), (520, 96, 32, 6), (1100, 300, 32, 7), (700, 700, 32, 8),
-                                         (1000, 61, 13, 9)])
+                                         (1000, 61, 13, 9), (700, 700, 64, 10), (1100, 300, 64, 11), (300, 173, 48, 12),
+                                         (129, 1, 64, 13), (520, 96, 40, 14)])
 def test_qr_dd_against_the_oracle(m, n, nb, seed):
     print(f"[case] qr dd {m}x{n} nb={nb}", flush=True)
     rng = np.random.default_rng(seed)
@@ -62,8 +63,8 @@ def test_qr_dd_refusals():
     lib = md.lib()
     assert lib.mdgemm_qr_dd(10, 20, 8, A.data_ptr(), tau.data_ptr(), ws.data_ptr(), ws.numel(), None) == \
         md.MDGEMM_EINVAL  # m < n
-    assert lib.mdgemm_qr_dd(20, 10, 33, A.data_ptr(), tau.data_ptr(), ws.data_ptr(), ws.numel(), None) == \
-        md.MDGEMM_EINVAL  # nb > 32
+    assert lib.mdgemm_qr_dd(20, 10, 65, A.data_ptr(), tau.data_ptr(), ws.data_ptr(), ws.numel(), None) == \
+        md.MDGEMM_EINVAL  # nb > 64
     need = lib.mdgemm_qr_dd_workspace_bytes(20, 10, 8)
     assert lib.mdgemm_qr_dd(20, 10, 8, A.data_ptr(), tau.data_ptr(), ws.data_ptr(), need - 1, None) == \
         md.MDGEMM_EWORKSPACE
