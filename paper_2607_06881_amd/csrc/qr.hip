@@ -324,7 +324,7 @@ __global__ void __launch_bounds__(256) qr_pack_v_kernel(int64_t m, int64_t n, in
 // G = V^T V (jb x jb) of the factored panel, in double-double arithmetic, in
 // two launches: workgroups of kGramRows rows stage their rows of V (1 on the
 // diagonal, the stored vectors below, 0 above) in LDS and write the partial sums
-// of all kMaxNb x kMaxNb entries; one workgroup of 1024 threads then adds the
+// of all kMaxNb x kMaxNb entries; a second launch (one thread per entry) adds the
 // partials of each entry in workgroup order and writes G [2][jb][jb].
 constexpr int kGramRows = 32;
 
@@ -355,52 +355,71 @@ __global__ void __launch_bounds__(kColThreads) qr_gram_partial_kernel(int64_t m,
   }
 }
 
-constexpr int kGramThreads = 1024;
+// one thread per entry of G, the partials added in workgroup order, eight loads
+// issued at a time
+constexpr int kGramThreads = 256;
 
 __global__ void __launch_bounds__(kGramThreads) qr_gram_reduce_kernel(int jb, int64_t groups,
                                                                       const double* __restrict__ pg,
                                                                       double* __restrict__ Gout) {
-  for (int e = threadIdx.x; e < kMaxNb * kMaxNb; e += kGramThreads) {
-    const int l = e / kMaxNb, c = e % kMaxNb;
-    if (l >= jb || c >= jb) continue;
-    dd s = {0.0, 0.0};
-    for (int64_t b = 0; b < groups; ++b) s = dd_add(s, ldd(pg, groups * kMaxNb * kMaxNb, b * kMaxNb * kMaxNb + e));
-    std_(Gout, static_cast<int64_t>(jb) * jb, static_cast<int64_t>(l) * jb + c, s);
+  const int e = blockIdx.x * kGramThreads + threadIdx.x;
+  const int l = e / kMaxNb, c = e % kMaxNb;
+  if (l >= jb || c >= jb) return;
+  const int64_t plane = groups * kMaxNb * kMaxNb;
+  dd s = {0.0, 0.0};
+  for (int64_t b0 = 0; b0 < groups; b0 += 8) {
+    dd v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      v[u] = b0 + u < groups ? ldd(pg, plane, (b0 + u) * kMaxNb * kMaxNb + e) : dd{0.0, 0.0};
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (b0 + u < groups) s = dd_add(s, v[u]);
   }
+  std_(Gout, static_cast<int64_t>(jb) * jb, static_cast<int64_t>(l) * jb + c, s);
 }
 
 // T (upper triangular, jb x jb) of I - V T V^T = H_0 ... H_{jb-1} from
 // G = V^T V and tau: T(j, j) = tau_j, T(0:j, j) = -tau_j T(0:j, 0:j) G(0:j, j);
-// writes the transpose Tt.  One wave, serial in j; T and G in dynamic LDS,
-// 2 jb^2 double-doubles (128 KB at jb = 64).
+// writes the transpose Tt.  Serial in j; for each j the sum of row i is split
+// over the kTLanes consecutive lanes of the row (lane q takes l = i + q,
+// i + q + kTLanes, ...) and reduced by shuffles within the wave, the result
+// taken from lane 0 (a fixed order).  T and G in dynamic LDS, 2 jb^2
+// double-doubles (128 KB at jb = 64).
+constexpr int kTLanes = 16;
 __host__ __device__ constexpr size_t qr_t_lds(int jb) { return 2 * sizeof(dd) * static_cast<size_t>(jb) * jb; }
 
-__global__ void __launch_bounds__(64) qr_t_kernel(int jb, int64_t n, int64_t j0, const double* __restrict__ G,
-                                                  const double* __restrict__ tau, double* __restrict__ Tt) {
+__device__ inline dd shfl_xor_dd(dd v, int off) { return {__shfl_xor(v.hi, off, 64), __shfl_xor(v.lo, off, 64)}; }
+
+__global__ void __launch_bounds__(kMaxNb * kTLanes) qr_t_kernel(int jb, int64_t n, int64_t j0,
+                                                              const double* __restrict__ G,
+                                                              const double* __restrict__ tau,
+                                                              double* __restrict__ Tt) {
   extern __shared__ dd tsm[];
   dd* T = tsm;             // T[i * jb + c]
   dd* Gs = tsm + jb * jb;  // G[l * jb + c]
-  const int i = threadIdx.x;
+  const int tid = threadIdx.x, i = tid / kTLanes, q = tid % kTLanes;
   const int64_t pg = static_cast<int64_t>(jb) * jb;
-  if (i < jb)
-    for (int c = 0; c < jb; ++c) {
-      T[i * jb + c] = {0.0, 0.0};
-      Gs[i * jb + c] = ldd(G, pg, static_cast<int64_t>(i) * jb + c);
-    }
+  for (int e = tid; e < jb * jb; e += kMaxNb * kTLanes) {
+    T[e] = {0.0, 0.0};
+    Gs[e] = ldd(G, pg, e);
+  }
   __syncthreads();
   for (int j = 0; j < jb; ++j) {
-    const dd tj = ldd(tau, n, j0 + j);
     dd s = {0.0, 0.0};
-    if (i < j) {
-      for (int l = i; l < j; ++l) s = dd_add(s, dd_mul(T[i * jb + l], Gs[l * jb + j]));
+    if (i < j)
+      for (int l = i + q; l < j; l += kTLanes) s = dd_add(s, dd_mul(T[i * jb + l], Gs[l * jb + j]));
+    for (int off = kTLanes / 2; off > 0; off >>= 1) s = dd_add(s, shfl_xor_dd(s, off));
+    if (q == 0 && i <= j) {
+      const dd tj = ldd(tau, n, j0 + j);
+      T[i * jb + j] = i < j ? dd_neg(dd_mul(tj, s)) : tj;
     }
     __syncthreads();
-    if (i < j) T[i * jb + j] = dd_neg(dd_mul(tj, s));
-    if (i == j) T[j * jb + j] = tj;
-    __syncthreads();
   }
-  if (i < jb)
-    for (int c = 0; c < jb; ++c) std_(Tt, pg, static_cast<int64_t>(c) * jb + i, T[i * jb + c]);
+  for (int e = tid; e < jb * jb; e += kMaxNb * kTLanes) {
+    const int r = e / jb, c = e % jb;
+    std_(Tt, pg, static_cast<int64_t>(c) * jb + r, T[e]);
+  }
 }
 
 // Copy the trailing block A(j0:m, c0:n) into a contiguous [2][mp][nc] array.
@@ -578,11 +597,12 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
     const unsigned ggroups = static_cast<unsigned>((mp + mdg::kGramRows - 1) / mdg::kGramRows);
     hipLaunchKernelGGL(mdg::qr_gram_partial_kernel, dim3(ggroups), dim3(mdg::kColThreads), 0, s, m, n, j0, jb, A,
                        pgram);
-    hipLaunchKernelGGL(mdg::qr_gram_reduce_kernel, dim3(1), dim3(mdg::kGramThreads), 0, s, jb,
-                       static_cast<int64_t>(ggroups), pgram, G);
+    hipLaunchKernelGGL(mdg::qr_gram_reduce_kernel, dim3(mdg::kMaxNb * mdg::kMaxNb / mdg::kGramThreads),
+                       dim3(mdg::kGramThreads), 0, s, jb, static_cast<int64_t>(ggroups), pgram, G);
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     int st = MDGEMM_OK;
-    hipLaunchKernelGGL(mdg::qr_t_kernel, dim3(1), dim3(64), mdg::qr_t_lds(jb), s, jb, n, j0, G, tau, Tt);
+    hipLaunchKernelGGL(mdg::qr_t_kernel, dim3(1), dim3(mdg::kMaxNb * mdg::kTLanes), mdg::qr_t_lds(jb), s, jb, n, j0,
+                       G, tau, Tt);
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     if ((st = mdgemm_ex(jb, nc, mp, 2, Vt, X, W, &o)) != MDGEMM_OK) return st;   // W = V^T X
     if ((st = mdgemm_ex(jb, nc, jb, 2, Tt, W, W2, &o)) != MDGEMM_OK) return st;  // W2 = T^T W
