@@ -156,7 +156,7 @@ __global__ void __launch_bounds__(kPanelThreads) qr_panel_kernel(int64_t m, int6
 //     pivot row entering with v = 1.
 // Every block writes all of its partial slots (zeros when it holds no row at or
 // below the pivot), so the sums never read a stale slot.
-constexpr int kPanelRows = 64;
+constexpr int kPanelRows = 32;
 constexpr int kColThreads = 256;  // 32 column lanes x 8 row groups
 constexpr int64_t kSmallPanel = 256;
 
