@@ -1,5 +1,7 @@
 """GPU checks of the blocked Householder QR in double-double (mdgemm_qr_dd),
-the downstream application whose trailing updates run on mdgemm.
+the downstream application whose trailing updates run on mdgemm.  Panels of
+more than 256 rows take the multi-workgroup path (two launches per column), up
+to 70000 rows (2188 workgroups per launch).
 
 The GPU factorization is checked in double-double arithmetic by the CPU
 oracle: the residual max |A - Q R| / max |A| and the orthogonality
@@ -27,7 +29,7 @@ DEV = torch.device("cuda:0")
 @pytest.mark.parametrize("m,n,nb,seed", [(256, 128, 32, 1), (300, 173, 32, 2), (64, 64, 16, 3), (129, 1, 8, 4),
                                          (100, 37, 7, 5), (520, 96, 32, 6), (1100, 300, 32, 7), (700, 700, 32, 8),
                                          (1000, 61, 13, 9), (700, 700, 64, 10), (1100, 300, 64, 11), (300, 173, 48, 12),
-                                         (129, 1, 64, 13), (520, 96, 40, 14)])
+                                         (129, 1, 64, 13), (520, 96, 40, 14), (70000, 40, 32, 15)])
 def test_qr_dd_against_the_oracle(m, n, nb, seed):
     print(f"[case] qr dd {m}x{n} nb={nb}", flush=True)
     rng = np.random.default_rng(seed)
