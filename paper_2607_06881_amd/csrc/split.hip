@@ -142,17 +142,21 @@ __global__ void __launch_bounds__(256) split_panel_kernel(int64_t rows, int64_t 
 }
 
 // The panel layout of split_panel_kernel for multiple doubles of up to four
-// limbs, a block per tile of 64 lines x 16 k values, in two phases:
+// limbs, by tiles of 64 lines x 16 k values; a block takes the tiles of its 64
+// lines at k steps of gridDim.y tiles (up to four), each in two phases:
 //  - load: the tile's limbs go through LDS, so that every global load of a wave
 //    reads whole 128-byte lines whichever operand it is (A's lines are rows, 16
 //    consecutive k values of a row per 16 lanes; B's lines are columns, 64
-//    consecutive columns per wave), the padding positions loading +0.0;
+//    consecutive columns per wave), the padding positions loading +0.0; the
+//    next tile's loads are issued before the current tile is split;
 //  - split: each thread takes 4 consecutive lines of one k value, so that every
-//    digit store is one 16-byte vector (a wave writes 1 KiB of a panel row).
+//    digit store is one 16-byte vector (a wave writes 256 bytes of each of four
+//    FP32 panel rows).
 // kFast selects floor_on_grid_128 (digit windows w S <= 128, NW = 2) or
-// floor_on_grid_256 (w S <= 256, NW = 4); otherwise floor_on_grid with NW words.  The digit fields are read upward from bit 0 in a
-// two-word window as in store_digits; the window position is the same for all
-// four elements (and all lanes), so only the words differ.
+// floor_on_grid_256 (w S <= 256, NW = 4); otherwise floor_on_grid with NW
+// words.  The digit fields are read upward from bit 0 in a two-word window as
+// in store_digits; the window position is the same for all four elements (and
+// all lanes), so only the words differ.
 constexpr int kTileLines = 64, kTileK = 16, kTilePitch = kTileLines + 4;  // LDS row pitch in doubles
 
 __host__ __device__ constexpr size_t split_tile_lds(int L) {
@@ -196,8 +200,7 @@ __global__ void __launch_bounds__(256) split_tile_kernel(int64_t rows, int64_t c
 #pragma unroll
   for (int i = 0; i < 4; ++i) e[i] = c0 + qc + i < Cn ? E[c0 + qc + i] : 0;
   const uint64_t mask = (1ull << w) - 1ull;
-  // load-phase positions (fixed per thread) and the tile's limbs in registers;
-  // the next tile's loads are issued before the current tile is split
+  // load-phase positions (fixed per thread) and the tile's limbs in registers
   int lk[4], lc[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
