@@ -70,3 +70,54 @@ def test_qr_dd_refusals():
     need = lib.mdgemm_qr_dd_workspace_bytes(20, 10, 8)
     assert lib.mdgemm_qr_dd(20, 10, 8, A.data_ptr(), tau.data_ptr(), ws.data_ptr(), need - 1, None) == \
         md.MDGEMM_EWORKSPACE
+
+
+@pytest.mark.parametrize("m,n,nb", [(600, 100, 32), (200, 90, 64)])
+def test_qr_dd_triangular_and_zero_columns(m, n, nb):
+    # an upper triangular A with a diagonal of mixed signs and a zero column:
+    # every column has nothing below its pivot (sigma = 0), so each reflection
+    # is the identity (tau = 0, x_1 >= 0) or flips the row (tau = 2, v = e_1),
+    # and the stored vectors are zero.  R is A with the rows of negative pivots
+    # negated.  Within the first panel the arithmetic is exact (the oracle agrees
+    # bit for bit); the later columns pass through the trailing products, whose
+    # digits on each line's grid keep the error within the product's bound, so
+    # there the high limbs are exact and the low limbs within 1e-28 of each
+    # entry (tall panels take the multi-workgroup path at m = 600)
+    print(f"[case] qr dd triangular {m}x{n} nb={nb}", flush=True)
+    rng = np.random.default_rng(m + n)
+    A = workloads.make_operand(rng, 2, m, n, "normal")
+    A[:, np.tril_indices(m, -1, n)[0], np.tril_indices(m, -1, n)[1]] = 0.0
+    A[:, :, 7] = 0.0
+    QRg, taug = md.mdgemm_qr_dd(torch.from_numpy(A).to(DEV).clone(), nb=nb)
+    torch.cuda.synchronize()
+    QR, tau = QRg.cpu().numpy(), taug.cpu().numpy()
+    QRo, tauo = coracle.qr_dd(A)
+    flip = A[0][np.arange(n), np.arange(n)] < 0.0
+    assert np.array_equal(tau, tauo)
+    assert np.array_equal(tau[0], np.where(flip, 2.0, 0.0)) and not tau[1].any()
+    assert np.array_equal(QR[:, :, :nb], QRo[:, :, :nb])
+    assert not np.tril(QR[0], -1).any() and not np.tril(QR[1], -1).any()
+    R = np.where(flip[None, :, None], -A[:, :n], A[:, :n])
+    assert np.array_equal(np.triu(QR[0][:n]), np.triu(R[0]))
+    lo = np.abs(np.triu(QR[1][:n]) - np.triu(R[1]))
+    assert (lo <= 1e-28 * np.abs(np.triu(R[0]))).all()
+
+
+def test_qr_dd_rank_deficient():
+    # repeated columns: after the first copy is eliminated the second has (nearly)
+    # nothing left below its pivot; the factorization stays orthogonal and exact
+    # to double-double level
+    m, n = 500, 60
+    print("[case] qr dd rank deficient", flush=True)
+    rng = np.random.default_rng(21)
+    A = workloads.make_operand(rng, 2, m, n, "normal")
+    A[:, :, 30:40] = A[:, :, 0:10]
+    A[:, :, 50] = 2.0 * A[:, :, 3]
+    QRg, taug = md.mdgemm_qr_dd(torch.from_numpy(A).to(DEV).clone(), nb=32)
+    torch.cuda.synchronize()
+    QR, tau = QRg.cpu().numpy(), taug.cpu().numpy()
+    assert np.isfinite(QR).all() and np.isfinite(tau).all()
+    assert nonoverlap_all(QR) and nonoverlap_all(tau)
+    res, orth, _ = coracle.qr_dd_check(A, QR, tau)
+    print(f"[result] qr rank deficient: residual {res:.2e}, orthogonality {orth:.2e}", flush=True)
+    assert res < 1e-28 and orth < 1e-28
