@@ -190,8 +190,17 @@ __global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, i
     // the same order in every block
     const dd tprev = ldd(tau, n, j0 + j - 1);
     for (int g0 = 0; g0 < jb - j; g0 += 32) {
+      // partials b = rg, rg + 8, ... in that order, eight loads in flight
       dd s = {0.0, 0.0};
-      for (int64_t b = rg; b < G; b += 8) s = dd_add(s, ldd(pw, G * kMaxNb, b * kMaxNb + g0 + cc));
+      for (int64_t b0 = rg; b0 < G; b0 += 64) {
+        dd v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          v[u] = b0 + 8 * u < G ? ldd(pw, G * kMaxNb, (b0 + 8 * u) * kMaxNb + g0 + cc) : dd{0.0, 0.0};
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (b0 + 8 * u < G) s = dd_add(s, v[u]);
+      }
       red[tid] = s;
       __syncthreads();
       if (rg == 0) {
