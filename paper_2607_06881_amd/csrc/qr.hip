@@ -44,6 +44,8 @@ __device__ inline void std_(double* P, int64_t plane, int64_t idx, dd v) {
   P[plane + idx] = v.lo;
 }
 
+__device__ inline dd shfl_xor_dd(dd v, int off) { return {__shfl_xor(v.hi, off, 64), __shfl_xor(v.lo, off, 64)}; }
+
 // Sum of one dd per thread over the workgroup (tree in LDS); the result in red[0].
 __device__ inline dd block_sum(dd v, dd* red) {
   const int tid = threadIdx.x;
@@ -160,18 +162,22 @@ constexpr int kPanelRows = 32;
 constexpr int kColThreads = 256;  // 32 column lanes x 8 row groups
 constexpr int64_t kSmallPanel = 256;
 
+// Sum of one dd per thread over the 256 threads: a butterfly within each wave,
+// then the four wave sums in a fixed order; every thread gets the result.
 __device__ inline dd block_sum256(dd v, dd* red) {
+  for (int off = 32; off > 0; off >>= 1) v = dd_add(v, shfl_xor_dd(v, off));
   const int tid = threadIdx.x;
-  red[tid] = v;
+  if ((tid & 63) == 0) red[tid >> 6] = v;
   __syncthreads();
-  for (int s = kColThreads / 2; s > 0; s >>= 1) {
-    if (tid < s) red[tid] = dd_add(red[tid], red[tid + s]);
-    __syncthreads();
-  }
-  const dd r = red[0];
+  const dd r = dd_add(dd_add(red[0], red[1]), dd_add(red[2], red[3]));
   __syncthreads();
   return r;
 }
+
+constexpr int kRowGroups = kColThreads / 32;                // 8
+constexpr int kRowsPerThread = kPanelRows / kRowGroups;      // rows rb + rg + 8 q, q < 4
+constexpr int kColGroups = kMaxNb / 32;                      // columns c0 + 32 h + cc, h < 2
+static_assert(kPanelRows % kRowGroups == 0 && kMaxNb % 32 == 0, "thread layout of the column kernels");
 
 __global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, int64_t n, int64_t j0, int jb, int j,
                                                                     double* __restrict__ A,
@@ -185,6 +191,28 @@ __global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, i
   const int tid = threadIdx.x, cc = tid & 31, rg = tid >> 5;
   const int64_t G = gridDim.x;
   const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kPanelRows, re = min(m, rb + kPanelRows);
+  const int64_t r0 = j0 + j, rp = r0 - 1;  // the pivot rows of column j and of column j - 1
+  // The entries this thread updates, loaded before the partials are folded (they
+  // do not depend on them): rows rb + rg + 8 q of columns j + 32 h + cc from the
+  // previous pivot row down (column j alone, from its pivot down, when j = 0),
+  // and v_{j-1} at the same rows (1 at its pivot row).
+  dd av[kColGroups][kRowsPerThread], vv[kRowsPerThread];
+  const int64_t rlo = j > 0 ? rp : r0;
+#pragma unroll
+  for (int h = 0; h < kColGroups; ++h) {
+    const int c = j + 32 * h + cc;
+#pragma unroll
+    for (int q = 0; q < kRowsPerThread; ++q) {
+      const int64_t r = rb + rg + kRowGroups * q;
+      const bool ok = c < jb && (j > 0 || c == j) && r >= rlo && r < re;
+      av[h][q] = ok ? ldd(A, plane, r * n + j0 + c) : dd{0.0, 0.0};
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kRowsPerThread; ++q) {
+    const int64_t r = rb + rg + kRowGroups * q;
+    vv[q] = j > 0 && r > rp && r < re ? ldd(A, plane, r * n + j0 + j - 1) : dd{r == rp ? 1.0 : 0.0, 0.0};
+  }
   if (j > 0) {
     // w_c = tau_{j-1} sum_b pw[b][c - j] for c = j + g0 + cc, 32 columns at a time:
     // the same order in every block
@@ -210,35 +238,37 @@ __global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, i
       }
       __syncthreads();
     }
-    const int64_t rp = j0 + j - 1;  // the previous pivot row (v = 1 there)
-    for (int g0 = 0; g0 < jb - j; g0 += 32) {
-      const int c = j + g0 + cc;
+    // a_c <- a_c - (tau w_c) v at the rows from the previous pivot down
+#pragma unroll
+    for (int h = 0; h < kColGroups; ++h) {
+      const int c = j + 32 * h + cc;
       if (c < jb) {
-        const dd t = tw[g0 + cc];
-        for (int64_t r = rb + rg; r < re; r += 8) {
-          if (r < rp) continue;
-          const dd v = r == rp ? dd{1.0, 0.0} : ldd(A, plane, r * n + j0 + j - 1);
-          const int64_t idx = r * n + j0 + c;
-          std_(A, plane, idx, dd_sub(ldd(A, plane, idx), dd_mul(t, v)));
+        const dd t = tw[32 * h + cc];
+#pragma unroll
+        for (int q = 0; q < kRowsPerThread; ++q) {
+          const int64_t r = rb + rg + kRowGroups * q;
+          if (r >= rp && r < re) {
+            av[h][q] = dd_sub(av[h][q], dd_mul(t, vv[q]));
+            std_(A, plane, r * n + j0 + c, av[h][q]);
+          }
         }
       }
     }
-    __syncthreads();  // the block's writes of column j before its sum of squares
   }
-  const int64_t r0 = j0 + j;
+  // the block's part of sigma_j (column j below its pivot, held by lane cc = 0
+  // of each row group) and x1 = a(r0, j) from the block holding the pivot row
   dd part = {0.0, 0.0};
-  if (tid < kPanelRows) {
-    const int64_t r = rb + tid;
-    if (r > r0 && r < re) {
-      const dd a = ldd(A, plane, r * n + j0 + j);
-      part = dd_mul(a, a);
+  if (cc == 0) {
+#pragma unroll
+    for (int q = 0; q < kRowsPerThread; ++q) {
+      const int64_t r = rb + rg + kRowGroups * q;
+      if (r > r0 && r < re) part = dd_add(part, dd_mul(av[0][q], av[0][q]));
+      if (r == r0) std_(px1, kMaxNb, j, av[0][q]);
     }
-    if (r == r0) std_(px1, kMaxNb, j, ldd(A, plane, r * n + j0 + j));
   }
   const dd sig = block_sum256(part, red);
   if (tid == 0) std_(psig, G, blockIdx.x, sig);
 }
-
 __global__ void __launch_bounds__(kColThreads) qr_col_reflect_kernel(int64_t m, int64_t n, int64_t j0, int jb, int j,
                                                                      double* __restrict__ A, double* __restrict__ tau,
                                                                      const double* __restrict__ psig,
@@ -253,6 +283,24 @@ __global__ void __launch_bounds__(kColThreads) qr_col_reflect_kernel(int64_t m, 
   const int64_t G = gridDim.x;
   const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kPanelRows, re = min(m, rb + kPanelRows);
   const int64_t r0 = j0 + j;
+  // Loaded before sigma is formed (none of them depends on it): column j below
+  // the pivot (one row per thread of the first 32) and the trailing columns
+  // j + 1 + 32 h + cc at rows rb + rg + 8 q at or below the pivot.
+  dd xv = {0.0, 0.0};
+  if (tid < kPanelRows) {
+    const int64_t r = rb + tid;
+    if (r > r0 && r < re) xv = ldd(A, plane, r * n + j0 + j);
+  }
+  dd av[kColGroups][kRowsPerThread];
+#pragma unroll
+  for (int h = 0; h < kColGroups; ++h) {
+    const int c = j + 1 + 32 * h + cc;
+#pragma unroll
+    for (int q = 0; q < kRowsPerThread; ++q) {
+      const int64_t r = rb + rg + kRowGroups * q;
+      av[h][q] = c < jb && r >= r0 && r < re ? ldd(A, plane, r * n + j0 + c) : dd{0.0, 0.0};
+    }
+  }
   dd part = {0.0, 0.0};
   for (int64_t b = tid; b < G; b += kColThreads) part = dd_add(part, ldd(psig, G, b));
   const dd sigma = block_sum256(part, red);
@@ -286,27 +334,32 @@ __global__ void __launch_bounds__(kColThreads) qr_col_reflect_kernel(int64_t m, 
       v = {1.0, 0.0};
     } else if (r > r0 && r < re) {
       // mode 2: v = x / v1; otherwise v = e_1, zero below the pivot
-      v = mode == 2 ? dd_div(ldd(A, plane, r * n + j0 + j), s_scale) : dd{0.0, 0.0};
+      v = mode == 2 ? dd_div(xv, s_scale) : dd{0.0, 0.0};
       std_(A, plane, r * n + j0 + j, v);
     }
     vs[tid] = v;
   }
   __syncthreads();
   // partial w_c = v^T a_c over the block's rows at or below the pivot, for
-  // c = j + 1 + g0 + cc, 32 columns at a time (slot g0 + cc)
-  for (int g0 = 0; g0 < jb - j - 1; g0 += 32) {
-    const int c = j + 1 + g0 + cc;
+  // c = j + 1 + 32 h + cc (slot 32 h + cc), rows in increasing order
+#pragma unroll
+  for (int h = 0; h < kColGroups; ++h) {
+    if (32 * h >= jb - j - 1) break;
+    const int c = j + 1 + 32 * h + cc;
     dd acc = {0.0, 0.0};
     if (c < jb) {
-      for (int64_t r = rb + rg; r < re; r += 8)
-        if (r >= r0) acc = dd_add(acc, dd_mul(vs[r - rb], ldd(A, plane, r * n + j0 + c)));
+#pragma unroll
+      for (int q = 0; q < kRowsPerThread; ++q) {
+        const int64_t r = rb + rg + kRowGroups * q;
+        if (r >= r0 && r < re) acc = dd_add(acc, dd_mul(vs[r - rb], av[h][q]));
+      }
     }
     red[tid] = acc;
     __syncthreads();
     if (rg == 0) {
       dd w = red[cc];
       for (int g = 1; g < 8; ++g) w = dd_add(w, red[g * 32 + cc]);
-      std_(pw, G * kMaxNb, static_cast<int64_t>(blockIdx.x) * kMaxNb + g0 + cc, w);
+      std_(pw, G * kMaxNb, static_cast<int64_t>(blockIdx.x) * kMaxNb + 32 * h + cc, w);
     }
     __syncthreads();
   }
@@ -398,7 +451,6 @@ __global__ void __launch_bounds__(kGramThreads) qr_gram_reduce_kernel(int jb, in
 constexpr int kTLanes = 16;
 __host__ __device__ constexpr size_t qr_t_lds(int jb) { return 2 * sizeof(dd) * static_cast<size_t>(jb) * jb; }
 
-__device__ inline dd shfl_xor_dd(dd v, int off) { return {__shfl_xor(v.hi, off, 64), __shfl_xor(v.lo, off, 64)}; }
 
 __global__ void __launch_bounds__(kMaxNb * kTLanes) qr_t_kernel(int jb, int64_t n, int64_t j0,
                                                               const double* __restrict__ G,
