@@ -201,9 +201,15 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
 // (lanes 16h..16h+15 read row 4kg + h, 16 consecutive columns) then touches four
 // different 16-bank groups for h = 0..3: conflict-free.  Panels are k-major and
 // zero-padded to k multiple of 32, m / n multiple of 128.
+//
+// Outputs of at most 64 rows (the V^T X products of a blocked QR) take tiles of
+// kRows = 64 rows: the same 128 columns and waves, each wave 32 x 64, A's LDS
+// rows 64 floats (one copy instruction fills four), swizzled the same way.  A
+// 128-row tile would spend half of its MFMAs on padding rows.
 constexpr int BK32 = 32;
-constexpr int ROW32 = 128;  // floats per LDS row
+constexpr int ROW32 = 128;  // floats per LDS row of B (and of A for 128-row tiles)
 
+template <int kRows>
 __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, int64_t n, int64_t kp, int64_t mp,
                                                                    int64_t np, int tiles_n, int ntiles,
                                                                    const float* __restrict__ DAt,
@@ -211,7 +217,10 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
                                                                    double* __restrict__ out,
                                                                    const uint32_t* __restrict__ jobs,
                                                                    const uint32_t* __restrict__ pairs) {
-  __shared__ float As[2][BK32 * ROW32];
+  static_assert(kRows == 128 || kRows == 64, "tile rows");
+  constexpr int kMI = kRows / 32;       // 16-row blocks per wave, and A copy instructions per wave and step
+  constexpr int kRowsA = 256 / kRows;   // A rows filled by one copy instruction
+  __shared__ float As[2][BK32 * kRows];
   __shared__ float Bs[2][BK32 * ROW32];
 
   // tile order as in slice_gemm_kernel
@@ -223,7 +232,7 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
   const int tiles_m = ntiles / tiles_n;
   const int gsz = kGroup * tiles_n, g = t / gsz, first = g * kGroup;
   const int rows_in = min(kGroup, tiles_m - first), within = t - g * gsz;
-  const int64_t m0 = static_cast<int64_t>(first + within % rows_in) * BM;
+  const int64_t m0 = static_cast<int64_t>(first + within % rows_in) * kRows;
   const int64_t n0 = static_cast<int64_t>(within / rows_in) * BN;
   const int job = blockIdx.y;
   const uint32_t jw = jobs[3 * job], kw = jobs[3 * job + 2];
@@ -240,18 +249,27 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
   const int64_t kb0 = min(chunk * csz, nkb_all), nkb = min(csz, nkb_all - kb0);
   const int64_t niter = nkb * npairs;
 
-  // Copies: wave w fills rows 8w .. 8w+7 of each tile, two rows per instruction
-  // (q = 0..3); lane L lands at row 8w + 2q + L/32, granule L%32, and fetches
-  // the panel granule (L%32) ^ (((2q + L/32) & 3) << 2) of that row.
+  // Copies: wave w fills rows 8w .. 8w+7 of each tile.  B: two rows per
+  // instruction (q = 0..3); lane L lands at row 8w + 2q + L/32, granule L%32, and
+  // fetches the panel granule (L%32) ^ (((2q + L/32) & 3) << 2) of that row.  A:
+  // the same with kRows / 4 granules per row, kRowsA rows per instruction.
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int half = lane >> 5, gran = lane & 31;
-  int32_t off_a[4], off_b[4];  // per-lane source offsets in floats, rows 2q + half of the wave's block
+  const int row_in_a = lane / (kRows / 4), gran_a = lane % (kRows / 4);
+  int32_t off_a[kMI], off_b[4];  // per-lane source offsets in floats, relative to the wave's first row
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int r = 2 * q + half;
     const int sg = gran ^ ((r & 3) << 2);
-    off_a[q] = static_cast<int32_t>(r * mp + 4 * sg);
+    if (kRows == 128) off_a[q % kMI] = static_cast<int32_t>(r * mp + 4 * sg);
     off_b[q] = static_cast<int32_t>(r * np + 4 * sg);
+  }
+  if (kRows == 64) {
+#pragma unroll
+    for (int q = 0; q < kMI; ++q) {
+      const int r = kRowsA * q + row_in_a;
+      off_a[q] = static_cast<int32_t>(r * mp + 4 * (gran_a ^ ((r & 3) << 2)));
+    }
   }
   int lpi = 0;
   int64_t lkb = 0;
@@ -266,8 +284,9 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
   auto issue = [&](int stage) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a + off_a[q]),
-                                       (lds_void*)(&As[stage][(8 * wave_u + 2 * q) * ROW32]), 16, 0, 0);
+      if (q < kMI)
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(a + off_a[q]),
+                                         (lds_void*)(&As[stage][(8 * wave_u + kRowsA * q) * kRows]), 16, 0, 0);
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(b + off_b[q]),
                                        (lds_void*)(&Bs[stage][(8 * wave_u + 2 * q) * ROW32]), 16, 0, 0);
     }
@@ -283,21 +302,23 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
     }
   };
 
-  d4 acc[4][4];
+  d4 acc[kMI][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < kMI; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
 
-  // Fragments: lane l = 16h + c reads row 4kg + h, column block i at
-  // ((i ^ h) * 16 + c) after the swizzle (wr * 64 floats = 16 granules is untouched).
+  // Fragments: lane l = 16h + c reads row 4kg + h; the wave's column block
+  // kMI * wr + i (16 floats each) lies at block (kMI * wr + i) ^ h after the
+  // swizzle (for 128-row tiles that is wr * 64 + ((i ^ h) << 4): the swizzle
+  // stays within the wave's 64 floats).
   const int h = lane >> 4, c = lane & 15;
-  int fa[4], fb[4];
+  int fa[kMI], fb[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    fa[i] = h * ROW32 + wr * 64 + ((i ^ h) << 4) + c;
-    fb[i] = h * ROW32 + wc * 64 + ((i ^ h) << 4) + c;
-  }
+  for (int i = 0; i < kMI; ++i)
+    fa[i] = h * kRows + (kRows == 128 ? wr * 64 + ((i ^ h) << 4) : ((kMI * wr + i) ^ h) << 4) + c;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) fb[i] = h * ROW32 + wc * 64 + ((i ^ h) << 4) + c;
   if (niter > 0) issue(0);
   for (int64_t it = 0; it < niter; ++it) {
     const int cur = static_cast<int>(it & 1);
@@ -305,26 +326,26 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
     __syncthreads();                     // everyone's are; everyone is done reading the other stage
     const float* as = As[cur];
     const float* bs = Bs[cur];
-    float af[BK32 / 4][4], bf[BK32 / 4][4];
-    // fragments of k groups 2g and 2g + 1 (8 LDS instructions)
+    float af[BK32 / 4][kMI], bf[BK32 / 4][4];
+    // fragments of k groups 2g and 2g + 1 (2 (kMI + 4) LDS instructions)
     auto read = [&](int g) {
 #pragma unroll
       for (int kg = 2 * g; kg < 2 * g + 2; ++kg)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          af[kg][i] = as[kg * 4 * ROW32 + fa[i]];
+          if (i < kMI) af[kg][i] = as[kg * 4 * kRows + fa[i]];
           bf[kg][i] = bs[kg * 4 * ROW32 + fb[i]];
         }
     };
     auto mfma = [&](int kg) {
-      double ad[4], bd[4];
+      double ad[kMI], bd[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        ad[i] = static_cast<double>(af[kg][i]);
+        if (i < kMI) ad[i] = static_cast<double>(af[kg][i]);
         bd[i] = static_cast<double>(bf[kg][i]);
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kMI; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ad[i], bd[j], acc[i][j], 0, 0, 0);
@@ -358,12 +379,12 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
 
   double* o = out + out_plane * m * n;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < kMI; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t gi = m0 + wr * 64 + i * 16 + 4 * r + (lane >> 4);
+        const int64_t gi = m0 + wr * (kRows / 2) + i * 16 + 4 * r + (lane >> 4);
         const int64_t gj = n0 + wc * 64 + j * 16 + (lane & 15);
         if (gi < m && gj < n) o[gi * n + gj] = acc[i][j][r];
       }
@@ -389,12 +410,17 @@ hipError_t launch_slice_gemm32(int64_t m, int64_t n, int64_t k, const float* DAt
   if (m == 0 || n == 0 || jobs.njobs == 0) return hipSuccess;
   const int64_t mp = panel_mn(m), np = panel_mn(n), kp = panel_k32(k);
   const int64_t tiles_n = np / BN;
-  const int64_t ntiles = (mp / BM) * tiles_n;
+  const bool skinny = m <= 64;  // one 64-row tile row (within the panel's 128 padded rows)
+  const int64_t ntiles = (skinny ? 1 : mp / BM) * tiles_n;
   // per-lane copy offsets are 32-bit: 7 rows of a panel plus a row's width
   if (ntiles > 0x7fffffff || jobs.njobs > 65535 || mp > (1 << 27) || np > (1 << 27)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(slice_gemm32_kernel, dim3(static_cast<unsigned>(ntiles), static_cast<unsigned>(jobs.njobs)),
-                     dim3(kThreads), 0, stream, m, n, kp, mp, np, static_cast<int>(tiles_n),
-                     static_cast<int>(ntiles), DAt, DBp, out, jobs.jobs, jobs.pairs);
+  const dim3 grid(static_cast<unsigned>(ntiles), static_cast<unsigned>(jobs.njobs));
+  if (skinny)
+    hipLaunchKernelGGL(slice_gemm32_kernel<64>, grid, dim3(kThreads), 0, stream, m, n, kp, mp, np,
+                       static_cast<int>(tiles_n), static_cast<int>(ntiles), DAt, DBp, out, jobs.jobs, jobs.pairs);
+  else
+    hipLaunchKernelGGL(slice_gemm32_kernel<128>, grid, dim3(kThreads), 0, stream, m, n, kp, mp, np,
+                       static_cast<int>(tiles_n), static_cast<int>(ntiles), DAt, DBp, out, jobs.jobs, jobs.pairs);
   return hipGetLastError();
 }
 
