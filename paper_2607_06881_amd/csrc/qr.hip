@@ -442,44 +442,59 @@ __global__ void __launch_bounds__(kGramThreads) qr_gram_reduce_kernel(int jb, in
 }
 
 // T (upper triangular, jb x jb) of I - V T V^T = H_0 ... H_{jb-1} from
-// G = V^T V and tau: T(j, j) = tau_j, T(0:j, j) = -tau_j T(0:j, 0:j) G(0:j, j);
-// writes the transpose Tt.  Serial in j; for each j the sum of row i is split
-// over the kTLanes consecutive lanes of the row (lane q takes l = i + q,
-// i + q + kTLanes, ...) and reduced by shuffles within the wave, the result
-// taken from lane 0 (a fixed order).  T and G in dynamic LDS, 2 jb^2
-// double-doubles (128 KB at jb = 64).
-constexpr int kTLanes = 16;
-__host__ __device__ constexpr size_t qr_t_lds(int jb) { return 2 * sizeof(dd) * static_cast<size_t>(jb) * jb; }
+// G = V^T V and tau, by the recursive form of the compact WY factor (Elmroth
+// and Gustavson): for V = [V1 V2], T = [T11 T12; 0 T22] with T12 = -T11
+// (V1^T V2) T22.  The jb columns are padded to 64 (tau = 0, G = 0 there, which
+// leaves the leading jb x jb block unchanged) and the recursion runs bottom up:
+// at half width h = 1, 2, .., 32, the 32 / h diagonal blocks of width 2h form
+// X = G12 T22 (phase 1) and then T12 = -T11 X (phase 2), one entry per thread,
+// each a dot product in increasing index order.  Six levels of two phases
+// instead of 64 dependent steps.  Writes the transpose Tt.  T, G and X in
+// dynamic LDS (kTLds bytes).
+constexpr int kTThreads = 1024;
+constexpr int kTPad = 64;                                     // the padded width
+constexpr int kTX = kTPad * kTPad / 4;                        // entries of X at h = 32
+constexpr size_t kTLds = sizeof(dd) * (2 * kTPad * kTPad + kTX);  // 144 KB
+static_assert(kMaxNb <= kTPad && kTX <= kTThreads, "one X entry per thread");
 
-
-__global__ void __launch_bounds__(kMaxNb * kTLanes) qr_t_kernel(int jb, int64_t n, int64_t j0,
-                                                              const double* __restrict__ G,
-                                                              const double* __restrict__ tau,
-                                                              double* __restrict__ Tt) {
+__global__ void __launch_bounds__(kTThreads) qr_t_kernel(int jb, int64_t n, int64_t j0,
+                                                        const double* __restrict__ G,
+                                                        const double* __restrict__ tau,
+                                                        double* __restrict__ Tt) {
   extern __shared__ dd tsm[];
-  dd* T = tsm;             // T[i * jb + c]
-  dd* Gs = tsm + jb * jb;  // G[l * jb + c]
-  const int tid = threadIdx.x, i = tid / kTLanes, q = tid % kTLanes;
+  dd* T = tsm;                     // T[i * kTPad + c]
+  dd* Gs = tsm + kTPad * kTPad;    // G[l * kTPad + c]
+  dd* X = Gs + kTPad * kTPad;      // X of every block of a level, h x h each
+  const int tid = threadIdx.x;
   const int64_t pg = static_cast<int64_t>(jb) * jb;
-  for (int e = tid; e < jb * jb; e += kMaxNb * kTLanes) {
-    T[e] = {0.0, 0.0};
-    Gs[e] = ldd(G, pg, e);
+  for (int e = tid; e < kTPad * kTPad; e += kTThreads) {
+    const int r = e / kTPad, c = e % kTPad;
+    const bool in = r < jb && c < jb;
+    Gs[e] = in ? ldd(G, pg, static_cast<int64_t>(r) * jb + c) : dd{0.0, 0.0};
+    T[e] = r == c && r < jb ? ldd(tau, n, j0 + r) : dd{0.0, 0.0};
   }
   __syncthreads();
-  for (int j = 0; j < jb; ++j) {
-    dd s = {0.0, 0.0};
-    if (i < j)
-      for (int l = i + q; l < j; l += kTLanes) s = dd_add(s, dd_mul(T[i * jb + l], Gs[l * jb + j]));
-    for (int off = kTLanes / 2; off > 0; off >>= 1) s = dd_add(s, shfl_xor_dd(s, off));
-    if (q == 0 && i <= j) {
-      const dd tj = ldd(tau, n, j0 + j);
-      T[i * jb + j] = i < j ? dd_neg(dd_mul(tj, s)) : tj;
+  for (int h = 1; h < kTPad; h *= 2) {
+    const int e = tid, hh = h * h, bb = e / hh, w = e % hh, i = w / h, j = w % h;
+    const int a = 2 * h * bb;  // the block's first index
+    const bool act = e < (kTPad / 2) * h;
+    if (act) {  // X(i, j) = sum over l <= j of G(a + i, a + h + l) T(a + h + l, a + h + j)
+      dd s = {0.0, 0.0};
+      for (int l = 0; l <= j; ++l)
+        s = dd_add(s, dd_mul(Gs[(a + i) * kTPad + a + h + l], T[(a + h + l) * kTPad + a + h + j]));
+      X[e] = s;
+    }
+    __syncthreads();
+    if (act) {  // T(a + i, a + h + j) = -sum over l >= i of T(a + i, a + l) X(l, j)
+      dd s = {0.0, 0.0};
+      for (int l = i; l < h; ++l) s = dd_add(s, dd_mul(T[(a + i) * kTPad + a + l], X[bb * hh + l * h + j]));
+      T[(a + i) * kTPad + a + h + j] = dd_neg(s);
     }
     __syncthreads();
   }
-  for (int e = tid; e < jb * jb; e += kMaxNb * kTLanes) {
+  for (int e = tid; e < jb * jb; e += kTThreads) {
     const int r = e / jb, c = e % jb;
-    std_(Tt, pg, static_cast<int64_t>(c) * jb + r, T[e]);
+    std_(Tt, pg, static_cast<int64_t>(c) * jb + r, T[r * kTPad + c]);
   }
 }
 
@@ -607,13 +622,13 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
       (a0 < t0 + tbytes && t0 < a0 + abytes))
     return MDGEMM_EINVAL;
   const hipStream_t s = static_cast<hipStream_t>(stream);
-  // the T kernel's dynamic LDS beyond 64 KB (panels wider than 45 columns):
-  // allowed once for the kernel (a failure shows up as a launch error below)
+  // the T kernel's dynamic LDS beyond 64 KB: allowed once for the kernel (a
+  // failure shows up as a launch error below)
   static std::once_flag once;
   std::call_once(once, [] {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&mdg::qr_t_kernel),
                               hipFuncAttributeMaxDynamicSharedMemorySize,
-                              static_cast<int>(mdg::qr_t_lds(mdg::kMaxNb)));
+                              static_cast<int>(mdg::kTLds));
     (void)hipGetLastError();
   });
   char* ws = static_cast<char*>(workspace);
@@ -662,8 +677,7 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
                        dim3(mdg::kGramThreads), 0, s, jb, static_cast<int64_t>(ggroups), pgram, G);
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     int st = MDGEMM_OK;
-    hipLaunchKernelGGL(mdg::qr_t_kernel, dim3(1), dim3(mdg::kMaxNb * mdg::kTLanes), mdg::qr_t_lds(jb), s, jb, n, j0,
-                       G, tau, Tt);
+    hipLaunchKernelGGL(mdg::qr_t_kernel, dim3(1), dim3(mdg::kTThreads), mdg::kTLds, s, jb, n, j0, G, tau, Tt);
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     if ((st = mdgemm_ex(jb, nc, mp, 2, Vt, X, W, &o)) != MDGEMM_OK) return st;   // W = V^T X
     if ((st = mdgemm_ex(jb, nc, jb, 2, Tt, W, W2, &o)) != MDGEMM_OK) return st;  // W2 = T^T W
