@@ -46,16 +46,15 @@ __device__ inline void std_(double* P, int64_t plane, int64_t idx, dd v) {
 
 __device__ inline dd shfl_xor_dd(dd v, int off) { return {__shfl_xor(v.hi, off, 64), __shfl_xor(v.lo, off, 64)}; }
 
-// Sum of one dd per thread over the workgroup (tree in LDS); the result in red[0].
+// Sum of one dd per thread over the workgroup: a butterfly within each wave,
+// then the 16 wave sums in a fixed order; every thread gets the result.
 __device__ inline dd block_sum(dd v, dd* red) {
+  for (int off = 32; off > 0; off >>= 1) v = dd_add(v, shfl_xor_dd(v, off));
   const int tid = threadIdx.x;
-  red[tid] = v;
+  if ((tid & 63) == 0) red[tid >> 6] = v;
   __syncthreads();
-  for (int s = kPanelThreads / 2; s > 0; s >>= 1) {
-    if (tid < s) red[tid] = dd_add(red[tid], red[tid + s]);
-    __syncthreads();
-  }
-  const dd r = red[0];
+  dd r = red[0];
+  for (int w = 1; w < kPanelThreads / 64; ++w) r = dd_add(r, red[w]);
   __syncthreads();
   return r;
 }
@@ -118,11 +117,14 @@ __global__ void __launch_bounds__(kPanelThreads) qr_panel_kernel(int64_t m, int6
         for (int64_t r = r0 + 1 + rg; r < m; r += 32)
           acc = dd_add(acc, dd_mul(ldd(A, plane, r * n + cj), ldd(A, plane, r * n + j0 + c)));
       }
-      red[tid] = acc;
+      // the two row groups of a wave (lanes cc and 32 + cc) first, then the 16
+      // waves in order
+      acc = dd_add(acc, shfl_xor_dd(acc, 32));
+      if ((tid & 63) < 32) red[(tid >> 6) * 32 + cc] = acc;
       __syncthreads();
       if (rg == 0 && c < jb) {
         dd w = ldd(A, plane, r0 * n + j0 + c);
-        for (int g = 0; g < 32; ++g) w = dd_add(w, red[g * 32 + cc]);
+        for (int g = 0; g < kPanelThreads / 64; ++g) w = dd_add(w, red[g * 32 + cc]);
         wv[g0 + cc] = dd_mul(t, w);
       }
       __syncthreads();
