@@ -7,8 +7,8 @@
 // v_j(j) = 1, v_j zero above row j).  Panels of nb <= 64 columns are factored in
 // double-double arithmetic (dd.h), by one workgroup for short panels and by many
 // for tall ones (see qr_col_update_kernel); the panel's reflections are
-// accumulated in the compact form I - V T V^T (T upper triangular, the forward
-// recurrence of Schreiber and Van Loan), and the trailing columns are updated as
+// accumulated in the compact form I - V T V^T (T upper triangular, by the
+// recursive form of Elmroth and Gustavson), and the trailing columns are updated as
 //     A2 <- A2 - V (T^T (V^T A2))
 // with three products on mdgemm_ex (double-double in, double-double out, at the
 // adaptive digit width).  On return A holds R on and above the diagonal and the
