@@ -195,8 +195,8 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
 // of 64.  Each fragment value is widened back to FP64 (v_cvt_f64_f32, exact)
 // right before its MFMAs.
 //
-// LDS rows are 128 floats without padding, so that one global_load_lds_dwordx4
-// (64 lanes x 16 bytes) fills two rows in place; instead of padding, the 16-byte
+// LDS rows are 128 floats without padding, so that one buffer_load_dwordx4 ...
+// lds (64 lanes x 16 bytes) fills two rows in place; instead of padding, the 16-byte
 // granules of row r are stored XOR-swizzled by (r & 3) << 2.  A fragment read
 // (lanes 16h..16h+15 read row 4kg + h, 16 consecutive columns) then touches four
 // different 16-bank groups for h = 0..3: conflict-free.  Panels are k-major and
@@ -209,6 +209,117 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm_kernel(int64_t m, int6
 constexpr int BK32 = 32;
 constexpr int ROW32 = 128;  // floats per LDS row of B (and of A for 128-row tiles)
 
+// The k loop of slice_gemm32_kernel.  The two LDS stages (A0, B0 and A1, B1)
+// are restrict parameters, so that the fragment reads of one stage carry alias
+// scopes that exclude the copies in flight into the other: the compiler then
+// makes no read wait for them, and the next step's copies go out right after
+// the barrier, a whole step (128 MFMAs per wave) ahead of their use.  The
+// copies are buffer loads into LDS (counted on vmcnt only) from a resource
+// based at the current pair's rows; the loop is unrolled by two so that each
+// step's stages are fixed.  The four stage buffers must be distinct arrays for
+// the scopes to hold (halves of one array were not told apart, and every read
+// then waited for the copies).  Measured against the copies issued after the
+// last read (32 MFMAs ahead): 1.7-1.9% less level-GEMM time on four workloads,
+// the same bits.
+template <int kRows>
+__device__ __forceinline__ void gemm32_k_loop(float* __restrict__ A0, float* __restrict__ B0, float* __restrict__ A1,
+                                              float* __restrict__ B1, const float* DAt, const float* DBp,
+                                              const uint32_t* pairs, int pfirst, int npairs, int64_t nkb,
+                                              int64_t plane_a, int64_t plane_b, int64_t mp, int64_t np,
+                                              int64_t row_a, int64_t row_b, int wave_u,
+                                              const int32_t (&off_a)[kRows / 32], const int32_t (&off_b)[4],
+                                              const int (&fa)[kRows / 32], const int (&fb)[4],
+                                              d4 (&acc)[kRows / 32][4]) {
+  constexpr int kMI = kRows / 32, kRowsA = 256 / kRows;
+  const int64_t niter = nkb * npairs;
+  int lpi = 0;
+  int64_t lkb = 0;
+  // The pair word is read (scalar load) where the copies switch to the next pair
+  // and used at once, so that no scalar load is pending while the fragment reads
+  // are: the LDS counter then orders the reads alone and each group of MFMAs
+  // waits for its own reads only.
+  uint32_t pr = pairs[pfirst];
+  const float* a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
+  const float* b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
+  auto issue = [&](float* An, float* Bn) {
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a), 0, 0xffffffff, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(b), 0, 0xffffffff, 0x00020000);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (q < kMI)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(An + (8 * wave_u + kRowsA * q) * kRows), 16,
+                                                 4 * off_a[q], 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(Bn + (8 * wave_u + 2 * q) * ROW32), 16,
+                                               4 * off_b[q], 0, 0, 0);
+    }
+    if (++lkb == nkb) {
+      lkb = 0;
+      ++lpi;
+      if (lpi < npairs) pr = pairs[pfirst + lpi];
+      a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
+      b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
+    } else {
+      a += BK32 * mp;
+      b += BK32 * np;
+    }
+  };
+  auto step = [&](const float* as, const float* bs, float* An, float* Bn, bool more) {
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // this wave's copies of this step are in LDS
+    __syncthreads();                          // everyone's are; everyone is done reading the other stage
+    if (more) issue(An, Bn);
+    __builtin_amdgcn_sched_barrier(0);
+    float af[BK32 / 4][kMI], bf[BK32 / 4][4];
+    // fragments of k groups 2g and 2g + 1 (2 (kMI + 4) LDS instructions)
+    auto read = [&](int g) {
+#pragma unroll
+      for (int kg = 2 * g; kg < 2 * g + 2; ++kg)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (i < kMI) af[kg][i] = as[kg * 4 * kRows + fa[i]];
+          bf[kg][i] = bs[kg * 4 * ROW32 + fb[i]];
+        }
+    };
+    auto mfma = [&](int kg) {
+      double ad[kMI], bd[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (i < kMI) ad[i] = static_cast<double>(af[kg][i]);
+        bd[i] = static_cast<double>(bf[kg][i]);
+      }
+#pragma unroll
+      for (int i = 0; i < kMI; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ad[i], bd[j], acc[i][j], 0, 0, 0);
+    };
+    // The reads go out in four groups, each one MFMA group ahead of its use, so
+    // that at most 16 are outstanding and every wait is a partial one.
+    // sched_barrier keeps the compiler from merging the groups back together.
+    read(0);
+    read(1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(0);
+    mfma(1);
+    __builtin_amdgcn_sched_barrier(0);
+    read(2);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(2);
+    mfma(3);
+    __builtin_amdgcn_sched_barrier(0);
+    read(3);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(4);
+    mfma(5);
+    mfma(6);
+    mfma(7);
+  };
+  if (niter > 0) issue(A0, B0);
+  for (int64_t it = 0; it < niter; it += 2) {
+    step(A0, B0, A1, B1, it + 1 < niter);
+    if (it + 1 < niter) step(A1, B1, A0, B0, it + 2 < niter);
+  }
+}
+
 template <int kRows>
 __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, int64_t n, int64_t kp, int64_t mp,
                                                                    int64_t np, int tiles_n, int ntiles,
@@ -220,8 +331,11 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
   static_assert(kRows == 128 || kRows == 64, "tile rows");
   constexpr int kMI = kRows / 32;       // 16-row blocks per wave, and A copy instructions per wave and step
   constexpr int kRowsA = 256 / kRows;   // A rows filled by one copy instruction
-  __shared__ float As[2][BK32 * kRows];
-  __shared__ float Bs[2][BK32 * ROW32];
+  // the two LDS stages as four arrays (the k loop takes them as restrict pointers)
+  __shared__ __attribute__((aligned(1024))) float A0s[BK32 * kRows];
+  __shared__ __attribute__((aligned(1024))) float B0s[BK32 * ROW32];
+  __shared__ __attribute__((aligned(1024))) float A1s[BK32 * kRows];
+  __shared__ __attribute__((aligned(1024))) float B1s[BK32 * ROW32];
 
   // tile order as in slice_gemm_kernel
   int t = blockIdx.x;
@@ -271,37 +385,7 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
       off_a[q] = static_cast<int32_t>(r * mp + 4 * (gran_a ^ ((r & 3) << 2)));
     }
   }
-  int lpi = 0;
-  int64_t lkb = 0;
-  // The pair word is read (scalar load) where the copies switch to the next pair
-  // and used at once, so that no scalar load is pending while the fragment reads
-  // are: the LDS counter then orders the reads alone and each group of MFMAs
-  // waits for its own reads only.
-  uint32_t pr = pairs[pfirst];
   const int64_t row_a = (kb0 * BK32 + 8 * wave_u) * mp + m0, row_b = (kb0 * BK32 + 8 * wave_u) * np + n0;
-  const float* a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
-  const float* b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
-  auto issue = [&](int stage) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (q < kMI)
-        __builtin_amdgcn_global_load_lds(static_cast<const void*>(a + off_a[q]),
-                                         (lds_void*)(&As[stage][(8 * wave_u + kRowsA * q) * kRows]), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(static_cast<const void*>(b + off_b[q]),
-                                       (lds_void*)(&Bs[stage][(8 * wave_u + 2 * q) * ROW32]), 16, 0, 0);
-    }
-    if (++lkb == nkb) {
-      lkb = 0;
-      ++lpi;
-      if (lpi < npairs) pr = pairs[pfirst + lpi];
-      a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
-      b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
-    } else {
-      a += BK32 * mp;
-      b += BK32 * np;
-    }
-  };
-
   d4 acc[kMI][4];
 #pragma unroll
   for (int i = 0; i < kMI; ++i)
@@ -319,63 +403,8 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
     fa[i] = h * kRows + (kRows == 128 ? wr * 64 + ((i ^ h) << 4) : ((kMI * wr + i) ^ h) << 4) + c;
 #pragma unroll
   for (int i = 0; i < 4; ++i) fb[i] = h * ROW32 + wc * 64 + ((i ^ h) << 4) + c;
-  if (niter > 0) issue(0);
-  for (int64_t it = 0; it < niter; ++it) {
-    const int cur = static_cast<int>(it & 1);
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // this wave's copies of step it are in LDS
-    __syncthreads();                     // everyone's are; everyone is done reading the other stage
-    const float* as = As[cur];
-    const float* bs = Bs[cur];
-    float af[BK32 / 4][kMI], bf[BK32 / 4][4];
-    // fragments of k groups 2g and 2g + 1 (2 (kMI + 4) LDS instructions)
-    auto read = [&](int g) {
-#pragma unroll
-      for (int kg = 2 * g; kg < 2 * g + 2; ++kg)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (i < kMI) af[kg][i] = as[kg * 4 * kRows + fa[i]];
-          bf[kg][i] = bs[kg * 4 * ROW32 + fb[i]];
-        }
-    };
-    auto mfma = [&](int kg) {
-      double ad[kMI], bd[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (i < kMI) ad[i] = static_cast<double>(af[kg][i]);
-        bd[i] = static_cast<double>(bf[kg][i]);
-      }
-#pragma unroll
-      for (int i = 0; i < kMI; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ad[i], bd[j], acc[i][j], 0, 0, 0);
-    };
-    // The reads go out in four groups, each one MFMA group ahead of its use, so
-    // that at most 16 are outstanding and every wait is a partial one; the copies
-    // of the next step follow the last read (no LDS read of this step comes after
-    // a copy in flight) and land while the last 32 MFMAs run.  sched_barrier
-    // keeps the compiler from merging the groups back together.
-    read(0);
-    read(1);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma(0);
-    mfma(1);
-    __builtin_amdgcn_sched_barrier(0);
-    read(2);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma(2);
-    mfma(3);
-    __builtin_amdgcn_sched_barrier(0);
-    read(3);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma(4);
-    mfma(5);
-    __builtin_amdgcn_sched_barrier(0);
-    if (it + 1 < niter) issue(cur ^ 1);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma(6);
-    mfma(7);
-  }
+  gemm32_k_loop<kRows>(A0s, B0s, A1s, B1s, DAt, DBp, pairs, pfirst, npairs, nkb, plane_a, plane_b, mp, np,
+                       row_a, row_b, wave_u, off_a, off_b, fa, fb, acc);
 
   double* o = out + out_plane * m * n;
 #pragma unroll
