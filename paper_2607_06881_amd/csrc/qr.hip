@@ -27,6 +27,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <mutex>
+#include <type_traits>
 
 #include "dd.h"
 #include "internal.h"
@@ -148,7 +149,9 @@ __global__ void __launch_bounds__(kPanelThreads) qr_panel_kernel(int64_t m, int6
 }
 
 // Tall panels (more than kSmallPanel rows) are factored by many workgroups, two
-// launches per column, each workgroup owning kPanelRows consecutive panel rows:
+// launches per column, each workgroup owning kRows consecutive panel rows (16 for
+// panels of at most kShortPanel rows, so that they still spread over the chip,
+// 32 above):
 //   qr_col_update_kernel(j): apply H_{j-1} to columns j .. jb-1 of the block's
 //     rows (w from the partial dot products of the previous launch), then write
 //     the block's part of sigma_j (rows below the pivot) and, from the block
@@ -160,7 +163,8 @@ __global__ void __launch_bounds__(kPanelThreads) qr_panel_kernel(int64_t m, int6
 //     pivot row entering with v = 1.
 // Every block writes all of its partial slots (zeros when it holds no row at or
 // below the pivot), so the sums never read a stale slot.
-constexpr int kPanelRows = 32;
+constexpr int kPanelRowsShort = 16, kPanelRowsTall = 32;
+constexpr int64_t kShortPanel = 2048;
 constexpr int kColThreads = 256;  // 32 column lanes x 8 row groups
 constexpr int64_t kSmallPanel = 256;
 
@@ -176,42 +180,44 @@ __device__ inline dd block_sum256(dd v, dd* red) {
   return r;
 }
 
-constexpr int kRowGroups = kColThreads / 32;                // 8
-constexpr int kRowsPerThread = kPanelRows / kRowGroups;      // rows rb + rg + 8 q, q < 4
+constexpr int kRowGroups = kColThreads / 32;                // 8: rows rb + rg + 8 q
 constexpr int kColGroups = kMaxNb / 32;                      // columns c0 + 32 h + cc, h < 2
-static_assert(kPanelRows % kRowGroups == 0 && kMaxNb % 32 == 0, "thread layout of the column kernels");
+static_assert(kPanelRowsShort % kRowGroups == 0 && kPanelRowsTall % kRowGroups == 0 && kMaxNb % 32 == 0,
+              "thread layout of the column kernels");
 
+template <int kRows>
 __global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, int64_t n, int64_t j0, int jb, int j,
                                                                     double* __restrict__ A,
                                                                     const double* __restrict__ tau,
                                                                     double* __restrict__ psig,
                                                                     const double* __restrict__ pw,
                                                                     double* __restrict__ px1) {
+  constexpr int kRPT = kRows / kRowGroups;  // rows per thread
   __shared__ dd red[kColThreads];
   __shared__ dd tw[kMaxNb];
   const int64_t plane = m * n;
   const int tid = threadIdx.x, cc = tid & 31, rg = tid >> 5;
   const int64_t G = gridDim.x;
-  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kPanelRows, re = min(m, rb + kPanelRows);
+  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kRows, re = min(m, rb + kRows);
   const int64_t r0 = j0 + j, rp = r0 - 1;  // the pivot rows of column j and of column j - 1
   // The entries this thread updates, loaded before the partials are folded (they
   // do not depend on them): rows rb + rg + 8 q of columns j + 32 h + cc from the
   // previous pivot row down (column j alone, from its pivot down, when j = 0),
   // and v_{j-1} at the same rows (1 at its pivot row).
-  dd av[kColGroups][kRowsPerThread], vv[kRowsPerThread];
+  dd av[kColGroups][kRPT], vv[kRPT];
   const int64_t rlo = j > 0 ? rp : r0;
 #pragma unroll
   for (int h = 0; h < kColGroups; ++h) {
     const int c = j + 32 * h + cc;
 #pragma unroll
-    for (int q = 0; q < kRowsPerThread; ++q) {
+    for (int q = 0; q < kRPT; ++q) {
       const int64_t r = rb + rg + kRowGroups * q;
       const bool ok = c < jb && (j > 0 || c == j) && r >= rlo && r < re;
       av[h][q] = ok ? ldd(A, plane, r * n + j0 + c) : dd{0.0, 0.0};
     }
   }
 #pragma unroll
-  for (int q = 0; q < kRowsPerThread; ++q) {
+  for (int q = 0; q < kRPT; ++q) {
     const int64_t r = rb + rg + kRowGroups * q;
     vv[q] = j > 0 && r > rp && r < re ? ldd(A, plane, r * n + j0 + j - 1) : dd{r == rp ? 1.0 : 0.0, 0.0};
   }
@@ -247,7 +253,7 @@ __global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, i
       if (c < jb) {
         const dd t = tw[32 * h + cc];
 #pragma unroll
-        for (int q = 0; q < kRowsPerThread; ++q) {
+        for (int q = 0; q < kRPT; ++q) {
           const int64_t r = rb + rg + kRowGroups * q;
           if (r >= rp && r < re) {
             av[h][q] = dd_sub(av[h][q], dd_mul(t, vv[q]));
@@ -262,7 +268,7 @@ __global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, i
   dd part = {0.0, 0.0};
   if (cc == 0) {
 #pragma unroll
-    for (int q = 0; q < kRowsPerThread; ++q) {
+    for (int q = 0; q < kRPT; ++q) {
       const int64_t r = rb + rg + kRowGroups * q;
       if (r > r0 && r < re) part = dd_add(part, dd_mul(av[0][q], av[0][q]));
       if (r == r0) std_(px1, kMaxNb, j, av[0][q]);
@@ -271,34 +277,36 @@ __global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, i
   const dd sig = block_sum256(part, red);
   if (tid == 0) std_(psig, G, blockIdx.x, sig);
 }
+template <int kRows>
 __global__ void __launch_bounds__(kColThreads) qr_col_reflect_kernel(int64_t m, int64_t n, int64_t j0, int jb, int j,
                                                                      double* __restrict__ A, double* __restrict__ tau,
                                                                      const double* __restrict__ psig,
                                                                      double* __restrict__ pw,
                                                                      const double* __restrict__ px1) {
+  constexpr int kRPT = kRows / kRowGroups;  // rows per thread
   __shared__ dd red[kColThreads];
-  __shared__ dd vs[kPanelRows];
+  __shared__ dd vs[kRows];
   __shared__ dd s_scale, s_tau;
   __shared__ int s_mode;
   const int64_t plane = m * n;
   const int tid = threadIdx.x, cc = tid & 31, rg = tid >> 5;
   const int64_t G = gridDim.x;
-  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kPanelRows, re = min(m, rb + kPanelRows);
+  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kRows, re = min(m, rb + kRows);
   const int64_t r0 = j0 + j;
   // Loaded before sigma is formed (none of them depends on it): column j below
   // the pivot (one row per thread of the first 32) and the trailing columns
   // j + 1 + 32 h + cc at rows rb + rg + 8 q at or below the pivot.
   dd xv = {0.0, 0.0};
-  if (tid < kPanelRows) {
+  if (tid < kRows) {
     const int64_t r = rb + tid;
     if (r > r0 && r < re) xv = ldd(A, plane, r * n + j0 + j);
   }
-  dd av[kColGroups][kRowsPerThread];
+  dd av[kColGroups][kRPT];
 #pragma unroll
   for (int h = 0; h < kColGroups; ++h) {
     const int c = j + 1 + 32 * h + cc;
 #pragma unroll
-    for (int q = 0; q < kRowsPerThread; ++q) {
+    for (int q = 0; q < kRPT; ++q) {
       const int64_t r = rb + rg + kRowGroups * q;
       av[h][q] = c < jb && r >= r0 && r < re ? ldd(A, plane, r * n + j0 + c) : dd{0.0, 0.0};
     }
@@ -329,7 +337,7 @@ __global__ void __launch_bounds__(kColThreads) qr_col_reflect_kernel(int64_t m, 
   }
   __syncthreads();
   const int mode = s_mode;
-  if (tid < kPanelRows) {
+  if (tid < kRows) {
     const int64_t r = rb + tid;
     dd v = {0.0, 0.0};
     if (r == r0) {
@@ -351,7 +359,7 @@ __global__ void __launch_bounds__(kColThreads) qr_col_reflect_kernel(int64_t m, 
     dd acc = {0.0, 0.0};
     if (c < jb) {
 #pragma unroll
-      for (int q = 0; q < kRowsPerThread; ++q) {
+      for (int q = 0; q < kRPT; ++q) {
         const int64_t r = rb + rg + kRowGroups * q;
         if (r >= r0 && r < re) acc = dd_add(acc, dd_mul(vs[r - rb], av[h][q]));
       }
@@ -565,7 +573,7 @@ bool qr_layout(int64_t m, int64_t n, int nb, QrLayout* L) {
   L->p = off;
   off += xbytes;
   // partial sums of the multi-workgroup panel: sigma [G], w [G][32], x1 [32]
-  const size_t groups = static_cast<size_t>((m + kPanelRows - 1) / kPanelRows);
+  const size_t groups = static_cast<size_t>((m + kPanelRowsShort - 1) / kPanelRowsShort);  // at most
   L->psig = off;
   off += align256(dd_bytes * groups);
   L->pw = off;
@@ -656,13 +664,20 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
     if (mp <= mdg::kSmallPanel) {
       hipLaunchKernelGGL(mdg::qr_panel_kernel, dim3(1), dim3(mdg::kPanelThreads), 0, s, m, n, j0, jb, A, tau);
     } else {
-      const unsigned groups = static_cast<unsigned>((mp + mdg::kPanelRows - 1) / mdg::kPanelRows);
-      for (int j = 0; j < jb; ++j) {
-        hipLaunchKernelGGL(mdg::qr_col_update_kernel, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0, jb, j, A,
-                           tau, psig, pw, px1);
-        hipLaunchKernelGGL(mdg::qr_col_reflect_kernel, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0, jb, j,
-                           A, tau, psig, pw, px1);
-      }
+      auto columns = [&](auto rows) {
+        constexpr int kRows = decltype(rows)::value;
+        const unsigned groups = static_cast<unsigned>((mp + kRows - 1) / kRows);
+        for (int j = 0; j < jb; ++j) {
+          hipLaunchKernelGGL(mdg::qr_col_update_kernel<kRows>, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0,
+                             jb, j, A, tau, psig, pw, px1);
+          hipLaunchKernelGGL(mdg::qr_col_reflect_kernel<kRows>, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0,
+                             jb, j, A, tau, psig, pw, px1);
+        }
+      };
+      if (mp > mdg::kShortPanel)
+        columns(std::integral_constant<int, mdg::kPanelRowsTall>{});
+      else
+        columns(std::integral_constant<int, mdg::kPanelRowsShort>{});
     }
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     if (nc == 0) break;
