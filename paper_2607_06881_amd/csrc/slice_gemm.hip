@@ -361,7 +361,6 @@ __global__ void __launch_bounds__(kThreads, 2) slice_gemm32_kernel(int64_t m, in
 
   const int64_t nkb_all = kp / BK32, csz = (nkb_all + ksplit - 1) / ksplit;
   const int64_t kb0 = min(chunk * csz, nkb_all), nkb = min(csz, nkb_all - kb0);
-  const int64_t niter = nkb * npairs;
 
   // Copies: wave w fills rows 8w .. 8w+7 of each tile.  B: two rows per
   // instruction (q = 0..3); lane L lands at row 8w + 2q + L/32, granule L%32, and
