@@ -380,15 +380,19 @@ bool panels_f32(const Planned& pl, int w) {
 // pair.  (Measured on 1024^3 double-double: 384 blocks split 4 ways run the
 // level GEMM at 87% of peak instead of 58%; 960 blocks gain nothing from a
 // split and the extra planes cost accumulation time.)
-int ksplit_for(int64_t m, int64_t n, int64_t k, const Planned& pl, bool f32) {
-  const int64_t tiles = (mdg::panel_mn(m) / mdg::kTileMN) * (mdg::panel_mn(n) / mdg::kTileMN);
-  const int64_t blocks = tiles * static_cast<int64_t>(pl.s.job_first.size());
-  const int64_t nkb = f32 ? mdg::panel_k32(k) / mdg::kTileK32 : mdg::panel_k(k) / mdg::kTileK;
+int ksplit_count(int64_t blocks, int64_t nkb) {
   constexpr int64_t kFull = 768, kTarget = 1280;
   if (blocks <= 0 || blocks >= kFull) return 1;
   int64_t sigma = (kTarget + blocks - 1) / blocks;
   sigma = std::min<int64_t>(sigma, std::min<int64_t>(8, nkb / 8));
   return static_cast<int>(std::max<int64_t>(sigma, 1));
+}
+
+int ksplit_for(int64_t m, int64_t n, int64_t k, const Planned& pl, bool f32) {
+  const int64_t tiles = (mdg::panel_mn(m) / mdg::kTileMN) * (mdg::panel_mn(n) / mdg::kTileMN);
+  const int64_t blocks = tiles * static_cast<int64_t>(pl.s.job_first.size());
+  const int64_t nkb = f32 ? mdg::panel_k32(k) / mdg::kTileK32 : mdg::panel_k(k) / mdg::kTileK;
+  return ksplit_count(blocks, nkb);
 }
 
 // The schedule a product runs: the planned one, split in k when it is small.
@@ -406,10 +410,19 @@ std::shared_ptr<const Planned> planned_for(int S, int T, int64_t m, int64_t n, i
 // heaviest level's pairs in series).  Each level belongs to one of the four
 // waves, levels dealt heaviest first to the least loaded wave; the product
 // qualifies while the most loaded wave runs at most 2048 MFMAs (about 55 us at
-// the matrix pipe's rate).  kc: the largest k chunk (a multiple of 4, at most
-// 256) whose digits fit the kernel's LDS beside the levels.
+// the matrix pipe's rate).  Beyond k (S + L) = 3840 (the limbs read and digits
+// written per line of a tile) the product is left to the staged path when that
+// path splits k (its level GEMM then spreads over the chip): the fused time
+// grows with k (S + L), about 85 us per 256 of k for double-double at 5-6
+// digits, and the measured crossover lies there (k = 384 fused and 512 staged
+// at 13-bit digits, 448 and 512 at 20 bits, double-double outputs of 17 x 33
+// and 64 x 960); without a k split the staged GEMM runs few blocks and the
+// fused path stays faster (256 x 400 x 256: 180 against 458 us).  kc: the
+// largest k chunk (a multiple of 4, at most 256) whose digits fit the kernel's
+// LDS beside the levels.
 constexpr int64_t kSmallMaxTiles = 256;
 constexpr int64_t kSmallMaxWaveMfma = 2048;
+constexpr int64_t kSmallMaxSplitWork = 3840;
 
 bool small_plan(int64_t m, int64_t n, int64_t k, int limbs, const Resolved& r, int* kc_out,
                 mdg::SmallLevelOwners* owners) {
@@ -420,6 +433,11 @@ bool small_plan(int64_t m, int64_t n, int64_t k, int limbs, const Resolved& r, i
   if (limbs > mdg::kSmallMaxLimbs || r.T + 1 > mdg::kSmallMaxLevels || k < 1 || r.w > 24) return false;
   if (r.w * r.S + 52 > 64 * mdg::kSmallSplitWords || r.w * r.T + 55 > 64 * mdg::kSmallAccumWords) return false;
   if (((m + 15) / 16) * ((n + 15) / 16) > kSmallMaxTiles) return false;
+  if (k * (r.S + limbs) > kSmallMaxSplitWork) {
+    // the staged pair schedule: T + 1 level jobs per 128 x 128 tile, FP32 panels
+    const int64_t tiles = (mdg::panel_mn(m) / mdg::kTileMN) * (mdg::panel_mn(n) / mdg::kTileMN);
+    if (ksplit_count(tiles * (r.T + 1), mdg::panel_k32(k) / mdg::kTileK32) > 1) return false;
+  }
   int load[4] = {0, 0, 0, 0};
   bool done[mdg::kSmallMaxLevels] = {};
   for (int rep = 0; rep <= r.T; ++rep) {
