@@ -198,6 +198,29 @@ def test_workspace_layout_of_staged_and_fused_products(lib):
     assert lay["np"] == 384 and lay["planes"] == 12 and lay["total"] == md.mdgemm_workspace_bytes(300, 270, 100, 3)
 
 
+def _fused(m, n, k, L, **opts):
+    try:
+        md.mdgemm_workspace_layout(m, n, k, L, **opts)
+    except md.MdgemmError as e:
+        return e.status == md.MDGEMM_EINVAL
+    return False
+
+
+def test_fused_path_leaves_long_k_to_a_k_split_staged_path(lib):
+    # k (S + L) above 3840 goes to the staged path when its level GEMM splits k
+    # (8 k steps of 32 per chunk, fewer than 768 blocks of 128 x 128 tiles and
+    # levels), and stays fused when it would not
+    auto = md.MDGEMM_SLICE_BITS_AUTO
+    assert _fused(17, 33, 384, 2)                          # 384 (8 + 2) = 3840
+    assert _fused(17, 33, 392, 2)                          # 3920, but 13 k steps: no split
+    assert not _fused(17, 33, 512, 2)                      # 16 k steps: split in 2
+    assert _fused(64, 960, 448, 2, slice_bits=auto)        # 20-bit digits, S = 6: 3584
+    assert not _fused(64, 960, 512, 2, slice_bits=auto)    # 4096, 16 k steps: split in 2
+    assert not _fused(64, 960, 1024, 2, slice_bits=auto)
+    assert _fused(256, 256, 400, 2)                        # 4000, but 13 k steps: no split
+    assert _fused(64, 64, 64, 2) and _fused(45, 60, 130, 4)
+
+
 def test_binding_refuses_cpu_tensors(lib):
     import torch
 
