@@ -213,14 +213,16 @@ constexpr int ROW32 = 128;  // floats per LDS row of B (and of A for 128-row til
 // are restrict parameters, so that the fragment reads of one stage carry alias
 // scopes that exclude the copies in flight into the other: the compiler then
 // makes no read wait for them, and the next step's copies go out right after
-// the barrier, a whole step (128 MFMAs per wave) ahead of their use.  The
+// the step's first fragment reads, a whole step (128 MFMAs per wave) ahead of
+// their use.  The
 // copies are buffer loads into LDS (counted on vmcnt only) from a resource
 // based at the current pair's rows; the loop is unrolled by two so that each
 // step's stages are fixed.  The four stage buffers must be distinct arrays for
 // the scopes to hold (halves of one array were not told apart, and every read
 // then waited for the copies).  Measured against the copies issued after the
 // last read (32 MFMAs ahead): 1.7-1.9% less level-GEMM time on four workloads,
-// the same bits.
+// the same bits; issuing them after the first two read groups instead of
+// before them, another 0.3-0.6%.
 template <int kRows>
 __device__ __forceinline__ void gemm32_k_loop(float* __restrict__ A0, float* __restrict__ B0, float* __restrict__ A1,
                                               float* __restrict__ B1, const float* DAt, const float* DBp,
@@ -266,8 +268,6 @@ __device__ __forceinline__ void gemm32_k_loop(float* __restrict__ A0, float* __r
   auto step = [&](const float* as, const float* bs, float* An, float* Bn, bool more) {
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // this wave's copies of this step are in LDS
     __syncthreads();                          // everyone's are; everyone is done reading the other stage
-    if (more) issue(An, Bn);
-    __builtin_amdgcn_sched_barrier(0);
     float af[BK32 / 4][kMI], bf[BK32 / 4][4];
     // fragments of k groups 2g and 2g + 1 (2 (kMI + 4) LDS instructions)
     auto read = [&](int g) {
@@ -297,6 +297,8 @@ __device__ __forceinline__ void gemm32_k_loop(float* __restrict__ A0, float* __r
     // sched_barrier keeps the compiler from merging the groups back together.
     read(0);
     read(1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (more) issue(An, Bn);
     __builtin_amdgcn_sched_barrier(0);
     mfma(0);
     mfma(1);
