@@ -214,15 +214,14 @@ constexpr int ROW32 = 128;  // floats per LDS row of B (and of A for 128-row til
 // scopes that exclude the copies in flight into the other: the compiler then
 // makes no read wait for them, and the next step's copies go out right after
 // the step's first fragment reads, a whole step (128 MFMAs per wave) ahead of
-// their use.  The
-// copies are buffer loads into LDS (counted on vmcnt only) from a resource
-// based at the current pair's rows; the loop is unrolled by two so that each
-// step's stages are fixed.  The four stage buffers must be distinct arrays for
-// the scopes to hold (halves of one array were not told apart, and every read
-// then waited for the copies).  Measured against the copies issued after the
-// last read (32 MFMAs ahead): 1.7-1.9% less level-GEMM time on four workloads,
-// the same bits; issuing them after the first two read groups instead of
-// before them, another 0.3-0.6%.
+// their use.  The copies are buffer loads into LDS (counted on vmcnt only) from
+// a resource based at the current pair's rows; the loop is unrolled by two so
+// that each step's stages are fixed.  The four stage buffers must be distinct
+// arrays for the scopes to hold (halves of one array were not told apart, and
+// every read then waited for the copies).  Measured against the copies issued
+// after the last read (32 MFMAs ahead): 1.7-1.9% less level-GEMM time on four
+// workloads, the same bits; issuing them after the first two read groups
+// instead of before them, another 0.3-0.6%.
 template <int kRows>
 __device__ __forceinline__ void gemm32_k_loop(float* __restrict__ A0, float* __restrict__ B0, float* __restrict__ A1,
                                               float* __restrict__ B1, const float* DAt, const float* DBp,
