@@ -28,6 +28,9 @@ constexpr int kTileK = 16;    // level-GEMM k step
 inline int64_t panel_k(int64_t k) { return (k + kTileK - 1) / kTileK * kTileK; }
 // FP32 panels (every digit and digit sum below 2^24) use 32-deep k steps.
 constexpr int kTileK32 = 32;
+// Word 3 of the raw buffer descriptors of the buffer-to-LDS copies (the level
+// GEMM kernels): the DATA_FORMAT field (bits 15-18) set to 4, 32-bit elements.
+constexpr int kBufferWord3 = 0x00020000;
 inline int64_t panel_k32(int64_t k) { return (k + kTileK32 - 1) / kTileK32 * kTileK32; }
 inline int64_t panel_mn(int64_t x) { return (x + kTileMN - 1) / kTileMN * kTileMN; }
 

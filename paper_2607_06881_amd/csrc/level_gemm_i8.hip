@@ -95,8 +95,8 @@ __device__ __forceinline__ void tile_loop(int8_t* __restrict__ P0, int8_t* __res
                                           const int8_t* b, uint32_t na, uint32_t nb, int nst, uint32_t qs,
                                           uint32_t lo0, uint32_t lo1, int fa0, int fa1, int fb0, int fb1, int wave,
                                           v4i (&acc)[8][4]) {
-  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a), 0, na, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(b), 0, nb, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a), 0, na, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(b), 0, nb, kBufferWord3);
   // copy q (0..3) of stage s into buffer P: tile rows 32 wave + 8q .. +7 of A and of B
   auto copy = [&](int8_t* P, int s, int q) {
     const uint32_t so = static_cast<uint32_t>(s) * kStage + static_cast<uint32_t>(q) * qs;

@@ -243,8 +243,11 @@ __device__ __forceinline__ void gemm32_k_loop(float* __restrict__ A0, float* __r
   const float* a = DAt + static_cast<int64_t>(pr & 0xffffu) * plane_a + row_a;
   const float* b = DBp + static_cast<int64_t>(pr >> 16) * plane_b + row_b;
   auto issue = [&](float* An, float* Bn) {
-    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a), 0, 0xffffffff, 0x00020000);
-    const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(b), 0, 0xffffffff, 0x00020000);
+    // the largest record count: no range limit (the copies stay within the panels)
+    const __amdgpu_buffer_rsrc_t ra =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a), 0, 0xffffffff, kBufferWord3);
+    const __amdgpu_buffer_rsrc_t rb =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(b), 0, 0xffffffff, kBufferWord3);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if (q < kMI)
