@@ -38,6 +38,29 @@ constexpr int kTile = 16;
 constexpr int kThreads = 256;
 constexpr int kBatch = 4;  // elements whose limbs a thread loads before splitting them
 
+// The S digits of one element (limbs xs, grid exponent g) to out[s * stride],
+// FP32.  Digit windows of at most 128 bits (w S <= 128: double-double at 13-bit
+// digits and the adaptive widths) take the 128-bit integer floor, windows of at
+// most 256 bits (triple- and quad-double) the 256-bit one, the others the
+// general one (the same digits).
+template <int NW, int ML>
+__device__ inline void split_into(const double (&xs)[ML], int L, int g, int S, int w, float* __restrict__ out,
+                                  int64_t stride) {
+  if (w * S <= 128) {
+    uint64_t I[2];
+    const bool neg = floor_on_grid_128<ML>(xs, L, g, I);
+    store_digits<2, float>(I, S, w, neg, out, stride);
+  } else if (w * S <= 256) {
+    uint64_t I[4];
+    const bool neg = floor_on_grid_256<ML>(xs, L, g, I);
+    store_digits<4, float>(I, S, w, neg, out, stride);
+  } else {
+    uint64_t I[NW];
+    const bool neg = floor_on_grid<NW, ML>(xs, L, g, I);
+    store_digits<NW, float>(I, S, w, neg, out, stride);
+  }
+}
+
 __device__ inline int wave_max_i(int v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v = max(v, __shfl_xor(v, off, 64));
@@ -117,9 +140,7 @@ __global__ void __launch_bounds__(kThreads) small_product_kernel(int64_t m, int6
         const int e = e0 + b * kThreads + tid, row = e / kn4, kk = e - row * kn4;
         if (e >= kTile * kn4) break;
         float* out = sA + row * lda + kk;
-        uint64_t I[NWS];
-        const bool neg = floor_on_grid<NWS, ML>(xs[b], L, eA[row] - w * S, I);  // zero limbs: zero digits
-        store_digits<NWS, float>(I, S, w, neg, out, kTile * lda);
+        split_into<NWS, ML>(xs[b], L, eA[row] - w * S, S, w, out, kTile * lda);  // zero limbs: zero digits
       }
     }
     for (int e0 = 0; e0 < kn4 * kTile; e0 += kThreads * kBatch) {
@@ -136,9 +157,7 @@ __global__ void __launch_bounds__(kThreads) small_product_kernel(int64_t m, int6
         const int e = e0 + b * kThreads + tid, kk = e >> 4, col = e & 15;
         if (e >= kn4 * kTile) break;
         float* out = sB + kk * kTile + col;
-        uint64_t I[NWS];
-        const bool neg = floor_on_grid<NWS, ML>(xs[b], L, eB[col] - w * S, I);
-        store_digits<NWS, float>(I, S, w, neg, out, kc * kTile);
+        split_into<NWS, ML>(xs[b], L, eB[col] - w * S, S, w, out, kc * kTile);
       }
     }
     __syncthreads();
