@@ -87,7 +87,8 @@ __global__ void __launch_bounds__(256) accumulate_kernel(int64_t m, int64_t n, i
     uint64_t N[NW];
     accumulate_levels<NW>(N, G, levels, w, plane, idx);
     const uint64_t ext = (N[NW - 1] >> 63) ? ~0ull : 0ull;
-    for (int w = 0; w < kZWords; ++w) Z[static_cast<int64_t>(w) * plane + idx] = static_cast<int64_t>(w < NW ? word_at<NW>(N, w) : ext);
+    for (int w = 0; w < kZWords; ++w)
+      Z[static_cast<int64_t>(w) * plane + idx] = static_cast<int64_t>(w < NW ? word_at<NW>(N, w) : ext);
   }
 }
 

@@ -99,7 +99,9 @@ bool width_ok(int S, int w) { return S >= 1 && S <= MDGEMM_MAX_SLICES && w >= 1 
                                      S * w <= mdg::kMaxDigitBits; }
 
 // w (levels - 1) + 55 bits must fit the widest accumulation (kZWords words)
-bool levels_ok(int levels, int w) { return levels >= 1 && levels <= mdg::kMaxLevels && mdg::accum_words(levels, w) <= mdg::kZWords; }
+bool levels_ok(int levels, int w) {
+  return levels >= 1 && levels <= mdg::kMaxLevels && mdg::accum_words(levels, w) <= mdg::kZWords;
+}
 
 // ---- schedules -------------------------------------------------------------
 

@@ -243,7 +243,8 @@ __global__ void __launch_bounds__(256) zero_i32_kernel(int32_t* __restrict__ p, 
 
 bool level_gemm_i8_fits(int64_t kp, int S) {
   const int64_t ld = kI8Pad + static_cast<int64_t>(S) * kp;
-  return S >= 1 && S <= kI8MaxSlices && kp > 0 && kp % kStage == 0 && static_cast<int64_t>(kTile) * ld < (int64_t{1} << 31);
+  return S >= 1 && S <= kI8MaxSlices && kp > 0 && kp % kStage == 0 &&
+         static_cast<int64_t>(kTile) * ld < (int64_t{1} << 31);
 }
 
 hipError_t launch_level_gemm_i8(int64_t m, int64_t n, int64_t kp, int S, int T, const int8_t* DA, const int8_t* DBt,

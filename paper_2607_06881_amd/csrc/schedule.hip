@@ -457,7 +457,8 @@ Schedule split_k(const Schedule& s, int sigma) {
       ent.push_back({s.job_out[j], 1});
     } else {
       const int pl = s.job_out[j];
-      for (int e = s.plane_first[pl]; e < s.plane_first[pl + 1]; ++e) ent.push_back({s.entry_level[e], s.entry_coef[e]});
+      for (int e = s.plane_first[pl]; e < s.plane_first[pl + 1]; ++e)
+        ent.push_back({s.entry_level[e], s.entry_coef[e]});
     }
     for (int c = 0; c < sigma; ++c) {
       r.job_first.push_back(s.job_first[j]);

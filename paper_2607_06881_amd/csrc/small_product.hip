@@ -219,15 +219,17 @@ __global__ void __launch_bounds__(kThreads) small_product_kernel(int64_t m, int6
 
 size_t small_product_lds(int S, int T, int kc) {
   return sizeof(double) * static_cast<size_t>(T + 1) * kTile * kTile +
-         sizeof(float) * static_cast<size_t>(S) * kTile * (kc + 1) + sizeof(float) * static_cast<size_t>(S) * kc * kTile;
+         sizeof(float) * static_cast<size_t>(S) * kTile * (kc + 1) +
+         sizeof(float) * static_cast<size_t>(S) * kc * kTile;
 }
 
 hipError_t launch_small_product(int64_t m, int64_t n, int64_t k, int L, int S, int T, int w, int kc,
                                 const SmallLevelOwners& owners, const double* A, const double* B, double* C,
                                 hipStream_t stream) {
   if (m == 0 || n == 0) return hipSuccess;
-  if (L < 1 || L > kSmallMaxLimbs || S < 1 || w < 1 || w > 24 || T < 0 || T > 2 * S - 2 || T + 1 > kSmallMaxLevels || kc < 4 ||
-      kc % 4 != 0 || k < 1 || w * S + 52 > 64 * kSmallSplitWords || w * T + 55 > 64 * kSmallAccumWords)
+  if (L < 1 || L > kSmallMaxLimbs || S < 1 || w < 1 || w > 24 || T < 0 || T > 2 * S - 2 ||
+      T + 1 > kSmallMaxLevels || kc < 4 || kc % 4 != 0 || k < 1 || w * S + 52 > 64 * kSmallSplitWords ||
+      w * T + 55 > 64 * kSmallAccumWords)
     return hipErrorInvalidValue;
   const size_t lds = small_product_lds(S, T, kc);
   if (lds > kSmallMaxLds) return hipErrorInvalidValue;
