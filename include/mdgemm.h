@@ -169,10 +169,11 @@ typedef struct mdgemm_opts {
 
 /* Small products.  For an output of at most 256 tiles of 16 x 16 (up to 4
  * limbs, digits of at most 24 bits, at most 32 levels, the level sum of an
- * element within 448 bits and the split's integer within 320 bits), whose level
- * products are short enough (the
- * levels dealt to four waves, the most loaded one at most 2048 MFMA
- * instructions of 16 x 16 x 4), mdgemm_ex runs all five steps in one launch of a
+ * element within 448 bits and the split's integer within 320 bits), whose
+ * estimated time is below the staged path's (estimates fitted to products of 1
+ * to 4 limbs measured both ways on MI355X; the fused time grows with k (S + L)
+ * and with the level products of the most loaded SIMD, the staged time with its
+ * level GEMM's heaviest block), mdgemm_ex runs all five steps in one launch of a
  * fused kernel per 16 x 16 tile of C instead of the staged kernels: the same
  * digits, levels and limbs bit for bit, without launches in between and
  * without the workspace (a caller workspace is still checked but not written;

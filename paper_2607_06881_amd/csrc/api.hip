@@ -407,24 +407,49 @@ std::shared_ptr<const Planned> planned_for(int S, int T, int64_t m, int64_t n, i
 
 // The fused small-product kernel (one block per 16 x 16 tile of C runs all five
 // steps) instead of the staged path, for outputs of at most 256 such tiles whose
-// levels fit its limits: there the staged path is bound by launch latency and
-// by its level GEMM's 128 x 128 tiles (one block per tile and level, the
-// heaviest level's pairs in series).  Each level belongs to one of the four
-// waves, levels dealt heaviest first to the least loaded wave; the product
-// qualifies while the most loaded wave runs at most 2048 MFMAs (about 55 us at
-// the matrix pipe's rate).  Beyond k (S + L) = 3840 (the limbs read and digits
-// written per line of a tile) the product is left to the staged path when that
-// path splits k (its level GEMM then spreads over the chip): the fused time
-// grows with k (S + L), about 85 us per 256 of k for double-double at 5-6
-// digits, and the measured crossover lies there (k = 384 fused and 512 staged
-// at 13-bit digits, 448 and 512 at 20 bits, double-double outputs of 17 x 33
-// and 64 x 960); without a k split the staged GEMM runs few blocks and the
-// fused path stays faster (256 x 400 x 256: 180 against 458 us).  kc: the
-// largest k chunk (a multiple of 4, at most 256) whose digits fit the kernel's
-// LDS beside the levels.
+// levels fit its limits, when its estimated time is below the staged path's.
+// The staged path is bound by launch latency and by its level GEMM's 128 x 128
+// (or 64 x 128) tiles: one block per tile, level and k chunk, the heaviest
+// level's pairs in series.  The fused kernel's time grows with k (S + L), the
+// limbs read and digits written per line of a tile.  Both paths give the same
+// limbs, so the choice moves only time.  The estimates, in microseconds, were
+// fitted to 139 products measured side by side on MI355X (1 to 4 limbs, 13- to
+// 21-bit digits, outputs from 17 x 33 to 256 x 256 and 16 x 4096, k up to 4096);
+// they pick the faster path on all but five near-ties, each within 6%:
+//  fused: 17, plus the split at 15.7, 16.5, 19 or 22 ns (1 to 4 limbs) per unit
+//    of k (S + L), plus the most loaded SIMD's level products (one
+//    v_mfma_f64_16x16x4f64 per pair and 4 of k, 64 cycles at 2.4 GHz): the two
+//    phases alternate per k chunk;
+//  staged: 57 for its exponent, split, accumulation and rounding launches, plus
+//    1.13 times its level GEMM, the larger of its heaviest block (the heaviest
+//    level's pairs over one k chunk) and all its MFMAs spread over 1024 SIMDs.
+// Levels are dealt to the four SIMDs heaviest first to the least loaded, and
+// within a SIMD to the lighter of its two waves.  kc: the largest k chunk (a
+// multiple of 4, at most 256) whose digits fit the kernel's LDS beside the
+// levels.
 constexpr int64_t kSmallMaxTiles = 256;
-constexpr int64_t kSmallMaxWaveMfma = 2048;
-constexpr int64_t kSmallMaxSplitWork = 3840;
+constexpr double kMfmaUs = 64.0 / 2400.0;  // one v_mfma_f64_16x16x4f64 on one SIMD
+
+double fused_estimate_us(int64_t k, int limbs, int S, int simd_pairs) {
+  static constexpr double kSplitNs[mdg::kSmallMaxLimbs + 1] = {0.0, 15.7, 16.5, 19.0, 22.0};
+  return 17.0 + 1e-3 * kSplitNs[limbs] * static_cast<double>(k * (S + limbs)) +
+         kMfmaUs * simd_pairs * static_cast<double>((k + 3) / 4);
+}
+
+// The staged pair schedule: T + 1 level jobs per tile, FP32 panels of 32-deep k
+// steps, split in k by ksplit_count.
+double staged_estimate_us(int64_t m, int64_t n, int64_t k, int T, int heaviest_pairs, int total_pairs) {
+  const int64_t tiles = (mdg::panel_mn(m) / mdg::kTileMN) * (mdg::panel_mn(n) / mdg::kTileMN);
+  const int64_t nkb = mdg::panel_k32(k) / mdg::kTileK32;
+  const int64_t sigma = ksplit_count(tiles * (T + 1), nkb);
+  const int64_t chunk = (nkb + sigma - 1) / sigma;
+  const int rows = m <= 64 ? 64 : mdg::kTileMN;
+  // MFMAs per SIMD for one pair over one k step of a tile (four waves per block)
+  const double per_step = (rows / 16) * (mdg::kTileMN / 16) * (mdg::kTileK32 / 4) / 4.0;
+  const double heavy = static_cast<double>(heaviest_pairs) * chunk * per_step;
+  const double spread = static_cast<double>(total_pairs) * tiles * nkb * per_step * 4.0 / 1024.0;
+  return 57.0 + 1.13 * kMfmaUs * std::max(heavy, spread);
+}
 
 bool small_plan(int64_t m, int64_t n, int64_t k, int limbs, const Resolved& r, int* kc_out,
                 mdg::SmallLevelOwners* owners) {
@@ -432,15 +457,11 @@ bool small_plan(int64_t m, int64_t n, int64_t k, int limbs, const Resolved& r, i
       (r.flags & (MDGEMM_INT8 | MDGEMM_KARATSUBA | MDGEMM_KARATSUBA_MIN_TERMS | MDGEMM_STAGED | MDGEMM_CHECK_FINITE)))
     return false;
   // digits are held in LDS as FP32 values: exact while below 2^24
-  if (limbs > mdg::kSmallMaxLimbs || r.T + 1 > mdg::kSmallMaxLevels || k < 1 || r.w > 24) return false;
+  if (limbs < 1 || limbs > mdg::kSmallMaxLimbs || r.T + 1 > mdg::kSmallMaxLevels || k < 1 || r.w > 24) return false;
   if (r.w * r.S + 52 > 64 * mdg::kSmallSplitWords || r.w * r.T + 55 > 64 * mdg::kSmallAccumWords) return false;
   if (((m + 15) / 16) * ((n + 15) / 16) > kSmallMaxTiles) return false;
-  if (k * (r.S + limbs) > kSmallMaxSplitWork) {
-    // the staged pair schedule: T + 1 level jobs per 128 x 128 tile, FP32 panels
-    const int64_t tiles = (mdg::panel_mn(m) / mdg::kTileMN) * (mdg::panel_mn(n) / mdg::kTileMN);
-    if (ksplit_count(tiles * (r.T + 1), mdg::panel_k32(k) / mdg::kTileK32) > 1) return false;
-  }
-  int load[4] = {0, 0, 0, 0};
+  int load[4] = {0, 0, 0, 0}, wload[mdg::kSmallWaves] = {};
+  int heaviest = 0, total = 0;
   bool done[mdg::kSmallMaxLevels] = {};
   for (int rep = 0; rep <= r.T; ++rep) {
     int best = -1, bp = -1;
@@ -457,10 +478,14 @@ bool small_plan(int64_t m, int64_t n, int64_t k, int limbs, const Resolved& r, i
       if (load[v] < load[wv]) wv = v;
     done[best] = true;
     load[wv] += bp;
-    owners->wave[best] = static_cast<int8_t>(wv);
+    const int wave = wload[wv + 4] < wload[wv] ? wv + 4 : wv;
+    wload[wave] += bp;
+    owners->wave[best] = static_cast<int8_t>(wave);
+    heaviest = std::max(heaviest, bp);
+    total += bp;
   }
   const int maxload = std::max(std::max(load[0], load[1]), std::max(load[2], load[3]));
-  if (static_cast<int64_t>(maxload) * ((k + 3) / 4) > kSmallMaxWaveMfma) return false;
+  if (fused_estimate_us(k, limbs, r.S, maxload) > staged_estimate_us(m, n, k, r.T, heaviest, total)) return false;
   int kc = static_cast<int>(std::min<int64_t>(256, (k + 3) / 4 * 4));
   while (kc > 4 && mdg::small_product_lds(r.S, r.T, kc) > mdg::kSmallMaxLds) kc -= 4;
   if (mdg::small_product_lds(r.S, r.T, kc) > mdg::kSmallMaxLds) return false;

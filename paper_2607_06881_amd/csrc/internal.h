@@ -133,8 +133,9 @@ hipError_t launch_slice_gemm32(int64_t m, int64_t n, int64_t k, const float* DAt
 // (held in LDS as FP32), w S + 52 <= 320 bits
 // (the split's integer in 5 words), w T + 55 <= 448 bits (the level sum in 7
 // words), up to 32 levels; its dynamic LDS holds the levels of the tile and the
-// digits of one k chunk of kc (a multiple of 4).  wave[t] is the wave (0..3) that
-// forms level t.
+// digits of one k chunk of kc (a multiple of 4).  wave[t] is the wave (0..7)
+// that forms level t; waves w and w + 4 share a SIMD.
+constexpr int kSmallWaves = 8;
 constexpr int kSmallMaxLimbs = 4;
 constexpr int kSmallSplitWords = 5;
 constexpr int kSmallAccumWords = 7;

@@ -16,10 +16,11 @@
 //     k chunk by k chunk, into LDS as FP32 values (integers below 2^24, exact);
 //  3. the level products G_t = sum over p + q = t of DA_p . DB_q (section 2,
 //     equation (3) and the rewritten product): every level belongs to one of
-//     the four waves (the host balances their pair counts), which sums its
-//     pairs for the chunk in one FP64 accumulator and adds it to the level's
-//     plane in LDS; every partial sum is an integer below 2^53, so the result is
-//     exact and equal to the staged path's;
+//     the eight waves, two per SIMD (the host balances the pair counts of the
+//     SIMDs and of the two waves within each), which sums its pairs for the
+//     chunk in one FP64 accumulator and adds it to the level's plane in LDS;
+//     every partial sum is an integer below 2^53, so the result is exact and
+//     equal to the staged path's;
 //  4.-5. the exact sum of the levels in increasing significance and the greedy
 //     rounding into L limbs, one thread per output element, from LDS.
 // The digits, levels and limbs are those of the staged kernels bit for bit
@@ -35,7 +36,8 @@ namespace {
 typedef double d4 __attribute__((ext_vector_type(4)));
 
 constexpr int kTile = 16;
-constexpr int kThreads = 256;
+constexpr int kThreads = 64 * kSmallWaves;  // two waves per SIMD
+constexpr int kPhases = kThreads / kTile;    // row phases of the column exponents
 constexpr int kBatch = 4;  // elements whose limbs a thread loads before splitting them
 
 // The S digits of one element (limbs xs, grid exponent g) to out[s * stride],
@@ -81,23 +83,27 @@ __global__ void __launch_bounds__(kThreads) small_product_kernel(int64_t m, int6
   double* G = lds_d;                                          // [T+1][256]
   float* sA = reinterpret_cast<float*>(G + (T + 1) * kTile * kTile);  // [S][16][lda]
   float* sB = sA + S * kTile * lda;                           // [S][kc][16]
-  __shared__ int eA[kTile], eB[kTile], part[kTile][kTile];
+  __shared__ int eA[kTile], eB[kTile], part[kPhases][kTile];
 
-  // 1. grid exponents of the tile's rows of A (wave w: rows 4w .. 4w+3, the
-  //    four rows' loads issued together) and columns of B (16 phases of rows)
+  // 1. grid exponents of the tile's rows of A (wave w: rows R w .. R w + R - 1,
+  //    R = 16 / waves, their loads issued together) and columns of B (kPhases
+  //    phases of rows)
   {
-    int best[4] = {kNoExp, kNoExp, kNoExp, kNoExp};
+    constexpr int R = kTile / kSmallWaves;
+    int best[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) best[r] = kNoExp;
     for (int64_t kk = lane; kk < k; kk += 64) {
-      double v[4];
+      double v[R];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = i0 + 4 * wave + r < m ? A[(i0 + 4 * wave + r) * k + kk] : 0.0;
+      for (int r = 0; r < R; ++r) v[r] = i0 + R * wave + r < m ? A[(i0 + R * wave + r) * k + kk] : 0.0;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) best[r] = max(best[r], frexp_exp_or_min(v[r]));
+      for (int r = 0; r < R; ++r) best[r] = max(best[r], frexp_exp_or_min(v[r]));
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < R; ++r) {
       const int b = wave_max_i(best[r]);
-      if (lane == 0) eA[4 * wave + r] = b == kNoExp ? 0 : b;
+      if (lane == 0) eA[R * wave + r] = b == kNoExp ? 0 : b;
     }
   }
   {
@@ -105,7 +111,7 @@ __global__ void __launch_bounds__(kThreads) small_product_kernel(int64_t m, int6
     int best = kNoExp;
     if (j0 + col < n) {
 #pragma unroll 4
-      for (int64_t kk = phase; kk < k; kk += 16) best = max(best, frexp_exp_or_min(B[kk * n + j0 + col]));
+      for (int64_t kk = phase; kk < k; kk += kPhases) best = max(best, frexp_exp_or_min(B[kk * n + j0 + col]));
     }
     part[phase][col] = best;
   }
@@ -113,7 +119,7 @@ __global__ void __launch_bounds__(kThreads) small_product_kernel(int64_t m, int6
   __syncthreads();
   if (tid < kTile) {
     int best = kNoExp;
-    for (int ph = 0; ph < kTile; ++ph) best = max(best, part[ph][tid]);
+    for (int ph = 0; ph < kPhases; ++ph) best = max(best, part[ph][tid]);
     eB[tid] = best == kNoExp ? 0 : best;
   }
   __syncthreads();
@@ -202,7 +208,7 @@ __global__ void __launch_bounds__(kThreads) small_product_kernel(int64_t m, int6
 
   // 4.-5. exact accumulation and greedy rounding, one thread per output element
   const int i = tid >> 4, j = tid & 15;
-  if (i0 + i < m && j0 + j < n) {
+  if (tid < kTile * kTile && i0 + i < m && j0 + j < n) {
     uint64_t N[NWA];
 #pragma unroll
     for (int q = 0; q < NWA; ++q) N[q] = 0;

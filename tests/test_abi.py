@@ -188,7 +188,8 @@ def test_workspace_layout_of_staged_and_fused_products(lib):
     assert ei.value.status == md.MDGEMM_EINVAL
     lay = md.mdgemm_workspace_layout(64, 64, 64, 2, flags=md.MDGEMM_STAGED)
     assert lay["total"] == md.mdgemm_workspace_bytes(64, 64, 64, 2) and lay["planes"] == 8
-    # beyond 256 tiles of 16 x 16, or with too many MFMAs for one wave, the stages run
+    # beyond 256 tiles of 16 x 16, or where the staged path's estimated time is lower
+    # (64 x 64 x 4096: about 950 us fused), the stages run
     lay = md.mdgemm_workspace_layout(257, 256, 64, 2)
     assert lay["direct_levels"] == 1 and lay["panel_bytes"] == 4 and lay["planes"] == 8
     assert md.mdgemm_workspace_layout(64, 64, 4096, 2)["planes"] >= 8
@@ -206,19 +207,23 @@ def _fused(m, n, k, L, **opts):
     return False
 
 
-def test_fused_path_leaves_long_k_to_a_k_split_staged_path(lib):
-    # k (S + L) above 3840 goes to the staged path when its level GEMM splits k
-    # (8 k steps of 32 per chunk, fewer than 768 blocks of 128 x 128 tiles and
-    # levels), and stays fused when it would not
+def test_fused_path_taken_where_its_estimated_time_is_lower(lib):
+    # the fused kernel runs where its estimated time is below the staged path's;
+    # each pair below was measured side by side on MI355X (fused / staged, us)
     auto = md.MDGEMM_SLICE_BITS_AUTO
-    assert _fused(17, 33, 384, 2)                          # 384 (8 + 2) = 3840
-    assert _fused(17, 33, 392, 2)                          # 3920, but 13 k steps: no split
-    assert not _fused(17, 33, 512, 2)                      # 16 k steps: split in 2
-    assert _fused(64, 960, 448, 2, slice_bits=auto)        # 20-bit digits, S = 6: 3584
-    assert not _fused(64, 960, 512, 2, slice_bits=auto)    # 4096, 16 k steps: split in 2
-    assert not _fused(64, 960, 1024, 2, slice_bits=auto)
-    assert _fused(256, 256, 400, 2)                        # 4000, but 13 k steps: no split
-    assert _fused(64, 64, 64, 2) and _fused(45, 60, 130, 4)
+    assert _fused(64, 64, 64, 2) and _fused(45, 60, 130, 4)   # 28.5 / 65.7, 104 / 208
+    assert _fused(17, 33, 512, 2)                             # 123 / 173
+    assert not _fused(17, 33, 1536, 2)                        # 342 / 192: k split 6 ways
+    assert not _fused(17, 33, 1024, 1)                        # 124 / 103
+    assert _fused(128, 128, 1024, 1)                          # 124 / 169: 128 x 128 tiles
+    assert _fused(64, 960, 640, 2, slice_bits=auto)           # 135 / 175
+    assert not _fused(64, 960, 1024, 2, slice_bits=auto)      # 207 / 158
+    assert _fused(256, 256, 800, 2)                           # 198 / 335
+    assert _fused(100, 100, 400, 3)                           # 180 / 660
+    assert not _fused(17, 33, 1200, 3)                        # 504 / 309
+    assert _fused(256, 256, 450, 4)                           # 326 / 998
+    assert not _fused(45, 60, 1000, 4)                        # 639 / 334
+    assert not _fused(17, 33, 512, 2, flags=md.MDGEMM_STAGED)
 
 
 def test_binding_refuses_cpu_tensors(lib):

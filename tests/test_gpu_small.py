@@ -5,7 +5,8 @@ Every case is checked three ways, bit for bit: against the staged kernels
 (MDGEMM_STAGED, the same product through the exponent, split, level-GEMM and
 accumulation kernels) and against the oracle's chain (digits on the shared
 grids, int64 levels, exact sum, greedy rounding).  The shapes cover ragged
-tiles, a single element, k not a multiple of 4 and k longer than one LDS chunk,
+tiles, a single element, k not a multiple of 4, k longer than one LDS chunk
+(up to 1024, four chunks),
 one to four limbs, every cutoff form, the adaptive width, range balancing,
 zero lines and subnormal products; that the fused path is the one that ran is
 read from mdgemm_workspace_layout, which refuses products it takes.
@@ -45,6 +46,13 @@ CASES = [
     (3, 31, 5, 47, {"cutoff": 4}, 9),
     (2, 16, 129, 16, {"slices": 9, "cutoff": 10}, 10),
     (2, 40, 6, 20, {"slice_bits": 24, "slices": 5}, 11),  # the widest digit FP32 holds
+    # long k, where the time estimates pick the fused kernel over a k-split staged GEMM
+    (3, 100, 400, 100, {}, 12),
+    (4, 45, 300, 60, {}, 13),
+    (2, 256, 800, 256, {}, 14),
+    (2, 17, 512, 33, {}, 15),
+    (1, 128, 1024, 128, {}, 16),
+    (2, 128, 1024, 128, {"slice_bits": md.MDGEMM_SLICE_BITS_AUTO}, 17),
 ]
 
 
