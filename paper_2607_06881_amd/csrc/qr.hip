@@ -5,8 +5,8 @@
 // A [2][m][n] (limb-major double-double, m >= n) is factored as A = Q R with
 // Q = H_0 H_1 ... H_{n-1}, H_j = I - tau_j v_j v_j^T (Householder reflections,
 // v_j(j) = 1, v_j zero above row j).  Panels of nb <= 64 columns are factored in
-// double-double arithmetic (dd.h), by one workgroup for short panels and by many
-// for tall ones (see qr_col_update_kernel); the panel's reflections are
+// double-double arithmetic (dd.h) by many workgroups, one launch per column
+// (see qr_col_step_kernel); the panel's reflections are
 // accumulated in the compact form I - V T V^T (T upper triangular, by the
 // recursive form of Elmroth and Gustavson), and the trailing columns are updated as
 //     A2 <- A2 - V (T^T (V^T A2))
@@ -36,7 +36,6 @@
 namespace mdg {
 namespace {
 
-constexpr int kPanelThreads = 1024;
 constexpr int kMaxNb = 64;  // panel width; the kernels take its columns 32 at a time
 
 __device__ inline dd ldd(const double* P, int64_t plane, int64_t idx) { return {P[idx], P[plane + idx]}; }
@@ -45,42 +44,108 @@ __device__ inline void std_(double* P, int64_t plane, int64_t idx, dd v) {
   P[plane + idx] = v.lo;
 }
 
-__device__ inline dd shfl_xor_dd(dd v, int off) { return {__shfl_xor(v.hi, off, 64), __shfl_xor(v.lo, off, 64)}; }
+// A panel is factored by many workgroups, one launch per step s = 0 .. jb, each
+// workgroup owning kRows consecutive panel rows (16 for panels of at most
+// kShortPanel rows, so that they still spread over the chip, 32 above).  Step s
+// finishes column s - 1 and starts column s:
+//   every block sums the partials of step s - 1 in the same order (so all
+//   blocks agree bit for bit): d_c = x^T a_c over the rows below the pivot, x
+//   the column s - 1, c >= s - 1 (d_{s-1} = sigma), and takes the pivot row's
+//   entries p_c (p_{s-1} = x1); it forms the Householder scalars, block 0 writes
+//   the diagonal and tau, and each block scales its rows of x into v = x / v1
+//   and applies the reflection to columns c >= s at its rows from the pivot
+//   down with w_c = v^T a_c = p_c + d_c / v1 (v is 1 at the pivot);
+//   then each block writes its part of d_c for column s (c >= s) and the block
+//   holding the pivot row writes that row's entries p_c.
+// One reduction per column serves both the norm and the reflection's dot
+// products, since both are sums over the rows below the pivot.  The partials
+// alternate between two buffers (step s reads buffer (s - 1) & 1 and writes
+// s & 1), and every block writes all of its partial slots (zeros where it holds
+// no row below the pivot), so a sum never reads a stale or concurrently written
+// slot.
+constexpr int kPanelRowsShort = 16, kPanelRowsTall = 32;
+constexpr int64_t kShortPanel = 2048;
+constexpr int kColThreads = 256;  // 32 column lanes x 8 row groups
 
-// Sum of one dd per thread over the workgroup: a butterfly within each wave,
-// then the 16 wave sums in a fixed order; every thread gets the result.
-__device__ inline dd block_sum(dd v, dd* red) {
-  for (int off = 32; off > 0; off >>= 1) v = dd_add(v, shfl_xor_dd(v, off));
-  const int tid = threadIdx.x;
-  if ((tid & 63) == 0) red[tid >> 6] = v;
-  __syncthreads();
-  dd r = red[0];
-  for (int w = 1; w < kPanelThreads / 64; ++w) r = dd_add(r, red[w]);
-  __syncthreads();
-  return r;
-}
+constexpr int kRowGroups = kColThreads / 32;                // 8: rows rb + rg + 8 q
+constexpr int kColGroups = kMaxNb / 32;                      // columns c0 + 32 h + cc, h < 2
+static_assert(kPanelRowsShort % kRowGroups == 0 && kPanelRowsTall % kRowGroups == 0 && kMaxNb % 32 == 0,
+              "thread layout of the column kernels");
+static_assert(kPanelRowsShort <= 64 && kPanelRowsTall <= 64, "one row per thread of the first two waves");
 
-// Factor the panel A(j0:m, j0:j0+jb) in place.  Thread layout for the updates:
-// column cc = tid % 32 of the remaining panel columns, row group rg = tid / 32.
-__global__ void __launch_bounds__(kPanelThreads) qr_panel_kernel(int64_t m, int64_t n, int64_t j0, int jb,
-                                                                 double* __restrict__ A, double* __restrict__ tau) {
-  __shared__ dd red[kPanelThreads];
-  __shared__ dd wv[kMaxNb];
+// pd: two buffers of [2][G][kMaxNb] (hi plane, lo plane); prow: two of [2][kMaxNb]
+template <int kRows>
+__global__ void __launch_bounds__(kColThreads) qr_col_step_kernel(int64_t m, int64_t n, int64_t j0, int jb, int s,
+                                                                  double* __restrict__ A, double* __restrict__ tau,
+                                                                  double* __restrict__ pd,
+                                                                  double* __restrict__ prow) {
+  constexpr int kRPT = kRows / kRowGroups;  // rows per thread
+  __shared__ dd red[kColThreads];
+  __shared__ dd td[kMaxNb], tw[kMaxNb], vs[kRows], xs[kRows];
   __shared__ dd s_scale, s_tau;
-  __shared__ int s_mode;  // 0: H = I, 1: v = e_1 (tau = 2), 2: general
+  __shared__ int s_mode;
   const int64_t plane = m * n;
   const int tid = threadIdx.x, cc = tid & 31, rg = tid >> 5;
-  for (int j = 0; j < jb; ++j) {
-    const int64_t r0 = j0 + j, cj = j0 + j;
-    // sigma = sum of squares below the pivot
-    dd part = {0.0, 0.0};
-    for (int64_t r = r0 + 1 + tid; r < m; r += kPanelThreads) {
-      const dd a = ldd(A, plane, r * n + cj);
-      part = dd_add(part, dd_mul(a, a));
+  const int64_t G = gridDim.x, pplane = G * kMaxNb;
+  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kRows, re = min(m, rb + kRows);
+  const int64_t r0 = j0 + s, rp = r0 - 1;  // the pivot rows of column s and of column s - 1
+  const double* pd_in = pd + ((s + 1) & 1) * 2 * pplane;
+  double* pd_out = pd + (s & 1) * 2 * pplane;
+  const double* prow_in = prow + ((s + 1) & 1) * 2 * kMaxNb;
+  double* prow_out = prow + (s & 1) * 2 * kMaxNb;
+
+  // Loaded first (none depends on the sums): columns s + 32 h + cc at rows
+  // rb + rg + 8 q from the previous pivot down (from the pivot of column s when
+  // s = 0), column s - 1 below its pivot (one row per thread of the first
+  // kRows), and the pivot row's entries of step s - 1.
+  const int64_t rlo = s > 0 ? rp : r0;
+  dd av[kColGroups][kRPT];
+#pragma unroll
+  for (int h = 0; h < kColGroups; ++h) {
+    const int c = s + 32 * h + cc;
+#pragma unroll
+    for (int q = 0; q < kRPT; ++q) {
+      const int64_t r = rb + rg + kRowGroups * q;
+      av[h][q] = c < jb && r >= rlo && r < re ? ldd(A, plane, r * n + j0 + c) : dd{0.0, 0.0};
     }
-    const dd sigma = block_sum(part, red);
+  }
+  if (s > 0) {
+    const int ncols = jb - s + 1;  // c = s - 1 .. jb - 1
+    dd xv = {0.0, 0.0}, pv = {0.0, 0.0};
+    if (tid < kRows) {
+      const int64_t r = rb + tid;
+      if (r > rp && r < re) xv = ldd(A, plane, r * n + j0 + s - 1);
+    }
+    // x1 for thread 0; p_c (c = s + t) for thread 64 + t, which forms tau w_c
+    if (tid == 0) pv = ldd(prow_in, kMaxNb, 0);
+    if (tid >= 64 && tid < 64 + ncols - 1) pv = ldd(prow_in, kMaxNb, tid - 63);
+    // d_c, 32 columns at a time: partials b = rg, rg + 8, ... in that order,
+    // eight loads in flight
+    for (int g0 = 0; g0 < ncols; g0 += 32) {
+      dd sum = {0.0, 0.0};
+      if (g0 + cc < ncols) {
+        for (int64_t b0 = rg; b0 < G; b0 += 64) {
+          dd v[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            v[u] = b0 + 8 * u < G ? ldd(pd_in, pplane, (b0 + 8 * u) * kMaxNb + g0 + cc) : dd{0.0, 0.0};
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            if (b0 + 8 * u < G) sum = dd_add(sum, v[u]);
+        }
+      }
+      red[tid] = sum;
+      __syncthreads();
+      if (rg == 0) {
+        dd d = red[cc];
+        for (int g = 1; g < 8; ++g) d = dd_add(d, red[g * 32 + cc]);
+        td[g0 + cc] = d;
+      }
+      __syncthreads();
+    }
+    // the Householder scalars of column s - 1 from sigma = d_{s-1} and x1 = p_{s-1}
     if (tid == 0) {
-      const dd x1 = ldd(A, plane, r0 * n + cj);
+      const dd sigma = td[0], x1 = pv;
       dd diag;
       if (sigma.hi == 0.0) {
         s_mode = x1.hi < 0.0 ? 1 : 0;
@@ -95,281 +160,81 @@ __global__ void __launch_bounds__(kPanelThreads) qr_panel_kernel(int64_t m, int6
         s_mode = 2;
         diag = mu;
       }
-      std_(A, plane, r0 * n + cj, diag);
-      std_(tau, n, cj, s_tau);
+      if (blockIdx.x == 0) {
+        std_(A, plane, rp * n + j0 + s - 1, diag);
+        std_(tau, n, j0 + s - 1, s_tau);
+      }
     }
     __syncthreads();
     const int mode = s_mode;
-    if (mode == 2) {
-      const dd v1 = s_scale;
-      for (int64_t r = r0 + 1 + tid; r < m; r += kPanelThreads)
-        std_(A, plane, r * n + cj, dd_div(ldd(A, plane, r * n + cj), v1));
-    } else {  // v = e_1: the stored vector is zero below the pivot
-      for (int64_t r = r0 + 1 + tid; r < m; r += kPanelThreads) std_(A, plane, r * n + cj, dd{0.0, 0.0});
+    // v at the block's rows (1 at the pivot; mode 2: x / v1 below it, else 0),
+    // and tau w_c for c = s + tid: w_c = p_c + d_c / v1 (p_c alone when v = e_1)
+    if (tid < kRows) {
+      const int64_t r = rb + tid;
+      dd v = {0.0, 0.0};
+      if (r == rp) {
+        v = {1.0, 0.0};
+      } else if (r > rp && r < re) {
+        v = mode == 2 ? dd_div(xv, s_scale) : dd{0.0, 0.0};
+        std_(A, plane, r * n + j0 + s - 1, v);
+      }
+      vs[tid] = v;
+    }
+    if (tid >= 64 && tid < 64 + ncols - 1) {
+      const int t = tid - 64;
+      const dd w = mode == 2 ? dd_add(pv, dd_div(td[t + 1], s_scale)) : pv;
+      tw[t] = dd_mul(s_tau, w);
     }
     __syncthreads();
-    if (mode == 0) continue;  // H_j = I
-    const dd t = s_tau;
-    // w_c = v^T a_c for the remaining columns c = j + 1 + g0 + cc, 32 at a time (v(r0) = 1)
-    for (int g0 = 0; g0 < jb - j - 1; g0 += 32) {
-      const int c = j + 1 + g0 + cc;
-      dd acc = {0.0, 0.0};
-      if (c < jb && mode == 2) {
-        for (int64_t r = r0 + 1 + rg; r < m; r += 32)
-          acc = dd_add(acc, dd_mul(ldd(A, plane, r * n + cj), ldd(A, plane, r * n + j0 + c)));
-      }
-      // the two row groups of a wave (lanes cc and 32 + cc) first, then the 16
-      // waves in order
-      acc = dd_add(acc, shfl_xor_dd(acc, 32));
-      if ((tid & 63) < 32) red[(tid >> 6) * 32 + cc] = acc;
-      __syncthreads();
-      if (rg == 0 && c < jb) {
-        dd w = ldd(A, plane, r0 * n + j0 + c);
-        for (int g = 0; g < kPanelThreads / 64; ++g) w = dd_add(w, red[g * 32 + cc]);
-        wv[g0 + cc] = dd_mul(t, w);
-      }
-      __syncthreads();
-    }
-    // a_c <- a_c - tau w_c v
-    for (int g0 = 0; g0 < jb - j - 1; g0 += 32) {
-      const int c = j + 1 + g0 + cc;
-      if (c < jb) {
-        const dd tw = wv[g0 + cc];
-        if (rg == 0) std_(A, plane, r0 * n + j0 + c, dd_sub(ldd(A, plane, r0 * n + j0 + c), tw));
-        if (mode == 2) {
-          for (int64_t r = r0 + 1 + rg; r < m; r += 32) {
-            const int64_t idx = r * n + j0 + c;
-            std_(A, plane, idx, dd_sub(ldd(A, plane, idx), dd_mul(tw, ldd(A, plane, r * n + cj))));
-          }
-        }
-      }
-    }
-    __syncthreads();
-  }
-}
-
-// Tall panels (more than kSmallPanel rows) are factored by many workgroups, two
-// launches per column, each workgroup owning kRows consecutive panel rows (16 for
-// panels of at most kShortPanel rows, so that they still spread over the chip,
-// 32 above):
-//   qr_col_update_kernel(j): apply H_{j-1} to columns j .. jb-1 of the block's
-//     rows (w from the partial dot products of the previous launch), then write
-//     the block's part of sigma_j (rows below the pivot) and, from the block
-//     that holds the pivot row, x1 = a(r0, j);
-//   qr_col_reflect_kernel(j): every block forms sigma_j from all partials in the
-//     same order and the Householder scalars from it (so all blocks agree bit for
-//     bit), block 0 writes the diagonal and tau_j, each block scales its rows of
-//     column j into v and writes its partial dot products v^T a_c (c > j), the
-//     pivot row entering with v = 1.
-// Every block writes all of its partial slots (zeros when it holds no row at or
-// below the pivot), so the sums never read a stale slot.
-constexpr int kPanelRowsShort = 16, kPanelRowsTall = 32;
-constexpr int64_t kShortPanel = 2048;
-constexpr int kColThreads = 256;  // 32 column lanes x 8 row groups
-constexpr int64_t kSmallPanel = 256;
-
-// Sum of one dd per thread over the 256 threads: a butterfly within each wave,
-// then the four wave sums in a fixed order; every thread gets the result.
-__device__ inline dd block_sum256(dd v, dd* red) {
-  for (int off = 32; off > 0; off >>= 1) v = dd_add(v, shfl_xor_dd(v, off));
-  const int tid = threadIdx.x;
-  if ((tid & 63) == 0) red[tid >> 6] = v;
-  __syncthreads();
-  const dd r = dd_add(dd_add(red[0], red[1]), dd_add(red[2], red[3]));
-  __syncthreads();
-  return r;
-}
-
-constexpr int kRowGroups = kColThreads / 32;                // 8: rows rb + rg + 8 q
-constexpr int kColGroups = kMaxNb / 32;                      // columns c0 + 32 h + cc, h < 2
-static_assert(kPanelRowsShort % kRowGroups == 0 && kPanelRowsTall % kRowGroups == 0 && kMaxNb % 32 == 0,
-              "thread layout of the column kernels");
-
-template <int kRows>
-__global__ void __launch_bounds__(kColThreads) qr_col_update_kernel(int64_t m, int64_t n, int64_t j0, int jb, int j,
-                                                                    double* __restrict__ A,
-                                                                    const double* __restrict__ tau,
-                                                                    double* __restrict__ psig,
-                                                                    const double* __restrict__ pw,
-                                                                    double* __restrict__ px1) {
-  constexpr int kRPT = kRows / kRowGroups;  // rows per thread
-  __shared__ dd red[kColThreads];
-  __shared__ dd tw[kMaxNb];
-  const int64_t plane = m * n;
-  const int tid = threadIdx.x, cc = tid & 31, rg = tid >> 5;
-  const int64_t G = gridDim.x;
-  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kRows, re = min(m, rb + kRows);
-  const int64_t r0 = j0 + j, rp = r0 - 1;  // the pivot rows of column j and of column j - 1
-  // The entries this thread updates, loaded before the partials are folded (they
-  // do not depend on them): rows rb + rg + 8 q of columns j + 32 h + cc from the
-  // previous pivot row down (column j alone, from its pivot down, when j = 0),
-  // and v_{j-1} at the same rows (1 at its pivot row).
-  dd av[kColGroups][kRPT], vv[kRPT];
-  const int64_t rlo = j > 0 ? rp : r0;
-#pragma unroll
-  for (int h = 0; h < kColGroups; ++h) {
-    const int c = j + 32 * h + cc;
-#pragma unroll
-    for (int q = 0; q < kRPT; ++q) {
-      const int64_t r = rb + rg + kRowGroups * q;
-      const bool ok = c < jb && (j > 0 || c == j) && r >= rlo && r < re;
-      av[h][q] = ok ? ldd(A, plane, r * n + j0 + c) : dd{0.0, 0.0};
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < kRPT; ++q) {
-    const int64_t r = rb + rg + kRowGroups * q;
-    vv[q] = j > 0 && r > rp && r < re ? ldd(A, plane, r * n + j0 + j - 1) : dd{r == rp ? 1.0 : 0.0, 0.0};
-  }
-  if (j > 0) {
-    // w_c = tau_{j-1} sum_b pw[b][c - j] for c = j + g0 + cc, 32 columns at a time:
-    // the same order in every block
-    const dd tprev = ldd(tau, n, j0 + j - 1);
-    for (int g0 = 0; g0 < jb - j; g0 += 32) {
-      // partials b = rg, rg + 8, ... in that order, eight loads in flight
-      dd s = {0.0, 0.0};
-      for (int64_t b0 = rg; b0 < G; b0 += 64) {
-        dd v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-          v[u] = b0 + 8 * u < G ? ldd(pw, G * kMaxNb, (b0 + 8 * u) * kMaxNb + g0 + cc) : dd{0.0, 0.0};
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-          if (b0 + 8 * u < G) s = dd_add(s, v[u]);
-      }
-      red[tid] = s;
-      __syncthreads();
-      if (rg == 0) {
-        dd w = red[cc];
-        for (int g = 1; g < 8; ++g) w = dd_add(w, red[g * 32 + cc]);
-        tw[g0 + cc] = dd_mul(tprev, w);
-      }
-      __syncthreads();
-    }
     // a_c <- a_c - (tau w_c) v at the rows from the previous pivot down
 #pragma unroll
     for (int h = 0; h < kColGroups; ++h) {
-      const int c = j + 32 * h + cc;
+      const int c = s + 32 * h + cc;
       if (c < jb) {
         const dd t = tw[32 * h + cc];
 #pragma unroll
         for (int q = 0; q < kRPT; ++q) {
           const int64_t r = rb + rg + kRowGroups * q;
           if (r >= rp && r < re) {
-            av[h][q] = dd_sub(av[h][q], dd_mul(t, vv[q]));
+            av[h][q] = dd_sub(av[h][q], dd_mul(t, vs[r - rb]));
             std_(A, plane, r * n + j0 + c, av[h][q]);
           }
         }
       }
     }
   }
-  // the block's part of sigma_j (column j below its pivot, held by lane cc = 0
-  // of each row group) and x1 = a(r0, j) from the block holding the pivot row
-  dd part = {0.0, 0.0};
+  if (s == jb) return;
+  // column s below its pivot, from lane cc = 0 of each row group, for all lanes
   if (cc == 0) {
 #pragma unroll
     for (int q = 0; q < kRPT; ++q) {
       const int64_t r = rb + rg + kRowGroups * q;
-      if (r > r0 && r < re) part = dd_add(part, dd_mul(av[0][q], av[0][q]));
-      if (r == r0) std_(px1, kMaxNb, j, av[0][q]);
-    }
-  }
-  const dd sig = block_sum256(part, red);
-  if (tid == 0) std_(psig, G, blockIdx.x, sig);
-}
-template <int kRows>
-__global__ void __launch_bounds__(kColThreads) qr_col_reflect_kernel(int64_t m, int64_t n, int64_t j0, int jb, int j,
-                                                                     double* __restrict__ A, double* __restrict__ tau,
-                                                                     const double* __restrict__ psig,
-                                                                     double* __restrict__ pw,
-                                                                     const double* __restrict__ px1) {
-  constexpr int kRPT = kRows / kRowGroups;  // rows per thread
-  __shared__ dd red[kColThreads];
-  __shared__ dd vs[kRows];
-  __shared__ dd s_scale, s_tau;
-  __shared__ int s_mode;
-  const int64_t plane = m * n;
-  const int tid = threadIdx.x, cc = tid & 31, rg = tid >> 5;
-  const int64_t G = gridDim.x;
-  const int64_t rb = j0 + static_cast<int64_t>(blockIdx.x) * kRows, re = min(m, rb + kRows);
-  const int64_t r0 = j0 + j;
-  // Loaded before sigma is formed (none of them depends on it): column j below
-  // the pivot (one row per thread of the first 32) and the trailing columns
-  // j + 1 + 32 h + cc at rows rb + rg + 8 q at or below the pivot.
-  dd xv = {0.0, 0.0};
-  if (tid < kRows) {
-    const int64_t r = rb + tid;
-    if (r > r0 && r < re) xv = ldd(A, plane, r * n + j0 + j);
-  }
-  dd av[kColGroups][kRPT];
-#pragma unroll
-  for (int h = 0; h < kColGroups; ++h) {
-    const int c = j + 1 + 32 * h + cc;
-#pragma unroll
-    for (int q = 0; q < kRPT; ++q) {
-      const int64_t r = rb + rg + kRowGroups * q;
-      av[h][q] = c < jb && r >= r0 && r < re ? ldd(A, plane, r * n + j0 + c) : dd{0.0, 0.0};
-    }
-  }
-  dd part = {0.0, 0.0};
-  for (int64_t b = tid; b < G; b += kColThreads) part = dd_add(part, ldd(psig, G, b));
-  const dd sigma = block_sum256(part, red);
-  if (tid == 0) {
-    const dd x1 = ldd(px1, kMaxNb, j);
-    dd diag;
-    if (sigma.hi == 0.0) {
-      s_mode = x1.hi < 0.0 ? 1 : 0;
-      s_tau = s_mode ? dd{2.0, 0.0} : dd{0.0, 0.0};
-      diag = s_mode ? dd_neg(x1) : x1;
-    } else {
-      const dd mu = dd_sqrt(dd_add(dd_mul(x1, x1), sigma));
-      const dd v1 = x1.hi <= 0.0 ? dd_sub(x1, mu) : dd_neg(dd_div(sigma, dd_add(x1, mu)));
-      const dd v1sq = dd_mul(v1, v1);
-      s_tau = dd_div(dd_mul_d(v1sq, 2.0), dd_add(sigma, v1sq));
-      s_scale = v1;
-      s_mode = 2;
-      diag = mu;
-    }
-    if (blockIdx.x == 0) {
-      std_(A, plane, r0 * n + j0 + j, diag);
-      std_(tau, n, j0 + j, s_tau);
+      xs[rg + kRowGroups * q] = r > r0 && r < re ? av[0][q] : dd{0.0, 0.0};
     }
   }
   __syncthreads();
-  const int mode = s_mode;
-  if (tid < kRows) {
-    const int64_t r = rb + tid;
-    dd v = {0.0, 0.0};
-    if (r == r0) {
-      v = {1.0, 0.0};
-    } else if (r > r0 && r < re) {
-      // mode 2: v = x / v1; otherwise v = e_1, zero below the pivot
-      v = mode == 2 ? dd_div(xv, s_scale) : dd{0.0, 0.0};
-      std_(A, plane, r * n + j0 + j, v);
-    }
-    vs[tid] = v;
-  }
-  __syncthreads();
-  // partial w_c = v^T a_c over the block's rows at or below the pivot, for
-  // c = j + 1 + 32 h + cc (slot 32 h + cc), rows in increasing order
+  // partial d_c = x^T a_c over the block's rows below the pivot, for
+  // c = s + 32 h + cc (slot 32 h + cc), rows in increasing order; the pivot
+  // row's entries from the block that holds it
 #pragma unroll
   for (int h = 0; h < kColGroups; ++h) {
-    if (32 * h >= jb - j - 1) break;
-    const int c = j + 1 + 32 * h + cc;
+    if (32 * h >= jb - s) break;
+    const int c = s + 32 * h + cc;
     dd acc = {0.0, 0.0};
     if (c < jb) {
 #pragma unroll
       for (int q = 0; q < kRPT; ++q) {
         const int64_t r = rb + rg + kRowGroups * q;
-        if (r >= r0 && r < re) acc = dd_add(acc, dd_mul(vs[r - rb], av[h][q]));
+        if (r > r0 && r < re) acc = dd_add(acc, dd_mul(xs[rg + kRowGroups * q], av[h][q]));
+        if (r == r0) std_(prow_out, kMaxNb, 32 * h + cc, av[h][q]);
       }
     }
     red[tid] = acc;
     __syncthreads();
     if (rg == 0) {
-      dd w = red[cc];
-      for (int g = 1; g < 8; ++g) w = dd_add(w, red[g * 32 + cc]);
-      std_(pw, G * kMaxNb, static_cast<int64_t>(blockIdx.x) * kMaxNb + 32 * h + cc, w);
+      dd d = red[cc];
+      for (int g = 1; g < 8; ++g) d = dd_add(d, red[g * 32 + cc]);
+      std_(pd_out, pplane, static_cast<int64_t>(blockIdx.x) * kMaxNb + 32 * h + cc, d);
     }
     __syncthreads();
   }
@@ -536,7 +401,7 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // Workspace parts of the QR: V, Vt, G (V^T V), Tt, X (trailing block), W, W2, P,
 // then the workspace of the largest mdgemm_ex call.
 struct QrLayout {
-  size_t v = 0, vt = 0, g = 0, tt = 0, x = 0, w = 0, w2 = 0, p = 0, psig = 0, pw = 0, px1 = 0, pgram = 0, gemm = 0,
+  size_t v = 0, vt = 0, g = 0, tt = 0, x = 0, w = 0, w2 = 0, p = 0, pd = 0, prow = 0, pgram = 0, gemm = 0,
          gemm_bytes = 0, total = 0;
 };
 
@@ -572,14 +437,13 @@ bool qr_layout(int64_t m, int64_t n, int nb, QrLayout* L) {
   off += wbytes;
   L->p = off;
   off += xbytes;
-  // partial sums of the multi-workgroup panel: sigma [G], w [G][32], x1 [32]
+  // partial sums of the multi-workgroup panel, two buffers each: the dot
+  // products [G][kMaxNb] and the pivot row [kMaxNb]
   const size_t groups = static_cast<size_t>((m + kPanelRowsShort - 1) / kPanelRowsShort);  // at most
-  L->psig = off;
-  off += align256(dd_bytes * groups);
-  L->pw = off;
-  off += align256(dd_bytes * groups * kMaxNb);
-  L->px1 = off;
-  off += align256(dd_bytes * kMaxNb);
+  L->pd = off;
+  off += align256(2 * dd_bytes * groups * kMaxNb);
+  L->prow = off;
+  off += align256(2 * dd_bytes * kMaxNb);
   L->pgram = off;
   off += align256(dd_bytes * static_cast<size_t>((m + kGramRows - 1) / kGramRows) * kMaxNb * kMaxNb);
   // the largest workspace of the three products of any panel: V^T X, T^T W, V W2
@@ -650,9 +514,8 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
   double* W = reinterpret_cast<double*>(ws + L.w);
   double* W2 = reinterpret_cast<double*>(ws + L.w2);
   double* P = reinterpret_cast<double*>(ws + L.p);
-  double* psig = reinterpret_cast<double*>(ws + L.psig);
-  double* pw = reinterpret_cast<double*>(ws + L.pw);
-  double* px1 = reinterpret_cast<double*>(ws + L.px1);
+  double* pd = reinterpret_cast<double*>(ws + L.pd);
+  double* prow = reinterpret_cast<double*>(ws + L.prow);
   double* pgram = reinterpret_cast<double*>(ws + L.pgram);
   mdgemm_opts o = mdg::qr_gemm_opts();
   o.stream = stream;
@@ -661,24 +524,17 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
   for (int64_t j0 = 0; j0 < n; j0 += nb) {
     const int jb = static_cast<int>(std::min<int64_t>(nb, n - j0));
     const int64_t mp = m - j0, c0 = j0 + jb, nc = n - c0;
-    if (mp <= mdg::kSmallPanel) {
-      hipLaunchKernelGGL(mdg::qr_panel_kernel, dim3(1), dim3(mdg::kPanelThreads), 0, s, m, n, j0, jb, A, tau);
-    } else {
-      auto columns = [&](auto rows) {
-        constexpr int kRows = decltype(rows)::value;
-        const unsigned groups = static_cast<unsigned>((mp + kRows - 1) / kRows);
-        for (int j = 0; j < jb; ++j) {
-          hipLaunchKernelGGL(mdg::qr_col_update_kernel<kRows>, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0,
-                             jb, j, A, tau, psig, pw, px1);
-          hipLaunchKernelGGL(mdg::qr_col_reflect_kernel<kRows>, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0,
-                             jb, j, A, tau, psig, pw, px1);
-        }
-      };
-      if (mp > mdg::kShortPanel)
-        columns(std::integral_constant<int, mdg::kPanelRowsTall>{});
-      else
-        columns(std::integral_constant<int, mdg::kPanelRowsShort>{});
-    }
+    auto columns = [&](auto rows) {
+      constexpr int kRows = decltype(rows)::value;
+      const unsigned groups = static_cast<unsigned>((mp + kRows - 1) / kRows);
+      for (int step = 0; step <= jb; ++step)
+        hipLaunchKernelGGL(mdg::qr_col_step_kernel<kRows>, dim3(groups), dim3(mdg::kColThreads), 0, s, m, n, j0, jb,
+                           step, A, tau, pd, prow);
+    };
+    if (mp > mdg::kShortPanel)
+      columns(std::integral_constant<int, mdg::kPanelRowsTall>{});
+    else
+      columns(std::integral_constant<int, mdg::kPanelRowsShort>{});
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     if (nc == 0) break;
     hipLaunchKernelGGL(mdg::qr_pack_v_kernel, dim3(mdg::blocks_for(mp * jb)), dim3(256), 0, s, m, n, j0, jb, A, V,

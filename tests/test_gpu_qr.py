@@ -1,6 +1,6 @@
 """GPU checks of the blocked Householder QR in double-double (mdgemm_qr_dd),
 the downstream application whose trailing updates run on mdgemm.  Panels of
-more than 256 rows take the multi-workgroup path (two launches per column), up
+more than 256 rows take the multi-workgroup path (one launch per column), up
 to 70000 rows (2188 workgroups per launch).
 
 The GPU factorization is checked in double-double arithmetic by the CPU
