@@ -66,6 +66,7 @@ __device__ inline void std_(double* P, int64_t plane, int64_t idx, dd v) {
 constexpr int kPanelRowsShort = 16, kPanelRowsTall = 32;
 constexpr int64_t kShortPanel = 2048;
 constexpr int kColThreads = 256;  // 32 column lanes x 8 row groups
+constexpr int kFoldBatch = 8;    // partial sums a thread loads per column group before adding them
 
 constexpr int kRowGroups = kColThreads / 32;                // 8: rows rb + rg + 8 q
 constexpr int kColGroups = kMaxNb / 32;                      // columns c0 + 32 h + cc, h < 2
@@ -80,7 +81,7 @@ __global__ void __launch_bounds__(kColThreads) qr_col_step_kernel(int64_t m, int
                                                                   double* __restrict__ pd,
                                                                   double* __restrict__ prow) {
   constexpr int kRPT = kRows / kRowGroups;  // rows per thread
-  __shared__ dd red[kColThreads];
+  __shared__ dd red2[kColGroups][kColThreads];
   __shared__ dd td[kMaxNb], tw[kMaxNb], vs[kRows], xs[kRows];
   __shared__ dd s_scale, s_tau;
   __shared__ int s_mode;
@@ -119,27 +120,36 @@ __global__ void __launch_bounds__(kColThreads) qr_col_step_kernel(int64_t m, int
     // x1 for thread 0; p_c (c = s + t) for thread 64 + t, which forms tau w_c
     if (tid == 0) pv = ldd(prow_in, kMaxNb, 0);
     if (tid >= 64 && tid < 64 + ncols - 1) pv = ldd(prow_in, kMaxNb, tid - 63);
-    // d_c, 32 columns at a time: partials b = rg, rg + 8, ... in that order,
-    // eight loads in flight
-    for (int g0 = 0; g0 < ncols; g0 += 32) {
-      dd sum = {0.0, 0.0};
-      if (g0 + cc < ncols) {
-        for (int64_t b0 = rg; b0 < G; b0 += 64) {
-          dd v[8];
+    // d_c for the columns g = cc and g = 32 + cc of both groups at once:
+    // partials b = rg, rg + 8, ... in that order, up to kFoldBatch loads in
+    // flight per group (all of them when G <= 8 kFoldBatch), then the eight row
+    // groups in order
+    {
+      dd sum[kColGroups];
 #pragma unroll
-          for (int u = 0; u < 8; ++u)
-            v[u] = b0 + 8 * u < G ? ldd(pd_in, pplane, (b0 + 8 * u) * kMaxNb + g0 + cc) : dd{0.0, 0.0};
+      for (int h = 0; h < kColGroups; ++h) sum[h] = {0.0, 0.0};
+      for (int64_t b0 = rg; b0 < G; b0 += kRowGroups * kFoldBatch) {
+        dd v[kColGroups][kFoldBatch];
 #pragma unroll
-          for (int u = 0; u < 8; ++u)
-            if (b0 + 8 * u < G) sum = dd_add(sum, v[u]);
-        }
+        for (int h = 0; h < kColGroups; ++h)
+#pragma unroll
+          for (int u = 0; u < kFoldBatch; ++u) {
+            const int64_t b = b0 + kRowGroups * u;
+            v[h][u] = b < G && 32 * h + cc < ncols ? ldd(pd_in, pplane, b * kMaxNb + 32 * h + cc) : dd{0.0, 0.0};
+          }
+#pragma unroll
+        for (int h = 0; h < kColGroups; ++h)
+#pragma unroll
+          for (int u = 0; u < kFoldBatch; ++u)
+            if (b0 + kRowGroups * u < G) sum[h] = dd_add(sum[h], v[h][u]);
       }
-      red[tid] = sum;
+#pragma unroll
+      for (int h = 0; h < kColGroups; ++h) red2[h][tid] = sum[h];
       __syncthreads();
-      if (rg == 0) {
-        dd d = red[cc];
-        for (int g = 1; g < 8; ++g) d = dd_add(d, red[g * 32 + cc]);
-        td[g0 + cc] = d;
+      if (rg < kColGroups) {
+        dd d = red2[rg][cc];
+        for (int g = 1; g < kRowGroups; ++g) d = dd_add(d, red2[rg][g * 32 + cc]);
+        td[32 * rg + cc] = d;
       }
       __syncthreads();
     }
@@ -214,29 +224,30 @@ __global__ void __launch_bounds__(kColThreads) qr_col_step_kernel(int64_t m, int
   }
   __syncthreads();
   // partial d_c = x^T a_c over the block's rows below the pivot, for
-  // c = s + 32 h + cc (slot 32 h + cc), rows in increasing order; the pivot
-  // row's entries from the block that holds it
+  // c = s + 32 h + cc (slot 32 h + cc), rows in increasing order, both column
+  // groups in one pass; the pivot row's entries from the block that holds it
+  {
+    dd acc[kColGroups];
 #pragma unroll
-  for (int h = 0; h < kColGroups; ++h) {
-    if (32 * h >= jb - s) break;
-    const int c = s + 32 * h + cc;
-    dd acc = {0.0, 0.0};
-    if (c < jb) {
+    for (int h = 0; h < kColGroups; ++h) {
+      const int c = s + 32 * h + cc;
+      acc[h] = {0.0, 0.0};
+      if (c < jb) {
 #pragma unroll
-      for (int q = 0; q < kRPT; ++q) {
-        const int64_t r = rb + rg + kRowGroups * q;
-        if (r > r0 && r < re) acc = dd_add(acc, dd_mul(xs[rg + kRowGroups * q], av[h][q]));
-        if (r == r0) std_(prow_out, kMaxNb, 32 * h + cc, av[h][q]);
+        for (int q = 0; q < kRPT; ++q) {
+          const int64_t r = rb + rg + kRowGroups * q;
+          if (r > r0 && r < re) acc[h] = dd_add(acc[h], dd_mul(xs[rg + kRowGroups * q], av[h][q]));
+          if (r == r0) std_(prow_out, kMaxNb, 32 * h + cc, av[h][q]);
+        }
       }
-    }
-    red[tid] = acc;
-    __syncthreads();
-    if (rg == 0) {
-      dd d = red[cc];
-      for (int g = 1; g < 8; ++g) d = dd_add(d, red[g * 32 + cc]);
-      std_(pd_out, pplane, static_cast<int64_t>(blockIdx.x) * kMaxNb + 32 * h + cc, d);
+      red2[h][tid] = acc[h];
     }
     __syncthreads();
+    if (rg < kColGroups && 32 * rg < jb - s) {
+      dd d = red2[rg][cc];
+      for (int g = 1; g < kRowGroups; ++g) d = dd_add(d, red2[rg][g * 32 + cc]);
+      std_(pd_out, pplane, static_cast<int64_t>(blockIdx.x) * kMaxNb + 32 * rg + cc, d);
+    }
   }
 }
 
