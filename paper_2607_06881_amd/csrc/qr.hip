@@ -44,6 +44,19 @@ __device__ inline void std_(double* P, int64_t plane, int64_t idx, dd v) {
   P[plane + idx] = v.lo;
 }
 
+// The sum of x[0 .. N) (N a power of two) in a fixed pairwise tree,
+// ((x0 + x1) + (x2 + x3)) + ...: depth log2 N instead of N - 1 dependent adds,
+// the same order wherever it is called.  x is overwritten.
+template <int N>
+__device__ inline dd tree_sum(dd* x) {
+  static_assert(N > 0 && (N & (N - 1)) == 0, "a power of two");
+#pragma unroll
+  for (int w = 1; w < N; w *= 2)
+#pragma unroll
+    for (int i = 0; i + w < N; i += 2 * w) x[i] = dd_add(x[i], x[i + w]);
+  return x[0];
+}
+
 // A panel is factored by many workgroups, one launch per step s = 0 .. jb, each
 // workgroup owning kRows consecutive panel rows (16 for panels of at most
 // kShortPanel rows, so that they still spread over the chip, 32 above).  Step s
@@ -121,9 +134,10 @@ __global__ void __launch_bounds__(kColThreads) qr_col_step_kernel(int64_t m, int
     if (tid == 0) pv = ldd(prow_in, kMaxNb, 0);
     if (tid >= 64 && tid < 64 + ncols - 1) pv = ldd(prow_in, kMaxNb, tid - 63);
     // d_c for the columns g = cc and g = 32 + cc of both groups at once:
-    // partials b = rg, rg + 8, ... in that order, up to kFoldBatch loads in
-    // flight per group (all of them when G <= 8 kFoldBatch), then the eight row
-    // groups in order
+    // partials b = rg, rg + 8, ... in batches of kFoldBatch loads in flight per
+    // group (all of them when G <= 8 kFoldBatch), each batch summed in a tree
+    // (entries beyond G are zeros) and the batches in order, then the eight row
+    // groups in a tree
     {
       dd sum[kColGroups];
 #pragma unroll
@@ -138,18 +152,16 @@ __global__ void __launch_bounds__(kColThreads) qr_col_step_kernel(int64_t m, int
             v[h][u] = b < G && 32 * h + cc < ncols ? ldd(pd_in, pplane, b * kMaxNb + 32 * h + cc) : dd{0.0, 0.0};
           }
 #pragma unroll
-        for (int h = 0; h < kColGroups; ++h)
-#pragma unroll
-          for (int u = 0; u < kFoldBatch; ++u)
-            if (b0 + kRowGroups * u < G) sum[h] = dd_add(sum[h], v[h][u]);
+        for (int h = 0; h < kColGroups; ++h) sum[h] = dd_add(sum[h], tree_sum<kFoldBatch>(v[h]));
       }
 #pragma unroll
       for (int h = 0; h < kColGroups; ++h) red2[h][tid] = sum[h];
       __syncthreads();
       if (rg < kColGroups) {
-        dd d = red2[rg][cc];
-        for (int g = 1; g < kRowGroups; ++g) d = dd_add(d, red2[rg][g * 32 + cc]);
-        td[32 * rg + cc] = d;
+        dd t[kRowGroups];
+#pragma unroll
+        for (int g = 0; g < kRowGroups; ++g) t[g] = red2[rg][g * 32 + cc];
+        td[32 * rg + cc] = tree_sum<kRowGroups>(t);
       }
       __syncthreads();
     }
@@ -224,29 +236,30 @@ __global__ void __launch_bounds__(kColThreads) qr_col_step_kernel(int64_t m, int
   }
   __syncthreads();
   // partial d_c = x^T a_c over the block's rows below the pivot, for
-  // c = s + 32 h + cc (slot 32 h + cc), rows in increasing order, both column
-  // groups in one pass; the pivot row's entries from the block that holds it
+  // c = s + 32 h + cc (slot 32 h + cc): each thread's rows and then the eight
+  // row groups in trees, both column groups in one pass; the pivot row's
+  // entries from the block that holds it
   {
     dd acc[kColGroups];
 #pragma unroll
     for (int h = 0; h < kColGroups; ++h) {
       const int c = s + 32 * h + cc;
-      acc[h] = {0.0, 0.0};
-      if (c < jb) {
+      dd pr[kRPT];
 #pragma unroll
-        for (int q = 0; q < kRPT; ++q) {
-          const int64_t r = rb + rg + kRowGroups * q;
-          if (r > r0 && r < re) acc[h] = dd_add(acc[h], dd_mul(xs[rg + kRowGroups * q], av[h][q]));
-          if (r == r0) std_(prow_out, kMaxNb, 32 * h + cc, av[h][q]);
-        }
+      for (int q = 0; q < kRPT; ++q) {
+        const int64_t r = rb + rg + kRowGroups * q;
+        pr[q] = c < jb && r > r0 && r < re ? dd_mul(xs[rg + kRowGroups * q], av[h][q]) : dd{0.0, 0.0};
+        if (c < jb && r == r0) std_(prow_out, kMaxNb, 32 * h + cc, av[h][q]);
       }
+      acc[h] = tree_sum<kRPT>(pr);
       red2[h][tid] = acc[h];
     }
     __syncthreads();
     if (rg < kColGroups && 32 * rg < jb - s) {
-      dd d = red2[rg][cc];
-      for (int g = 1; g < kRowGroups; ++g) d = dd_add(d, red2[rg][g * 32 + cc]);
-      std_(pd_out, pplane, static_cast<int64_t>(blockIdx.x) * kMaxNb + 32 * rg + cc, d);
+      dd t[kRowGroups];
+#pragma unroll
+      for (int g = 0; g < kRowGroups; ++g) t[g] = red2[rg][g * 32 + cc];
+      std_(pd_out, pplane, static_cast<int64_t>(blockIdx.x) * kMaxNb + 32 * rg + cc, tree_sum<kRowGroups>(t));
     }
   }
 }
