@@ -50,6 +50,8 @@ def lib():
         L.oracle_qr_dd.argtypes = [_i64, _i64, _dp, _dp]
         L.oracle_qr_dd.restype = ctypes.c_int
         L.oracle_qr_dd_check.argtypes = [_i64, _i64, _dp, _dp, _dp, _dp, _dp]
+        L.oracle_taylor_dd.argtypes = [_i64, _i64, ctypes.c_int, _dp, _dp, _dp]
+        L.oracle_taylor_dd.restype = ctypes.c_int
         L.oracle_qr_dd_check.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -192,3 +194,17 @@ def qr_dd_check(A0, QR, tau):
     if st:
         raise ValueError(f"oracle_qr_dd_check failed: {st}")
     return float(out[0]), float(out[1]), Q
+
+
+def taylor_dd(A, B):
+    """X [d+1][2][n][r]: the Taylor coefficients of the solution of A(t) X(t) = B(t)
+    modulo t^(d+1) (A [d+1][2][n][n], B [d+1][2][n][r]), each X_k from
+    A_0 X_k = B_k - sum_{i=1..k} A_i X_{k-i} by the QR of A_0, in double-double."""
+    A, B = _f64(A), _f64(B)
+    nd, _, n, _ = A.shape
+    r = B.shape[3]
+    X = np.zeros((nd, 2, n, r), dtype=np.float64)
+    st = lib().oracle_taylor_dd(n, r, nd - 1, _d(A), _d(B), _d(X))
+    if st:
+        raise ValueError(f"oracle_taylor_dd failed: {st}")
+    return X

@@ -706,3 +706,99 @@ int oracle_qr_dd_check(int64_t m, int64_t n, const double* A0, const double* QR,
   free(Q);
   return ORACLE_OK;
 }
+
+/* ------------------------------------------------------------------------- */
+/* 6. Taylor series of the solution of a linear system of power series (the   */
+/*    application the paper names for the QR, section 5)                        */
+/* ------------------------------------------------------------------------- */
+
+/* A(t) X(t) = B(t) modulo t^(d+1) for A [d+1][2][n][n], B [d+1][2][n][r]:
+ * comparing the coefficients of t^k, A_0 X_k = B_k - sum_{i=1..k} A_i X_{k-i}.
+ * Each X_k is formed as written, in double-double: the right-hand side entry by
+ * entry (each product sum in increasing index, then subtracted), then the
+ * solve with the QR of A_0 (oracle_qr_dd): y = Q^T rhs by the reflections
+ * H_0, H_1, ... in turn, then back substitution R x = y.  X [d+1][2][n][r]. */
+int oracle_taylor_dd(int64_t n, int64_t r, int d, const double* A, const double* B, double* X) {
+  if (n < 1 || r < 1 || d < 0) return ORACLE_EINVAL;
+  const int64_t PA = n * n, PB = n * r;
+  double* QR = (double*)malloc(sizeof(double) * 2 * (size_t)PA);
+  double* tau = (double*)malloc(sizeof(double) * 2 * (size_t)n);
+  double* y = (double*)malloc(sizeof(double) * 2 * (size_t)PB);
+  if (!QR || !tau || !y) {
+    free(QR);
+    free(tau);
+    free(y);
+    return ORACLE_EINVAL;
+  }
+  memcpy(QR, A, sizeof(double) * 2 * (size_t)PA);
+  int st = oracle_qr_dd(n, n, QR, tau);
+#define QA(i, c, l) QR[(l) * PA + (i) * n + (c)]
+#define YY(i, c, l) y[(l) * PB + (i) * r + (c)]
+  for (int k = 0; st == ORACLE_OK && k <= d; ++k) {
+    const double* Bk = B + (int64_t)k * 2 * PB;
+    double* Xk = X + (int64_t)k * 2 * PB;
+    /* rhs = B_k - sum_{i=1..k} A_i X_{k-i} */
+    for (int64_t i = 0; i < n; ++i)
+      for (int64_t c = 0; c < r; ++c) {
+        double v[2] = {Bk[i * r + c], Bk[PB + i * r + c]}, t[2];
+        for (int a = 1; a <= k; ++a) {
+          const double* Ai = A + (int64_t)a * 2 * PA;
+          const double* Xj = X + (int64_t)(k - a) * 2 * PB;
+          double s[2] = {0.0, 0.0};
+          for (int64_t l = 0; l < n; ++l) {
+            double p[2] = {Ai[i * n + l], Ai[PA + i * n + l]}, q[2] = {Xj[l * r + c], Xj[PB + l * r + c]};
+            dd_mul(p, q, t);
+            dd_add(s, t, s);
+          }
+          dd_sub(v, s, v);
+        }
+        YY(i, c, 0) = v[0];
+        YY(i, c, 1) = v[1];
+      }
+    /* y = Q^T rhs: H_j = I - tau_j v_j v_j^T for j = 0, 1, ... (v_j(j) = 1) */
+    for (int64_t j = 0; j < n; ++j) {
+      double tj[2] = {tau[j], tau[n + j]}, t[2];
+      if (tj[0] == 0.0) continue;
+      for (int64_t c = 0; c < r; ++c) {
+        double w[2] = {YY(j, c, 0), YY(j, c, 1)};
+        for (int64_t i = j + 1; i < n; ++i) {
+          double v[2] = {QA(i, j, 0), QA(i, j, 1)}, q[2] = {YY(i, c, 0), YY(i, c, 1)};
+          dd_mul(v, q, t);
+          dd_add(w, t, w);
+        }
+        double tw[2], q0[2] = {YY(j, c, 0), YY(j, c, 1)};
+        dd_mul(tj, w, tw);
+        dd_sub(q0, tw, q0);
+        YY(j, c, 0) = q0[0];
+        YY(j, c, 1) = q0[1];
+        for (int64_t i = j + 1; i < n; ++i) {
+          double v[2] = {QA(i, j, 0), QA(i, j, 1)}, q[2] = {YY(i, c, 0), YY(i, c, 1)};
+          dd_mul(tw, v, t);
+          dd_sub(q, t, q);
+          YY(i, c, 0) = q[0];
+          YY(i, c, 1) = q[1];
+        }
+      }
+    }
+    /* R x = y, rows from the bottom */
+    for (int64_t c = 0; c < r; ++c)
+      for (int64_t i = n - 1; i >= 0; --i) {
+        double s[2] = {YY(i, c, 0), YY(i, c, 1)}, t[2];
+        for (int64_t l = i + 1; l < n; ++l) {
+          double rr[2] = {QA(i, l, 0), QA(i, l, 1)}, x[2] = {Xk[l * r + c], Xk[PB + l * r + c]};
+          dd_mul(rr, x, t);
+          dd_sub(s, t, s);
+        }
+        double rii[2] = {QA(i, i, 0), QA(i, i, 1)}, q[2];
+        dd_div(s, rii, q);
+        Xk[i * r + c] = q[0];
+        Xk[PB + i * r + c] = q[1];
+      }
+  }
+#undef QA
+#undef YY
+  free(QR);
+  free(tau);
+  free(y);
+  return st;
+}
