@@ -466,6 +466,31 @@ size_t mdgemm_qr_dd_workspace_bytes(int64_t m, int64_t n, int nb);
 int mdgemm_qr_dd(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspace, size_t workspace_bytes,
                  void* stream);
 
+/* ---- application: Taylor series of the solution of a power-series system ----
+ * The application the paper names for the QR (section 5): the coefficients of
+ * X(t) = X_0 + X_1 t + ... + X_d t^d with A(t) X(t) = B(t) modulo t^(d+1). */
+
+/* Workspace bytes of mdgemm_taylor_dd (SIZE_MAX for invalid arguments: n in
+ * 1..32768, r in 1..2^20, d in 0..1024). */
+size_t mdgemm_taylor_dd_workspace_bytes(int64_t n, int64_t r, int d);
+
+/* Solve A(t) X(t) = B(t) modulo t^(d+1) for matrix power series in
+ * double-double: A [d+1][2][n][n] holds A_0 .. A_d, B [d+1][2][n][r] holds
+ * B_0 .. B_d, X [d+1][2][n][r] receives X_0 .. X_d (each coefficient a limb-major
+ * double-double block), such that A_0 X_k = B_k - sum_{i=1..k} A_i X_{k-i}.
+ * A_0 must be nonsingular (a singular or numerically singular A_0 leaves
+ * non-finite or meaningless values in X; no check is made).  Method: the QR of
+ * A_0 (as mdgemm_qr_dd, 64-column panels) with its reflections applied to an
+ * identity block, which gives Q^T; blocked back substitution with R turns it
+ * into M = R^-1 Q^T; then for each degree X_k = M (B_k - [A_k ... A_1]
+ * [X_0; ...; X_{k-1}]), two products on mdgemm_ex at the adaptive digit width.
+ * workspace: caller-owned device buffer of mdgemm_taylor_dd_workspace_bytes()
+ * bytes, overlapping none of A, B and X; X overlaps neither A nor B.  Stream
+ * ordered; returns MDGEMM_OK, MDGEMM_EINVAL, MDGEMM_EWORKSPACE or a status of
+ * mdgemm_ex.  Inputs must be finite and normalized double-doubles. */
+int mdgemm_taylor_dd(int64_t n, int64_t r, int d, const double* A, const double* B, double* X, void* workspace,
+                     size_t workspace_bytes, void* stream);
+
 /* ---- calibration (measurement aids, not part of the product) ---------------
  * The rates the stages are measured against, on the caller's device. */
 

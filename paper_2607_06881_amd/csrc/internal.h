@@ -194,4 +194,13 @@ hipError_t launch_zero_f64(double* p, int64_t count, hipStream_t stream);
 hipError_t launch_nonfinite_scan(const double* X, int64_t count, int32_t* flag, hipStream_t stream);
 hipError_t launch_set_i32(int32_t* p, int64_t count, int32_t value, hipStream_t stream);
 
+// Householder QR in double-double of the first nf columns of A [2][m][n]
+// (limb-major, nf <= m), with the reflections applied to the columns nf .. n - 1
+// as well, which then hold Q^T times their input; tau [2][n] (entries 0 .. nf - 1
+// written).  Panels of nb <= 64 columns.  qr_core_workspace gives the bytes of
+// the workspace qr_core takes (SIZE_MAX for invalid sizes); qr_core checks no
+// overlaps and returns an mdgemm status.
+size_t qr_core_workspace(int64_t m, int64_t nf, int64_t n, int nb);
+int qr_core(int64_t m, int64_t nf, int64_t n, int nb, double* A, double* tau, void* workspace, hipStream_t s);
+
 }  // namespace mdg

@@ -438,7 +438,9 @@ mdgemm_opts qr_gemm_opts() {
   return o;
 }
 
-bool qr_layout(int64_t m, int64_t n, int nb, QrLayout* L) {
+// nf: the columns factored; n: all columns of A (the reflections are applied to
+// columns nf .. n - 1 as well)
+bool qr_layout(int64_t m, int64_t nf, int64_t n, int nb, QrLayout* L) {
   const size_t dd_bytes = 2 * sizeof(double);
   const size_t vbytes = align256(dd_bytes * static_cast<size_t>(m) * nb);
   const size_t xbytes = align256(dd_bytes * static_cast<size_t>(m) * static_cast<size_t>(n));
@@ -473,8 +475,8 @@ bool qr_layout(int64_t m, int64_t n, int nb, QrLayout* L) {
   // the largest workspace of the three products of any panel: V^T X, T^T W, V W2
   mdgemm_opts o = qr_gemm_opts();
   size_t need = 0;
-  for (int64_t j0 = 0; j0 < n; j0 += nb) {
-    const int64_t jb = std::min<int64_t>(nb, n - j0), mp = m - j0, nc = n - j0 - jb;
+  for (int64_t j0 = 0; j0 < nf; j0 += nb) {
+    const int64_t jb = std::min<int64_t>(nb, nf - j0), mp = m - j0, nc = n - j0 - jb;
     const size_t c[3] = {nc ? mdgemm_workspace_bytes(jb, nc, mp, 2, &o) : 0,
                          nc ? mdgemm_workspace_bytes(jb, nc, jb, 2, &o) : 0,
                          nc ? mdgemm_workspace_bytes(mp, nc, jb, 2, &o) : 0};
@@ -498,8 +500,7 @@ extern "C" {
 size_t mdgemm_qr_dd_workspace_bytes(int64_t m, int64_t n, int nb) {
   if (m < 1 || n < 1 || m < n || nb < 1 || nb > mdg::kMaxNb || m > (int64_t{1} << 20) || n > (int64_t{1} << 20))
     return SIZE_MAX;
-  mdg::QrLayout L;
-  return mdg::qr_layout(m, n, nb, &L) ? L.total : SIZE_MAX;
+  return mdg::qr_core_workspace(m, n, n, nb);
 }
 
 }  // extern "C"
@@ -510,16 +511,32 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
             void* stream) {
   if (m < 1 || n < 1 || m < n || nb < 1 || nb > mdg::kMaxNb || !A || !tau || !workspace) return MDGEMM_EINVAL;
   if (m > (int64_t{1} << 20) || n > (int64_t{1} << 20)) return MDGEMM_EINVAL;
-  mdg::QrLayout L;
-  if (!mdg::qr_layout(m, n, nb, &L)) return MDGEMM_EINVAL;
-  if (workspace_bytes < L.total) return MDGEMM_EWORKSPACE;
+  const size_t need = mdg::qr_core_workspace(m, n, n, nb);
+  if (need == SIZE_MAX) return MDGEMM_EINVAL;
+  if (workspace_bytes < need) return MDGEMM_EWORKSPACE;
   const uintptr_t w0 = reinterpret_cast<uintptr_t>(workspace), a0 = reinterpret_cast<uintptr_t>(A),
                   t0 = reinterpret_cast<uintptr_t>(tau);
   const uintptr_t abytes = sizeof(double) * 2 * static_cast<uintptr_t>(m) * n, tbytes = sizeof(double) * 2 * n;
-  if ((w0 < a0 + abytes && a0 < w0 + L.total) || (w0 < t0 + tbytes && t0 < w0 + L.total) ||
+  if ((w0 < a0 + abytes && a0 < w0 + need) || (w0 < t0 + tbytes && t0 < w0 + need) ||
       (a0 < t0 + tbytes && t0 < a0 + abytes))
     return MDGEMM_EINVAL;
-  const hipStream_t s = static_cast<hipStream_t>(stream);
+  return mdg::qr_core(m, n, n, nb, A, tau, workspace, static_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+namespace mdg {
+
+size_t qr_core_workspace(int64_t m, int64_t nf, int64_t n, int nb) {
+  if (m < 1 || nf < 1 || nf > m || n < nf || nb < 1 || nb > kMaxNb) return SIZE_MAX;
+  QrLayout L;
+  return qr_layout(m, nf, n, nb, &L) ? L.total : SIZE_MAX;
+}
+
+int qr_core(int64_t m, int64_t nf, int64_t n, int nb, double* A, double* tau, void* workspace, hipStream_t s) {
+  QrLayout L;
+  if (!qr_layout(m, nf, n, nb, &L)) return MDGEMM_EINVAL;
+  void* const stream = s;
   // the T kernel's dynamic LDS beyond 64 KB: allowed once for the kernel (a
   // failure shows up as a launch error below)
   static std::once_flag once;
@@ -545,8 +562,8 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
   o.stream = stream;
   o.workspace = ws + L.gemm;
   o.workspace_bytes = L.gemm_bytes;
-  for (int64_t j0 = 0; j0 < n; j0 += nb) {
-    const int jb = static_cast<int>(std::min<int64_t>(nb, n - j0));
+  for (int64_t j0 = 0; j0 < nf; j0 += nb) {
+    const int jb = static_cast<int>(std::min<int64_t>(nb, nf - j0));
     const int64_t mp = m - j0, c0 = j0 + jb, nc = n - c0;
     auto columns = [&](auto rows) {
       constexpr int kRows = decltype(rows)::value;
@@ -585,7 +602,7 @@ int qr_impl(int64_t m, int64_t n, int nb, double* A, double* tau, void* workspac
   return MDGEMM_OK;
 }
 
-}  // namespace
+}  // namespace mdg
 
 extern "C" {
 

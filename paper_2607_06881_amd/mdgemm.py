@@ -89,6 +89,8 @@ EXPORTED = (
     "mdgemm_schedule_levels",
     "mdgemm_qr_dd_workspace_bytes",
     "mdgemm_qr_dd",
+    "mdgemm_taylor_dd_workspace_bytes",
+    "mdgemm_taylor_dd",
     "mdgemm_probe_mfma_f64",
     "mdgemm_probe_copy",
     "mdgemm_probe_stream",
@@ -179,6 +181,10 @@ def lib() -> ctypes.CDLL:
         L.mdgemm_qr_dd_workspace_bytes.restype = ctypes.c_size_t
         L.mdgemm_qr_dd.argtypes = [_i64, _i64, ctypes.c_int, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.mdgemm_qr_dd.restype = ctypes.c_int
+        L.mdgemm_taylor_dd_workspace_bytes.argtypes = [_i64, _i64, ctypes.c_int]
+        L.mdgemm_taylor_dd_workspace_bytes.restype = ctypes.c_size_t
+        L.mdgemm_taylor_dd.argtypes = [_i64, _i64, ctypes.c_int, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+        L.mdgemm_taylor_dd.restype = ctypes.c_int
         L.mdgemm_probe_mfma_f64.argtypes = [_i64, _i64, _vp, _vp]
         L.mdgemm_probe_mfma_f64.restype = ctypes.c_int64
         L.mdgemm_probe_copy.argtypes = [_vp, _vp, _i64, _vp]
@@ -604,3 +610,31 @@ def mdgemm_qr_dd(A: torch.Tensor, nb: int = 64, workspace: Optional[torch.Tensor
     _check(lib().mdgemm_qr_dd(m, n, nb, _ptr(A), _ptr(tau), _ptr(workspace), workspace.numel(), _stream(stream)),
            "mdgemm_qr_dd")
     return A, tau
+
+
+def mdgemm_taylor_dd(A: torch.Tensor, B: torch.Tensor, X: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """The Taylor coefficients X [d+1, 2, n, r] of the solution of A(t) X(t) = B(t)
+    modulo t^(d+1), for the double-double coefficients A [d+1, 2, n, n] and
+    B [d+1, 2, n, r] (A_0 nonsingular)."""
+    _dev_tensor(A, torch.float64, "A")
+    _dev_tensor(B, torch.float64, "B")
+    if A.dim() != 4 or A.shape[1] != 2 or A.shape[2] != A.shape[3]:
+        raise ValueError("A must hold d + 1 double-double matrices [d + 1, 2, n, n]")
+    nd, _, n, _ = A.shape
+    if B.dim() != 4 or B.shape[0] != nd or B.shape[1] != 2 or B.shape[2] != n:
+        raise ValueError("B must be [d + 1, 2, n, r] with the d and n of A")
+    r = B.shape[3]
+    if X is None:
+        X = torch.empty((nd, 2, n, r), dtype=torch.float64, device=A.device)
+    _dev_tensor(X, torch.float64, "X")
+    if tuple(X.shape) != (nd, 2, n, r):
+        raise ValueError("X must be [d + 1, 2, n, r]")
+    if workspace is None:
+        need = int(lib().mdgemm_taylor_dd_workspace_bytes(n, r, nd - 1))
+        if need == 2**64 - 1:
+            _check(MDGEMM_EINVAL, "mdgemm_taylor_dd_workspace_bytes")
+        workspace = torch.empty(need, dtype=torch.uint8, device=A.device)
+    _check(lib().mdgemm_taylor_dd(n, r, nd - 1, _ptr(A), _ptr(B), _ptr(X), _ptr(workspace), workspace.numel(),
+                                  _stream(stream)), "mdgemm_taylor_dd")
+    return X

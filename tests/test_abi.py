@@ -226,6 +226,22 @@ def test_fused_path_taken_where_its_estimated_time_is_lower(lib):
     assert not _fused(17, 33, 512, 2, flags=md.MDGEMM_STAGED)
 
 
+def test_taylor_refusals(lib):
+    # sizes out of range have no workspace; null pointers and a short workspace
+    # are refused before any device work
+    big = 2**64 - 1
+    assert lib.mdgemm_taylor_dd_workspace_bytes(0, 1, 0) == big
+    assert lib.mdgemm_taylor_dd_workspace_bytes(4, 0, 0) == big
+    assert lib.mdgemm_taylor_dd_workspace_bytes(4, 1, -1) == big
+    assert lib.mdgemm_taylor_dd_workspace_bytes(40000, 1, 0) == big
+    need = lib.mdgemm_taylor_dd_workspace_bytes(20, 3, 2)
+    assert 0 < need < big and need > lib.mdgemm_taylor_dd_workspace_bytes(20, 3, 1)
+    assert lib.mdgemm_taylor_dd(20, 3, 2, None, None, None, None, need, None) == md.MDGEMM_EINVAL
+    fake = ctypes.c_void_p(1 << 40)
+    assert lib.mdgemm_taylor_dd(20, 3, 2, fake, ctypes.c_void_p(2 << 40), ctypes.c_void_p(3 << 40),
+                                ctypes.c_void_p(4 << 40), need - 1, None) == md.MDGEMM_EWORKSPACE
+
+
 def test_binding_refuses_cpu_tensors(lib):
     import torch
 
