@@ -37,7 +37,8 @@ Prints one JSON line:
   steps each beside the headline, which keeps the paper's separate pair
   products on the FP64 matrix cores;
 * ``--extras`` adds ``karatsuba_adaptive``, ``sign_groups`` (section 3's
-  sign grouping, four products, the same limbs) and ``qr_dd`` (the
+  sign grouping, four products, the same limbs), ``taylor_dd`` (the QR's
+  application to power-series systems, timed) and ``qr_dd`` (the
   double-double Householder QR built on the product) lines;
 * ``cpu_baseline``: the CPU oracle's classic multiple-double GEMM (one
   sequential inner product per element, all host cores) timed on a bounded
@@ -159,6 +160,50 @@ def stage_probes(md, torch, dev, stream, mixes, reps=3):
         out[key] = {"GB/s": round(gbs, 1), "count": count, "reads": reads, "writes": writes}
         del src, dst
     return out
+
+
+def taylor_dd_line(md, torch, dev, stream, no_cpu, n=1024, r=64, d=8, reps=3):
+    """The QR's application: the Taylor coefficients of the solution of
+    A(t) X(t) = B(t) modulo t^(d+1) (mdgemm_taylor_dd) for a seeded series of
+    n x n double-double coefficients (A_i normal / sqrt(n), A_0 + 2 I, so A_0 is
+    well conditioned) and n x r right-hand sides, timed with HIP events around
+    the call; its parity is the Taylor tests'.  Beside it, the oracle's
+    degree-by-degree QR solve of a 128 x 128, r = 8, d = 4 series (CPU)."""
+    import numpy as np
+
+    def series(nn, rr, dd, seed):
+        rng = np.random.default_rng(seed)
+        A = rng.standard_normal((dd + 1, 2, nn, nn)) / np.sqrt(nn)
+        A[:, 1] *= 2.0 ** -60 * rng.uniform(-1, 1, size=(dd + 1, nn, nn))
+        A[0, 0] += 2.0 * np.eye(nn)
+        B = rng.standard_normal((dd + 1, 2, nn, rr))
+        B[:, 1] *= 2.0 ** -60 * rng.uniform(-1, 1, size=(dd + 1, nn, rr))
+        return A, B
+
+    A_h, B_h = series(n, r, d, 7)
+    Ag, Bg = torch.from_numpy(A_h).to(dev), torch.from_numpy(B_h).to(dev)
+    need = int(md.lib().mdgemm_taylor_dd_workspace_bytes(n, r, d))
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    X = md.mdgemm_taylor_dd(Ag, Bg, workspace=ws, stream=stream)  # warm-up
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    times = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        e0.record(stream)
+        md.mdgemm_taylor_dd(Ag, Bg, X=X, workspace=ws, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    res = {"n": n, "r": r, "d": d, "ms": round(float(np.median(times)), 3), "workspace_bytes": need}
+    del ws, X, Ag, Bg
+    if not no_cpu:
+        from oracle import coracle
+
+        a, b = series(128, 8, 4, 8)
+        t0 = time.perf_counter()
+        coracle.taylor_dd(a, b)
+        res["cpu_oracle_128_r8_d4_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
+    return res
 
 
 def qr_dd_line(md, torch, dev, stream, A, no_cpu, nb=64, reps=3):
@@ -608,6 +653,7 @@ def main(argv=None) -> int:
         out["sign_groups"] = grouped(md.MDGEMM_GROUP_SIGN)
     if args.extras and L == 2:
         out["qr_dd"] = qr_dd_line(md, torch, dev, stream, A, args.no_cpu_baseline)
+        out["taylor_dd"] = taylor_dd_line(md, torch, dev, stream, args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, A_h, B_h, args.cpu_seconds)
     print(json.dumps(out), flush=True)

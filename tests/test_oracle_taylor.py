@@ -17,6 +17,7 @@ import numpy as np
 
 from oracle import coracle
 
+
 def _scalar(coeffs, d):
     out = np.zeros((d + 1, 2, 1, 1))
     for k, c in enumerate(coeffs):
