@@ -72,26 +72,35 @@ __global__ void __launch_bounds__(256) tl_identity_kernel(int64_t n, double* __r
   }
 }
 
-// Y <- R^-1 Y for an upper triangular jb x jb block R (jb <= kTaylorNb, staged
-// in LDS) and a jb x w block Y, in place, one thread per column of Y: back
-// substitution y_i = (y_i - sum_{l > i} R(i, l) y_l) / R(i, i), the sum in
-// increasing l.
-__global__ void __launch_bounds__(256) tl_trsm_kernel(int jb, int64_t w, const double* __restrict__ R,
-                                                      int64_t rplane, int64_t rld, double* __restrict__ Y,
-                                                      int64_t yplane, int64_t yld) {
-  __shared__ dd sR[kTaylorNb * kTaylorNb];
+// Y <- R^-1 Y for an upper triangular jb x jb block R (jb <= kTaylorNb = 64)
+// and a jb x w block Y, in place: one wave per column of Y, lane l holding row
+// l, kTrsmWaves columns per workgroup.  Right-looking back substitution: for
+// i = jb - 1 down to 0, lane i forms x_i = y_i / R(i, i), which every lane
+// takes by a shuffle, and the lanes l < i subtract R(l, i) x_i from their y_l.
+// R is staged transposed in LDS (lanes read consecutive entries).
+constexpr int kTrsmWaves = 4;
+__global__ void __launch_bounds__(64 * kTrsmWaves) tl_trsm_kernel(int jb, int64_t w, const double* __restrict__ R,
+                                                                  int64_t rplane, int64_t rld,
+                                                                  double* __restrict__ Y, int64_t yplane,
+                                                                  int64_t yld) {
+  static_assert(kTaylorNb == 64, "one lane per row of the diagonal block");
+  __shared__ dd rt[kTaylorNb][kTaylorNb];  // rt[i][l] = R(l, i) for l <= i, else 0
   for (int e = threadIdx.x; e < jb * jb; e += blockDim.x) {
     const int i = e / jb, l = e - i * jb;
-    sR[i * kTaylorNb + l] = l >= i ? tl_load(R, rplane, i * rld + l) : dd{0.0, 0.0};
+    rt[i][l] = l <= i ? tl_load(R, rplane, l * rld + i) : dd{0.0, 0.0};
   }
   __syncthreads();
-  const int64_t c = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * kTrsmWaves + (threadIdx.x >> 6);
   if (c >= w) return;
+  dd y = lane < jb ? tl_load(Y, yplane, lane * yld + c) : dd{0.0, 0.0};
   for (int i = jb - 1; i >= 0; --i) {
-    dd s = tl_load(Y, yplane, i * yld + c);
-    for (int l = i + 1; l < jb; ++l) s = dd_sub(s, dd_mul(sR[i * kTaylorNb + l], tl_load(Y, yplane, l * yld + c)));
-    tl_store(Y, yplane, i * yld + c, dd_div(s, sR[i * kTaylorNb + i]));
+    const dd q = dd_div(y, rt[i][i]);  // meaningful on lane i
+    const dd x = {__shfl(q.hi, i, 64), __shfl(q.lo, i, 64)};
+    if (lane == i) y = x;
+    else if (lane < i) y = dd_sub(y, dd_mul(rt[i][lane], x));
   }
+  if (lane < jb) tl_store(Y, yplane, lane * yld + c, y);
 }
 
 inline unsigned grid_for(int64_t count) {
@@ -214,8 +223,8 @@ int taylor_impl(int64_t n, int64_t r, int d, const double* A, const double* B, d
       hipLaunchKernelGGL(tl_sub_kernel, dim3(grid_for(ppb)), dim3(256), 0, s, int64_t{jb}, n, Y + j0 * n2, pa, n2, Pb,
                          ppb, n, Y + j0 * n2, pa, n2);
     }
-    hipLaunchKernelGGL(tl_trsm_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, s, jb, n,
-                       Aug + j0 * n2 + j0, pa, n2, Y + j0 * n2, pa, n2);
+    hipLaunchKernelGGL(tl_trsm_kernel, dim3(static_cast<unsigned>((n + kTrsmWaves - 1) / kTrsmWaves)),
+                       dim3(64 * kTrsmWaves), 0, s, jb, n, Aug + j0 * n2 + j0, pa, n2, Y + j0 * n2, pa, n2);
     if (!ok()) return MDGEMM_EHIP;
   }
   hipLaunchKernelGGL(tl_copy_kernel, dim3(grid_for(pn)), dim3(256), 0, s, n, n, Y, pa, n2, M, pn, n);
