@@ -9,6 +9,9 @@ on mdgemm_ex per degree.
   n = 1, a ragged n): X against the oracle's degree-by-degree QR solve in
   double-double, to a relative 1e-27 (both are accurate to the conditioning of
   A_0 times the double-double unit roundoff, 1e-30 here).
+* n = 2100 (QR panels taller than 2048 rows, 33 back-substitution blocks): a
+  banded nilpotent case exact in integers, and a random system whose identity
+  A(t) X(t) = B(t) holds to float64 rounding (the oracle is too slow there).
 """
 
 import numpy as np
@@ -78,3 +81,54 @@ def test_taylor_against_the_oracle(n, r, d, seed):
         print(f"[result] taylor n={n} k={k}: max |X - X_oracle| / max |X| = {err / scale:.2e}", flush=True)
         assert err <= 1e-27 * scale, (k, err / scale)
         assert np.allclose(got, want, rtol=1e-12, atol=1e-14 * scale)
+
+
+def test_taylor_large_banded_nilpotent_exact():
+    # n above 2048: the first QR panels take 32-row workgroups, 33 back-substitution
+    # blocks; N has three superdiagonals, so its powers stay small integers
+    n, r, d = 2100, 3, 4
+    print(f"[case] taylor banded nilpotent n={n} r={r} d={d}", flush=True)
+    rng = np.random.default_rng(23)
+    N = np.zeros((n, n), dtype=np.int64)
+    for off in (1, 2, 3):
+        N += np.diag(rng.integers(-1, 2, size=n - off), off)
+    Bi = rng.integers(-50, 50, size=(d + 1, n, r))
+    A = np.zeros((d + 1, 2, n, n))
+    A[0, 0] = np.eye(n)
+    A[1, 0] = -N
+    B = np.zeros((d + 1, 2, n, r))
+    B[:, 0] = Bi
+    X = md.mdgemm_taylor_dd(torch.from_numpy(A).to(DEV), torch.from_numpy(B).to(DEV))
+    torch.cuda.synchronize()
+    Xh = X.cpu().numpy()
+    # want[k] = sum_j N^j B_{k-j} = B_k + N want[k-1], exact in int64
+    want = [Bi[0]]
+    for k in range(1, d + 1):
+        want.append(Bi[k] + N @ want[-1])
+    for k in range(d + 1):
+        assert np.array_equal(Xh[k, 0], want[k].astype(np.float64)), k
+        assert not Xh[k, 1].any(), k
+
+
+def test_taylor_large_random_residual():
+    # a random well-conditioned system at n = 2100: the identity A(t) X(t) = B(t)
+    # holds to float64 rounding (the double-double accuracy is the oracle tests')
+    n, r, d = 2100, 3, 2
+    print(f"[case] taylor random n={n} r={r} d={d}", flush=True)
+    rng = np.random.default_rng(29)
+    A = np.zeros((d + 1, 2, n, n))
+    B = np.zeros((d + 1, 2, n, r))
+    for k in range(d + 1):
+        A[k, 0], A[k, 1] = _dd(rng, (n, n), 1.0 / np.sqrt(n))
+        B[k, 0], B[k, 1] = _dd(rng, (n, r))
+    A[0, 0] += 2.0 * np.eye(n)
+    X = md.mdgemm_taylor_dd(torch.from_numpy(A).to(DEV), torch.from_numpy(B).to(DEV))
+    torch.cuda.synchronize()
+    Xh = X.cpu().numpy()
+    assert np.isfinite(Xh).all()
+    for k in range(d + 1):
+        res = sum(A[i, 0] @ Xh[k - i, 0] for i in range(k + 1)) - B[k, 0]
+        scale = np.abs(B[k, 0]).max() + sum(np.abs(A[i, 0]).max() * np.abs(Xh[k - i, 0]).max() * np.sqrt(n)
+                                           for i in range(k + 1))
+        print(f"[result] taylor n={n} k={k}: float64 residual / scale = {np.abs(res).max() / scale:.2e}", flush=True)
+        assert np.abs(res).max() <= 1e-13 * scale, k
