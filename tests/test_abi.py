@@ -240,6 +240,11 @@ def test_taylor_refusals(lib):
     fake = ctypes.c_void_p(1 << 40)
     assert lib.mdgemm_taylor_dd(20, 3, 2, fake, ctypes.c_void_p(2 << 40), ctypes.c_void_p(3 << 40),
                                 ctypes.c_void_p(4 << 40), need - 1, None) == md.MDGEMM_EWORKSPACE
+    # X on top of A, or the workspace on top of B: refused
+    assert lib.mdgemm_taylor_dd(20, 3, 2, fake, ctypes.c_void_p(2 << 40), ctypes.c_void_p((1 << 40) + 64),
+                                ctypes.c_void_p(4 << 40), need, None) == md.MDGEMM_EINVAL
+    assert lib.mdgemm_taylor_dd(20, 3, 2, fake, ctypes.c_void_p(2 << 40), ctypes.c_void_p(3 << 40),
+                                ctypes.c_void_p((2 << 40) - 64), need, None) == md.MDGEMM_EINVAL
 
 
 def test_binding_refuses_cpu_tensors(lib):
