@@ -453,10 +453,10 @@ size_t mdgemm_qr_dd_workspace_bytes(int64_t m, int64_t n, int nb);
  * v_j zero above row j.  On return A holds R on and above the diagonal (R(j, j)
  * >= 0) and v_j below it (LAPACK's convention), tau [2][n] the tau_j (all in
  * double-double).  Panels of nb columns (1..64) are factored in double-double
- * arithmetic (Golub and Van Loan's Householder vector; one workgroup for panels
- * of at most 256 rows, else workgroups of 16 rows (panels of at most 2048 rows)
- * or 32 rows with one launch per column, a single reduction serving both the
- * column's norm and the reflection's dot products);
+ * arithmetic (Golub and Van Loan's Householder vector) by workgroups of 8 rows
+ * (panels of at most 1024 rows), 16 (at most 2048) or 32, one launch per column,
+ * a single reduction serving both the column's norm and the reflection's dot
+ * products;
  * each panel's reflections are accumulated as I - V T V^T (T upper triangular)
  * and the columns to its right updated as A2 - V (T^T (V^T A2)), three products
  * on mdgemm_ex at the adaptive digit width.  workspace: caller-owned device buffer of

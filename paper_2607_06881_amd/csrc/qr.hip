@@ -58,9 +58,10 @@ __device__ inline dd tree_sum(dd* x) {
 }
 
 // A panel is factored by many workgroups, one launch per step s = 0 .. jb, each
-// workgroup owning kRows consecutive panel rows (16 for panels of at most
-// kShortPanel rows, so that they still spread over the chip, 32 above).  Step s
-// finishes column s - 1 and starts column s:
+// workgroup owning kRows consecutive panel rows (8 for panels of at most
+// kSmallPanel rows and 16 for at most kShortPanel, so that short panels still
+// spread over the chip, 32 above).  Step s finishes column s - 1 and starts
+// column s:
 //   every block sums the partials of step s - 1 in the same order (so all
 //   blocks agree bit for bit): d_c = x^T a_c over the rows below the pivot, x
 //   the column s - 1, c >= s - 1 (d_{s-1} = sigma), and takes the pivot row's
@@ -76,14 +77,15 @@ __device__ inline dd tree_sum(dd* x) {
 // s & 1), and every block writes all of its partial slots (zeros where it holds
 // no row below the pivot), so a sum never reads a stale or concurrently written
 // slot.
-constexpr int kPanelRowsShort = 16, kPanelRowsTall = 32;
-constexpr int64_t kShortPanel = 2048;
+constexpr int kPanelRowsSmall = 8, kPanelRowsShort = 16, kPanelRowsTall = 32;
+constexpr int64_t kSmallPanel = 1024, kShortPanel = 2048;
 constexpr int kColThreads = 256;  // 32 column lanes x 8 row groups
 constexpr int kFoldBatch = 8;    // partial sums a thread loads per column group before adding them
 
 constexpr int kRowGroups = kColThreads / 32;                // 8: rows rb + rg + 8 q
 constexpr int kColGroups = kMaxNb / 32;                      // columns c0 + 32 h + cc, h < 2
-static_assert(kPanelRowsShort % kRowGroups == 0 && kPanelRowsTall % kRowGroups == 0 && kMaxNb % 32 == 0,
+static_assert(kPanelRowsSmall % kRowGroups == 0 && kPanelRowsShort % kRowGroups == 0 &&
+                  kPanelRowsTall % kRowGroups == 0 && kMaxNb % 32 == 0,
               "thread layout of the column kernels");
 static_assert(kPanelRowsShort <= 64 && kPanelRowsTall <= 64, "one row per thread of the first two waves");
 
@@ -465,7 +467,7 @@ bool qr_layout(int64_t m, int64_t nf, int64_t n, int nb, QrLayout* L) {
   off += xbytes;
   // partial sums of the multi-workgroup panel, two buffers each: the dot
   // products [G][kMaxNb] and the pivot row [kMaxNb]
-  const size_t groups = static_cast<size_t>((m + kPanelRowsShort - 1) / kPanelRowsShort);  // at most
+  const size_t groups = static_cast<size_t>((m + kPanelRowsSmall - 1) / kPanelRowsSmall);  // at most
   L->pd = off;
   off += align256(2 * dd_bytes * groups * kMaxNb);
   L->prow = off;
@@ -574,8 +576,10 @@ int qr_core(int64_t m, int64_t nf, int64_t n, int nb, double* A, double* tau, vo
     };
     if (mp > mdg::kShortPanel)
       columns(std::integral_constant<int, mdg::kPanelRowsTall>{});
-    else
+    else if (mp > mdg::kSmallPanel)
       columns(std::integral_constant<int, mdg::kPanelRowsShort>{});
+    else
+      columns(std::integral_constant<int, mdg::kPanelRowsSmall>{});
     if (hipGetLastError() != hipSuccess) return MDGEMM_EHIP;
     if (nc == 0) break;
     hipLaunchKernelGGL(mdg::qr_pack_v_kernel, dim3(mdg::blocks_for(mp * jb)), dim3(256), 0, s, m, n, j0, jb, A, V,

@@ -1,7 +1,7 @@
 """GPU checks of the blocked Householder QR in double-double (mdgemm_qr_dd),
-the downstream application whose trailing updates run on mdgemm.  Panels of
-more than 256 rows take the multi-workgroup path (one launch per column), up
-to 70000 rows (2188 workgroups per launch).
+the downstream application whose trailing updates run on mdgemm.  Every panel
+takes the multi-workgroup path (one launch per column; workgroups of 8, 16 or
+32 rows by the panel's height), up to 70000 rows (2188 workgroups per launch).
 
 The GPU factorization is checked in double-double arithmetic by the CPU
 oracle: the residual max |A - Q R| / max |A| and the orthogonality
